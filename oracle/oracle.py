@@ -1,0 +1,241 @@
+"""ctypes wrapper of the CPU oracle (liboracle_rvqsd.so).
+
+TEST INFRASTRUCTURE: only the tests, the smoke check and the benchmark's
+CPU-baseline leg use this module.  It imports nothing from the GPU package.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboracle_rvqsd.so")
+SRC_PATH = os.path.join(HERE, "rvqsd_oracle.c")
+
+DRAFT_SAMPLED, DRAFT_GREEDY, DRAFT_SELF = 0, 1, 2
+MAX_ROUNDS = 16
+TRACE_ROWS = 16
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the oracle with gcc (fp64, no FMA contraction, OpenMP over output rows)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off", "-fopenmp", "-shared", "-fPIC",
+           "-o", LIB_PATH + ".tmp", SRC_PATH, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(LIB_PATH + ".tmp", LIB_PATH)
+    return LIB_PATH
+
+
+class OrcCfg(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_layers", "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "n_codes", "vocab", "max_draft",
+        "dtype", "qk_norm", "topk", "draft_len", "draft_mode")] + [
+        ("rms_eps", ctypes.c_double), ("rope_base", ctypes.c_double), ("temperature", ctypes.c_double)]
+
+
+class OrcStats(ctypes.Structure):
+    _fields_ = [("target_calls", ctypes.c_int32), ("rounds", ctypes.c_int32), ("drafted", ctypes.c_int32),
+                ("accepted", ctypes.c_int32), ("accept_mask", ctypes.c_uint32)]
+
+    def as_dict(self):
+        return {k: int(getattr(self, k)) for k, _ in self._fields_}
+
+
+class OrcRound(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int32), ("kp", ctypes.c_int32), ("n_rows", ctypes.c_int32), ("m_new", ctypes.c_int32),
+                ("drafts", ctypes.c_int32 * 16), ("accepted", ctypes.c_int32), ("token", ctypes.c_int32),
+                ("margin", ctypes.c_double), ("topk_gap", ctypes.c_double)]
+
+
+class OrcTrace(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.POINTER(OrcRound)), ("verify_logits", ctypes.POINTER(ctypes.c_double)),
+                ("draft_logits", ctypes.POINTER(ctypes.c_double)), ("max_rounds", ctypes.c_int32),
+                ("n_rounds", ctypes.c_int32)]
+
+
+PROBE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_double), ctypes.c_int32)
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        i32, f64, vp = ctypes.c_int32, ctypes.c_double, ctypes.c_void_p
+        L.orc_create.restype = vp
+        L.orc_create.argtypes = [P(OrcCfg), vp, ctypes.c_size_t, P(i32)]
+        L.orc_destroy.argtypes = [vp]
+        L.orc_set_threads.argtypes = [i32]
+        L.orc_get_threads.restype = i32
+        L.orc_forward.argtypes = [vp, vp, vp, i32, vp]
+        L.orc_logits.argtypes = [vp, vp, i32, i32, vp]
+        L.orc_topk_softmax.argtypes = [vp, i32, i32, f64, vp, vp]
+        L.orc_sample.argtypes = [vp, vp, i32, f64]
+        L.orc_accept_or_resample.argtypes = [vp, vp, i32, vp, vp, i32, i32, f64, f64, P(i32)]
+        L.orc_ar_frame.argtypes = [vp, vp, i32, vp, vp]
+        L.orc_spec_frame.argtypes = [vp, vp, i32, vp, vp, P(OrcStats), P(OrcTrace), PROBE_FN, vp]
+        L.orc_uniforms_from_seed.argtypes = [ctypes.c_uint64, i32, vp]
+        L.orc_splitmix64_at.restype = ctypes.c_uint64
+        L.orc_splitmix64_at.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        for name in ("orc_forward", "orc_logits", "orc_topk_softmax", "orc_sample", "orc_accept_or_resample",
+                     "orc_ar_frame", "orc_spec_frame", "orc_abi_version"):
+            getattr(L, name).restype = i32
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _check(st: int, what: str):
+    if st < 0:
+        raise OracleError(f"{what} failed with status {st}")
+    return st
+
+
+class Oracle:
+    """One oracle model.  Shape fields follow the weight blob's header."""
+
+    def __init__(self, blob: bytes, *, n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, n_codes, vocab,
+                 max_draft, dtype, topk, temperature, draft_len, draft_mode=DRAFT_SAMPLED, qk_norm=1,
+                 rms_eps=1e-6, rope_base=1e6):
+        self.cfg = OrcCfg(n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, n_codes, vocab, max_draft, dtype,
+                          qk_norm, topk, draft_len, draft_mode, rms_eps, rope_base, temperature)
+        self._blob = bytes(blob)
+        st = ctypes.c_int32(0)
+        self._h = lib().orc_create(ctypes.byref(self.cfg), ctypes.c_char_p(self._blob), len(self._blob),
+                                   ctypes.byref(st))
+        if not self._h:
+            raise OracleError(f"orc_create failed with status {st.value}")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().orc_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+    @property
+    def H(self):
+        return self.cfg.hidden
+
+    @property
+    def V(self):
+        return self.cfg.vocab
+
+    @property
+    def n(self):
+        return self.cfg.n_codes
+
+    def forward(self, f: np.ndarray, in_codes) -> np.ndarray:
+        """Final-normed hidden states of positions 0..len(in_codes) (fp64)."""
+        f = np.ascontiguousarray(f, dtype=np.float32)
+        ic = np.ascontiguousarray(np.asarray(in_codes, dtype=np.int32).reshape(-1))
+        n_pos = ic.size + 1
+        out = np.zeros((n_pos, self.H), dtype=np.float64)
+        _check(lib().orc_forward(self._h, _ptr(f), _ptr(ic) if ic.size else None, n_pos, _ptr(out)), "orc_forward")
+        return out
+
+    def logits(self, h: np.ndarray, head: int, offset: int = 0) -> np.ndarray:
+        h = np.ascontiguousarray(h, dtype=np.float64)
+        out = np.zeros(self.V, dtype=np.float64)
+        _check(lib().orc_logits(self._h, _ptr(h), head, offset, _ptr(out)), "orc_logits")
+        return out
+
+    def ar_frame(self, f, c0: int, uni) -> np.ndarray:
+        f = np.ascontiguousarray(f, dtype=np.float32)
+        u = np.ascontiguousarray(uni, dtype=np.float32)
+        out = np.zeros(self.n, dtype=np.int32)
+        _check(lib().orc_ar_frame(self._h, _ptr(f), int(c0), _ptr(u), _ptr(out)), "orc_ar_frame")
+        return out
+
+    def spec_frame(self, f, c0: int, uni, trace: bool = False, probe=None, logits: bool = False):
+        """Returns (codes, stats dict, trace dict or None)."""
+        f = np.ascontiguousarray(f, dtype=np.float32)
+        u = np.ascontiguousarray(uni, dtype=np.float32)
+        out = np.zeros(self.n, dtype=np.int32)
+        st = OrcStats()
+        tr_p = None
+        if trace:
+            rounds = (OrcRound * MAX_ROUNDS)()
+            vl = dl = None
+            if logits:
+                vl = np.zeros((MAX_ROUNDS, TRACE_ROWS, self.V), dtype=np.float64)
+                dl = np.zeros((MAX_ROUNDS, TRACE_ROWS, self.V), dtype=np.float64)
+            tr = OrcTrace(rounds, vl.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if logits else None,
+                          dl.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if logits else None, MAX_ROUNDS, 0)
+            tr_p = ctypes.byref(tr)
+        cb = PROBE_FN(probe) if probe is not None else PROBE_FN()
+        _check(lib().orc_spec_frame(self._h, _ptr(f), int(c0), _ptr(u), _ptr(out), ctypes.byref(st), tr_p, cb, None),
+               "orc_spec_frame")
+        tdict = None
+        if trace:
+            rs = []
+            for i in range(tr.n_rounds):
+                r = rounds[i]
+                rs.append(dict(m=r.m, kp=r.kp, n_rows=r.n_rows, m_new=r.m_new, drafts=list(r.drafts[:r.kp]),
+                               accepted=r.accepted, token=r.token, margin=r.margin, topk_gap=r.topk_gap))
+            tdict = {"rounds": rs}
+            if logits:
+                tdict["verify_logits"] = vl[:tr.n_rounds]
+                tdict["draft_logits"] = dl[:tr.n_rounds]
+        return out, st.as_dict(), tdict
+
+
+def topk_softmax(logits, topk: int, temperature: float):
+    lg = np.ascontiguousarray(logits, dtype=np.float64)
+    idx = np.zeros(lg.size, dtype=np.int32)
+    pr = np.zeros(lg.size, dtype=np.float64)
+    k = _check(lib().orc_topk_softmax(_ptr(lg), lg.size, topk, temperature, _ptr(idx), _ptr(pr)), "topk_softmax")
+    return idx[:k].copy(), pr[:k].copy()
+
+
+def sample(idx, prob, u: float) -> int:
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    prob = np.ascontiguousarray(prob, dtype=np.float64)
+    return _check(lib().orc_sample(_ptr(idx), _ptr(prob), idx.size, float(u)), "sample")
+
+
+def accept_or_resample(pidx, pp, qidx, qp, d: int, u_acc: float, u_samp: float):
+    """(accepted: bool, token): token = d when accepted, else the residual sample."""
+    pidx = np.ascontiguousarray(pidx, dtype=np.int32)
+    pp = np.ascontiguousarray(pp, dtype=np.float64)
+    qidx = np.ascontiguousarray(qidx, dtype=np.int32)
+    qp = np.ascontiguousarray(qp, dtype=np.float64)
+    tok = ctypes.c_int32(-1)
+    a = _check(lib().orc_accept_or_resample(_ptr(pidx), _ptr(pp), pidx.size, _ptr(qidx), _ptr(qp), qidx.size,
+                                            int(d), float(u_acc), float(u_samp), ctypes.byref(tok)),
+               "accept_or_resample")
+    return (True, int(d)) if a == 1 else (False, int(tok.value))
+
+
+def uniforms_from_seed(seed: int, n_codes: int = 15) -> np.ndarray:
+    out = np.zeros((n_codes, 3), dtype=np.float32)
+    lib().orc_uniforms_from_seed(ctypes.c_uint64(seed), n_codes, _ptr(out))
+    return out
+
+
+def splitmix64_at(seed: int, n: int) -> int:
+    return int(lib().orc_splitmix64_at(ctypes.c_uint64(seed), ctypes.c_uint64(n)))
+
+
+def set_threads(n: int):
+    lib().orc_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().orc_get_threads())
