@@ -1,0 +1,165 @@
+/* rvqsd.h -- C ABI of the MI355X (gfx950) library for RVQ-position-aware
+ * speculative decoding of the inner MultiCodeDecoder loop.
+ *
+ * Paper: "RVQ Position Aware Speculative Decoding for On Device Text to
+ * Speech". Per 80 ms audio frame, an outer decoder emits the coarse code c_0
+ * and an inner decoder emits the 15 residual codes c_1..c_15 one at a time
+ * (Fig. 1). This library runs that inner loop speculatively: the model's own
+ * per-position heads, fed the anchor hidden state plus a per-distance offset
+ * b_j, draft the next K codes (Sec. 2.2, Fig. 3); one verification pass over
+ * the committed code and the drafts decides them with the standard
+ * speculative acceptance rule and residual resampling, which keeps the output
+ * distribution equal to plain top-k sampling (Sec. 2.2, Sec. 3.2).
+ *
+ * Conventions
+ *  - All functions return an rvqsd_status; negative values are errors and
+ *    rvqsd_last_error() (thread-local) holds a message. No C++ exception
+ *    crosses this boundary.
+ *  - "host" pointers are ordinary CPU memory; "device" pointers are HIP
+ *    device allocations on the device current when the model was created.
+ *  - Codes and positions are int32; activations, logits and probabilities are
+ *    fp32 on the device; sampling decisions are taken in fp64.
+ *  - Uniform table layout: float[n_codes][3] in [0,1), row s-1 for code
+ *    position s, columns (u_draft, u_accept, u_sample).
+ */
+#ifndef RVQSD_H
+#define RVQSD_H
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RVQSD_ABI_VERSION 1
+
+typedef int32_t rvqsd_status;
+#define RVQSD_OK 0
+#define RVQSD_EINVAL (-1)       /* bad configuration, shape, code value or null pointer */
+#define RVQSD_EBLOB (-2)        /* weight blob size / magic / version / shape mismatch */
+#define RVQSD_ENOMEM (-3)       /* device or pinned host allocation failed */
+#define RVQSD_EHIP (-4)         /* HIP runtime error; message kept in rvqsd_last_error() */
+#define RVQSD_EUNSUPPORTED (-5) /* configuration the kernels do not support (see rvqsd_create) */
+#define RVQSD_ENUMERIC (-6)     /* every logit of a row was non-finite */
+#define RVQSD_ETIMEOUT (-7)     /* a workgroup waited too long for another (kernel exited early) */
+
+#define RVQSD_DTYPE_F32 0
+#define RVQSD_DTYPE_BF16 1
+
+/* Model configuration. The shape fields must equal the weight blob's header. */
+typedef struct {
+  int32_t abi_version; /* RVQSD_ABI_VERSION */
+  int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn;
+  int32_t n_codes;     /* residual codes per frame, 1..15 */
+  int32_t vocab;       /* codebook size per position, 2..65536 */
+  int32_t max_draft;   /* offsets stored in the blob */
+  int32_t dtype;       /* RVQSD_DTYPE_*: storage of the matrices */
+  int32_t qk_norm;     /* 1: per-head RMSNorm of q and k before RoPE */
+  int32_t topk;        /* 1..256 */
+  int32_t draft_len;   /* K, 0..min(max_draft, 14); 0 = plain autoregressive sampling */
+  int32_t draft_greedy;/* 0: drafts sampled from the draft distribution; 1: its argmax */
+  int32_t reserved[3];
+  double rms_eps, rope_base, temperature;
+} rvqsd_cfg;
+
+/* One weight blob (host memory): 64-byte header + tensors, layout documented
+ * in paper_2609_37007_amd/synth.py. rvqsd_create copies it; the caller keeps
+ * ownership and may free it on return. */
+typedef struct {
+  const void* data;
+  uint64_t bytes;
+} rvqsd_weights;
+
+/* Per-frame statistics. */
+typedef struct {
+  int32_t target_calls; /* verification passes including the 2-row prefix pass */
+  int32_t rounds;       /* speculative rounds after the prefix pass */
+  int32_t drafted;      /* sum over rounds of the drafts verified */
+  int32_t accepted;     /* accepted drafts */
+  uint32_t accept_mask; /* bit s set when the draft at code position s was accepted */
+  int32_t status;       /* device-side status of this frame (RVQSD_OK or an error) */
+  uint64_t weight_bytes;/* algorithmic bytes the frame's passes must read (weights + gathered rows + KV) */
+  uint64_t clk_start, clk_end; /* device constant clock (100 MHz) at kernel start / end */
+} rvqsd_stats;
+
+/* Optional per-round trace (device buffers, caller-owned). Any pointer may be NULL.
+ *  logits: float[max_rounds][rvqsd_trace_slots(model)][vocab]: slot r < 16 = verify
+ *          logits of row r (position first_pos + r), slot 16 + r*K + (j-1) = draft
+ *          logits LMH_{s+j}(h_s + b_j) of row r.
+ *  rounds: int32[max_rounds][32]: m, K', first_pos, rows, m_new, accepted, token,
+ *          pass index, drafts d_{m+1..m+K'} at [8..8+K'), then reserved.
+ *  clock:  uint64[max_rounds][5*n_layers+5]: device clock at each phase end of a pass
+ *          (workgroup 0's view), last entry = pass end. */
+typedef struct {
+  float* logits;
+  int32_t* rounds;
+  uint64_t* clock;
+  int32_t max_rounds;
+} rvqsd_trace;
+
+typedef struct rvqsd_model rvqsd_model;
+typedef struct rvqsd_stream rvqsd_stream;
+
+/* Static information about a created model. */
+typedef struct {
+  int32_t workgroups;       /* workgroups of the frame kernel (one per compute unit) */
+  int32_t threads;          /* threads per workgroup */
+  int32_t max_rows;         /* rows per pass the kernel is instantiated for */
+  int32_t trace_slots;      /* logit slots per traced round */
+  uint64_t lds_bytes;       /* dynamic LDS per workgroup */
+  uint64_t layer_weight_bytes; /* bytes of the L decoder layers (matrices + gains) */
+  uint64_t head_bytes;      /* bytes of one LM head (vocab x hidden) */
+  uint64_t emb_row_bytes;   /* bytes of one embedding row */
+  uint64_t device_weight_bytes; /* device memory holding the weights */
+} rvqsd_info;
+
+/* Create a model: validates cfg against the blob, copies the weights to the
+ * current HIP device. Errors: EINVAL (bad cfg / NULL), EBLOB, EUNSUPPORTED
+ * (hidden, q/kv width and ffn must be multiples of 512 for bf16 and 256 for
+ * f32, head_dim a multiple of 64, n_kv_heads <= 256 workgroups, ...), ENOMEM, EHIP. */
+rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_model** out);
+void rvqsd_destroy(rvqsd_model* m);
+rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out);
+
+/* Create a decode stream on a caller-owned hipStream_t (borrowed, never
+ * destroyed; NULL = the null stream). max_streams is the number of
+ * independent frame streams decoded together and must be 1 in this version.
+ * A stream owns its device work buffers and pinned staging; use one host
+ * thread per stream. */
+rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, rvqsd_stream** out);
+void rvqsd_stream_destroy(rvqsd_stream* s);
+
+/* Decode one frame (host pointers, synchronous): frame_hidden float[hidden],
+ * c0 in [0, vocab), uniforms expanded from rng_seed with SplitMix64 (see
+ * rvqsd_uniforms_from_seed). Writes out_codes[n_codes] (codes c_1..c_n) and
+ * *out_stats (nullable) only on success. */
+rvqsd_status rvqsd_decode_frame(rvqsd_stream* s, const float* frame_hidden, int32_t c0, uint64_t rng_seed,
+                                int32_t* out_codes, rvqsd_stats* out_stats);
+
+/* Same with a caller-supplied uniform table (host float[n_codes][3]). */
+rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, int32_t c0, const float* uniforms,
+                                  int32_t* out_codes, rvqsd_stats* out_stats);
+
+/* Enqueue one frame on the stream with device pointers only; returns after
+ * the launch, the caller synchronises. d_c0: int32[1]; d_uniforms:
+ * float[n_codes][3]; d_out_codes: int32[n_codes]; d_stats: rvqsd_stats[1]
+ * (written by the device; its status field reports device-side errors).
+ * Inputs must stay valid until the stream reaches the frame. */
+rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidden, const int32_t* d_c0,
+                                      const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats);
+
+/* Install (trace != NULL) or remove (NULL) a per-round trace for later frames of this stream. */
+rvqsd_status rvqsd_set_trace(rvqsd_stream* s, const rvqsd_trace* trace);
+
+/* The library's uniform generator (host only): uniform i = (n_codes*3 table
+ * order) is the top 24 bits of the (i+1)-th SplitMix64 output (Steele, Lea,
+ * Flood 2014) for the given seed, times 2^-24. out: float[n_codes][3]. */
+rvqsd_status rvqsd_uniforms_from_seed(uint64_t seed, int32_t n_codes, float* out);
+
+const char* rvqsd_status_str(rvqsd_status st);
+const char* rvqsd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,463 @@
+// rvqsd_api.cpp -- host runtime behind the C ABI declared in include/rvqsd.h.
+//
+// Owns the device copy of the weights (the blob payload, header stripped, so
+// every tensor starts 16-byte aligned), the per-stream exchange buffers and
+// the launch of the persistent frame kernel. No exception crosses the ABI.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+
+#include "../../include/rvqsd.h"
+#include "rvqsd_internal.h"
+
+using namespace rvqsd;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int set_err(int st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+#define HIPCHK(expr)                                                                     \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess) return set_err(RVQSD_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+uint32_t rd32(const unsigned char* p) {
+  return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) | ((uint32_t)p[3] << 24);
+}
+
+uint64_t splitmix64_at(uint64_t seed, uint64_t n) {
+  uint64_t z = seed + (n + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Allocation failures can be injected by tests: RVQSD_TEST_FAIL_ALLOC=n fails the n-th device allocation.
+int g_alloc_count = 0;
+hipError_t dev_alloc(void** p, size_t bytes) {
+  const char* f = getenv("RVQSD_TEST_FAIL_ALLOC");
+  ++g_alloc_count;
+  if (f && atoi(f) == g_alloc_count) {
+    *p = nullptr;
+    return hipErrorOutOfMemory;
+  }
+  return hipMalloc(p, bytes);
+}
+
+}  // namespace
+
+struct rvqsd_model {
+  rvqsd_cfg cfg;
+  int device;
+  int nwg;
+  int mr;               // rows the kernel is instantiated for
+  int wbytes;           // bytes per matrix element
+  size_t lds_bytes;
+  int stage_cols;
+  void* dweights;
+  uint64_t dweight_bytes;
+  KParams base;         // weight offsets and dimensions (buffers filled per stream)
+};
+
+struct rvqsd_stream {
+  rvqsd_model* m;
+  hipStream_t stream;
+  KParams kp;           // host copy of the parameter block
+  KParams* dkp;         // device copy
+  void* dbuf;           // all exchange buffers in one allocation
+  size_t dbuf_bytes;
+  uint64_t* status;
+  // synchronous-path staging
+  float* h_in;          // pinned: frame hidden [H], uniforms [n][3], c0 (as int bits)
+  int32_t* h_out;       // pinned: codes [n], then stats
+  float* d_in;
+  int32_t* d_out;
+  uint32_t epoch;       // tag base of the next frame
+  uint32_t epoch_step;
+};
+
+namespace {
+
+int validate_cfg(const rvqsd_cfg* c, int nwg) {
+  if (c->abi_version != RVQSD_ABI_VERSION)
+    return set_err(RVQSD_EINVAL, "abi_version %d, library is %d", c->abi_version, RVQSD_ABI_VERSION);
+  if (c->n_layers <= 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->ffn <= 0 || c->n_codes < 1 || c->n_codes > kMaxCodes || c->vocab < 2 || c->max_draft < 0 ||
+      c->topk < 1 || c->draft_len < 0 || c->draft_len > c->max_draft || !(c->temperature > 0.0) ||
+      !(c->rms_eps > 0.0) || !(c->rope_base > 0.0) || (c->dtype != RVQSD_DTYPE_F32 && c->dtype != RVQSD_DTYPE_BF16) ||
+      (c->n_q_heads % c->n_kv_heads) != 0 || (c->qk_norm != 0 && c->qk_norm != 1) ||
+      (c->draft_greedy != 0 && c->draft_greedy != 1))
+    return set_err(RVQSD_EINVAL, "invalid configuration field");
+  const int epc = c->dtype == RVQSD_DTYPE_F32 ? 4 : 8;
+  const int qd = c->n_q_heads * c->head_dim;
+  const int quant = 64 * epc;
+  if (c->hidden % quant || qd % quant || c->ffn % quant)
+    return set_err(RVQSD_EUNSUPPORTED, "hidden, n_q_heads*head_dim and ffn must be multiples of %d", quant);
+  if (c->hidden / epc > kThreads || qd / epc > kThreads || c->ffn / epc > kThreads)
+    return set_err(RVQSD_EUNSUPPORTED, "a reduction dimension exceeds %d elements", kThreads * epc);
+  if (c->head_dim % 64 || c->head_dim > 256) return set_err(RVQSD_EUNSUPPORTED, "head_dim must be 64, 128, 192 or 256");
+  if (c->topk > kMaxTopk) return set_err(RVQSD_EUNSUPPORTED, "topk > %d", kMaxTopk);
+  if (c->vocab > 16384) return set_err(RVQSD_EUNSUPPORTED, "vocab > 16384");
+  if (c->draft_len > 14) return set_err(RVQSD_EUNSUPPORTED, "draft_len > 14");
+  if (c->n_q_heads > nwg) return set_err(RVQSD_EUNSUPPORTED, "more query heads than workgroups");
+  if (kSlotDraft0 + (c->draft_len + 1) * c->draft_len > nwg)
+    return set_err(RVQSD_EUNSUPPORTED, "not enough workgroups for the sampling slots");
+  if ((c->hidden + nwg - 1) / nwg > 32) return set_err(RVQSD_EUNSUPPORTED, "hidden > 32 * workgroups");
+  return RVQSD_OK;
+}
+
+// Work-area floats needed by every phase for a given staging width.
+size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
+  const int H = c->hidden, qd = c->n_q_heads * c->head_dim, kd = c->n_kv_heads * c->head_dim, F = c->ffn;
+  const int V = c->vocab, d = c->head_dim, K = c->draft_len;
+  const int cpw = (H + nwg - 1) / nwg;
+  const int rpw_qkv = (qd + 2 * kd + nwg - 1) / nwg;
+  const int fpw = (F + nwg - 1) / nwg;
+  int nh_max = 2 * K + 1 < c->n_codes ? 2 * K + 1 : c->n_codes;
+  if (nh_max < 1) nh_max = 1;
+  const int wph_min = nwg / nh_max;
+  const int rpw_heads = (V + wph_min - 1) / wph_min;
+  int rows_out = rpw_qkv;
+  if (2 * fpw > rows_out) rows_out = 2 * fpw;
+  if (rpw_heads > rows_out) rows_out = rpw_heads;
+  size_t w = (size_t)mr * H + (size_t)rows_out * mr;
+  const size_t proj = (size_t)mr * stage_cols + (size_t)cpw * mr;
+  const size_t attn = (size_t)5 * kMaxRows * d + kMaxRows * kMaxPos;
+  const size_t samp = (size_t)V + 2 * kMaxTopk + 2 + 2 * 3 * kMaxTopk + kMaxTopk + 8;
+  if (proj > w) w = proj;
+  if (attn > w) w = attn;
+  if (samp > w) w = samp;
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rvqsd_last_error(void) { return g_err; }
+
+const char* rvqsd_status_str(rvqsd_status st) {
+  switch (st) {
+    case RVQSD_OK: return "ok";
+    case RVQSD_EINVAL: return "invalid argument";
+    case RVQSD_EBLOB: return "bad weight blob";
+    case RVQSD_ENOMEM: return "out of memory";
+    case RVQSD_EHIP: return "HIP runtime error";
+    case RVQSD_EUNSUPPORTED: return "unsupported configuration";
+    case RVQSD_ENUMERIC: return "non-finite logits";
+    case RVQSD_ETIMEOUT: return "workgroup wait timed out";
+    default: return "unknown status";
+  }
+}
+
+rvqsd_status rvqsd_uniforms_from_seed(uint64_t seed, int32_t n_codes, float* out) {
+  if (!out || n_codes < 1 || n_codes > kMaxCodes) return set_err(RVQSD_EINVAL, "bad arguments");
+  for (int i = 0; i < n_codes * 3; ++i)
+    out[i] = (float)((double)(splitmix64_at(seed, (uint64_t)i) >> 40) * (1.0 / 16777216.0));
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_model** out) {
+  if (!w || !cfg || !out || !w->data) return set_err(RVQSD_EINVAL, "null argument");
+  *out = nullptr;
+  int dev = 0;
+  HIPCHK(hipGetDevice(&dev));
+  hipDeviceProp_t prop;
+  HIPCHK(hipGetDeviceProperties(&prop, dev));
+  const int nwg = prop.multiProcessorCount;
+  int st = validate_cfg(cfg, nwg);
+  if (st) return st;
+  if (!prop.cooperativeLaunch) return set_err(RVQSD_EUNSUPPORTED, "device lacks cooperative launch");
+
+  // blob header
+  const unsigned char* b = (const unsigned char*)w->data;
+  if (w->bytes < 64 || memcmp(b, "RVQSDW1\0", 8) != 0 || rd32(b + 8) != 1)
+    return set_err(RVQSD_EBLOB, "bad magic or version");
+  const uint32_t want[10] = {(uint32_t)cfg->dtype, (uint32_t)cfg->n_layers, (uint32_t)cfg->hidden,
+                             (uint32_t)cfg->n_q_heads, (uint32_t)cfg->n_kv_heads, (uint32_t)cfg->head_dim,
+                             (uint32_t)cfg->ffn, (uint32_t)cfg->n_codes, (uint32_t)cfg->vocab,
+                             (uint32_t)cfg->max_draft};
+  for (int i = 0; i < 10; ++i)
+    if (rd32(b + 12 + 4 * i) != want[i]) return set_err(RVQSD_EBLOB, "header field %d = %u, cfg has %u", i, rd32(b + 12 + 4 * i), want[i]);
+
+  KParams k;
+  memset(&k, 0, sizeof(k));
+  k.L = cfg->n_layers;
+  k.H = cfg->hidden;
+  k.nq = cfg->n_q_heads;
+  k.nkv = cfg->n_kv_heads;
+  k.d = cfg->head_dim;
+  k.F = cfg->ffn;
+  k.n_codes = cfg->n_codes;
+  k.V = cfg->vocab;
+  k.K = cfg->draft_len;
+  k.topk = cfg->topk;
+  k.greedy = cfg->draft_greedy;
+  k.qk_norm = cfg->qk_norm;
+  k.max_draft = cfg->max_draft;
+  k.qdim = k.nq * k.d;
+  k.kvdim = k.nkv * k.d;
+  k.nqkv = k.qdim + 2 * k.kvdim;
+  k.rms_eps = (float)cfg->rms_eps;
+  k.temperature = cfg->temperature;
+  k.rope_base = cfg->rope_base;
+  k.nwg = nwg;
+  const uint64_t wb = cfg->dtype == RVQSD_DTYPE_F32 ? 4 : 2;
+  const uint64_t H = k.H, qd = k.qdim, kd = k.kvdim, F = k.F, d = k.d, V = k.V, n = k.n_codes;
+  uint64_t o = 0;
+  k.o_attn_norm = o; o += H * 4;
+  k.o_wq = o; o += qd * H * wb;
+  k.o_wk = o; o += kd * H * wb;
+  k.o_wv = o; o += kd * H * wb;
+  k.o_qn = o; o += d * 4;
+  k.o_kn = o; o += d * 4;
+  k.o_wo = o; o += H * qd * wb;
+  k.o_mlp_norm = o; o += H * 4;
+  k.o_wg = o; o += F * H * wb;
+  k.o_wu = o; o += F * H * wb;
+  k.o_wd = o; o += H * F * wb;
+  k.layer_stride = o;
+  o = k.layer_stride * k.L;
+  k.o_final_norm = o; o += H * 4;
+  k.table_stride = V * H * wb;
+  k.o_emb0 = o; o += n * k.table_stride;
+  k.o_lmh1 = o; o += n * k.table_stride;
+  k.o_offsets = o; o += (uint64_t)cfg->max_draft * H * 4;
+  if (w->bytes != 64 + o) return set_err(RVQSD_EBLOB, "blob has %llu bytes, expected %llu", (unsigned long long)w->bytes, (unsigned long long)(64 + o));
+
+  rvqsd_model* m = new (std::nothrow) rvqsd_model;
+  if (!m) return set_err(RVQSD_ENOMEM, "host allocation");
+  memset(m, 0, sizeof(*m));
+  m->cfg = *cfg;
+  m->device = dev;
+  m->nwg = nwg;
+  m->mr = frame_max_rows(cfg->draft_len);
+  m->wbytes = (int)wb;
+  m->dweight_bytes = o;
+  // LDS: stage the widest activation if it fits, else the down projection polls its chunks directly
+  const int cpw = (k.H + nwg - 1) / nwg;
+  const size_t head = (size_t)frame_lds_head_floats(m->mr, cpw);
+  const size_t budget = (size_t)prop.sharedMemPerBlock - 6 * 1024;  // leave room for static shared state
+  int stage = (int)(qd > F ? qd : F);
+  if ((head + work_floats(cfg, nwg, m->mr, stage)) * 4 > budget) stage = (int)(qd > H ? qd : H);
+  const size_t lds = (head + work_floats(cfg, nwg, m->mr, stage)) * 4;
+  if (lds > budget) {
+    delete m;
+    return set_err(RVQSD_EUNSUPPORTED, "needs %zu bytes of LDS per workgroup, %zu available", lds, budget);
+  }
+  m->lds_bytes = lds;
+  m->stage_cols = stage;
+  k.stage_cols = stage;
+  hipError_t e = dev_alloc(&m->dweights, o);
+  if (e != hipSuccess) {
+    delete m;
+    return set_err(RVQSD_ENOMEM, "device weights (%llu bytes): %s", (unsigned long long)o, hipGetErrorString(e));
+  }
+  e = hipMemcpy(m->dweights, b + 64, o, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(m->dweights);
+    delete m;
+    return set_err(RVQSD_EHIP, "weight upload: %s", hipGetErrorString(e));
+  }
+  k.wbase = (const uint8_t*)m->dweights;
+  m->base = k;
+  *out = m;
+  return RVQSD_OK;
+}
+
+void rvqsd_destroy(rvqsd_model* m) {
+  if (!m) return;
+  (void)hipFree(m->dweights);
+  delete m;
+}
+
+rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out) {
+  if (!m || !out) return set_err(RVQSD_EINVAL, "null argument");
+  out->workgroups = m->nwg;
+  out->threads = kThreads;
+  out->max_rows = m->mr;
+  out->trace_slots = kSlotDraft0 + kMaxRows * m->cfg.draft_len;
+  out->lds_bytes = m->lds_bytes;
+  out->layer_weight_bytes = m->base.layer_stride * (uint64_t)m->base.L;
+  out->head_bytes = m->base.table_stride;
+  out->emb_row_bytes = (uint64_t)m->base.H * m->wbytes;
+  out->device_weight_bytes = m->dweight_bytes;
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, rvqsd_stream** out) {
+  if (!m || !out) return set_err(RVQSD_EINVAL, "null argument");
+  if (max_streams != 1) return set_err(RVQSD_EUNSUPPORTED, "max_streams must be 1");
+  *out = nullptr;
+  rvqsd_stream* s = new (std::nothrow) rvqsd_stream;
+  if (!s) return set_err(RVQSD_ENOMEM, "host allocation");
+  memset(s, 0, sizeof(*s));
+  s->m = m;
+  s->stream = (hipStream_t)hip_stream;
+  KParams k = m->base;
+  k.n_slots = kSlotDraft0 + kMaxRows * k.K;
+  k.drec_words = 1 + 3 * kMaxTopk;
+  const size_t H = k.H, V = k.V;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return at;
+  };
+  const size_t o_x = take(kMaxRows * H * 8), o_qkv = take((size_t)kMaxRows * k.nqkv * 8),
+               o_attn = take((size_t)kMaxRows * k.qdim * 8), o_act = take((size_t)kMaxRows * k.F * 8),
+               o_log = take((size_t)2 * k.n_slots * V * 8), o_vres = take((size_t)2 * kMaxRows * 8),
+               o_drec = take((size_t)2 * k.n_slots * k.drec_words * 8),
+               o_kvc = take((size_t)k.nq * k.L * kMaxPos * 2 * k.d * 4), o_status = take(8),
+               o_in = take(((size_t)H + 3 * kMaxCodes + 4) * 4), o_out = take((kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64),
+               o_kp = take(sizeof(KParams));
+  s->dbuf_bytes = off;
+  hipError_t e = dev_alloc(&s->dbuf, off);
+  if (e != hipSuccess) {
+    delete s;
+    return set_err(RVQSD_ENOMEM, "stream buffers (%zu bytes): %s", off, hipGetErrorString(e));
+  }
+  e = hipMemset(s->dbuf, 0, off);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_in, ((size_t)H + 3 * kMaxCodes + 4) * 4, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_out, (kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    if (s->h_in) hipHostFree(s->h_in);
+    (void)hipFree(s->dbuf);
+    delete s;
+    return set_err(RVQSD_ENOMEM, "stream staging: %s", hipGetErrorString(e));
+  }
+  uint8_t* base = (uint8_t*)s->dbuf;
+  k.xb = (uint64_t*)(base + o_x);
+  k.qkvb = (uint64_t*)(base + o_qkv);
+  k.attnb = (uint64_t*)(base + o_attn);
+  k.actb = (uint64_t*)(base + o_act);
+  k.logb = (uint64_t*)(base + o_log);
+  k.vres = (uint64_t*)(base + o_vres);
+  k.drec = (uint64_t*)(base + o_drec);
+  k.kvc = (float*)(base + o_kvc);
+  k.status = (uint64_t*)(base + o_status);
+  s->status = k.status;
+  s->d_in = (float*)(base + o_in);
+  s->d_out = (int32_t*)(base + o_out);
+  s->dkp = (KParams*)(base + o_kp);
+  s->kp = k;
+  e = hipMemcpy(s->dkp, &s->kp, sizeof(KParams), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipHostFree(s->h_in);
+    (void)hipHostFree(s->h_out);
+    (void)hipFree(s->dbuf);
+    delete s;
+    return set_err(RVQSD_EHIP, "parameter upload: %s", hipGetErrorString(e));
+  }
+  const int tags_per_frame = kMaxPos * phases_per_pass(k.L) + 2;
+  s->epoch_step = (uint32_t)((tags_per_frame + 4095) & ~4095);
+  s->epoch = s->epoch_step;
+  *out = s;
+  return RVQSD_OK;
+}
+
+void rvqsd_stream_destroy(rvqsd_stream* s) {
+  if (!s) return;
+  (void)hipStreamSynchronize(s->stream);
+  (void)hipHostFree(s->h_in);
+  (void)hipHostFree(s->h_out);
+  (void)hipFree(s->dbuf);
+  delete s;
+}
+
+rvqsd_status rvqsd_set_trace(rvqsd_stream* s, const rvqsd_trace* t) {
+  if (!s) return set_err(RVQSD_EINVAL, "null stream");
+  if (t && t->max_rounds < 0) return set_err(RVQSD_EINVAL, "max_rounds < 0");
+  s->kp.tr_logits = t ? t->logits : nullptr;
+  s->kp.tr_rounds = t ? t->rounds : nullptr;
+  s->kp.tr_clock = t ? t->clock : nullptr;
+  s->kp.tr_max_rounds = t ? t->max_rounds : 0;
+  HIPCHK(hipStreamSynchronize(s->stream));
+  HIPCHK(hipMemcpy(s->dkp, &s->kp, sizeof(KParams), hipMemcpyHostToDevice));
+  return RVQSD_OK;
+}
+
+static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t* d_c0, const float* d_u,
+                               int32_t* d_codes, rvqsd_stats* d_stats) {
+  // tags of stale words from earlier frames never equal a later frame's tags; on wrap, clear everything
+  if ((uint64_t)s->epoch + 2ull * s->epoch_step >= 0xFFFFFFFFull) {
+    HIPCHK(hipMemsetAsync(s->dbuf, 0, (uint8_t*)s->d_in - (uint8_t*)s->dbuf, s->stream));
+    s->epoch = s->epoch_step;
+  }
+  FrameArgs fa;
+  fa.frame_hidden = d_fh;
+  fa.c0 = d_c0;
+  fa.uniforms = d_u;
+  fa.out_codes = d_codes;
+  fa.out_stats = d_stats;
+  fa.epoch_base = s->epoch;
+  s->epoch += s->epoch_step;
+  char err[256];
+  int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, (void*)s->stream, s->m->lds_bytes, err,
+                        sizeof(err));
+  if (st) return set_err(st, "%s", err);
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidden, const int32_t* d_c0,
+                                      const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats) {
+  if (!s || !d_frame_hidden || !d_c0 || !d_uniforms || !d_out_codes || !d_stats)
+    return set_err(RVQSD_EINVAL, "null argument");
+  return launch_one(s, d_frame_hidden, d_c0, d_uniforms, d_out_codes, d_stats);
+}
+
+rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, int32_t c0, const float* uniforms,
+                                  int32_t* out_codes, rvqsd_stats* out_stats) {
+  if (!s || !frame_hidden || !uniforms || !out_codes) return set_err(RVQSD_EINVAL, "null argument");
+  const rvqsd_cfg& c = s->m->cfg;
+  if (c0 < 0 || c0 >= c.vocab) return set_err(RVQSD_EINVAL, "c0 = %d outside [0, %d)", c0, c.vocab);
+  const int H = c.hidden, n = c.n_codes;
+  for (int i = 0; i < 3 * n; ++i)
+    if (!(uniforms[i] >= 0.f && uniforms[i] < 1.f)) return set_err(RVQSD_EINVAL, "uniform %d outside [0, 1)", i);
+  for (int i = 0; i < H; ++i)
+    if (!std::isfinite(frame_hidden[i])) return set_err(RVQSD_EINVAL, "frame_hidden[%d] is not finite", i);
+  // pinned staging: hidden [H] | uniforms [3n] | c0
+  memcpy(s->h_in, frame_hidden, (size_t)H * 4);
+  memcpy(s->h_in + H, uniforms, (size_t)3 * n * 4);
+  memcpy(s->h_in + H + 3 * kMaxCodes, &c0, 4);
+  const size_t in_bytes = ((size_t)H + 3 * kMaxCodes + 1) * 4;
+  HIPCHK(hipMemcpyAsync(s->d_in, s->h_in, in_bytes, hipMemcpyHostToDevice, s->stream));
+  int32_t* d_codes = s->d_out;
+  rvqsd_stats* d_stats = (rvqsd_stats*)(s->d_out + kMaxCodes + 1);
+  int st = launch_one(s, s->d_in, (const int32_t*)(s->d_in + H + 3 * kMaxCodes), s->d_in + H, d_codes, d_stats);
+  if (st) return st;
+  const size_t out_bytes = (kMaxCodes + 1) * 4 + sizeof(rvqsd_stats);
+  HIPCHK(hipMemcpyAsync(s->h_out, s->d_out, out_bytes, hipMemcpyDeviceToHost, s->stream));
+  HIPCHK(hipStreamSynchronize(s->stream));
+  rvqsd_stats hs;
+  memcpy(&hs, s->h_out + kMaxCodes + 1, sizeof(hs));
+  if (hs.status != RVQSD_OK) return set_err(hs.status, "device reported %s", rvqsd_status_str(hs.status));
+  memcpy(out_codes, s->h_out, (size_t)n * 4);
+  if (out_stats) *out_stats = hs;
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_decode_frame(rvqsd_stream* s, const float* frame_hidden, int32_t c0, uint64_t rng_seed,
+                                int32_t* out_codes, rvqsd_stats* out_stats) {
+  if (!s) return set_err(RVQSD_EINVAL, "null stream");
+  float u[kMaxCodes * 3];
+  rvqsd_status st = rvqsd_uniforms_from_seed(rng_seed, s->m->cfg.n_codes, u);
+  if (st) return st;
+  return rvqsd_decode_frame_u(s, frame_hidden, c0, u, out_codes, out_stats);
+}
+
+}  // extern "C"

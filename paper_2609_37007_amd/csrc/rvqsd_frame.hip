@@ -1,0 +1,1291 @@
+// rvqsd_frame.hip -- persistent frame kernel (gfx950) for RVQ-position-aware speculative decoding.
+//
+// One cooperative launch decodes one frame: the 2-row prefix pass, then
+// speculative rounds until the 15 residual codes are committed (paper Fig. 1
+// inner loop, Sec. 2.2 drafting and verification). Every pass runs, for each
+// decoder layer, five phases (QKV, attention, O, gate/up, down), then the
+// per-position LM heads and the fused top-k / softmax / accept / resample /
+// draft phase. The accept chain of a round is folded into the start of the
+// next pass: every workgroup reads the per-position verdicts and derives the
+// new anchor itself, so no phase is spent on it.
+//
+// Workgroups exchange activations through 64-bit words whose high half is a
+// tag (frame epoch + pass + phase) and whose low half is the fp32 payload.
+// Producers write them and consumers poll them with relaxed device-scope
+// atomic accesses: no cache-wide fences, no grid barrier. Every wait is
+// bounded; a timed-out or failed workgroup records an error in the device
+// status word, and every other wait gives up as soon as it sees it, so the
+// grid always drains.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rvqsd_internal.h"
+
+namespace rvqsd {
+
+typedef uint16_t bf16_t;
+
+constexpr uint64_t kTimeoutTicks = 200ull * 1000 * 1000;  // 2 s of the 100 MHz device clock
+
+// ------------------------------------------------------------------ helpers
+
+// Pointers taken from the parameter block are generic; every device-memory
+// access goes through these casts so that it compiles to a global (not flat)
+// instruction.
+#define RVQSD_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ RVQSD_GLOBAL T* G(T* q) {
+  return (RVQSD_GLOBAL T*)q;
+}
+template <typename T>
+__device__ __forceinline__ const RVQSD_GLOBAL T* G(const T* q) {
+  return (const RVQSD_GLOBAL T*)q;
+}
+
+__device__ __forceinline__ uint64_t xload(const uint64_t* p) {
+  return __hip_atomic_load(G(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void xstore(uint64_t* p, uint32_t tag, uint32_t payload) {
+  __hip_atomic_store(G(p), ((uint64_t)tag << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void xstoref(uint64_t* p, uint32_t tag, float v) { xstore(p, tag, __float_as_uint(v)); }
+__device__ __forceinline__ uint64_t dclock() { return __builtin_amdgcn_s_memrealtime(); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_sumd(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_maxd(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
+  return v;
+}
+// inclusive prefix sum over the 64 lanes
+__device__ __forceinline__ int wave_scan_incl(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+__device__ __forceinline__ double wave_scan_incld(double v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    double t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+// 16 bytes of weights (a builtin vector type, so address-space qualified loads copy it)
+typedef uint32_t W16 __attribute__((ext_vector_type(4)));
+
+template <typename WT>
+struct WTraits;
+template <>
+struct WTraits<float> {
+  static constexpr int EPC = 4;  // elements per 16-byte chunk
+  __device__ static __forceinline__ void widen(const W16& c, float* w) {
+    w[0] = __uint_as_float(c.x);
+    w[1] = __uint_as_float(c.y);
+    w[2] = __uint_as_float(c.z);
+    w[3] = __uint_as_float(c.w);
+  }
+  __device__ static __forceinline__ float one(const float* p, size_t i) { return G(p)[i]; }
+};
+template <>
+struct WTraits<bf16_t> {
+  static constexpr int EPC = 8;
+  __device__ static __forceinline__ void widen(const W16& c, float* w) {
+    w[0] = __uint_as_float(c.x << 16);
+    w[1] = __uint_as_float(c.x & 0xffff0000u);
+    w[2] = __uint_as_float(c.y << 16);
+    w[3] = __uint_as_float(c.y & 0xffff0000u);
+    w[4] = __uint_as_float(c.z << 16);
+    w[5] = __uint_as_float(c.z & 0xffff0000u);
+    w[6] = __uint_as_float(c.w << 16);
+    w[7] = __uint_as_float(c.w & 0xffff0000u);
+  }
+  __device__ static __forceinline__ float one(const bf16_t* p, size_t i) { return __uint_as_float((uint32_t)G(p)[i] << 16); }
+};
+
+// ---------------------------------------------------------- shared state
+
+struct Shared {
+  FrameArgs fa;
+  int abort;
+  int pass, m, kp, first_pos, rows;
+  int prev_anchor_row;  // row, in the previous pass, of the current anchor m
+  int codes[kMaxPos + 1];
+  int drafts[kMaxPos + 1];
+  int in_code[kMaxPos + 1];  // code consumed at position s (s >= 1)
+  float rstd[kMaxRows];
+  // statistics (kept by every workgroup, written by workgroup 0)
+  int st_calls, st_rounds, st_drafted, st_accepted;
+  unsigned st_mask;
+  unsigned long long st_bytes;
+  // sampling scratch
+  unsigned hist[256];
+  int iscan[kWaves];
+  int sel_digit, sel_kk, n_sup, n_q;
+  int tok, acc;
+  // vectors of the LM head this workgroup multiplies (heads phase)
+  int hv_n, hv_row[kMaxRows], hv_off[kMaxRows], hv_slot[kMaxRows];
+};
+
+struct Ctx {
+  const KParams* p;
+  Shared* sh;
+  float* dyn;       // dynamic LDS
+  float* xown;      // [kMaxRows][cpw] residual columns owned by this workgroup
+  float* red;       // [kWaves][RPT * MR] reduction scratch
+  float* work;      // union area
+  int cpw;          // residual columns per workgroup
+  uint32_t tag_base;
+};
+
+__device__ __forceinline__ uint32_t tag_of(const Ctx& c, int pass, int phase) {
+  return c.tag_base + (uint32_t)(pass * phases_per_pass(c.p->L) + phase + 1);
+}
+
+__device__ __forceinline__ bool status_set(const KParams* p, uint32_t epoch) {
+  uint64_t s = __hip_atomic_load(G(p->status), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return (uint32_t)(s >> 32) == epoch && (int32_t)(uint32_t)s != 0;
+}
+__device__ __forceinline__ void status_raise(const KParams* p, uint32_t epoch, int code) {
+  __hip_atomic_store(G(p->status), ((uint64_t)epoch << 32) | (uint32_t)code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Poll n tagged words; addr(i) gives word i, sink(i, payload) receives it.
+// Per-thread words: i = tid, tid + kThreads, ... Returns false if this thread gave up.
+template <typename Addr, typename Sink>
+__device__ __forceinline__ bool poll_words(const Ctx& c, int n, uint32_t tag, Addr addr, Sink sink) {
+  for (int base = 0; base < n; base += 4 * kThreads) {
+    int idx[4];
+    bool got[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      idx[k] = base + k * kThreads + (int)threadIdx.x;
+      got[k] = idx[k] >= n;
+    }
+    uint64_t t0 = 0;
+    int spins = 0;
+    while (true) {
+      uint64_t v[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (!got[k]) v[k] = xload(addr(idx[k]));
+      bool all = true;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!got[k]) {
+          if ((uint32_t)(v[k] >> 32) == tag) {
+            got[k] = true;
+            sink(idx[k], (uint32_t)v[k]);
+          } else {
+            all = false;
+          }
+        }
+      }
+      if (all) break;
+      if ((++spins & 31) == 0) {
+        uint64_t now = dclock();
+        if (t0 == 0) {
+          t0 = now;
+        } else if (now - t0 > kTimeoutTicks) {
+          status_raise(c.p, c.tag_base, RVQSD_ETIMEOUT);
+          return false;
+        }
+        if (status_set(c.p, c.tag_base)) return false;
+      }
+    }
+  }
+  return true;
+}
+
+template <typename Sink>
+__device__ __forceinline__ bool poll_range(const Ctx& c, const uint64_t* src, int n, uint32_t tag, Sink sink) {
+  return poll_words(c, n, tag, [=](int i) { return src + i; }, sink);
+}
+
+// Barrier of the workgroup that also agrees on abort.
+__device__ __forceinline__ bool wg_sync_ok(const Ctx& c, bool ok) {
+  if (!ok) c.sh->abort = 1;
+  __syncthreads();
+  return c.sh->abort == 0;
+}
+
+// --------------------------------------------------------------- weights
+
+template <typename WT>
+__device__ __forceinline__ const WT* wptr(const KParams* p, uint64_t off) {
+  return reinterpret_cast<const WT*>(p->wbase + off);
+}
+__device__ __forceinline__ const float* fptr(const KParams* p, uint64_t off) {
+  return reinterpret_cast<const float*>(p->wbase + off);
+}
+__device__ __forceinline__ uint64_t layer_off(const KParams* p, int l, uint64_t o) {
+  return (uint64_t)l * p->layer_stride + o;
+}
+
+// ------------------------------------------------------------------ GEMV
+// Computes out[r][m] = sum_k W[row r][k] * X[m][k] for the workgroup's nrows
+// rows (r < nrows) and MR activation rows. Thread (rg, kc): kc = 16-byte chunk
+// of the reduction dimension, rg = row group; rows r = rg + i * n_rg.
+// The weight chunks of the first batch are loaded before the activations are
+// awaited, so the weight stream overlaps the wait.
+
+template <typename WT, int MR, int RPT>
+struct Gemv {
+  static constexpr int EPC = WTraits<WT>::EPC;
+  int nkc, n_rg, rg, kc, nrows;
+  bool active;
+  W16 wreg[RPT];
+
+  __device__ __forceinline__ void setup(int K, int nrows_) {
+    nkc = K / EPC;
+    n_rg = kThreads / nkc;
+    rg = (int)threadIdx.x / nkc;
+    kc = (int)threadIdx.x % nkc;
+    active = rg < n_rg;
+    nrows = nrows_;
+  }
+  template <typename RowPtr>
+  __device__ __forceinline__ void load(int batch, RowPtr rowptr) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      int r = rg + (batch * RPT + i) * n_rg;
+      if (active && r < nrows) {
+        const WT* w = rowptr(r) + (size_t)kc * EPC;
+        wreg[i] = *G(reinterpret_cast<const W16*>(w));
+      } else {
+        wreg[i] = (W16)(0u);
+      }
+    }
+  }
+  // xg: this thread's activation chunk [MR][EPC]; results to out[r * MR + m] (LDS)
+  template <typename RowPtr>
+  __device__ __forceinline__ void run(const Ctx& c, const float (&xg)[MR][EPC], RowPtr rowptr, float* out) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int rows_per_thread = (nrows + n_rg - 1) / n_rg;
+    const int nbatch = (rows_per_thread + RPT - 1) / RPT;
+    const int wpg = nkc / 64;  // waves per row group
+    for (int b = 0; b < nbatch; ++b) {
+      if (b > 0) load(b, rowptr);
+      float acc[RPT][MR];
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        float w[EPC];
+        WTraits<WT>::widen(wreg[i], w);
+#pragma unroll
+        for (int m = 0; m < MR; ++m) {
+          float a = 0.f;
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) a = fmaf(w[e], xg[m][e], a);
+          acc[i][m] = a;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < RPT; ++i)
+#pragma unroll
+        for (int m = 0; m < MR; ++m) {
+          float v = wave_sum(acc[i][m]);
+          if (lane == 0) c.red[wave * (RPT * MR) + i * MR + m] = v;
+        }
+      __syncthreads();
+      const int total = n_rg * RPT * MR;
+      for (int t = threadIdx.x; t < total; t += kThreads) {
+        int g = t / (RPT * MR), im = t % (RPT * MR), i = im / MR, m = im % MR;
+        int r = g + (b * RPT + i) * n_rg;
+        if (r < nrows) {
+          float s = 0.f;
+          for (int w = g * wpg; w < (g + 1) * wpg; ++w) s += c.red[w * (RPT * MR) + im];
+          out[r * MR + m] = s;
+        }
+      }
+      __syncthreads();
+    }
+  }
+};
+
+// thread's chunk from staged LDS activations xs[MR][ld], optionally * gain[k] * rstd[m]
+template <int MR, int EPC>
+__device__ __forceinline__ void chunk_from_lds(const float* xs, int ld, int kc, const float* gain, const float* rstd,
+                                               float (&xg)[MR][EPC]) {
+  float g[EPC];
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) g[e] = gain ? G(gain)[kc * EPC + e] : 1.f;
+#pragma unroll
+  for (int m = 0; m < MR; ++m) {
+    float r = rstd ? rstd[m] : 1.f;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) xg[m][e] = xs[m * ld + kc * EPC + e] * g[e] * r;
+  }
+}
+
+// Stage R rows of a tagged activation buffer [kMaxRows][ncols] into LDS xs[MR][ncols]
+// (rows >= R zero-filled).
+template <int MR>
+__device__ __forceinline__ bool stage_tagged(const Ctx& c, const uint64_t* src, int ncols, int R, uint32_t tag, float* xs) {
+  for (int i = threadIdx.x; i < (MR - R) * ncols; i += kThreads) xs[R * ncols + i] = 0.f;
+  bool ok = poll_range(c, src, R * ncols, tag, [&](int i, uint32_t v) { xs[i] = __uint_as_float(v); });
+  return wg_sync_ok(c, ok);
+}
+
+// rstd[m] = 1 / sqrt(mean(xs[m]^2) + eps) for m < R, 0 above.
+template <int MR>
+__device__ __forceinline__ void row_rstd(const Ctx& c, const float* xs, int ncols, int R) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int m = wave; m < MR; m += kWaves) {
+    float s = 0.f;
+    if (m < R)
+      for (int k = lane; k < ncols; k += 64) s += xs[m * ncols + k] * xs[m * ncols + k];
+    s = wave_sum(s);
+    if (lane == 0) c.sh->rstd[m] = m < R ? 1.f / sqrtf(s / (float)ncols + c.p->rms_eps) : 0.f;
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------- pass phases
+
+// Layer-0 input rows: position 0 = frame hidden vector, position s >= 1 = E_{s-1}[code consumed at s].
+template <typename WT, int MR>
+__device__ __forceinline__ void gather_rows(const Ctx& c, float* xs) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows;
+  for (int i = threadIdx.x; i < MR * H; i += kThreads) {
+    int r = i / H, k = i % H;
+    float v = 0.f;
+    if (r < R) {
+      int s = sh->first_pos + r;
+      if (s == 0) {
+        v = G(sh->fa.frame_hidden)[k];
+      } else {
+        const WT* tab = wptr<WT>(p, p->o_emb0 + (uint64_t)(s - 1) * p->table_stride);
+        v = WTraits<WT>::one(tab, (size_t)sh->in_code[s] * H + k);
+      }
+    }
+    xs[i] = v;
+  }
+  __syncthreads();
+}
+
+template <typename WT, int MR, int RPT>
+__device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows, N = p->nqkv;
+  const int rpw = (N + p->nwg - 1) / p->nwg, row0 = blockIdx.x * rpw;
+  const int nrows = max(0, min(rpw, N - row0));
+  const WT* wq = wptr<WT>(p, layer_off(p, l, p->o_wq));
+  const WT* wk = wptr<WT>(p, layer_off(p, l, p->o_wk));
+  const WT* wv = wptr<WT>(p, layer_off(p, l, p->o_wv));
+  const int qd = p->qdim, kd = p->kvdim;
+  auto rowptr = [&](int r) -> const WT* {
+    int o = row0 + r;
+    if (o < qd) return wq + (size_t)o * H;
+    if (o < qd + kd) return wk + (size_t)(o - qd) * H;
+    return wv + (size_t)(o - qd - kd) * H;
+  };
+  Gemv<WT, MR, RPT> g;
+  g.setup(H, nrows);
+  g.load(0, rowptr);
+  float* xs = c.work;
+  float* out = c.work + MR * H;
+  if (l == 0) {
+    gather_rows<WT, MR>(c, xs);
+    // keep this workgroup's residual columns
+    const int o0 = blockIdx.x * c.cpw;
+    for (int i = threadIdx.x; i < kMaxRows * c.cpw; i += kThreads) {
+      int m = i / c.cpw, j = i % c.cpw;
+      c.xown[i] = (m < MR && o0 + j < H) ? xs[m * H + o0 + j] : 0.f;
+    }
+  } else {
+    if (nrows == 0) return true;
+    if (!stage_tagged<MR>(c, p->xb, H, R, tag_of(c, sh->pass, 5 * (l - 1) + kPhDown), xs)) return false;
+  }
+  row_rstd<MR>(c, xs, H, R);
+  if (nrows > 0) {
+    float xg[MR][Gemv<WT, MR, RPT>::EPC];
+    if (g.active) chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, fptr(p, layer_off(p, l, p->o_attn_norm)), sh->rstd, xg);
+    g.run(c, xg, rowptr, out);
+    const uint32_t tag = tag_of(c, sh->pass, 5 * l + kPhQKV);
+    for (int i = threadIdx.x; i < R * nrows; i += kThreads) {
+      int m = i / nrows, r = i % nrows;
+      xstoref(p->qkvb + (size_t)m * N + row0 + r, tag, out[r * MR + m]);
+    }
+  }
+  return true;
+}
+
+// Attention for query head h = blockIdx.x (h < nq). Keeps this head's KV cache.
+template <int MR>
+__device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int h = blockIdx.x;
+  if (h >= p->nq) return true;
+  const int d = p->d, R = sh->rows, N = p->nqkv, fp = sh->first_pos;
+  const int g = h / (p->nq / p->nkv);
+  const int qoff = h * d, koff = p->qdim + g * d, voff = p->qdim + p->kvdim + g * d;
+  float* qs = c.work;              // [R][d]
+  float* ks = qs + kMaxRows * d;   // [R][d]
+  float* vs = ks + kMaxRows * d;   // [R][d]
+  float* kc = vs + kMaxRows * d;   // [kMaxPos][d]
+  float* vc = kc + kMaxPos * d;    // [kMaxPos][d]
+  float* sc = vc + kMaxPos * d;    // [kMaxRows][kMaxPos]
+  const uint32_t tag = tag_of(c, sh->pass, 5 * l + kPhQKV);
+  // q of head h, k and v of kv head g, for every row of the pass; qs, ks, vs are
+  // consecutive [kMaxRows][d] blocks and v of kv head g follows k at +kvdim
+  const int rd = R * d, kvdim = p->kvdim;
+  const uint64_t* qkvb = p->qkvb;
+  bool ok = poll_words(
+      c, 3 * rd, tag,
+      [=](int i) {
+        const int part = i / rd, rem = i - part * rd, r = rem / d, k = rem - r * d;
+        const int off = part == 0 ? qoff : koff + (part - 1) * kvdim;
+        return qkvb + (size_t)r * N + off + k;
+      },
+      [=](int i, uint32_t v) {
+        const int part = i / rd, rem = i - part * rd;
+        qs[part * kMaxRows * d + rem] = __uint_as_float(v);
+      });
+  if (!wg_sync_ok(c, ok)) return false;
+  // per-head RMSNorm of q and k, then rotate-half RoPE at the row's position
+  const float* qn = fptr(p, layer_off(p, l, p->o_qn));
+  const float* kn = fptr(p, layer_off(p, l, p->o_kn));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int v = wave; v < 2 * R; v += kWaves) {
+    float* x = v < R ? qs + v * d : ks + (v - R) * d;
+    const float* gn = v < R ? qn : kn;
+    const int r = v < R ? v : v - R;
+    float s = 0.f;
+    for (int i = lane; i < d; i += 64) s += x[i] * x[i];
+    s = wave_sum(s);
+    const float rs = p->qk_norm ? 1.f / sqrtf(s / (float)d + p->rms_eps) : 1.f;
+    const int pos = fp + r, half = d / 2;
+    for (int i = lane; i < half; i += 64) {
+      float a = x[i], b = x[i + half];
+      if (p->qk_norm) {
+        a = a * rs * G(gn)[i];
+        b = b * rs * G(gn)[i + half];
+      }
+      double theta = (double)pos * pow(p->rope_base, -2.0 * (double)i / (double)d);
+      float cs = (float)cos(theta), sn = (float)sin(theta);
+      x[i] = a * cs - b * sn;
+      x[i + half] = b * cs + a * sn;
+    }
+  }
+  __syncthreads();
+  // append k, v of this pass's rows to the private cache, then read positions 0..fp+R-1
+  RVQSD_GLOBAL float* cache = G(p->kvc) + ((size_t)h * p->L + l) * kMaxPos * 2 * d;
+  for (int i = threadIdx.x; i < R * d; i += kThreads) {
+    int r = i / d, k = i % d;
+    cache[((size_t)(fp + r) * 2 + 0) * d + k] = ks[i];
+    cache[((size_t)(fp + r) * 2 + 1) * d + k] = vs[i];
+  }
+  __syncthreads();
+  const int npos = fp + R;
+  for (int i = threadIdx.x; i < npos * d; i += kThreads) {
+    int t = i / d, k = i % d;
+    kc[i] = cache[((size_t)t * 2 + 0) * d + k];
+    vc[i] = cache[((size_t)t * 2 + 1) * d + k];
+  }
+  __syncthreads();
+  const float scale = 1.f / sqrtf((float)d);
+  for (int i = threadIdx.x; i < R * npos; i += kThreads) {
+    int r = i / npos, t = i % npos;
+    float s = -INFINITY;
+    if (t <= fp + r) {
+      s = 0.f;
+      for (int k = 0; k < d; ++k) s = fmaf(qs[r * d + k], kc[t * d + k], s);
+      s *= scale;
+    }
+    sc[r * kMaxPos + t] = s;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < R) {
+    const int r = threadIdx.x;
+    float mx = -INFINITY;
+    for (int t = 0; t <= fp + r; ++t) mx = fmaxf(mx, sc[r * kMaxPos + t]);
+    float z = 0.f;
+    for (int t = 0; t <= fp + r; ++t) {
+      float e = expf(sc[r * kMaxPos + t] - mx);
+      sc[r * kMaxPos + t] = e;
+      z += e;
+    }
+    for (int t = 0; t <= fp + r; ++t) sc[r * kMaxPos + t] /= z;
+  }
+  __syncthreads();
+  const uint32_t otag = tag_of(c, sh->pass, 5 * l + kPhAttn);
+  for (int i = threadIdx.x; i < R * d; i += kThreads) {
+    int r = i / d, k = i % d;
+    float o = 0.f;
+    for (int t = 0; t <= fp + r; ++t) o = fmaf(sc[r * kMaxPos + t], vc[t * d + k], o);
+    xstoref(p->attnb + (size_t)r * p->qdim + qoff + k, otag, o);
+  }
+  return true;
+}
+
+// O projection (layer l) or down projection: x_own += W * act; publish x_own.
+template <typename WT, int MR, int RPT>
+__device__ __forceinline__ bool phase_proj(const Ctx& c, int l, bool is_down) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows;
+  const int K = is_down ? p->F : p->qdim;
+  const int row0 = blockIdx.x * c.cpw;
+  const int nrows = max(0, min(c.cpw, H - row0));
+  const WT* W = wptr<WT>(p, layer_off(p, l, is_down ? p->o_wd : p->o_wo));
+  auto rowptr = [&](int r) -> const WT* { return W + (size_t)(row0 + r) * K; };
+  if (nrows == 0) return true;
+  Gemv<WT, MR, RPT> g;
+  g.setup(K, nrows);
+  g.load(0, rowptr);
+  const uint64_t* src = is_down ? p->actb : p->attnb;
+  const uint32_t tag = tag_of(c, sh->pass, 5 * l + (is_down ? kPhGU : kPhAttn));
+  constexpr int EPC = Gemv<WT, MR, RPT>::EPC;
+  float xg[MR][EPC];
+  float* out = c.work + (size_t)MR * p->stage_cols;
+  if (K <= p->stage_cols) {
+    float* xs = c.work;
+    if (!stage_tagged<MR>(c, src, K, R, tag, xs)) return false;
+    if (g.active) chunk_from_lds<MR, EPC>(xs, K, g.kc, nullptr, nullptr, xg);
+  } else {
+    // one thread per chunk (n_rg == 1): poll the chunk directly
+    bool ok = true;
+#pragma unroll
+    for (int m = 0; m < MR; ++m)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) xg[m][e] = 0.f;
+    if (g.active) {
+      for (int m = 0; m < R && ok; ++m) {
+        const uint64_t* s = src + (size_t)m * K + (size_t)g.kc * EPC;
+        uint64_t t0 = 0;
+        int spins = 0;
+        int have = 0;
+        while (have != (1 << EPC) - 1) {
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) {
+            if (!(have & (1 << e))) {
+              uint64_t v = xload(s + e);
+              if ((uint32_t)(v >> 32) == tag) {
+                have |= 1 << e;
+#pragma unroll
+                for (int mm = 0; mm < MR; ++mm)
+                  if (mm == m) xg[mm][e] = __uint_as_float((uint32_t)v);
+              }
+            }
+          }
+          if (have == (1 << EPC) - 1) break;
+          if ((++spins & 31) == 0) {
+            uint64_t now = dclock();
+            if (t0 == 0) t0 = now;
+            else if (now - t0 > kTimeoutTicks) { status_raise(p, c.tag_base, RVQSD_ETIMEOUT); ok = false; break; }
+            if (status_set(p, c.tag_base)) { ok = false; break; }
+          }
+        }
+      }
+    }
+    if (!wg_sync_ok(c, ok)) return false;
+  }
+  if (nrows > 0) {
+    g.run(c, xg, rowptr, out);
+    const uint32_t otag = tag_of(c, sh->pass, 5 * l + (is_down ? kPhDown : kPhO));
+    for (int i = threadIdx.x; i < R * nrows; i += kThreads) {
+      int m = i / nrows, r = i % nrows;
+      float v = c.xown[m * c.cpw + r] + out[r * MR + m];
+      c.xown[m * c.cpw + r] = v;
+      xstoref(p->xb + (size_t)m * H + row0 + r, otag, v);
+    }
+  }
+  __syncthreads();
+  return true;
+}
+
+template <typename WT, int MR, int RPT>
+__device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows, F = p->F;
+  const int fpw = (F + p->nwg - 1) / p->nwg, f0 = blockIdx.x * fpw;
+  const int nf = max(0, min(fpw, F - f0));
+  const WT* wg = wptr<WT>(p, layer_off(p, l, p->o_wg));
+  const WT* wu = wptr<WT>(p, layer_off(p, l, p->o_wu));
+  auto rowptr = [&](int r) -> const WT* { return ((r & 1) ? wu : wg) + (size_t)(f0 + (r >> 1)) * H; };
+  Gemv<WT, MR, RPT> g;
+  g.setup(H, 2 * nf);
+  g.load(0, rowptr);
+  if (nf == 0) return true;
+  float* xs = c.work;
+  float* out = c.work + MR * H;
+  if (!stage_tagged<MR>(c, p->xb, H, R, tag_of(c, sh->pass, 5 * l + kPhO), xs)) return false;
+  row_rstd<MR>(c, xs, H, R);
+  {
+    float xg[MR][Gemv<WT, MR, RPT>::EPC];
+    if (g.active) chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, fptr(p, layer_off(p, l, p->o_mlp_norm)), sh->rstd, xg);
+    g.run(c, xg, rowptr, out);
+    const uint32_t tag = tag_of(c, sh->pass, 5 * l + kPhGU);
+    for (int i = threadIdx.x; i < R * nf; i += kThreads) {
+      int m = i / nf, j = i % nf;
+      float gt = out[(2 * j) * MR + m], up = out[(2 * j + 1) * MR + m];
+      float a = gt / (1.f + expf(-gt)) * up;
+      xstoref(p->actb + (size_t)m * F + f0 + j, tag, a);
+    }
+  }
+  return true;
+}
+
+// Pass geometry helpers ---------------------------------------------------
+// verify rows: prefix -> row 1 only; later passes -> every row.
+__device__ __forceinline__ bool is_verify_row(const Shared* sh, int r) { return sh->pass == 0 ? r == 1 : true; }
+// rows whose position can become the next anchor (and therefore need drafts)
+__device__ __forceinline__ int drafts_of_row(const KParams* p, const Shared* sh, int r) {
+  const int s = sh->first_pos + r;
+  if (s < 1 || s > p->n_codes - 1) return 0;
+  if (sh->pass == 0 && r != 1) return 0;
+  return min(p->K, p->n_codes - s);
+}
+__device__ __forceinline__ int draft_slot(const KParams* p, int r, int j) { return kSlotDraft0 + r * p->K + (j - 1); }
+
+template <typename WT, int MR, int RPT>
+__device__ __forceinline__ bool phase_heads(const Ctx& c) {
+  const KParams* p = c.p;
+  Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows, V = p->V, L = p->L;
+  // heads touched by this pass
+  int t_lo = 1 << 20, t_hi = -1;
+  for (int r = 0; r < R; ++r) {
+    const int s = sh->first_pos + r;
+    if (is_verify_row(sh, r) && s >= 1) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
+    const int nd = drafts_of_row(p, sh, r);
+    if (nd > 0) { t_lo = min(t_lo, s + 1); t_hi = max(t_hi, s + nd); }
+  }
+  const int nh = t_hi - t_lo + 1;
+  const int wph = p->nwg / nh;
+  const int hi = blockIdx.x / wph;
+  const int t = t_lo + hi;
+  const int rpw = (V + wph - 1) / wph, v0 = (blockIdx.x % wph) * rpw;
+  const int nrows = hi < nh ? max(0, min(rpw, V - v0)) : 0;
+  if (nrows == 0) return true;
+  // this head's vectors: (row, offset j); j = 0 is the verify row at position t
+  if (threadIdx.x == 0) {
+    int nv = 0;
+    for (int r = 0; r < R && nv < MR; ++r) {
+      const int s = sh->first_pos + r;
+      if (s == t && is_verify_row(sh, r)) {
+        sh->hv_row[nv] = r; sh->hv_off[nv] = 0; sh->hv_slot[nv] = r; ++nv;
+      }
+      const int nd = drafts_of_row(p, sh, r);
+      const int j = t - s;
+      if (j >= 1 && j <= nd && nv < MR) {
+        sh->hv_row[nv] = r; sh->hv_off[nv] = j; sh->hv_slot[nv] = draft_slot(p, r, j); ++nv;
+      }
+    }
+    sh->hv_n = nv;
+  }
+  const WT* W = wptr<WT>(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
+  auto rowptr = [&](int r) -> const WT* { return W + (size_t)(v0 + r) * H; };
+  Gemv<WT, MR, RPT> g;
+  g.setup(H, nrows);
+  g.load(0, rowptr);
+  float* xs = c.work;
+  float* out = c.work + MR * H;
+  if (!stage_tagged<MR>(c, p->xb, H, R, tag_of(c, sh->pass, 5 * (L - 1) + kPhDown), xs)) return false;
+  row_rstd<MR>(c, xs, H, R);
+  constexpr int EPC = Gemv<WT, MR, RPT>::EPC;
+  float xg[MR][EPC];
+  const float* gn = fptr(p, p->o_final_norm);
+  const float* ofs = fptr(p, p->o_offsets);
+  const int nv = sh->hv_n;
+#pragma unroll
+  for (int v = 0; v < MR; ++v) {
+    const bool use = g.active && v < nv;
+    const int vr = use ? sh->hv_row[v] : 0, vo = use ? sh->hv_off[v] : 0;
+    const float rs = use ? sh->rstd[vr] : 0.f;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+      float val = 0.f;
+      if (use) {
+        const int k = g.kc * EPC + e;
+        val = xs[vr * H + k] * rs * G(gn)[k];
+        if (vo > 0) val += G(ofs)[(size_t)(vo - 1) * H + k];
+      }
+      xg[v][e] = val;
+    }
+  }
+  g.run(c, xg, rowptr, out);
+  const uint32_t tag = tag_of(c, sh->pass, ph_heads(L));
+  for (int i = threadIdx.x; i < nv * nrows; i += kThreads) {
+    const int v = i / nrows, r = i % nrows;
+    xstoref(p->logb + ((size_t)(sh->pass & 1) * p->n_slots + sh->hv_slot[v]) * V + v0 + r, tag, out[r * MR + v]);
+  }
+  return true;
+}
+
+// --------------------------------------------------------------- sampling
+// order-preserving key of a float; NaN lowest
+__device__ __forceinline__ uint32_t fkey(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// exclusive prefix over the workgroup in thread order; returns total via *total
+__device__ __forceinline__ int block_excl_scan(Shared* sh, int v, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = wave_scan_incl(v);
+  if (lane == 63) sh->iscan[wave] = inc;
+  __syncthreads();
+  int off = 0, tot = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    if (w < wave) off += sh->iscan[w];
+    tot += sh->iscan[w];
+  }
+  __syncthreads();
+  *total = tot;
+  return off + inc - v;
+}
+
+// Top-k of lg[V] (ties -> lower index), support in ascending token order:
+// sidx[n], slog[n]. Returns n (<= topk).
+__device__ __forceinline__ int topk_select(const Ctx& c, const float* lg, int V, int topk, int* sidx, float* slog) {
+  Shared* sh = c.sh;
+  const int ept = (V + kThreads - 1) / kThreads;
+  const int i0 = threadIdx.x * ept;
+  const int kk0 = min(topk, V);
+  uint32_t prefix = 0, pmask = 0;
+  int kk = kk0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = threadIdx.x; i < 256; i += kThreads) sh->hist[i] = 0;
+    __syncthreads();
+    for (int e = 0; e < ept; ++e) {
+      int i = i0 + e;
+      if (i < V) {
+        uint32_t k = fkey(lg[i]);
+        if ((k & pmask) == prefix) atomicAdd(&sh->hist[(k >> shift) & 255u], 1u);
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const int lane = threadIdx.x;
+      int b[4], loc = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { b[q] = (int)sh->hist[4 * lane + q]; loc += b[q]; }
+      // number of elements in bins of higher lanes
+      int incl_from_top = loc;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        int t = __shfl_down(incl_from_top, o, 64);
+        if (lane + o < 64) incl_from_top += t;
+      }
+      int above = incl_from_top - loc;
+#pragma unroll
+      for (int q = 3; q >= 0; --q) {
+        if (above < kk && kk <= above + b[q]) {
+          sh->sel_digit = 4 * lane + q;
+          sh->sel_kk = kk - above;
+        }
+        above += b[q];
+      }
+    }
+    __syncthreads();
+    prefix |= (uint32_t)sh->sel_digit << shift;
+    pmask |= 255u << shift;
+    kk = sh->sel_kk;
+    __syncthreads();
+  }
+  // prefix = key of the kk0-th largest; take every key above it and the kk lowest-index equal keys
+  int n_eq = 0;
+  for (int e = 0; e < ept; ++e) {
+    int i = i0 + e;
+    if (i < V && fkey(lg[i]) == prefix) ++n_eq;
+  }
+  int tot;
+  int eq_before = block_excl_scan(sh, n_eq, &tot);
+  int n_sel = 0;
+  unsigned selmask = 0;
+  for (int e = 0; e < ept; ++e) {
+    int i = i0 + e;
+    if (i >= V) break;
+    uint32_t k = fkey(lg[i]);
+    bool s = k > prefix;
+    if (k == prefix) {
+      s = eq_before < kk;
+      ++eq_before;
+    }
+    if (s) { selmask |= 1u << e; ++n_sel; }
+  }
+  int pos = block_excl_scan(sh, n_sel, &tot);
+  for (int e = 0; e < ept; ++e) {
+    if (selmask & (1u << e)) {
+      sidx[pos] = i0 + e;
+      slog[pos] = lg[i0 + e];
+      ++pos;
+    }
+  }
+  __syncthreads();
+  return tot;
+}
+
+// wave 0: probabilities of the top-k support, p = exp((l - max)/T) / Z in fp64
+__device__ __forceinline__ void softmax_support(const float* slog, int n, double T, double* prob) {
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  double mx = -INFINITY;
+  for (int i = lane; i < n; i += 64) mx = fmax(mx, (double)slog[i]);
+  mx = wave_maxd(mx);
+  double z = 0.0;
+  for (int i = lane; i < n; i += 64) {
+    double w = exp(((double)slog[i] - mx) / T);
+    prob[i] = w;
+    z += w;
+  }
+  z = wave_sumd(z);
+  for (int i = lane; i < n; i += 64) prob[i] = prob[i] / z;
+}
+
+// wave 0: inverse CDF of weights w[0..n) (ascending token order) at u; returns position
+__device__ __forceinline__ int inverse_cdf(const double* w, int n, double u) {
+  const int lane = threadIdx.x;
+  const int per = (n + 63) / 64;
+  const int b = lane * per;
+  double loc = 0.0;
+  for (int q = 0; q < per; ++q)
+    if (b + q < n) loc += w[b + q];
+  double incl = wave_scan_incld(loc);
+  double z = __shfl(incl, 63, 64);
+  double thr = u * z;
+  double cum = incl - loc;
+  int found = -1;
+  for (int q = 0; q < per; ++q) {
+    if (b + q < n) {
+      cum += w[b + q];
+      if (found < 0 && cum > thr) found = b + q;
+    }
+  }
+  unsigned long long bal = __ballot(found >= 0);
+  if (bal) {
+    int src = __ffsll((long long)bal) - 1;
+    return __shfl(found, src, 64);
+  }
+  int last = -1;
+  for (int q = 0; q < per; ++q)
+    if (b + q < n && w[b + q] > 0.0) last = b + q;
+  for (int o = 32; o > 0; o >>= 1) last = max(last, __shfl_xor(last, o, 64));
+  return last < 0 ? n - 1 : last;
+}
+
+__device__ __forceinline__ double ufetch(const Shared* sh, int s, int slot) {
+  return (double)G(sh->fa.uniforms)[(s - 1) * 3 + slot];
+}
+
+// Role of this workgroup's slot in the sampling phase: row >= 0 if active;
+// j = 0 for a verify row, else draft offset j of that row.
+__device__ __forceinline__ void slot_role(const KParams* p, const Shared* sh, int slot, int* row, int* j) {
+  *row = -1;
+  *j = 0;
+  const int R = sh->rows;
+  if (slot < kSlotDraft0) {
+    if (slot < R && is_verify_row(sh, slot)) *row = slot;
+  } else if (p->K > 0) {
+    const int q = slot - kSlotDraft0;
+    const int r = q / p->K, jj = q % p->K + 1;
+    if (r < R && jj <= drafts_of_row(p, sh, r)) {
+      *row = r;
+      *j = jj;
+    }
+  }
+}
+
+__device__ __forceinline__ int support_size(const KParams* p) { return p->topk < p->V ? p->topk : p->V; }
+
+template <int MR>
+__device__ __forceinline__ bool phase_sample(const Ctx& c) {
+  const KParams* p = c.p;
+  Shared* sh = c.sh;
+  const int V = p->V, slot = blockIdx.x, par = sh->pass & 1;
+  int row, j;
+  slot_role(p, sh, slot, &row, &j);
+  if (row < 0) return true;
+  const uint32_t tag = tag_of(c, sh->pass, ph_heads(p->L));
+  const uint32_t otag = tag_of(c, sh->pass, ph_sample(p->L));
+  float* lg = c.work;                                          // [V]
+  int* sidx = reinterpret_cast<int*>(lg + V);                  // [kMaxTopk]
+  float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);     // [kMaxTopk]
+  double* prob = reinterpret_cast<double*>(
+      (reinterpret_cast<uintptr_t>(slog + kMaxTopk) + 7) & ~(uintptr_t)7);  // [kMaxTopk]
+  double* qprob = prob + kMaxTopk;                             // [kMaxTopk]
+  double* res = qprob + kMaxTopk;                              // [kMaxTopk]
+  int* qidx = reinterpret_cast<int*>(res + kMaxTopk);          // [kMaxTopk]
+  const uint64_t* src = p->logb + ((size_t)par * p->n_slots + slot) * V;
+  bool ok = poll_range(c, src, V, tag, [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); });
+  if (!wg_sync_ok(c, ok)) return false;
+  if (p->tr_logits && sh->pass < p->tr_max_rounds)
+    for (int i = threadIdx.x; i < V; i += kThreads)
+      G(p->tr_logits)[((size_t)sh->pass * p->n_slots + slot) * V + i] = lg[i];
+  const int n = topk_select(c, lg, V, p->topk, sidx, slog);
+  if (threadIdx.x < 64) {
+    bool fin = false;
+    for (int i = threadIdx.x; i < n; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
+    if (!__any(fin) && threadIdx.x == 0) status_raise(p, c.tag_base, RVQSD_ENUMERIC);
+  }
+  softmax_support(slog, n, p->temperature, prob);
+  __syncthreads();
+  const int t = sh->first_pos + row + j;  // code position decided by this slot
+  if (j > 0) {
+    // draft for position t from the hidden state of `row` plus offset b_j
+    uint64_t* rec = p->drec + ((size_t)par * p->n_slots + slot) * p->drec_words;
+    if (threadIdx.x < 64) {
+      int pos;
+      if (p->greedy) {
+        double best = -1.0;
+        int bi = n;
+        for (int i = threadIdx.x; i < n; i += 64)
+          if (prob[i] > best) { best = prob[i]; bi = i; }
+        for (int o = 32; o > 0; o >>= 1) {
+          double ob = __shfl_xor(best, o, 64);
+          int oi = __shfl_xor(bi, o, 64);
+          if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+        }
+        pos = bi;
+      } else {
+        pos = inverse_cdf(prob, n, ufetch(sh, t, 0));
+      }
+      if (threadIdx.x == 0) sh->tok = sidx[pos];
+    }
+    __syncthreads();
+    const int nq = p->greedy ? 1 : n;
+    const int tok = sh->tok;
+    for (int i = threadIdx.x; i < nq; i += kThreads) {
+      const int idx = p->greedy ? tok : sidx[i];
+      const double pr = p->greedy ? 1.0 : prob[i];
+      const uint64_t bits = (uint64_t)__double_as_longlong(pr);
+      xstore(rec + 1 + 3 * i + 0, otag, (uint32_t)idx);
+      xstore(rec + 1 + 3 * i + 1, otag, (uint32_t)bits);
+      xstore(rec + 1 + 3 * i + 2, otag, (uint32_t)(bits >> 32));
+    }
+    if (threadIdx.x == 0) xstore(rec, otag, (uint32_t)tok);
+    return true;
+  }
+  // verify row at position t
+  const int jv = t - sh->m;  // 1-based draft index in this round
+  if (sh->pass > 0 && jv <= sh->kp) {
+    // accept test of d_t against q_t, drafted last pass from the anchor's row
+    const int prev_slot = draft_slot(p, sh->prev_anchor_row, jv);
+    const uint64_t* rec = p->drec + ((size_t)(par ^ 1) * p->n_slots + prev_slot) * p->drec_words;
+    const uint32_t ptag = tag_of(c, sh->pass - 1, ph_sample(p->L));
+    const int nq = p->greedy ? 1 : support_size(p);
+    ok = poll_range(c, rec + 1, 3 * nq, ptag, [&](int i, uint32_t v) {
+      const int e = i / 3, f = i % 3;
+      if (f == 0) qidx[e] = (int)v;
+      else reinterpret_cast<uint32_t*>(qprob + e)[f - 1] = v;
+    });
+    if (!wg_sync_ok(c, ok)) return false;
+    if (threadIdx.x < 64) {
+      const int d = sh->drafts[t];
+      double pd = 0.0, qd = 0.0;
+      for (int i = threadIdx.x; i < n; i += 64)
+        if (sidx[i] == d) pd = prob[i];
+      for (int i = threadIdx.x; i < nq; i += 64)
+        if (qidx[i] == d) qd = qprob[i];
+      pd = wave_sumd(pd);
+      qd = wave_sumd(qd);
+      const bool accept = ufetch(sh, t, 1) * qd < pd;
+      int tok = d;
+      if (!accept) {
+        // residual max(0, p - q) on p's support; q looked up by binary search (ascending tokens)
+        double rs = 0.0;
+        for (int i = threadIdx.x; i < n; i += 64) {
+          const int x = sidx[i];
+          int lo = 0, hi2 = nq;
+          while (lo < hi2) {
+            const int mid = (lo + hi2) >> 1;
+            if (qidx[mid] < x) lo = mid + 1;
+            else hi2 = mid;
+          }
+          const double qx = (lo < nq && qidx[lo] == x) ? qprob[lo] : 0.0;
+          const double v = prob[i] - qx;
+          res[i] = v > 0.0 ? v : 0.0;
+          rs += res[i];
+        }
+        rs = wave_sumd(rs);
+        if (!(rs > 0.0))
+          for (int i = threadIdx.x; i < n; i += 64) res[i] = prob[i];
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        const int pos = inverse_cdf(res, n, ufetch(sh, t, 2));
+        tok = sidx[pos];
+      }
+      if (threadIdx.x == 0) xstore(p->vres + (size_t)par * kMaxRows + row, otag, (uint32_t)tok | (accept ? 0x80000000u : 0u));
+    }
+  } else {
+    // the prefix token c_1, or the extra token after every draft was accepted
+    if (threadIdx.x < 64) {
+      const int pos = inverse_cdf(prob, n, ufetch(sh, t, 2));
+      if (threadIdx.x == 0) xstore(p->vres + (size_t)par * kMaxRows + row, otag, (uint32_t)sidx[pos]);
+    }
+  }
+  return true;
+}
+
+// Read every verdict and every candidate draft token of the pass just sampled
+// (one word per thread), commit codes, pick the next anchor and its drafts.
+// Returns false on abort. Leaves sh->m == n_codes when the frame is complete.
+__device__ __forceinline__ bool commit_and_advance(const Ctx& c) {
+  const KParams* p = c.p;
+  Shared* sh = c.sh;
+  const int n = p->n_codes, par = sh->pass & 1, R = sh->rows, K = p->K;
+  const uint32_t tag = tag_of(c, sh->pass, ph_sample(p->L));
+  __shared__ uint32_t vr[kMaxRows];
+  __shared__ int dtok[kMaxRows][kMaxCodes + 1];
+  __shared__ short wlist[kMaxRows * (kMaxCodes + 1)];  // r * 16 + j, j = 0 for the verdict of row r
+  __shared__ int nlist;
+  if (threadIdx.x == 0) {
+    int k = 0;
+    for (int r = 0; r < R; ++r) {
+      if (is_verify_row(sh, r)) wlist[k++] = (short)(r * 16);
+      const int nd = drafts_of_row(p, sh, r);
+      for (int jj = 1; jj <= nd; ++jj) wlist[k++] = (short)(r * 16 + jj);
+    }
+    nlist = k;
+  }
+  __syncthreads();
+  bool ok = poll_words(
+      c, nlist, tag,
+      [=](int i) -> const uint64_t* {
+        const int e = wlist[i], r = e >> 4, jj = e & 15;
+        if (jj == 0) return p->vres + (size_t)par * kMaxRows + r;
+        return p->drec + ((size_t)par * p->n_slots + draft_slot(p, r, jj)) * p->drec_words;
+      },
+      [&](int i, uint32_t v) {
+        const int e = wlist[i], r = e >> 4, jj = e & 15;
+        if (jj == 0) vr[r] = v;
+        else dtok[r][jj] = (int)v;
+      });
+  if (!wg_sync_ok(c, ok)) return false;
+  if (threadIdx.x == 0) {
+    const int m = sh->m, kp = sh->kp;
+    int m_new = -1, acc = 0, tok = -1;
+    if (sh->pass == 0) {
+      sh->codes[1] = (int)(vr[1] & 0x7fffffffu);
+      m_new = 1;
+      tok = sh->codes[1];
+    } else {
+      for (int j = 1; j <= kp; ++j) {
+        const uint32_t v = vr[j - 1];
+        if (v & 0x80000000u) {
+          sh->codes[m + j] = sh->drafts[m + j];
+          ++acc;
+          sh->st_mask |= 1u << (m + j);
+        } else {
+          sh->codes[m + j] = (int)(v & 0x7fffffffu);
+          m_new = m + j;
+          tok = sh->codes[m_new];
+          break;
+        }
+      }
+      if (m_new < 0) {
+        if (R > kp) {
+          sh->codes[m + kp + 1] = (int)(vr[kp] & 0x7fffffffu);
+          m_new = m + kp + 1;
+          tok = sh->codes[m_new];
+        } else {
+          m_new = n;
+        }
+      }
+      sh->st_rounds += 1;
+      sh->st_drafted += kp;
+      sh->st_accepted += acc;
+    }
+    sh->st_calls += 1;
+    if (blockIdx.x == 0 && p->tr_rounds && sh->pass < p->tr_max_rounds) {
+      int32_t* tr = p->tr_rounds + (size_t)sh->pass * kTraceRoundInts;
+      tr[0] = m; tr[1] = kp; tr[2] = sh->first_pos; tr[3] = R; tr[4] = m_new; tr[5] = acc; tr[6] = tok;
+      tr[7] = sh->pass;
+      for (int j = 1; j <= kp; ++j) tr[7 + j] = sh->drafts[m + j];
+    }
+    if (m_new < n) {
+      const int arow = m_new - sh->first_pos;
+      const int nd = min(K, n - m_new);
+      for (int jj = 1; jj <= nd; ++jj) sh->drafts[m_new + jj] = dtok[arow][jj];
+      sh->prev_anchor_row = arow;
+      sh->kp = nd;
+      sh->rows = min(nd + 1, n - m_new);
+      sh->first_pos = m_new + 1;
+      sh->in_code[m_new + 1] = sh->codes[m_new];
+      for (int r = 1; r < sh->rows; ++r) sh->in_code[m_new + 1 + r] = sh->drafts[m_new + r];
+    }
+    sh->m = m_new;
+    sh->pass += 1;
+  }
+  __syncthreads();
+  return true;
+}
+
+// algorithmic bytes one pass must read: layer weights, the heads it touches,
+// the gathered embedding rows and the KV cache it attends over
+__device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c, int wbytes) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  int t_lo = 1 << 20, t_hi = -1;
+  for (int r = 0; r < sh->rows; ++r) {
+    const int s = sh->first_pos + r;
+    if (is_verify_row(sh, r) && s >= 1) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
+    const int nd = drafts_of_row(p, sh, r);
+    if (nd > 0) { t_lo = min(t_lo, s + 1); t_hi = max(t_hi, s + nd); }
+  }
+  unsigned long long b = (unsigned long long)p->L * p->layer_stride;
+  b += (unsigned long long)(t_hi - t_lo + 1) * p->V * p->H * wbytes;
+  for (int r = 0; r < sh->rows; ++r) b += (sh->first_pos + r == 0) ? 4ull * p->H : (unsigned long long)p->H * wbytes;
+  b += (unsigned long long)p->L * (sh->first_pos + sh->rows) * p->nkv * p->d * 2 * 4;
+  return b;
+}
+
+template <typename WT, int MR>
+__global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
+  constexpr int RPT = MR <= 8 ? 8 : 4;
+  __shared__ Shared shs;
+  extern __shared__ float dyn[];
+  const KParams* p = gp;
+  Ctx c;
+  c.p = p;
+  c.sh = &shs;
+  c.cpw = (p->H + p->nwg - 1) / p->nwg;
+  c.dyn = dyn;
+  c.xown = dyn;
+  c.red = dyn + kMaxRows * c.cpw;
+  c.work = c.red + kWaves * RPT * MR;
+  c.tag_base = fa.epoch_base;
+  const uint64_t t_start = dclock();
+  const int c0 = fa.c0[0];
+  const bool c0_ok = c0 >= 0 && c0 < p->V;
+  if (threadIdx.x == 0) {
+    shs.fa = fa;
+    shs.abort = c0_ok ? 0 : 1;
+    shs.pass = 0;
+    shs.m = 0;
+    shs.kp = 0;
+    shs.first_pos = 0;
+    shs.rows = 2;
+    shs.prev_anchor_row = 0;
+    shs.codes[0] = c0;
+    shs.in_code[1] = c0;
+    shs.st_calls = shs.st_rounds = shs.st_drafted = shs.st_accepted = 0;
+    shs.st_mask = 0;
+    shs.st_bytes = 0;
+  }
+  __syncthreads();
+  bool ok = c0_ok;
+  const int wbytes = (int)sizeof(WT);
+  const int L = p->L;
+  while (ok) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) shs.st_bytes += pass_bytes(c, wbytes);
+    const bool clk_on = blockIdx.x == 0 && p->tr_clock && shs.pass < p->tr_max_rounds;
+    uint64_t* clk_row = clk_on ? p->tr_clock + (size_t)shs.pass * (phases_per_pass(L) + 1) : nullptr;
+    for (int l = 0; l < L && ok; ++l) {
+      ok = phase_qkv<WT, MR, RPT>(c, l);
+      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 0] = dclock();
+      if (ok) ok = phase_attn<MR>(c, l);
+      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 1] = dclock();
+      if (ok) ok = phase_proj<WT, MR, RPT>(c, l, false);
+      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 2] = dclock();
+      if (ok) ok = phase_gu<WT, MR, RPT>(c, l);
+      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 3] = dclock();
+      if (ok) ok = phase_proj<WT, MR, RPT>(c, l, true);
+      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 4] = dclock();
+    }
+    if (ok) ok = phase_heads<WT, MR, RPT>(c);
+    if (clk_on && threadIdx.x == 0) clk_row[ph_heads(L)] = dclock();
+    if (ok) ok = phase_sample<MR>(c);
+    if (clk_on && threadIdx.x == 0) clk_row[ph_sample(L)] = dclock();
+    ok = wg_sync_ok(c, ok);
+    if (ok) ok = commit_and_advance(c);
+    if (clk_on && threadIdx.x == 0) clk_row[ph_sample(L) + 1] = dclock();
+    if (!ok || shs.m >= p->n_codes) break;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    rvqsd_stats* st = fa.out_stats;
+    st->target_calls = shs.st_calls;
+    st->rounds = shs.st_rounds;
+    st->drafted = shs.st_drafted;
+    st->accepted = shs.st_accepted;
+    st->accept_mask = shs.st_mask;
+    const uint64_t sw = __hip_atomic_load(G(p->status), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int32_t status = ((uint32_t)(sw >> 32) == fa.epoch_base) ? (int32_t)(uint32_t)sw : 0;
+    if (!c0_ok) status = RVQSD_EINVAL;
+    if (status == 0 && !ok) status = RVQSD_ETIMEOUT;
+    st->status = status;
+    st->weight_bytes = shs.st_bytes;
+    st->clk_start = t_start;
+    st->clk_end = dclock();
+    for (int s2 = 1; s2 <= p->n_codes; ++s2) fa.out_codes[s2 - 1] = ok ? shs.codes[s2] : -1;
+  }
+}
+
+// ------------------------------------------------------------------- host
+
+int frame_max_rows(int K) {
+  const int need = K + 1 < 2 ? 2 : K + 1;
+  if (need <= 2) return 2;
+  if (need <= 4) return 4;
+  if (need <= 5) return 5;
+  if (need <= 8) return 8;
+  return 16;
+}
+
+// floats of the per-workgroup regions in front of the work area
+int frame_lds_head_floats(int mr, int cpw) {
+  const int rpt = mr <= 8 ? 8 : 4;
+  return kMaxRows * cpw + kWaves * rpt * mr;
+}
+
+template <typename WT, int MR>
+static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* stream, size_t lds, char* err, size_t errlen) {
+  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR>);
+  static size_t attr_bytes = 0;  // per instantiation
+  if (lds > attr_bytes) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) {
+      snprintf(err, errlen, "hipFuncSetAttribute(%zu bytes LDS): %s", lds, hipGetErrorString(e));
+      return RVQSD_EHIP;
+    }
+    attr_bytes = lds;
+  }
+  const KParams* gpp = gp;
+  FrameArgs fac = fa;
+  void* args[] = {&gpp, &fac};
+  hipError_t e = hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(kThreads), args, (unsigned)lds,
+                                            reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    snprintf(err, errlen, "hipLaunchCooperativeKernel: %s", hipGetErrorString(e));
+    return RVQSD_EHIP;
+  }
+  return RVQSD_OK;
+}
+
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream, size_t lds_bytes,
+                 char* err, size_t errlen) {
+#define RVQSD_CASE(T, M) \
+  if (mr == M) return launch_t<T, M>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+  if (dtype == RVQSD_DTYPE_F32) {
+    RVQSD_CASE(float, 2) RVQSD_CASE(float, 4) RVQSD_CASE(float, 5) RVQSD_CASE(float, 8) RVQSD_CASE(float, 16)
+  } else {
+    RVQSD_CASE(bf16_t, 2) RVQSD_CASE(bf16_t, 4) RVQSD_CASE(bf16_t, 5) RVQSD_CASE(bf16_t, 8) RVQSD_CASE(bf16_t, 16)
+  }
+#undef RVQSD_CASE
+  snprintf(err, errlen, "no kernel for %d rows", mr);
+  return RVQSD_EUNSUPPORTED;
+}
+
+}  // namespace rvqsd

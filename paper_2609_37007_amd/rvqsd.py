@@ -1,0 +1,211 @@
+"""Python binding of librvqsd.so (argument marshalling only).
+
+Every step of the decode runs in the HIP library; this module converts
+arguments and raises on error.  It fails loudly when the library is missing:
+there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "librvqsd.so")
+
+RVQSD_ABI_VERSION = 1
+OK, EINVAL, EBLOB, ENOMEM, EHIP, EUNSUPPORTED, ENUMERIC, ETIMEOUT = 0, -1, -2, -3, -4, -5, -6, -7
+DTYPE_F32, DTYPE_BF16 = 0, 1
+TRACE_ROUND_INTS = 32
+
+# every symbol include/rvqsd.h declares
+EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_stream_destroy",
+           "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_set_trace",
+           "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
+
+
+class rvqsd_cfg(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "abi_version", "n_layers", "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "n_codes", "vocab",
+        "max_draft", "dtype", "qk_norm", "topk", "draft_len", "draft_greedy")] + [
+        ("reserved", ctypes.c_int32 * 3), ("rms_eps", ctypes.c_double), ("rope_base", ctypes.c_double),
+        ("temperature", ctypes.c_double)]
+
+
+class rvqsd_weights(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("bytes", ctypes.c_uint64)]
+
+
+class rvqsd_stats(ctypes.Structure):
+    _fields_ = [("target_calls", ctypes.c_int32), ("rounds", ctypes.c_int32), ("drafted", ctypes.c_int32),
+                ("accepted", ctypes.c_int32), ("accept_mask", ctypes.c_uint32), ("status", ctypes.c_int32),
+                ("weight_bytes", ctypes.c_uint64), ("clk_start", ctypes.c_uint64), ("clk_end", ctypes.c_uint64)]
+
+    def as_dict(self):
+        return {k: int(getattr(self, k)) for k, _ in self._fields_}
+
+
+STATS_DTYPE = np.dtype([("target_calls", np.int32), ("rounds", np.int32), ("drafted", np.int32),
+                        ("accepted", np.int32), ("accept_mask", np.uint32), ("status", np.int32),
+                        ("weight_bytes", np.uint64), ("clk_start", np.uint64), ("clk_end", np.uint64)])
+assert STATS_DTYPE.itemsize == ctypes.sizeof(rvqsd_stats)
+
+
+class rvqsd_trace(ctypes.Structure):
+    _fields_ = [("logits", ctypes.c_void_p), ("rounds", ctypes.c_void_p), ("clock", ctypes.c_void_p),
+                ("max_rounds", ctypes.c_int32)]
+
+
+class rvqsd_info(ctypes.Structure):
+    _fields_ = [("workgroups", ctypes.c_int32), ("threads", ctypes.c_int32), ("max_rows", ctypes.c_int32),
+                ("trace_slots", ctypes.c_int32), ("lds_bytes", ctypes.c_uint64),
+                ("layer_weight_bytes", ctypes.c_uint64), ("head_bytes", ctypes.c_uint64),
+                ("emb_row_bytes", ctypes.c_uint64), ("device_weight_bytes", ctypes.c_uint64)]
+
+    def as_dict(self):
+        return {k: int(getattr(self, k)) for k, _ in self._fields_}
+
+
+class RvqsdError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load librvqsd.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_37007_amd.build_ext`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, vp, i32 = ctypes.POINTER, ctypes.c_void_p, ctypes.c_int32
+        L.rvqsd_create.argtypes = [P(rvqsd_weights), P(rvqsd_cfg), P(vp)]
+        L.rvqsd_destroy.argtypes = [vp]
+        L.rvqsd_destroy.restype = None
+        L.rvqsd_model_info.argtypes = [vp, P(rvqsd_info)]
+        L.rvqsd_stream_create.argtypes = [vp, vp, i32, P(vp)]
+        L.rvqsd_stream_destroy.argtypes = [vp]
+        L.rvqsd_stream_destroy.restype = None
+        L.rvqsd_decode_frame.argtypes = [vp, vp, i32, ctypes.c_uint64, vp, P(rvqsd_stats)]
+        L.rvqsd_decode_frame_u.argtypes = [vp, vp, i32, vp, vp, P(rvqsd_stats)]
+        L.rvqsd_decode_frame_async.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.rvqsd_set_trace.argtypes = [vp, P(rvqsd_trace)]
+        L.rvqsd_uniforms_from_seed.argtypes = [ctypes.c_uint64, i32, vp]
+        L.rvqsd_status_str.argtypes = [i32]
+        L.rvqsd_status_str.restype = ctypes.c_char_p
+        L.rvqsd_last_error.argtypes = []
+        L.rvqsd_last_error.restype = ctypes.c_char_p
+        for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_decode_frame",
+                  "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_set_trace", "rvqsd_uniforms_from_seed"):
+            getattr(L, n).restype = i32
+        _lib = L
+    return _lib
+
+
+def _check(st: int, what: str):
+    if st != OK:
+        raise RvqsdError(st, f"{what}: {lib().rvqsd_last_error().decode()}")
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def make_cfg(*, n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, n_codes, vocab, max_draft, dtype, topk,
+             temperature, draft_len, draft_greedy=0, qk_norm=1, rms_eps=1e-6, rope_base=1e6) -> rvqsd_cfg:
+    c = rvqsd_cfg()
+    c.abi_version = RVQSD_ABI_VERSION
+    for k, v in dict(n_layers=n_layers, hidden=hidden, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
+                     head_dim=head_dim, ffn=ffn, n_codes=n_codes, vocab=vocab, max_draft=max_draft, dtype=dtype,
+                     qk_norm=qk_norm, topk=topk, draft_len=draft_len, draft_greedy=draft_greedy).items():
+        setattr(c, k, int(v))
+    c.rms_eps, c.rope_base, c.temperature = float(rms_eps), float(rope_base), float(temperature)
+    return c
+
+
+def uniforms_from_seed(seed: int, n_codes: int = 15) -> np.ndarray:
+    out = np.zeros((n_codes, 3), dtype=np.float32)
+    _check(lib().rvqsd_uniforms_from_seed(ctypes.c_uint64(seed), n_codes, _ptr(out)), "rvqsd_uniforms_from_seed")
+    return out
+
+
+class Model:
+    """rvqsd_create / rvqsd_destroy / rvqsd_model_info."""
+
+    def __init__(self, blob: bytes, cfg: rvqsd_cfg):
+        self.cfg = cfg
+        self._blob = bytes(blob)
+        w = rvqsd_weights(ctypes.cast(ctypes.c_char_p(self._blob), ctypes.c_void_p), len(self._blob))
+        h = ctypes.c_void_p()
+        _check(lib().rvqsd_create(ctypes.byref(w), ctypes.byref(cfg), ctypes.byref(h)), "rvqsd_create")
+        self._h = h
+        self._blob = None  # the library copied the weights
+
+    def info(self) -> dict:
+        i = rvqsd_info()
+        _check(lib().rvqsd_model_info(self._h, ctypes.byref(i)), "rvqsd_model_info")
+        return i.as_dict()
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().rvqsd_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+
+class Stream:
+    """rvqsd_stream_create and the decode calls; ``hip_stream`` is a raw hipStream_t (int) or None."""
+
+    def __init__(self, model: Model, hip_stream=None, max_streams: int = 1):
+        self.model = model
+        self.n = model.cfg.n_codes
+        h = ctypes.c_void_p()
+        _check(lib().rvqsd_stream_create(model._h, ctypes.c_void_p(hip_stream or 0), max_streams, ctypes.byref(h)),
+               "rvqsd_stream_create")
+        self._h = h
+        self._trace = None
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().rvqsd_stream_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+    def decode_frame(self, frame_hidden, c0: int, rng_seed: int):
+        f = np.ascontiguousarray(frame_hidden, dtype=np.float32)
+        out = np.zeros(self.n, dtype=np.int32)
+        st = rvqsd_stats()
+        _check(lib().rvqsd_decode_frame(self._h, _ptr(f), int(c0), ctypes.c_uint64(rng_seed), _ptr(out),
+                                        ctypes.byref(st)), "rvqsd_decode_frame")
+        return out, st.as_dict()
+
+    def decode_frame_u(self, frame_hidden, c0: int, uniforms):
+        f = np.ascontiguousarray(frame_hidden, dtype=np.float32)
+        u = np.ascontiguousarray(uniforms, dtype=np.float32)
+        out = np.zeros(self.n, dtype=np.int32)
+        st = rvqsd_stats()
+        _check(lib().rvqsd_decode_frame_u(self._h, _ptr(f), int(c0), _ptr(u), _ptr(out), ctypes.byref(st)),
+               "rvqsd_decode_frame_u")
+        return out, st.as_dict()
+
+    def decode_frame_async(self, d_frame_hidden: int, d_c0: int, d_uniforms: int, d_out_codes: int, d_stats: int):
+        """Device pointers (ints, e.g. torch tensor data_ptr()); enqueues only."""
+        _check(lib().rvqsd_decode_frame_async(self._h, ctypes.c_void_p(d_frame_hidden), ctypes.c_void_p(d_c0),
+                                              ctypes.c_void_p(d_uniforms), ctypes.c_void_p(d_out_codes),
+                                              ctypes.c_void_p(d_stats)), "rvqsd_decode_frame_async")
+
+    def set_trace(self, logits_ptr: int = 0, rounds_ptr: int = 0, clock_ptr: int = 0, max_rounds: int = 0):
+        if not (logits_ptr or rounds_ptr or clock_ptr):
+            _check(lib().rvqsd_set_trace(self._h, None), "rvqsd_set_trace")
+            self._trace = None
+            return
+        t = rvqsd_trace(logits_ptr or None, rounds_ptr or None, clock_ptr or None, max_rounds)
+        _check(lib().rvqsd_set_trace(self._h, ctypes.byref(t)), "rvqsd_set_trace")
+        self._trace = t
