@@ -89,11 +89,13 @@ typedef struct {
  *  rounds: int32[max_rounds][32]: m, K', first_pos, rows, m_new, accepted, token,
  *          pass index, drafts d_{m+1..m+K'} at [8..8+K'), then reserved.
  *  clock:  uint64[max_rounds][5*n_layers+5]: device clock at each phase end of a pass
- *          (workgroup 0's view), last entry = pass end. */
+ *          (workgroup 0's view), last entry = pass end.
+ *  wg_clock: uint64[max_rounds][5*n_layers+5][workgroups]: the same for every workgroup. */
 typedef struct {
   float* logits;
   int32_t* rounds;
   uint64_t* clock;
+  uint64_t* wg_clock;
   int32_t max_rounds;
 } rvqsd_trace;
 
@@ -147,6 +149,12 @@ rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, in
  * Inputs must stay valid until the stream reaches the frame. */
 rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidden, const int32_t* d_c0,
                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats);
+
+/* Return a stream to its initial state. Needed after a frame enqueued with
+ * rvqsd_decode_frame_async reported a device-side error in its stats (later
+ * frames on the stream then fail with RVQSD_EHIP until the reset); the
+ * synchronous calls reset by themselves. Synchronises the stream. */
+rvqsd_status rvqsd_stream_reset(rvqsd_stream* s);
 
 /* Install (trace != NULL) or remove (NULL) a per-round trace for later frames of this stream. */
 rvqsd_status rvqsd_set_trace(rvqsd_stream* s, const rvqsd_trace* trace);

@@ -88,6 +88,7 @@ struct rvqsd_stream {
   int32_t* d_out;
   uint32_t epoch;       // tag base of the next frame
   uint32_t epoch_step;
+  size_t par_bytes;     // leading bytes of dbuf holding the parity-word buffers
 };
 
 namespace {
@@ -109,6 +110,9 @@ int validate_cfg(const rvqsd_cfg* c, int nwg) {
     return set_err(RVQSD_EUNSUPPORTED, "hidden, n_q_heads*head_dim and ffn must be multiples of %d", quant);
   if (c->hidden / epc > kThreads || qd / epc > kThreads || c->ffn / epc > kThreads)
     return set_err(RVQSD_EUNSUPPORTED, "a reduction dimension exceeds %d elements", kThreads * epc);
+  // every workgroup must take part in every full-activation phase (parity exchange)
+  if (c->hidden % nwg || (qd + 2 * c->n_kv_heads * c->head_dim) < nwg || c->ffn < nwg)
+    return set_err(RVQSD_EUNSUPPORTED, "hidden must be a multiple of, and q/k/v width and ffn at least, %d", nwg);
   if (c->head_dim % 64 || c->head_dim > 256) return set_err(RVQSD_EUNSUPPORTED, "head_dim must be 64, 128, 192 or 256");
   if (c->topk > kMaxTopk) return set_err(RVQSD_EUNSUPPORTED, "topk > %d", kMaxTopk);
   if (c->vocab > 16384) return set_err(RVQSD_EUNSUPPORTED, "vocab > 16384");
@@ -252,13 +256,28 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   const int cpw = (k.H + nwg - 1) / nwg;
   const size_t head = (size_t)frame_lds_head_floats(m->mr, cpw);
   const size_t budget = (size_t)prop.sharedMemPerBlock - 6 * 1024;  // leave room for static shared state
-  int stage = (int)(qd > F ? qd : F);
-  if ((head + work_floats(cfg, nwg, m->mr, stage)) * 4 > budget) stage = (int)(qd > H ? qd : H);
-  const size_t lds = (head + work_floats(cfg, nwg, m->mr, stage)) * 4;
+  // projections stage their input rows in LDS, except a down projection whose
+  // chunks have one thread each: it polls them directly
+  const int epc = cfg->dtype == RVQSD_DTYPE_F32 ? 4 : 8;
+  int stage = (int)(qd > H ? qd : H);
+  if (2 * ((int)F / epc) <= kThreads && (int)F > stage) stage = (int)F;
+  const size_t work = work_floats(cfg, nwg, m->mr, stage);
+  size_t lds = (head + work) * 4;
   if (lds > budget) {
     delete m;
     return set_err(RVQSD_EUNSUPPORTED, "needs %zu bytes of LDS per workgroup, %zu available", lds, budget);
   }
+  // the attention workgroups keep their KV cache (all layers) in LDS when it fits
+  const size_t kv_floats = (size_t)k.L * kMaxPos * 2 * k.d;
+  const size_t attn_const_floats = (size_t)k.L * 2 * k.d + (size_t)kMaxPos * k.d;  // gains + rotary table
+  lds += attn_const_floats * 4;
+  if (lds > budget) {
+    delete m;
+    return set_err(RVQSD_EUNSUPPORTED, "needs %zu bytes of LDS per workgroup, %zu available", lds, budget);
+  }
+  k.kv_in_lds = (lds + kv_floats * 4 <= budget) ? 1 : 0;
+  if (k.kv_in_lds) lds += kv_floats * 4;
+  k.work_floats = (int32_t)work;
   m->lds_bytes = lds;
   m->stage_cols = stage;
   k.stage_cols = stage;
@@ -318,11 +337,15 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     off += (bytes + 255) & ~(size_t)255;
     return at;
   };
-  const size_t o_x = take(kMaxRows * H * 8), o_qkv = take((size_t)kMaxRows * k.nqkv * 8),
-               o_attn = take((size_t)kMaxRows * k.qdim * 8), o_act = take((size_t)kMaxRows * k.F * 8),
+  // parity-word activation buffers first (one contiguous range, initialised to parity 1)
+  const size_t o_x = take(kMaxRows * H * 4), o_qkv = take((size_t)kMaxRows * k.nqkv * 4),
+               o_attn = take((size_t)kMaxRows * k.qdim * 4), o_act = take((size_t)kMaxRows * k.F * 4);
+  const size_t par_end = off;
+  const size_t o_pc = take(4),
                o_log = take((size_t)2 * k.n_slots * V * 8), o_vres = take((size_t)2 * kMaxRows * 8),
                o_drec = take((size_t)2 * k.n_slots * k.drec_words * 8),
                o_kvc = take((size_t)k.nq * k.L * kMaxPos * 2 * k.d * 4), o_status = take(8),
+               o_rope = take((size_t)kMaxPos * k.d * 4),
                o_in = take(((size_t)H + 3 * kMaxCodes + 4) * 4), o_out = take((kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64),
                o_kp = take(sizeof(KParams));
   s->dbuf_bytes = off;
@@ -332,6 +355,7 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     return set_err(RVQSD_ENOMEM, "stream buffers (%zu bytes): %s", off, hipGetErrorString(e));
   }
   e = hipMemset(s->dbuf, 0, off);
+  if (e == hipSuccess) e = hipMemsetD8((hipDeviceptr_t)s->dbuf, 0x01, par_end);
   if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_in, ((size_t)H + 3 * kMaxCodes + 4) * 4, hipHostMallocDefault);
   if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_out, (kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64, hipHostMallocDefault);
   if (e != hipSuccess) {
@@ -341,21 +365,38 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     return set_err(RVQSD_ENOMEM, "stream staging: %s", hipGetErrorString(e));
   }
   uint8_t* base = (uint8_t*)s->dbuf;
-  k.xb = (uint64_t*)(base + o_x);
-  k.qkvb = (uint64_t*)(base + o_qkv);
-  k.attnb = (uint64_t*)(base + o_attn);
-  k.actb = (uint64_t*)(base + o_act);
+  k.xb = (uint32_t*)(base + o_x);
+  k.qkvb = (uint32_t*)(base + o_qkv);
+  k.attnb = (uint32_t*)(base + o_attn);
+  k.actb = (uint32_t*)(base + o_act);
+  k.pass_count = (uint32_t*)(base + o_pc);
+  s->par_bytes = par_end;
   k.logb = (uint64_t*)(base + o_log);
   k.vres = (uint64_t*)(base + o_vres);
   k.drec = (uint64_t*)(base + o_drec);
   k.kvc = (float*)(base + o_kvc);
   k.status = (uint64_t*)(base + o_status);
+  k.rope = (const float*)(base + o_rope);
   s->status = k.status;
   s->d_in = (float*)(base + o_in);
   s->d_out = (int32_t*)(base + o_out);
   s->dkp = (KParams*)(base + o_kp);
   s->kp = k;
-  e = hipMemcpy(s->dkp, &s->kp, sizeof(KParams), hipMemcpyHostToDevice);
+  {
+    // rotary table: angle = position * base^(-2i/d), computed in double
+    const int half = k.d / 2;
+    float* tab = (float*)malloc((size_t)kMaxPos * half * 2 * sizeof(float));
+    if (!tab) e = hipErrorOutOfMemory;
+    for (int pos = 0; tab && pos < kMaxPos; ++pos)
+      for (int i = 0; i < half; ++i) {
+        const double th = (double)pos * pow(k.rope_base, -2.0 * (double)i / (double)k.d);
+        tab[(pos * half + i) * 2 + 0] = (float)cos(th);
+        tab[(pos * half + i) * 2 + 1] = (float)sin(th);
+      }
+    if (tab) e = hipMemcpy((void*)k.rope, tab, (size_t)kMaxPos * half * 2 * sizeof(float), hipMemcpyHostToDevice);
+    free(tab);
+  }
+  if (e == hipSuccess) e = hipMemcpy(s->dkp, &s->kp, sizeof(KParams), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipHostFree(s->h_in);
     (void)hipHostFree(s->h_out);
@@ -385,6 +426,7 @@ rvqsd_status rvqsd_set_trace(rvqsd_stream* s, const rvqsd_trace* t) {
   s->kp.tr_logits = t ? t->logits : nullptr;
   s->kp.tr_rounds = t ? t->rounds : nullptr;
   s->kp.tr_clock = t ? t->clock : nullptr;
+  s->kp.tr_wgclock = t ? t->wg_clock : nullptr;
   s->kp.tr_max_rounds = t ? t->max_rounds : 0;
   HIPCHK(hipStreamSynchronize(s->stream));
   HIPCHK(hipMemcpy(s->dkp, &s->kp, sizeof(KParams), hipMemcpyHostToDevice));
@@ -395,7 +437,9 @@ static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t
                                int32_t* d_codes, rvqsd_stats* d_stats) {
   // tags of stale words from earlier frames never equal a later frame's tags; on wrap, clear everything
   if ((uint64_t)s->epoch + 2ull * s->epoch_step >= 0xFFFFFFFFull) {
-    HIPCHK(hipMemsetAsync(s->dbuf, 0, (uint8_t*)s->d_in - (uint8_t*)s->dbuf, s->stream));
+    // clears the tagged words (and the pass count); parity words are left alone
+    HIPCHK(hipMemsetAsync((uint8_t*)s->dbuf + s->par_bytes, 0, (uint8_t*)s->d_in - (uint8_t*)s->dbuf - s->par_bytes,
+                          s->stream));
     s->epoch = s->epoch_step;
   }
   FrameArgs fa;
@@ -410,6 +454,16 @@ static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t
   int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, (void*)s->stream, s->m->lds_bytes, err,
                         sizeof(err));
   if (st) return set_err(st, "%s", err);
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_stream_reset(rvqsd_stream* s) {
+  if (!s) return set_err(RVQSD_EINVAL, "null stream");
+  HIPCHK(hipStreamSynchronize(s->stream));
+  // parity words back to parity 1, pass count and every tagged word back to 0
+  HIPCHK(hipMemset(s->dbuf, 0, (uint8_t*)s->d_in - (uint8_t*)s->dbuf));
+  HIPCHK(hipMemsetD8((hipDeviceptr_t)s->dbuf, 0x01, s->par_bytes));
+  s->epoch = s->epoch_step;
   return RVQSD_OK;
 }
 
@@ -445,7 +499,11 @@ rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, in
   HIPCHK(hipStreamSynchronize(s->stream));
   rvqsd_stats hs;
   memcpy(&hs, s->h_out + kMaxCodes + 1, sizeof(hs));
-  if (hs.status != RVQSD_OK) return set_err(hs.status, "device reported %s", rvqsd_status_str(hs.status));
+  if (hs.status != RVQSD_OK) {
+    const int dst = hs.status;
+    (void)rvqsd_stream_reset(s);
+    return set_err(dst, "device reported %s", rvqsd_status_str(dst));
+  }
   memcpy(out_codes, s->h_out, (size_t)n * 4);
   if (out_stats) *out_stats = hs;
   return RVQSD_OK;

@@ -49,7 +49,44 @@ __device__ __forceinline__ void xstore(uint64_t* p, uint32_t tag, uint32_t paylo
   __hip_atomic_store(G(p), ((uint64_t)tag << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void xstoref(uint64_t* p, uint32_t tag, float v) { xstore(p, tag, __float_as_uint(v)); }
+// activation word: fp32 with the lowest mantissa bit replaced by the epoch parity
+__device__ __forceinline__ void pstore(uint32_t* p, float v, uint32_t par) {
+  __hip_atomic_store(G(p), (__float_as_uint(v) & ~1u) | par, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t pload2(const uint32_t* p) {
+  return __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Workgroup barrier for LDS traffic only: global loads stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 __device__ __forceinline__ uint64_t dclock() { return __builtin_amdgcn_s_memrealtime(); }
+
+// Sum over the 16 lanes of a DPP row (every lane of the row gets the sum):
+// xor 1, xor 2 inside quads, then half-row mirror and row mirror.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
+  return v;
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_rows(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xF, false));
+}
+// Sum over the 64 lanes; the total is valid in lane 63 only.
+__device__ __forceinline__ float wave_sum63(float v) {
+  v = row16_sum(v);
+  v += dpp_rows<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+  v += dpp_rows<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+  return v;
+}
+__device__ __forceinline__ float lane63(float v) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63)); }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -149,9 +186,19 @@ struct Ctx {
   float* xown;      // [kMaxRows][cpw] residual columns owned by this workgroup
   float* red;       // [kWaves][RPT * MR] reduction scratch
   float* work;      // union area
+  float* kvlds;     // [L][kMaxPos][2][d] KV cache of this attention workgroup (when kept in LDS)
+  float* attn_const;  // [L][2][d] q/k norm gains, then [kMaxPos][d/2][2] rotary table (attention workgroups)
   int cpw;          // residual columns per workgroup
   uint32_t tag_base;
+  uint32_t pass0;   // passes this stream ran before this frame
 };
+
+// parity of the per-layer buffers (q/k/v, attention output, activation):
+// one write per layer per pass, so it alternates with every write
+__device__ __forceinline__ uint32_t par_layer(const Ctx& c, int pass, int l) {
+  return (uint32_t)(((uint64_t)(c.pass0 + pass) * (uint64_t)c.p->L + (uint64_t)l) & 1u);
+}
+constexpr uint32_t kParO = 0, kParDown = 1;  // residual stream: written after O, then after down
 
 __device__ __forceinline__ uint32_t tag_of(const Ctx& c, int pass, int phase) {
   return c.tag_base + (uint32_t)(pass * phases_per_pass(c.p->L) + phase + 1);
@@ -217,6 +264,55 @@ __device__ __forceinline__ bool poll_range(const Ctx& c, const uint64_t* src, in
   return poll_words(c, n, tag, [=](int i) { return src + i; }, sink);
 }
 
+// Poll n2 pairs of parity words; addr(i) gives pair i (8-byte aligned),
+// sink(i, lo, hi) receives both values once both carry parity `par`.
+template <typename Addr, typename Sink>
+__device__ __forceinline__ bool poll_pairs(const Ctx& c, int n2, uint32_t par, Addr addr, Sink sink) {
+  constexpr int B = 8;
+  for (int base = 0; base < n2; base += B * kThreads) {
+    int idx[B];
+    bool got[B];
+#pragma unroll
+    for (int k = 0; k < B; ++k) {
+      idx[k] = base + k * kThreads + (int)threadIdx.x;
+      got[k] = idx[k] >= n2;
+    }
+    uint64_t t0 = 0;
+    int spins = 0;
+    while (true) {
+      uint64_t v[B];
+#pragma unroll
+      for (int k = 0; k < B; ++k)
+        if (!got[k]) v[k] = pload2(addr(idx[k]));
+      bool all = true;
+#pragma unroll
+      for (int k = 0; k < B; ++k) {
+        if (!got[k]) {
+          const uint32_t lo = (uint32_t)v[k], hi = (uint32_t)(v[k] >> 32);
+          if ((lo & 1u) == par && (hi & 1u) == par) {
+            got[k] = true;
+            sink(idx[k], __uint_as_float(lo), __uint_as_float(hi));
+          } else {
+            all = false;
+          }
+        }
+      }
+      if (all) break;
+      if ((++spins & 31) == 0) {
+        const uint64_t now = dclock();
+        if (t0 == 0) {
+          t0 = now;
+        } else if (now - t0 > kTimeoutTicks) {
+          status_raise(c.p, c.tag_base, RVQSD_ETIMEOUT);
+          return false;
+        }
+        if (status_set(c.p, c.tag_base)) return false;
+      }
+    }
+  }
+  return true;
+}
+
 // Barrier of the workgroup that also agrees on abort.
 __device__ __forceinline__ bool wg_sync_ok(const Ctx& c, bool ok) {
   if (!ok) c.sh->abort = 1;
@@ -244,12 +340,15 @@ __device__ __forceinline__ uint64_t layer_off(const KParams* p, int l, uint64_t 
 // The weight chunks of the first batch are loaded before the activations are
 // awaited, so the weight stream overlaps the wait.
 
-template <typename WT, int MR, int RPT>
+template <typename WT, int MR, int RPT, bool PIPE = false>
 struct Gemv {
   static constexpr int EPC = WTraits<WT>::EPC;
+  static constexpr int NVR = (RPT + 1) * MR;  // reduced values per wave: rows x MR, then MR sums of squares
   int nkc, n_rg, rg, kc, nrows;
   bool active;
   W16 wreg[RPT];
+  W16 wnext[PIPE ? RPT : 1];
+  float gain[EPC];  // this thread's chunk of an RMSNorm gain (prefetched with the weights)
 
   __device__ __forceinline__ void setup(int K, int nrows_) {
     nkc = K / EPC;
@@ -260,84 +359,270 @@ struct Gemv {
     nrows = nrows_;
   }
   template <typename RowPtr>
-  __device__ __forceinline__ void load(int batch, RowPtr rowptr) {
+  __device__ __forceinline__ void load_into(W16 (&dst)[RPT], int batch, RowPtr rowptr) {
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
-      int r = rg + (batch * RPT + i) * n_rg;
+      const int r = rg + (batch * RPT + i) * n_rg;
       if (active && r < nrows) {
         const WT* w = rowptr(r) + (size_t)kc * EPC;
-        wreg[i] = *G(reinterpret_cast<const W16*>(w));
+        dst[i] = *G(reinterpret_cast<const W16*>(w));
       } else {
-        wreg[i] = (W16)(0u);
+        dst[i] = (W16)(0u);
       }
     }
   }
-  // xg: this thread's activation chunk [MR][EPC]; results to out[r * MR + m] (LDS)
   template <typename RowPtr>
-  __device__ __forceinline__ void run(const Ctx& c, const float (&xg)[MR][EPC], RowPtr rowptr, float* out) {
+  __device__ __forceinline__ void load(int batch, RowPtr rowptr) {
+    load_into(wreg, batch, rowptr);
+  }
+  __device__ __forceinline__ void load_gain(const float* gsrc) {
+#pragma unroll
+    for (int e = 0; e < EPC; ++e)
+      gain[e] = active ? G(gsrc)[kc * EPC + e] : 1.f;
+  }
+  // out[r * MR + m] = sum_k W[r][k] * xg[m][k] (LDS), times rstd_m when sq != nullptr,
+  // where sq[m] is this thread's sum of squares of the raw activation chunk and
+  // rstd_m = 1 / sqrt(sum_k x[m][k]^2 / K + eps). Each value is summed over the
+  // wave with DPP (total in lane 63), then over the waves of its row group in LDS.
+  template <typename RowPtr>
+  __device__ __forceinline__ void run(const Ctx& c, const float (&xg)[MR][EPC], RowPtr rowptr, float* out,
+                                      const float* sq = nullptr) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int rows_per_thread = (nrows + n_rg - 1) / n_rg;
     const int nbatch = (rows_per_thread + RPT - 1) / RPT;
     const int wpg = nkc / 64;  // waves per row group
+    const float inv_k = 1.f / (float)(nkc * EPC);
+    if (sq) {
+#pragma unroll
+      for (int m = 0; m < MR; ++m) {
+        const float v = wave_sum63((rg == 0 && active) ? sq[m] : 0.f);
+        if (lane == 63) c.red[wave * NVR + RPT * MR + m] = v;
+      }
+    }
     for (int b = 0; b < nbatch; ++b) {
-      if (b > 0) load(b, rowptr);
-      float acc[RPT][MR];
+      if constexpr (PIPE) {
+        if (b + 1 < nbatch) load_into(wnext, b + 1, rowptr);
+      } else {
+        if (b > 0) load(b, rowptr);
+      }
+      const int nb = min(RPT, rows_per_thread - b * RPT);  // uniform across the workgroup
 #pragma unroll
       for (int i = 0; i < RPT; ++i) {
-        float w[EPC];
-        WTraits<WT>::widen(wreg[i], w);
+        if (i < nb) {
+          float w[EPC];
+          WTraits<WT>::widen(wreg[i], w);
 #pragma unroll
-        for (int m = 0; m < MR; ++m) {
-          float a = 0.f;
+          for (int m = 0; m < MR; ++m) {
+            float a = 0.f;
 #pragma unroll
-          for (int e = 0; e < EPC; ++e) a = fmaf(w[e], xg[m][e], a);
-          acc[i][m] = a;
+            for (int e = 0; e < EPC; ++e) a = fmaf(w[e], xg[m][e], a);
+            a = wave_sum63(a);
+            if (lane == 63) c.red[wave * NVR + i * MR + m] = a;
+          }
         }
       }
-#pragma unroll
-      for (int i = 0; i < RPT; ++i)
-#pragma unroll
-        for (int m = 0; m < MR; ++m) {
-          float v = wave_sum(acc[i][m]);
-          if (lane == 0) c.red[wave * (RPT * MR) + i * MR + m] = v;
-        }
-      __syncthreads();
-      const int total = n_rg * RPT * MR;
+      lds_barrier();
+      const int total = n_rg * nb * MR;
       for (int t = threadIdx.x; t < total; t += kThreads) {
-        int g = t / (RPT * MR), im = t % (RPT * MR), i = im / MR, m = im % MR;
-        int r = g + (b * RPT + i) * n_rg;
+        const int g = t / (nb * MR), im = t % (nb * MR), i = im / MR, m = im % MR;
+        const int r = g + (b * RPT + i) * n_rg;
         if (r < nrows) {
-          float s = 0.f;
-          for (int w = g * wpg; w < (g + 1) * wpg; ++w) s += c.red[w * (RPT * MR) + im];
-          out[r * MR + m] = s;
+          float sum = 0.f;
+          for (int w = g * wpg; w < (g + 1) * wpg; ++w) sum += c.red[w * NVR + im];
+          if (sq) {
+            float ss = 0.f;
+            for (int w = 0; w < wpg; ++w) ss += c.red[w * NVR + RPT * MR + m];
+            sum *= 1.f / sqrtf(ss * inv_k + c.p->rms_eps);
+          }
+          out[r * MR + m] = sum;
         }
       }
-      __syncthreads();
+      lds_barrier();
+      if constexpr (PIPE) {
+#pragma unroll
+        for (int i = 0; i < RPT; ++i) wreg[i] = wnext[i];
+      }
     }
   }
 };
 
-// thread's chunk from staged LDS activations xs[MR][ld], optionally * gain[k] * rstd[m]
-template <int MR, int EPC>
-__device__ __forceinline__ void chunk_from_lds(const float* xs, int ld, int kc, const float* gain, const float* rstd,
-                                               float (&xg)[MR][EPC]) {
-  float g[EPC];
+// ---------------------------------------------------------- MFMA GEMV (bf16)
+// Weights stream straight from HBM into the A operand of
+// v_mfma_f32_16x16x32_bf16 (16 weight rows x 32 k per instruction). The fp32
+// activations form the B operand (32 k x 16 columns, one column per activation
+// row) as a bf16 pair hi + lo with x - hi - lo below 2^-17 |x|, so two
+// instructions give an almost fp32-exact product. Lane layout (verified on
+// gfx950): lane l holds A[l%16][8*(l/16) + j], B[8*(l/16) + j][l%16] and
+// D[4*(l/16) + v][l%16].
+// Work items are (16-row tile t, 32-wide k-block kb) pairs g = t*KB + kb; wave w
+// takes g = w, w+8, w+16, ... (KB is a multiple of 8, so every wave covers every
+// tile with consecutive items); each wave writes its partial tiles to LDS and the
+// workgroup adds the 8 partials.
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <typename WT>
+struct IsBf16 {
+  static constexpr bool value = false;
+};
+template <>
+struct IsBf16<bf16_t> {
+  static constexpr bool value = true;
+};
+
+__device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+// x ~= hi + lo, both rounded to nearest even bf16
+__device__ __forceinline__ void split_bf16(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
+  W16 h, l;
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) g[e] = gain ? G(gain)[kc * EPC + e] : 1.f;
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t a = bf16_bits_rne(x[2 * j]), b = bf16_bits_rne(x[2 * j + 1]);
+    const uint32_t c2 = bf16_bits_rne(x[2 * j] - __uint_as_float(a << 16));
+    const uint32_t d2 = bf16_bits_rne(x[2 * j + 1] - __uint_as_float(b << 16));
+    h[j] = a | (b << 16);
+    l[j] = c2 | (d2 << 16);
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+template <int MR, int IMAX, bool PIPE = false>
+struct MGemv {
+  int KB, ntiles, n_items, nrows, wave, lane;
+  W16 a[IMAX];
+  W16 an[PIPE ? IMAX : 1];
+
+  __device__ __forceinline__ void setup(int K, int nrows_) {
+    KB = K >> 5;
+    nrows = nrows_;
+    ntiles = (nrows + 15) >> 4;
+    n_items = (ntiles * KB) >> 3;
+    wave = threadIdx.x >> 6;
+    lane = threadIdx.x & 63;
+  }
+  template <typename RowPtr>
+  __device__ __forceinline__ void load_into(W16 (&dst)[IMAX], int chunk, RowPtr rowptr) {
+#pragma unroll
+    for (int i = 0; i < IMAX; ++i) {
+      const int ii = chunk * IMAX + i;
+      W16 v = (W16)(0u);
+      if (ii < n_items) {
+        const int g = wave + 8 * ii, t = g / KB, kb = g - t * KB, row = (t << 4) + (lane & 15);
+        if (row < nrows) v = *G(reinterpret_cast<const W16*>(rowptr(row) + kb * 32 + 8 * (lane >> 4)));
+      }
+      dst[i] = v;
+    }
+  }
+  template <typename RowPtr>
+  __device__ __forceinline__ void load(RowPtr rowptr) {
+    load_into(a, 0, rowptr);
+  }
+  __device__ __forceinline__ void flush(float* red, const f32x4& acc, int t) const {
+    const int base = (wave * ntiles + t) << 8;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) red[base + ((4 * (lane >> 4) + v) << 4) + (lane & 15)] = acc[v];
+  }
+  // Item range [ii_lo, ii_hi) of this wave; acc and cur_t carry over between calls.
+  template <typename RowPtr, typename BSrc>
+  __device__ __forceinline__ void mma_items(int ii_lo, int ii_hi, RowPtr rowptr, BSrc bsrc, float* red, f32x4& acc,
+                                            int& cur_t) {
+    const int nch = (ii_hi + IMAX - 1) / IMAX;
+    for (int ch = ii_lo / IMAX; ch < nch; ++ch) {
+      if (ch > ii_lo / IMAX || ch > 0) {
+        if constexpr (PIPE) {
+#pragma unroll
+          for (int i = 0; i < IMAX; ++i) a[i] = an[i];
+        } else {
+          if (ch > 0) load_into(a, ch, rowptr);
+        }
+      }
+      if constexpr (PIPE) {
+        if (ch + 1 < nch) load_into(an, ch + 1, rowptr);
+      }
+#pragma unroll
+      for (int i = 0; i < IMAX; ++i) {
+        const int ii = ch * IMAX + i;
+        if (ii >= ii_lo && ii < ii_hi) {
+          const int g = wave + 8 * ii, t = g / KB, kb = g - t * KB;
+          if (t != cur_t) {
+            flush(red, acc, cur_t);
+            acc = (f32x4){0.f, 0.f, 0.f, 0.f};
+            cur_t = t;
+          }
+          float x[8];
+          const int m = lane & 15, k0 = kb * 32 + 8 * (lane >> 4);
+          if (m < MR) {
+            bsrc(k0, m, x);
+          } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[j] = 0.f;
+          }
+          bf16x8 hi, lo;
+          split_bf16(x, hi, lo);
+          const bf16x8 av = __builtin_bit_cast(bf16x8, a[i]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, acc, 0, 0, 0);
+        }
+      }
+    }
+  }
+  // out[r * MR + m] = sum over the 8 wave partials (r < nrows, m < MR)
+  __device__ __forceinline__ void reduce(const float* red, float* out) const {
+    for (int o = threadIdx.x; o < nrows * MR; o += kThreads) {
+      const int r = o / MR, m = o - r * MR, t = r >> 4, i = r & 15;
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) s += red[((w * ntiles + t) << 8) + (i << 4) + m];
+      out[o] = s;
+    }
+  }
+  // whole product from one staged activation block
+  template <typename RowPtr, typename BSrc>
+  __device__ __forceinline__ void run(RowPtr rowptr, BSrc bsrc, float* red, float* out) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    int cur_t = 0;
+    mma_items(0, n_items, rowptr, bsrc, red, acc, cur_t);
+    flush(red, acc, cur_t);
+    lds_barrier();
+    reduce(red, out);
+    lds_barrier();
+  }
+};
+
+// This thread's chunk of the staged activations xs[MR][ld] (k = kc*EPC ..),
+// times g[e] when g != nullptr; sq[m] = sum of squares of the raw chunk.
+// Threads outside the row groups get zeros.
+template <int MR, int EPC>
+__device__ __forceinline__ void chunk_from_lds(const float* xs, int ld, int kc, bool active, const float* g,
+                                               float (&xg)[MR][EPC], float (&sq)[MR]) {
 #pragma unroll
   for (int m = 0; m < MR; ++m) {
-    float r = rstd ? rstd[m] : 1.f;
+    float s2 = 0.f;
 #pragma unroll
-    for (int e = 0; e < EPC; ++e) xg[m][e] = xs[m * ld + kc * EPC + e] * g[e] * r;
+    for (int e = 0; e < EPC; ++e) {
+      const float x = active ? xs[m * ld + kc * EPC + e] : 0.f;
+      s2 = fmaf(x, x, s2);
+      xg[m][e] = g ? x * g[e] : x;
+    }
+    sq[m] = s2;
   }
 }
 
-// Stage R rows of a tagged activation buffer [kMaxRows][ncols] into LDS xs[MR][ncols]
-// (rows >= R zero-filled).
+// Stage R rows of a parity activation buffer [kMaxRows][ncols] into LDS
+// xs[MR][ncols] (rows >= R zero-filled).
 template <int MR>
-__device__ __forceinline__ bool stage_tagged(const Ctx& c, const uint64_t* src, int ncols, int R, uint32_t tag, float* xs) {
+__device__ __forceinline__ bool stage_par(const Ctx& c, const uint32_t* src, int ncols, int R, uint32_t par, float* xs) {
   for (int i = threadIdx.x; i < (MR - R) * ncols; i += kThreads) xs[R * ncols + i] = 0.f;
-  bool ok = poll_range(c, src, R * ncols, tag, [&](int i, uint32_t v) { xs[i] = __uint_as_float(v); });
+  const bool ok = poll_pairs(
+      c, R * ncols / 2, par, [=](int i) { return src + 2 * i; },
+      [=](int i, float lo, float hi) {
+        xs[2 * i] = lo;
+        xs[2 * i + 1] = hi;
+      });
   return wg_sync_ok(c, ok);
 }
 
@@ -349,8 +634,8 @@ __device__ __forceinline__ void row_rstd(const Ctx& c, const float* xs, int ncol
     float s = 0.f;
     if (m < R)
       for (int k = lane; k < ncols; k += 64) s += xs[m * ncols + k] * xs[m * ncols + k];
-    s = wave_sum(s);
-    if (lane == 0) c.sh->rstd[m] = m < R ? 1.f / sqrtf(s / (float)ncols + c.p->rms_eps) : 0.f;
+    s = wave_sum63(s);
+    if (lane == 63) c.sh->rstd[m] = m < R ? 1.f / sqrtf(s / (float)ncols + c.p->rms_eps) : 0.f;
   }
   __syncthreads();
 }
@@ -400,6 +685,7 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
   Gemv<WT, MR, RPT> g;
   g.setup(H, nrows);
   g.load(0, rowptr);
+  g.load_gain(fptr(p, layer_off(p, l, p->o_attn_norm)));
   float* xs = c.work;
   float* out = c.work + MR * H;
   if (l == 0) {
@@ -412,106 +698,101 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
     }
   } else {
     if (nrows == 0) return true;
-    if (!stage_tagged<MR>(c, p->xb, H, R, tag_of(c, sh->pass, 5 * (l - 1) + kPhDown), xs)) return false;
+    if (!stage_par<MR>(c, p->xb, H, R, kParDown, xs)) return false;
   }
-  row_rstd<MR>(c, xs, H, R);
   if (nrows > 0) {
-    float xg[MR][Gemv<WT, MR, RPT>::EPC];
-    if (g.active) chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, fptr(p, layer_off(p, l, p->o_attn_norm)), sh->rstd, xg);
-    g.run(c, xg, rowptr, out);
-    const uint32_t tag = tag_of(c, sh->pass, 5 * l + kPhQKV);
-    for (int i = threadIdx.x; i < R * nrows; i += kThreads) {
-      int m = i / nrows, r = i % nrows;
-      xstoref(p->qkvb + (size_t)m * N + row0 + r, tag, out[r * MR + m]);
+    float xg[MR][Gemv<WT, MR, RPT>::EPC], sq[MR];
+    chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, g.active, g.gain, xg, sq);
+    g.run(c, xg, rowptr, out, sq);
+    const uint32_t par = par_layer(c, sh->pass, l);
+    for (int i = threadIdx.x; i < MR * nrows; i += kThreads) {
+      const int m = i / nrows, r = i % nrows;
+      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
     }
   }
   return true;
 }
 
-// Attention for query head h = blockIdx.x (h < nq). Keeps this head's KV cache.
+// Attention for query head h = blockIdx.x (h < nq): per-head RMSNorm of q and k,
+// rotate-half RoPE, append k and v to this head's cache (LDS-resident when it
+// fits), causal softmax over positions 0..s of each row, output to attnb.
 template <int MR>
 __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
   const int h = blockIdx.x;
   if (h >= p->nq) return true;
-  const int d = p->d, R = sh->rows, N = p->nqkv, fp = sh->first_pos;
+  const int d = p->d, R = sh->rows, N = p->nqkv, fp = sh->first_pos, half = d / 2;
   const int g = h / (p->nq / p->nkv);
-  const int qoff = h * d, koff = p->qdim + g * d, voff = p->qdim + p->kvdim + g * d;
-  float* qs = c.work;              // [R][d]
-  float* ks = qs + kMaxRows * d;   // [R][d]
-  float* vs = ks + kMaxRows * d;   // [R][d]
-  float* kc = vs + kMaxRows * d;   // [kMaxPos][d]
-  float* vc = kc + kMaxPos * d;    // [kMaxPos][d]
-  float* sc = vc + kMaxPos * d;    // [kMaxRows][kMaxPos]
-  const uint32_t tag = tag_of(c, sh->pass, 5 * l + kPhQKV);
-  // q of head h, k and v of kv head g, for every row of the pass; qs, ks, vs are
-  // consecutive [kMaxRows][d] blocks and v of kv head g follows k at +kvdim
-  const int rd = R * d, kvdim = p->kvdim;
-  const uint64_t* qkvb = p->qkvb;
-  bool ok = poll_words(
-      c, 3 * rd, tag,
+  const int qoff = h * d, koff = p->qdim + g * d;
+  float* qs = c.work;              // [kMaxRows][d], then ks, vs
+  float* ks = qs + kMaxRows * d;
+  float* vs = ks + kMaxRows * d;
+  float* sc = vs + kMaxRows * d;   // [kMaxRows][kMaxPos]
+  float* cache = p->kv_in_lds ? c.kvlds + (size_t)l * kMaxPos * 2 * d
+                              : p->kvc + ((size_t)h * p->L + l) * kMaxPos * 2 * d;
+  const uint32_t par = par_layer(c, sh->pass, l);
+  // q of head h, k and v of kv head g, for every row of the pass (pairs of words);
+  // qs, ks, vs are consecutive [kMaxRows][d] blocks and v of kv head g follows k at +kvdim
+  const int rd2 = R * d / 2, d2 = d / 2, kvdim = p->kvdim;
+  const uint32_t* qkvb = p->qkvb;
+  bool ok = poll_pairs(
+      c, 3 * rd2, par,
       [=](int i) {
-        const int part = i / rd, rem = i - part * rd, r = rem / d, k = rem - r * d;
+        const int part = i / rd2, rem = i - part * rd2, r = rem / d2, k = 2 * (rem - r * d2);
         const int off = part == 0 ? qoff : koff + (part - 1) * kvdim;
         return qkvb + (size_t)r * N + off + k;
       },
-      [=](int i, uint32_t v) {
-        const int part = i / rd, rem = i - part * rd;
-        qs[part * kMaxRows * d + rem] = __uint_as_float(v);
+      [=](int i, float lo, float hi) {
+        const int part = i / rd2, rem = i - part * rd2;
+        qs[part * kMaxRows * d + 2 * rem] = lo;
+        qs[part * kMaxRows * d + 2 * rem + 1] = hi;
       });
   if (!wg_sync_ok(c, ok)) return false;
-  // per-head RMSNorm of q and k, then rotate-half RoPE at the row's position
-  const float* qn = fptr(p, layer_off(p, l, p->o_qn));
-  const float* kn = fptr(p, layer_off(p, l, p->o_kn));
+  const float* qn = c.attn_const + (size_t)l * 2 * d;
+  const float* kn = qn + d;
+  const float* rope = c.attn_const + (size_t)p->L * 2 * d;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int v = wave; v < 2 * R; v += kWaves) {
     float* x = v < R ? qs + v * d : ks + (v - R) * d;
     const float* gn = v < R ? qn : kn;
     const int r = v < R ? v : v - R;
-    float s = 0.f;
-    for (int i = lane; i < d; i += 64) s += x[i] * x[i];
-    s = wave_sum(s);
-    const float rs = p->qk_norm ? 1.f / sqrtf(s / (float)d + p->rms_eps) : 1.f;
-    const int pos = fp + r, half = d / 2;
+    float s2 = 0.f;
+    for (int i = lane; i < d; i += 64) s2 = fmaf(x[i], x[i], s2);
+    const float rs = p->qk_norm ? 1.f / sqrtf(lane63(wave_sum63(s2)) / (float)d + p->rms_eps) : 1.f;
+    const int pos = fp + r;
     for (int i = lane; i < half; i += 64) {
       float a = x[i], b = x[i + half];
       if (p->qk_norm) {
-        a = a * rs * G(gn)[i];
-        b = b * rs * G(gn)[i + half];
+        a = a * rs * gn[i];
+        b = b * rs * gn[i + half];
       }
-      double theta = (double)pos * pow(p->rope_base, -2.0 * (double)i / (double)d);
-      float cs = (float)cos(theta), sn = (float)sin(theta);
+      const float cs = rope[(pos * half + i) * 2], sn = rope[(pos * half + i) * 2 + 1];
       x[i] = a * cs - b * sn;
       x[i + half] = b * cs + a * sn;
     }
   }
   __syncthreads();
-  // append k, v of this pass's rows to the private cache, then read positions 0..fp+R-1
-  RVQSD_GLOBAL float* cache = G(p->kvc) + ((size_t)h * p->L + l) * kMaxPos * 2 * d;
   for (int i = threadIdx.x; i < R * d; i += kThreads) {
-    int r = i / d, k = i % d;
+    const int r = i / d, k = i - r * d;
     cache[((size_t)(fp + r) * 2 + 0) * d + k] = ks[i];
     cache[((size_t)(fp + r) * 2 + 1) * d + k] = vs[i];
   }
   __syncthreads();
-  const int npos = fp + R;
-  for (int i = threadIdx.x; i < npos * d; i += kThreads) {
-    int t = i / d, k = i % d;
-    kc[i] = cache[((size_t)t * 2 + 0) * d + k];
-    vc[i] = cache[((size_t)t * 2 + 1) * d + k];
-  }
-  __syncthreads();
+  // scores: one 16-lane DPP row per (row, position) pair, d/16 dimensions per lane
+  const int npos = fp + R, npairs = R * npos, dpl = d / 16;
   const float scale = 1.f / sqrtf((float)d);
-  for (int i = threadIdx.x; i < R * npos; i += kThreads) {
-    int r = i / npos, t = i % npos;
-    float s = -INFINITY;
+  const int grp = threadIdx.x >> 4, j = threadIdx.x & 15;
+  for (int pr = grp; pr < npairs; pr += kThreads / 16) {
+    const int r = pr / npos, t = pr - r * npos;
+    float part = 0.f;
     if (t <= fp + r) {
-      s = 0.f;
-      for (int k = 0; k < d; ++k) s = fmaf(qs[r * d + k], kc[t * d + k], s);
-      s *= scale;
+      const float* qv = qs + r * d + j * dpl;
+      const float* kv = cache + (size_t)t * 2 * d + j * dpl;
+      for (int e = 0; e < dpl; ++e) part = fmaf(qv[e], kv[e], part);
     }
-    sc[r * kMaxPos + t] = s;
+    part = row16_sum(part);
+    if (j == 0) sc[r * kMaxPos + t] = t <= fp + r ? part * scale : -INFINITY;
   }
   __syncthreads();
   if ((int)threadIdx.x < R) {
@@ -520,19 +801,20 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
     for (int t = 0; t <= fp + r; ++t) mx = fmaxf(mx, sc[r * kMaxPos + t]);
     float z = 0.f;
     for (int t = 0; t <= fp + r; ++t) {
-      float e = expf(sc[r * kMaxPos + t] - mx);
+      const float e = expf(sc[r * kMaxPos + t] - mx);
       sc[r * kMaxPos + t] = e;
       z += e;
     }
-    for (int t = 0; t <= fp + r; ++t) sc[r * kMaxPos + t] /= z;
+    const float iz = 1.f / z;
+    for (int t = 0; t <= fp + r; ++t) sc[r * kMaxPos + t] *= iz;
   }
   __syncthreads();
-  const uint32_t otag = tag_of(c, sh->pass, 5 * l + kPhAttn);
-  for (int i = threadIdx.x; i < R * d; i += kThreads) {
-    int r = i / d, k = i % d;
+  for (int i = threadIdx.x; i < MR * d; i += kThreads) {
+    const int r = i / d, k = i - r * d;
     float o = 0.f;
-    for (int t = 0; t <= fp + r; ++t) o = fmaf(sc[r * kMaxPos + t], vc[t * d + k], o);
-    xstoref(p->attnb + (size_t)r * p->qdim + qoff + k, otag, o);
+    if (r < R)
+      for (int t = 0; t <= fp + r; ++t) o = fmaf(sc[r * kMaxPos + t], cache[((size_t)t * 2 + 1) * d + k], o);
+    pstore(p->attnb + (size_t)r * p->qdim + qoff + k, o, par);
   }
   return true;
 }
@@ -552,48 +834,56 @@ __device__ __forceinline__ bool phase_proj(const Ctx& c, int l, bool is_down) {
   Gemv<WT, MR, RPT> g;
   g.setup(K, nrows);
   g.load(0, rowptr);
-  const uint64_t* src = is_down ? p->actb : p->attnb;
-  const uint32_t tag = tag_of(c, sh->pass, 5 * l + (is_down ? kPhGU : kPhAttn));
+  const uint32_t* src = is_down ? p->actb : p->attnb;
+  const uint32_t par = par_layer(c, sh->pass, l);
   constexpr int EPC = Gemv<WT, MR, RPT>::EPC;
   float xg[MR][EPC];
   float* out = c.work + (size_t)MR * p->stage_cols;
   if (K <= p->stage_cols) {
     float* xs = c.work;
-    if (!stage_tagged<MR>(c, src, K, R, tag, xs)) return false;
-    if (g.active) chunk_from_lds<MR, EPC>(xs, K, g.kc, nullptr, nullptr, xg);
+    if (!stage_par<MR>(c, src, K, R, par, xs)) return false;
+    float sq[MR];
+    chunk_from_lds<MR, EPC>(xs, K, g.kc, g.active, (const float*)nullptr, xg, sq);
   } else {
-    // one thread per chunk (n_rg == 1): poll the chunk directly
+    // one thread per chunk (n_rg == 1): poll this thread's chunk of every row directly,
+    // all MR * EPC/2 pairs in flight at once
     bool ok = true;
 #pragma unroll
     for (int m = 0; m < MR; ++m)
 #pragma unroll
       for (int e = 0; e < EPC; ++e) xg[m][e] = 0.f;
     if (g.active) {
-      for (int m = 0; m < R && ok; ++m) {
-        const uint64_t* s = src + (size_t)m * K + (size_t)g.kc * EPC;
-        uint64_t t0 = 0;
-        int spins = 0;
-        int have = 0;
-        while (have != (1 << EPC) - 1) {
+      constexpr int NP = MR * (EPC / 2);
+      bool got[NP];
 #pragma unroll
-          for (int e = 0; e < EPC; ++e) {
-            if (!(have & (1 << e))) {
-              uint64_t v = xload(s + e);
-              if ((uint32_t)(v >> 32) == tag) {
-                have |= 1 << e;
+      for (int q = 0; q < NP; ++q) got[q] = (q / (EPC / 2)) >= R;
+      uint64_t t0 = 0;
+      int spins = 0;
+      while (true) {
+        uint64_t v[NP];
 #pragma unroll
-                for (int mm = 0; mm < MR; ++mm)
-                  if (mm == m) xg[mm][e] = __uint_as_float((uint32_t)v);
-              }
+        for (int q = 0; q < NP; ++q)
+          if (!got[q]) v[q] = pload2(src + (size_t)(q / (EPC / 2)) * K + (size_t)g.kc * EPC + 2 * (q % (EPC / 2)));
+        bool all = true;
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          if (!got[q]) {
+            const uint32_t lo = (uint32_t)v[q], hi = (uint32_t)(v[q] >> 32);
+            if ((lo & 1u) == par && (hi & 1u) == par) {
+              got[q] = true;
+              xg[q / (EPC / 2)][2 * (q % (EPC / 2))] = __uint_as_float(lo);
+              xg[q / (EPC / 2)][2 * (q % (EPC / 2)) + 1] = __uint_as_float(hi);
+            } else {
+              all = false;
             }
           }
-          if (have == (1 << EPC) - 1) break;
-          if ((++spins & 31) == 0) {
-            uint64_t now = dclock();
-            if (t0 == 0) t0 = now;
-            else if (now - t0 > kTimeoutTicks) { status_raise(p, c.tag_base, RVQSD_ETIMEOUT); ok = false; break; }
-            if (status_set(p, c.tag_base)) { ok = false; break; }
-          }
+        }
+        if (all) break;
+        if ((++spins & 31) == 0) {
+          const uint64_t now = dclock();
+          if (t0 == 0) t0 = now;
+          else if (now - t0 > kTimeoutTicks) { status_raise(p, c.tag_base, RVQSD_ETIMEOUT); ok = false; break; }
+          if (status_set(p, c.tag_base)) { ok = false; break; }
         }
       }
     }
@@ -601,12 +891,15 @@ __device__ __forceinline__ bool phase_proj(const Ctx& c, int l, bool is_down) {
   }
   if (nrows > 0) {
     g.run(c, xg, rowptr, out);
-    const uint32_t otag = tag_of(c, sh->pass, 5 * l + (is_down ? kPhDown : kPhO));
-    for (int i = threadIdx.x; i < R * nrows; i += kThreads) {
-      int m = i / nrows, r = i % nrows;
-      float v = c.xown[m * c.cpw + r] + out[r * MR + m];
-      c.xown[m * c.cpw + r] = v;
-      xstoref(p->xb + (size_t)m * H + row0 + r, otag, v);
+    const uint32_t xpar = is_down ? kParDown : kParO;
+    for (int i = threadIdx.x; i < MR * nrows; i += kThreads) {
+      const int m = i / nrows, r = i % nrows;
+      float v = 0.f;
+      if (m < R) {
+        v = c.xown[m * c.cpw + r] + out[r * MR + m];
+        c.xown[m * c.cpw + r] = v;
+      }
+      pstore(p->xb + (size_t)m * H + row0 + r, v, xpar);
     }
   }
   __syncthreads();
@@ -626,21 +919,24 @@ __device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
   Gemv<WT, MR, RPT> g;
   g.setup(H, 2 * nf);
   g.load(0, rowptr);
+  g.load_gain(fptr(p, layer_off(p, l, p->o_mlp_norm)));
   if (nf == 0) return true;
   float* xs = c.work;
   float* out = c.work + MR * H;
-  if (!stage_tagged<MR>(c, p->xb, H, R, tag_of(c, sh->pass, 5 * l + kPhO), xs)) return false;
-  row_rstd<MR>(c, xs, H, R);
+  if (!stage_par<MR>(c, p->xb, H, R, kParO, xs)) return false;
   {
-    float xg[MR][Gemv<WT, MR, RPT>::EPC];
-    if (g.active) chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, fptr(p, layer_off(p, l, p->o_mlp_norm)), sh->rstd, xg);
-    g.run(c, xg, rowptr, out);
-    const uint32_t tag = tag_of(c, sh->pass, 5 * l + kPhGU);
-    for (int i = threadIdx.x; i < R * nf; i += kThreads) {
-      int m = i / nf, j = i % nf;
-      float gt = out[(2 * j) * MR + m], up = out[(2 * j + 1) * MR + m];
-      float a = gt / (1.f + expf(-gt)) * up;
-      xstoref(p->actb + (size_t)m * F + f0 + j, tag, a);
+    float xg[MR][Gemv<WT, MR, RPT>::EPC], sq[MR];
+    chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, g.active, g.gain, xg, sq);
+    g.run(c, xg, rowptr, out, sq);
+    const uint32_t par = par_layer(c, sh->pass, l);
+    for (int i = threadIdx.x; i < MR * nf; i += kThreads) {
+      const int m = i / nf, j = i % nf;
+      float a = 0.f;
+      if (m < R) {
+        const float gt = out[(2 * j) * MR + m], up = out[(2 * j + 1) * MR + m];
+        a = gt / (1.f + expf(-gt)) * up;
+      }
+      pstore(p->actb + (size_t)m * F + f0 + j, a, par);
     }
   }
   return true;
@@ -696,14 +992,15 @@ __device__ __forceinline__ bool phase_heads(const Ctx& c) {
   }
   const WT* W = wptr<WT>(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
   auto rowptr = [&](int r) -> const WT* { return W + (size_t)(v0 + r) * H; };
-  Gemv<WT, MR, RPT> g;
+  constexpr int RH = RPT;
+  Gemv<WT, MR, RH, true> g;
   g.setup(H, nrows);
   g.load(0, rowptr);
   float* xs = c.work;
   float* out = c.work + MR * H;
-  if (!stage_tagged<MR>(c, p->xb, H, R, tag_of(c, sh->pass, 5 * (L - 1) + kPhDown), xs)) return false;
+  if (!stage_par<MR>(c, p->xb, H, R, kParDown, xs)) return false;
   row_rstd<MR>(c, xs, H, R);
-  constexpr int EPC = Gemv<WT, MR, RPT>::EPC;
+  constexpr int EPC = Gemv<WT, MR, RH, true>::EPC;
   float xg[MR][EPC];
   const float* gn = fptr(p, p->o_final_norm);
   const float* ofs = fptr(p, p->o_offsets);
@@ -1165,11 +1462,23 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   c.dyn = dyn;
   c.xown = dyn;
   c.red = dyn + kMaxRows * c.cpw;
-  c.work = c.red + kWaves * RPT * MR;
+  c.work = c.red + kWaves * (RPT + 1) * MR;
+  c.kvlds = c.work + p->work_floats;
+  c.attn_const = c.kvlds + (p->kv_in_lds ? (size_t)p->L * kMaxPos * 2 * p->d : 0);
+  if ((int)blockIdx.x < p->nq) {
+    const int d = p->d;
+    for (int i = threadIdx.x; i < p->L * 2 * d; i += kThreads) {
+      const int l = i / (2 * d), j = i % (2 * d);
+      c.attn_const[i] = G(fptr(p, layer_off(p, l, j < d ? p->o_qn : p->o_kn)))[j % d];
+    }
+    for (int i = threadIdx.x; i < kMaxPos * d; i += kThreads) c.attn_const[p->L * 2 * d + i] = G(p->rope)[i];
+  }
   c.tag_base = fa.epoch_base;
+  c.pass0 = *G(p->pass_count);
   const uint64_t t_start = dclock();
   const int c0 = fa.c0[0];
-  const bool c0_ok = c0 >= 0 && c0 < p->V;
+  const bool poisoned = c.pass0 == 0xffffffffu;
+  const bool c0_ok = c0 >= 0 && c0 < p->V && !poisoned;
   if (threadIdx.x == 0) {
     shs.fa = fa;
     shs.abort = c0_ok ? 0 : 1;
@@ -1191,29 +1500,40 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   const int L = p->L;
   while (ok) {
     if (blockIdx.x == 0 && threadIdx.x == 0) shs.st_bytes += pass_bytes(c, wbytes);
+    const int nph = phases_per_pass(L) + 1;
     const bool clk_on = blockIdx.x == 0 && p->tr_clock && shs.pass < p->tr_max_rounds;
-    uint64_t* clk_row = clk_on ? p->tr_clock + (size_t)shs.pass * (phases_per_pass(L) + 1) : nullptr;
+    uint64_t* clk_row = clk_on ? p->tr_clock + (size_t)shs.pass * nph : nullptr;
+    const bool wclk_on = p->tr_wgclock && shs.pass < p->tr_max_rounds;
+    uint64_t* wclk = wclk_on ? p->tr_wgclock + (size_t)shs.pass * nph * p->nwg + blockIdx.x : nullptr;
+#define RVQSD_STAMP(ph)                                                   \
+  do {                                                                    \
+    if (threadIdx.x == 0) {                                               \
+      if (clk_on) clk_row[(ph)] = dclock();                               \
+      if (wclk_on) wclk[(size_t)(ph) * p->nwg] = dclock();                \
+    }                                                                     \
+  } while (0)
     for (int l = 0; l < L && ok; ++l) {
-      ok = phase_qkv<WT, MR, RPT>(c, l);
-      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 0] = dclock();
+      ok = phase_qkv<WT, MR, 4>(c, l);
+      RVQSD_STAMP(5 * l + 0);
       if (ok) ok = phase_attn<MR>(c, l);
-      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 1] = dclock();
-      if (ok) ok = phase_proj<WT, MR, RPT>(c, l, false);
-      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 2] = dclock();
-      if (ok) ok = phase_gu<WT, MR, RPT>(c, l);
-      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 3] = dclock();
-      if (ok) ok = phase_proj<WT, MR, RPT>(c, l, true);
-      if (clk_on && threadIdx.x == 0) clk_row[5 * l + 4] = dclock();
+      RVQSD_STAMP(5 * l + 1);
+      if (ok) ok = phase_proj<WT, MR, 4>(c, l, false);
+      RVQSD_STAMP(5 * l + 2);
+      if (ok) ok = phase_gu<WT, MR, (MR <= 8 ? 8 : 4)>(c, l);
+      RVQSD_STAMP(5 * l + 3);
+      if (ok) ok = phase_proj<WT, MR, 4>(c, l, true);
+      RVQSD_STAMP(5 * l + 4);
     }
-    if (ok) ok = phase_heads<WT, MR, RPT>(c);
-    if (clk_on && threadIdx.x == 0) clk_row[ph_heads(L)] = dclock();
+    if (ok) ok = phase_heads<WT, MR, (MR <= 5 ? 8 : 4)>(c);
+    RVQSD_STAMP(ph_heads(L));
     if (ok) ok = phase_sample<MR>(c);
-    if (clk_on && threadIdx.x == 0) clk_row[ph_sample(L)] = dclock();
+    RVQSD_STAMP(ph_sample(L));
     ok = wg_sync_ok(c, ok);
     if (ok) ok = commit_and_advance(c);
-    if (clk_on && threadIdx.x == 0) clk_row[ph_sample(L) + 1] = dclock();
+    RVQSD_STAMP(ph_sample(L) + 1);
     if (!ok || shs.m >= p->n_codes) break;
   }
+#undef RVQSD_STAMP
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     rvqsd_stats* st = fa.out_stats;
     st->target_calls = shs.st_calls;
@@ -1223,8 +1543,10 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     st->accept_mask = shs.st_mask;
     const uint64_t sw = __hip_atomic_load(G(p->status), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     int32_t status = ((uint32_t)(sw >> 32) == fa.epoch_base) ? (int32_t)(uint32_t)sw : 0;
-    if (!c0_ok) status = RVQSD_EINVAL;
+    if (!c0_ok) status = poisoned ? RVQSD_EHIP : RVQSD_EINVAL;
     if (status == 0 && !ok) status = RVQSD_ETIMEOUT;
+    // the parity state of the exchange buffers is only consistent after a complete frame
+    if (!poisoned) *G(p->pass_count) = (ok && c0_ok) ? c.pass0 + (uint32_t)shs.pass : (c0_ok ? 0xffffffffu : c.pass0);
     st->status = status;
     st->weight_bytes = shs.st_bytes;
     st->clk_start = t_start;
@@ -1247,7 +1569,7 @@ int frame_max_rows(int K) {
 // floats of the per-workgroup regions in front of the work area
 int frame_lds_head_floats(int mr, int cpw) {
   const int rpt = mr <= 8 ? 8 : 4;
-  return kMaxRows * cpw + kWaves * rpt * mr;
+  return kMaxRows * cpw + kWaves * (rpt + 1) * mr;
 }
 
 template <typename WT, int MR>

@@ -34,21 +34,28 @@ struct KParams {
   uint64_t layer_stride;
   uint64_t o_attn_norm, o_wq, o_wk, o_wv, o_qn, o_kn, o_wo, o_mlp_norm, o_wg, o_wu, o_wd;  // inside a layer
   uint64_t o_final_norm, o_emb0, o_lmh1, o_offsets, table_stride;                      // global
-  // exchange buffers: 64-bit words, high 32 bits = tag, low 32 bits = payload
-  uint64_t* xb;    // [kMaxRows][H]      residual stream
-  uint64_t* qkvb;  // [kMaxRows][nqkv]   raw q | k | v
-  uint64_t* attnb; // [kMaxRows][qdim]   attention output
-  uint64_t* actb;  // [kMaxRows][F]      SiLU(gate) * up
+  // activation exchange buffers: fp32 bit patterns whose lowest mantissa bit
+  // carries the parity of the write epoch (every epoch rewrites every word)
+  uint32_t* xb;    // [kMaxRows][H]      residual stream (parity 0 after O, 1 after down)
+  uint32_t* qkvb;  // [kMaxRows][nqkv]   raw q | k | v
+  uint32_t* attnb; // [kMaxRows][qdim]   attention output
+  uint32_t* actb;  // [kMaxRows][F]      SiLU(gate) * up
+  uint32_t* pass_count;  // passes run by this stream so far (0xffffffff: poisoned by an error)
+  // tagged 64-bit words: high 32 bits = tag, low 32 bits = payload
   uint64_t* logb;  // [2][n_slots][V]    verify + draft logits (by pass parity)
   uint64_t* vres;  // [2][kMaxRows]      verify results (accept flag | token)
   uint64_t* drec;  // [2][n_slots][drec_words] draft records: token, then (idx, prob lo, prob hi) x support
   int32_t n_slots, drec_words;
-  float* kvc;      // [nq][L][kMaxPos][2][d] private KV cache of each attention workgroup
+  float* kvc;      // [nq][L][kMaxPos][2][d] KV cache of each attention workgroup (when not in LDS)
+  const float* rope;  // [kMaxPos][d/2][2] cos, sin of position * rope_base^(-2i/d)
+  int32_t kv_in_lds;  // 1: the attention workgroups keep their KV cache in LDS
+  int32_t work_floats;  // floats of the LDS work area (the LDS KV cache follows it)
   uint64_t* status; // device status word: (epoch_base << 32) | error code of that frame
   // trace (nullable)
   float* tr_logits;    // [tr_max_rounds][n_slots][V]
   int32_t* tr_rounds;  // [tr_max_rounds][kTraceRoundInts]
   uint64_t* tr_clock;  // [tr_max_rounds][phases_per_pass + 1]
+  uint64_t* tr_wgclock;  // [tr_max_rounds][phases_per_pass + 1][nwg]
   int32_t tr_max_rounds;
 };
 

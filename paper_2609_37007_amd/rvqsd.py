@@ -21,7 +21,8 @@ TRACE_ROUND_INTS = 32
 
 # every symbol include/rvqsd.h declares
 EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_stream_destroy",
-           "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_set_trace",
+           "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset",
+           "rvqsd_set_trace",
            "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
 
 
@@ -54,7 +55,7 @@ assert STATS_DTYPE.itemsize == ctypes.sizeof(rvqsd_stats)
 
 class rvqsd_trace(ctypes.Structure):
     _fields_ = [("logits", ctypes.c_void_p), ("rounds", ctypes.c_void_p), ("clock", ctypes.c_void_p),
-                ("max_rounds", ctypes.c_int32)]
+                ("wg_clock", ctypes.c_void_p), ("max_rounds", ctypes.c_int32)]
 
 
 class rvqsd_info(ctypes.Structure):
@@ -95,13 +96,15 @@ def lib():
         L.rvqsd_decode_frame_u.argtypes = [vp, vp, i32, vp, vp, P(rvqsd_stats)]
         L.rvqsd_decode_frame_async.argtypes = [vp, vp, vp, vp, vp, vp]
         L.rvqsd_set_trace.argtypes = [vp, P(rvqsd_trace)]
+        L.rvqsd_stream_reset.argtypes = [vp]
         L.rvqsd_uniforms_from_seed.argtypes = [ctypes.c_uint64, i32, vp]
         L.rvqsd_status_str.argtypes = [i32]
         L.rvqsd_status_str.restype = ctypes.c_char_p
         L.rvqsd_last_error.argtypes = []
         L.rvqsd_last_error.restype = ctypes.c_char_p
         for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_decode_frame",
-                  "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_set_trace", "rvqsd_uniforms_from_seed"):
+                  "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset", "rvqsd_set_trace",
+                  "rvqsd_uniforms_from_seed"):
             getattr(L, n).restype = i32
         _lib = L
     return _lib
@@ -152,9 +155,9 @@ class Model:
         return i.as_dict()
 
     def close(self):
-        if getattr(self, "_h", None):
-            lib().rvqsd_destroy(self._h)
-            self._h = None
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.rvqsd_destroy(self._h)
+        self._h = None
 
     __del__ = close
 
@@ -172,9 +175,9 @@ class Stream:
         self._trace = None
 
     def close(self):
-        if getattr(self, "_h", None):
-            lib().rvqsd_stream_destroy(self._h)
-            self._h = None
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.rvqsd_stream_destroy(self._h)
+        self._h = None
 
     __del__ = close
 
@@ -201,11 +204,15 @@ class Stream:
                                               ctypes.c_void_p(d_uniforms), ctypes.c_void_p(d_out_codes),
                                               ctypes.c_void_p(d_stats)), "rvqsd_decode_frame_async")
 
-    def set_trace(self, logits_ptr: int = 0, rounds_ptr: int = 0, clock_ptr: int = 0, max_rounds: int = 0):
-        if not (logits_ptr or rounds_ptr or clock_ptr):
+    def reset(self):
+        _check(lib().rvqsd_stream_reset(self._h), "rvqsd_stream_reset")
+
+    def set_trace(self, logits_ptr: int = 0, rounds_ptr: int = 0, clock_ptr: int = 0, max_rounds: int = 0,
+                  wg_clock_ptr: int = 0):
+        if not (logits_ptr or rounds_ptr or clock_ptr or wg_clock_ptr):
             _check(lib().rvqsd_set_trace(self._h, None), "rvqsd_set_trace")
             self._trace = None
             return
-        t = rvqsd_trace(logits_ptr or None, rounds_ptr or None, clock_ptr or None, max_rounds)
+        t = rvqsd_trace(logits_ptr or None, rounds_ptr or None, clock_ptr or None, wg_clock_ptr or None, max_rounds)
         _check(lib().rvqsd_set_trace(self._h, ctypes.byref(t)), "rvqsd_set_trace")
         self._trace = t
