@@ -88,7 +88,8 @@ struct rvqsd_stream {
   int32_t* d_out;
   uint32_t epoch;       // tag base of the next frame
   uint32_t epoch_step;
-  size_t par_bytes;     // leading bytes of dbuf holding the parity-word buffers
+  size_t par_begin, par_end;  // byte range of dbuf holding the parity-word buffers (pass count follows)
+  size_t tag_begin, tag_end;  // byte range of dbuf holding the tagged words
 };
 
 namespace {
@@ -337,15 +338,19 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     off += (bytes + 255) & ~(size_t)255;
     return at;
   };
-  // parity-word activation buffers first (one contiguous range, initialised to parity 1)
+  // Layout: constants | parity words (initialised to parity 1) | pass count |
+  // tagged words (cleared to tag 0) | scratch, staging and the parameter block.
+  const size_t o_rope = take((size_t)kMaxPos * k.d * 4);
+  const size_t par_begin = off;
   const size_t o_x = take(kMaxRows * H * 4), o_qkv = take((size_t)kMaxRows * k.nqkv * 4),
                o_attn = take((size_t)kMaxRows * k.qdim * 4), o_act = take((size_t)kMaxRows * k.F * 4);
   const size_t par_end = off;
-  const size_t o_pc = take(4),
-               o_log = take((size_t)2 * k.n_slots * V * 8), o_vres = take((size_t)2 * kMaxRows * 8),
-               o_drec = take((size_t)2 * k.n_slots * k.drec_words * 8),
-               o_kvc = take((size_t)k.nq * k.L * kMaxPos * 2 * k.d * 4), o_status = take(8),
-               o_rope = take((size_t)kMaxPos * k.d * 4),
+  const size_t o_pc = take(4);
+  const size_t tag_begin = off;
+  const size_t o_log = take((size_t)2 * k.n_slots * V * 8), o_vres = take((size_t)2 * kMaxRows * 8),
+               o_drec = take((size_t)2 * k.n_slots * k.drec_words * 8), o_status = take(8);
+  const size_t tag_end = off;
+  const size_t o_kvc = take((size_t)k.nq * k.L * kMaxPos * 2 * k.d * 4),
                o_in = take(((size_t)H + 3 * kMaxCodes + 4) * 4), o_out = take((kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64),
                o_kp = take(sizeof(KParams));
   s->dbuf_bytes = off;
@@ -355,11 +360,11 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     return set_err(RVQSD_ENOMEM, "stream buffers (%zu bytes): %s", off, hipGetErrorString(e));
   }
   e = hipMemset(s->dbuf, 0, off);
-  if (e == hipSuccess) e = hipMemsetD8((hipDeviceptr_t)s->dbuf, 0x01, par_end);
+  if (e == hipSuccess) e = hipMemsetD8((hipDeviceptr_t)((uint8_t*)s->dbuf + par_begin), 0x01, par_end - par_begin);
   if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_in, ((size_t)H + 3 * kMaxCodes + 4) * 4, hipHostMallocDefault);
   if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_out, (kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64, hipHostMallocDefault);
   if (e != hipSuccess) {
-    if (s->h_in) hipHostFree(s->h_in);
+    if (s->h_in) (void)hipHostFree(s->h_in);
     (void)hipFree(s->dbuf);
     delete s;
     return set_err(RVQSD_ENOMEM, "stream staging: %s", hipGetErrorString(e));
@@ -370,7 +375,10 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
   k.attnb = (uint32_t*)(base + o_attn);
   k.actb = (uint32_t*)(base + o_act);
   k.pass_count = (uint32_t*)(base + o_pc);
-  s->par_bytes = par_end;
+  s->par_begin = par_begin;
+  s->par_end = par_end;
+  s->tag_begin = tag_begin;
+  s->tag_end = tag_end;
   k.logb = (uint64_t*)(base + o_log);
   k.vres = (uint64_t*)(base + o_vres);
   k.drec = (uint64_t*)(base + o_drec);
@@ -437,9 +445,8 @@ static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t
                                int32_t* d_codes, rvqsd_stats* d_stats) {
   // tags of stale words from earlier frames never equal a later frame's tags; on wrap, clear everything
   if ((uint64_t)s->epoch + 2ull * s->epoch_step >= 0xFFFFFFFFull) {
-    // clears the tagged words (and the pass count); parity words are left alone
-    HIPCHK(hipMemsetAsync((uint8_t*)s->dbuf + s->par_bytes, 0, (uint8_t*)s->d_in - (uint8_t*)s->dbuf - s->par_bytes,
-                          s->stream));
+    // clears the tagged words only: the parity words and the pass count keep their state
+    HIPCHK(hipMemsetAsync((uint8_t*)s->dbuf + s->tag_begin, 0, s->tag_end - s->tag_begin, s->stream));
     s->epoch = s->epoch_step;
   }
   FrameArgs fa;
@@ -461,8 +468,10 @@ rvqsd_status rvqsd_stream_reset(rvqsd_stream* s) {
   if (!s) return set_err(RVQSD_EINVAL, "null stream");
   HIPCHK(hipStreamSynchronize(s->stream));
   // parity words back to parity 1, pass count and every tagged word back to 0
-  HIPCHK(hipMemset(s->dbuf, 0, (uint8_t*)s->d_in - (uint8_t*)s->dbuf));
-  HIPCHK(hipMemsetD8((hipDeviceptr_t)s->dbuf, 0x01, s->par_bytes));
+  uint8_t* base = (uint8_t*)s->dbuf;
+  HIPCHK(hipMemsetD8((hipDeviceptr_t)(base + s->par_begin), 0x01, s->par_end - s->par_begin));
+  HIPCHK(hipMemset(base + s->par_end, 0, s->tag_end - s->par_end));
+  HIPCHK(hipDeviceSynchronize());
   s->epoch = s->epoch_step;
   return RVQSD_OK;
 }

@@ -710,6 +710,8 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
       pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
     }
   }
+  // the next phase reuses the work area: no wave may still be reading it
+  lds_barrier();
   return true;
 }
 
@@ -816,6 +818,8 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
       for (int t = 0; t <= fp + r; ++t) o = fmaf(sc[r * kMaxPos + t], cache[((size_t)t * 2 + 1) * d + k], o);
     pstore(p->attnb + (size_t)r * p->qdim + qoff + k, o, par);
   }
+  // the next phase reuses the work area (scores, q, k, v): no wave may still be reading it
+  lds_barrier();
   return true;
 }
 
@@ -939,6 +943,7 @@ __device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
       pstore(p->actb + (size_t)m * F + f0 + j, a, par);
     }
   }
+  lds_barrier();  // the work area is reused by the next phase
   return true;
 }
 
@@ -1027,6 +1032,7 @@ __device__ __forceinline__ bool phase_heads(const Ctx& c) {
     const int v = i / nrows, r = i % nrows;
     xstoref(p->logb + ((size_t)(sh->pass & 1) * p->n_slots + sh->hv_slot[v]) * V + v0 + r, tag, out[r * MR + v]);
   }
+  lds_barrier();  // the work area is reused by the next phase
   return true;
 }
 

@@ -1,0 +1,608 @@
+"""GPU parity: the HIP library against the CPU oracle on the same seeded inputs.
+
+Every call goes through the C ABI (librvqsd.so).  Three levels, in order of
+strength:
+
+* logits: every verify and draft logit row the frame kernel produced (traced)
+  against the oracle's fp64 forward on the same inputs -- max-abs within 1e-4
+  for fp32 weights and 2e-2 for bf16 weights with fp32 accumulation;
+* decisions: the kernel's traced fp32 logits fed to the oracle's decision
+  primitives (top-k softmax, inverse-CDF sampling, the acceptance rule with
+  residual resampling, Sec. 2.2) must reproduce the kernel's drafts, accepts and
+  codes bit for bit, except a threshold closer than 1e-6 to the uniform;
+* end to end: codes and statistics of the oracle run from scratch; a frame may
+  differ only where the oracle's own decision margin or top-k gap lies within
+  what the measured logit error can flip (counted, and bounded).
+
+Plus the distributional check of Sec. 3.2 (lossless output): 1e5 frames,
+chi-square against the exact law and against plain autoregressive sampling.
+"""
+from __future__ import annotations
+
+import functools
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2609_37007_amd import synth as S
+from tests.helpers import make_oracle, shape_kwargs
+
+torch = pytest.importorskip("torch")
+from paper_2609_37007_amd import rvqsd as R  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+LOGIT_TOL = {S.DTYPE_F32: 1e-4, S.DTYPE_BF16: 2e-2}
+SLOT_DRAFT0 = 16
+CDF_EXCUSE = 1e-6
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    R.lib()
+
+
+@functools.lru_cache(maxsize=4)
+def blob_of(s: S.ModelShape, head_scale: float = 1.0) -> bytes:
+    return S.make_weights(s, seed=0, head_scale=head_scale)
+
+
+def shape_with(base: S.ModelShape, **kw) -> S.ModelShape:
+    d = {f: getattr(base, f) for f in base.__dataclass_fields__}
+    d.update(kw)
+    return S.ModelShape(**d)
+
+
+class Rig:
+    """A GPU model + stream and an oracle with the same configuration."""
+
+    def __init__(self, s, topk, K, T=0.9, greedy=0, head_scale=1.0, hip_stream=None):
+        self.s, self.topk, self.K, self.T, self.greedy = s, topk, K, T, greedy
+        blob = blob_of(s, head_scale)
+        self.model = R.Model(blob, R.make_cfg(**shape_kwargs(s), topk=topk, temperature=T, draft_len=K,
+                                              draft_greedy=greedy))
+        self.stream = R.Stream(self.model, hip_stream=hip_stream)
+        self.orc = make_oracle(s, blob, topk=topk, temperature=T, draft_len=K,
+                               draft_mode=O.DRAFT_GREEDY if greedy else O.DRAFT_SAMPLED)
+        self.slots = self.model.info()["trace_slots"]
+
+    def close(self):
+        self.stream.close()
+        self.model.close()
+        self.orc.close()
+
+    def traced(self, f, c0, u, max_rounds=16):
+        V = self.s.vocab
+        lg = torch.zeros((max_rounds, self.slots, V), dtype=torch.float32, device="cuda")
+        rd = torch.full((max_rounds, R.TRACE_ROUND_INTS), -1, dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        self.stream.set_trace(lg.data_ptr(), rd.data_ptr(), 0, max_rounds)
+        try:
+            codes, st = self.stream.decode_frame_u(f, int(c0), u)
+        finally:
+            self.stream.set_trace()
+        torch.cuda.synchronize()
+        return codes, st, lg.cpu().numpy(), rd.cpu().numpy()[:st["target_calls"]]
+
+
+# ------------------------------------------------------------------ trace logic
+
+def pass_rows(K, n, row):
+    """Verify rows and (row, j) draft slots the kernel computes in one pass."""
+    fp, R_, ps = int(row[2]), int(row[3]), int(row[7])
+    verify = [r for r in range(R_) if (ps > 0 or r == 1) and fp + r >= 1]
+    drafts = []
+    for r in range(R_):
+        s = fp + r
+        if s < 1 or s > n - 1 or (ps == 0 and r != 1):
+            continue
+        drafts += [(r, j) for j in range(1, min(K, n - s) + 1)]
+    return verify, drafts
+
+
+def pass_inputs(codes_full, row):
+    """Codes consumed by positions 1 .. first_pos+rows-1 of a traced pass:
+    committed codes up to the anchor m, then the round's drafts."""
+    m, fp, R_ = int(row[0]), int(row[2]), int(row[3])
+    ic = []
+    for s in range(1, fp + R_):
+        x = s - 1
+        ic.append(int(codes_full[x]) if x <= m else int(row[8 + (x - m - 1)]))
+    return ic
+
+
+def logit_error(rig, f, c0, codes, lg, rd):
+    """Max-abs difference of every traced logit row from the oracle's fp64 logits."""
+    K, n = rig.K, rig.s.n_codes
+    codes_full = [int(c0)] + [int(c) for c in codes]
+    worst = 0.0
+    for i, row in enumerate(rd):
+        h = rig.orc.forward(f, pass_inputs(codes_full, row))
+        fp = int(row[2])
+        verify, drafts = pass_rows(K, n, row)
+        for r in verify:
+            ref = rig.orc.logits(h[fp + r], fp + r, 0)
+            worst = max(worst, float(np.abs(lg[i, r].astype(np.float64) - ref).max()))
+        for r, j in drafts:
+            ref = rig.orc.logits(h[fp + r], fp + r + j, j)
+            worst = max(worst, float(np.abs(lg[i, SLOT_DRAFT0 + r * K + j - 1].astype(np.float64) - ref).max()))
+    return worst
+
+
+def cdf_margin(prob, u):
+    """Distance of u from the nearest step of the normalised ascending-index CDF."""
+    c = np.cumsum(prob) / prob.sum()
+    return float(np.min(np.abs(c - u)))
+
+
+def residual_probs(pi, pp, qi, qp):
+    q = dict(zip((int(x) for x in qi), (float(x) for x in qp)))
+    r = np.array([max(0.0, float(p) - q.get(int(i), 0.0)) for i, p in zip(pi, pp)])
+    return r if r.sum() > 0 else np.asarray(pp, dtype=np.float64)
+
+
+class _Excused(Exception):
+    pass
+
+
+def replay(rig, lg, rd, u, codes):
+    """Re-take every decision of the frame from the kernel's own logits with the
+    oracle's primitives.  Returns 1 when the frame diverged at a decision whose
+    threshold lies within 1e-6 of its uniform (summation-order rounding), else 0."""
+    K, n, topk, T = rig.K, rig.s.n_codes, rig.topk, rig.T
+
+    def check(gpu, mine, margin, what):
+        if gpu == mine:
+            return
+        assert margin < CDF_EXCUSE, f"{what}: kernel {gpu}, oracle primitives {mine}, margin {margin:.3g}"
+        raise _Excused
+
+    mine = {}
+    try:
+        for i, row in enumerate(rd):
+            m, kp, fp, R_, m_new, acc, tok = (int(x) for x in row[:7])
+            if i == 0:
+                pi, pp = O.topk_softmax(lg[0, 1], topk, T)
+                us = float(u[0, 2])
+                check(tok, O.sample(pi, pp, us), cdf_margin(pp, us), "prefix sample")
+                assert m_new == 1
+                mine[1] = tok
+                continue
+            arow = m - int(rd[i - 1][2])
+            n_acc, my_new = 0, None
+            for j in range(1, kp + 1):
+                ud, ua, us = (float(x) for x in u[m + j - 1])
+                qi, qp = O.topk_softmax(lg[i - 1, SLOT_DRAFT0 + arow * K + j - 1], topk, T)
+                d = int(row[8 + j - 1])
+                if rig.greedy:
+                    check(d, int(qi[int(np.argmax(qp))]), 0.0, f"greedy draft {m + j}")
+                    qi, qp = np.array([d], dtype=np.int32), np.array([1.0])
+                else:
+                    check(d, O.sample(qi, qp, ud), cdf_margin(qp, ud), f"draft {m + j}")
+                pi, pp = O.topk_softmax(lg[i, j - 1], topk, T)
+                ok, t = O.accept_or_resample(pi, pp, qi, qp, d, ua, us)
+                pd = dict(zip(pi.tolist(), pp.tolist())).get(d, 0.0)
+                qd = dict(zip(qi.tolist(), qp.tolist())).get(d, 0.0)
+                gpu_ok = j <= acc
+                check(gpu_ok, ok, abs(ua - pd / qd) if qd > 0 else 1.0, f"accept {m + j}")
+                if not ok:
+                    check(tok, t, cdf_margin(residual_probs(pi, pp, qi, qp), us), f"residual {m + j}")
+                    my_new = m + j
+                    break
+                mine[m + j] = d
+                n_acc += 1
+            if my_new is None:
+                if m + kp < n:
+                    pi, pp = O.topk_softmax(lg[i, kp], topk, T)
+                    us = float(u[m + kp, 2])
+                    check(tok, O.sample(pi, pp, us), cdf_margin(pp, us), f"bonus {m + kp + 1}")
+                    my_new = m + kp + 1
+                else:
+                    my_new = n
+            assert (m_new, acc) == (my_new, n_acc), (i, row[:8].tolist(), my_new, n_acc)
+            if my_new > m + n_acc:
+                mine[my_new] = tok
+    except _Excused:
+        return 1
+    assert sorted(mine) == list(range(1, n + 1))
+    assert [mine[s] for s in range(1, n + 1)] == [int(c) for c in codes]
+    return 0
+
+
+def compare_end_to_end(rig, f, c0, u, codes, stats, logit_err):
+    """True when the oracle from scratch gives the same frame; False when the
+    first differing round is within reach of the measured logit error."""
+    oc, ost, otr = rig.orc.spec_frame(f, int(c0), u, trace=True)
+    if np.array_equal(oc, codes):
+        for k in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
+            assert stats[k] == ost[k], (k, stats[k], ost[k])
+        return True
+    # the kernel committed a different sequence: excusable only near a threshold
+    flip = 5.0 * max(logit_err, 1e-7) / rig.T
+    near = [r for r in otr["rounds"] if r["margin"] < flip or r["topk_gap"] < 2 * max(logit_err, 1e-7)]
+    assert near, f"codes differ with no decision near a threshold: gpu {codes.tolist()} oracle {oc.tolist()}"
+    return False
+
+
+def check_frames(rig, frames, f, c0, u, excuse_frac=0.1):
+    tol = LOGIT_TOL[rig.s.dtype]
+    excused = 0
+    worst = 0.0
+    for i in frames:
+        codes, st, lg, rd = rig.traced(f[i], c0[i], u[i])
+        assert st["status"] == 0
+        err = logit_error(rig, f[i], c0[i], codes, lg, rd)
+        worst = max(worst, err)
+        assert err <= tol, f"frame {i}: logit max-abs {err:.3g} > {tol}"
+        ex = replay(rig, lg, rd, u[i], codes)
+        if not compare_end_to_end(rig, f[i], c0[i], u[i], codes, st, err) or ex:
+            excused += 1
+    assert excused <= max(1, int(excuse_frac * len(frames))), excused
+    return worst, excused
+
+
+# ------------------------------------------------------------------ tests
+
+def test_tiny_fp32_32_frames():
+    """2-layer fp32 model, draft length 3, top-k 8: all 32 frames."""
+    s = S.TINY
+    rig = Rig(s, topk=8, K=3)
+    f, c0 = S.frame_inputs(s, 32)
+    u = S.uniforms(32)
+    print(f"tiny fp32 K=3: 32 frames", flush=True)
+    worst, excused = check_frames(rig, range(32), f, c0, u)
+    print(f"max logit error {worst:.3g}, excused frames {excused}", flush=True)
+    rig.close()
+
+
+def test_mcd1024_bf16_sampled_frames():
+    """The 1024-wide bf16 model at draft length 4, top-k 50: traced frames of the
+    1000-frame workload, full logit/decision/end-to-end parity."""
+    s = S.MCD_1024
+    rig = Rig(s, topk=50, K=4)
+    f, c0 = S.frame_inputs(s, 1000)
+    u = S.uniforms(1000)
+    print("mcd1024 bf16 K=4: frames 0, 1, 2, 999", flush=True)
+    worst, excused = check_frames(rig, [0, 1, 2, 999], f, c0, u)
+    print(f"max logit error {worst:.3g}, excused frames {excused}", flush=True)
+    rig.close()
+
+
+def test_mcd1024_async_launch_matches_oracle():
+    """The benchmark's launch configuration: device-resident inputs, one async
+    launch per frame on a torch stream, frames of the 1000-frame workload."""
+    s = S.MCD_1024
+    ts = torch.cuda.current_stream()
+    rig = Rig(s, topk=50, K=4, hip_stream=ts.cuda_stream)
+    N = 1000
+    f, c0 = S.frame_inputs(s, N)
+    u = S.uniforms(N)
+    pick = [0, 3, 250, 777, 998]
+    d_f = torch.from_numpy(f).cuda()
+    d_c0 = torch.from_numpy(c0).cuda()
+    d_u = torch.from_numpy(np.ascontiguousarray(u)).cuda()
+    d_codes = torch.full((N, s.n_codes), -1, dtype=torch.int32, device="cuda")
+    sb = R.STATS_DTYPE.itemsize
+    d_st = torch.zeros(N * sb, dtype=torch.uint8, device="cuda")
+    H, n = s.hidden, s.n_codes
+    for i in range(N):
+        rig.stream.decode_frame_async(d_f.data_ptr() + i * H * 4, d_c0.data_ptr() + i * 4,
+                                      d_u.data_ptr() + i * n * 12, d_codes.data_ptr() + i * n * 4,
+                                      d_st.data_ptr() + i * sb)
+    torch.cuda.synchronize()
+    codes = d_codes.cpu().numpy()
+    st = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)
+    assert (st["status"] == 0).all()
+    assert ((codes >= 0) & (codes < s.vocab)).all()
+    # every frame: the committed-code count equals the accounting of its rounds
+    assert (st["target_calls"] == st["rounds"] + 1).all()
+    assert (st["accepted"] <= st["drafted"]).all()
+    for i in pick:
+        oc, ost, _ = rig.orc.spec_frame(f[i], int(c0[i]), u[i])
+        assert np.array_equal(oc, codes[i]), (i, oc.tolist(), codes[i].tolist())
+        assert int(st["accept_mask"][i]) == ost["accept_mask"]
+    rig.close()
+
+
+def test_k0_is_autoregressive():
+    s = S.TINY
+    rig = Rig(s, topk=8, K=0)
+    f, c0 = S.frame_inputs(s, 8)
+    u = S.uniforms(8)
+    for i in range(8):
+        codes, st = rig.stream.decode_frame_u(f[i], int(c0[i]), u[i])
+        assert st["target_calls"] == s.n_codes and st["drafted"] == 0
+        assert np.array_equal(codes, rig.orc.ar_frame(f[i], int(c0[i]), u[i]))
+    rig.close()
+
+
+@pytest.mark.parametrize("K", [1, 2, 14])
+def test_tiny_draft_lengths(K):
+    s = S.TINY
+    rig = Rig(s, topk=8, K=K)
+    f, c0 = S.frame_inputs(s, 4)
+    u = S.uniforms(4)
+    check_frames(rig, range(4), f, c0, u)
+    rig.close()
+
+
+@pytest.mark.parametrize("K", [1, 7, 14])
+def test_mcd1024_draft_lengths(K):
+    s = S.MCD_1024
+    rig = Rig(s, topk=50, K=K)
+    f, c0 = S.frame_inputs(s, 2)
+    u = S.uniforms(2)
+    check_frames(rig, range(2), f, c0, u)
+    rig.close()
+
+
+def test_mcd1024_peaked_heads():
+    """LM heads scaled 6x (peaked logits, high acceptance)."""
+    s = S.MCD_1024
+    rig = Rig(s, topk=50, K=4, head_scale=6.0)
+    f, c0 = S.frame_inputs(s, 2)
+    u = S.uniforms(2)
+    check_frames(rig, range(2), f, c0, u)
+    rig.close()
+
+
+def test_topk1_is_greedy_ar():
+    s = S.TINY
+    rig = Rig(s, topk=1, K=3)
+    f, c0 = S.frame_inputs(s, 4)
+    u = S.uniforms(4)
+    for i in range(4):
+        codes, st = rig.stream.decode_frame_u(f[i], int(c0[i]), u[i])
+        assert np.array_equal(codes, rig.orc.ar_frame(f[i], int(c0[i]), u[i]))
+    rig.close()
+
+
+@pytest.mark.parametrize("topk,T,greedy", [(64, 0.9, 0), (8, 0.9, 1), (8, 0.5, 0), (8, 2.0, 0)])
+def test_tiny_sampling_variants(topk, T, greedy):
+    """Full-vocabulary support, greedy drafts, low and high temperature."""
+    s = S.TINY
+    rig = Rig(s, topk=topk, K=3, T=T, greedy=greedy)
+    f, c0 = S.frame_inputs(s, 4)
+    u = S.uniforms(4)
+    check_frames(rig, range(4), f, c0, u)
+    rig.close()
+
+
+def test_mcd1024_max_topk():
+    s = S.MCD_1024
+    rig = Rig(s, topk=256, K=4)
+    f, c0 = S.frame_inputs(s, 1)
+    u = S.uniforms(1)
+    check_frames(rig, [0], f, c0, u)
+    rig.close()
+
+
+@pytest.mark.parametrize("n_codes", [1, 2, 5])
+def test_short_frames(n_codes):
+    """Fewer residual codes than the draft window (frame end truncates drafts)."""
+    s = shape_with(S.TINY, n_codes=n_codes, max_draft=4)
+    rig = Rig(s, topk=8, K=min(3, s.max_draft))
+    f, c0 = S.frame_inputs(s, 4)
+    u = S.uniforms(4, n_codes)
+    check_frames(rig, range(4), f, c0, u)
+    rig.close()
+
+
+def test_ragged_vocab():
+    """A codebook size that is not a multiple of the tile widths."""
+    s = shape_with(S.TINY, vocab=100)
+    rig = Rig(s, topk=10, K=3)
+    f, c0 = S.frame_inputs(s, 4)
+    u = S.uniforms(4)
+    check_frames(rig, range(4), f, c0, u)
+    rig.close()
+
+
+def test_seed_path_matches_uniform_table():
+    s = S.TINY
+    rig = Rig(s, topk=8, K=3)
+    f, c0 = S.frame_inputs(s, 3)
+    for i, seed in enumerate([0, 12345, 2**63 + 7]):
+        a, sa = rig.stream.decode_frame(f[i], int(c0[i]), seed)
+        u = O.uniforms_from_seed(seed)
+        assert np.array_equal(u, R.uniforms_from_seed(seed))
+        b, sb = rig.stream.decode_frame_u(f[i], int(c0[i]), u)
+        assert np.array_equal(a, b) and sa["accept_mask"] == sb["accept_mask"]
+        oc, _, _ = rig.orc.spec_frame(f[i], int(c0[i]), u)
+        assert np.array_equal(a, oc)
+    rig.close()
+
+
+def test_two_streams_share_a_model():
+    s = S.TINY
+    rig = Rig(s, topk=8, K=3)
+    st2 = R.Stream(rig.model)
+    f, c0 = S.frame_inputs(s, 4)
+    u = S.uniforms(4)
+    for i in range(4):
+        a, _ = rig.stream.decode_frame_u(f[i], int(c0[i]), u[i])
+        b, _ = st2.decode_frame_u(f[3 - i], int(c0[3 - i]), u[3 - i])
+        assert np.array_equal(a, rig.orc.spec_frame(f[i], int(c0[i]), u[i])[0])
+        assert np.array_equal(b, rig.orc.spec_frame(f[3 - i], int(c0[3 - i]), u[3 - i])[0])
+    st2.close()
+    rig.close()
+
+
+def test_invalid_inputs_and_recovery():
+    s = S.TINY
+    ts = torch.cuda.current_stream()
+    rig = Rig(s, topk=8, K=3, hip_stream=ts.cuda_stream)
+    f, c0 = S.frame_inputs(s, 2)
+    u = S.uniforms(2)
+    with pytest.raises(R.RvqsdError) as e:
+        rig.stream.decode_frame_u(f[0], s.vocab, u[0])
+    assert e.value.status == R.EINVAL
+    bad = u[0].copy()
+    bad[3, 1] = 1.0
+    with pytest.raises(R.RvqsdError) as e:
+        rig.stream.decode_frame_u(f[0], int(c0[0]), bad)
+    assert e.value.status == R.EINVAL
+    nan = f[0].copy()
+    nan[7] = np.nan
+    with pytest.raises(R.RvqsdError) as e:
+        rig.stream.decode_frame_u(nan, int(c0[0]), u[0])
+    assert e.value.status == R.EINVAL
+    # a device-side invalid c0 is reported in the frame's stats; the stream stays usable
+    d_f = torch.from_numpy(f[0]).cuda()
+    d_c0 = torch.tensor([-5], dtype=torch.int32, device="cuda")
+    d_u = torch.from_numpy(np.ascontiguousarray(u[0])).cuda()
+    d_codes = torch.zeros(s.n_codes, dtype=torch.int32, device="cuda")
+    d_st = torch.zeros(R.STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    rig.stream.decode_frame_async(d_f.data_ptr(), d_c0.data_ptr(), d_u.data_ptr(), d_codes.data_ptr(),
+                                  d_st.data_ptr())
+    torch.cuda.synchronize()
+    st = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)[0]
+    assert int(st["status"]) == R.EINVAL
+    codes, _ = rig.stream.decode_frame_u(f[1], int(c0[1]), u[1])
+    assert np.array_equal(codes, rig.orc.spec_frame(f[1], int(c0[1]), u[1])[0])
+    rig.stream.reset()
+    codes, _ = rig.stream.decode_frame_u(f[0], int(c0[0]), u[0])
+    assert np.array_equal(codes, rig.orc.spec_frame(f[0], int(c0[0]), u[0])[0])
+    rig.close()
+
+
+def test_blob_and_config_errors():
+    s = S.TINY
+    blob = bytearray(blob_of(s))
+    cfg = R.make_cfg(**shape_kwargs(s), topk=8, temperature=0.9, draft_len=3)
+
+    def status_of(b, c):
+        try:
+            R.Model(bytes(b), c).close()
+        except R.RvqsdError as e:
+            return e.status
+        return R.OK
+
+    bad = bytearray(blob)
+    bad[0] = ord("X")
+    assert status_of(bad, cfg) == R.EBLOB
+    assert status_of(blob[:-4], cfg) == R.EBLOB
+    cfg2 = R.make_cfg(**{**shape_kwargs(s), "vocab": 65}, topk=8, temperature=0.9, draft_len=3)
+    assert status_of(blob, cfg2) == R.EBLOB
+    for kw in ({"topk": 0}, {"draft_len": 15}, {"temperature": 0.0}):
+        args = dict(topk=8, temperature=0.9, draft_len=3)
+        args.update(kw)
+        assert status_of(blob, R.make_cfg(**shape_kwargs(s), **args)) in (R.EINVAL, R.EUNSUPPORTED)
+    odd = R.make_cfg(**{**shape_kwargs(s), "hidden": 300}, topk=8, temperature=0.9, draft_len=3)
+    assert status_of(blob, odd) in (R.EUNSUPPORTED, R.EINVAL)
+    assert status_of(blob, cfg) == R.OK
+
+
+# ------------------------------------------------------------------ distribution
+
+def _decode_many(rig, f, c0, U):
+    """Decode N frames with the same input and per-frame uniforms U[N][n][3]."""
+    n = rig.s.n_codes
+    N = U.shape[0]
+    d_f = torch.from_numpy(np.ascontiguousarray(f)).cuda()
+    d_c0 = torch.tensor([int(c0)], dtype=torch.int32, device="cuda")
+    d_u = torch.from_numpy(np.ascontiguousarray(U)).cuda()
+    d_codes = torch.full((N, n), -1, dtype=torch.int32, device="cuda")
+    sb = R.STATS_DTYPE.itemsize
+    d_st = torch.zeros(N * sb, dtype=torch.uint8, device="cuda")
+    for i in range(N):
+        rig.stream.decode_frame_async(d_f.data_ptr(), d_c0.data_ptr(), d_u.data_ptr() + i * n * 12,
+                                      d_codes.data_ptr() + i * n * 4, d_st.data_ptr() + i * sb)
+        if i % 20000 == 19999:
+            torch.cuda.synchronize()
+            print(f"  {i + 1} frames", flush=True)
+    torch.cuda.synchronize()
+    st = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)
+    assert (st["status"] == 0).all()
+    return d_codes.cpu().numpy(), st
+
+
+def _fresh_uniforms(N, n, seed):
+    u = np.random.default_rng(seed).random((N, n, 3)).astype(np.float32)
+    return np.minimum(u, np.float32(np.nextafter(np.float32(1.0), np.float32(0.0))))
+
+
+def _merge_small(obs, exp, min_exp=5.0):
+    """Pool the cells with expected count < min_exp into one cell."""
+    small = exp < min_exp
+    o = list(obs[~small]) + ([obs[small].sum()] if small.any() else [])
+    e = list(exp[~small]) + ([exp[small].sum()] if small.any() else [])
+    return np.array(o, dtype=np.float64), np.array(e, dtype=np.float64)
+
+
+CHI_N = 100_000
+P_MIN = 1e-3
+_spec_cache = {}
+
+
+def _spec_samples():
+    if "spec" not in _spec_cache:
+        s = S.TINY
+        rig = Rig(s, topk=8, K=3, hip_stream=torch.cuda.current_stream().cuda_stream)
+        f, c0 = S.frame_inputs(s, 1)
+        print(f"speculative K=3: {CHI_N} frames", flush=True)
+        codes, st = _decode_many(rig, f[0], c0[0], _fresh_uniforms(CHI_N, s.n_codes, 77))
+        _spec_cache["spec"] = (codes, st, f[0], int(c0[0]))
+        rig.close()
+    return _spec_cache["spec"]
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(600)
+def test_chi_square_against_exact_law():
+    """c_1 against the exact p_1 and (c_1, c_2) against the exact joint law."""
+    from scipy import stats as ss
+    s = S.TINY
+    codes, st, f, c0 = _spec_samples()
+    orc = make_oracle(s, blob_of(s), topk=8, temperature=0.9, draft_len=3)
+    h = orc.forward(f, [c0])
+    pi, pp = O.topk_softmax(orc.logits(h[1], 1, 0), 8, 0.9)
+    p1 = np.zeros(s.vocab)
+    p1[pi] = pp
+    obs = np.bincount(codes[:, 0], minlength=s.vocab).astype(np.float64)
+    assert obs[p1 == 0].sum() == 0, "a code outside the top-k support was emitted"
+    o, e = _merge_small(obs[p1 > 0], CHI_N * p1[p1 > 0])
+    p_a = ss.chisquare(o, e).pvalue
+    joint = np.zeros((s.vocab, s.vocab))
+    for c1 in pi:
+        h2 = orc.forward(f, [c0, int(c1)])
+        qi, qp = O.topk_softmax(orc.logits(h2[2], 2, 0), 8, 0.9)
+        joint[c1, qi] = p1[c1] * qp
+    obs2 = np.zeros_like(joint)
+    np.add.at(obs2, (codes[:, 0], codes[:, 1]), 1)
+    assert obs2[joint == 0].sum() == 0
+    o, e = _merge_small(obs2[joint > 0], CHI_N * joint[joint > 0])
+    p_b = ss.chisquare(o, e).pvalue
+    orc.close()
+    print(f"chi-square p-values: c1 {p_a:.4f}, (c1,c2) {p_b:.4f}; tokens/call "
+          f"{s.n_codes * CHI_N / st['target_calls'].sum():.3f}", flush=True)
+    assert p_a > P_MIN and p_b > P_MIN
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(600)
+def test_chi_square_against_autoregressive():
+    """Per-position marginals of the speculative output against plain top-k
+    autoregressive sampling (draft length 0) from an independent uniform stream."""
+    from scipy import stats as ss
+    s = S.TINY
+    codes, _, f, c0 = _spec_samples()
+    rig = Rig(s, topk=8, K=0, hip_stream=torch.cuda.current_stream().cuda_stream)
+    print(f"autoregressive: {CHI_N} frames", flush=True)
+    ar, st = _decode_many(rig, f, c0, _fresh_uniforms(CHI_N, s.n_codes, 78))
+    rig.close()
+    assert (st["target_calls"] == s.n_codes).all()
+    ps = []
+    for pos in range(s.n_codes):
+        a = np.bincount(codes[:, pos], minlength=s.vocab)
+        b = np.bincount(ar[:, pos], minlength=s.vocab)
+        keep = (a + b) >= 10
+        tab = np.stack([np.append(a[keep], a[~keep].sum()), np.append(b[keep], b[~keep].sum())])
+        tab = tab[:, tab.sum(0) > 0]
+        ps.append(ss.chi2_contingency(tab)[1])
+    print("per-position homogeneity p-values:", " ".join(f"{p:.3f}" for p in ps), flush=True)
+    assert min(ps) > P_MIN, ps
