@@ -136,16 +136,29 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
   if (nh_max < 1) nh_max = 1;
   const int wph_min = nwg / nh_max;
   const int rpw_heads = (V + wph_min - 1) / wph_min;
-  int rows_out = rpw_qkv;
-  if (2 * fpw > rows_out) rows_out = 2 * fpw;
-  if (rpw_heads > rows_out) rows_out = rpw_heads;
-  size_t w = (size_t)mr * H + (size_t)rows_out * mr;
-  const size_t proj = (size_t)mr * stage_cols + (size_t)cpw * mr;
-  const size_t attn = (size_t)5 * kMaxRows * d + kMaxRows * kMaxPos;
-  const size_t samp = (size_t)V + 2 * kMaxTopk + 2 + 2 * 3 * kMaxTopk + kMaxTopk + 8;
-  if (proj > w) w = proj;
-  if (attn > w) w = attn;
-  if (samp > w) w = samp;
+  auto tiles = [](int rows) { return (size_t)((rows + 15) / 16); };
+  size_t w = 0;
+  auto need = [&](size_t f) {
+    if (f > w) w = f;
+  };
+  if (c->dtype == RVQSD_DTYPE_BF16 && mr <= 8) {
+    // MFMA phases: split activations, chunk sums of squares, wave partial tiles, outputs
+    // split rows carry 4 words of padding; wave partials: 1 tile (QKV, O, down),
+    // 2 (gate/up), 5 (heads) at a time
+    need((size_t)mr * (H + 4) + (size_t)mr * (H / 8) + kWaves * 256 + tiles(rpw_qkv) * 16 * mr + (size_t)mr * H);
+    need((size_t)mr * (H + 4) + (size_t)mr * (H / 8) + kWaves * 2 * 256 + tiles(2 * fpw) * 16 * mr);
+    need((size_t)mr * (qd + 4) + kWaves * 256 + tiles(cpw) * 16 * mr);
+    need((size_t)mr * (F + 4) + kWaves * 256 + tiles(cpw) * 16 * mr);
+    need((size_t)mr * H + (size_t)mr * (H + 4) + kWaves * 5 * 256 + tiles(rpw_heads) * 16 * mr);
+  } else {
+    int rows_out = rpw_qkv;
+    if (2 * fpw > rows_out) rows_out = 2 * fpw;
+    if (rpw_heads > rows_out) rows_out = rpw_heads;
+    need((size_t)mr * H + (size_t)rows_out * mr);
+    need((size_t)mr * stage_cols + (size_t)cpw * mr);
+  }
+  need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4));  // attention: q, k, v rows + the head's KV
+  need((size_t)V + 2 * kMaxTopk + 2 + 2 * 3 * kMaxTopk + kMaxTopk + 8);  // sampling
   return w;
 }
 
@@ -251,6 +264,12 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   m->device = dev;
   m->nwg = nwg;
   m->mr = frame_max_rows(cfg->draft_len);
+  if (cfg->dtype == RVQSD_DTYPE_BF16 && m->mr <= 8 &&
+      (k.H > 512 * kUptH || k.qdim > 512 * kUptQ || k.F > 512 * kUptF)) {
+    delete m;
+    return set_err(RVQSD_EUNSUPPORTED, "bf16 matrix path takes hidden <= %d, n_q_heads*head_dim <= %d, ffn <= %d",
+                   512 * kUptH, 512 * kUptQ, 512 * kUptF);
+  }
   m->wbytes = (int)wb;
   m->dweight_bytes = o;
   // LDS: stage the widest activation if it fits, else the down projection polls its chunks directly
@@ -268,16 +287,12 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
     delete m;
     return set_err(RVQSD_EUNSUPPORTED, "needs %zu bytes of LDS per workgroup, %zu available", lds, budget);
   }
-  // the attention workgroups keep their KV cache (all layers) in LDS when it fits
-  const size_t kv_floats = (size_t)k.L * kMaxPos * 2 * k.d;
   const size_t attn_const_floats = (size_t)k.L * 2 * k.d + (size_t)kMaxPos * k.d;  // gains + rotary table
   lds += attn_const_floats * 4;
   if (lds > budget) {
     delete m;
     return set_err(RVQSD_EUNSUPPORTED, "needs %zu bytes of LDS per workgroup, %zu available", lds, budget);
   }
-  k.kv_in_lds = (lds + kv_floats * 4 <= budget) ? 1 : 0;
-  if (k.kv_in_lds) lds += kv_floats * 4;
   k.work_floats = (int32_t)work;
   m->lds_bytes = lds;
   m->stage_cols = stage;

@@ -27,6 +27,13 @@ typedef uint16_t bf16_t;
 
 constexpr uint64_t kTimeoutTicks = 200ull * 1000 * 1000;  // 2 s of the 100 MHz device clock
 
+// The thread index behind an empty asm: values derived from it cannot be
+// hoisted out of the pass loop, which keeps them from living across phases.
+__device__ __forceinline__ int tid() {
+  int t = (int)threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
 // ------------------------------------------------------------------ helpers
 
 // Pointers taken from the parameter block are generic; every device-memory
@@ -105,7 +112,7 @@ __device__ __forceinline__ double wave_maxd(double v) {
 }
 // inclusive prefix sum over the 64 lanes
 __device__ __forceinline__ int wave_scan_incl(int v) {
-  const int lane = threadIdx.x & 63;
+  const int lane = tid() & 63;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     int t = __shfl_up(v, o, 64);
@@ -114,7 +121,7 @@ __device__ __forceinline__ int wave_scan_incl(int v) {
   return v;
 }
 __device__ __forceinline__ double wave_scan_incld(double v) {
-  const int lane = threadIdx.x & 63;
+  const int lane = tid() & 63;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     double t = __shfl_up(v, o, 64);
@@ -186,7 +193,6 @@ struct Ctx {
   float* xown;      // [kMaxRows][cpw] residual columns owned by this workgroup
   float* red;       // [kWaves][RPT * MR] reduction scratch
   float* work;      // union area
-  float* kvlds;     // [L][kMaxPos][2][d] KV cache of this attention workgroup (when kept in LDS)
   float* attn_const;  // [L][2][d] q/k norm gains, then [kMaxPos][d/2][2] rotary table (attention workgroups)
   int cpw;          // residual columns per workgroup
   uint32_t tag_base;
@@ -221,7 +227,7 @@ __device__ __forceinline__ bool poll_words(const Ctx& c, int n, uint32_t tag, Ad
     bool got[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      idx[k] = base + k * kThreads + (int)threadIdx.x;
+      idx[k] = base + k * kThreads + tid();
       got[k] = idx[k] >= n;
     }
     uint64_t t0 = 0;
@@ -274,7 +280,7 @@ __device__ __forceinline__ bool poll_pairs(const Ctx& c, int n2, uint32_t par, A
     bool got[B];
 #pragma unroll
     for (int k = 0; k < B; ++k) {
-      idx[k] = base + k * kThreads + (int)threadIdx.x;
+      idx[k] = base + k * kThreads + tid();
       got[k] = idx[k] >= n2;
     }
     uint64_t t0 = 0;
@@ -353,8 +359,8 @@ struct Gemv {
   __device__ __forceinline__ void setup(int K, int nrows_) {
     nkc = K / EPC;
     n_rg = kThreads / nkc;
-    rg = (int)threadIdx.x / nkc;
-    kc = (int)threadIdx.x % nkc;
+    rg = tid() / nkc;
+    kc = tid() % nkc;
     active = rg < n_rg;
     nrows = nrows_;
   }
@@ -387,7 +393,7 @@ struct Gemv {
   template <typename RowPtr>
   __device__ __forceinline__ void run(const Ctx& c, const float (&xg)[MR][EPC], RowPtr rowptr, float* out,
                                       const float* sq = nullptr) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = tid() & 63, wave = tid() >> 6;
     const int rows_per_thread = (nrows + n_rg - 1) / n_rg;
     const int nbatch = (rows_per_thread + RPT - 1) / RPT;
     const int wpg = nkc / 64;  // waves per row group
@@ -423,7 +429,7 @@ struct Gemv {
       }
       lds_barrier();
       const int total = n_rg * nb * MR;
-      for (int t = threadIdx.x; t < total; t += kThreads) {
+      for (int t = tid(); t < total; t += kThreads) {
         const int g = t / (nb * MR), im = t % (nb * MR), i = im / MR, m = im % MR;
         const int r = g + (b * RPT + i) * n_rg;
         if (r < nrows) {
@@ -447,17 +453,19 @@ struct Gemv {
 };
 
 // ---------------------------------------------------------- MFMA GEMV (bf16)
-// Weights stream straight from HBM into the A operand of
-// v_mfma_f32_16x16x32_bf16 (16 weight rows x 32 k per instruction). The fp32
-// activations form the B operand (32 k x 16 columns, one column per activation
-// row) as a bf16 pair hi + lo with x - hi - lo below 2^-17 |x|, so two
-// instructions give an almost fp32-exact product. Lane layout (verified on
-// gfx950): lane l holds A[l%16][8*(l/16) + j], B[8*(l/16) + j][l%16] and
-// D[4*(l/16) + v][l%16].
-// Work items are (16-row tile t, 32-wide k-block kb) pairs g = t*KB + kb; wave w
-// takes g = w, w+8, w+16, ... (KB is a multiple of 8, so every wave covers every
-// tile with consecutive items); each wave writes its partial tiles to LDS and the
-// workgroup adds the 8 partials.
+// For bf16 weights and up to 8 activation rows the projections run on
+// v_mfma_f32_16x16x32_bf16. Lane layout of that instruction (checked on gfx950):
+// lane l holds A[l%16][8*(l/16) + j], B[8*(l/16) + j][l%16] and returns
+// D[4*(l/16) + v][l%16]. A = 16 weight rows, B = activations (column m = row m
+// of the pass). The order of the 32 products inside one instruction is free, so
+// lane group q = l/16 takes the 16 consecutive k's 64u + 16q .. 64u + 16q + 15 of
+// a 64-wide unit u in two instructions: each lane loads 32 contiguous bytes of
+// its weight row and the four groups read the row's full 128-byte line.
+// The fp32 activations enter as a bf16 pair hi + lo (|x - hi - lo| <= 2^-16 |x|),
+// so each unit is four instructions and the product keeps fp32-level accuracy.
+// Units (16-row tile t, unit u) are g = t * U + u with U = K / 64 a multiple of
+// 8; wave w takes g = w, w + 8, ..., so each wave holds one accumulator per tile
+// and the 8 wave partials are added once in LDS.
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -470,128 +478,267 @@ template <>
 struct IsBf16<bf16_t> {
   static constexpr bool value = true;
 };
+template <typename WT, int MR>
+struct UseMfma {
+  static constexpr bool value = IsBf16<WT>::value && MR <= 8;
+};
 
 __device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
-// x ~= hi + lo, both rounded to nearest even bf16
-__device__ __forceinline__ void split_bf16(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
-  W16 h, l;
+// 8 floats -> hi (8 bf16) and lo (8 bf16, the rounded remainder)
+__device__ __forceinline__ void split8(const float (&x)[8], W16& hi, W16& lo) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const uint32_t a = bf16_bits_rne(x[2 * j]), b = bf16_bits_rne(x[2 * j + 1]);
-    const uint32_t c2 = bf16_bits_rne(x[2 * j] - __uint_as_float(a << 16));
-    const uint32_t d2 = bf16_bits_rne(x[2 * j + 1] - __uint_as_float(b << 16));
-    h[j] = a | (b << 16);
-    l[j] = c2 | (d2 << 16);
+    const uint32_t ra = bf16_bits_rne(x[2 * j] - __uint_as_float(a << 16));
+    const uint32_t rb = bf16_bits_rne(x[2 * j + 1] - __uint_as_float(b << 16));
+    hi[j] = a | (b << 16);
+    lo[j] = ra | (rb << 16);
   }
-  hi = __builtin_bit_cast(bf16x8, h);
-  lo = __builtin_bit_cast(bf16x8, l);
 }
 
-template <int MR, int IMAX, bool PIPE = false>
-struct MGemv {
-  int KB, ntiles, n_items, nrows, wave, lane;
-  W16 a[IMAX];
-  W16 an[PIPE ? IMAX : 1];
+// Split activations in LDS: row m, 8-element chunk q -> 8 words at m * (K + 4) + q * 8:
+// 4 words of hi, then 4 words of lo. The 4 words of padding per row put the 16
+// rows that one MFMA operand read touches on different LDS banks.
+__device__ __forceinline__ int split_stride(int K) { return K + 4; }
+__device__ __forceinline__ void put_split(uint32_t* xsp, int stride, int m, int q, const float (&x)[8]) {
+  W16 hi, lo;
+  split8(x, hi, lo);
+  *reinterpret_cast<W16*>(xsp + (size_t)m * stride + q * 8) = hi;
+  *reinterpret_cast<W16*>(xsp + (size_t)m * stride + q * 8 + 4) = lo;
+}
+
+// Poll rows 0..R-1 of a parity activation buffer [kMaxRows][K] chunk by chunk
+// (8 floats = 4 words of 8 bytes) and store them split into xsp. With GAIN the
+// stored value is gain[k] * x (gain global, [K]) and sqc ([R][K/8]) receives
+// each chunk's sum of squares of the raw x for the row's RMSNorm.
+// Chunk i of the pass is handled by thread i % kThreads; up to CB chunks per
+// thread are in flight at once.
+template <int CB, bool GAIN>
+__device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, int K, int R, uint32_t par,
+                                            const float* gain, uint32_t* xsp, float* sqc) {
+  const int nch = K >> 3, total = R * nch;
+  for (int base = 0; base < total; base += CB * kThreads) {
+    uint32_t pending = 0;  // bit 4b + w: word w of chunk b still missing
+#pragma unroll
+    for (int b = 0; b < CB; ++b)
+      if (base + b * kThreads + tid() < total) pending |= 0xfu << (4 * b);
+    float gv[GAIN ? CB : 1][8];
+    if constexpr (GAIN) {
+#pragma unroll
+      for (int b = 0; b < CB; ++b) {
+        const int idx = base + b * kThreads + tid();
+        const int kq = idx < total ? (idx % nch) * 8 : 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) gv[b][e] = G(gain)[kq + e];
+      }
+    }
+    uint64_t v[CB][4];
+    uint64_t t0 = 0;
+    int spins = 0;
+    while (pending) {
+#pragma unroll
+      for (int b = 0; b < CB; ++b) {
+        const int idx = base + b * kThreads + tid();
+        const int m = idx / nch, q = idx - m * nch;
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          if (pending & (1u << (4 * b + w))) v[b][w] = pload2(src + (size_t)m * K + q * 8 + 2 * w);
+      }
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          if (pending & (1u << (4 * b + w))) {
+            const uint32_t lo = (uint32_t)v[b][w], hi = (uint32_t)(v[b][w] >> 32);
+            if ((lo & 1u) == par && (hi & 1u) == par) pending &= ~(1u << (4 * b + w));
+          }
+      if (!pending) break;
+      if ((++spins & 31) == 0) {
+        const uint64_t now = dclock();
+        if (t0 == 0) {
+          t0 = now;
+        } else if (now - t0 > kTimeoutTicks) {
+          status_raise(c.p, c.tag_base, RVQSD_ETIMEOUT);
+          return wg_sync_ok(c, false);
+        }
+        if (status_set(c.p, c.tag_base)) return wg_sync_ok(c, false);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < CB; ++b) {
+      const int idx = base + b * kThreads + tid();
+      if (idx < total) {
+        float x[8], s2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          x[2 * w] = __uint_as_float((uint32_t)v[b][w]);
+          x[2 * w + 1] = __uint_as_float((uint32_t)(v[b][w] >> 32));
+        }
+        if constexpr (GAIN) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            s2 = fmaf(x[e], x[e], s2);
+            x[e] *= gv[b][e];
+          }
+          sqc[idx] = s2;
+        }
+        const int m = idx / nch;
+        put_split(xsp, split_stride(K), m, idx - m * nch, x);
+      }
+    }
+  }
+  return wg_sync_ok(c, true);
+}
+
+// rstd[m] = 1 / sqrt(sum of the row's chunk sums / K + eps), m < R (one wave per row).
+__device__ __forceinline__ void rstd_from_chunks(const Ctx& c, const float* sqc, int K, int R) {
+  const int lane = tid() & 63, wave = tid() >> 6, nch = K >> 3;
+  for (int m = wave; m < R; m += kWaves) {
+    float s = 0.f;
+    for (int q = lane; q < nch; q += 64) s += sqc[m * nch + q];
+    s = wave_sum63(s);
+    if (lane == 63) c.sh->rstd[m] = 1.f / sqrtf(s / (float)K + c.p->rms_eps);
+  }
+  __syncthreads();
+}
+
+// out[r * MR + m] = sum_k W[row r][k] * X[m][k] for the workgroup's nrows rows,
+// W bf16 row-major with row pointer rowptr(r), X split in LDS (xsp, rows < R).
+// Wave w owns the 64-wide units u = w, w + 8, ... (upt = K / 512 of them) of
+// every 16-row tile, so one read of a unit's B operand serves all tiles. Up to
+// NT tiles are held at a time (tile groups), UPT >= upt. Each wave writes its
+// partial tiles to red[kWaves][NT][256]; reduce() adds the 8 partials.
+template <int MR, int NT, int UPT>
+struct MTile {
+  int U, upt, ntiles, nrows, wave, lane;
+  W16 a[NT][UPT][2];
 
   __device__ __forceinline__ void setup(int K, int nrows_) {
-    KB = K >> 5;
+    U = K >> 6;
+    upt = U >> 3;
     nrows = nrows_;
     ntiles = (nrows + 15) >> 4;
-    n_items = (ntiles * KB) >> 3;
-    wave = threadIdx.x >> 6;
-    lane = threadIdx.x & 63;
+    wave = __builtin_amdgcn_readfirstlane(tid() >> 6);
+    lane = tid() & 63;
   }
+  // weights of tiles tb .. tb + NT - 1
   template <typename RowPtr>
-  __device__ __forceinline__ void load_into(W16 (&dst)[IMAX], int chunk, RowPtr rowptr) {
+  __device__ __forceinline__ void load(int tb, RowPtr rowptr) {
 #pragma unroll
-    for (int i = 0; i < IMAX; ++i) {
-      const int ii = chunk * IMAX + i;
-      W16 v = (W16)(0u);
-      if (ii < n_items) {
-        const int g = wave + 8 * ii, t = g / KB, kb = g - t * KB, row = (t << 4) + (lane & 15);
-        if (row < nrows) v = *G(reinterpret_cast<const W16*>(rowptr(row) + kb * 32 + 8 * (lane >> 4)));
-      }
-      dst[i] = v;
-    }
-  }
-  template <typename RowPtr>
-  __device__ __forceinline__ void load(RowPtr rowptr) {
-    load_into(a, 0, rowptr);
-  }
-  __device__ __forceinline__ void flush(float* red, const f32x4& acc, int t) const {
-    const int base = (wave * ntiles + t) << 8;
+    for (int tt = 0; tt < NT; ++tt) {
+      const int row = ((tb + tt) << 4) + (lane & 15);
 #pragma unroll
-    for (int v = 0; v < 4; ++v) red[base + ((4 * (lane >> 4) + v) << 4) + (lane & 15)] = acc[v];
-  }
-  // Item range [ii_lo, ii_hi) of this wave; acc and cur_t carry over between calls.
-  template <typename RowPtr, typename BSrc>
-  __device__ __forceinline__ void mma_items(int ii_lo, int ii_hi, RowPtr rowptr, BSrc bsrc, float* red, f32x4& acc,
-                                            int& cur_t) {
-    const int nch = (ii_hi + IMAX - 1) / IMAX;
-    for (int ch = ii_lo / IMAX; ch < nch; ++ch) {
-      if (ch > ii_lo / IMAX || ch > 0) {
-        if constexpr (PIPE) {
-#pragma unroll
-          for (int i = 0; i < IMAX; ++i) a[i] = an[i];
-        } else {
-          if (ch > 0) load_into(a, ch, rowptr);
+      for (int j = 0; j < UPT; ++j) {
+        W16 v0 = (W16)(0u), v1 = (W16)(0u);
+        if (tb + tt < ntiles && j < upt && row < nrows) {
+          const bf16_t* w = rowptr(row) + (wave + 8 * j) * 64 + 16 * (lane >> 4);
+          v0 = *G(reinterpret_cast<const W16*>(w));
+          v1 = *G(reinterpret_cast<const W16*>(w + 8));
         }
-      }
-      if constexpr (PIPE) {
-        if (ch + 1 < nch) load_into(an, ch + 1, rowptr);
-      }
-#pragma unroll
-      for (int i = 0; i < IMAX; ++i) {
-        const int ii = ch * IMAX + i;
-        if (ii >= ii_lo && ii < ii_hi) {
-          const int g = wave + 8 * ii, t = g / KB, kb = g - t * KB;
-          if (t != cur_t) {
-            flush(red, acc, cur_t);
-            acc = (f32x4){0.f, 0.f, 0.f, 0.f};
-            cur_t = t;
-          }
-          float x[8];
-          const int m = lane & 15, k0 = kb * 32 + 8 * (lane >> 4);
-          if (m < MR) {
-            bsrc(k0, m, x);
-          } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = 0.f;
-          }
-          bf16x8 hi, lo;
-          split_bf16(x, hi, lo);
-          const bf16x8 av = __builtin_bit_cast(bf16x8, a[i]);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, acc, 0, 0, 0);
-        }
+        a[tt][j][0] = v0;
+        a[tt][j][1] = v1;
       }
     }
   }
-  // out[r * MR + m] = sum over the 8 wave partials (r < nrows, m < MR)
-  __device__ __forceinline__ void reduce(const float* red, float* out) const {
-    for (int o = threadIdx.x; o < nrows * MR; o += kThreads) {
-      const int r = o / MR, m = o - r * MR, t = r >> 4, i = r & 15;
+  // B operand of unit j for this lane (zero for activation rows >= R)
+  __device__ __forceinline__ void load_b(const uint32_t* xrow, bool live, int j, W16 (&bv)[4]) const {
+    if (live) {
+      const uint32_t* bp = xrow + (size_t)(wave + 8 * j) * 64;
+      bv[0] = *reinterpret_cast<const W16*>(bp);
+      bv[1] = *reinterpret_cast<const W16*>(bp + 4);
+      bv[2] = *reinterpret_cast<const W16*>(bp + 8);
+      bv[3] = *reinterpret_cast<const W16*>(bp + 12);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) bv[q] = (W16)(0u);
+    }
+  }
+  // tiles tb .. tb + NT - 1 (weights already loaded when preloaded); the hi and
+  // lo products accumulate separately
+  template <typename RowPtr>
+  __device__ __forceinline__ void mma(int tb, bool preloaded, RowPtr rowptr, const uint32_t* xsp, int R, float* red) {
+    const int m = lane & 15, q = lane >> 4;
+    const bool live = m < R;
+    if (!preloaded) load(tb, rowptr);
+    const uint32_t* xrow = xsp + (size_t)m * split_stride(U * 64) + 16 * q;
+    f32x4 acc[NT][2];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) acc[tt][0] = acc[tt][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    W16 b[UPT][4];
+    load_b(xrow, live, 0, b[0]);
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+      if (j < upt) {
+        if (j + 1 < UPT && j + 1 < upt) load_b(xrow, live, j + 1, b[j + 1]);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+          if (tb + tt < ntiles) {
+            const bf16x8 a0 = __builtin_bit_cast(bf16x8, a[tt][j][0]), a1 = __builtin_bit_cast(bf16x8, a[tt][j][1]);
+            acc[tt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, b[j][0]), acc[tt][0], 0, 0, 0);
+            acc[tt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, b[j][1]), acc[tt][1], 0, 0, 0);
+            acc[tt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, b[j][2]), acc[tt][0], 0, 0, 0);
+            acc[tt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, b[j][3]), acc[tt][1], 0, 0, 0);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+      if (tb + tt < ntiles) {
+        const f32x4 s4 = acc[tt][0] + acc[tt][1];
+        float* dst = red + ((size_t)(wave * NT + tt) << 8);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) dst[((4 * q + v) << 4) + m] = s4[v];
+      }
+    }
+  }
+  // out[r * MR + mm] for rows r of tiles tb .. tb + NT - 1 (r < nrows), mm < MR: the
+  // sum of the 8 wave partials, times rstd[mm] when given
+  __device__ __forceinline__ void reduce(const float* red, float* out, const float* rstd, int tb) const {
+    const int r0 = tb << 4, r1 = min((tb + NT) << 4, nrows);
+    for (int o = tid(); o < (r1 - r0) * MR; o += kThreads) {
+      const int r = r0 + o / MR, mm = o % MR, t = (r >> 4) - tb, i = r & 15;
       float s = 0.f;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) s += red[((w * ntiles + t) << 8) + (i << 4) + m];
-      out[o] = s;
+      for (int w = 0; w < kWaves; ++w) s += red[((w * NT + t) << 8) + (i << 4) + mm];
+      out[r * MR + mm] = rstd ? s * rstd[mm] : s;
     }
   }
-  // whole product from one staged activation block
-  template <typename RowPtr, typename BSrc>
-  __device__ __forceinline__ void run(RowPtr rowptr, BSrc bsrc, float* red, float* out) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    int cur_t = 0;
-    mma_items(0, n_items, rowptr, bsrc, red, acc, cur_t);
-    flush(red, acc, cur_t);
-    lds_barrier();
-    reduce(red, out);
-    lds_barrier();
+  // whole product for nrows rows: tile groups of NT, weights of the first group preloaded
+  template <typename RowPtr>
+  __device__ __forceinline__ void run(RowPtr rowptr, const uint32_t* xsp, int R, float* red, float* out,
+                                      const float* rstd) {
+    for (int tb = 0; tb < ntiles; tb += NT) {
+      mma(tb, tb == 0, rowptr, xsp, R, red);
+      lds_barrier();
+      reduce(red, out, rstd, tb);
+      lds_barrier();
+    }
   }
 };
+
+// Split rows 0..R-1 of fp32 activations xs[MR][K] into xsp, times gain
+// (global, nullable); sqc (nullable) receives each chunk's sum of squares of
+// the raw values.
+__device__ __forceinline__ void split_rows(const float* xs, uint32_t* xsp, int K, int R, const float* gain, float* sqc) {
+  const int nch = K >> 3;
+  for (int idx = tid(); idx < R * nch; idx += kThreads) {
+    const int m = idx / nch, q = idx - m * nch;
+    float x[8], s2 = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float v = xs[(size_t)idx * 8 + e];
+      s2 = fmaf(v, v, s2);
+      x[e] = gain ? v * G(gain)[q * 8 + e] : v;
+    }
+    put_split(xsp, split_stride(K), m, q, x);
+    if (sqc) sqc[idx] = s2;
+  }
+  __syncthreads();
+}
 
 // This thread's chunk of the staged activations xs[MR][ld] (k = kc*EPC ..),
 // times g[e] when g != nullptr; sq[m] = sum of squares of the raw chunk.
@@ -616,7 +763,7 @@ __device__ __forceinline__ void chunk_from_lds(const float* xs, int ld, int kc, 
 // xs[MR][ncols] (rows >= R zero-filled).
 template <int MR>
 __device__ __forceinline__ bool stage_par(const Ctx& c, const uint32_t* src, int ncols, int R, uint32_t par, float* xs) {
-  for (int i = threadIdx.x; i < (MR - R) * ncols; i += kThreads) xs[R * ncols + i] = 0.f;
+  for (int i = tid(); i < (MR - R) * ncols; i += kThreads) xs[R * ncols + i] = 0.f;
   const bool ok = poll_pairs(
       c, R * ncols / 2, par, [=](int i) { return src + 2 * i; },
       [=](int i, float lo, float hi) {
@@ -629,7 +776,7 @@ __device__ __forceinline__ bool stage_par(const Ctx& c, const uint32_t* src, int
 // rstd[m] = 1 / sqrt(mean(xs[m]^2) + eps) for m < R, 0 above.
 template <int MR>
 __device__ __forceinline__ void row_rstd(const Ctx& c, const float* xs, int ncols, int R) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = tid() & 63, wave = tid() >> 6;
   for (int m = wave; m < MR; m += kWaves) {
     float s = 0.f;
     if (m < R)
@@ -648,7 +795,7 @@ __device__ __forceinline__ void gather_rows(const Ctx& c, float* xs) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
   const int H = p->H, R = sh->rows;
-  for (int i = threadIdx.x; i < MR * H; i += kThreads) {
+  for (int i = tid(); i < MR * H; i += kThreads) {
     int r = i / H, k = i % H;
     float v = 0.f;
     if (r < R) {
@@ -692,7 +839,7 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
     gather_rows<WT, MR>(c, xs);
     // keep this workgroup's residual columns
     const int o0 = blockIdx.x * c.cpw;
-    for (int i = threadIdx.x; i < kMaxRows * c.cpw; i += kThreads) {
+    for (int i = tid(); i < kMaxRows * c.cpw; i += kThreads) {
       int m = i / c.cpw, j = i % c.cpw;
       c.xown[i] = (m < MR && o0 + j < H) ? xs[m * H + o0 + j] : 0.f;
     }
@@ -705,7 +852,7 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
     chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, g.active, g.gain, xg, sq);
     g.run(c, xg, rowptr, out, sq);
     const uint32_t par = par_layer(c, sh->pass, l);
-    for (int i = threadIdx.x; i < MR * nrows; i += kThreads) {
+    for (int i = tid(); i < MR * nrows; i += kThreads) {
       const int m = i / nrows, r = i % nrows;
       pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
     }
@@ -715,9 +862,32 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
   return true;
 }
 
+// Sum over the 32 lanes of each half of the wave (every lane gets its half's sum).
+__device__ __forceinline__ float half_sum(float v) {
+  v = row16_sum(v);
+  v += dpp_rows<0x142, 0xA>(v);  // rows 1 and 3 += last lane of rows 0 and 2
+  const float a = lane63(v) , b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 31));
+  return (tid() & 32) ? a : b;
+}
+// max over the 16 lanes of each DPP row, in every lane of the row
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
+  return v;
+}
+__device__ __forceinline__ float lane_val(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
 // Attention for query head h = blockIdx.x (h < nq): per-head RMSNorm of q and k,
-// rotate-half RoPE, append k and v to this head's cache (LDS-resident when it
-// fits), causal softmax over positions 0..s of each row, output to attnb.
+// rotate-half RoPE, causal softmax over positions 0..s of each row, output to
+// attnb. The KV cache of the head lives in device memory ([L][kMaxPos][2][d],
+// k after norm and RoPE, v raw); the positions committed by earlier passes are
+// prefetched into LDS while the workgroup waits for this pass's q, k and v.
+// In LDS each position's k and v are padded to 2d + 4 floats so that the 16
+// positions read by one wave fall on different banks.
 template <int MR>
 __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   const KParams* p = c.p;
@@ -727,12 +897,22 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   const int d = p->d, R = sh->rows, N = p->nqkv, fp = sh->first_pos, half = d / 2;
   const int g = h / (p->nq / p->nkv);
   const int qoff = h * d, koff = p->qdim + g * d;
+  const int ps = 2 * d + 4;        // LDS floats per position
   float* qs = c.work;              // [kMaxRows][d], then ks, vs
   float* ks = qs + kMaxRows * d;
   float* vs = ks + kMaxRows * d;
-  float* sc = vs + kMaxRows * d;   // [kMaxRows][kMaxPos]
-  float* cache = p->kv_in_lds ? c.kvlds + (size_t)l * kMaxPos * 2 * d
-                              : p->kvc + ((size_t)h * p->L + l) * kMaxPos * 2 * d;
+  float* kv = vs + kMaxRows * d;   // [kMaxPos][ps]: k, v of every position
+  uint64_t* gkv = reinterpret_cast<uint64_t*>(p->kvc + ((size_t)h * p->L + l) * kMaxPos * 2 * d);
+  const int lane = tid() & 63, wave = tid() >> 6;
+  // past positions 0 .. fp-1: issue the loads now, store them to LDS after the wait
+  constexpr int KVW = 8;  // 64-bit words per thread: up to 16 positions x 2 x 128 floats
+  const int past_words = fp * d;  // fp * 2d floats = fp * d words
+  uint64_t pw[KVW];
+#pragma unroll
+  for (int i = 0; i < KVW; ++i) {
+    const int wi = tid() + i * kThreads;
+    pw[i] = wi < past_words ? xload(gkv + wi) : 0ull;
+  }
   const uint32_t par = par_layer(c, sh->pass, l);
   // q of head h, k and v of kv head g, for every row of the pass (pairs of words);
   // qs, ks, vs are consecutive [kMaxRows][d] blocks and v of kv head g follows k at +kvdim
@@ -750,75 +930,115 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
         qs[part * kMaxRows * d + 2 * rem] = lo;
         qs[part * kMaxRows * d + 2 * rem + 1] = hi;
       });
+#pragma unroll
+  for (int i = 0; i < KVW; ++i) {
+    const int wi = tid() + i * kThreads;
+    if (wi < past_words) {
+      const int pos = wi / d, w = wi - pos * d;
+      reinterpret_cast<uint64_t*>(kv + (size_t)pos * ps)[w] = pw[i];
+    }
+  }
   if (!wg_sync_ok(c, ok)) return false;
+  // per-head RMSNorm + RoPE of q (vectors 0..R-1) and k (R..2R-1), one half-wave
+  // per vector; lane i of the half holds dimensions i + 32 j and their rotation
+  // partners i + 32 j + d/2.
   const float* qn = c.attn_const + (size_t)l * 2 * d;
   const float* kn = qn + d;
   const float* rope = c.attn_const + (size_t)p->L * 2 * d;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int v = wave; v < 2 * R; v += kWaves) {
-    float* x = v < R ? qs + v * d : ks + (v - R) * d;
-    const float* gn = v < R ? qn : kn;
-    const int r = v < R ? v : v - R;
-    float s2 = 0.f;
-    for (int i = lane; i < d; i += 64) s2 = fmaf(x[i], x[i], s2);
-    const float rs = p->qk_norm ? 1.f / sqrtf(lane63(wave_sum63(s2)) / (float)d + p->rms_eps) : 1.f;
+  const int hl = lane & 31;
+  for (int v = 2 * wave + (lane >> 5); v < 2 * R; v += 2 * kWaves) {
+    const bool isq = v < R;
+    const int r = isq ? v : v - R;
+    const float* x = isq ? qs + r * d : ks + r * d;
+    const float* gn = isq ? qn : kn;
     const int pos = fp + r;
-    for (int i = lane; i < half; i += 64) {
-      float a = x[i], b = x[i + half];
-      if (p->qk_norm) {
-        a = a * rs * gn[i];
-        b = b * rs * gn[i + half];
+    float a[4], b[4];
+    float s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = hl + 32 * j;
+      a[j] = i < half ? x[i] : 0.f;
+      b[j] = i < half ? x[i + half] : 0.f;
+      s2 = fmaf(a[j], a[j], fmaf(b[j], b[j], s2));
+    }
+    const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)d + p->rms_eps) : 1.f;
+    float* dst = isq ? qs + r * d : kv + (size_t)pos * ps;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = hl + 32 * j;
+      if (i < half) {
+        float u = a[j], w = b[j];
+        if (p->qk_norm) {
+          u = u * rs * gn[i];
+          w = w * rs * gn[i + half];
+        }
+        const float cs = rope[(pos * half + i) * 2], sn = rope[(pos * half + i) * 2 + 1];
+        dst[i] = u * cs - w * sn;
+        dst[i + half] = w * cs + u * sn;
       }
-      const float cs = rope[(pos * half + i) * 2], sn = rope[(pos * half + i) * 2 + 1];
-      x[i] = a * cs - b * sn;
-      x[i + half] = b * cs + a * sn;
+    }
+    if (!isq) {
+      // v of this row next to its k
+      for (int i = hl; i < d; i += 32) kv[(size_t)pos * ps + d + i] = vs[r * d + i];
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < R * d; i += kThreads) {
-    const int r = i / d, k = i - r * d;
-    cache[((size_t)(fp + r) * 2 + 0) * d + k] = ks[i];
-    cache[((size_t)(fp + r) * 2 + 1) * d + k] = vs[i];
-  }
-  __syncthreads();
-  // scores: one 16-lane DPP row per (row, position) pair, d/16 dimensions per lane
-  const int npos = fp + R, npairs = R * npos, dpl = d / 16;
+  // one wave per row: lane = (position t = lane / 4, quarter j = lane % 4 of the dimensions)
   const float scale = 1.f / sqrtf((float)d);
-  const int grp = threadIdx.x >> 4, j = threadIdx.x & 15;
-  for (int pr = grp; pr < npairs; pr += kThreads / 16) {
-    const int r = pr / npos, t = pr - r * npos;
-    float part = 0.f;
-    if (t <= fp + r) {
-      const float* qv = qs + r * d + j * dpl;
-      const float* kv = cache + (size_t)t * 2 * d + j * dpl;
-      for (int e = 0; e < dpl; ++e) part = fmaf(qv[e], kv[e], part);
+  const int t = lane >> 2, qj = lane & 3, dq = d / 4;
+  for (int r = wave; r < MR; r += kWaves) {
+    if (r < R) {
+      const int last = fp + r;  // causal: positions 0 .. last
+      float part = 0.f;
+      if (t <= last) {
+        const float4* qv = reinterpret_cast<const float4*>(qs + r * d + qj * dq);
+        const float4* kk = reinterpret_cast<const float4*>(kv + (size_t)t * ps + qj * dq);
+        float p0 = 0.f, p1 = 0.f;
+#pragma unroll 4
+        for (int e = 0; e < dq / 4; ++e) {
+          const float4 qa = qv[e], ka = kk[e];
+          p0 = fmaf(qa.x, ka.x, p0);
+          p1 = fmaf(qa.y, ka.y, p1);
+          p0 = fmaf(qa.z, ka.z, p0);
+          p1 = fmaf(qa.w, ka.w, p1);
+        }
+        part = p0 + p1;
+      }
+      part += dpp<0xB1>(part);  // quad sums: xor 1, xor 2
+      part += dpp<0x4E>(part);
+      const float sc = t <= last ? part * scale : -INFINITY;
+      const float rm = row16_max(sc);
+      const float mx = fmaxf(fmaxf(lane_val(rm, 15), lane_val(rm, 31)), fmaxf(lane_val(rm, 47), lane_val(rm, 63)));
+      const float e = t <= last ? expf(sc - mx) : 0.f;
+      const float rsum = row16_sum(qj == 0 ? e : 0.f);
+      const float z = (lane_val(rsum, 15) + lane_val(rsum, 31)) + (lane_val(rsum, 47) + lane_val(rsum, 63));
+      const float pr = e / z;
+      // o[r][i] = sum_t pr_t v[t][i] for i = lane + 64 j (head_dim <= 256)
+      float o[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int tt = 0; tt < kMaxPos; ++tt) {
+        if (tt <= last) {
+          const float pt = lane_val(pr, 4 * tt);
+          const float* vv = kv + (size_t)tt * ps + d;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (lane + 64 * j < d) o[j] = fmaf(pt, vv[lane + 64 * j], o[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (lane + 64 * j < d) pstore(p->attnb + (size_t)r * p->qdim + qoff + lane + 64 * j, o[j], par);
+    } else {
+      for (int i = lane; i < d; i += 64) pstore(p->attnb + (size_t)r * p->qdim + qoff + i, 0.f, par);
     }
-    part = row16_sum(part);
-    if (j == 0) sc[r * kMaxPos + t] = t <= fp + r ? part * scale : -INFINITY;
   }
-  __syncthreads();
-  if ((int)threadIdx.x < R) {
-    const int r = threadIdx.x;
-    float mx = -INFINITY;
-    for (int t = 0; t <= fp + r; ++t) mx = fmaxf(mx, sc[r * kMaxPos + t]);
-    float z = 0.f;
-    for (int t = 0; t <= fp + r; ++t) {
-      const float e = expf(sc[r * kMaxPos + t] - mx);
-      sc[r * kMaxPos + t] = e;
-      z += e;
-    }
-    const float iz = 1.f / z;
-    for (int t = 0; t <= fp + r; ++t) sc[r * kMaxPos + t] *= iz;
+  // device copy of the new k, v for later passes (after the outputs are out)
+  for (int wi = tid(); wi < R * d; wi += kThreads) {
+    const int pos = fp + wi / d, w = wi % d;
+    __hip_atomic_store(G(gkv + (size_t)pos * d + w), reinterpret_cast<const uint64_t*>(kv + (size_t)pos * ps)[w],
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  __syncthreads();
-  for (int i = threadIdx.x; i < MR * d; i += kThreads) {
-    const int r = i / d, k = i - r * d;
-    float o = 0.f;
-    if (r < R)
-      for (int t = 0; t <= fp + r; ++t) o = fmaf(sc[r * kMaxPos + t], cache[((size_t)t * 2 + 1) * d + k], o);
-    pstore(p->attnb + (size_t)r * p->qdim + qoff + k, o, par);
-  }
-  // the next phase reuses the work area (scores, q, k, v): no wave may still be reading it
+  // the next phase reuses the work area: no wave may still be reading it
   lds_barrier();
   return true;
 }
@@ -896,7 +1116,7 @@ __device__ __forceinline__ bool phase_proj(const Ctx& c, int l, bool is_down) {
   if (nrows > 0) {
     g.run(c, xg, rowptr, out);
     const uint32_t xpar = is_down ? kParDown : kParO;
-    for (int i = threadIdx.x; i < MR * nrows; i += kThreads) {
+    for (int i = tid(); i < MR * nrows; i += kThreads) {
       const int m = i / nrows, r = i % nrows;
       float v = 0.f;
       if (m < R) {
@@ -933,7 +1153,7 @@ __device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
     chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, g.active, g.gain, xg, sq);
     g.run(c, xg, rowptr, out, sq);
     const uint32_t par = par_layer(c, sh->pass, l);
-    for (int i = threadIdx.x; i < MR * nf; i += kThreads) {
+    for (int i = tid(); i < MR * nf; i += kThreads) {
       const int m = i / nf, j = i % nf;
       float a = 0.f;
       if (m < R) {
@@ -942,6 +1162,136 @@ __device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
       }
       pstore(p->actb + (size_t)m * F + f0 + j, a, par);
     }
+  }
+  lds_barrier();  // the work area is reused by the next phase
+  return true;
+}
+
+// ------------------------------------------------ MFMA phases (bf16, <= 8 rows)
+// Same partition of weight rows over workgroups as the phases above; the
+// weights of the first round are loaded before the wait for the activations.
+
+template <int MR>
+__device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows, N = p->nqkv;
+  const int rpw = (N + p->nwg - 1) / p->nwg, row0 = blockIdx.x * rpw;
+  const int nrows = max(0, min(rpw, N - row0));
+  const bf16_t* wq = wptr<bf16_t>(p, layer_off(p, l, p->o_wq));
+  const bf16_t* wk = wptr<bf16_t>(p, layer_off(p, l, p->o_wk));
+  const bf16_t* wv = wptr<bf16_t>(p, layer_off(p, l, p->o_wv));
+  const int qd = p->qdim, kd = p->kvdim;
+  auto rowptr = [&](int r) -> const bf16_t* {
+    const int o = row0 + r;
+    if (o < qd) return wq + (size_t)o * H;
+    if (o < qd + kd) return wk + (size_t)(o - qd) * H;
+    return wv + (size_t)(o - qd - kd) * H;
+  };
+  MTile<MR, 1, kUptH> mt;
+  mt.setup(H, nrows);
+  mt.load(0, rowptr);
+  const float* gain = fptr(p, layer_off(p, l, p->o_attn_norm));
+  uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);  // [MR][H + 4] split
+  float* sqc = c.work + MR * (H + 4);                   // [MR][H/8]
+  float* red = sqc + MR * (H >> 3);                     // [kWaves][1][256]
+  float* out = red + kWaves * 256;                      // [nrows][MR]
+  float* xs = out + mt.ntiles * 16 * MR;                // [MR][H] fp32 gathered rows (layer 0)
+  if (l == 0) {
+    gather_rows<bf16_t, MR>(c, xs);
+    // keep this workgroup's residual columns
+    const int o0 = blockIdx.x * c.cpw;
+    for (int i = tid(); i < kMaxRows * c.cpw; i += kThreads) {
+      const int m = i / c.cpw, j = i % c.cpw;
+      c.xown[i] = (m < MR && o0 + j < H) ? xs[m * H + o0 + j] : 0.f;
+    }
+    __syncthreads();
+    split_rows(xs, xsp, H, R, gain, sqc);
+  } else {
+    if (nrows == 0) return true;
+    if (!stage_split<2, true>(c, p->xb, H, R, kParDown, gain, xsp, sqc)) return false;
+  }
+  if (nrows > 0) {
+    rstd_from_chunks(c, sqc, H, R);
+    mt.run(rowptr, xsp, R, red, out, sh->rstd);
+    const uint32_t par = par_layer(c, sh->pass, l);
+    for (int i = tid(); i < MR * nrows; i += kThreads) {
+      const int m = i / nrows, r = i % nrows;
+      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
+    }
+  }
+  lds_barrier();  // the work area is reused by the next phase
+  return true;
+}
+
+// O projection (layer l) or down projection: x_own += W * act; publish x_own.
+template <int MR, int CB, int UPT>
+__device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows;
+  const int K = is_down ? p->F : p->qdim;
+  const int row0 = blockIdx.x * c.cpw;
+  const int nrows = max(0, min(c.cpw, H - row0));
+  if (nrows == 0) return true;
+  const bf16_t* W = wptr<bf16_t>(p, layer_off(p, l, is_down ? p->o_wd : p->o_wo));
+  auto rowptr = [&](int r) -> const bf16_t* { return W + (size_t)(row0 + r) * K; };
+  MTile<MR, 1, UPT> mt;
+  mt.setup(K, nrows);
+  mt.load(0, rowptr);
+  uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);  // [MR][K + 4] split
+  float* red = c.work + MR * (K + 4);                   // [kWaves][1][256]
+  float* out = red + kWaves * 256;                      // [nrows][MR]
+  const uint32_t* src = is_down ? p->actb : p->attnb;
+  const uint32_t par = par_layer(c, sh->pass, l);
+  if (!stage_split<CB, false>(c, src, K, R, par, nullptr, xsp, nullptr)) return false;
+  mt.run(rowptr, xsp, R, red, out, nullptr);
+  const uint32_t xpar = is_down ? kParDown : kParO;
+  for (int i = tid(); i < MR * nrows; i += kThreads) {
+    const int m = i / nrows, r = i % nrows;
+    float v = 0.f;
+    if (m < R) {
+      v = c.xown[m * c.cpw + r] + out[r * MR + m];
+      c.xown[m * c.cpw + r] = v;
+    }
+    pstore(p->xb + (size_t)m * H + row0 + r, v, xpar);
+  }
+  __syncthreads();
+  return true;
+}
+
+// gate and up rows interleaved (2j = gate row f0 + j, 2j + 1 = up row); act = SiLU(gate) * up.
+template <int MR>
+__device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows, F = p->F;
+  const int fpw = (F + p->nwg - 1) / p->nwg, f0 = blockIdx.x * fpw;
+  const int nf = max(0, min(fpw, F - f0));
+  if (nf == 0) return true;
+  const bf16_t* wg = wptr<bf16_t>(p, layer_off(p, l, p->o_wg));
+  const bf16_t* wu = wptr<bf16_t>(p, layer_off(p, l, p->o_wu));
+  auto rowptr = [&](int r) -> const bf16_t* { return ((r & 1) ? wu : wg) + (size_t)(f0 + (r >> 1)) * H; };
+  MTile<MR, 2, kUptH> mt;
+  mt.setup(H, 2 * nf);
+  mt.load(0, rowptr);
+  uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);  // [MR][H + 4] split
+  float* sqc = c.work + MR * (H + 4);                   // [MR][H/8]
+  float* red = sqc + MR * (H >> 3);                     // [kWaves][2][256]
+  float* out = red + kWaves * 2 * 256;                  // [2 nf][MR]
+  const float* gain = fptr(p, layer_off(p, l, p->o_mlp_norm));
+  if (!stage_split<2, true>(c, p->xb, H, R, kParO, gain, xsp, sqc)) return false;
+  rstd_from_chunks(c, sqc, H, R);
+  mt.run(rowptr, xsp, R, red, out, sh->rstd);
+  const uint32_t par = par_layer(c, sh->pass, l);
+  for (int i = tid(); i < MR * nf; i += kThreads) {
+    const int m = i / nf, j = i % nf;
+    float a = 0.f;
+    if (m < R) {
+      const float gt = out[(2 * j) * MR + m], up = out[(2 * j + 1) * MR + m];
+      a = gt / (1.f + expf(-gt)) * up;
+    }
+    pstore(p->actb + (size_t)m * F + f0 + j, a, par);
   }
   lds_barrier();  // the work area is reused by the next phase
   return true;
@@ -980,7 +1330,7 @@ __device__ __forceinline__ bool phase_heads(const Ctx& c) {
   const int nrows = hi < nh ? max(0, min(rpw, V - v0)) : 0;
   if (nrows == 0) return true;
   // this head's vectors: (row, offset j); j = 0 is the verify row at position t
-  if (threadIdx.x == 0) {
+  if (tid() == 0) {
     int nv = 0;
     for (int r = 0; r < R && nv < MR; ++r) {
       const int s = sh->first_pos + r;
@@ -1028,7 +1378,101 @@ __device__ __forceinline__ bool phase_heads(const Ctx& c) {
   }
   g.run(c, xg, rowptr, out);
   const uint32_t tag = tag_of(c, sh->pass, ph_heads(L));
-  for (int i = threadIdx.x; i < nv * nrows; i += kThreads) {
+  for (int i = tid(); i < nv * nrows; i += kThreads) {
+    const int v = i / nrows, r = i % nrows;
+    xstoref(p->logb + ((size_t)(sh->pass & 1) * p->n_slots + sh->hv_slot[v]) * V + v0 + r, tag, out[r * MR + v]);
+  }
+  lds_barrier();  // the work area is reused by the next phase
+  return true;
+}
+
+// LM heads on MFMA: same head/row assignment as phase_heads. The vectors of a
+// head (verify rows and h_s + b_j draft rows, final-normed) form the B columns;
+// the head's rows are processed in groups of 4 tiles.
+template <int MR>
+__device__ __forceinline__ bool phase_heads_m(const Ctx& c) {
+  const KParams* p = c.p;
+  Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows, V = p->V, L = p->L;
+  int t_lo = 1 << 20, t_hi = -1;
+  for (int r = 0; r < R; ++r) {
+    const int s = sh->first_pos + r;
+    if (is_verify_row(sh, r) && s >= 1) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
+    const int nd = drafts_of_row(p, sh, r);
+    if (nd > 0) { t_lo = min(t_lo, s + 1); t_hi = max(t_hi, s + nd); }
+  }
+  const int nh = t_hi - t_lo + 1;
+  const int wph = p->nwg / nh;
+  const int hi = blockIdx.x / wph;
+  const int t = t_lo + hi;
+  const int rpw = (V + wph - 1) / wph, v0 = (blockIdx.x % wph) * rpw;
+  const int nrows = hi < nh ? max(0, min(rpw, V - v0)) : 0;
+  if (nrows == 0) return true;
+  const bf16_t* W = wptr<bf16_t>(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
+  auto rowptr = [&](int r) -> const bf16_t* { return W + (size_t)(v0 + r) * H; };
+  constexpr int TG = 5;  // tiles per group
+  MTile<MR, TG, kUptH> mt;
+  mt.setup(H, nrows);
+  mt.load(0, rowptr);
+  if (tid() == 0) {
+    int nv = 0;
+    for (int r = 0; r < R && nv < MR; ++r) {
+      const int s = sh->first_pos + r;
+      if (s == t && is_verify_row(sh, r)) {
+        sh->hv_row[nv] = r; sh->hv_off[nv] = 0; sh->hv_slot[nv] = r; ++nv;
+      }
+      const int nd = drafts_of_row(p, sh, r);
+      const int j = t - s;
+      if (j >= 1 && j <= nd && nv < MR) {
+        sh->hv_row[nv] = r; sh->hv_off[nv] = j; sh->hv_slot[nv] = draft_slot(p, r, j); ++nv;
+      }
+    }
+    sh->hv_n = nv;
+  }
+  __syncthreads();
+  const int nv = sh->hv_n, nch = H >> 3;
+  // this thread's vector chunks: final-norm gain and offset values, fetched before the wait
+  constexpr int VC = (MR * 128 + kThreads - 1) / kThreads;  // chunks per thread at hidden <= 1024
+  const float* gn = fptr(p, p->o_final_norm);
+  const float* ofs = fptr(p, p->o_offsets);
+  float* xs = c.work;                                         // [MR][H] fp32
+  uint32_t* vsp = reinterpret_cast<uint32_t*>(xs + MR * H);   // [MR][H + 4] split vectors
+  float* red = xs + MR * H + MR * (H + 4);                    // [kWaves][TG][256]
+  float* out = red + kWaves * TG * 256;                       // [nrows][MR]
+  for (int base = 0; base < nv * nch; base += VC * kThreads) {
+    float gq[VC][8], oq[VC][8];
+#pragma unroll
+    for (int b = 0; b < VC; ++b) {
+      const int idx = base + b * kThreads + tid();
+      const int v = idx / nch, q = idx - v * nch;
+      const int vo = idx < nv * nch ? sh->hv_off[v] : 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        gq[b][e] = idx < nv * nch ? G(gn)[q * 8 + e] : 0.f;
+        oq[b][e] = vo > 0 ? G(ofs)[(size_t)(vo - 1) * H + q * 8 + e] : 0.f;
+      }
+    }
+    if (base == 0) {
+      if (!stage_par<MR>(c, p->xb, H, R, kParDown, xs)) return false;
+      row_rstd<MR>(c, xs, H, R);
+    }
+#pragma unroll
+    for (int b = 0; b < VC; ++b) {
+      const int idx = base + b * kThreads + tid();
+      if (idx < nv * nch) {
+        const int v = idx / nch, q = idx - v * nch, vr = sh->hv_row[v];
+        const float rs = sh->rstd[vr];
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = xs[vr * H + q * 8 + e] * rs * gq[b][e] + oq[b][e];
+        put_split(vsp, split_stride(H), v, q, x);
+      }
+    }
+  }
+  __syncthreads();
+  mt.run(rowptr, vsp, nv, red, out, nullptr);
+  const uint32_t tag = tag_of(c, sh->pass, ph_heads(L));
+  for (int i = tid(); i < nv * nrows; i += kThreads) {
     const int v = i / nrows, r = i % nrows;
     xstoref(p->logb + ((size_t)(sh->pass & 1) * p->n_slots + sh->hv_slot[v]) * V + v0 + r, tag, out[r * MR + v]);
   }
@@ -1046,7 +1490,7 @@ __device__ __forceinline__ uint32_t fkey(float f) {
 
 // exclusive prefix over the workgroup in thread order; returns total via *total
 __device__ __forceinline__ int block_excl_scan(Shared* sh, int v, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = tid() & 63, wave = tid() >> 6;
   int inc = wave_scan_incl(v);
   if (lane == 63) sh->iscan[wave] = inc;
   __syncthreads();
@@ -1065,12 +1509,12 @@ __device__ __forceinline__ int block_excl_scan(Shared* sh, int v, int* total) {
 __device__ __forceinline__ int topk_select(const Ctx& c, const float* lg, int V, int topk, int* sidx, float* slog) {
   Shared* sh = c.sh;
   const int ept = (V + kThreads - 1) / kThreads;
-  const int i0 = threadIdx.x * ept;
+  const int i0 = tid() * ept;
   const int kk0 = min(topk, V);
   uint32_t prefix = 0, pmask = 0;
   int kk = kk0;
   for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = threadIdx.x; i < 256; i += kThreads) sh->hist[i] = 0;
+    for (int i = tid(); i < 256; i += kThreads) sh->hist[i] = 0;
     __syncthreads();
     for (int e = 0; e < ept; ++e) {
       int i = i0 + e;
@@ -1080,8 +1524,8 @@ __device__ __forceinline__ int topk_select(const Ctx& c, const float* lg, int V,
       }
     }
     __syncthreads();
-    if (threadIdx.x < 64) {
-      const int lane = threadIdx.x;
+    if (tid() < 64) {
+      const int lane = tid();
       int b[4], loc = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) { b[q] = (int)sh->hist[4 * lane + q]; loc += b[q]; }
@@ -1143,8 +1587,8 @@ __device__ __forceinline__ int topk_select(const Ctx& c, const float* lg, int V,
 
 // wave 0: probabilities of the top-k support, p = exp((l - max)/T) / Z in fp64
 __device__ __forceinline__ void softmax_support(const float* slog, int n, double T, double* prob) {
-  if (threadIdx.x >= 64) return;
-  const int lane = threadIdx.x;
+  if (tid() >= 64) return;
+  const int lane = tid();
   double mx = -INFINITY;
   for (int i = lane; i < n; i += 64) mx = fmax(mx, (double)slog[i]);
   mx = wave_maxd(mx);
@@ -1160,7 +1604,7 @@ __device__ __forceinline__ void softmax_support(const float* slog, int n, double
 
 // wave 0: inverse CDF of weights w[0..n) (ascending token order) at u; returns position
 __device__ __forceinline__ int inverse_cdf(const double* w, int n, double u) {
-  const int lane = threadIdx.x;
+  const int lane = tid();
   const int per = (n + 63) / 64;
   const int b = lane * per;
   double loc = 0.0;
@@ -1235,13 +1679,13 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
   bool ok = poll_range(c, src, V, tag, [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); });
   if (!wg_sync_ok(c, ok)) return false;
   if (p->tr_logits && sh->pass < p->tr_max_rounds)
-    for (int i = threadIdx.x; i < V; i += kThreads)
+    for (int i = tid(); i < V; i += kThreads)
       G(p->tr_logits)[((size_t)sh->pass * p->n_slots + slot) * V + i] = lg[i];
   const int n = topk_select(c, lg, V, p->topk, sidx, slog);
-  if (threadIdx.x < 64) {
+  if (tid() < 64) {
     bool fin = false;
-    for (int i = threadIdx.x; i < n; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
-    if (!__any(fin) && threadIdx.x == 0) status_raise(p, c.tag_base, RVQSD_ENUMERIC);
+    for (int i = tid(); i < n; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
+    if (!__any(fin) && tid() == 0) status_raise(p, c.tag_base, RVQSD_ENUMERIC);
   }
   softmax_support(slog, n, p->temperature, prob);
   __syncthreads();
@@ -1249,12 +1693,12 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
   if (j > 0) {
     // draft for position t from the hidden state of `row` plus offset b_j
     uint64_t* rec = p->drec + ((size_t)par * p->n_slots + slot) * p->drec_words;
-    if (threadIdx.x < 64) {
+    if (tid() < 64) {
       int pos;
       if (p->greedy) {
         double best = -1.0;
         int bi = n;
-        for (int i = threadIdx.x; i < n; i += 64)
+        for (int i = tid(); i < n; i += 64)
           if (prob[i] > best) { best = prob[i]; bi = i; }
         for (int o = 32; o > 0; o >>= 1) {
           double ob = __shfl_xor(best, o, 64);
@@ -1265,12 +1709,12 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
       } else {
         pos = inverse_cdf(prob, n, ufetch(sh, t, 0));
       }
-      if (threadIdx.x == 0) sh->tok = sidx[pos];
+      if (tid() == 0) sh->tok = sidx[pos];
     }
     __syncthreads();
     const int nq = p->greedy ? 1 : n;
     const int tok = sh->tok;
-    for (int i = threadIdx.x; i < nq; i += kThreads) {
+    for (int i = tid(); i < nq; i += kThreads) {
       const int idx = p->greedy ? tok : sidx[i];
       const double pr = p->greedy ? 1.0 : prob[i];
       const uint64_t bits = (uint64_t)__double_as_longlong(pr);
@@ -1278,7 +1722,7 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
       xstore(rec + 1 + 3 * i + 1, otag, (uint32_t)bits);
       xstore(rec + 1 + 3 * i + 2, otag, (uint32_t)(bits >> 32));
     }
-    if (threadIdx.x == 0) xstore(rec, otag, (uint32_t)tok);
+    if (tid() == 0) xstore(rec, otag, (uint32_t)tok);
     return true;
   }
   // verify row at position t
@@ -1295,12 +1739,12 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
       else reinterpret_cast<uint32_t*>(qprob + e)[f - 1] = v;
     });
     if (!wg_sync_ok(c, ok)) return false;
-    if (threadIdx.x < 64) {
+    if (tid() < 64) {
       const int d = sh->drafts[t];
       double pd = 0.0, qd = 0.0;
-      for (int i = threadIdx.x; i < n; i += 64)
+      for (int i = tid(); i < n; i += 64)
         if (sidx[i] == d) pd = prob[i];
-      for (int i = threadIdx.x; i < nq; i += 64)
+      for (int i = tid(); i < nq; i += 64)
         if (qidx[i] == d) qd = qprob[i];
       pd = wave_sumd(pd);
       qd = wave_sumd(qd);
@@ -1309,7 +1753,7 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
       if (!accept) {
         // residual max(0, p - q) on p's support; q looked up by binary search (ascending tokens)
         double rs = 0.0;
-        for (int i = threadIdx.x; i < n; i += 64) {
+        for (int i = tid(); i < n; i += 64) {
           const int x = sidx[i];
           int lo = 0, hi2 = nq;
           while (lo < hi2) {
@@ -1324,19 +1768,19 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
         }
         rs = wave_sumd(rs);
         if (!(rs > 0.0))
-          for (int i = threadIdx.x; i < n; i += 64) res[i] = prob[i];
+          for (int i = tid(); i < n; i += 64) res[i] = prob[i];
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         const int pos = inverse_cdf(res, n, ufetch(sh, t, 2));
         tok = sidx[pos];
       }
-      if (threadIdx.x == 0) xstore(p->vres + (size_t)par * kMaxRows + row, otag, (uint32_t)tok | (accept ? 0x80000000u : 0u));
+      if (tid() == 0) xstore(p->vres + (size_t)par * kMaxRows + row, otag, (uint32_t)tok | (accept ? 0x80000000u : 0u));
     }
   } else {
     // the prefix token c_1, or the extra token after every draft was accepted
-    if (threadIdx.x < 64) {
+    if (tid() < 64) {
       const int pos = inverse_cdf(prob, n, ufetch(sh, t, 2));
-      if (threadIdx.x == 0) xstore(p->vres + (size_t)par * kMaxRows + row, otag, (uint32_t)sidx[pos]);
+      if (tid() == 0) xstore(p->vres + (size_t)par * kMaxRows + row, otag, (uint32_t)sidx[pos]);
     }
   }
   return true;
@@ -1354,7 +1798,7 @@ __device__ __forceinline__ bool commit_and_advance(const Ctx& c) {
   __shared__ int dtok[kMaxRows][kMaxCodes + 1];
   __shared__ short wlist[kMaxRows * (kMaxCodes + 1)];  // r * 16 + j, j = 0 for the verdict of row r
   __shared__ int nlist;
-  if (threadIdx.x == 0) {
+  if (tid() == 0) {
     int k = 0;
     for (int r = 0; r < R; ++r) {
       if (is_verify_row(sh, r)) wlist[k++] = (short)(r * 16);
@@ -1377,7 +1821,7 @@ __device__ __forceinline__ bool commit_and_advance(const Ctx& c) {
         else dtok[r][jj] = (int)v;
       });
   if (!wg_sync_ok(c, ok)) return false;
-  if (threadIdx.x == 0) {
+  if (tid() == 0) {
     const int m = sh->m, kp = sh->kp;
     int m_new = -1, acc = 0, tok = -1;
     if (sh->pass == 0) {
@@ -1459,7 +1903,7 @@ template <typename WT, int MR>
 __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
   constexpr int RPT = MR <= 8 ? 8 : 4;
   __shared__ Shared shs;
-  extern __shared__ float dyn[];
+  extern __shared__ __align__(16) float dyn[];
   const KParams* p = gp;
   Ctx c;
   c.p = p;
@@ -1469,15 +1913,14 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   c.xown = dyn;
   c.red = dyn + kMaxRows * c.cpw;
   c.work = c.red + kWaves * (RPT + 1) * MR;
-  c.kvlds = c.work + p->work_floats;
-  c.attn_const = c.kvlds + (p->kv_in_lds ? (size_t)p->L * kMaxPos * 2 * p->d : 0);
+  c.attn_const = c.work + p->work_floats;
   if ((int)blockIdx.x < p->nq) {
     const int d = p->d;
-    for (int i = threadIdx.x; i < p->L * 2 * d; i += kThreads) {
+    for (int i = tid(); i < p->L * 2 * d; i += kThreads) {
       const int l = i / (2 * d), j = i % (2 * d);
       c.attn_const[i] = G(fptr(p, layer_off(p, l, j < d ? p->o_qn : p->o_kn)))[j % d];
     }
-    for (int i = threadIdx.x; i < kMaxPos * d; i += kThreads) c.attn_const[p->L * 2 * d + i] = G(p->rope)[i];
+    for (int i = tid(); i < kMaxPos * d; i += kThreads) c.attn_const[p->L * 2 * d + i] = G(p->rope)[i];
   }
   c.tag_base = fa.epoch_base;
   c.pass0 = *G(p->pass_count);
@@ -1485,7 +1928,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   const int c0 = fa.c0[0];
   const bool poisoned = c.pass0 == 0xffffffffu;
   const bool c0_ok = c0 >= 0 && c0 < p->V && !poisoned;
-  if (threadIdx.x == 0) {
+  if (tid() == 0) {
     shs.fa = fa;
     shs.abort = c0_ok ? 0 : 1;
     shs.pass = 0;
@@ -1505,7 +1948,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   const int wbytes = (int)sizeof(WT);
   const int L = p->L;
   while (ok) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) shs.st_bytes += pass_bytes(c, wbytes);
+    if (blockIdx.x == 0 && tid() == 0) shs.st_bytes += pass_bytes(c, wbytes);
     const int nph = phases_per_pass(L) + 1;
     const bool clk_on = blockIdx.x == 0 && p->tr_clock && shs.pass < p->tr_max_rounds;
     uint64_t* clk_row = clk_on ? p->tr_clock + (size_t)shs.pass * nph : nullptr;
@@ -1513,24 +1956,41 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     uint64_t* wclk = wclk_on ? p->tr_wgclock + (size_t)shs.pass * nph * p->nwg + blockIdx.x : nullptr;
 #define RVQSD_STAMP(ph)                                                   \
   do {                                                                    \
-    if (threadIdx.x == 0) {                                               \
+    if (tid() == 0) {                                               \
       if (clk_on) clk_row[(ph)] = dclock();                               \
       if (wclk_on) wclk[(size_t)(ph) * p->nwg] = dclock();                \
     }                                                                     \
   } while (0)
     for (int l = 0; l < L && ok; ++l) {
-      ok = phase_qkv<WT, MR, 4>(c, l);
+      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<MR>(c, l);
+      else ok = phase_qkv<WT, MR, 4>(c, l);
       RVQSD_STAMP(5 * l + 0);
       if (ok) ok = phase_attn<MR>(c, l);
       RVQSD_STAMP(5 * l + 1);
-      if (ok) ok = phase_proj<WT, MR, 4>(c, l, false);
+      if constexpr (UseMfma<WT, MR>::value) {
+        if (ok) ok = phase_proj_m<MR, (MR + 1) / 2, kUptQ>(c, l, false);
+      } else {
+        if (ok) ok = phase_proj<WT, MR, 4>(c, l, false);
+      }
       RVQSD_STAMP(5 * l + 2);
-      if (ok) ok = phase_gu<WT, MR, (MR <= 8 ? 8 : 4)>(c, l);
+      if constexpr (UseMfma<WT, MR>::value) {
+        if (ok) ok = phase_gu_m<MR>(c, l);
+      } else {
+        if (ok) ok = phase_gu<WT, MR, (MR <= 8 ? 8 : 4)>(c, l);
+      }
       RVQSD_STAMP(5 * l + 3);
-      if (ok) ok = phase_proj<WT, MR, 4>(c, l, true);
+      if constexpr (UseMfma<WT, MR>::value) {
+        if (ok) ok = phase_proj_m<MR, (3 * MR + 3) / 4, kUptF>(c, l, true);
+      } else {
+        if (ok) ok = phase_proj<WT, MR, 4>(c, l, true);
+      }
       RVQSD_STAMP(5 * l + 4);
     }
-    if (ok) ok = phase_heads<WT, MR, (MR <= 5 ? 8 : 4)>(c);
+    if constexpr (UseMfma<WT, MR>::value) {
+      if (ok) ok = phase_heads_m<MR>(c);
+    } else {
+      if (ok) ok = phase_heads<WT, MR, (MR <= 5 ? 8 : 4)>(c);
+    }
     RVQSD_STAMP(ph_heads(L));
     if (ok) ok = phase_sample<MR>(c);
     RVQSD_STAMP(ph_sample(L));
@@ -1540,7 +2000,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     if (!ok || shs.m >= p->n_codes) break;
   }
 #undef RVQSD_STAMP
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (blockIdx.x == 0 && tid() == 0) {
     rvqsd_stats* st = fa.out_stats;
     st->target_calls = shs.st_calls;
     st->rounds = shs.st_rounds;

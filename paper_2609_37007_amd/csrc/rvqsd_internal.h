@@ -14,6 +14,9 @@ constexpr int kMaxRows = 16;           // rows of one pass (K+1 <= 15, prefix 2)
 constexpr int kSlotDraft0 = kMaxRows;  // logit slot of the first draft row
 constexpr int kMaxTopk = 256;
 constexpr int kTraceRoundInts = 32;    // ints per traced round
+// MFMA path (bf16 weights, <= 8 rows per pass): 512-wide k units per wave, i.e.
+// the largest hidden, q width and FFN it takes are 512 times these.
+constexpr int kUptH = 2, kUptQ = 4, kUptF = 6;
 
 // Phase ids inside a pass (tag = epoch_base + pass * phases_per_pass + phase + 1).
 constexpr int kPhQKV = 0, kPhAttn = 1, kPhO = 2, kPhGU = 3, kPhDown = 4;  // + 5 * layer
@@ -46,10 +49,9 @@ struct KParams {
   uint64_t* vres;  // [2][kMaxRows]      verify results (accept flag | token)
   uint64_t* drec;  // [2][n_slots][drec_words] draft records: token, then (idx, prob lo, prob hi) x support
   int32_t n_slots, drec_words;
-  float* kvc;      // [nq][L][kMaxPos][2][d] KV cache of each attention workgroup (when not in LDS)
+  float* kvc;      // [nq][L][kMaxPos][2][d] KV cache of each attention workgroup (k after norm and RoPE, v)
   const float* rope;  // [kMaxPos][d/2][2] cos, sin of position * rope_base^(-2i/d)
-  int32_t kv_in_lds;  // 1: the attention workgroups keep their KV cache in LDS
-  int32_t work_floats;  // floats of the LDS work area (the LDS KV cache follows it)
+  int32_t work_floats;  // floats of the LDS work area (the attention constants follow it)
   uint64_t* status; // device status word: (epoch_base << 32) | error code of that frame
   // trace (nullable)
   float* tr_logits;    // [tr_max_rounds][n_slots][V]
