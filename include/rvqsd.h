@@ -90,13 +90,16 @@ typedef struct {
  *          pass index, drafts d_{m+1..m+K'} at [8..8+K'), then reserved.
  *  clock:  uint64[max_rounds][5*n_layers+5]: device clock at each phase end of a pass
  *          (workgroup 0's view), last entry = pass end.
- *  wg_clock: uint64[max_rounds][5*n_layers+5][workgroups]: the same for every workgroup. */
+ *  wg_clock: uint64[max_rounds][5*n_layers+5][workgroups]: the same for every workgroup.
+ *  wg_ready: uint64[max_rounds][5*n_layers+5][workgroups]: device clock at which each
+ *          workgroup held every input of the phase (after its last wait), 0 if it had none. */
 typedef struct {
   float* logits;
   int32_t* rounds;
   uint64_t* clock;
   uint64_t* wg_clock;
   int32_t max_rounds;
+  uint64_t* wg_ready;
 } rvqsd_trace;
 
 typedef struct rvqsd_model rvqsd_model;

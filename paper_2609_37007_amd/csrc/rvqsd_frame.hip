@@ -60,6 +60,13 @@ __device__ __forceinline__ void xstoref(uint64_t* p, uint32_t tag, float v) { xs
 __device__ __forceinline__ void pstore(uint32_t* p, float v, uint32_t par) {
   __hip_atomic_store(G(p), (__float_as_uint(v) & ~1u) | par, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// q/k/v word: fp32 with the three lowest mantissa bits replaced by the write's layer epoch
+// mod 8 (bit 0 is the parity the per-layer readers check). The fused attention path reads
+// these words only every L-th layer, so a parity bit alone would also match the copy
+// written two layers earlier; the epoch matches only the current write.
+__device__ __forceinline__ void estore(uint32_t* p, float v, uint32_t ep) {
+  __hip_atomic_store(G(p), (__float_as_uint(v) & ~7u) | (ep & 7u), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ uint64_t pload2(const uint32_t* p) {
   return __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -110,6 +117,59 @@ __device__ __forceinline__ double wave_maxd(double v) {
   for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
   return v;
 }
+// Inclusive prefix sum over the 64 lanes with DPP: shifts 1, 2, 4, 8 inside each row
+// of 16 lanes, then the last lane of row 0 (2) is added to rows 1, 3 (2, 3).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dppi(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, false);
+}
+__device__ __forceinline__ int wave_scan_incl_dpp(int v) {
+  v += dppi<0x111, 0xF>(v);  // row_shr:1
+  v += dppi<0x112, 0xF>(v);  // row_shr:2
+  v += dppi<0x114, 0xF>(v);  // row_shr:4
+  v += dppi<0x118, 0xF>(v);  // row_shr:8
+  v += dppi<0x142, 0xA>(v);  // row_bcast:15
+  v += dppi<0x143, 0xC>(v);  // row_bcast:31
+  return v;
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dppd(double v) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROWS, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROWS, 0xF, false);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ double wave_scan_incl_dppd(double v) {
+  v += dppd<0x111, 0xF>(v);
+  v += dppd<0x112, 0xF>(v);
+  v += dppd<0x114, 0xF>(v);
+  v += dppd<0x118, 0xF>(v);
+  v += dppd<0x142, 0xA>(v);
+  v += dppd<0x143, 0xC>(v);
+  return v;
+}
+__device__ __forceinline__ double lane_vald(double v, int l) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// sum / max over the 64 lanes (every lane gets the result): rows of 16 with DPP, then the 4 row totals
+__device__ __forceinline__ double wave_sumd_dpp(double v) {
+  v += dppd<0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
+  v += dppd<0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
+  v += dppd<0x141, 0xF>(v);  // row_half_mirror
+  v += dppd<0x140, 0xF>(v);  // row_mirror
+  return (lane_vald(v, 15) + lane_vald(v, 31)) + (lane_vald(v, 47) + lane_vald(v, 63));
+}
+__device__ __forceinline__ double wave_maxd_dpp(double v) {
+  v = fmax(v, dppd<0xB1, 0xF>(v));
+  v = fmax(v, dppd<0x4E, 0xF>(v));
+  v = fmax(v, dppd<0x141, 0xF>(v));
+  v = fmax(v, dppd<0x140, 0xF>(v));
+  return fmax(fmax(lane_vald(v, 15), lane_vald(v, 31)), fmax(lane_vald(v, 47), lane_vald(v, 63)));
+}
+
 // inclusive prefix sum over the 64 lanes
 __device__ __forceinline__ int wave_scan_incl(int v) {
   const int lane = tid() & 63;
@@ -182,6 +242,12 @@ struct Shared {
   int iscan[kWaves];
   int sel_digit, sel_kk, n_sup, n_q;
   int tok, acc;
+  float uni[kMaxCodes * 3];  // this frame's uniforms (draft, accept, sample) per position 1..15
+  float wmx[kWaves], wmn[kWaves];
+  int wbad[kWaves];
+  int sel_b, c_above, c_b, n_cand;
+  int cand_idx[kTopkCand];
+  float cand_val[kTopkCand];
   // vectors of the LM head this workgroup multiplies (heads phase)
   int hv_n, hv_row[kMaxRows], hv_off[kMaxRows], hv_slot[kMaxRows];
 };
@@ -194,15 +260,23 @@ struct Ctx {
   float* red;       // [kWaves][RPT * MR] reduction scratch
   float* work;      // union area
   float* attn_const;  // [L][2][d] q/k norm gains, then [kMaxPos][d/2][2] rotary table (attention workgroups)
+  _Float16* kvk;    // fused path: [nkv][kMaxPos][128] keys (after norm and RoPE) of this workgroup's layer
+  _Float16* kvv;    // fused path: [nkv][128][kMaxPos] values, transposed
+  float* xres;      // fused path: [MR][kFusedRows] residual rows of this workgroup's O rows
   int cpw;          // residual columns per workgroup
   uint32_t tag_base;
   uint32_t pass0;   // passes this stream ran before this frame
+  uint64_t* rdy;    // trace: this workgroup's input-complete stamp of the current phase (nullable)
 };
 
 // parity of the per-layer buffers (q/k/v, attention output, activation):
 // one write per layer per pass, so it alternates with every write
 __device__ __forceinline__ uint32_t par_layer(const Ctx& c, int pass, int l) {
   return (uint32_t)(((uint64_t)(c.pass0 + pass) * (uint64_t)c.p->L + (uint64_t)l) & 1u);
+}
+// layer epoch mod 8 of the q/k/v buffer (its bit 0 is par_layer)
+__device__ __forceinline__ uint32_t epoch_layer(const Ctx& c, int pass, int l) {
+  return (uint32_t)(((uint64_t)(c.pass0 + pass) * (uint64_t)c.p->L + (uint64_t)l) & 7u);
 }
 constexpr uint32_t kParO = 0, kParDown = 1;  // residual stream: written after O, then after down
 
@@ -323,6 +397,7 @@ __device__ __forceinline__ bool poll_pairs(const Ctx& c, int n2, uint32_t par, A
 __device__ __forceinline__ bool wg_sync_ok(const Ctx& c, bool ok) {
   if (!ok) c.sh->abort = 1;
   __syncthreads();
+  if (c.rdy && tid() == 0) *G(c.rdy) = __builtin_amdgcn_s_memrealtime();
   return c.sh->abort == 0;
 }
 
@@ -516,9 +591,12 @@ __device__ __forceinline__ void put_split(uint32_t* xsp, int stride, int m, int 
 // each chunk's sum of squares of the raw x for the row's RMSNorm.
 // Chunk i of the pass is handled by thread i % kThreads; up to CB chunks per
 // thread are in flight at once.
+// Keep range (kdst nullable): the raw values of columns kc0 .. kc0 + kn - 1 also go to
+// kdst[m * kstride + column - kc0] (the residual values a later phase adds to).
 template <int CB, bool GAIN>
 __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, int K, int R, uint32_t par,
-                                            const float* gain, uint32_t* xsp, float* sqc) {
+                                            const float* gain, uint32_t* xsp, float* sqc,
+                                            float* kdst = nullptr, int kc0 = 0, int kn = 0, int kstride = 0) {
   const int nch = K >> 3, total = R * nch;
   for (int base = 0; base < total; base += CB * kThreads) {
     uint32_t pending = 0;  // bit 4b + w: word w of chunk b still missing
@@ -577,6 +655,15 @@ __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, i
           x[2 * w] = __uint_as_float((uint32_t)v[b][w]);
           x[2 * w + 1] = __uint_as_float((uint32_t)(v[b][w] >> 32));
         }
+        const int m = idx / nch;
+        if (kdst) {
+          const int q0 = (idx - m * nch) * 8;
+          if (q0 + 8 > kc0 && q0 < kc0 + kn) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (q0 + e >= kc0 && q0 + e < kc0 + kn) kdst[m * kstride + (q0 + e - kc0)] = x[e];
+          }
+        }
         if constexpr (GAIN) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -585,7 +672,6 @@ __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, i
           }
           sqc[idx] = s2;
         }
-        const int m = idx / nch;
         put_split(xsp, split_stride(K), m, idx - m * nch, x);
       }
     }
@@ -851,10 +937,10 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
     float xg[MR][Gemv<WT, MR, RPT>::EPC], sq[MR];
     chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, g.active, g.gain, xg, sq);
     g.run(c, xg, rowptr, out, sq);
-    const uint32_t par = par_layer(c, sh->pass, l);
+    const uint32_t ep = epoch_layer(c, sh->pass, l);
     for (int i = tid(); i < MR * nrows; i += kThreads) {
       const int m = i / nrows, r = i % nrows;
-      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
+      estore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, ep);
     }
   }
   // the next phase reuses the work area: no wave may still be reading it
@@ -1171,19 +1257,41 @@ __device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
 // Same partition of weight rows over workgroups as the phases above; the
 // weights of the first round are loaded before the wait for the activations.
 
-template <int MR>
+// rows of the fused O projection one member of layer l's set takes (see phase_attn_o_fused)
+constexpr int kFusedRows = 32;  // O rows one member takes at most
+__device__ __forceinline__ int fused_set_size(const KParams* p, int l) { return (p->nwg - l + p->L - 1) / p->L; }
+__device__ __forceinline__ void fused_rows(const KParams* p, int l, int* row0, int* nrows) {
+  const int S = fused_set_size(p, l), rpm = (p->H + S - 1) / S;
+  *row0 = ((int)blockIdx.x / p->L) * rpm;
+  *nrows = max(0, min(rpm, p->H - *row0));
+}
+
+// FUSED: a member of layer l's set also keeps the layer input of its O rows (the residual
+// the fused O projection adds) while it stages that input.
+template <int MR, bool FUSED = false>
 __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
   const int H = p->H, R = sh->rows, N = p->nqkv;
+  int f0 = 0, fn = 0;
+  if (FUSED && (int)blockIdx.x % p->L == l) fused_rows(p, l, &f0, &fn);
   const int rpw = (N + p->nwg - 1) / p->nwg, row0 = blockIdx.x * rpw;
   const int nrows = max(0, min(rpw, N - row0));
   const bf16_t* wq = wptr<bf16_t>(p, layer_off(p, l, p->o_wq));
   const bf16_t* wk = wptr<bf16_t>(p, layer_off(p, l, p->o_wk));
   const bf16_t* wv = wptr<bf16_t>(p, layer_off(p, l, p->o_wv));
   const int qd = p->qdim, kd = p->kvdim;
+  // FUSED: workgroup w < 8 (nq + nkv) takes rows 8j .. 8j + 7 and 64 + 8j .. 64 + 8j + 7 of q/k head
+  // w / 8 (j = w % 8), so every RoPE pair of its rows is its own; the v workgroups keep plain rows
+  const int nqk = (p->nq + p->nkv) * 8;
+  const bool qkrot = FUSED && (int)blockIdx.x < nqk;
+  const int qk_head = (int)blockIdx.x >> 3, qk_j = (int)blockIdx.x & 7;
+  auto outrow = [&](int r) -> int {
+    if (qkrot) return qk_head * 128 + (r < 8 ? 8 * qk_j + r : 64 + 8 * qk_j + (r - 8));
+    return row0 + r;
+  };
   auto rowptr = [&](int r) -> const bf16_t* {
-    const int o = row0 + r;
+    const int o = outrow(r);
     if (o < qd) return wq + (size_t)o * H;
     if (o < qd + kd) return wk + (size_t)(o - qd) * H;
     return wv + (size_t)(o - qd - kd) * H;
@@ -1205,19 +1313,58 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
       const int m = i / c.cpw, j = i % c.cpw;
       c.xown[i] = (m < MR && o0 + j < H) ? xs[m * H + o0 + j] : 0.f;
     }
+    for (int i = tid(); i < MR * fn; i += kThreads) {
+      const int m = i / fn, j = i - m * fn;
+      c.xres[m * kFusedRows + j] = xs[m * H + f0 + j];
+    }
     __syncthreads();
     split_rows(xs, xsp, H, R, gain, sqc);
   } else {
-    if (nrows == 0) return true;
-    if (!stage_split<2, true>(c, p->xb, H, R, kParDown, gain, xsp, sqc)) return false;
+    if (nrows == 0 && fn == 0) return true;
+    if (!stage_split<2, true>(c, p->xb, H, R, kParDown, gain, xsp, sqc, fn > 0 ? c.xres : nullptr, f0, fn,
+                              kFusedRows))
+      return false;
   }
   if (nrows > 0) {
     rstd_from_chunks(c, sqc, H, R);
     mt.run(rowptr, xsp, R, red, out, sh->rstd);
-    const uint32_t par = par_layer(c, sh->pass, l);
-    for (int i = tid(); i < MR * nrows; i += kThreads) {
-      const int m = i / nrows, r = i % nrows;
-      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
+    const uint32_t ep = epoch_layer(c, sh->pass, l);
+    if (qkrot) {
+      // q / k rows: publish RoPE(x * gain) at the row's position and the partial sum of squares of
+      // the raw x over these 16 dimensions; the consumer scales by 1 / sqrt(sum / d + eps)
+      // (the per-head RMSNorm is a per-vector scale, the rotation keeps it)
+      const int t = tid();
+      if (t < 64) {
+        const int m = t >> 3, jp = t & 7, i = 8 * qk_j + jp;
+        float a = 0.f, b = 0.f;
+        if (m < MR && m < R) {
+          a = out[jp * MR + m];
+          b = out[(8 + jp) * MR + m];
+        }
+        float ss = fmaf(a, a, b * b);
+        ss += dpp<0xB1>(ss);   // quad
+        ss += dpp<0x4E>(ss);
+        ss += dpp<0x141>(ss);  // half row of 8
+        if (m < MR) {
+          if (p->qk_norm) {
+            const float* gn = fptr(p, layer_off(p, l, qk_head < p->nq ? p->o_qn : p->o_kn));
+            a *= G(gn)[i];
+            b *= G(gn)[i + 64];
+          }
+          const int pos = min(sh->first_pos + m, kMaxPos - 1);
+          const float cs = G(p->rope)[(pos * 64 + i) * 2], sn = G(p->rope)[(pos * 64 + i) * 2 + 1];
+          const float ra = a * cs - b * sn, rb = b * cs + a * sn;
+          estore(p->qkvb + (size_t)m * N + qk_head * 128 + i, m < R ? ra : 0.f, ep);
+          estore(p->qkvb + (size_t)m * N + qk_head * 128 + i + 64, m < R ? rb : 0.f, ep);
+          if (jp == 0)
+            estore(p->qkss + ((size_t)m * (p->nq + p->nkv) + qk_head) * 8 + qk_j, m < R ? ss : 0.f, ep);
+        }
+      }
+    } else {
+      for (int i = tid(); i < MR * nrows; i += kThreads) {
+        const int m = i / nrows, r = i % nrows;
+        estore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, ep);
+      }
     }
   }
   lds_barrier();  // the work area is reused by the next phase
@@ -1261,7 +1408,8 @@ __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) 
 }
 
 // gate and up rows interleaved (2j = gate row f0 + j, 2j + 1 = up row); act = SiLU(gate) * up.
-template <int MR>
+// KEEP: also keep this workgroup's raw residual columns (the fused path's down projection adds them).
+template <int MR, bool KEEP = false>
 __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -1280,7 +1428,10 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
   float* red = sqc + MR * (H >> 3);                     // [kWaves][2][256]
   float* out = red + kWaves * 2 * 256;                  // [2 nf][MR]
   const float* gain = fptr(p, layer_off(p, l, p->o_mlp_norm));
-  if (!stage_split<2, true>(c, p->xb, H, R, kParO, gain, xsp, sqc)) return false;
+  // KEEP: this workgroup's residual columns (the down projection's rows) go to xown
+  if (!stage_split<2, true>(c, p->xb, H, R, kParO, gain, xsp, sqc, KEEP ? c.xown : nullptr,
+                            c.cpw * (int)blockIdx.x, c.cpw, c.cpw))
+    return false;
   rstd_from_chunks(c, sqc, H, R);
   mt.run(rowptr, xsp, R, red, out, sh->rstd);
   const uint32_t par = par_layer(c, sh->pass, l);
@@ -1292,6 +1443,286 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
       a = gt / (1.f + expf(-gt)) * up;
     }
     pstore(p->actb + (size_t)m * F + f0 + j, a, par);
+  }
+  lds_barrier();  // the work area is reused by the next phase
+  return true;
+}
+
+// ----------------------------------- fused attention + O projection (bf16, <= 5 rows)
+// For the 16 q / 8 kv head, head_dim 128 shape, layer l's attention and O
+// projection run on the workgroups w with w % L == l (the set of layer l). Every
+// member keeps layer l's whole KV cache in LDS for the frame (fp16 keys after
+// norm and RoPE, fp16 values stored transposed) and computes the attention of all
+// heads itself, so the q/k/v exchange feeds the O projection directly and the
+// attention output never leaves the workgroup. Member k takes O rows
+// [k * rpm, (k + 1) * rpm), rpm = ceil(H / set size).
+//
+// Wave g handles kv head g and its q heads 2g, 2g + 1: lane i holds dimensions i
+// and i + 64 of each vector, so the rotate-half RoPE pairs stay in one lane. The
+// scores S^T = K Q^T run on v_mfma_f32_16x16x32_f16 (A = 16 cached positions, B =
+// the wave's <= 10 query vectors as an fp16 hi + lo pair); their result layout is
+// exactly the B operand of v_mfma_f32_16x16x16_f16, so O^T = V^T P^T follows with P
+// as an fp16 hi + lo pair and no transpose. Wave g then owns the O projection's k
+// units of its own heads (columns 256g .. 256g + 255), reading its attention output
+// back from LDS it wrote itself, so the only workgroup barrier after the wait is the
+// one before the cross-wave sum of the O tiles.
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+
+template <int MR>
+__device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
+  constexpr int D = 128, HALF = 64;
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int L = p->L;
+  if ((int)blockIdx.x % L != l) return true;
+  const int H = p->H, R = sh->rows, N = p->nqkv, fp = sh->first_pos;
+  int row0, nrows;
+  fused_rows(p, l, &row0, &nrows);
+  if (nrows == 0) return true;
+  const int qdim = p->qdim, kvdim = p->kvdim;
+  const int lane = tid() & 63, wave = tid() >> 6, g = wave;
+  const int vec = lane & 15, q4 = lane >> 4;
+  const uint32_t ep = epoch_layer(c, sh->pass, l);
+
+  // the residual rows (xres) were kept by this workgroup's QKV phase of the same layer
+  bool ok = true;
+
+  // ---- wave g: q of heads 2g, 2g + 1, k and v of kv head g, rows 0 .. R-1 (slot s = type * MR + r)
+  float va[4 * MR], vb[4 * MR];
+#pragma unroll
+  for (int s2 = 0; s2 < 4 * MR; ++s2) va[s2] = vb[s2] = 0.f;
+  // partial sums of squares: vector v = type * MR + r (type 0, 1: q heads 2g, 2g + 1; 2: k head g),
+  // parts 2 (lane % 4) and 2 (lane % 4) + 1 in lane 4 v + lane % 4 (v < 3 MR)
+  const int sv = lane >> 2, stype = sv / MR, sr = sv - stype * MR;
+  const bool slive = sv < 3 * MR && sr < R;
+  const int shead = stype < 2 ? 2 * g + stype : p->nq + g;
+  const uint32_t* ssrc = p->qkss + ((size_t)sr * (p->nq + p->nkv) + shead) * 8 + 2 * (lane & 3);
+  float ps0 = 0.f, ps1 = 0.f;
+  {
+    uint64_t pend = 0;
+#pragma unroll
+    for (int s2 = 0; s2 < 4 * MR; ++s2)
+      if (s2 % MR < R) pend |= 3ull << (2 * s2);
+    if (slive) pend |= 3ull << 62;
+    uint64_t t0 = 0;
+    int spins = 0;
+    while (ok && pend) {
+      // loads straight into the value registers; a word counts once its parity is this epoch's
+#pragma unroll
+      for (int s2 = 0; s2 < 4 * MR; ++s2) {
+        const int type = s2 / MR, r = s2 % MR;
+        const int col = type < 2 ? (2 * g + type) * D : qdim + (type - 2) * kvdim + g * D;
+        const uint32_t* src = p->qkvb + (size_t)r * N + col + lane;
+        if (pend & (1ull << (2 * s2)))
+          va[s2] = __uint_as_float(__hip_atomic_load(G(src), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        if (pend & (1ull << (2 * s2 + 1)))
+          vb[s2] = __uint_as_float(__hip_atomic_load(G(src + HALF), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      }
+      if (pend & (1ull << 62)) ps0 = __uint_as_float(__hip_atomic_load(G(ssrc), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      if (pend & (1ull << 63)) ps1 = __uint_as_float(__hip_atomic_load(G(ssrc + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+#pragma unroll
+      for (int s2 = 0; s2 < 4 * MR; ++s2) {
+        if ((__float_as_uint(va[s2]) & 7u) == ep) pend &= ~(1ull << (2 * s2));
+        if ((__float_as_uint(vb[s2]) & 7u) == ep) pend &= ~(1ull << (2 * s2 + 1));
+      }
+      if ((__float_as_uint(ps0) & 7u) == ep) pend &= ~(1ull << 62);
+      if ((__float_as_uint(ps1) & 7u) == ep) pend &= ~(1ull << 63);
+      // every lane of the wave must agree before leaving
+      if (!__any(pend != 0)) break;
+      if ((++spins & 31) == 0) {
+        const uint64_t now = dclock();
+        if (t0 == 0) t0 = now;
+        else if (now - t0 > kTimeoutTicks) { status_raise(p, c.tag_base, RVQSD_ETIMEOUT); ok = false; break; }
+        if (status_set(p, c.tag_base)) { ok = false; break; }
+      }
+    }
+  }
+  _Float16* Kg = c.kvk + (size_t)g * kMaxPos * D;  // [pos][D]
+  _Float16* Vg = c.kvv + (size_t)g * D * kMaxPos;  // [dim][pos]
+  _Float16* xs16 = reinterpret_cast<_Float16*>(c.work);  // the split area, addressed in halves
+  uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);   // [MR][qdim + 4] split attention output
+  const int xst = qdim + 4;
+  f32x4 oacc[2];
+  oacc[0] = oacc[1] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  if (ok) {
+    // per-head RMSNorm (q, k) and RoPE, then keys and values into the cache, queries (fp16 hi/lo,
+    // the split chunk layout) into this wave's own columns of the split area
+    // RMSNorm scale of each q / k vector from its 8 partial sums (one quad of lanes per vector)
+    float tq = (slive ? ps0 : 0.f) + (slive ? ps1 : 0.f);
+    tq += dpp<0xB1>(tq);
+    tq += dpp<0x4E>(tq);
+    const float rsl = p->qk_norm ? rsqrtf(tq / (float)D + p->rms_eps) : 1.f;
+    float rs[3 * MR];
+#pragma unroll
+    for (int s2 = 0; s2 < 3 * MR; ++s2) rs[s2] = lane_val(rsl, 4 * s2);
+#pragma unroll
+    for (int s2 = 0; s2 < 3 * MR; ++s2) {
+      const int type = s2 / MR, r = s2 % MR;
+      {
+        // published already gained and rotated: only the vector's scale remains
+        const float ra = va[s2] * rs[s2], rb = vb[s2] * rs[s2];
+        if (type == 2) {
+          const int pos = fp + r;
+          if (r < R) {
+            Kg[pos * D + lane] = (_Float16)ra;
+            Kg[pos * D + lane + HALF] = (_Float16)rb;
+          }
+        } else {
+          const int col = (2 * g + type) * D;  // column of dimension 0 of this head
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int k = col + lane + h * HALF;
+            const float x = h ? rb : ra;
+            const _Float16 hi = (_Float16)x;
+            const _Float16 lo = (_Float16)(x - (float)hi);
+            const int wbase = r * xst + (k >> 3) * 8, e = k & 7;
+            xs16[(wbase + (e >> 1)) * 2 + (e & 1)] = hi;
+            xs16[(wbase + 4 + (e >> 1)) * 2 + (e & 1)] = lo;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < MR; ++r) {
+      if (r < R) {
+        const int pos = fp + r;
+        Vg[lane * kMaxPos + pos] = (_Float16)va[3 * MR + r];
+        Vg[(lane + HALF) * kMaxPos + pos] = (_Float16)vb[3 * MR + r];
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // scores S^T[pos][vector], vector = gi * R + r (query head 2g + gi, row r)
+    const int NV = 2 * R;
+    const bool vlive = vec < NV;
+    const int gi = vlive ? vec / R : 0, vr = vlive ? vec - gi * R : 0;
+    const int hq = 2 * g + gi;
+    f32x4 sacc = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int cc = 0; cc < D / 32; ++cc) {
+      const f16x8 a = *reinterpret_cast<const f16x8*>(Kg + vec * D + 32 * cc + 8 * q4);
+      f16x8 bh = (f16x8)((_Float16)0.f), bl = (f16x8)((_Float16)0.f);
+      if (vlive) {
+        const int wb = vr * xst + (hq * 16 + 4 * cc + q4) * 8;
+        bh = *reinterpret_cast<const f16x8*>(xsp + wb);
+        bl = *reinterpret_cast<const f16x8*>(xsp + wb + 4);
+      }
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bh, sacc, 0, 0, 0);
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bl, sacc, 0, 0, 0);
+    }
+    // causal softmax over positions 0 .. fp + r of each vector (column vec; positions 4 q4 + v)
+    const float scale = 1.f / sqrtf((float)D);
+    const int last = fp + vr;
+    float sc[4], mx = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      sc[v] = (vlive && 4 * q4 + v <= last) ? sacc[v] * scale : -INFINITY;
+      mx = fmaxf(mx, sc[v]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float e4[4], z = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      e4[v] = sc[v] > -INFINITY ? expf(sc[v] - mx) : 0.f;
+      z += e4[v];
+    }
+    z += __shfl_xor(z, 16, 64);
+    z += __shfl_xor(z, 32, 64);
+    f16x4 ph, pl;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float pr = vlive ? e4[v] / z : 0.f;
+      ph[v] = (_Float16)pr;
+      pl[v] = (_Float16)(pr - (float)ph[v]);
+    }
+    // O^T[dim][vector] = V^T P^T in 16-dimension tiles; written back split (bf16 hi/lo)
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t) {
+      const f16x4 a = *reinterpret_cast<const f16x4*>(Vg + (16 * t + vec) * kMaxPos + 4 * q4);
+      f32x4 o = __builtin_amdgcn_mfma_f32_16x16x16f16(a, ph, (f32x4){0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_16x16x16f16(a, pl, o, 0, 0, 0);
+      if (vlive) {
+        const int k0 = hq * D + 16 * t + 4 * q4;  // four consecutive columns
+        uint32_t hw[2], lw[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const uint32_t h0 = bf16_bits_rne(o[2 * j]), h1 = bf16_bits_rne(o[2 * j + 1]);
+          const uint32_t l0 = bf16_bits_rne(o[2 * j] - __uint_as_float(h0 << 16));
+          const uint32_t l1 = bf16_bits_rne(o[2 * j + 1] - __uint_as_float(h1 << 16));
+          hw[j] = h0 | (h1 << 16);
+          lw[j] = l0 | (l1 << 16);
+        }
+        const int wb = vr * xst + (k0 >> 3) * 8 + ((k0 >> 2) & 1) * 2;
+        *reinterpret_cast<uint2*>(xsp + wb) = make_uint2(hw[0], hw[1]);
+        *reinterpret_cast<uint2*>(xsp + wb + 4) = make_uint2(lw[0], lw[1]);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // O projection partials over this wave's units 4g .. 4g + 3 (activation rows = columns of B):
+    // this member's weight rows (two 16-row tiles)
+    const bf16_t* W = wptr<bf16_t>(p, layer_off(p, l, p->o_wo));
+    W16 wa[2][4][2];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const int row = (tt << 4) + vec;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        W16 v0 = (W16)(0u), v1 = (W16)(0u);
+        if (row < nrows) {
+          const bf16_t* w = W + (size_t)(row0 + row) * qdim + (4 * g + j) * 64 + 16 * q4;
+          v0 = *G(reinterpret_cast<const W16*>(w));
+          v1 = *G(reinterpret_cast<const W16*>(w + 8));
+        }
+        wa[tt][j][0] = v0;
+        wa[tt][j][1] = v1;
+      }
+    }
+    const bool live = vec < R;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      W16 bv[4];
+      if (live) {
+        const uint32_t* bp = xsp + (size_t)vec * xst + (4 * g + j) * 64 + 16 * q4;
+        bv[0] = *reinterpret_cast<const W16*>(bp);
+        bv[1] = *reinterpret_cast<const W16*>(bp + 4);
+        bv[2] = *reinterpret_cast<const W16*>(bp + 8);
+        bv[3] = *reinterpret_cast<const W16*>(bp + 12);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bv[q] = (W16)(0u);
+      }
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const bf16x8 a0 = __builtin_bit_cast(bf16x8, wa[tt][j][0]), a1 = __builtin_bit_cast(bf16x8, wa[tt][j][1]);
+        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, bv[0]), oacc[tt], 0, 0, 0);
+        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, bv[1]), oacc[tt], 0, 0, 0);
+        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, bv[2]), oacc[tt], 0, 0, 0);
+        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, bv[3]), oacc[tt], 0, 0, 0);
+      }
+    }
+  }
+  // wave partial tiles to LDS (after the split area), then the cross-wave sum
+  float* red = c.work + MR * xst;  // [kWaves][2][256]
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    float* dst = red + ((size_t)(wave * 2 + tt) << 8);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) dst[((4 * q4 + v) << 4) + vec] = oacc[tt][v];
+  }
+  if (!wg_sync_ok(c, ok)) return false;
+  for (int o = tid(); o < nrows * MR; o += kThreads) {
+    const int r = o / MR, m = o - r * MR, tt = r >> 4, i = r & 15;
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) sum += red[((w * 2 + tt) << 8) + (i << 4) + m];
+    const float v = m < R ? c.xres[m * kFusedRows + r] + sum : 0.f;
+    pstore(p->xb + (size_t)m * H + row0 + r, v, kParO);
   }
   lds_barrier();  // the work area is reused by the next phase
   return true;
@@ -1491,15 +1922,15 @@ __device__ __forceinline__ uint32_t fkey(float f) {
 // exclusive prefix over the workgroup in thread order; returns total via *total
 __device__ __forceinline__ int block_excl_scan(Shared* sh, int v, int* total) {
   const int lane = tid() & 63, wave = tid() >> 6;
-  int inc = wave_scan_incl(v);
+  int inc = wave_scan_incl_dpp(v);
   if (lane == 63) sh->iscan[wave] = inc;
-  __syncthreads();
+  lds_barrier();
   int off = 0, tot = 0;
   for (int w = 0; w < kWaves; ++w) {
     if (w < wave) off += sh->iscan[w];
     tot += sh->iscan[w];
   }
-  __syncthreads();
+  lds_barrier();
   *total = tot;
   return off + inc - v;
 }
@@ -1585,20 +2016,153 @@ __device__ __forceinline__ int topk_select(const Ctx& c, const float* lg, int V,
   return tot;
 }
 
+__device__ __forceinline__ float row16_min(float v) {
+  v = fminf(v, dpp<0xB1>(v));
+  v = fminf(v, dpp<0x4E>(v));
+  v = fminf(v, dpp<0x141>(v));
+  v = fminf(v, dpp<0x140>(v));
+  return v;
+}
+
+// Top-k of lg[V] (ties -> lower index) through value buckets, support in ascending
+// token order: sidx[n], slog[n]. The values are binned by b(v) = floor((max - v) *
+// B / (max - min)), which never increases with v, so every value in a bucket
+// below the one holding the k-th largest is strictly larger than every value in
+// or above it; only that boundary bucket is ranked element by element (value,
+// then index; +0 and -0 tie as in a plain comparison). Returns -1 (and leaves the
+// outputs alone) when the row needs the general path: a value that is not
+// finite, all values equal, or more than kTopkCand values in the boundary bucket.
+__device__ int topk_buckets(const Ctx& c, const float* lg, int V, int topk, int* sidx, float* slog,
+                            unsigned* hist) {
+  Shared* sh = c.sh;
+  const int ept = (V + kThreads - 1) / kThreads;
+  const int i0 = tid() * ept;
+  const int kk0 = min(topk, V);
+  const int lane = tid() & 63, wave = tid() >> 6;
+  for (int i = tid(); i < kTopkBuckets; i += kThreads) hist[i] = 0u;
+  float mx = -INFINITY, mn = INFINITY;
+  bool bad = false;
+  for (int e = 0; e < ept; ++e) {
+    const int i = i0 + e;
+    if (i < V) {
+      const float v = lg[i];
+      bad |= !(fabsf(v) <= 3.402823466e38f);
+      mx = fmaxf(mx, v);
+      mn = fminf(mn, v);
+    }
+  }
+  mx = row16_max(mx);
+  mn = row16_min(mn);
+  mx = fmaxf(fmaxf(lane_val(mx, 15), lane_val(mx, 31)), fmaxf(lane_val(mx, 47), lane_val(mx, 63)));
+  mn = fminf(fminf(lane_val(mn, 15), lane_val(mn, 31)), fminf(lane_val(mn, 47), lane_val(mn, 63)));
+  const bool wbad = __any(bad);
+  if (lane == 0) {
+    sh->wmx[wave] = mx;
+    sh->wmn[wave] = mn;
+    sh->wbad[wave] = wbad ? 1 : 0;
+  }
+  lds_barrier();
+  int anybad = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    mx = fmaxf(mx, sh->wmx[w]);
+    mn = fminf(mn, sh->wmn[w]);
+    anybad |= sh->wbad[w];
+  }
+  if (anybad || !(mx > mn)) return -1;
+  const float scale = (float)kTopkBuckets / (mx - mn);
+  auto bucket = [&](float v) -> int {
+    const int b = (int)((mx - v) * scale);
+    return b < kTopkBuckets - 1 ? b : kTopkBuckets - 1;
+  };
+  for (int e = 0; e < ept; ++e) {
+    const int i = i0 + e;
+    if (i < V) atomicAdd(&hist[bucket(lg[i])], 1u);
+  }
+  lds_barrier();
+  if (wave == 0) {
+    constexpr int BPL = kTopkBuckets / 64;  // buckets per lane
+    int loc = 0;
+#pragma unroll
+    for (int q = 0; q < BPL; ++q) loc += (int)hist[BPL * lane + q];
+    const int incl = wave_scan_incl_dpp(loc);
+    const unsigned long long hit = __ballot(incl >= kk0);
+    const int L = __ffsll((long long)hit) - 1;  // the total is V >= kk0, so some lane hits
+    if (lane == L) {
+      int cum = incl - loc;
+      for (int q = 0; q < BPL; ++q) {
+        const int h = (int)hist[BPL * lane + q];
+        if (cum + h >= kk0) {
+          sh->sel_b = BPL * lane + q;
+          sh->c_above = cum;
+          sh->c_b = h;
+          break;
+        }
+        cum += h;
+      }
+      sh->n_cand = 0;
+    }
+  }
+  lds_barrier();
+  const int B = sh->sel_b, c_above = sh->c_above, c_b = sh->c_b;
+  if (c_b > kTopkCand) return -1;
+  for (int e = 0; e < ept; ++e) {
+    const int i = i0 + e;
+    if (i < V && bucket(lg[i]) == B) {
+      const int k = atomicAdd(&sh->n_cand, 1);
+      sh->cand_idx[k] = i;
+      sh->cand_val[k] = lg[i];
+    }
+  }
+  lds_barrier();
+  const int need = kk0 - c_above;
+  int n_sel = 0;
+  unsigned selmask = 0;
+  for (int e = 0; e < ept; ++e) {
+    const int i = i0 + e;
+    if (i >= V) break;
+    const float v = lg[i];
+    const int b = bucket(v);
+    bool sel = b < B;
+    if (b == B) {
+      int rank = 0;
+      for (int j = 0; j < c_b; ++j) {
+        const float vj = sh->cand_val[j];
+        rank += (vj > v || (vj == v && sh->cand_idx[j] < i)) ? 1 : 0;
+      }
+      sel = rank < need;
+    }
+    if (sel) {
+      selmask |= 1u << e;
+      ++n_sel;
+    }
+  }
+  int tot;
+  int pos = block_excl_scan(sh, n_sel, &tot);
+  for (int e = 0; e < ept; ++e) {
+    if (selmask & (1u << e)) {
+      sidx[pos] = i0 + e;
+      slog[pos] = lg[i0 + e];
+      ++pos;
+    }
+  }
+  lds_barrier();
+  return tot;
+}
+
 // wave 0: probabilities of the top-k support, p = exp((l - max)/T) / Z in fp64
 __device__ __forceinline__ void softmax_support(const float* slog, int n, double T, double* prob) {
   if (tid() >= 64) return;
   const int lane = tid();
   double mx = -INFINITY;
   for (int i = lane; i < n; i += 64) mx = fmax(mx, (double)slog[i]);
-  mx = wave_maxd(mx);
+  mx = wave_maxd_dpp(mx);
   double z = 0.0;
   for (int i = lane; i < n; i += 64) {
     double w = exp(((double)slog[i] - mx) / T);
     prob[i] = w;
     z += w;
   }
-  z = wave_sumd(z);
+  z = wave_sumd_dpp(z);
   for (int i = lane; i < n; i += 64) prob[i] = prob[i] / z;
 }
 
@@ -1610,8 +2174,8 @@ __device__ __forceinline__ int inverse_cdf(const double* w, int n, double u) {
   double loc = 0.0;
   for (int q = 0; q < per; ++q)
     if (b + q < n) loc += w[b + q];
-  double incl = wave_scan_incld(loc);
-  double z = __shfl(incl, 63, 64);
+  double incl = wave_scan_incl_dppd(loc);
+  double z = lane_vald(incl, 63);
   double thr = u * z;
   double cum = incl - loc;
   int found = -1;
@@ -1634,7 +2198,7 @@ __device__ __forceinline__ int inverse_cdf(const double* w, int n, double u) {
 }
 
 __device__ __forceinline__ double ufetch(const Shared* sh, int s, int slot) {
-  return (double)G(sh->fa.uniforms)[(s - 1) * 3 + slot];
+  return (double)sh->uni[(s - 1) * 3 + slot];
 }
 
 // Role of this workgroup's slot in the sampling phase: row >= 0 if active;
@@ -1676,12 +2240,31 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
   double* res = qprob + kMaxTopk;                              // [kMaxTopk]
   int* qidx = reinterpret_cast<int*>(res + kMaxTopk);          // [kMaxTopk]
   const uint64_t* src = p->logb + ((size_t)par * p->n_slots + slot) * V;
-  bool ok = poll_range(c, src, V, tag, [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); });
+  // a verify row with a draft: q of that draft was published by the previous pass, so it
+  // is fetched first, while this pass's logits are still on their way
+  const int t_pos = sh->first_pos + row + j;
+  const int jv_pos = t_pos - sh->m;
+  const bool has_draft = j == 0 && sh->pass > 0 && jv_pos <= sh->kp;
+  const int nq = p->greedy ? 1 : support_size(p);
+  bool ok = true;
+  if (has_draft) {
+    const int prev_slot = draft_slot(p, sh->prev_anchor_row, jv_pos);
+    const uint64_t* rec = p->drec + ((size_t)(par ^ 1) * p->n_slots + prev_slot) * p->drec_words;
+    const uint32_t ptag = tag_of(c, sh->pass - 1, ph_sample(p->L));
+    ok = poll_range(c, rec + 1, 3 * nq, ptag, [&](int i, uint32_t v) {
+      const int e = i / 3, f = i % 3;
+      if (f == 0) qidx[e] = (int)v;
+      else reinterpret_cast<uint32_t*>(qprob + e)[f - 1] = v;
+    });
+  }
+  if (ok) ok = poll_range(c, src, V, tag, [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); });
   if (!wg_sync_ok(c, ok)) return false;
   if (p->tr_logits && sh->pass < p->tr_max_rounds)
     for (int i = tid(); i < V; i += kThreads)
       G(p->tr_logits)[((size_t)sh->pass * p->n_slots + slot) * V + i] = lg[i];
-  const int n = topk_select(c, lg, V, p->topk, sidx, slog);
+  unsigned* hist = reinterpret_cast<unsigned*>(qidx + kMaxTopk);  // [kTopkBuckets]
+  int n = topk_buckets(c, lg, V, p->topk, sidx, slog, hist);
+  if (n < 0) n = topk_select(c, lg, V, p->topk, sidx, slog);
   if (tid() < 64) {
     bool fin = false;
     for (int i = tid(); i < n; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
@@ -1726,19 +2309,8 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
     return true;
   }
   // verify row at position t
-  const int jv = t - sh->m;  // 1-based draft index in this round
-  if (sh->pass > 0 && jv <= sh->kp) {
+  if (has_draft) {
     // accept test of d_t against q_t, drafted last pass from the anchor's row
-    const int prev_slot = draft_slot(p, sh->prev_anchor_row, jv);
-    const uint64_t* rec = p->drec + ((size_t)(par ^ 1) * p->n_slots + prev_slot) * p->drec_words;
-    const uint32_t ptag = tag_of(c, sh->pass - 1, ph_sample(p->L));
-    const int nq = p->greedy ? 1 : support_size(p);
-    ok = poll_range(c, rec + 1, 3 * nq, ptag, [&](int i, uint32_t v) {
-      const int e = i / 3, f = i % 3;
-      if (f == 0) qidx[e] = (int)v;
-      else reinterpret_cast<uint32_t*>(qprob + e)[f - 1] = v;
-    });
-    if (!wg_sync_ok(c, ok)) return false;
     if (tid() < 64) {
       const int d = sh->drafts[t];
       double pd = 0.0, qd = 0.0;
@@ -1746,8 +2318,8 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
         if (sidx[i] == d) pd = prob[i];
       for (int i = tid(); i < nq; i += 64)
         if (qidx[i] == d) qd = qprob[i];
-      pd = wave_sumd(pd);
-      qd = wave_sumd(qd);
+      pd = wave_sumd_dpp(pd);
+      qd = wave_sumd_dpp(qd);
       const bool accept = ufetch(sh, t, 1) * qd < pd;
       int tok = d;
       if (!accept) {
@@ -1766,7 +2338,7 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
           res[i] = v > 0.0 ? v : 0.0;
           rs += res[i];
         }
-        rs = wave_sumd(rs);
+        rs = wave_sumd_dpp(rs);
         if (!(rs > 0.0))
           for (int i = tid(); i < n; i += 64) res[i] = prob[i];
         __builtin_amdgcn_wave_barrier();
@@ -1899,7 +2471,7 @@ __device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c, int wbyte
   return b;
 }
 
-template <typename WT, int MR>
+template <typename WT, int MR, bool FUSED>
 __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
   constexpr int RPT = MR <= 8 ? 8 : 4;
   __shared__ Shared shs;
@@ -1914,7 +2486,15 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   c.red = dyn + kMaxRows * c.cpw;
   c.work = c.red + kWaves * (RPT + 1) * MR;
   c.attn_const = c.work + p->work_floats;
-  if ((int)blockIdx.x < p->nq) {
+  c.kvk = reinterpret_cast<_Float16*>(c.work + p->work_floats);
+  c.kvv = c.kvk + (size_t)p->nkv * kMaxPos * 128;
+  c.xres = reinterpret_cast<float*>(c.kvv + (size_t)p->nkv * 128 * kMaxPos);
+  if constexpr (FUSED) {
+    // the frame's KV cache starts zeroed: masked positions then hold finite values
+    uint4* z = reinterpret_cast<uint4*>(c.kvk);
+    const int n16 = p->nkv * kMaxPos * 128 * 2 * 2 / 16;
+    for (int i = tid(); i < n16; i += kThreads) z[i] = make_uint4(0u, 0u, 0u, 0u);
+  } else if ((int)blockIdx.x < p->nq) {
     const int d = p->d;
     for (int i = tid(); i < p->L * 2 * d; i += kThreads) {
       const int l = i / (2 * d), j = i % (2 * d);
@@ -1922,8 +2502,10 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     }
     for (int i = tid(); i < kMaxPos * d; i += kThreads) c.attn_const[p->L * 2 * d + i] = G(p->rope)[i];
   }
+  if (tid() < 3 * p->n_codes) shs.uni[tid()] = G(fa.uniforms)[tid()];
   c.tag_base = fa.epoch_base;
   c.pass0 = *G(p->pass_count);
+  c.rdy = nullptr;
   const uint64_t t_start = dclock();
   const int c0 = fa.c0[0];
   const bool poisoned = c.pass0 == 0xffffffffu;
@@ -1954,6 +2536,10 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     uint64_t* clk_row = clk_on ? p->tr_clock + (size_t)shs.pass * nph : nullptr;
     const bool wclk_on = p->tr_wgclock && shs.pass < p->tr_max_rounds;
     uint64_t* wclk = wclk_on ? p->tr_wgclock + (size_t)shs.pass * nph * p->nwg + blockIdx.x : nullptr;
+    uint64_t* wrdy = (p->tr_wgready && shs.pass < p->tr_max_rounds)
+                         ? p->tr_wgready + (size_t)shs.pass * nph * p->nwg + blockIdx.x
+                         : nullptr;
+#define RVQSD_READY(ph) c.rdy = wrdy ? wrdy + (size_t)(ph) * p->nwg : nullptr
 #define RVQSD_STAMP(ph)                                                   \
   do {                                                                    \
     if (tid() == 0) {                                               \
@@ -1961,24 +2547,44 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
       if (wclk_on) wclk[(size_t)(ph) * p->nwg] = dclock();                \
     }                                                                     \
   } while (0)
-    for (int l = 0; l < L && ok; ++l) {
+    for (int l = 0; l < L && ok && FUSED; ++l) {
+      RVQSD_READY(5 * l + 0);
+      ok = phase_qkv_m<MR, true>(c, l);
+      RVQSD_STAMP(5 * l + 0);
+      RVQSD_READY(5 * l + 1);
+      if (ok) ok = phase_attn_o_fused<MR>(c, l);
+      RVQSD_STAMP(5 * l + 1);
+      RVQSD_STAMP(5 * l + 2);
+      RVQSD_READY(5 * l + 3);
+      if (ok) ok = phase_gu_m<MR, true>(c, l);
+      RVQSD_STAMP(5 * l + 3);
+      RVQSD_READY(5 * l + 4);
+      if (ok) ok = phase_proj_m<MR, (3 * MR + 3) / 4, kUptF>(c, l, true);
+      RVQSD_STAMP(5 * l + 4);
+    }
+    for (int l = 0; l < L && ok && !FUSED; ++l) {
+      RVQSD_READY(5 * l + 0);
       if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<MR>(c, l);
       else ok = phase_qkv<WT, MR, 4>(c, l);
       RVQSD_STAMP(5 * l + 0);
+      RVQSD_READY(5 * l + 1);
       if (ok) ok = phase_attn<MR>(c, l);
       RVQSD_STAMP(5 * l + 1);
+      RVQSD_READY(5 * l + 2);
       if constexpr (UseMfma<WT, MR>::value) {
         if (ok) ok = phase_proj_m<MR, (MR + 1) / 2, kUptQ>(c, l, false);
       } else {
         if (ok) ok = phase_proj<WT, MR, 4>(c, l, false);
       }
       RVQSD_STAMP(5 * l + 2);
+      RVQSD_READY(5 * l + 3);
       if constexpr (UseMfma<WT, MR>::value) {
         if (ok) ok = phase_gu_m<MR>(c, l);
       } else {
         if (ok) ok = phase_gu<WT, MR, (MR <= 8 ? 8 : 4)>(c, l);
       }
       RVQSD_STAMP(5 * l + 3);
+      RVQSD_READY(5 * l + 4);
       if constexpr (UseMfma<WT, MR>::value) {
         if (ok) ok = phase_proj_m<MR, (3 * MR + 3) / 4, kUptF>(c, l, true);
       } else {
@@ -1986,20 +2592,25 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
       }
       RVQSD_STAMP(5 * l + 4);
     }
+    RVQSD_READY(ph_heads(L));
     if constexpr (UseMfma<WT, MR>::value) {
       if (ok) ok = phase_heads_m<MR>(c);
     } else {
       if (ok) ok = phase_heads<WT, MR, (MR <= 5 ? 8 : 4)>(c);
     }
     RVQSD_STAMP(ph_heads(L));
+    RVQSD_READY(ph_sample(L));
     if (ok) ok = phase_sample<MR>(c);
     RVQSD_STAMP(ph_sample(L));
+    c.rdy = nullptr;
     ok = wg_sync_ok(c, ok);
+    RVQSD_READY(ph_sample(L) + 1);
     if (ok) ok = commit_and_advance(c);
     RVQSD_STAMP(ph_sample(L) + 1);
     if (!ok || shs.m >= p->n_codes) break;
   }
 #undef RVQSD_STAMP
+#undef RVQSD_READY
   if (blockIdx.x == 0 && tid() == 0) {
     rvqsd_stats* st = fa.out_stats;
     st->target_calls = shs.st_calls;
@@ -2038,9 +2649,9 @@ int frame_lds_head_floats(int mr, int cpw) {
   return kMaxRows * cpw + kWaves * (rpt + 1) * mr;
 }
 
-template <typename WT, int MR>
+template <typename WT, int MR, bool FUSED>
 static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* stream, size_t lds, char* err, size_t errlen) {
-  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR>);
+  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR, FUSED>);
   static size_t attr_bytes = 0;  // per instantiation
   if (lds > attr_bytes) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -2062,10 +2673,15 @@ static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* strea
   return RVQSD_OK;
 }
 
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream, size_t lds_bytes,
-                 char* err, size_t errlen) {
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, bool fused, void* stream,
+                 size_t lds_bytes, char* err, size_t errlen) {
 #define RVQSD_CASE(T, M) \
-  if (mr == M) return launch_t<T, M>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+  if (mr == M) return launch_t<T, M, false>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+  if (fused && dtype == RVQSD_DTYPE_BF16) {
+    if (mr == 2) return launch_t<bf16_t, 2, true>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+    if (mr == 4) return launch_t<bf16_t, 4, true>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+    if (mr == 5) return launch_t<bf16_t, 5, true>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+  }
   if (dtype == RVQSD_DTYPE_F32) {
     RVQSD_CASE(float, 2) RVQSD_CASE(float, 4) RVQSD_CASE(float, 5) RVQSD_CASE(float, 8) RVQSD_CASE(float, 16)
   } else {

@@ -14,6 +14,8 @@ constexpr int kMaxRows = 16;           // rows of one pass (K+1 <= 15, prefix 2)
 constexpr int kSlotDraft0 = kMaxRows;  // logit slot of the first draft row
 constexpr int kMaxTopk = 256;
 constexpr int kTraceRoundInts = 32;    // ints per traced round
+constexpr int kTopkCand = 64;          // values the boundary bucket of the bucket top-k may hold
+constexpr int kTopkBuckets = 1024;     // value buckets of the bucket top-k
 // MFMA path (bf16 weights, <= 8 rows per pass): 512-wide k units per wave, i.e.
 // the largest hidden, q width and FFN it takes are 512 times these.
 constexpr int kUptH = 2, kUptQ = 4, kUptF = 6;
@@ -40,7 +42,8 @@ struct KParams {
   // activation exchange buffers: fp32 bit patterns whose lowest mantissa bit
   // carries the parity of the write epoch (every epoch rewrites every word)
   uint32_t* xb;    // [kMaxRows][H]      residual stream (parity 0 after O, 1 after down)
-  uint32_t* qkvb;  // [kMaxRows][nqkv]   raw q | k | v
+  uint32_t* qkvb;  // [kMaxRows][nqkv]   q | k | v (fused path: q, k after norm gain and RoPE, unscaled)
+  uint32_t* qkss;  // [kMaxRows][nq + nkv][8] fused path: partial sums of squares of raw q, k (8 parts a head)
   uint32_t* attnb; // [kMaxRows][qdim]   attention output
   uint32_t* actb;  // [kMaxRows][F]      SiLU(gate) * up
   uint32_t* pass_count;  // passes run by this stream so far (0xffffffff: poisoned by an error)
@@ -58,6 +61,7 @@ struct KParams {
   int32_t* tr_rounds;  // [tr_max_rounds][kTraceRoundInts]
   uint64_t* tr_clock;  // [tr_max_rounds][phases_per_pass + 1]
   uint64_t* tr_wgclock;  // [tr_max_rounds][phases_per_pass + 1][nwg]
+  uint64_t* tr_wgready;  // [tr_max_rounds][phases_per_pass + 1][nwg] input-complete time
   int32_t tr_max_rounds;
 };
 
@@ -72,8 +76,11 @@ struct FrameArgs {
 };
 
 // Host entry into the kernel translation unit. gp: KParams in device memory.
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream, size_t lds_bytes,
-                 char* err, size_t errlen);
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, bool fused, void* stream,
+                 size_t lds_bytes, char* err, size_t errlen);
+// floats after the work area used by the fused attention path: fp16 KV cache of one
+// layer (kv heads x 16 positions x 128 x 2 halves) and the O rows' residual values
+inline int fused_extra_floats(int nkv, int mr) { return nkv * kMaxPos * 128 + mr * 32; }
 int frame_lds_head_floats(int mr, int cpw);
 int frame_max_rows(int K);
 

@@ -55,7 +55,7 @@ assert STATS_DTYPE.itemsize == ctypes.sizeof(rvqsd_stats)
 
 class rvqsd_trace(ctypes.Structure):
     _fields_ = [("logits", ctypes.c_void_p), ("rounds", ctypes.c_void_p), ("clock", ctypes.c_void_p),
-                ("wg_clock", ctypes.c_void_p), ("max_rounds", ctypes.c_int32)]
+                ("wg_clock", ctypes.c_void_p), ("max_rounds", ctypes.c_int32), ("wg_ready", ctypes.c_void_p)]
 
 
 class rvqsd_info(ctypes.Structure):
@@ -208,11 +208,12 @@ class Stream:
         _check(lib().rvqsd_stream_reset(self._h), "rvqsd_stream_reset")
 
     def set_trace(self, logits_ptr: int = 0, rounds_ptr: int = 0, clock_ptr: int = 0, max_rounds: int = 0,
-                  wg_clock_ptr: int = 0):
-        if not (logits_ptr or rounds_ptr or clock_ptr or wg_clock_ptr):
+                  wg_clock_ptr: int = 0, wg_ready_ptr: int = 0):
+        if not (logits_ptr or rounds_ptr or clock_ptr or wg_clock_ptr or wg_ready_ptr):
             _check(lib().rvqsd_set_trace(self._h, None), "rvqsd_set_trace")
             self._trace = None
             return
-        t = rvqsd_trace(logits_ptr or None, rounds_ptr or None, clock_ptr or None, wg_clock_ptr or None, max_rounds)
+        t = rvqsd_trace(logits_ptr or None, rounds_ptr or None, clock_ptr or None, wg_clock_ptr or None, max_rounds,
+                        wg_ready_ptr or None)
         _check(lib().rvqsd_set_trace(self._h, ctypes.byref(t)), "rvqsd_set_trace")
         self._trace = t
