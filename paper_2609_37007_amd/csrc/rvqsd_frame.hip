@@ -670,15 +670,43 @@ __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, i
             s2 = fmaf(x[e], x[e], s2);
             x[e] *= gv[b][e];
           }
-          sqc[idx] = s2;
         }
         put_split(xsp, split_stride(K), m, idx - m * nch, x);
+      }
+      if constexpr (GAIN) {
+        // the 64 chunks of a wave belong to one row (K is a multiple of 512): one sum per wave,
+        // sqc[idx / 64] (row m owns sqc[m * K / 512 ..])
+        const int i0 = base + b * kThreads + (tid() & ~63);
+        if (i0 < total) {
+          float s2 = 0.f;
+          if (idx < total) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              const float a0 = __uint_as_float((uint32_t)v[b][w]), a1 = __uint_as_float((uint32_t)(v[b][w] >> 32));
+              s2 = fmaf(a0, a0, fmaf(a1, a1, s2));
+            }
+          }
+          s2 = wave_sum63(s2);
+          if ((tid() & 63) == 63) sqc[i0 >> 6] = s2;
+        }
       }
     }
   }
   return wg_sync_ok(c, true);
 }
+// 1 / sqrt(mean of squares + eps) of staged row m from the per-wave sums of stage_split / split_rows
+__device__ __forceinline__ float rstd_of(const Ctx& c, const float* sqc, int K, int m) {
+  const int G = K >> 9;
+  float s = 0.f;
+  for (int k = 0; k < G; ++k) s += sqc[m * G + k];
+  return 1.f / sqrtf(s / (float)K + c.p->rms_eps);
+}
 
+// rstd[m] from the per-wave sums of stage_split / split_rows, m < R.
+__device__ __forceinline__ void rstd_from_chunks_w(const Ctx& c, const float* sqc, int K, int R) {
+  if (tid() < R) c.sh->rstd[tid()] = rstd_of(c, sqc, K, tid());
+  __syncthreads();
+}
 // rstd[m] = 1 / sqrt(sum of the row's chunk sums / K + eps), m < R (one wave per row).
 __device__ __forceinline__ void rstd_from_chunks(const Ctx& c, const float* sqc, int K, int R) {
   const int lane = tid() & 63, wave = tid() >> 6, nch = K >> 3;
@@ -793,6 +821,19 @@ struct MTile {
       out[r * MR + mm] = rstd ? s * rstd[mm] : s;
     }
   }
+  // one tile group (ntiles <= NT, weights preloaded), wave partials in red after the barrier;
+  // psum(red, r, m) then gives the product of row r and activation row m
+  __device__ __forceinline__ void run1(const uint32_t* xsp, int R, float* red) {
+    mma(0, true, [](int) -> const bf16_t* { return nullptr; }, xsp, R, red);
+    lds_barrier();
+  }
+  __device__ __forceinline__ float psum(const float* red, int r, int m) const {
+    const int t = r >> 4, i = r & 15;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += red[((w * NT + t) << 8) + (i << 4) + m];
+    return s;
+  }
   // whole product for nrows rows: tile groups of NT, weights of the first group preloaded
   template <typename RowPtr>
   __device__ __forceinline__ void run(RowPtr rowptr, const uint32_t* xsp, int R, float* red, float* out,
@@ -810,18 +851,27 @@ struct MTile {
 // (global, nullable); sqc (nullable) receives each chunk's sum of squares of
 // the raw values.
 __device__ __forceinline__ void split_rows(const float* xs, uint32_t* xsp, int K, int R, const float* gain, float* sqc) {
-  const int nch = K >> 3;
-  for (int idx = tid(); idx < R * nch; idx += kThreads) {
-    const int m = idx / nch, q = idx - m * nch;
-    float x[8], s2 = 0.f;
+  const int nch = K >> 3, total = R * nch;
+  for (int base = 0; base < total; base += kThreads) {
+    const int idx = base + tid();
+    float s2 = 0.f;
+    if (idx < total) {
+      const int m = idx / nch, q = idx - m * nch;
+      float x[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float v = xs[(size_t)idx * 8 + e];
-      s2 = fmaf(v, v, s2);
-      x[e] = gain ? v * G(gain)[q * 8 + e] : v;
+      for (int e = 0; e < 8; ++e) {
+        const float v = xs[(size_t)idx * 8 + e];
+        s2 = fmaf(v, v, s2);
+        x[e] = gain ? v * G(gain)[q * 8 + e] : v;
+      }
+      put_split(xsp, split_stride(K), m, q, x);
     }
-    put_split(xsp, split_stride(K), m, q, x);
-    if (sqc) sqc[idx] = s2;
+    // one sum per wave (64 chunks of one row, K a multiple of 512), as stage_split
+    const int i0 = base + (tid() & ~63);
+    if (sqc && i0 < total) {
+      s2 = wave_sum63(s2);
+      if ((tid() & 63) == 63) sqc[i0 >> 6] = s2;
+    }
   }
   __syncthreads();
 }
@@ -1299,6 +1349,19 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   MTile<MR, 1, kUptH> mt;
   mt.setup(H, nrows);
   mt.load(0, rowptr);
+  // q / k rows (FUSED): this thread's norm gains and rotary factors, fetched before the wait
+  float rg0 = 1.f, rg1 = 1.f, rcs = 1.f, rsn = 0.f;
+  if (qkrot && tid() < 64) {
+    const int m = tid() >> 3, i = 8 * qk_j + (tid() & 7);
+    if (p->qk_norm) {
+      const float* gn = fptr(p, layer_off(p, l, qk_head < p->nq ? p->o_qn : p->o_kn));
+      rg0 = G(gn)[i];
+      rg1 = G(gn)[i + 64];
+    }
+    const int pos = min(sh->first_pos + m, kMaxPos - 1);
+    rcs = G(p->rope)[(pos * 64 + i) * 2];
+    rsn = G(p->rope)[(pos * 64 + i) * 2 + 1];
+  }
   const float* gain = fptr(p, layer_off(p, l, p->o_attn_norm));
   uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);  // [MR][H + 4] split
   float* sqc = c.work + MR * (H + 4);                   // [MR][H/8]
@@ -1325,9 +1388,8 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
                               kFusedRows))
       return false;
   }
-  if (nrows > 0) {
-    rstd_from_chunks(c, sqc, H, R);
-    mt.run(rowptr, xsp, R, red, out, sh->rstd);
+  if (nrows > 0 && mt.ntiles <= 1) {
+    mt.run1(xsp, R, red);
     const uint32_t ep = epoch_layer(c, sh->pass, l);
     if (qkrot) {
       // q / k rows: publish RoPE(x * gain) at the row's position and the partial sum of squares of
@@ -1338,22 +1400,18 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
         const int m = t >> 3, jp = t & 7, i = 8 * qk_j + jp;
         float a = 0.f, b = 0.f;
         if (m < MR && m < R) {
-          a = out[jp * MR + m];
-          b = out[(8 + jp) * MR + m];
+          const float rs = rstd_of(c, sqc, H, m);
+          a = mt.psum(red, jp, m) * rs;
+          b = mt.psum(red, 8 + jp, m) * rs;
         }
         float ss = fmaf(a, a, b * b);
         ss += dpp<0xB1>(ss);   // quad
         ss += dpp<0x4E>(ss);
         ss += dpp<0x141>(ss);  // half row of 8
         if (m < MR) {
-          if (p->qk_norm) {
-            const float* gn = fptr(p, layer_off(p, l, qk_head < p->nq ? p->o_qn : p->o_kn));
-            a *= G(gn)[i];
-            b *= G(gn)[i + 64];
-          }
-          const int pos = min(sh->first_pos + m, kMaxPos - 1);
-          const float cs = G(p->rope)[(pos * 64 + i) * 2], sn = G(p->rope)[(pos * 64 + i) * 2 + 1];
-          const float ra = a * cs - b * sn, rb = b * cs + a * sn;
+          a *= rg0;
+          b *= rg1;
+          const float ra = a * rcs - b * rsn, rb = b * rcs + a * rsn;
           estore(p->qkvb + (size_t)m * N + qk_head * 128 + i, m < R ? ra : 0.f, ep);
           estore(p->qkvb + (size_t)m * N + qk_head * 128 + i + 64, m < R ? rb : 0.f, ep);
           if (jp == 0)
@@ -1362,9 +1420,17 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
       }
     } else {
       for (int i = tid(); i < MR * nrows; i += kThreads) {
-        const int m = i / nrows, r = i % nrows;
-        estore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, ep);
+        const int r = i / MR, m = i - r * MR;
+        estore(p->qkvb + (size_t)m * N + row0 + r, m < R ? mt.psum(red, r, m) * rstd_of(c, sqc, H, m) : 0.f, ep);
       }
+    }
+  } else if (nrows > 0) {
+    rstd_from_chunks_w(c, sqc, H, R);
+    mt.run(rowptr, xsp, R, red, out, sh->rstd);
+    const uint32_t ep = epoch_layer(c, sh->pass, l);
+    for (int i = tid(); i < MR * nrows; i += kThreads) {
+      const int m = i / nrows, r = i % nrows;
+      estore(p->qkvb + (size_t)m * N + outrow(r), m < R ? out[r * MR + m] : 0.f, ep);
     }
   }
   lds_barrier();  // the work area is reused by the next phase
@@ -1392,18 +1458,31 @@ __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) 
   const uint32_t* src = is_down ? p->actb : p->attnb;
   const uint32_t par = par_layer(c, sh->pass, l);
   if (!stage_split<CB, false>(c, src, K, R, par, nullptr, xsp, nullptr)) return false;
-  mt.run(rowptr, xsp, R, red, out, nullptr);
   const uint32_t xpar = is_down ? kParDown : kParO;
-  for (int i = tid(); i < MR * nrows; i += kThreads) {
-    const int m = i / nrows, r = i % nrows;
-    float v = 0.f;
-    if (m < R) {
-      v = c.xown[m * c.cpw + r] + out[r * MR + m];
-      c.xown[m * c.cpw + r] = v;
+  if (mt.ntiles <= 1) {
+    mt.run1(xsp, R, red);
+    for (int i = tid(); i < MR * nrows; i += kThreads) {
+      const int r = i / MR, m = i - r * MR;
+      float v = 0.f;
+      if (m < R) {
+        v = c.xown[m * c.cpw + r] + mt.psum(red, r, m);
+        c.xown[m * c.cpw + r] = v;
+      }
+      pstore(p->xb + (size_t)m * H + row0 + r, v, xpar);
     }
-    pstore(p->xb + (size_t)m * H + row0 + r, v, xpar);
+  } else {
+    mt.run(rowptr, xsp, R, red, out, nullptr);
+    for (int i = tid(); i < MR * nrows; i += kThreads) {
+      const int m = i / nrows, r = i % nrows;
+      float v = 0.f;
+      if (m < R) {
+        v = c.xown[m * c.cpw + r] + out[r * MR + m];
+        c.xown[m * c.cpw + r] = v;
+      }
+      pstore(p->xb + (size_t)m * H + row0 + r, v, xpar);
+    }
   }
-  __syncthreads();
+  lds_barrier();  // the work area is reused by the next phase
   return true;
 }
 
@@ -1432,17 +1511,31 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
   if (!stage_split<2, true>(c, p->xb, H, R, kParO, gain, xsp, sqc, KEEP ? c.xown : nullptr,
                             c.cpw * (int)blockIdx.x, c.cpw, c.cpw))
     return false;
-  rstd_from_chunks(c, sqc, H, R);
-  mt.run(rowptr, xsp, R, red, out, sh->rstd);
   const uint32_t par = par_layer(c, sh->pass, l);
-  for (int i = tid(); i < MR * nf; i += kThreads) {
-    const int m = i / nf, j = i % nf;
-    float a = 0.f;
-    if (m < R) {
-      const float gt = out[(2 * j) * MR + m], up = out[(2 * j + 1) * MR + m];
-      a = gt / (1.f + expf(-gt)) * up;
+  if (mt.ntiles <= 2) {
+    mt.run1(xsp, R, red);
+    for (int i = tid(); i < MR * nf; i += kThreads) {
+      const int j = i / MR, m = i - j * MR;
+      float a = 0.f;
+      if (m < R) {
+        const float rs = rstd_of(c, sqc, H, m);
+        const float gt = mt.psum(red, 2 * j, m) * rs, up = mt.psum(red, 2 * j + 1, m) * rs;
+        a = gt / (1.f + expf(-gt)) * up;
+      }
+      pstore(p->actb + (size_t)m * F + f0 + j, a, par);
     }
-    pstore(p->actb + (size_t)m * F + f0 + j, a, par);
+  } else {
+    rstd_from_chunks_w(c, sqc, H, R);
+    mt.run(rowptr, xsp, R, red, out, sh->rstd);
+    for (int i = tid(); i < MR * nf; i += kThreads) {
+      const int m = i / nf, j = i % nf;
+      float a = 0.f;
+      if (m < R) {
+        const float gt = out[(2 * j) * MR + m], up = out[(2 * j + 1) * MR + m];
+        a = gt / (1.f + expf(-gt)) * up;
+      }
+      pstore(p->actb + (size_t)m * F + f0 + j, a, par);
+    }
   }
   lds_barrier();  // the work area is reused by the next phase
   return true;
@@ -1457,8 +1550,8 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
 // attention output never leaves the workgroup. Member k takes O rows
 // [k * rpm, (k + 1) * rpm), rpm = ceil(H / set size).
 //
-// Wave g handles kv head g and its q heads 2g, 2g + 1: lane i holds dimensions i
-// and i + 64 of each vector, so the rotate-half RoPE pairs stay in one lane. The
+// Wave g handles kv head g and its q heads 2g, 2g + 1; the QKV producers already
+// applied the q/k norm gains and RoPE, so lane i simply holds dimensions 2i, 2i + 1. The
 // scores S^T = K Q^T run on v_mfma_f32_16x16x32_f16 (A = 16 cached positions, B =
 // the wave's <= 10 query vectors as an fp16 hi + lo pair); their result layout is
 // exactly the B operand of v_mfma_f32_16x16x16_f16, so O^T = V^T P^T follows with P
@@ -1469,6 +1562,7 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 template <int MR>
 __device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
@@ -1489,46 +1583,58 @@ __device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
   // the residual rows (xres) were kept by this workgroup's QKV phase of the same layer
   bool ok = true;
 
-  // ---- wave g: q of heads 2g, 2g + 1, k and v of kv head g, rows 0 .. R-1 (slot s = type * MR + r)
-  float va[4 * MR], vb[4 * MR];
+  // O weights of this member's rows (two 16-row tiles), k units 4g .. 4g + 3 of wave g, in flight
+  // during the wait
+  const bf16_t* W = wptr<bf16_t>(p, layer_off(p, l, p->o_wo));
+  W16 wa[2][4][2];
 #pragma unroll
-  for (int s2 = 0; s2 < 4 * MR; ++s2) va[s2] = vb[s2] = 0.f;
+  for (int tt = 0; tt < 2; ++tt) {
+    const int row = (tt << 4) + vec;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      W16 v0 = (W16)(0u), v1 = (W16)(0u);
+      if (row < nrows) {
+        const bf16_t* w = W + (size_t)(row0 + row) * qdim + (4 * g + j) * 64 + 16 * q4;
+        v0 = *G(reinterpret_cast<const W16*>(w));
+        v1 = *G(reinterpret_cast<const W16*>(w + 8));
+      }
+      wa[tt][j][0] = v0;
+      wa[tt][j][1] = v1;
+    }
+  }
+  // ---- wave g: q of heads 2g, 2g + 1, k and v of kv head g, rows 0 .. R-1 (slot s = type * MR + r);
+  // lane i holds dimensions 2i and 2i + 1 of each vector (one 64-bit word)
+  uint64_t vw[4 * MR];
+#pragma unroll
+  for (int s2 = 0; s2 < 4 * MR; ++s2) vw[s2] = 0ull;
   // partial sums of squares: vector v = type * MR + r (type 0, 1: q heads 2g, 2g + 1; 2: k head g),
   // parts 2 (lane % 4) and 2 (lane % 4) + 1 in lane 4 v + lane % 4 (v < 3 MR)
   const int sv = lane >> 2, stype = sv / MR, sr = sv - stype * MR;
   const bool slive = sv < 3 * MR && sr < R;
   const int shead = stype < 2 ? 2 * g + stype : p->nq + g;
   const uint32_t* ssrc = p->qkss + ((size_t)sr * (p->nq + p->nkv) + shead) * 8 + 2 * (lane & 3);
-  float ps0 = 0.f, ps1 = 0.f;
+  uint64_t psw = 0ull;
   {
-    uint64_t pend = 0;
+    uint32_t pend = 0;
 #pragma unroll
     for (int s2 = 0; s2 < 4 * MR; ++s2)
-      if (s2 % MR < R) pend |= 3ull << (2 * s2);
-    if (slive) pend |= 3ull << 62;
+      if (s2 % MR < R) pend |= 1u << s2;
+    if (slive) pend |= 1u << 31;
     uint64_t t0 = 0;
     int spins = 0;
     while (ok && pend) {
-      // loads straight into the value registers; a word counts once its parity is this epoch's
+      // loads straight into the value registers; a word counts once it carries this epoch
 #pragma unroll
       for (int s2 = 0; s2 < 4 * MR; ++s2) {
         const int type = s2 / MR, r = s2 % MR;
         const int col = type < 2 ? (2 * g + type) * D : qdim + (type - 2) * kvdim + g * D;
-        const uint32_t* src = p->qkvb + (size_t)r * N + col + lane;
-        if (pend & (1ull << (2 * s2)))
-          va[s2] = __uint_as_float(__hip_atomic_load(G(src), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        if (pend & (1ull << (2 * s2 + 1)))
-          vb[s2] = __uint_as_float(__hip_atomic_load(G(src + HALF), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        if (pend & (1u << s2)) vw[s2] = pload2(p->qkvb + (size_t)r * N + col + 2 * lane);
       }
-      if (pend & (1ull << 62)) ps0 = __uint_as_float(__hip_atomic_load(G(ssrc), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-      if (pend & (1ull << 63)) ps1 = __uint_as_float(__hip_atomic_load(G(ssrc + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      if (pend & (1u << 31)) psw = pload2(ssrc);
 #pragma unroll
-      for (int s2 = 0; s2 < 4 * MR; ++s2) {
-        if ((__float_as_uint(va[s2]) & 7u) == ep) pend &= ~(1ull << (2 * s2));
-        if ((__float_as_uint(vb[s2]) & 7u) == ep) pend &= ~(1ull << (2 * s2 + 1));
-      }
-      if ((__float_as_uint(ps0) & 7u) == ep) pend &= ~(1ull << 62);
-      if ((__float_as_uint(ps1) & 7u) == ep) pend &= ~(1ull << 63);
+      for (int s2 = 0; s2 < 4 * MR; ++s2)
+        if (((uint32_t)vw[s2] & 7u) == ep && ((uint32_t)(vw[s2] >> 32) & 7u) == ep) pend &= ~(1u << s2);
+      if (((uint32_t)psw & 7u) == ep && ((uint32_t)(psw >> 32) & 7u) == ep) pend &= ~(1u << 31);
       // every lane of the wave must agree before leaving
       if (!__any(pend != 0)) break;
       if ((++spins & 31) == 0) {
@@ -1541,55 +1647,43 @@ __device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
   }
   _Float16* Kg = c.kvk + (size_t)g * kMaxPos * D;  // [pos][D]
   _Float16* Vg = c.kvv + (size_t)g * D * kMaxPos;  // [dim][pos]
-  _Float16* xs16 = reinterpret_cast<_Float16*>(c.work);  // the split area, addressed in halves
   uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);   // [MR][qdim + 4] split attention output
   const int xst = qdim + 4;
   f32x4 oacc[2];
   oacc[0] = oacc[1] = (f32x4){0.f, 0.f, 0.f, 0.f};
   if (ok) {
-    // per-head RMSNorm (q, k) and RoPE, then keys and values into the cache, queries (fp16 hi/lo,
-    // the split chunk layout) into this wave's own columns of the split area
-    // RMSNorm scale of each q / k vector from its 8 partial sums (one quad of lanes per vector)
-    float tq = (slive ? ps0 : 0.f) + (slive ? ps1 : 0.f);
+    // RMSNorm scale of each q / k vector from its 8 partial sums (one quad of lanes per vector); the
+    // published q and k already carry the norm gain and the rotation, so only this scale remains
+    float tq = slive ? __uint_as_float((uint32_t)psw) + __uint_as_float((uint32_t)(psw >> 32)) : 0.f;
     tq += dpp<0xB1>(tq);
     tq += dpp<0x4E>(tq);
     const float rsl = p->qk_norm ? rsqrtf(tq / (float)D + p->rms_eps) : 1.f;
-    float rs[3 * MR];
 #pragma unroll
-    for (int s2 = 0; s2 < 3 * MR; ++s2) rs[s2] = lane_val(rsl, 4 * s2);
-#pragma unroll
-    for (int s2 = 0; s2 < 3 * MR; ++s2) {
+    for (int s2 = 0; s2 < 4 * MR; ++s2) {
       const int type = s2 / MR, r = s2 % MR;
-      {
-        // published already gained and rotated: only the vector's scale remains
-        const float ra = va[s2] * rs[s2], rb = vb[s2] * rs[s2];
-        if (type == 2) {
-          const int pos = fp + r;
-          if (r < R) {
-            Kg[pos * D + lane] = (_Float16)ra;
-            Kg[pos * D + lane + HALF] = (_Float16)rb;
-          }
-        } else {
-          const int col = (2 * g + type) * D;  // column of dimension 0 of this head
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int k = col + lane + h * HALF;
-            const float x = h ? rb : ra;
-            const _Float16 hi = (_Float16)x;
-            const _Float16 lo = (_Float16)(x - (float)hi);
-            const int wbase = r * xst + (k >> 3) * 8, e = k & 7;
-            xs16[(wbase + (e >> 1)) * 2 + (e & 1)] = hi;
-            xs16[(wbase + 4 + (e >> 1)) * 2 + (e & 1)] = lo;
-          }
+      const float rs = type < 3 ? lane_val(rsl, 4 * s2) : 1.f;
+      const float x0 = __uint_as_float((uint32_t)vw[s2]) * rs, x1 = __uint_as_float((uint32_t)(vw[s2] >> 32)) * rs;
+      if (type == 2) {
+        // key of position fp + r: dimensions 2 lane, 2 lane + 1
+        if (r < R) {
+          const f16x2 kk = {(_Float16)x0, (_Float16)x1};
+          *reinterpret_cast<f16x2*>(Kg + (fp + r) * D + 2 * lane) = kk;
         }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < MR; ++r) {
-      if (r < R) {
-        const int pos = fp + r;
-        Vg[lane * kMaxPos + pos] = (_Float16)va[3 * MR + r];
-        Vg[(lane + HALF) * kMaxPos + pos] = (_Float16)vb[3 * MR + r];
+      } else if (type == 3) {
+        if (r < R) {
+          Vg[(2 * lane) * kMaxPos + fp + r] = (_Float16)x0;
+          Vg[(2 * lane + 1) * kMaxPos + fp + r] = (_Float16)x1;
+        }
+      } else {
+        // query (row r, head 2g + type): fp16 hi / lo pairs in the split chunk layout of this
+        // wave's own columns
+        const int k = (2 * g + type) * D + 2 * lane;
+        const _Float16 h0 = (_Float16)x0, h1 = (_Float16)x1;
+        const f16x2 hi = {h0, h1};
+        const f16x2 lo = {(_Float16)(x0 - (float)h0), (_Float16)(x1 - (float)h1)};
+        uint32_t* wq = xsp + r * xst + (k >> 3) * 8 + ((k & 7) >> 1);
+        *reinterpret_cast<f16x2*>(wq) = hi;
+        *reinterpret_cast<f16x2*>(wq + 4) = lo;
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -1633,9 +1727,10 @@ __device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
     z += __shfl_xor(z, 16, 64);
     z += __shfl_xor(z, 32, 64);
     f16x4 ph, pl;
+    const float rz = vlive ? __builtin_amdgcn_rcpf(z) : 0.f;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const float pr = vlive ? e4[v] / z : 0.f;
+      const float pr = e4[v] * rz;
       ph[v] = (_Float16)pr;
       pl[v] = (_Float16)(pr - (float)ph[v]);
     }
@@ -1650,11 +1745,10 @@ __device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
         uint32_t hw[2], lw[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          const uint32_t h0 = bf16_bits_rne(o[2 * j]), h1 = bf16_bits_rne(o[2 * j + 1]);
-          const uint32_t l0 = bf16_bits_rne(o[2 * j] - __uint_as_float(h0 << 16));
-          const uint32_t l1 = bf16_bits_rne(o[2 * j + 1] - __uint_as_float(h1 << 16));
-          hw[j] = h0 | (h1 << 16);
-          lw[j] = l0 | (l1 << 16);
+          const __bf16 b0 = (__bf16)o[2 * j], b1 = (__bf16)o[2 * j + 1];
+          const __bf16 c0 = (__bf16)(o[2 * j] - (float)b0), c1 = (__bf16)(o[2 * j + 1] - (float)b1);
+          hw[j] = (uint32_t)__builtin_bit_cast(uint16_t, b0) | ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
+          lw[j] = (uint32_t)__builtin_bit_cast(uint16_t, c0) | ((uint32_t)__builtin_bit_cast(uint16_t, c1) << 16);
         }
         const int wb = vr * xst + (k0 >> 3) * 8 + ((k0 >> 2) & 1) * 2;
         *reinterpret_cast<uint2*>(xsp + wb) = make_uint2(hw[0], hw[1]);
@@ -1664,25 +1758,7 @@ __device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // O projection partials over this wave's units 4g .. 4g + 3 (activation rows = columns of B):
-    // this member's weight rows (two 16-row tiles)
-    const bf16_t* W = wptr<bf16_t>(p, layer_off(p, l, p->o_wo));
-    W16 wa[2][4][2];
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const int row = (tt << 4) + vec;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        W16 v0 = (W16)(0u), v1 = (W16)(0u);
-        if (row < nrows) {
-          const bf16_t* w = W + (size_t)(row0 + row) * qdim + (4 * g + j) * 64 + 16 * q4;
-          v0 = *G(reinterpret_cast<const W16*>(w));
-          v1 = *G(reinterpret_cast<const W16*>(w + 8));
-        }
-        wa[tt][j][0] = v0;
-        wa[tt][j][1] = v1;
-      }
-    }
+    // O projection partials over this wave's units 4g .. 4g + 3 (activation rows = columns of B)
     const bool live = vec < R;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
