@@ -66,6 +66,7 @@ struct rvqsd_model {
   int nwg;
   int mr;               // rows the kernel is instantiated for
   bool fused;           // attention fused into the O projection (16/8 heads of 128, bf16, <= 5 rows)
+  int mode;             // kernel mode (see launch_frame)
   int wbytes;           // bytes per matrix element
   size_t lds_bytes;
   int stage_cols;
@@ -159,7 +160,7 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols, bool fus
     need((size_t)mr * stage_cols + (size_t)cpw * mr);
   }
   if (fused) need((size_t)mr * (qd + 4) + kWaves * 2 * 256);  // split attention output + O tiles
-  else need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4));  // attention: q, k, v rows + the head's KV
+  else need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4) + 2 * kMaxRows * 8);  // attention: q, k, v rows, the head's KV, partial norms
   need((size_t)V + 2 * kMaxTopk + 2 + 2 * 3 * kMaxTopk + kMaxTopk + kTopkBuckets + 8);  // sampling
   return w;
 }
@@ -282,10 +283,10 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
     const int set_min = nwg / k.L;
     const int fpw = (k.F + nwg - 1) / nwg;
     // (the QKV phase gives each workgroup 16 rows: whole RoPE pairs of one head)
-    m->fused = cfg->dtype == RVQSD_DTYPE_BF16 && m->mr <= 5 && k.d == 128 && k.nkv == 8 && k.nq == 16 &&
-               k.nqkv == 16 * nwg &&
-               set_min > 0 && (k.H + set_min - 1) / set_min <= 32 && (nwg - 1) * fpw < k.F &&
-               getenv("RVQSD_NO_FUSED_ATTENTION") == nullptr;
+    m->fused = cfg->dtype == RVQSD_DTYPE_BF16 && cfg->kv_fp16 && m->mr <= 5 && k.d == 128 && k.nkv == 8 &&
+               k.nq == 16 && k.nqkv == 16 * nwg && set_min > 0 && (k.H + set_min - 1) / set_min <= 32 &&
+               (nwg - 1) * fpw < k.F;
+    m->mode = m->fused ? 2 : 0;
   }
   // LDS: stage the widest activation if it fits, else the down projection polls its chunks directly
   const int cpw = (k.H + nwg - 1) / nwg;
@@ -299,7 +300,10 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   if (m->fused) {
     // the fused layout must also fit the LDS; otherwise the separate attention phase is used
     const size_t fl = (head + work_floats(cfg, nwg, m->mr, stage, true) + (size_t)fused_extra_floats(k.nkv, m->mr)) * 4;
-    if (fl > budget) m->fused = false;
+    if (fl > budget) {
+      m->fused = false;
+      m->mode = 0;
+    }
   }
   const size_t work = work_floats(cfg, nwg, m->mr, stage, m->fused);
   size_t lds = (head + work) * 4;
@@ -497,7 +501,7 @@ static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t
   fa.epoch_base = s->epoch;
   s->epoch += s->epoch_step;
   char err[256];
-  int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, s->m->fused, (void*)s->stream, s->m->lds_bytes, err,
+  int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, s->m->mode, (void*)s->stream, s->m->lds_bytes, err,
                         sizeof(err));
   if (st) return set_err(st, "%s", err);
   return RVQSD_OK;

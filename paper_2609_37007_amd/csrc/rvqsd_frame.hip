@@ -1024,7 +1024,9 @@ __device__ __forceinline__ float lane_val(float v, int l) {
 // prefetched into LDS while the workgroup waits for this pass's q, k and v.
 // In LDS each position's k and v are padded to 2d + 4 floats so that the 16
 // positions read by one wave fall on different banks.
-template <int MR>
+// ROT: the QKV producers already applied the q/k norm gains and RoPE and published the
+// partial sums of squares of the raw vectors (8 per head and row); only the scale remains.
+template <int MR, bool ROT = false>
 __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -1054,14 +1056,28 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   // qs, ks, vs are consecutive [kMaxRows][d] blocks and v of kv head g follows k at +kvdim
   const int rd2 = R * d / 2, d2 = d / 2, kvdim = p->kvdim;
   const uint32_t* qkvb = p->qkvb;
+  // ROT: partial sums of squares, vector v < 2R (q rows, then k rows), 8 parts as 4 pairs
+  float* pss = kv + (size_t)kMaxPos * ps;  // [2 kMaxRows][8]
+  const int nss = ROT ? 2 * R * 4 : 0, nhd = p->nq + p->nkv;
+  const uint32_t* qkss = p->qkss;
   bool ok = poll_pairs(
-      c, 3 * rd2, par,
+      c, 3 * rd2 + nss, par,
       [=](int i) {
+        if (ROT && i >= 3 * rd2) {
+          const int j = i - 3 * rd2, v = j >> 2, r = v < R ? v : v - R, hd = v < R ? h : p->nq + g;
+          return qkss + ((size_t)r * nhd + hd) * 8 + 2 * (j & 3);
+        }
         const int part = i / rd2, rem = i - part * rd2, r = rem / d2, k = 2 * (rem - r * d2);
         const int off = part == 0 ? qoff : koff + (part - 1) * kvdim;
         return qkvb + (size_t)r * N + off + k;
       },
       [=](int i, float lo, float hi) {
+        if (ROT && i >= 3 * rd2) {
+          const int j = i - 3 * rd2;
+          pss[2 * j] = lo;
+          pss[2 * j + 1] = hi;
+          return;
+        }
         const int part = i / rd2, rem = i - part * rd2;
         qs[part * kMaxRows * d + 2 * rem] = lo;
         qs[part * kMaxRows * d + 2 * rem + 1] = hi;
@@ -1097,20 +1113,36 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
       b[j] = i < half ? x[i + half] : 0.f;
       s2 = fmaf(a[j], a[j], fmaf(b[j], b[j], s2));
     }
-    const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)d + p->rms_eps) : 1.f;
     float* dst = isq ? qs + r * d : kv + (size_t)pos * ps;
+    if constexpr (ROT) {
+      // gained and rotated by the producers: the norm scale from the 8 partial sums
+      float t8 = 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = hl + 32 * j;
-      if (i < half) {
-        float u = a[j], w = b[j];
-        if (p->qk_norm) {
-          u = u * rs * gn[i];
-          w = w * rs * gn[i + half];
+      for (int k = 0; k < 8; ++k) t8 += pss[v * 8 + k];
+      const float rs = p->qk_norm ? 1.f / sqrtf(t8 / (float)d + p->rms_eps) : 1.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = hl + 32 * j;
+        if (i < half) {
+          dst[i] = a[j] * rs;
+          dst[i + half] = b[j] * rs;
         }
-        const float cs = rope[(pos * half + i) * 2], sn = rope[(pos * half + i) * 2 + 1];
-        dst[i] = u * cs - w * sn;
-        dst[i + half] = w * cs + u * sn;
+      }
+    } else {
+      const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)d + p->rms_eps) : 1.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = hl + 32 * j;
+        if (i < half) {
+          float u = a[j], w = b[j];
+          if (p->qk_norm) {
+            u = u * rs * gn[i];
+            w = w * rs * gn[i + half];
+          }
+          const float cs = rope[(pos * half + i) * 2], sn = rope[(pos * half + i) * 2 + 1];
+          dst[i] = u * cs - w * sn;
+          dst[i + half] = w * cs + u * sn;
+        }
       }
     }
     if (!isq) {
@@ -1119,8 +1151,15 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
     }
   }
   __syncthreads();
+  // device copy of the new k, v for later passes: the stores go out while the scores are computed
+  for (int wi = tid(); wi < R * d; wi += kThreads) {
+    const int pos = fp + wi / d, w = wi % d;
+    __hip_atomic_store(G(gkv + (size_t)pos * d + w), reinterpret_cast<const uint64_t*>(kv + (size_t)pos * ps)[w],
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   // one wave per row: lane = (position t = lane / 4, quarter j = lane % 4 of the dimensions)
   const float scale = 1.f / sqrtf((float)d);
+  const int npos = fp + R;  // positions holding this pass's keys and values
   const int t = lane >> 2, qj = lane & 3, dq = d / 4;
   for (int r = wave; r < MR; r += kWaves) {
     if (r < R) {
@@ -1148,12 +1187,13 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
       const float e = t <= last ? expf(sc - mx) : 0.f;
       const float rsum = row16_sum(qj == 0 ? e : 0.f);
       const float z = (lane_val(rsum, 15) + lane_val(rsum, 31)) + (lane_val(rsum, 47) + lane_val(rsum, 63));
-      const float pr = e / z;
-      // o[r][i] = sum_t pr_t v[t][i] for i = lane + 64 j (head_dim <= 256)
+      const float pr = e * __builtin_amdgcn_rcpf(z);
+      // o[r][i] = sum_t pr_t v[t][i] for i = lane + 64 j (head_dim <= 256); positions after this
+      // row's own hold this pass's later rows with weight 0, so only the pass-wide bound branches
       float o[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int tt = 0; tt < kMaxPos; ++tt) {
-        if (tt <= last) {
+        if (tt < npos) {
           const float pt = lane_val(pr, 4 * tt);
           const float* vv = kv + (size_t)tt * ps + d;
 #pragma unroll
@@ -1167,12 +1207,6 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
     } else {
       for (int i = lane; i < d; i += 64) pstore(p->attnb + (size_t)r * p->qdim + qoff + i, 0.f, par);
     }
-  }
-  // device copy of the new k, v for later passes (after the outputs are out)
-  for (int wi = tid(); wi < R * d; wi += kThreads) {
-    const int pos = fp + wi / d, w = wi % d;
-    __hip_atomic_store(G(gkv + (size_t)pos * d + w), reinterpret_cast<const uint64_t*>(kv + (size_t)pos * ps)[w],
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   // the next phase reuses the work area: no wave may still be reading it
   lds_barrier();
@@ -1318,7 +1352,7 @@ __device__ __forceinline__ void fused_rows(const KParams* p, int l, int* row0, i
 
 // FUSED: a member of layer l's set also keeps the layer input of its O rows (the residual
 // the fused O projection adds) while it stages that input.
-template <int MR, bool FUSED = false>
+template <int MR, bool ROT = false, bool FUSED = false>
 __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -1331,10 +1365,10 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   const bf16_t* wk = wptr<bf16_t>(p, layer_off(p, l, p->o_wk));
   const bf16_t* wv = wptr<bf16_t>(p, layer_off(p, l, p->o_wv));
   const int qd = p->qdim, kd = p->kvdim;
-  // FUSED: workgroup w < 8 (nq + nkv) takes rows 8j .. 8j + 7 and 64 + 8j .. 64 + 8j + 7 of q/k head
+  // ROT: workgroup w < 8 (nq + nkv) takes rows 8j .. 8j + 7 and 64 + 8j .. 64 + 8j + 7 of q/k head
   // w / 8 (j = w % 8), so every RoPE pair of its rows is its own; the v workgroups keep plain rows
   const int nqk = (p->nq + p->nkv) * 8;
-  const bool qkrot = FUSED && (int)blockIdx.x < nqk;
+  const bool qkrot = ROT && (int)blockIdx.x < nqk;
   const int qk_head = (int)blockIdx.x >> 3, qk_j = (int)blockIdx.x & 7;
   auto outrow = [&](int r) -> int {
     if (qkrot) return qk_head * 128 + (r < 8 ? 8 * qk_j + r : 64 + 8 * qk_j + (r - 8));
@@ -2547,8 +2581,9 @@ __device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c, int wbyte
   return b;
 }
 
-template <typename WT, int MR, bool FUSED>
+template <typename WT, int MR, int MODE>
 __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
+  constexpr bool FUSED = MODE == 2, ROT = MODE >= 1;
   constexpr int RPT = MR <= 8 ? 8 : 4;
   __shared__ Shared shs;
   extern __shared__ __align__(16) float dyn[];
@@ -2625,7 +2660,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   } while (0)
     for (int l = 0; l < L && ok && FUSED; ++l) {
       RVQSD_READY(5 * l + 0);
-      ok = phase_qkv_m<MR, true>(c, l);
+      ok = phase_qkv_m<MR, true, true>(c, l);
       RVQSD_STAMP(5 * l + 0);
       RVQSD_READY(5 * l + 1);
       if (ok) ok = phase_attn_o_fused<MR>(c, l);
@@ -2640,11 +2675,11 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     }
     for (int l = 0; l < L && ok && !FUSED; ++l) {
       RVQSD_READY(5 * l + 0);
-      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<MR>(c, l);
+      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<MR, ROT, false>(c, l);
       else ok = phase_qkv<WT, MR, 4>(c, l);
       RVQSD_STAMP(5 * l + 0);
       RVQSD_READY(5 * l + 1);
-      if (ok) ok = phase_attn<MR>(c, l);
+      if (ok) ok = phase_attn<MR, ROT>(c, l);
       RVQSD_STAMP(5 * l + 1);
       RVQSD_READY(5 * l + 2);
       if constexpr (UseMfma<WT, MR>::value) {
@@ -2725,9 +2760,9 @@ int frame_lds_head_floats(int mr, int cpw) {
   return kMaxRows * cpw + kWaves * (rpt + 1) * mr;
 }
 
-template <typename WT, int MR, bool FUSED>
+template <typename WT, int MR, int MODE>
 static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* stream, size_t lds, char* err, size_t errlen) {
-  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR, FUSED>);
+  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR, MODE>);
   static size_t attr_bytes = 0;  // per instantiation
   if (lds > attr_bytes) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -2749,14 +2784,14 @@ static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* strea
   return RVQSD_OK;
 }
 
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, bool fused, void* stream,
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, int mode, void* stream,
                  size_t lds_bytes, char* err, size_t errlen) {
 #define RVQSD_CASE(T, M) \
-  if (mr == M) return launch_t<T, M, false>(gp, fa, nwg, stream, lds_bytes, err, errlen);
-  if (fused && dtype == RVQSD_DTYPE_BF16) {
-    if (mr == 2) return launch_t<bf16_t, 2, true>(gp, fa, nwg, stream, lds_bytes, err, errlen);
-    if (mr == 4) return launch_t<bf16_t, 4, true>(gp, fa, nwg, stream, lds_bytes, err, errlen);
-    if (mr == 5) return launch_t<bf16_t, 5, true>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+  if (mr == M) return launch_t<T, M, 0>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+  if (mode == 2 && dtype == RVQSD_DTYPE_BF16) {
+    if (mr == 2) return launch_t<bf16_t, 2, 2>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+    if (mr == 4) return launch_t<bf16_t, 4, 2>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+    if (mr == 5) return launch_t<bf16_t, 5, 2>(gp, fa, nwg, stream, lds_bytes, err, errlen);
   }
   if (dtype == RVQSD_DTYPE_F32) {
     RVQSD_CASE(float, 2) RVQSD_CASE(float, 4) RVQSD_CASE(float, 5) RVQSD_CASE(float, 8) RVQSD_CASE(float, 16)

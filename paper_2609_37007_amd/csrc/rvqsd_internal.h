@@ -76,7 +76,10 @@ struct FrameArgs {
 };
 
 // Host entry into the kernel translation unit. gp: KParams in device memory.
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, bool fused, void* stream,
+// mode 0: separate attention phase, fp32 KV cache; 2: (cfg kv_fp16) attention fused into the
+// O projection with an fp16 KV cache, the QKV producers applying the q/k norm gains and RoPE
+// (bf16, 16 q / 8 kv heads of 128, 16 q/k/v rows per workgroup, <= 5 rows per pass)
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, int mode, void* stream,
                  size_t lds_bytes, char* err, size_t errlen);
 // floats after the work area used by the fused attention path: fp16 KV cache of one
 // layer (kv heads x 16 positions x 128 x 2 halves) and the O rows' residual values
