@@ -58,11 +58,7 @@ typedef struct {
   int32_t topk;        /* 1..256 */
   int32_t draft_len;   /* K, 0..min(max_draft, 14); 0 = plain autoregressive sampling */
   int32_t draft_greedy;/* 0: drafts sampled from the draft distribution; 1: its argmax */
-  int32_t kv_fp16;     /* 1: for the 16 q / 8 kv heads of 128 shape (bf16, draft_len <= 4), keep each
-                          layer's KV cache in LDS as fp16 and fuse attention into the O projection:
-                          one exchange fewer per layer, logits within ~1.5e-3 instead of ~2e-5 of fp64.
-                          Other shapes ignore it. 0: fp32 KV cache, separate attention phase. */
-  int32_t reserved[2];
+  int32_t reserved[3];
   double rms_eps, rope_base, temperature;
 } rvqsd_cfg;
 

@@ -65,8 +65,6 @@ struct rvqsd_model {
   int device;
   int nwg;
   int mr;               // rows the kernel is instantiated for
-  bool fused;           // attention fused into the O projection (16/8 heads of 128, bf16, <= 5 rows)
-  int mode;             // kernel mode (see launch_frame)
   int wbytes;           // bytes per matrix element
   size_t lds_bytes;
   int stage_cols;
@@ -128,7 +126,7 @@ int validate_cfg(const rvqsd_cfg* c, int nwg) {
 }
 
 // Work-area floats needed by every phase for a given staging width.
-size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols, bool fused) {
+size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
   const int H = c->hidden, qd = c->n_q_heads * c->head_dim, kd = c->n_kv_heads * c->head_dim, F = c->ffn;
   const int V = c->vocab, d = c->head_dim, K = c->draft_len;
   const int cpw = (H + nwg - 1) / nwg;
@@ -159,8 +157,7 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols, bool fus
     need((size_t)mr * H + (size_t)rows_out * mr);
     need((size_t)mr * stage_cols + (size_t)cpw * mr);
   }
-  if (fused) need((size_t)mr * (qd + 4) + kWaves * 2 * 256);  // split attention output + O tiles
-  else need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4) + 2 * kMaxRows * 8);  // attention: q, k, v rows, the head's KV, partial norms
+  need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4));  // attention: q, k, v rows and the head's KV
   need((size_t)V + 2 * kMaxTopk + 2 + 2 * 3 * kMaxTopk + kMaxTopk + kTopkBuckets + 8);  // sampling
   return w;
 }
@@ -275,19 +272,6 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   }
   m->wbytes = (int)wb;
   m->dweight_bytes = o;
-  {
-    // fused attention: the 16 q / 8 kv heads of 128 shape with bf16 weights and <= 5 rows per
-    // pass; every layer's set of workgroups (w % L == l) must cover the hidden rows at <= 32
-    // rows a member, and every workgroup must own gate/up features (it keeps its residual
-    // columns while staging the gate/up input)
-    const int set_min = nwg / k.L;
-    const int fpw = (k.F + nwg - 1) / nwg;
-    // (the QKV phase gives each workgroup 16 rows: whole RoPE pairs of one head)
-    m->fused = cfg->dtype == RVQSD_DTYPE_BF16 && cfg->kv_fp16 && m->mr <= 5 && k.d == 128 && k.nkv == 8 &&
-               k.nq == 16 && k.nqkv == 16 * nwg && set_min > 0 && (k.H + set_min - 1) / set_min <= 32 &&
-               (nwg - 1) * fpw < k.F;
-    m->mode = m->fused ? 2 : 0;
-  }
   // LDS: stage the widest activation if it fits, else the down projection polls its chunks directly
   const int cpw = (k.H + nwg - 1) / nwg;
   const size_t head = (size_t)frame_lds_head_floats(m->mr, cpw);
@@ -297,22 +281,13 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   const int epc = cfg->dtype == RVQSD_DTYPE_F32 ? 4 : 8;
   int stage = (int)(qd > H ? qd : H);
   if (2 * ((int)F / epc) <= kThreads && (int)F > stage) stage = (int)F;
-  if (m->fused) {
-    // the fused layout must also fit the LDS; otherwise the separate attention phase is used
-    const size_t fl = (head + work_floats(cfg, nwg, m->mr, stage, true) + (size_t)fused_extra_floats(k.nkv, m->mr)) * 4;
-    if (fl > budget) {
-      m->fused = false;
-      m->mode = 0;
-    }
-  }
-  const size_t work = work_floats(cfg, nwg, m->mr, stage, m->fused);
+  const size_t work = work_floats(cfg, nwg, m->mr, stage);
   size_t lds = (head + work) * 4;
   if (lds > budget) {
     delete m;
     return set_err(RVQSD_EUNSUPPORTED, "needs %zu bytes of LDS per workgroup, %zu available", lds, budget);
   }
-  const size_t attn_const_floats = m->fused ? (size_t)fused_extra_floats(k.nkv, m->mr)  // KV cache + residual rows
-                                            : (size_t)k.L * 2 * k.d + (size_t)kMaxPos * k.d;  // gains + rotary table
+  const size_t attn_const_floats = (size_t)k.L * 2 * k.d + (size_t)kMaxPos * k.d;  // q/k gains + rotary table
   lds += attn_const_floats * 4;
   if (lds > budget) {
     delete m;
@@ -383,7 +358,6 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
   const size_t o_rope = take((size_t)kMaxPos * k.d * 4);
   const size_t par_begin = off;
   const size_t o_x = take(kMaxRows * H * 4), o_qkv = take((size_t)kMaxRows * k.nqkv * 4),
-               o_qkss = take((size_t)kMaxRows * (k.nq + k.nkv) * 8 * 4),
                o_attn = take((size_t)kMaxRows * k.qdim * 4), o_act = take((size_t)kMaxRows * k.F * 4);
   const size_t par_end = off;
   const size_t o_pc = take(4);
@@ -413,7 +387,6 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
   uint8_t* base = (uint8_t*)s->dbuf;
   k.xb = (uint32_t*)(base + o_x);
   k.qkvb = (uint32_t*)(base + o_qkv);
-  k.qkss = (uint32_t*)(base + o_qkss);
   k.attnb = (uint32_t*)(base + o_attn);
   k.actb = (uint32_t*)(base + o_act);
   k.pass_count = (uint32_t*)(base + o_pc);
@@ -501,7 +474,7 @@ static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t
   fa.epoch_base = s->epoch;
   s->epoch += s->epoch_step;
   char err[256];
-  int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, s->m->mode, (void*)s->stream, s->m->lds_bytes, err,
+  int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, (void*)s->stream, s->m->lds_bytes, err,
                         sizeof(err));
   if (st) return set_err(st, "%s", err);
   return RVQSD_OK;

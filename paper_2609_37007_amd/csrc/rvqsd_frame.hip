@@ -60,13 +60,6 @@ __device__ __forceinline__ void xstoref(uint64_t* p, uint32_t tag, float v) { xs
 __device__ __forceinline__ void pstore(uint32_t* p, float v, uint32_t par) {
   __hip_atomic_store(G(p), (__float_as_uint(v) & ~1u) | par, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// q/k/v word: fp32 with the three lowest mantissa bits replaced by the write's layer epoch
-// mod 8 (bit 0 is the parity the per-layer readers check). The fused attention path reads
-// these words only every L-th layer, so a parity bit alone would also match the copy
-// written two layers earlier; the epoch matches only the current write.
-__device__ __forceinline__ void estore(uint32_t* p, float v, uint32_t ep) {
-  __hip_atomic_store(G(p), (__float_as_uint(v) & ~7u) | (ep & 7u), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 __device__ __forceinline__ uint64_t pload2(const uint32_t* p) {
   return __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -260,9 +253,6 @@ struct Ctx {
   float* red;       // [kWaves][RPT * MR] reduction scratch
   float* work;      // union area
   float* attn_const;  // [L][2][d] q/k norm gains, then [kMaxPos][d/2][2] rotary table (attention workgroups)
-  _Float16* kvk;    // fused path: [nkv][kMaxPos][128] keys (after norm and RoPE) of this workgroup's layer
-  _Float16* kvv;    // fused path: [nkv][128][kMaxPos] values, transposed
-  float* xres;      // fused path: [MR][kFusedRows] residual rows of this workgroup's O rows
   int cpw;          // residual columns per workgroup
   uint32_t tag_base;
   uint32_t pass0;   // passes this stream ran before this frame
@@ -273,10 +263,6 @@ struct Ctx {
 // one write per layer per pass, so it alternates with every write
 __device__ __forceinline__ uint32_t par_layer(const Ctx& c, int pass, int l) {
   return (uint32_t)(((uint64_t)(c.pass0 + pass) * (uint64_t)c.p->L + (uint64_t)l) & 1u);
-}
-// layer epoch mod 8 of the q/k/v buffer (its bit 0 is par_layer)
-__device__ __forceinline__ uint32_t epoch_layer(const Ctx& c, int pass, int l) {
-  return (uint32_t)(((uint64_t)(c.pass0 + pass) * (uint64_t)c.p->L + (uint64_t)l) & 7u);
 }
 constexpr uint32_t kParO = 0, kParDown = 1;  // residual stream: written after O, then after down
 
@@ -591,12 +577,9 @@ __device__ __forceinline__ void put_split(uint32_t* xsp, int stride, int m, int 
 // each chunk's sum of squares of the raw x for the row's RMSNorm.
 // Chunk i of the pass is handled by thread i % kThreads; up to CB chunks per
 // thread are in flight at once.
-// Keep range (kdst nullable): the raw values of columns kc0 .. kc0 + kn - 1 also go to
-// kdst[m * kstride + column - kc0] (the residual values a later phase adds to).
 template <int CB, bool GAIN>
 __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, int K, int R, uint32_t par,
-                                            const float* gain, uint32_t* xsp, float* sqc,
-                                            float* kdst = nullptr, int kc0 = 0, int kn = 0, int kstride = 0) {
+                                            const float* gain, uint32_t* xsp, float* sqc) {
   const int nch = K >> 3, total = R * nch;
   for (int base = 0; base < total; base += CB * kThreads) {
     uint32_t pending = 0;  // bit 4b + w: word w of chunk b still missing
@@ -656,14 +639,6 @@ __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, i
           x[2 * w + 1] = __uint_as_float((uint32_t)(v[b][w] >> 32));
         }
         const int m = idx / nch;
-        if (kdst) {
-          const int q0 = (idx - m * nch) * 8;
-          if (q0 + 8 > kc0 && q0 < kc0 + kn) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (q0 + e >= kc0 && q0 + e < kc0 + kn) kdst[m * kstride + (q0 + e - kc0)] = x[e];
-          }
-        }
         if constexpr (GAIN) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -987,10 +962,10 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
     float xg[MR][Gemv<WT, MR, RPT>::EPC], sq[MR];
     chunk_from_lds<MR, Gemv<WT, MR, RPT>::EPC>(xs, H, g.kc, g.active, g.gain, xg, sq);
     g.run(c, xg, rowptr, out, sq);
-    const uint32_t ep = epoch_layer(c, sh->pass, l);
+    const uint32_t par = par_layer(c, sh->pass, l);
     for (int i = tid(); i < MR * nrows; i += kThreads) {
       const int m = i / nrows, r = i % nrows;
-      estore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, ep);
+      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
     }
   }
   // the next phase reuses the work area: no wave may still be reading it
@@ -1024,9 +999,7 @@ __device__ __forceinline__ float lane_val(float v, int l) {
 // prefetched into LDS while the workgroup waits for this pass's q, k and v.
 // In LDS each position's k and v are padded to 2d + 4 floats so that the 16
 // positions read by one wave fall on different banks.
-// ROT: the QKV producers already applied the q/k norm gains and RoPE and published the
-// partial sums of squares of the raw vectors (8 per head and row); only the scale remains.
-template <int MR, bool ROT = false>
+template <int MR>
 __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -1056,28 +1029,14 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   // qs, ks, vs are consecutive [kMaxRows][d] blocks and v of kv head g follows k at +kvdim
   const int rd2 = R * d / 2, d2 = d / 2, kvdim = p->kvdim;
   const uint32_t* qkvb = p->qkvb;
-  // ROT: partial sums of squares, vector v < 2R (q rows, then k rows), 8 parts as 4 pairs
-  float* pss = kv + (size_t)kMaxPos * ps;  // [2 kMaxRows][8]
-  const int nss = ROT ? 2 * R * 4 : 0, nhd = p->nq + p->nkv;
-  const uint32_t* qkss = p->qkss;
   bool ok = poll_pairs(
-      c, 3 * rd2 + nss, par,
+      c, 3 * rd2, par,
       [=](int i) {
-        if (ROT && i >= 3 * rd2) {
-          const int j = i - 3 * rd2, v = j >> 2, r = v < R ? v : v - R, hd = v < R ? h : p->nq + g;
-          return qkss + ((size_t)r * nhd + hd) * 8 + 2 * (j & 3);
-        }
         const int part = i / rd2, rem = i - part * rd2, r = rem / d2, k = 2 * (rem - r * d2);
         const int off = part == 0 ? qoff : koff + (part - 1) * kvdim;
         return qkvb + (size_t)r * N + off + k;
       },
       [=](int i, float lo, float hi) {
-        if (ROT && i >= 3 * rd2) {
-          const int j = i - 3 * rd2;
-          pss[2 * j] = lo;
-          pss[2 * j + 1] = hi;
-          return;
-        }
         const int part = i / rd2, rem = i - part * rd2;
         qs[part * kMaxRows * d + 2 * rem] = lo;
         qs[part * kMaxRows * d + 2 * rem + 1] = hi;
@@ -1114,35 +1073,19 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
       s2 = fmaf(a[j], a[j], fmaf(b[j], b[j], s2));
     }
     float* dst = isq ? qs + r * d : kv + (size_t)pos * ps;
-    if constexpr (ROT) {
-      // gained and rotated by the producers: the norm scale from the 8 partial sums
-      float t8 = 0.f;
+    const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)d + p->rms_eps) : 1.f;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) t8 += pss[v * 8 + k];
-      const float rs = p->qk_norm ? 1.f / sqrtf(t8 / (float)d + p->rms_eps) : 1.f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = hl + 32 * j;
-        if (i < half) {
-          dst[i] = a[j] * rs;
-          dst[i + half] = b[j] * rs;
+    for (int j = 0; j < 4; ++j) {
+      const int i = hl + 32 * j;
+      if (i < half) {
+        float u = a[j], w = b[j];
+        if (p->qk_norm) {
+          u = u * rs * gn[i];
+          w = w * rs * gn[i + half];
         }
-      }
-    } else {
-      const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)d + p->rms_eps) : 1.f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = hl + 32 * j;
-        if (i < half) {
-          float u = a[j], w = b[j];
-          if (p->qk_norm) {
-            u = u * rs * gn[i];
-            w = w * rs * gn[i + half];
-          }
-          const float cs = rope[(pos * half + i) * 2], sn = rope[(pos * half + i) * 2 + 1];
-          dst[i] = u * cs - w * sn;
-          dst[i + half] = w * cs + u * sn;
-        }
+        const float cs = rope[(pos * half + i) * 2], sn = rope[(pos * half + i) * 2 + 1];
+        dst[i] = u * cs - w * sn;
+        dst[i + half] = w * cs + u * sn;
       }
     }
     if (!isq) {
@@ -1341,41 +1284,19 @@ __device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
 // Same partition of weight rows over workgroups as the phases above; the
 // weights of the first round are loaded before the wait for the activations.
 
-// rows of the fused O projection one member of layer l's set takes (see phase_attn_o_fused)
-constexpr int kFusedRows = 32;  // O rows one member takes at most
-__device__ __forceinline__ int fused_set_size(const KParams* p, int l) { return (p->nwg - l + p->L - 1) / p->L; }
-__device__ __forceinline__ void fused_rows(const KParams* p, int l, int* row0, int* nrows) {
-  const int S = fused_set_size(p, l), rpm = (p->H + S - 1) / S;
-  *row0 = ((int)blockIdx.x / p->L) * rpm;
-  *nrows = max(0, min(rpm, p->H - *row0));
-}
-
-// FUSED: a member of layer l's set also keeps the layer input of its O rows (the residual
-// the fused O projection adds) while it stages that input.
-template <int MR, bool ROT = false, bool FUSED = false>
+template <int MR>
 __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
   const int H = p->H, R = sh->rows, N = p->nqkv;
-  int f0 = 0, fn = 0;
-  if (FUSED && (int)blockIdx.x % p->L == l) fused_rows(p, l, &f0, &fn);
   const int rpw = (N + p->nwg - 1) / p->nwg, row0 = blockIdx.x * rpw;
   const int nrows = max(0, min(rpw, N - row0));
   const bf16_t* wq = wptr<bf16_t>(p, layer_off(p, l, p->o_wq));
   const bf16_t* wk = wptr<bf16_t>(p, layer_off(p, l, p->o_wk));
   const bf16_t* wv = wptr<bf16_t>(p, layer_off(p, l, p->o_wv));
   const int qd = p->qdim, kd = p->kvdim;
-  // ROT: workgroup w < 8 (nq + nkv) takes rows 8j .. 8j + 7 and 64 + 8j .. 64 + 8j + 7 of q/k head
-  // w / 8 (j = w % 8), so every RoPE pair of its rows is its own; the v workgroups keep plain rows
-  const int nqk = (p->nq + p->nkv) * 8;
-  const bool qkrot = ROT && (int)blockIdx.x < nqk;
-  const int qk_head = (int)blockIdx.x >> 3, qk_j = (int)blockIdx.x & 7;
-  auto outrow = [&](int r) -> int {
-    if (qkrot) return qk_head * 128 + (r < 8 ? 8 * qk_j + r : 64 + 8 * qk_j + (r - 8));
-    return row0 + r;
-  };
   auto rowptr = [&](int r) -> const bf16_t* {
-    const int o = outrow(r);
+    const int o = row0 + r;
     if (o < qd) return wq + (size_t)o * H;
     if (o < qd + kd) return wk + (size_t)(o - qd) * H;
     return wv + (size_t)(o - qd - kd) * H;
@@ -1383,19 +1304,6 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   MTile<MR, 1, kUptH> mt;
   mt.setup(H, nrows);
   mt.load(0, rowptr);
-  // q / k rows (FUSED): this thread's norm gains and rotary factors, fetched before the wait
-  float rg0 = 1.f, rg1 = 1.f, rcs = 1.f, rsn = 0.f;
-  if (qkrot && tid() < 64) {
-    const int m = tid() >> 3, i = 8 * qk_j + (tid() & 7);
-    if (p->qk_norm) {
-      const float* gn = fptr(p, layer_off(p, l, qk_head < p->nq ? p->o_qn : p->o_kn));
-      rg0 = G(gn)[i];
-      rg1 = G(gn)[i + 64];
-    }
-    const int pos = min(sh->first_pos + m, kMaxPos - 1);
-    rcs = G(p->rope)[(pos * 64 + i) * 2];
-    rsn = G(p->rope)[(pos * 64 + i) * 2 + 1];
-  }
   const float* gain = fptr(p, layer_off(p, l, p->o_attn_norm));
   uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);  // [MR][H + 4] split
   float* sqc = c.work + MR * (H + 4);                   // [MR][H/8]
@@ -1410,61 +1318,26 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
       const int m = i / c.cpw, j = i % c.cpw;
       c.xown[i] = (m < MR && o0 + j < H) ? xs[m * H + o0 + j] : 0.f;
     }
-    for (int i = tid(); i < MR * fn; i += kThreads) {
-      const int m = i / fn, j = i - m * fn;
-      c.xres[m * kFusedRows + j] = xs[m * H + f0 + j];
-    }
     __syncthreads();
     split_rows(xs, xsp, H, R, gain, sqc);
   } else {
-    if (nrows == 0 && fn == 0) return true;
-    if (!stage_split<2, true>(c, p->xb, H, R, kParDown, gain, xsp, sqc, fn > 0 ? c.xres : nullptr, f0, fn,
-                              kFusedRows))
-      return false;
+    if (nrows == 0) return true;
+    if (!stage_split<2, true>(c, p->xb, H, R, kParDown, gain, xsp, sqc)) return false;
   }
   if (nrows > 0 && mt.ntiles <= 1) {
     mt.run1(xsp, R, red);
-    const uint32_t ep = epoch_layer(c, sh->pass, l);
-    if (qkrot) {
-      // q / k rows: publish RoPE(x * gain) at the row's position and the partial sum of squares of
-      // the raw x over these 16 dimensions; the consumer scales by 1 / sqrt(sum / d + eps)
-      // (the per-head RMSNorm is a per-vector scale, the rotation keeps it)
-      const int t = tid();
-      if (t < 64) {
-        const int m = t >> 3, jp = t & 7, i = 8 * qk_j + jp;
-        float a = 0.f, b = 0.f;
-        if (m < MR && m < R) {
-          const float rs = rstd_of(c, sqc, H, m);
-          a = mt.psum(red, jp, m) * rs;
-          b = mt.psum(red, 8 + jp, m) * rs;
-        }
-        float ss = fmaf(a, a, b * b);
-        ss += dpp<0xB1>(ss);   // quad
-        ss += dpp<0x4E>(ss);
-        ss += dpp<0x141>(ss);  // half row of 8
-        if (m < MR) {
-          a *= rg0;
-          b *= rg1;
-          const float ra = a * rcs - b * rsn, rb = b * rcs + a * rsn;
-          estore(p->qkvb + (size_t)m * N + qk_head * 128 + i, m < R ? ra : 0.f, ep);
-          estore(p->qkvb + (size_t)m * N + qk_head * 128 + i + 64, m < R ? rb : 0.f, ep);
-          if (jp == 0)
-            estore(p->qkss + ((size_t)m * (p->nq + p->nkv) + qk_head) * 8 + qk_j, m < R ? ss : 0.f, ep);
-        }
-      }
-    } else {
-      for (int i = tid(); i < MR * nrows; i += kThreads) {
-        const int r = i / MR, m = i - r * MR;
-        estore(p->qkvb + (size_t)m * N + row0 + r, m < R ? mt.psum(red, r, m) * rstd_of(c, sqc, H, m) : 0.f, ep);
-      }
+    const uint32_t par = par_layer(c, sh->pass, l);
+    for (int i = tid(); i < MR * nrows; i += kThreads) {
+      const int r = i / MR, m = i - r * MR;
+      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? mt.psum(red, r, m) * rstd_of(c, sqc, H, m) : 0.f, par);
     }
   } else if (nrows > 0) {
     rstd_from_chunks_w(c, sqc, H, R);
     mt.run(rowptr, xsp, R, red, out, sh->rstd);
-    const uint32_t ep = epoch_layer(c, sh->pass, l);
+    const uint32_t par = par_layer(c, sh->pass, l);
     for (int i = tid(); i < MR * nrows; i += kThreads) {
       const int m = i / nrows, r = i % nrows;
-      estore(p->qkvb + (size_t)m * N + outrow(r), m < R ? out[r * MR + m] : 0.f, ep);
+      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
     }
   }
   lds_barrier();  // the work area is reused by the next phase
@@ -1521,8 +1394,7 @@ __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) 
 }
 
 // gate and up rows interleaved (2j = gate row f0 + j, 2j + 1 = up row); act = SiLU(gate) * up.
-// KEEP: also keep this workgroup's raw residual columns (the fused path's down projection adds them).
-template <int MR, bool KEEP = false>
+template <int MR>
 __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -1541,10 +1413,7 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
   float* red = sqc + MR * (H >> 3);                     // [kWaves][2][256]
   float* out = red + kWaves * 2 * 256;                  // [2 nf][MR]
   const float* gain = fptr(p, layer_off(p, l, p->o_mlp_norm));
-  // KEEP: this workgroup's residual columns (the down projection's rows) go to xown
-  if (!stage_split<2, true>(c, p->xb, H, R, kParO, gain, xsp, sqc, KEEP ? c.xown : nullptr,
-                            c.cpw * (int)blockIdx.x, c.cpw, c.cpw))
-    return false;
+  if (!stage_split<2, true>(c, p->xb, H, R, kParO, gain, xsp, sqc)) return false;
   const uint32_t par = par_layer(c, sh->pass, l);
   if (mt.ntiles <= 2) {
     mt.run1(xsp, R, red);
@@ -1570,269 +1439,6 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
       }
       pstore(p->actb + (size_t)m * F + f0 + j, a, par);
     }
-  }
-  lds_barrier();  // the work area is reused by the next phase
-  return true;
-}
-
-// ----------------------------------- fused attention + O projection (bf16, <= 5 rows)
-// For the 16 q / 8 kv head, head_dim 128 shape, layer l's attention and O
-// projection run on the workgroups w with w % L == l (the set of layer l). Every
-// member keeps layer l's whole KV cache in LDS for the frame (fp16 keys after
-// norm and RoPE, fp16 values stored transposed) and computes the attention of all
-// heads itself, so the q/k/v exchange feeds the O projection directly and the
-// attention output never leaves the workgroup. Member k takes O rows
-// [k * rpm, (k + 1) * rpm), rpm = ceil(H / set size).
-//
-// Wave g handles kv head g and its q heads 2g, 2g + 1; the QKV producers already
-// applied the q/k norm gains and RoPE, so lane i simply holds dimensions 2i, 2i + 1. The
-// scores S^T = K Q^T run on v_mfma_f32_16x16x32_f16 (A = 16 cached positions, B =
-// the wave's <= 10 query vectors as an fp16 hi + lo pair); their result layout is
-// exactly the B operand of v_mfma_f32_16x16x16_f16, so O^T = V^T P^T follows with P
-// as an fp16 hi + lo pair and no transpose. Wave g then owns the O projection's k
-// units of its own heads (columns 256g .. 256g + 255), reading its attention output
-// back from LDS it wrote itself, so the only workgroup barrier after the wait is the
-// one before the cross-wave sum of the O tiles.
-
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-
-template <int MR>
-__device__ __forceinline__ bool phase_attn_o_fused(const Ctx& c, int l) {
-  constexpr int D = 128, HALF = 64;
-  const KParams* p = c.p;
-  const Shared* sh = c.sh;
-  const int L = p->L;
-  if ((int)blockIdx.x % L != l) return true;
-  const int H = p->H, R = sh->rows, N = p->nqkv, fp = sh->first_pos;
-  int row0, nrows;
-  fused_rows(p, l, &row0, &nrows);
-  if (nrows == 0) return true;
-  const int qdim = p->qdim, kvdim = p->kvdim;
-  const int lane = tid() & 63, wave = tid() >> 6, g = wave;
-  const int vec = lane & 15, q4 = lane >> 4;
-  const uint32_t ep = epoch_layer(c, sh->pass, l);
-
-  // the residual rows (xres) were kept by this workgroup's QKV phase of the same layer
-  bool ok = true;
-
-  // O weights of this member's rows (two 16-row tiles), k units 4g .. 4g + 3 of wave g, in flight
-  // during the wait
-  const bf16_t* W = wptr<bf16_t>(p, layer_off(p, l, p->o_wo));
-  W16 wa[2][4][2];
-#pragma unroll
-  for (int tt = 0; tt < 2; ++tt) {
-    const int row = (tt << 4) + vec;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      W16 v0 = (W16)(0u), v1 = (W16)(0u);
-      if (row < nrows) {
-        const bf16_t* w = W + (size_t)(row0 + row) * qdim + (4 * g + j) * 64 + 16 * q4;
-        v0 = *G(reinterpret_cast<const W16*>(w));
-        v1 = *G(reinterpret_cast<const W16*>(w + 8));
-      }
-      wa[tt][j][0] = v0;
-      wa[tt][j][1] = v1;
-    }
-  }
-  // ---- wave g: q of heads 2g, 2g + 1, k and v of kv head g, rows 0 .. R-1 (slot s = type * MR + r);
-  // lane i holds dimensions 2i and 2i + 1 of each vector (one 64-bit word)
-  uint64_t vw[4 * MR];
-#pragma unroll
-  for (int s2 = 0; s2 < 4 * MR; ++s2) vw[s2] = 0ull;
-  // partial sums of squares: vector v = type * MR + r (type 0, 1: q heads 2g, 2g + 1; 2: k head g),
-  // parts 2 (lane % 4) and 2 (lane % 4) + 1 in lane 4 v + lane % 4 (v < 3 MR)
-  const int sv = lane >> 2, stype = sv / MR, sr = sv - stype * MR;
-  const bool slive = sv < 3 * MR && sr < R;
-  const int shead = stype < 2 ? 2 * g + stype : p->nq + g;
-  const uint32_t* ssrc = p->qkss + ((size_t)sr * (p->nq + p->nkv) + shead) * 8 + 2 * (lane & 3);
-  uint64_t psw = 0ull;
-  {
-    uint32_t pend = 0;
-#pragma unroll
-    for (int s2 = 0; s2 < 4 * MR; ++s2)
-      if (s2 % MR < R) pend |= 1u << s2;
-    if (slive) pend |= 1u << 31;
-    uint64_t t0 = 0;
-    int spins = 0;
-    while (ok && pend) {
-      // loads straight into the value registers; a word counts once it carries this epoch
-#pragma unroll
-      for (int s2 = 0; s2 < 4 * MR; ++s2) {
-        const int type = s2 / MR, r = s2 % MR;
-        const int col = type < 2 ? (2 * g + type) * D : qdim + (type - 2) * kvdim + g * D;
-        if (pend & (1u << s2)) vw[s2] = pload2(p->qkvb + (size_t)r * N + col + 2 * lane);
-      }
-      if (pend & (1u << 31)) psw = pload2(ssrc);
-#pragma unroll
-      for (int s2 = 0; s2 < 4 * MR; ++s2)
-        if (((uint32_t)vw[s2] & 7u) == ep && ((uint32_t)(vw[s2] >> 32) & 7u) == ep) pend &= ~(1u << s2);
-      if (((uint32_t)psw & 7u) == ep && ((uint32_t)(psw >> 32) & 7u) == ep) pend &= ~(1u << 31);
-      // every lane of the wave must agree before leaving
-      if (!__any(pend != 0)) break;
-      if ((++spins & 31) == 0) {
-        const uint64_t now = dclock();
-        if (t0 == 0) t0 = now;
-        else if (now - t0 > kTimeoutTicks) { status_raise(p, c.tag_base, RVQSD_ETIMEOUT); ok = false; break; }
-        if (status_set(p, c.tag_base)) { ok = false; break; }
-      }
-    }
-  }
-  _Float16* Kg = c.kvk + (size_t)g * kMaxPos * D;  // [pos][D]
-  _Float16* Vg = c.kvv + (size_t)g * D * kMaxPos;  // [dim][pos]
-  uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);   // [MR][qdim + 4] split attention output
-  const int xst = qdim + 4;
-  f32x4 oacc[2];
-  oacc[0] = oacc[1] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  if (ok) {
-    // RMSNorm scale of each q / k vector from its 8 partial sums (one quad of lanes per vector); the
-    // published q and k already carry the norm gain and the rotation, so only this scale remains
-    float tq = slive ? __uint_as_float((uint32_t)psw) + __uint_as_float((uint32_t)(psw >> 32)) : 0.f;
-    tq += dpp<0xB1>(tq);
-    tq += dpp<0x4E>(tq);
-    const float rsl = p->qk_norm ? rsqrtf(tq / (float)D + p->rms_eps) : 1.f;
-#pragma unroll
-    for (int s2 = 0; s2 < 4 * MR; ++s2) {
-      const int type = s2 / MR, r = s2 % MR;
-      const float rs = type < 3 ? lane_val(rsl, 4 * s2) : 1.f;
-      const float x0 = __uint_as_float((uint32_t)vw[s2]) * rs, x1 = __uint_as_float((uint32_t)(vw[s2] >> 32)) * rs;
-      if (type == 2) {
-        // key of position fp + r: dimensions 2 lane, 2 lane + 1
-        if (r < R) {
-          const f16x2 kk = {(_Float16)x0, (_Float16)x1};
-          *reinterpret_cast<f16x2*>(Kg + (fp + r) * D + 2 * lane) = kk;
-        }
-      } else if (type == 3) {
-        if (r < R) {
-          Vg[(2 * lane) * kMaxPos + fp + r] = (_Float16)x0;
-          Vg[(2 * lane + 1) * kMaxPos + fp + r] = (_Float16)x1;
-        }
-      } else {
-        // query (row r, head 2g + type): fp16 hi / lo pairs in the split chunk layout of this
-        // wave's own columns
-        const int k = (2 * g + type) * D + 2 * lane;
-        const _Float16 h0 = (_Float16)x0, h1 = (_Float16)x1;
-        const f16x2 hi = {h0, h1};
-        const f16x2 lo = {(_Float16)(x0 - (float)h0), (_Float16)(x1 - (float)h1)};
-        uint32_t* wq = xsp + r * xst + (k >> 3) * 8 + ((k & 7) >> 1);
-        *reinterpret_cast<f16x2*>(wq) = hi;
-        *reinterpret_cast<f16x2*>(wq + 4) = lo;
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // scores S^T[pos][vector], vector = gi * R + r (query head 2g + gi, row r)
-    const int NV = 2 * R;
-    const bool vlive = vec < NV;
-    const int gi = vlive ? vec / R : 0, vr = vlive ? vec - gi * R : 0;
-    const int hq = 2 * g + gi;
-    f32x4 sacc = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int cc = 0; cc < D / 32; ++cc) {
-      const f16x8 a = *reinterpret_cast<const f16x8*>(Kg + vec * D + 32 * cc + 8 * q4);
-      f16x8 bh = (f16x8)((_Float16)0.f), bl = (f16x8)((_Float16)0.f);
-      if (vlive) {
-        const int wb = vr * xst + (hq * 16 + 4 * cc + q4) * 8;
-        bh = *reinterpret_cast<const f16x8*>(xsp + wb);
-        bl = *reinterpret_cast<const f16x8*>(xsp + wb + 4);
-      }
-      sacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bh, sacc, 0, 0, 0);
-      sacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bl, sacc, 0, 0, 0);
-    }
-    // causal softmax over positions 0 .. fp + r of each vector (column vec; positions 4 q4 + v)
-    const float scale = 1.f / sqrtf((float)D);
-    const int last = fp + vr;
-    float sc[4], mx = -INFINITY;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      sc[v] = (vlive && 4 * q4 + v <= last) ? sacc[v] * scale : -INFINITY;
-      mx = fmaxf(mx, sc[v]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    float e4[4], z = 0.f;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      e4[v] = sc[v] > -INFINITY ? expf(sc[v] - mx) : 0.f;
-      z += e4[v];
-    }
-    z += __shfl_xor(z, 16, 64);
-    z += __shfl_xor(z, 32, 64);
-    f16x4 ph, pl;
-    const float rz = vlive ? __builtin_amdgcn_rcpf(z) : 0.f;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const float pr = e4[v] * rz;
-      ph[v] = (_Float16)pr;
-      pl[v] = (_Float16)(pr - (float)ph[v]);
-    }
-    // O^T[dim][vector] = V^T P^T in 16-dimension tiles; written back split (bf16 hi/lo)
-#pragma unroll
-    for (int t = 0; t < D / 16; ++t) {
-      const f16x4 a = *reinterpret_cast<const f16x4*>(Vg + (16 * t + vec) * kMaxPos + 4 * q4);
-      f32x4 o = __builtin_amdgcn_mfma_f32_16x16x16f16(a, ph, (f32x4){0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-      o = __builtin_amdgcn_mfma_f32_16x16x16f16(a, pl, o, 0, 0, 0);
-      if (vlive) {
-        const int k0 = hq * D + 16 * t + 4 * q4;  // four consecutive columns
-        uint32_t hw[2], lw[2];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const __bf16 b0 = (__bf16)o[2 * j], b1 = (__bf16)o[2 * j + 1];
-          const __bf16 c0 = (__bf16)(o[2 * j] - (float)b0), c1 = (__bf16)(o[2 * j + 1] - (float)b1);
-          hw[j] = (uint32_t)__builtin_bit_cast(uint16_t, b0) | ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
-          lw[j] = (uint32_t)__builtin_bit_cast(uint16_t, c0) | ((uint32_t)__builtin_bit_cast(uint16_t, c1) << 16);
-        }
-        const int wb = vr * xst + (k0 >> 3) * 8 + ((k0 >> 2) & 1) * 2;
-        *reinterpret_cast<uint2*>(xsp + wb) = make_uint2(hw[0], hw[1]);
-        *reinterpret_cast<uint2*>(xsp + wb + 4) = make_uint2(lw[0], lw[1]);
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // O projection partials over this wave's units 4g .. 4g + 3 (activation rows = columns of B)
-    const bool live = vec < R;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      W16 bv[4];
-      if (live) {
-        const uint32_t* bp = xsp + (size_t)vec * xst + (4 * g + j) * 64 + 16 * q4;
-        bv[0] = *reinterpret_cast<const W16*>(bp);
-        bv[1] = *reinterpret_cast<const W16*>(bp + 4);
-        bv[2] = *reinterpret_cast<const W16*>(bp + 8);
-        bv[3] = *reinterpret_cast<const W16*>(bp + 12);
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) bv[q] = (W16)(0u);
-      }
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        const bf16x8 a0 = __builtin_bit_cast(bf16x8, wa[tt][j][0]), a1 = __builtin_bit_cast(bf16x8, wa[tt][j][1]);
-        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, bv[0]), oacc[tt], 0, 0, 0);
-        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, bv[1]), oacc[tt], 0, 0, 0);
-        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, bv[2]), oacc[tt], 0, 0, 0);
-        oacc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, bv[3]), oacc[tt], 0, 0, 0);
-      }
-    }
-  }
-  // wave partial tiles to LDS (after the split area), then the cross-wave sum
-  float* red = c.work + MR * xst;  // [kWaves][2][256]
-#pragma unroll
-  for (int tt = 0; tt < 2; ++tt) {
-    float* dst = red + ((size_t)(wave * 2 + tt) << 8);
-#pragma unroll
-    for (int v = 0; v < 4; ++v) dst[((4 * q4 + v) << 4) + vec] = oacc[tt][v];
-  }
-  if (!wg_sync_ok(c, ok)) return false;
-  for (int o = tid(); o < nrows * MR; o += kThreads) {
-    const int r = o / MR, m = o - r * MR, tt = r >> 4, i = r & 15;
-    float sum = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) sum += red[((w * 2 + tt) << 8) + (i << 4) + m];
-    const float v = m < R ? c.xres[m * kFusedRows + r] + sum : 0.f;
-    pstore(p->xb + (size_t)m * H + row0 + r, v, kParO);
   }
   lds_barrier();  // the work area is reused by the next phase
   return true;
@@ -2581,9 +2187,8 @@ __device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c, int wbyte
   return b;
 }
 
-template <typename WT, int MR, int MODE>
+template <typename WT, int MR>
 __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
-  constexpr bool FUSED = MODE == 2, ROT = MODE >= 1;
   constexpr int RPT = MR <= 8 ? 8 : 4;
   __shared__ Shared shs;
   extern __shared__ __align__(16) float dyn[];
@@ -2597,15 +2202,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   c.red = dyn + kMaxRows * c.cpw;
   c.work = c.red + kWaves * (RPT + 1) * MR;
   c.attn_const = c.work + p->work_floats;
-  c.kvk = reinterpret_cast<_Float16*>(c.work + p->work_floats);
-  c.kvv = c.kvk + (size_t)p->nkv * kMaxPos * 128;
-  c.xres = reinterpret_cast<float*>(c.kvv + (size_t)p->nkv * 128 * kMaxPos);
-  if constexpr (FUSED) {
-    // the frame's KV cache starts zeroed: masked positions then hold finite values
-    uint4* z = reinterpret_cast<uint4*>(c.kvk);
-    const int n16 = p->nkv * kMaxPos * 128 * 2 * 2 / 16;
-    for (int i = tid(); i < n16; i += kThreads) z[i] = make_uint4(0u, 0u, 0u, 0u);
-  } else if ((int)blockIdx.x < p->nq) {
+  if ((int)blockIdx.x < p->nq) {
     const int d = p->d;
     for (int i = tid(); i < p->L * 2 * d; i += kThreads) {
       const int l = i / (2 * d), j = i % (2 * d);
@@ -2658,28 +2255,13 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
       if (wclk_on) wclk[(size_t)(ph) * p->nwg] = dclock();                \
     }                                                                     \
   } while (0)
-    for (int l = 0; l < L && ok && FUSED; ++l) {
+    for (int l = 0; l < L && ok; ++l) {
       RVQSD_READY(5 * l + 0);
-      ok = phase_qkv_m<MR, true, true>(c, l);
-      RVQSD_STAMP(5 * l + 0);
-      RVQSD_READY(5 * l + 1);
-      if (ok) ok = phase_attn_o_fused<MR>(c, l);
-      RVQSD_STAMP(5 * l + 1);
-      RVQSD_STAMP(5 * l + 2);
-      RVQSD_READY(5 * l + 3);
-      if (ok) ok = phase_gu_m<MR, true>(c, l);
-      RVQSD_STAMP(5 * l + 3);
-      RVQSD_READY(5 * l + 4);
-      if (ok) ok = phase_proj_m<MR, (3 * MR + 3) / 4, kUptF>(c, l, true);
-      RVQSD_STAMP(5 * l + 4);
-    }
-    for (int l = 0; l < L && ok && !FUSED; ++l) {
-      RVQSD_READY(5 * l + 0);
-      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<MR, ROT, false>(c, l);
+      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<MR>(c, l);
       else ok = phase_qkv<WT, MR, 4>(c, l);
       RVQSD_STAMP(5 * l + 0);
       RVQSD_READY(5 * l + 1);
-      if (ok) ok = phase_attn<MR, ROT>(c, l);
+      if (ok) ok = phase_attn<MR>(c, l);
       RVQSD_STAMP(5 * l + 1);
       RVQSD_READY(5 * l + 2);
       if constexpr (UseMfma<WT, MR>::value) {
@@ -2760,9 +2342,9 @@ int frame_lds_head_floats(int mr, int cpw) {
   return kMaxRows * cpw + kWaves * (rpt + 1) * mr;
 }
 
-template <typename WT, int MR, int MODE>
+template <typename WT, int MR>
 static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* stream, size_t lds, char* err, size_t errlen) {
-  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR, MODE>);
+  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR>);
   static size_t attr_bytes = 0;  // per instantiation
   if (lds > attr_bytes) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -2784,15 +2366,10 @@ static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* strea
   return RVQSD_OK;
 }
 
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, int mode, void* stream,
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream,
                  size_t lds_bytes, char* err, size_t errlen) {
 #define RVQSD_CASE(T, M) \
-  if (mr == M) return launch_t<T, M, 0>(gp, fa, nwg, stream, lds_bytes, err, errlen);
-  if (mode == 2 && dtype == RVQSD_DTYPE_BF16) {
-    if (mr == 2) return launch_t<bf16_t, 2, 2>(gp, fa, nwg, stream, lds_bytes, err, errlen);
-    if (mr == 4) return launch_t<bf16_t, 4, 2>(gp, fa, nwg, stream, lds_bytes, err, errlen);
-    if (mr == 5) return launch_t<bf16_t, 5, 2>(gp, fa, nwg, stream, lds_bytes, err, errlen);
-  }
+  if (mr == M) return launch_t<T, M>(gp, fa, nwg, stream, lds_bytes, err, errlen);
   if (dtype == RVQSD_DTYPE_F32) {
     RVQSD_CASE(float, 2) RVQSD_CASE(float, 4) RVQSD_CASE(float, 5) RVQSD_CASE(float, 8) RVQSD_CASE(float, 16)
   } else {

@@ -42,8 +42,7 @@ struct KParams {
   // activation exchange buffers: fp32 bit patterns whose lowest mantissa bit
   // carries the parity of the write epoch (every epoch rewrites every word)
   uint32_t* xb;    // [kMaxRows][H]      residual stream (parity 0 after O, 1 after down)
-  uint32_t* qkvb;  // [kMaxRows][nqkv]   q | k | v (fused path: q, k after norm gain and RoPE, unscaled)
-  uint32_t* qkss;  // [kMaxRows][nq + nkv][8] fused path: partial sums of squares of raw q, k (8 parts a head)
+  uint32_t* qkvb;  // [kMaxRows][nqkv]   q | k | v
   uint32_t* attnb; // [kMaxRows][qdim]   attention output
   uint32_t* actb;  // [kMaxRows][F]      SiLU(gate) * up
   uint32_t* pass_count;  // passes run by this stream so far (0xffffffff: poisoned by an error)
@@ -76,14 +75,8 @@ struct FrameArgs {
 };
 
 // Host entry into the kernel translation unit. gp: KParams in device memory.
-// mode 0: separate attention phase, fp32 KV cache; 2: (cfg kv_fp16) attention fused into the
-// O projection with an fp16 KV cache, the QKV producers applying the q/k norm gains and RoPE
-// (bf16, 16 q / 8 kv heads of 128, 16 q/k/v rows per workgroup, <= 5 rows per pass)
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, int mode, void* stream,
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream,
                  size_t lds_bytes, char* err, size_t errlen);
-// floats after the work area used by the fused attention path: fp16 KV cache of one
-// layer (kv heads x 16 positions x 128 x 2 halves) and the O rows' residual values
-inline int fused_extra_floats(int nkv, int mr) { return nkv * kMaxPos * 128 + mr * 32; }
 int frame_lds_head_floats(int mr, int cpw);
 int frame_max_rows(int K);
 
