@@ -127,8 +127,11 @@ void rvqsd_destroy(rvqsd_model* m);
 rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out);
 
 /* Create a decode stream on a caller-owned hipStream_t (borrowed, never
- * destroyed; NULL = the null stream). max_streams is the number of
- * independent frame streams decoded together and must be 1 in this version.
+ * destroyed; NULL = the null stream). max_streams (1..16) is the number of
+ * independent frame streams the batched calls below decode together; with 1
+ * only the single-frame calls are available. Batched streams need bf16
+ * weights, max_streams * max(draft_len + 1, 2) <= 80 rows, hidden a multiple
+ * of 256 and q width and ffn multiples of 128 (else EUNSUPPORTED).
  * A stream owns its device work buffers and pinned staging; use one host
  * thread per stream. */
 rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, rvqsd_stream** out);
@@ -152,6 +155,34 @@ rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, in
  * Inputs must stay valid until the stream reaches the frame. */
 rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidden, const int32_t* d_c0,
                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats);
+
+/* Decode n independent frames with max_streams of them in flight (the
+ * multi-stream verification of a batch of utterances; each frame is the same
+ * problem as rvqsd_decode_frame_u). Frame f runs in lane f % max_streams after
+ * frame f - max_streams of that lane; every pass verifies the rows of all
+ * lanes at once, so each projection streams its weights once for up to 80 rows
+ * and the LM heads serve every lane whose rows need them (Sec. 2.2 applied per
+ * lane). Host arrays: frame_hidden float[n][hidden], c0 int32[n], uniforms
+ * float[n][n_codes][3]; outputs out_codes int32[n][n_codes], out_stats
+ * rvqsd_stats[n] (nullable; weight_bytes = the bytes the frame's passes would
+ * read alone). Synchronous. EINVAL for a bad c0, uniform or non-finite input
+ * (nothing decoded); device errors: the first frame status that is not OK. */
+rvqsd_status rvqsd_decode_frames_batched(rvqsd_stream* s, int32_t n, const float* frame_hidden, const int32_t* c0,
+                                         const float* uniforms, int32_t* out_codes, rvqsd_stats* out_stats);
+
+/* Same with device pointers only (same layouts, d_stats required); returns
+ * after the launch. A frame whose c0 is out of range gets status EINVAL and
+ * codes -1; after a device-side error every frame not completed gets that
+ * error in its status and codes -1. Inputs must stay valid until the stream
+ * reaches the launch. */
+rvqsd_status rvqsd_decode_frames_batched_async(rvqsd_stream* s, int32_t n, const float* d_frame_hidden,
+                                               const int32_t* d_c0, const float* d_uniforms, int32_t* d_out_codes,
+                                               rvqsd_stats* d_stats);
+
+/* Passes run by the last batched call of the stream and their algorithmic
+ * bytes (layer weights and each LM head used, once per pass; gathered rows;
+ * KV cache read). Synchronises the stream. */
+rvqsd_status rvqsd_batch_totals(rvqsd_stream* s, uint64_t* passes, uint64_t* bytes);
 
 /* Return a stream to its initial state. Needed after a frame enqueued with
  * rvqsd_decode_frame_async reported a device-side error in its stats (later

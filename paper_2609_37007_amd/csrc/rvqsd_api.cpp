@@ -90,6 +90,15 @@ struct rvqsd_stream {
   uint32_t epoch_step;
   size_t par_begin, par_end;  // byte range of dbuf holding the parity-word buffers (pass count follows)
   size_t tag_begin, tag_end;  // byte range of dbuf holding the tagged words
+  // batched path (max_streams > 1)
+  int lanes;            // frame streams decoded together
+  void* bbuf;           // batched work buffers; the barrier, status and totals words come first
+  size_t bsync_bytes;   // bytes of those words (cleared before every launch)
+  BParams bp;           // host copy of the batched parameter block
+  BParams* dbp;         // device copy
+  size_t blds;          // dynamic LDS of the batched kernel
+  void* bstage;         // device staging of the synchronous batched call
+  size_t bstage_bytes;
 };
 
 namespace {
@@ -160,6 +169,99 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
   need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4));  // attention: q, k, v rows and the head's KV
   need((size_t)V + 2 * kMaxTopk + 2 + 2 * 3 * kMaxTopk + kMaxTopk + kTopkBuckets + 8);  // sampling
   return w;
+}
+
+// Largest k split of a projection (K columns, kw k parts per workgroup) that divides K into
+// 64-wide steps and keeps the units (column groups x splits) within one per workgroup.
+int pick_ks(int K, int kw, int colgroups, int nwg) {
+  const int steps = K / (kw * 64);
+  int best = 1;
+  for (int ks = 1; ks <= steps; ++ks)
+    if (steps % ks == 0 && colgroups * ks <= nwg) best = ks;
+  return best;
+}
+
+// Work buffers and parameter block of the batched kernel.
+int batch_setup(rvqsd_stream* s, int lanes) {
+  const rvqsd_model* m = s->m;
+  const KParams& k = s->kp;
+  const rvqsd_cfg& c = m->cfg;
+  const int rpl = c.draft_len + 1 < 2 ? 2 : c.draft_len + 1;
+  const int M = lanes * rpl;
+  if (c.dtype != RVQSD_DTYPE_BF16) return set_err(RVQSD_EUNSUPPORTED, "batched streams need bf16 weights");
+  if (M > kBatchMaxRows)
+    return set_err(RVQSD_EUNSUPPORTED, "max_streams * max(draft_len + 1, 2) = %d rows > %d", M, kBatchMaxRows);
+  if (k.H % 256 || k.qdim % 128 || k.F % 128)
+    return set_err(RVQSD_EUNSUPPORTED, "batched streams need hidden %% 256 == 0, q width and ffn %% 128 == 0");
+  if (m->nwg < 8) return set_err(RVQSD_EUNSUPPORTED, "batched streams need at least 8 workgroups");
+  BParams b;
+  memset(&b, 0, sizeof(b));
+  b.lanes = lanes;
+  b.rpl = rpl;
+  b.M = M;
+  b.nwg = m->nwg;
+  b.ks_qkv = pick_ks(k.H, 2, (k.nqkv + 63) / 64, m->nwg);
+  b.ks_o = pick_ks(k.qdim, 2, (k.H + 63) / 64, m->nwg);
+  b.ks_down = pick_ks(k.F, 2, (k.H + 63) / 64, m->nwg);
+  b.hrows = M * (k.K + 1);
+  b.sup_words = 1 + 2 * k.topk;
+  const size_t kmax = (size_t)(k.H > k.qdim ? (k.H > k.F ? k.H : k.F) : (k.qdim > k.F ? k.qdim : k.F));
+  size_t part = (size_t)b.ks_qkv * M * k.nqkv;
+  if ((size_t)b.ks_o * M * k.H > part) part = (size_t)b.ks_o * M * k.H;
+  if ((size_t)b.ks_down * M * k.H > part) part = (size_t)b.ks_down * M * k.H;
+  const int kd = k.K > 0 ? k.K : 1;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return at;
+  };
+  const size_t o_bar = take(10 * 64 * 4), o_status = take(4), o_tot = take(16);
+  const size_t sync_bytes = off;
+  const size_t o_lane = take((size_t)lanes * kLaneInts * 4), o_x = take((size_t)M * k.H * 4),
+               o_a = take(2 * (size_t)M * kmax * 4), o_ah = take((size_t)b.hrows * k.H * 4),
+               o_part = take(part * 4), o_kv = take((size_t)lanes * k.L * k.nkv * kMaxPos * 2 * k.d * 4),
+               o_log = take((size_t)b.hrows * k.V * 4), o_vres = take((size_t)lanes * rpl * 4),
+               o_drec = take((size_t)2 * lanes * rpl * kd * b.sup_words * 8), o_bp = take(sizeof(BParams));
+  hipError_t e = dev_alloc(&s->bbuf, off);
+  if (e != hipSuccess) {
+    s->bbuf = nullptr;
+    return set_err(RVQSD_ENOMEM, "batched buffers (%zu bytes): %s", off, hipGetErrorString(e));
+  }
+  uint8_t* base = (uint8_t*)s->bbuf;
+  b.k = s->dkp;
+  b.bar = (uint32_t*)(base + o_bar);
+  b.status = (int32_t*)(base + o_status);
+  b.totals = (unsigned long long*)(base + o_tot);
+  b.lane = (int32_t*)(base + o_lane);
+  b.x = (float*)(base + o_x);
+  b.a = (uint32_t*)(base + o_a);
+  b.ah = (uint32_t*)(base + o_ah);
+  b.part = (float*)(base + o_part);
+  b.kv = (float*)(base + o_kv);
+  b.logits = (float*)(base + o_log);
+  b.vres = (int32_t*)(base + o_vres);
+  b.drec = (uint64_t*)(base + o_drec);
+  s->dbp = (BParams*)(base + o_bp);
+  s->bp = b;
+  s->bsync_bytes = sync_bytes;
+  s->lanes = lanes;
+  e = hipMemset(s->bbuf, 0, off);
+  if (e == hipSuccess) e = hipMemcpy(s->dbp, &s->bp, sizeof(BParams), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(s->bbuf);
+    s->bbuf = nullptr;
+    return set_err(RVQSD_EHIP, "batched buffers: %s", hipGetErrorString(e));
+  }
+  // LDS: projection tiles and the SiLU staging, attention rows, sampling arrays, one row
+  size_t lds = ((size_t)kWaves * kBatchMTiles * 256 + (size_t)kBatchMaxRows * 16) * 4;
+  const size_t attn = (size_t)(2 * kMaxRows + 2 * kMaxPos) * k.d * 4;
+  const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + 3 * kMaxTopk * 8 + kMaxTopk * 4 + kTopkBuckets * 4;
+  if (attn > lds) lds = attn;
+  if (samp > lds) lds = samp;
+  if ((size_t)k.H * 4 > lds) lds = (size_t)k.H * 4;
+  s->blds = lds + 64;
+  return RVQSD_OK;
 }
 
 }  // namespace
@@ -336,7 +438,7 @@ rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out) {
 
 rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, rvqsd_stream** out) {
   if (!m || !out) return set_err(RVQSD_EINVAL, "null argument");
-  if (max_streams != 1) return set_err(RVQSD_EUNSUPPORTED, "max_streams must be 1");
+  if (max_streams < 1 || max_streams > kMaxLanes) return set_err(RVQSD_EINVAL, "max_streams must be 1..%d", kMaxLanes);
   *out = nullptr;
   rvqsd_stream* s = new (std::nothrow) rvqsd_stream;
   if (!s) return set_err(RVQSD_ENOMEM, "host allocation");
@@ -430,6 +532,17 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
   const int tags_per_frame = kMaxPos * phases_per_pass(k.L) + 2;
   s->epoch_step = (uint32_t)((tags_per_frame + 4095) & ~4095);
   s->epoch = s->epoch_step;
+  s->lanes = 1;
+  if (max_streams > 1) {
+    const int st = batch_setup(s, max_streams);
+    if (st != RVQSD_OK) {
+      (void)hipHostFree(s->h_in);
+      (void)hipHostFree(s->h_out);
+      (void)hipFree(s->dbuf);
+      delete s;
+      return st;
+    }
+  }
   *out = s;
   return RVQSD_OK;
 }
@@ -440,6 +553,8 @@ void rvqsd_stream_destroy(rvqsd_stream* s) {
   (void)hipHostFree(s->h_in);
   (void)hipHostFree(s->h_out);
   (void)hipFree(s->dbuf);
+  if (s->bbuf) (void)hipFree(s->bbuf);
+  if (s->bstage) (void)hipFree(s->bstage);
   delete s;
 }
 
@@ -531,6 +646,95 @@ rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, in
   }
   memcpy(out_codes, s->h_out, (size_t)n * 4);
   if (out_stats) *out_stats = hs;
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_decode_frames_batched_async(rvqsd_stream* s, int32_t n, const float* d_frame_hidden,
+                                               const int32_t* d_c0, const float* d_uniforms, int32_t* d_out_codes,
+                                               rvqsd_stats* d_stats) {
+  if (!s) return set_err(RVQSD_EINVAL, "null stream");
+  if (n < 0) return set_err(RVQSD_EINVAL, "n = %d < 0", n);
+  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  if (n == 0) return RVQSD_OK;
+  if (!d_frame_hidden || !d_c0 || !d_uniforms || !d_out_codes || !d_stats) return set_err(RVQSD_EINVAL, "null argument");
+  HIPCHK(hipMemsetAsync(s->bbuf, 0, s->bsync_bytes, s->stream));
+  BCall call;
+  call.frame_hidden = d_frame_hidden;
+  call.c0 = d_c0;
+  call.uniforms = d_uniforms;
+  call.out_codes = d_out_codes;
+  call.out_stats = d_stats;
+  call.n = n;
+  char err[256];
+  const int st = launch_batch(s->dbp, call, s->m->nwg, (void*)s->stream, s->blds, err, sizeof(err));
+  if (st) return set_err(st, "%s", err);
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_decode_frames_batched(rvqsd_stream* s, int32_t n, const float* frame_hidden, const int32_t* c0,
+                                         const float* uniforms, int32_t* out_codes, rvqsd_stats* out_stats) {
+  if (!s) return set_err(RVQSD_EINVAL, "null stream");
+  if (n < 0) return set_err(RVQSD_EINVAL, "n = %d < 0", n);
+  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  if (n == 0) return RVQSD_OK;
+  if (!frame_hidden || !c0 || !uniforms || !out_codes) return set_err(RVQSD_EINVAL, "null argument");
+  const rvqsd_cfg& c = s->m->cfg;
+  const int H = c.hidden, nc = c.n_codes;
+  for (int f = 0; f < n; ++f)
+    if (c0[f] < 0 || c0[f] >= c.vocab) return set_err(RVQSD_EINVAL, "c0[%d] = %d outside [0, %d)", f, c0[f], c.vocab);
+  for (size_t i = 0; i < (size_t)n * 3 * nc; ++i)
+    if (!(uniforms[i] >= 0.f && uniforms[i] < 1.f)) return set_err(RVQSD_EINVAL, "uniform %zu outside [0, 1)", i);
+  for (size_t i = 0; i < (size_t)n * H; ++i)
+    if (!std::isfinite(frame_hidden[i])) return set_err(RVQSD_EINVAL, "frame_hidden[%zu] is not finite", i);
+  // device staging: hidden [n][H] | uniforms [n][3 nc] | c0 [n] | codes [n][nc] | stats [n]
+  const size_t b_h = (size_t)n * H * 4, b_u = (size_t)n * 3 * nc * 4, b_c = (size_t)n * 4, b_o = (size_t)n * nc * 4;
+  const size_t o_u = (b_h + 255) & ~(size_t)255, o_c = o_u + ((b_u + 255) & ~(size_t)255),
+               o_o = o_c + ((b_c + 255) & ~(size_t)255), o_s = o_o + ((b_o + 255) & ~(size_t)255),
+               need = o_s + (size_t)n * sizeof(rvqsd_stats);
+  if (need > s->bstage_bytes) {
+    if (s->bstage) (void)hipFree(s->bstage);
+    s->bstage = nullptr;
+    s->bstage_bytes = 0;
+    hipError_t e = dev_alloc(&s->bstage, need);
+    if (e != hipSuccess) {
+      s->bstage = nullptr;
+      return set_err(RVQSD_ENOMEM, "batched staging (%zu bytes): %s", need, hipGetErrorString(e));
+    }
+    s->bstage_bytes = need;
+  }
+  uint8_t* d = (uint8_t*)s->bstage;
+  HIPCHK(hipMemcpyAsync(d, frame_hidden, b_h, hipMemcpyHostToDevice, s->stream));
+  HIPCHK(hipMemcpyAsync(d + o_u, uniforms, b_u, hipMemcpyHostToDevice, s->stream));
+  HIPCHK(hipMemcpyAsync(d + o_c, c0, b_c, hipMemcpyHostToDevice, s->stream));
+  int st = rvqsd_decode_frames_batched_async(s, n, (const float*)d, (const int32_t*)(d + o_c), (const float*)(d + o_u),
+                                             (int32_t*)(d + o_o), (rvqsd_stats*)(d + o_s));
+  if (st) return st;
+  HIPCHK(hipMemcpyAsync(out_codes, d + o_o, b_o, hipMemcpyDeviceToHost, s->stream));
+  rvqsd_stats* hs = out_stats;
+  rvqsd_stats* tmp = nullptr;
+  if (!hs) {
+    tmp = (rvqsd_stats*)malloc((size_t)n * sizeof(rvqsd_stats));
+    if (!tmp) return set_err(RVQSD_ENOMEM, "host allocation");
+    hs = tmp;
+  }
+  hipError_t e = hipMemcpyAsync(hs, d + o_s, (size_t)n * sizeof(rvqsd_stats), hipMemcpyDeviceToHost, s->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+  int dev = RVQSD_OK;
+  for (int f = 0; e == hipSuccess && f < n && dev == RVQSD_OK; ++f) dev = hs[f].status;
+  free(tmp);
+  if (e != hipSuccess) return set_err(RVQSD_EHIP, "batched decode: %s", hipGetErrorString(e));
+  if (dev != RVQSD_OK) return set_err(dev, "device reported %s", rvqsd_status_str(dev));
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_batch_totals(rvqsd_stream* s, uint64_t* passes, uint64_t* bytes) {
+  if (!s || !passes || !bytes) return set_err(RVQSD_EINVAL, "null argument");
+  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  unsigned long long t[2];
+  HIPCHK(hipStreamSynchronize(s->stream));
+  HIPCHK(hipMemcpy(t, s->bp.totals, sizeof(t), hipMemcpyDeviceToHost));
+  *passes = t[0];
+  *bytes = t[1];
   return RVQSD_OK;
 }
 

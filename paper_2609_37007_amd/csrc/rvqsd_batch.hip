@@ -1,0 +1,920 @@
+// rvqsd_batch.hip -- batched verification kernel (gfx950): several independent
+// frame streams ("lanes") decoded together, every pass verifying all their
+// rows at once.
+//
+// The speculative round of each lane is the one of the single-stream kernel
+// (paper Sec. 2.2: offset drafts from the anchor's hidden state, one K+1-row
+// verification pass with a KV cache, top-k rejection sampling with residual
+// resampling). What changes is the shape: lane i owns rows i * rpl .. i * rpl +
+// rpl - 1 of a pass, so every projection multiplies M = lanes * rpl <= 80
+// activation rows by the weights it streams once, on MFMA tiles (five 16-row
+// tiles), and the LM heads group the rows of all lanes that need the same
+// per-position head.
+//
+// One cooperative launch runs every frame of the call. Lane i decodes frames
+// i, i + lanes, i + 2 lanes, ...; when its frame completes it writes the codes
+// and starts the next one in the same round, so lanes stay busy until their
+// frames run out. Each round is a fixed chain of phases separated by a grid
+// barrier:
+//   commit + row setup (lane workgroups) | per layer: QKV, attention, O,
+//   residual + norm, gate/up (SiLU * up fused), down, residual + norm |
+//   LM heads | top-k / softmax / draft / accept-or-resample.
+// Data crossing workgroups moves through device-coherent (sc1) loads and
+// stores; the barrier waits for this workgroup's stores to complete, so no
+// cache-wide fence is needed. Every wait is bounded: a workgroup that times
+// out records RVQSD_ETIMEOUT in the status word and every other one leaves at
+// its next barrier.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "rvqsd_device.h"
+#include "rvqsd_internal.h"
+
+namespace rvqsd {
+
+namespace {
+
+// ------------------------------------------------------------ memory helpers
+
+__device__ __forceinline__ uint32_t cld32(const void* p) {
+  return __hip_atomic_load(G(reinterpret_cast<const uint32_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t cld64(const void* p) {
+  return __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void cst32(void* p, uint32_t v) {
+  __hip_atomic_store(G(reinterpret_cast<uint32_t*>(p)), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void cst64(void* p, uint64_t v) {
+  __hip_atomic_store(G(reinterpret_cast<uint64_t*>(p)), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float cldf(const float* p) { return __uint_as_float(cld32(p)); }
+__device__ __forceinline__ void cstf(float* p, float v) { cst32(p, __float_as_uint(v)); }
+
+// 8 activations -> one split chunk (4 words bf16 hi, 4 words bf16 lo) at dst
+__device__ __forceinline__ void store_split(uint32_t* dst, const float (&x)[8]) {
+  W16 hi, lo;
+  split8(x, hi, lo);
+  cst64(dst + 0, (uint64_t)hi[0] | ((uint64_t)hi[1] << 32));
+  cst64(dst + 2, (uint64_t)hi[2] | ((uint64_t)hi[3] << 32));
+  cst64(dst + 4, (uint64_t)lo[0] | ((uint64_t)lo[1] << 32));
+  cst64(dst + 6, (uint64_t)lo[2] | ((uint64_t)lo[3] << 32));
+}
+__device__ __forceinline__ W16 load_w16c(const uint32_t* p) {
+  const uint64_t a = cld64(p), b = cld64(p + 2);
+  W16 r;
+  r[0] = (uint32_t)a;
+  r[1] = (uint32_t)(a >> 32);
+  r[2] = (uint32_t)b;
+  r[3] = (uint32_t)(b >> 32);
+  return r;
+}
+
+__device__ __forceinline__ const bf16_t* bw(const KParams* p, uint64_t off) {
+  return reinterpret_cast<const bf16_t*>(p->wbase + off);
+}
+__device__ __forceinline__ const float* bfw(const KParams* p, uint64_t off) {
+  return reinterpret_cast<const float*>(p->wbase + off);
+}
+__device__ __forceinline__ uint64_t boff(const KParams* p, int l, uint64_t o) { return (uint64_t)l * p->layer_stride + o; }
+
+__device__ __forceinline__ void raise_status(const BParams* bp, int code) {
+  int expected = 0;
+  __hip_atomic_compare_exchange_strong(G(bp->status), &expected, code, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------------ shared state
+
+struct BShared {
+  TopkShared tk;
+  int ln[kMaxLanes][kLaneInts];  // every lane's state, read at the start of the round
+  int abort;
+  int hl_n, hl_t;                // LM-head row list of the current unit
+  int hl_row[kBatchMaxRows];
+  float red[kWaves];
+  int vr[kMaxRows];              // commit: verdicts of the lane's rows
+  int dt[kMaxRows][kMaxCodes];   // commit: draft tokens of every row of the lane
+  int tok;
+};
+
+// ------------------------------------------------------------ grid barrier
+// Arrival counts per XCD group (workgroup w is counted in group w % 8), the
+// last arrival of a group bumps the top counter, the last group publishes the
+// generation. Before arriving, every wave waits for its own stores.
+__device__ bool grid_sync(const BParams* bp, uint32_t& gen, BShared* sh) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  ++gen;
+  if (tid() == 0) {
+    const int nwg = bp->nwg, x = (int)blockIdx.x & 7;
+    const uint32_t nx = (uint32_t)((nwg - x + 7) / 8);
+    uint32_t* bar = bp->bar;
+    const uint32_t prev = __hip_atomic_fetch_add(G(bar + 64 * (1 + x)), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev + 1 == gen * nx) {
+      const uint32_t p2 = __hip_atomic_fetch_add(G(bar), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (p2 + 1 == gen * 8u) cst32(bar + 64 * 9, gen);
+    }
+    int ab = 0, spins = 0;
+    uint64_t t0 = 0;
+    while (cld32(bar + 64 * 9) < gen) {
+      __builtin_amdgcn_s_sleep(1);
+      if ((++spins & 31) == 0) {
+        if (cld32(bp->status) != 0) {
+          ab = 1;
+          break;
+        }
+        const uint64_t now = dclock();
+        if (t0 == 0) {
+          t0 = now;
+        } else if (now - t0 > kTimeoutTicks) {
+          raise_status(bp, RVQSD_ETIMEOUT);
+          ab = 1;
+          break;
+        }
+      }
+    }
+    if (!ab && cld32(bp->status) != 0) ab = 1;
+    sh->abort = ab;
+  }
+  __syncthreads();
+  return sh->abort == 0;
+}
+
+// ------------------------------------------------------------ block helpers
+
+__device__ __forceinline__ float block_sum(BShared* sh, float v) {
+  v = wave_sum(v);
+  const int lane = tid() & 63, wave = tid() >> 6;
+  if (lane == 0) sh->red[wave] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) t += sh->red[w];
+  __syncthreads();
+  return t;
+}
+
+// ------------------------------------------------------------ pass geometry
+
+__device__ __forceinline__ bool row_is_verify(const int* st, int r) {
+  return r < st[kLnRows] && st[kLnFirst] + r >= 1 && (st[kLnPass] == 0 ? r == 1 : true);
+}
+__device__ __forceinline__ int row_drafts(const KParams* p, const int* st, int r) {
+  const int s = st[kLnFirst] + r;
+  if (r >= st[kLnRows] || s < 1 || s > p->n_codes - 1) return 0;
+  if (st[kLnPass] == 0 && r != 1) return 0;
+  return min(p->K, p->n_codes - s);
+}
+// LM-head input row of (lane row i, offset j) and whether it is used this pass
+__device__ __forceinline__ bool head_slot_used(const KParams* p, const int* st, int r, int j) {
+  if (!st[kLnActive]) return false;
+  return j == 0 ? row_is_verify(st, r) : j <= row_drafts(p, st, r);
+}
+
+// ------------------------------------------------------------ MFMA tile unit
+// Output features n0 .. n0 + 16 NTU - 1 (weight rows wrow(nt, m) of n-tile nt,
+// nullptr when outside the matrix) over k in [k0, k0 + klen), for the
+// activation rows rowof(i), i < 16 * mtiles (-1: padding). Wave w takes n-tile
+// w % NTU and the k part w / NTU; the KW = 8 / NTU parts are added in LDS in a
+// fixed order. On return red[(nt * kBatchMTiles + mt) * 256 + 4 * lane + v]
+// holds D[feature 16 nt + 4 (lane / 16) + v][row 16 mt + lane % 16].
+// MFMA roles as in the frame kernel: A = 16 weight rows, B = 16 activation
+// rows; lane group q = lane / 16 covers the 16 consecutive k of a 64-wide step
+// in two instructions, and the activation chunk of 8 enters as bf16 hi + lo.
+template <int NTU, typename WRow, typename RowOf>
+__device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uint32_t* A, int lda, int mtiles,
+                                          RowOf rowof, float* red) {
+  constexpr int KW = kWaves / NTU;
+  const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6), lane = tid() & 63;
+  const int nt = wave % NTU, kw = wave / NTU;
+  const int kper = klen / KW;
+  const int kb = k0 + kw * kper;
+  const int q = lane >> 4, ml = lane & 15;
+  const bf16_t* wr = wrow(nt, ml);
+  const bf16_t* wp = wr ? wr + kb + 16 * q : nullptr;
+  int arow[kBatchMTiles];
+#pragma unroll
+  for (int mt = 0; mt < kBatchMTiles; ++mt) arow[mt] = mt < mtiles ? rowof(16 * mt + ml) : -1;
+  f32x4 acc[kBatchMTiles];
+#pragma unroll
+  for (int mt = 0; mt < kBatchMTiles; ++mt) acc[mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  const int nsteps = kper >> 6;
+  for (int u = 0; u < nsteps; ++u) {
+    W16 a0 = (W16)(0u), a1 = (W16)(0u);
+    if (wp) {
+      a0 = *G(reinterpret_cast<const W16*>(wp + 64 * u));
+      a1 = *G(reinterpret_cast<const W16*>(wp + 64 * u + 8));
+    }
+    const int chunk = (kb + 64 * u + 16 * q) >> 3;
+    W16 bh0[kBatchMTiles], bl0[kBatchMTiles], bh1[kBatchMTiles], bl1[kBatchMTiles];
+#pragma unroll
+    for (int mt = 0; mt < kBatchMTiles; ++mt) {
+      bh0[mt] = bl0[mt] = bh1[mt] = bl1[mt] = (W16)(0u);
+      if (mt < mtiles && arow[mt] >= 0) {
+        const uint32_t* ap = A + (size_t)arow[mt] * lda + (size_t)chunk * 8;
+        bh0[mt] = load_w16c(ap);
+        bl0[mt] = load_w16c(ap + 4);
+        bh1[mt] = load_w16c(ap + 8);
+        bl1[mt] = load_w16c(ap + 12);
+      }
+    }
+    const bf16x8 x0 = __builtin_bit_cast(bf16x8, a0), x1 = __builtin_bit_cast(bf16x8, a1);
+#pragma unroll
+    for (int mt = 0; mt < kBatchMTiles; ++mt) {
+      if (mt < mtiles) {
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bh0[mt]), acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bl0[mt]), acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bh1[mt]), acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bl1[mt]), acc[mt], 0, 0, 0);
+      }
+    }
+  }
+#pragma unroll
+  for (int mt = 0; mt < kBatchMTiles; ++mt)
+    if (mt < mtiles)
+      *reinterpret_cast<f32x4*>(red + ((size_t)((kw * NTU + nt) * kBatchMTiles + mt) << 8) + 4 * lane) = acc[mt];
+  __syncthreads();
+  if (KW > 1) {
+    for (int e = tid(); e < NTU * mtiles * 256; e += kThreads) {
+      const int t = e / (mtiles * 256), rem = e - t * (mtiles * 256), mt = rem >> 8, x = rem & 255;
+      float s = red[((size_t)(t * kBatchMTiles + mt) << 8) + x];
+#pragma unroll
+      for (int k = 1; k < KW; ++k) s += red[((size_t)((k * NTU + t) * kBatchMTiles + mt) << 8) + x];
+      red[((size_t)(t * kBatchMTiles + mt) << 8) + x] = s;
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------ projections
+
+// Y partial sums: part[ks][i][n] = sum over k in split ks of A[i][k] W[n][k], for every row i < M.
+template <int NTU>
+__device__ void proj_partial(const BParams* bp, const bf16_t* W, int N, int K, int KS, const uint32_t* A, float* red) {
+  const int M = bp->M, mtiles = (M + 15) >> 4;
+  const int cg = (N + 16 * NTU - 1) / (16 * NTU), units = cg * KS, klen = K / KS;
+  float* part = bp->part;
+  for (int u = blockIdx.x; u < units; u += bp->nwg) {
+    const int g = u % cg, ks = u / cg, n0 = g * 16 * NTU;
+    gemm_unit<NTU>(
+        [&](int nt, int m) -> const bf16_t* {
+          const int f = n0 + 16 * nt + m;
+          return f < N ? W + (size_t)f * K : nullptr;
+        },
+        ks * klen, klen, A, K, mtiles, [&](int i) { return i < M ? i : -1; }, red);
+    for (int e = tid(); e < NTU * mtiles * 64; e += kThreads) {
+      const int nt = e / (mtiles * 64), rem = e - nt * (mtiles * 64), mt = rem >> 6, ln = rem & 63;
+      const int row = 16 * mt + (ln & 15), f = n0 + 16 * nt + 4 * (ln >> 4);
+      if (row < M && f < N) {
+        const float* s = red + ((size_t)(nt * kBatchMTiles + mt) << 8) + 4 * ln;
+        float* dst = part + ((size_t)ks * M + row) * N + f;
+        cst64(dst, (uint64_t)__float_as_uint(s[0]) | ((uint64_t)__float_as_uint(s[1]) << 32));
+        cst64(dst + 2, (uint64_t)__float_as_uint(s[2]) | ((uint64_t)__float_as_uint(s[3]) << 32));
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// gate/up: n-tile 0 = gate rows f0 .. f0 + 15, n-tile 1 = the same up rows, full k;
+// act = SiLU(gate) * up goes straight to the split input of the down projection.
+__device__ void phase_gu(const BParams* bp, int l, const uint32_t* A, uint32_t* Aout, float* red) {
+  const KParams* p = bp->k;
+  const int M = bp->M, mtiles = (M + 15) >> 4, H = p->H, F = p->F;
+  const bf16_t* wg = bw(p, boff(p, l, p->o_wg));
+  const bf16_t* wu = bw(p, boff(p, l, p->o_wu));
+  float* act = red + (size_t)kWaves * kBatchMTiles * 256;  // [80][16]
+  for (int u = blockIdx.x; u < F / 16; u += bp->nwg) {
+    const int f0 = u * 16;
+    gemm_unit<2>([&](int nt, int m) -> const bf16_t* { return (nt ? wu : wg) + (size_t)(f0 + m) * H; }, 0, H, A, H,
+                 mtiles, [&](int i) { return i < M ? i : -1; }, red);
+    for (int e = tid(); e < mtiles * 256; e += kThreads) {
+      const int mt = e >> 8, x = e & 255, ln = x >> 2, v = x & 3;
+      const float gt = red[((size_t)(0 * kBatchMTiles + mt) << 8) + x];
+      const float up = red[((size_t)(1 * kBatchMTiles + mt) << 8) + x];
+      act[(16 * mt + (ln & 15)) * 16 + 4 * (ln >> 4) + v] = gt / (1.f + expf(-gt)) * up;
+    }
+    __syncthreads();
+    for (int c = tid(); c < 2 * M; c += kThreads) {
+      const int row = c >> 1, h8 = c & 1;
+      float x8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x8[e] = act[row * 16 + 8 * h8 + e];
+      store_split(Aout + (size_t)row * F + f0 + 8 * h8, x8);
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------ attention
+// Unit (lane, q head h): q, k, v of the lane's rows from the QKV partial sums,
+// per-head RMSNorm and rotate-half RoPE, KV append (first q head of each kv
+// group), causal softmax attention over positions 0 .. s, output split into the
+// O projection's input.
+__device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout, float* lds) {
+  const KParams* p = bp->k;
+  const int d = p->d, nq = p->nq, grp = nq / p->nkv, N = p->nqkv, KS = bp->ks_qkv, M = bp->M, half = d / 2;
+  const int qdim = p->qdim, kvdim = p->kvdim, lane = tid() & 63, wave = tid() >> 6;
+  const float scale = 1.f / sqrtf((float)d);
+  float* qs = lds;                       // [kMaxRows][d]
+  float* kvs = qs + kMaxRows * d;        // [kMaxPos][2][d]
+  float* os = kvs + kMaxPos * 2 * d;     // [kMaxRows][d]
+  const float* qn = bfw(p, boff(p, l, p->o_qn));
+  const float* kn = bfw(p, boff(p, l, p->o_kn));
+  for (int u = blockIdx.x; u < bp->lanes * nq; u += bp->nwg) {
+    const int ln = u / nq, h = u - ln * nq, g = h / grp;
+    const int* st = sh->ln[ln];
+    if (!st[kLnActive]) continue;
+    const int fp = st[kLnFirst], R = st[kLnRows], row0 = ln * bp->rpl;
+    float* kvc = bp->kv + (((size_t)ln * p->L + l) * p->nkv + g) * kMaxPos * 2 * d;
+    for (int e = tid(); e < R * 3 * d; e += kThreads) {
+      const int r = e / (3 * d), w = e - r * 3 * d, part = w / d, i = w - part * d;
+      const int col = part == 0 ? h * d + i : qdim + (part - 1) * kvdim + g * d + i;
+      const float* src = bp->part + (size_t)(row0 + r) * N + col;
+      float s = 0.f;
+      for (int ks = 0; ks < KS; ++ks) s += cldf(src + (size_t)ks * M * N);
+      if (part == 0) qs[r * d + i] = s;
+      else kvs[(size_t)(fp + r) * 2 * d + (part - 1) * d + i] = s;
+    }
+    for (int e = tid(); e < fp * 2 * d; e += kThreads) kvs[e] = cldf(kvc + e);
+    __syncthreads();
+    // q rows (v < R) and k rows (v >= R): norm + RoPE, one wave per vector
+    for (int v = wave; v < 2 * R; v += kWaves) {
+      const bool isq = v < R;
+      const int r = isq ? v : v - R, pos = fp + r;
+      float* x = isq ? qs + r * d : kvs + (size_t)pos * 2 * d;
+      const float* gn = isq ? qn : kn;
+      float ss = 0.f;
+      for (int i = lane; i < d; i += 64) ss = fmaf(x[i], x[i], ss);
+      ss = wave_sum(ss);
+      const float rs = p->qk_norm ? 1.f / sqrtf(ss / (float)d + p->rms_eps) : 1.f;
+      for (int i = lane; i < half; i += 64) {
+        float a = x[i], b = x[i + half];
+        if (p->qk_norm) {
+          a = a * rs * G(gn)[i];
+          b = b * rs * G(gn)[i + half];
+        }
+        const float cs = G(p->rope)[(pos * half + i) * 2], sn = G(p->rope)[(pos * half + i) * 2 + 1];
+        x[i] = a * cs - b * sn;
+        x[i + half] = b * cs + a * sn;
+      }
+    }
+    __syncthreads();
+    if (h % grp == 0)
+      for (int e = tid(); e < R * 2 * d; e += kThreads) cstf(kvc + (size_t)fp * 2 * d + e, kvs[(size_t)fp * 2 * d + e]);
+    for (int r = wave; r < R; r += kWaves) {
+      const int s = fp + r;
+      float sc[kMaxPos];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < kMaxPos; ++t) {
+        sc[t] = -INFINITY;
+        if (t <= s) {
+          float a = 0.f;
+          for (int i = lane; i < d; i += 64) a = fmaf(qs[r * d + i], kvs[(size_t)t * 2 * d + i], a);
+          sc[t] = wave_sum(a) * scale;
+          mx = fmaxf(mx, sc[t]);
+        }
+      }
+      float z = 0.f;
+#pragma unroll
+      for (int t = 0; t < kMaxPos; ++t) {
+        sc[t] = t <= s ? expf(sc[t] - mx) : 0.f;
+        z += sc[t];
+      }
+      const float iz = 1.f / z;
+      for (int i = lane; i < d; i += 64) {
+        float o = 0.f;
+#pragma unroll
+        for (int t = 0; t < kMaxPos; ++t)
+          if (t <= s) o = fmaf(sc[t], kvs[(size_t)t * 2 * d + d + i], o);
+        os[r * d + i] = o * iz;
+      }
+    }
+    __syncthreads();
+    for (int c = tid(); c < R * (d / 8); c += kThreads) {
+      const int r = c / (d / 8), q8 = c - r * (d / 8);
+      float x8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x8[e] = os[r * d + 8 * q8 + e];
+      store_split(Aout + (size_t)(row0 + r) * qdim + h * d + 8 * q8, x8);
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------ residual + norm
+// Row i: x += sum of the KS partial sums of the projection just run, then the
+// next input: RMSNorm(x) * gain split into Aout (mode 0), or the final norm
+// h and the LM-head inputs h + b_j of the row's used slots (mode 1).
+__device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float* gain, uint32_t* Aout, int mode,
+                            float* xs) {
+  const KParams* p = bp->k;
+  const int H = p->H, M = bp->M, K = p->K;
+  for (int i = blockIdx.x; i < M; i += bp->nwg) {
+    const int ln = i / bp->rpl, r = i - ln * bp->rpl;
+    const int* st = sh->ln[ln];
+    if (!st[kLnActive] || r >= st[kLnRows]) continue;
+    float* x = bp->x + (size_t)i * H;
+    float ss = 0.f;
+    for (int e = tid(); e < H; e += kThreads) {
+      float v = cldf(x + e);
+      for (int ks = 0; ks < KS; ++ks) v += cldf(bp->part + ((size_t)ks * M + i) * H + e);
+      cstf(x + e, v);
+      xs[e] = v;
+      ss = fmaf(v, v, ss);
+    }
+    ss = block_sum(sh, ss);
+    const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
+    for (int c = tid(); c < H / 8; c += kThreads) {
+      float h8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h8[e] = xs[8 * c + e] * rs * G(gain)[8 * c + e];
+      if (mode == 0) {
+        store_split(Aout + (size_t)i * H + 8 * c, h8);
+      } else {
+        const float* ofs = bfw(p, p->o_offsets);
+        for (int j = 0; j <= K; ++j) {
+          if (!head_slot_used(p, st, r, j)) continue;
+          float y8[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) y8[e] = j == 0 ? h8[e] : h8[e] + G(ofs)[(size_t)(j - 1) * H + 8 * c + e];
+          store_split(bp->ah + ((size_t)i * (K + 1) + j) * H + 8 * c, y8);
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------ LM heads
+// Unit (head t, 64 vocabulary columns): every used slot (lane row, offset j)
+// whose position plus offset is t, i.e. the verify rows at position t and the
+// draft rows of distance j from it.
+__device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
+  const KParams* p = bp->k;
+  const int H = p->H, V = p->V, K = p->K, n = p->n_codes, rpl = bp->rpl;
+  const int cg = (V + 63) / 64, ncand = bp->lanes * rpl * (K + 1);
+  if (tid() == 0) sh->hl_t = -1;
+  __syncthreads();
+  for (int u = blockIdx.x; u < n * cg; u += bp->nwg) {
+    const int t = 1 + u / cg, gi = u % cg;
+    if (sh->hl_t != t) {
+      // row list of head t in candidate order
+      int cnt = 0;
+      for (int base = 0; base < ncand; base += kThreads) {
+        const int c = base + tid();
+        bool use = false;
+        if (c < ncand) {
+          const int ln = c / (rpl * (K + 1)), rem = c - ln * rpl * (K + 1), r = rem / (K + 1), j = rem - r * (K + 1);
+          const int* st = sh->ln[ln];
+          use = head_slot_used(p, st, r, j) && st[kLnFirst] + r + j == t;
+        }
+        int tot;
+        const int pos = block_excl_scan(&sh->tk, use ? 1 : 0, &tot);
+        if (use && cnt + pos < kBatchMaxRows) sh->hl_row[cnt + pos] = c;
+        cnt += tot;
+        __syncthreads();
+      }
+      if (tid() == 0) {
+        sh->hl_n = min(cnt, kBatchMaxRows);
+        sh->hl_t = t;
+        if (cnt > kBatchMaxRows) raise_status(bp, RVQSD_EUNSUPPORTED);
+      }
+      __syncthreads();
+    }
+    const int nr = sh->hl_n;
+    if (nr == 0) continue;
+    const int n0 = gi * 64;
+    const bf16_t* W = bw(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
+    gemm_unit<4>(
+        [&](int nt, int m) -> const bf16_t* {
+          const int f = n0 + 16 * nt + m;
+          return f < V ? W + (size_t)f * H : nullptr;
+        },
+        0, H, bp->ah, H, (nr + 15) >> 4, [&](int i) { return i < nr ? sh->hl_row[i] : -1; }, red);
+    for (int e = tid(); e < 4 * ((nr + 15) >> 4) * 256; e += kThreads) {
+      const int mtiles = (nr + 15) >> 4;
+      const int nt = e / (mtiles * 256), rem = e - nt * (mtiles * 256), mt = rem >> 8, x = rem & 255;
+      const int ln = x >> 2, v = x & 3;
+      const int i = 16 * mt + (ln & 15), f = n0 + 16 * nt + 4 * (ln >> 4) + v;
+      if (i < nr && f < V) cstf(bp->logits + (size_t)sh->hl_row[i] * V + f, red[((size_t)(nt * kBatchMTiles + mt) << 8) + x]);
+    }
+    __syncthreads();
+  }
+}
+
+// Algorithmic bytes of one batched pass: the layer weights and every LM head
+// some lane uses (each read once), the gathered embedding rows and the KV
+// cache every lane attends over.
+__device__ unsigned long long pass_bytes_batch(const BParams* bp, const BShared* sh) {
+  const KParams* p = bp->k;
+  unsigned long long b = (unsigned long long)p->L * p->layer_stride;
+  unsigned used = 0;  // bit t: head t used
+  for (int ln = 0; ln < bp->lanes; ++ln) {
+    const int* st = sh->ln[ln];
+    if (!st[kLnActive]) continue;
+    for (int r = 0; r < st[kLnRows]; ++r) {
+      const int s = st[kLnFirst] + r;
+      if (row_is_verify(st, r)) used |= 1u << s;
+      for (int j = 1; j <= row_drafts(p, st, r); ++j) used |= 1u << (s + j);
+      b += (s == 0) ? 4ull * p->H : 2ull * p->H;
+    }
+    b += (unsigned long long)p->L * (st[kLnFirst] + st[kLnRows]) * p->nkv * p->d * 2 * 4;
+  }
+  b += (unsigned long long)__popc(used) * p->table_stride;
+  return b;
+}
+
+// ------------------------------------------------------------ sampling
+// Slot (lane row r, offset j): top-k of its logits, tempered softmax in fp64,
+// then: j >= 1 -> draft d_{s+j} (inverse CDF at u_draft, or argmax) and its
+// proposal q, recorded for the next pass; j = 0 with a draft -> accept d iff
+// u_acc q(d) < p(d), else resample from max(0, p - q) at u_samp; j = 0
+// without a draft (prefix token, or the extra token after every draft was
+// accepted) -> sample p at u_samp. Verdict: token | accepted << 31.
+__device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, float* lds) {
+  const KParams* p = bp->k;
+  const int V = p->V, K = p->K, rpl = bp->rpl, n = p->n_codes, SW = bp->sup_words;
+  float* lg = lds;                                            // [V]
+  int* sidx = reinterpret_cast<int*>(lg + V);                 // [kMaxTopk]
+  float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);    // [kMaxTopk]
+  double* prob = reinterpret_cast<double*>(
+      (reinterpret_cast<uintptr_t>(slog + kMaxTopk) + 7) & ~(uintptr_t)7);  // [kMaxTopk]
+  double* qprob = prob + kMaxTopk;
+  double* res = qprob + kMaxTopk;
+  int* qidx = reinterpret_cast<int*>(res + kMaxTopk);         // [kMaxTopk]
+  unsigned* hist = reinterpret_cast<unsigned*>(qidx + kMaxTopk);  // [kTopkBuckets]
+  const int nslots = bp->lanes * rpl * (K + 1);
+  for (int u = blockIdx.x; u < nslots; u += bp->nwg) {
+    const int ln = u / (rpl * (K + 1)), rem = u - ln * rpl * (K + 1), r = rem / (K + 1), j = rem - r * (K + 1);
+    const int* st = sh->ln[ln];
+    if (!head_slot_used(p, st, r, j)) continue;
+    const int pass = st[kLnPass], s = st[kLnFirst] + r, t = s + j;
+    const float* U = call.uniforms + (size_t)st[kLnFrame] * n * 3;
+    const bool has_draft = j == 0 && pass > 0 && r + 1 <= st[kLnKp];
+    int nq = 0, dtok = -1;
+    if (has_draft) {
+      // q of d_t: drafted last pass from the anchor's row, offset r + 1
+      const uint64_t* rec = bp->drec + ((((size_t)((pass - 1) & 1) * bp->lanes + ln) * rpl + st[kLnPrevAnchor]) * K + r) * SW;
+      const uint64_t w0 = cld64(rec);
+      dtok = (int)(uint32_t)w0;
+      nq = (int)(w0 >> 32);
+      for (int i = tid(); i < nq; i += kThreads) {
+        qidx[i] = (int)(uint32_t)cld64(rec + 1 + i);
+        qprob[i] = __longlong_as_double((long long)cld64(rec + 1 + p->topk + i));
+      }
+    }
+    const float* src = bp->logits + (size_t)u * V;
+    for (int i = tid(); i < V; i += kThreads) lg[i] = cldf(src + i);
+    __syncthreads();
+    int ns = topk_buckets(&sh->tk, lg, V, p->topk, sidx, slog, hist);
+    if (ns < 0) ns = topk_select(&sh->tk, lg, V, p->topk, sidx, slog);
+    if (tid() < 64) {
+      bool fin = false;
+      for (int i = tid(); i < ns; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
+      if (!__any(fin) && tid() == 0) raise_status(bp, RVQSD_ENUMERIC);
+    }
+    softmax_support(slog, ns, p->temperature, prob);
+    __syncthreads();
+    if (j > 0) {
+      if (tid() < 64) {
+        int pos;
+        if (p->greedy) {
+          double best = -1.0;
+          int bi = ns;
+          for (int i = tid(); i < ns; i += 64)
+            if (prob[i] > best) { best = prob[i]; bi = i; }
+          for (int o = 32; o > 0; o >>= 1) {
+            const double ob = __shfl_xor(best, o, 64);
+            const int oi = __shfl_xor(bi, o, 64);
+            if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+          }
+          pos = bi;
+        } else {
+          pos = inverse_cdf(prob, ns, (double)U[(t - 1) * 3 + 0]);
+        }
+        if (tid() == 0) sh->tok = sidx[pos];
+      }
+      __syncthreads();
+      const int tok = sh->tok, nrec = p->greedy ? 1 : ns;
+      uint64_t* rec = bp->drec + ((((size_t)(pass & 1) * bp->lanes + ln) * rpl + r) * K + (j - 1)) * SW;
+      for (int i = tid(); i < nrec; i += kThreads) {
+        cst64(rec + 1 + i, (uint64_t)(uint32_t)(p->greedy ? tok : sidx[i]));
+        cst64(rec + 1 + p->topk + i, (uint64_t)__double_as_longlong(p->greedy ? 1.0 : prob[i]));
+      }
+      if (tid() == 0) cst64(rec, (uint64_t)(uint32_t)tok | ((uint64_t)(uint32_t)nrec << 32));
+    } else if (tid() < 64) {
+      int tok;
+      bool accept = false;
+      if (has_draft) {
+        double pd = 0.0, qd = 0.0;
+        for (int i = tid(); i < ns; i += 64)
+          if (sidx[i] == dtok) pd = prob[i];
+        for (int i = tid(); i < nq; i += 64)
+          if (qidx[i] == dtok) qd = qprob[i];
+        pd = wave_sumd_dpp(pd);
+        qd = wave_sumd_dpp(qd);
+        accept = (double)U[(t - 1) * 3 + 1] * qd < pd;
+        tok = dtok;
+        if (!accept) {
+          double rs = 0.0;
+          for (int i = tid(); i < ns; i += 64) {
+            const int x = sidx[i];
+            int lo = 0, hi2 = nq;
+            while (lo < hi2) {
+              const int mid = (lo + hi2) >> 1;
+              if (qidx[mid] < x) lo = mid + 1;
+              else hi2 = mid;
+            }
+            const double qx = (lo < nq && qidx[lo] == x) ? qprob[lo] : 0.0;
+            const double v = prob[i] - qx;
+            res[i] = v > 0.0 ? v : 0.0;
+            rs += res[i];
+          }
+          rs = wave_sumd_dpp(rs);
+          if (!(rs > 0.0))
+            for (int i = tid(); i < ns; i += 64) res[i] = prob[i];
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          tok = sidx[inverse_cdf(res, ns, (double)U[(t - 1) * 3 + 2])];
+        }
+      } else {
+        tok = sidx[inverse_cdf(prob, ns, (double)U[(t - 1) * 3 + 2])];
+      }
+      if (tid() == 0) cst32(bp->vres + ln * rpl + r, (uint32_t)tok | (accept ? 0x80000000u : 0u));
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------ commit + row setup
+// Lane workgroup: commit the verdicts of the pass just sampled, pick the next
+// anchor and its drafts (or finish the frame and start the lane's next one),
+// then gather and normalise the new rows (layer 0 input). first: no pass yet.
+__device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, bool first, float* xs,
+                            uint32_t* A0) {
+  const KParams* p = bp->k;
+  const int lane_id = blockIdx.x, rpl = bp->rpl, K = p->K, n = p->n_codes, H = p->H;
+  int* st = sh->ln[lane_id];
+  int* gst = bp->lane + (size_t)lane_id * kLaneInts;
+  if (first) {
+    for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = 0;
+    if (tid() == 0) st[kLnFrame] = lane_id - bp->lanes;
+  } else {
+    for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = (int)cld32(gst + i);
+  }
+  __syncthreads();
+  if (!first && st[kLnActive]) {
+    const int R = st[kLnRows];
+    for (int i = tid(); i < R; i += kThreads) sh->vr[i] = (int)cld32(bp->vres + lane_id * rpl + i);
+    const int par = st[kLnPass] & 1;
+    for (int i = tid(); i < R * K; i += kThreads) {
+      const int r = i / K, jj = i - r * K;
+      sh->dt[r][jj] = jj < row_drafts(p, st, r)
+                          ? (int)(uint32_t)cld64(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
+                          : -1;
+    }
+  }
+  __syncthreads();
+  if (tid() == 0) {
+    bool start = first || !st[kLnActive];
+    if (!first && st[kLnActive]) {
+      const int m = st[kLnM], kp = st[kLnKp], R = st[kLnRows], fp = st[kLnFirst];
+      int* codes = st + kLnCodes;
+      int m_new = -1, acc = 0;
+      if (st[kLnPass] == 0) {
+        codes[1] = sh->vr[1] & 0x7fffffff;
+        m_new = 1;
+      } else {
+        for (int j = 1; j <= kp; ++j) {
+          const int v = sh->vr[j - 1];
+          if (v & 0x80000000) {
+            codes[m + j] = st[kLnDrafts + m + j];
+            ++acc;
+            st[kLnMask] |= 1 << (m + j);
+          } else {
+            codes[m + j] = v & 0x7fffffff;
+            m_new = m + j;
+            break;
+          }
+        }
+        if (m_new < 0) {
+          if (R > kp) {
+            codes[m + kp + 1] = sh->vr[kp] & 0x7fffffff;
+            m_new = m + kp + 1;
+          } else {
+            m_new = n;
+          }
+        }
+        st[kLnRounds] += 1;
+        st[kLnDrafted] += kp;
+        st[kLnAccepted] += acc;
+      }
+      st[kLnCalls] += 1;
+      // every pass commits at least one code: a frame still open after n + 1 passes is a fault
+      if (st[kLnCalls] > n + 1) raise_status(bp, RVQSD_ETIMEOUT);
+      if (m_new < n) {
+        const int arow = m_new - fp;
+        const int nd = min(K, n - m_new);
+        for (int jj = 1; jj <= nd; ++jj) st[kLnDrafts + m_new + jj] = sh->dt[arow][jj - 1];
+        st[kLnPrevAnchor] = arow;
+        st[kLnKp] = nd;
+        st[kLnRows] = min(nd + 1, n - m_new);
+        st[kLnFirst] = m_new + 1;
+        st[kLnInCode + m_new + 1] = codes[m_new];
+        for (int r = 1; r < st[kLnRows]; ++r) st[kLnInCode + m_new + 1 + r] = st[kLnDrafts + m_new + r];
+        st[kLnM] = m_new;
+        st[kLnPass] += 1;
+      } else {
+        // frame complete
+        const int f = st[kLnFrame];
+        for (int s = 1; s <= n; ++s) call.out_codes[(size_t)f * n + s - 1] = codes[s];
+        rvqsd_stats o;
+        o.target_calls = st[kLnCalls];
+        o.rounds = st[kLnRounds];
+        o.drafted = st[kLnDrafted];
+        o.accepted = st[kLnAccepted];
+        o.accept_mask = (uint32_t)st[kLnMask];
+        o.status = RVQSD_OK;
+        o.weight_bytes = (uint64_t)(uint32_t)st[kLnBytesLo] | ((uint64_t)(uint32_t)st[kLnBytesHi] << 32);
+        o.clk_start = (uint64_t)(uint32_t)st[kLnClkLo] | ((uint64_t)(uint32_t)st[kLnClkHi] << 32);
+        o.clk_end = dclock();
+        call.out_stats[f] = o;
+        start = true;
+      }
+    }
+    if (start) {
+      // the lane's next frame with a valid c0
+      int f = st[kLnFrame] + bp->lanes;
+      while (f < call.n && (call.c0[f] < 0 || call.c0[f] >= p->V)) {
+        rvqsd_stats o = {};
+        o.status = RVQSD_EINVAL;
+        call.out_stats[f] = o;
+        for (int s = 0; s < n; ++s) call.out_codes[(size_t)f * n + s] = -1;
+        f += bp->lanes;
+      }
+      for (int i = 0; i < kLaneInts; ++i) st[i] = 0;
+      st[kLnFrame] = f;
+      if (f < call.n) {
+        const uint64_t now = dclock();
+        st[kLnActive] = 1;
+        st[kLnRows] = 2;
+        st[kLnCodes] = call.c0[f];
+        st[kLnInCode + 1] = call.c0[f];
+        st[kLnClkLo] = (int)(uint32_t)now;
+        st[kLnClkHi] = (int)(uint32_t)(now >> 32);
+      }
+    }
+    if (st[kLnActive]) {
+      // algorithmic bytes of this pass if the frame were decoded alone: layer weights,
+      // the heads it touches, the gathered rows and the KV cache it attends over
+      int t_lo = 1 << 20, t_hi = -1;
+      for (int r = 0; r < st[kLnRows]; ++r) {
+        const int s = st[kLnFirst] + r;
+        if (row_is_verify(st, r)) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
+        const int nd = row_drafts(p, st, r);
+        if (nd > 0) { t_lo = min(t_lo, s + 1); t_hi = max(t_hi, s + nd); }
+      }
+      unsigned long long b = (unsigned long long)p->L * p->layer_stride;
+      if (t_hi >= t_lo) b += (unsigned long long)(t_hi - t_lo + 1) * p->table_stride;
+      for (int r = 0; r < st[kLnRows]; ++r) b += (st[kLnFirst] + r == 0) ? 4ull * H : 2ull * H;
+      b += (unsigned long long)p->L * (st[kLnFirst] + st[kLnRows]) * p->nkv * p->d * 2 * 4;
+      b += (uint64_t)(uint32_t)st[kLnBytesLo] | ((uint64_t)(uint32_t)st[kLnBytesHi] << 32);
+      st[kLnBytesLo] = (int)(uint32_t)b;
+      st[kLnBytesHi] = (int)(uint32_t)(b >> 32);
+    }
+  }
+  __syncthreads();
+  for (int i = tid(); i < kLaneInts; i += kThreads) cst32(gst + i, (uint32_t)st[i]);
+  // layer-0 input of the lane's rows
+  if (!st[kLnActive]) return;
+  const float* g0 = bfw(p, p->o_attn_norm);
+  for (int r = 0; r < st[kLnRows]; ++r) {
+    const int s = st[kLnFirst] + r, i = lane_id * rpl + r;
+    float ss = 0.f;
+    for (int e = tid(); e < H; e += kThreads) {
+      float v;
+      if (s == 0) {
+        v = G(call.frame_hidden)[(size_t)st[kLnFrame] * H + e];
+      } else {
+        const bf16_t* tab = bw(p, p->o_emb0 + (uint64_t)(s - 1) * p->table_stride);
+        v = __uint_as_float((uint32_t)G(tab)[(size_t)st[kLnInCode + s] * H + e] << 16);
+      }
+      xs[e] = v;
+      cstf(bp->x + (size_t)i * H + e, v);
+      ss = fmaf(v, v, ss);
+    }
+    ss = block_sum(sh, ss);
+    const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
+    for (int c = tid(); c < H / 8; c += kThreads) {
+      float h8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h8[e] = xs[8 * c + e] * rs * G(g0)[8 * c + e];
+      store_split(A0 + (size_t)i * H + 8 * c, h8);
+    }
+    __syncthreads();
+  }
+}
+
+// A lane's frames that did not complete when the launch ended early
+__device__ void lane_abort(const BParams* bp, BShared* sh, const BCall& call) {
+  if (tid() != 0) return;
+  const int code = (int)cld32(bp->status);
+  const int n = bp->k->n_codes;
+  const int* st = sh->ln[blockIdx.x];
+  int f = st[kLnActive] ? st[kLnFrame] : st[kLnFrame] + bp->lanes;
+  if (f < 0) f = blockIdx.x;
+  for (; f < call.n; f += bp->lanes) {
+    rvqsd_stats o = {};
+    o.status = code ? code : RVQSD_ETIMEOUT;
+    call.out_stats[f] = o;
+    for (int s = 0; s < n; ++s) call.out_codes[(size_t)f * n + s] = -1;
+  }
+}
+
+__global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __restrict__ bpp, BCall call) {
+  __shared__ BShared shs;
+  extern __shared__ __align__(16) float dyn[];
+  const BParams* bp = bpp;
+  const KParams* p = bp->k;
+  BShared* sh = &shs;
+  uint32_t gen = 0;
+  const int L = p->L, H = p->H;
+  uint32_t* A0 = bp->a;
+  uint32_t* A1 = bp->a + (size_t)bp->M * max(max(H, p->qdim), p->F);
+  const bool lane_wg = (int)blockIdx.x < bp->lanes;
+  bool first = true, ok = true;
+  while (ok) {
+    if (lane_wg) lane_commit(bp, sh, call, first, dyn, A0);
+    first = false;
+    if (!(ok = grid_sync(bp, gen, sh))) break;
+    for (int i = tid(); i < bp->lanes * kLaneInts; i += kThreads)
+      sh->ln[i / kLaneInts][i % kLaneInts] = (int)cld32(bp->lane + i);
+    __syncthreads();
+    int any = 0;
+    for (int i = 0; i < bp->lanes; ++i) any |= sh->ln[i][kLnActive];
+    if (!any) break;
+    for (int l = 0; l < L && ok; ++l) {
+      proj_partial<4>(bp, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, bp->ks_qkv, A0, dyn);
+      ok = grid_sync(bp, gen, sh);
+      if (ok) phase_attn(bp, sh, l, A1, dyn);
+      ok = ok && grid_sync(bp, gen, sh);
+      if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
+      ok = ok && grid_sync(bp, gen, sh);
+      if (ok) phase_resid(bp, sh, bp->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, 0, dyn);
+      ok = ok && grid_sync(bp, gen, sh);
+      if (ok) phase_gu(bp, l, A0, A1, dyn);
+      ok = ok && grid_sync(bp, gen, sh);
+      if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wd)), H, p->F, bp->ks_down, A1, dyn);
+      ok = ok && grid_sync(bp, gen, sh);
+      if (ok) {
+        if (l + 1 < L) phase_resid(bp, sh, bp->ks_down, bfw(p, boff(p, l + 1, p->o_attn_norm)), A0, 0, dyn);
+        else phase_resid(bp, sh, bp->ks_down, bfw(p, p->o_final_norm), nullptr, 1, dyn);
+      }
+      ok = ok && grid_sync(bp, gen, sh);
+    }
+    if (!ok) break;
+    phase_heads(bp, sh, dyn);
+    if (!(ok = grid_sync(bp, gen, sh))) break;
+    phase_sample(bp, sh, call, dyn);
+    if (blockIdx.x == 0 && tid() == 0) {
+      bp->totals[0] += 1ull;
+      bp->totals[1] += pass_bytes_batch(bp, sh);
+    }
+    if (!(ok = grid_sync(bp, gen, sh))) break;
+  }
+  if (!ok && lane_wg) lane_abort(bp, sh, call);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------- host
+
+int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
+                 size_t errlen) {
+  const void* fn = reinterpret_cast<const void*>(&batch_kernel);
+  static size_t attr_bytes = 0;
+  if (lds_bytes > attr_bytes) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    if (e != hipSuccess) {
+      snprintf(err, errlen, "hipFuncSetAttribute(%zu bytes LDS): %s", lds_bytes, hipGetErrorString(e));
+      return RVQSD_EHIP;
+    }
+    attr_bytes = lds_bytes;
+  }
+  const BParams* bpp = bp;
+  BCall c = call;
+  void* args[] = {&bpp, &c};
+  hipError_t e = hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(kThreads), args, (unsigned)lds_bytes,
+                                            reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    snprintf(err, errlen, "hipLaunchCooperativeKernel: %s", hipGetErrorString(e));
+    return RVQSD_EHIP;
+  }
+  return RVQSD_OK;
+}
+
+}  // namespace rvqsd

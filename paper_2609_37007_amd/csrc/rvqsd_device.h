@@ -191,6 +191,27 @@ __device__ __forceinline__ float lane_val(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
+// MFMA operand and accumulator types (v_mfma_f32_16x16x32_bf16)
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// fp32 -> bf16 bits, round to nearest even
+__device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+// 8 floats -> hi (8 bf16) and lo (8 bf16, the rounded remainder)
+__device__ __forceinline__ void split8(const float (&x)[8], W16& hi, W16& lo) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t a = bf16_bits_rne(x[2 * j]), b = bf16_bits_rne(x[2 * j + 1]);
+    const uint32_t ra = bf16_bits_rne(x[2 * j] - __uint_as_float(a << 16));
+    const uint32_t rb = bf16_bits_rne(x[2 * j + 1] - __uint_as_float(b << 16));
+    hi[j] = a | (b << 16);
+    lo[j] = ra | (rb << 16);
+  }
+}
+
 // LDS scratch of the workgroup-wide top-k selection
 struct TopkShared {
   unsigned hist[256];

@@ -360,8 +360,6 @@ struct Gemv {
 // 8; wave w takes g = w, w + 8, ..., so each wave holds one accumulator per tile
 // and the 8 wave partials are added once in LDS.
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <typename WT>
 struct IsBf16 {
@@ -375,22 +373,6 @@ template <typename WT, int MR>
 struct UseMfma {
   static constexpr bool value = IsBf16<WT>::value && MR <= 8;
 };
-
-__device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-// 8 floats -> hi (8 bf16) and lo (8 bf16, the rounded remainder)
-__device__ __forceinline__ void split8(const float (&x)[8], W16& hi, W16& lo) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t a = bf16_bits_rne(x[2 * j]), b = bf16_bits_rne(x[2 * j + 1]);
-    const uint32_t ra = bf16_bits_rne(x[2 * j] - __uint_as_float(a << 16));
-    const uint32_t rb = bf16_bits_rne(x[2 * j + 1] - __uint_as_float(b << 16));
-    hi[j] = a | (b << 16);
-    lo[j] = ra | (rb << 16);
-  }
-}
 
 // Split activations in LDS: row m, 8-element chunk q -> 8 words at m * (K + 4) + q * 8:
 // 4 words of hi, then 4 words of lo. The 4 words of padding per row put the 16

@@ -77,6 +77,52 @@ struct FrameArgs {
 // Host entry into the kernel translation unit. gp: KParams in device memory.
 int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream,
                  size_t lds_bytes, char* err, size_t errlen);
+
+// ---------------------------------------------------------------- batched path
+// Independent frame streams ("lanes") verified together: lane i owns rows
+// i * rpl .. i * rpl + rpl - 1 of every pass (rpl = max(K + 1, 2)), so a
+// projection multiplies M = lanes * rpl rows at once on MFMA tiles.
+constexpr int kMaxLanes = 16;
+constexpr int kBatchMaxRows = 80;  // lanes * rpl: five 16-row MFMA tiles
+constexpr int kBatchMTiles = kBatchMaxRows / 16;
+// lane state record (int32 words)
+constexpr int kLnActive = 0, kLnFrame = 1, kLnPass = 2, kLnM = 3, kLnKp = 4, kLnFirst = 5, kLnRows = 6,
+              kLnPrevAnchor = 7, kLnCalls = 8, kLnRounds = 9, kLnDrafted = 10, kLnAccepted = 11, kLnMask = 12,
+              kLnStatus = 13, kLnBytesLo = 14, kLnBytesHi = 15, kLnClkLo = 16, kLnClkHi = 17,
+              kLnCodes = 32, kLnDrafts = 48, kLnInCode = 64, kLaneInts = 80;
+
+struct BParams {
+  const KParams* k;     // device copy of the stream's parameter block (dimensions, weights, rotary table)
+  int32_t lanes, rpl, M, nwg;
+  int32_t ks_qkv, ks_o, ks_down;  // k splits of the projections whose partial sums the next phase adds
+  int32_t hrows;        // LM-head input rows: M * (K + 1) (row i * (K + 1) + j: row i plus offset b_j)
+  int32_t sup_words;    // 64-bit words of one support record: 1 + 2 * topk
+  int32_t* lane;        // [lanes][kLaneInts]
+  float* x;             // [M][H] residual stream
+  uint32_t* a;          // [M][max(H, qdim, F)] split activations (8-element chunks: 4 words hi, 4 words lo)
+  uint32_t* ah;         // [hrows][H] split LM-head inputs
+  float* part;          // [max ks][M][max N] partial sums
+  float* kv;            // [lanes][L][nkv][kMaxPos][2][d] KV cache (k after norm and RoPE, v)
+  float* logits;        // [hrows][V]
+  int32_t* vres;        // [lanes][rpl] verdicts: token | accepted << 31
+  uint64_t* drec;       // [2][lanes][rpl][K][sup_words] draft records: token, idx[topk], prob bits[topk]
+  uint32_t* bar;        // barrier words: [0] top counter, [64 (1 + x)] counter of XCD x, [64 * 9] generation
+  int32_t* status;      // first device-side error of the launch (0 = none)
+  unsigned long long* totals;  // [0] passes (rounds of the batch), [1] their algorithmic bytes
+};
+
+// Per-call arguments (device pointers), passed by value.
+struct BCall {
+  const float* frame_hidden;  // [n][H]
+  const int32_t* c0;          // [n]
+  const float* uniforms;      // [n][n_codes][3]
+  int32_t* out_codes;         // [n][n_codes]
+  rvqsd_stats* out_stats;     // [n]
+  int32_t n;
+};
+
+int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
+                 size_t errlen);
 int frame_lds_head_floats(int mr, int cpw);
 int frame_max_rows(int K);
 

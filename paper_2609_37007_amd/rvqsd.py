@@ -22,8 +22,8 @@ TRACE_ROUND_INTS = 32
 # every symbol include/rvqsd.h declares
 EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_stream_destroy",
            "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset",
-           "rvqsd_set_trace",
-           "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
+           "rvqsd_set_trace", "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async",
+           "rvqsd_batch_totals", "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
 
 
 class rvqsd_cfg(ctypes.Structure):
@@ -96,6 +96,9 @@ def lib():
         L.rvqsd_decode_frame_u.argtypes = [vp, vp, i32, vp, vp, P(rvqsd_stats)]
         L.rvqsd_decode_frame_async.argtypes = [vp, vp, vp, vp, vp, vp]
         L.rvqsd_set_trace.argtypes = [vp, P(rvqsd_trace)]
+        L.rvqsd_decode_frames_batched.argtypes = [vp, i32, vp, vp, vp, vp, vp]
+        L.rvqsd_decode_frames_batched_async.argtypes = [vp, i32, vp, vp, vp, vp, vp]
+        L.rvqsd_batch_totals.argtypes = [vp, P(ctypes.c_uint64), P(ctypes.c_uint64)]
         L.rvqsd_stream_reset.argtypes = [vp]
         L.rvqsd_uniforms_from_seed.argtypes = [ctypes.c_uint64, i32, vp]
         L.rvqsd_status_str.argtypes = [i32]
@@ -104,6 +107,7 @@ def lib():
         L.rvqsd_last_error.restype = ctypes.c_char_p
         for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_decode_frame",
                   "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset", "rvqsd_set_trace",
+                  "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async", "rvqsd_batch_totals",
                   "rvqsd_uniforms_from_seed"):
             getattr(L, n).restype = i32
         _lib = L
@@ -203,6 +207,32 @@ class Stream:
         _check(lib().rvqsd_decode_frame_async(self._h, ctypes.c_void_p(d_frame_hidden), ctypes.c_void_p(d_c0),
                                               ctypes.c_void_p(d_uniforms), ctypes.c_void_p(d_out_codes),
                                               ctypes.c_void_p(d_stats)), "rvqsd_decode_frame_async")
+
+    def decode_frames_batched(self, frame_hidden, c0, uniforms):
+        """Host arrays [n][H], [n], [n][n_codes][3] -> (codes [n][n_codes], stats structured array [n])."""
+        f = np.ascontiguousarray(frame_hidden, dtype=np.float32)
+        c = np.ascontiguousarray(c0, dtype=np.int32)
+        u = np.ascontiguousarray(uniforms, dtype=np.float32)
+        nfr = int(c.shape[0])
+        out = np.full((nfr, self.n), -1, dtype=np.int32)
+        st = np.zeros(nfr, dtype=STATS_DTYPE)
+        _check(lib().rvqsd_decode_frames_batched(self._h, nfr, _ptr(f), _ptr(c), _ptr(u), _ptr(out), _ptr(st)),
+               "rvqsd_decode_frames_batched")
+        return out, st
+
+    def decode_frames_batched_async(self, n: int, d_frame_hidden: int, d_c0: int, d_uniforms: int,
+                                    d_out_codes: int, d_stats: int):
+        """Device pointers (ints); enqueues only."""
+        _check(lib().rvqsd_decode_frames_batched_async(self._h, int(n), ctypes.c_void_p(d_frame_hidden),
+                                                       ctypes.c_void_p(d_c0), ctypes.c_void_p(d_uniforms),
+                                                       ctypes.c_void_p(d_out_codes), ctypes.c_void_p(d_stats)),
+               "rvqsd_decode_frames_batched_async")
+
+    def batch_totals(self):
+        """(passes, algorithmic bytes) of the last batched call; synchronises the stream."""
+        a, b = ctypes.c_uint64(), ctypes.c_uint64()
+        _check(lib().rvqsd_batch_totals(self._h, ctypes.byref(a), ctypes.byref(b)), "rvqsd_batch_totals")
+        return int(a.value), int(b.value)
 
     def reset(self):
         _check(lib().rvqsd_stream_reset(self._h), "rvqsd_stream_reset")
