@@ -13,6 +13,12 @@ Workload (default): the 1024-wide MultiCodeDecoder (5 layers, hidden 1024, GQA
 frames.  Inputs are synthetic: frame hidden vectors N(0,1), c_0 uniform,
 uniforms pre-drawn from seed 1.
 
+With --streams S (2..16) the workload is S independent streams of the same
+model verified together (S x (K + 1) rows per pass, stream i with frame seeds
+2000 + i and uniform seeds 1000 + i, 500 frames per stream), run as one launch
+of the batched kernel through rvqsd_decode_frames_batched_async; `value` is
+then the aggregate codes/s of all streams.
+
 Prints ONE JSON line.  `roofline` prices the frame kernel against HBM
 bandwidth with the algorithmic bytes the device counts per frame (layer
 weights per pass, the distinct LM heads a pass touches, gathered embedding
@@ -82,7 +88,159 @@ def parse():
     ap.add_argument("--head-scale", type=float, default=1.0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--streams", type=int, default=1, help="independent streams verified together (1..16)")
+    ap.add_argument("--frames-per-stream", type=int, default=500)
     return ap.parse_args()
+
+
+def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order):
+    """Time the CPU oracle on frames `order` until `seconds` pass; returns the cpu_baseline object."""
+    from oracle import oracle as O
+    orc = O.Oracle(blob, n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
+                   head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
+                   dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K)
+    threads = O.get_threads()
+    print(f"[bench] oracle sample on {threads} threads, ~{seconds:.0f} s", file=sys.stderr, flush=True)
+    done, same = 0, 0
+    c_t0 = time.perf_counter()
+    while done < len(order) and (time.perf_counter() - c_t0) < seconds:
+        i = order[done]
+        oc, _, _ = orc.spec_frame(f[i], int(c0[i]), u[i])
+        same += int((oc == codes[i]).all())
+        done += 1
+    c_el = time.perf_counter() - c_t0
+    orc.close()
+    return {"value": round(s.n_codes * done / c_el, 3), "unit": "codes/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of the timed frames ({c_el:.1f} s, fp64 full-recompute oracle, OpenMP over output "
+                      f"rows); {same}/{done} frames give codes identical to the GPU's"}
+
+
+def run_streams(a) -> int:
+    """S streams verified together by the batched kernel: one launch for all frames."""
+    import numpy as np
+    import torch
+
+    from paper_2609_37007_amd import rvqsd as R
+    from paper_2609_37007_amd import synth as S
+
+    R.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    s = S.MCD_1024
+    topk, K = 50, (4 if a.draft_len is None else a.draft_len)
+    temperature = 0.9
+    ns, per = a.streams, a.frames_per_stream
+    n = s.n_codes
+    print(f"[bench] building weights; {ns} streams x {per} frames", file=sys.stderr, flush=True)
+    blob = S.make_weights(s, seed=0, head_scale=a.head_scale)
+    cfg = R.make_cfg(n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
+                     head_dim=s.head_dim, ffn=s.ffn, n_codes=n, vocab=s.vocab, max_draft=s.max_draft,
+                     dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    torch_stream = torch.cuda.current_stream(dev)
+    model = R.Model(blob, cfg)
+    info = model.info()
+    stream = R.Stream(model, hip_stream=torch_stream.cuda_stream, max_streams=ns)
+    # frame j of stream i is batched frame j * ns + i (lane i decodes stream i in order)
+    N = ns * per
+    f = np.zeros((N, s.hidden), dtype=np.float32)
+    c0 = np.zeros(N, dtype=np.int32)
+    u = np.zeros((N, n, 3), dtype=np.float32)
+    for i in range(ns):
+        fi, ci = S.frame_inputs(s, per, seed_hidden=2000 + i, seed_c0=3000 + i)
+        f[i::ns], c0[i::ns], u[i::ns] = fi, ci, S.uniforms(per, n, seed=1000 + i)
+    d_f = torch.from_numpy(f).to(dev)
+    d_c0 = torch.from_numpy(c0).to(dev)
+    d_u = torch.from_numpy(u).to(dev)
+    d_codes = torch.full((N, n), -1, dtype=torch.int32, device=dev)
+    sb = R.STATS_DTYPE.itemsize
+    d_stats = torch.zeros(N * sb, dtype=torch.uint8, device=dev)
+
+    def launch(count):
+        stream.decode_frames_batched_async(count, d_f.data_ptr(), d_c0.data_ptr(), d_u.data_ptr(),
+                                           d_codes.data_ptr(), d_stats.data_ptr())
+
+    W = max(1, a.warmup) * ns
+    print(f"[bench] warmup {min(W, N)} frames", file=sys.stderr, flush=True)
+    launch(min(W, N))
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    print(f"[bench] timing {N} frames", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    ev0.record(torch_stream)
+    launch(N)
+    ev1.record(torch_stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    launch_ms = ev0.elapsed_time(ev1)
+    passes, nbytes = stream.batch_totals()
+    st = np.frombuffer(d_stats.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)
+    codes = d_codes.cpu().numpy()
+    if (st["status"] != 0).any():
+        bad = int(np.argmax(st["status"] != 0))
+        print(f"[bench] frame {bad} failed with status {int(st['status'][bad])}", file=sys.stderr)
+        return 1
+    calls = int(st["target_calls"].sum())
+    achieved = nbytes / (launch_ms * 1e-3) / 1e9
+    cpu = None
+    if not a.no_cpu_baseline:
+        order = list(range(0, N, max(1, N // 64)))
+        cpu = oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, a.cpu_seconds, order)
+    out = {
+        "metric": METRIC,
+        "value": round(n * N / elapsed, 1),
+        "unit": "codes/s",
+        "n_gpus": 1,
+        "steps": N,
+        "warmup": min(W, N),
+        "ms_per_step": round(elapsed * 1e3 / N, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (random-init weights, seeded frame inputs and uniforms per stream)",
+        "config": {
+            "workload": (f"mcd1024 x {ns} streams: {s.n_layers} layers, hidden {s.hidden}, {s.n_q_heads}/"
+                         f"{s.n_kv_heads} heads x {s.head_dim}, ffn {s.ffn}, {n} codebooks of {s.vocab}, bf16 "
+                         f"weights; draft length {K}, top-k {topk}, temperature {temperature}; {ns} independent "
+                         f"streams verified together ({ns * max(K + 1, 2)} rows per pass), {per} frames each"),
+            "frames": N,
+            "streams": ns,
+            "draft_len": K,
+            "topk": topk,
+            "temperature": temperature,
+            "head_scale": a.head_scale,
+            "parallelism": "single GPU, one persistent workgroup per compute unit, one launch for all frames",
+        },
+        "per_stream_codes_per_s": round(n * N / elapsed / ns, 1),
+        "accepted_tokens_per_call": round(n * N / calls, 4),
+        "passes": passes,
+        "pass_us_mean": round(launch_ms * 1e3 / passes, 2),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "batch_kernel",
+            "algorithmic_bytes_per_launch": float(nbytes),
+            "algorithmic_bytes_per_pass": round(nbytes / passes, 1),
+            "launch_ms_mean": round(launch_ms, 4),
+        },
+        "cpu_baseline": cpu,
+        "device": torch.cuda.get_device_name(dev),
+        "workgroups": info["workgroups"],
+    }
+    del d_f, d_c0, d_u, d_codes, d_stats
+    torch.cuda.synchronize()
+    stream.close()
+    model.close()
+    torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def main() -> int:
@@ -93,6 +251,8 @@ def main() -> int:
               "has no multi-GPU path (independent streams would shard across GPUs with no exchange). "
               "Run with --gpus 1.", file=sys.stderr)
         return 2
+    if a.streams > 1:
+        return run_streams(a)
 
     import numpy as np
     import torch
@@ -176,23 +336,7 @@ def main() -> int:
 
     cpu = None
     if not a.no_cpu_baseline:
-        from oracle import oracle as O
-        orc = O.Oracle(blob, n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
-                       head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
-                       dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K)
-        threads = O.get_threads()
-        print(f"[bench] oracle sample on {threads} threads, ~{a.cpu_seconds:.0f} s", file=sys.stderr, flush=True)
-        done, same = 0, 0
-        c_t0 = time.perf_counter()
-        while done < steps and (time.perf_counter() - c_t0) < a.cpu_seconds:
-            oc, _, _ = orc.spec_frame(f[done], int(c0[done]), u[done])
-            same += int((oc == codes[done]).all())
-            done += 1
-        c_el = time.perf_counter() - c_t0
-        orc.close()
-        cpu = {"value": round(n * done / c_el, 3), "unit": "codes/s", "cores": threads, "kind": "oracle",
-               "sample": f"first {done} of the {steps} timed frames ({c_el:.1f} s, fp64 full-recompute oracle, "
-                         f"OpenMP over output rows); {same}/{done} frames give codes identical to the GPU's"}
+        cpu = oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, a.cpu_seconds, list(range(steps)))
 
     out = {
         "metric": METRIC,

@@ -176,7 +176,7 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
 int pick_ks(int K, int kw, int colgroups, int nwg) {
   const int steps = K / (kw * 64);
   int best = 1;
-  for (int ks = 1; ks <= steps; ++ks)
+  for (int ks = 1; ks <= steps && ks <= 32; ++ks)  // the partial-sum readers take at most 32 splits
     if (steps % ks == 0 && colgroups * ks <= nwg) best = ks;
   return best;
 }
@@ -191,8 +191,8 @@ int batch_setup(rvqsd_stream* s, int lanes) {
   if (c.dtype != RVQSD_DTYPE_BF16) return set_err(RVQSD_EUNSUPPORTED, "batched streams need bf16 weights");
   if (M > kBatchMaxRows)
     return set_err(RVQSD_EUNSUPPORTED, "max_streams * max(draft_len + 1, 2) = %d rows > %d", M, kBatchMaxRows);
-  if (k.H % 256 || k.qdim % 128 || k.F % 128)
-    return set_err(RVQSD_EUNSUPPORTED, "batched streams need hidden %% 256 == 0, q width and ffn %% 128 == 0");
+  if (k.H % 256 || k.qdim % 128 || k.F % 128 || k.H > 2048)
+    return set_err(RVQSD_EUNSUPPORTED, "batched streams need hidden %% 256 == 0 (<= 2048), q width and ffn %% 128 == 0");
   if (m->nwg < 8) return set_err(RVQSD_EUNSUPPORTED, "batched streams need at least 8 workgroups");
   BParams b;
   memset(&b, 0, sizeof(b));

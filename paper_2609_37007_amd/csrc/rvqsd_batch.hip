@@ -19,9 +19,10 @@
 //   commit + row setup (lane workgroups) | per layer: QKV, attention, O,
 //   residual + norm, gate/up (SiLU * up fused), down, residual + norm |
 //   LM heads | top-k / softmax / draft / accept-or-resample.
-// Data crossing workgroups moves through device-coherent (sc1) loads and
-// stores; the barrier waits for this workgroup's stores to complete, so no
-// cache-wide fence is needed. Every wait is bounded: a workgroup that times
+// Data crossing workgroups is written with device-coherent (sc1) stores; the
+// barrier waits for this workgroup's stores to complete before it arrives,
+// and after it one wave per workgroup runs an agent-scope acquire (cache
+// invalidate), so the next phase reads with plain, cached loads. Every wait is bounded: a workgroup that times
 // out records RVQSD_ETIMEOUT in the status word and every other one leaves at
 // its next barrier.
 #include <hip/hip_runtime.h>
@@ -40,16 +41,26 @@ namespace {
 __device__ __forceinline__ uint32_t cld32(const void* p) {
   return __hip_atomic_load(G(reinterpret_cast<const uint32_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint64_t cld64(const void* p) {
-  return __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 __device__ __forceinline__ void cst32(void* p, uint32_t v) {
   __hip_atomic_store(G(reinterpret_cast<uint32_t*>(p)), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void cst64(void* p, uint64_t v) {
   __hip_atomic_store(G(reinterpret_cast<uint64_t*>(p)), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float cldf(const float* p) { return __uint_as_float(cld32(p)); }
+// plain (cached) reads of data published before the last barrier
+__device__ __forceinline__ float ldf(const float* p) { return *G(p); }
+// Sum of KS <= kMaxSplit partial sums at p, p + stride, ... in split order; the loads are
+// issued together (a loop with a run-time bound would wait for each before the next).
+constexpr int kMaxSplit = 32;
+__device__ __forceinline__ float sum_parts(const float* p, size_t stride, int KS) {
+  float v[kMaxSplit];
+#pragma unroll
+  for (int k = 0; k < kMaxSplit; ++k) v[k] = k < KS ? ldf(p + k * stride) : 0.f;
+  float s = v[0];
+#pragma unroll
+  for (int k = 1; k < kMaxSplit; ++k) s += v[k];
+  return s;
+}
 __device__ __forceinline__ void cstf(float* p, float v) { cst32(p, __float_as_uint(v)); }
 
 // 8 activations -> one split chunk (4 words bf16 hi, 4 words bf16 lo) at dst
@@ -61,15 +72,7 @@ __device__ __forceinline__ void store_split(uint32_t* dst, const float (&x)[8]) 
   cst64(dst + 4, (uint64_t)lo[0] | ((uint64_t)lo[1] << 32));
   cst64(dst + 6, (uint64_t)lo[2] | ((uint64_t)lo[3] << 32));
 }
-__device__ __forceinline__ W16 load_w16c(const uint32_t* p) {
-  const uint64_t a = cld64(p), b = cld64(p + 2);
-  W16 r;
-  r[0] = (uint32_t)a;
-  r[1] = (uint32_t)(a >> 32);
-  r[2] = (uint32_t)b;
-  r[3] = (uint32_t)(b >> 32);
-  return r;
-}
+__device__ __forceinline__ W16 load_w16(const uint32_t* p) { return *G(reinterpret_cast<const W16*>(p)); }
 
 __device__ __forceinline__ const bf16_t* bw(const KParams* p, uint64_t off) {
   return reinterpret_cast<const bf16_t*>(p->wbase + off);
@@ -138,6 +141,8 @@ __device__ bool grid_sync(const BParams* bp, uint32_t& gen, BShared* sh) {
     if (!ab && cld32(bp->status) != 0) ab = 1;
     sh->abort = ab;
   }
+  // drop this CU's and this XCD's cached copies of lines written by others
+  if (tid() < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
   return sh->abort == 0;
 }
@@ -155,6 +160,8 @@ __device__ __forceinline__ float block_sum(BShared* sh, float v) {
   __syncthreads();
   return t;
 }
+
+constexpr int kRowChunks = 4;  // 8-element chunks per lane of a row held in registers (hidden <= 2048)
 
 // ------------------------------------------------------------ pass geometry
 
@@ -214,10 +221,10 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
       bh0[mt] = bl0[mt] = bh1[mt] = bl1[mt] = (W16)(0u);
       if (mt < mtiles && arow[mt] >= 0) {
         const uint32_t* ap = A + (size_t)arow[mt] * lda + (size_t)chunk * 8;
-        bh0[mt] = load_w16c(ap);
-        bl0[mt] = load_w16c(ap + 4);
-        bh1[mt] = load_w16c(ap + 8);
-        bl1[mt] = load_w16c(ap + 12);
+        bh0[mt] = load_w16(ap);
+        bl0[mt] = load_w16(ap + 4);
+        bh1[mt] = load_w16(ap + 8);
+        bl1[mt] = load_w16(ap + 12);
       }
     }
     const bf16x8 x0 = __builtin_bit_cast(bf16x8, a0), x1 = __builtin_bit_cast(bf16x8, a1);
@@ -332,13 +339,11 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
     for (int e = tid(); e < R * 3 * d; e += kThreads) {
       const int r = e / (3 * d), w = e - r * 3 * d, part = w / d, i = w - part * d;
       const int col = part == 0 ? h * d + i : qdim + (part - 1) * kvdim + g * d + i;
-      const float* src = bp->part + (size_t)(row0 + r) * N + col;
-      float s = 0.f;
-      for (int ks = 0; ks < KS; ++ks) s += cldf(src + (size_t)ks * M * N);
+      const float s = sum_parts(bp->part + (size_t)(row0 + r) * N + col, (size_t)M * N, KS);
       if (part == 0) qs[r * d + i] = s;
       else kvs[(size_t)(fp + r) * 2 * d + (part - 1) * d + i] = s;
     }
-    for (int e = tid(); e < fp * 2 * d; e += kThreads) kvs[e] = cldf(kvc + e);
+    for (int e = tid(); e < fp * 2 * d; e += kThreads) kvs[e] = ldf(kvc + e);
     __syncthreads();
     // q rows (v < R) and k rows (v >= R): norm + RoPE, one wave per vector
     for (int v = wave; v < 2 * R; v += kWaves) {
@@ -420,8 +425,7 @@ __device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float*
     float* x = bp->x + (size_t)i * H;
     float ss = 0.f;
     for (int e = tid(); e < H; e += kThreads) {
-      float v = cldf(x + e);
-      for (int ks = 0; ks < KS; ++ks) v += cldf(bp->part + ((size_t)ks * M + i) * H + e);
+      const float v = ldf(x + e) + sum_parts(bp->part + (size_t)i * H + e, (size_t)M * H, KS);
       cstf(x + e, v);
       xs[e] = v;
       ss = fmaf(v, v, ss);
@@ -559,16 +563,16 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
     if (has_draft) {
       // q of d_t: drafted last pass from the anchor's row, offset r + 1
       const uint64_t* rec = bp->drec + ((((size_t)((pass - 1) & 1) * bp->lanes + ln) * rpl + st[kLnPrevAnchor]) * K + r) * SW;
-      const uint64_t w0 = cld64(rec);
+      const uint64_t w0 = *G(rec);
       dtok = (int)(uint32_t)w0;
       nq = (int)(w0 >> 32);
       for (int i = tid(); i < nq; i += kThreads) {
-        qidx[i] = (int)(uint32_t)cld64(rec + 1 + i);
-        qprob[i] = __longlong_as_double((long long)cld64(rec + 1 + p->topk + i));
+        qidx[i] = (int)(uint32_t)*G(rec + 1 + i);
+        qprob[i] = __longlong_as_double((long long)*G(rec + 1 + p->topk + i));
       }
     }
     const float* src = bp->logits + (size_t)u * V;
-    for (int i = tid(); i < V; i += kThreads) lg[i] = cldf(src + i);
+    for (int i = tid(); i < V; i += kThreads) lg[i] = ldf(src + i);
     __syncthreads();
     int ns = topk_buckets(&sh->tk, lg, V, p->topk, sidx, slog, hist);
     if (ns < 0) ns = topk_select(&sh->tk, lg, V, p->topk, sidx, slog);
@@ -664,17 +668,17 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
     for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = 0;
     if (tid() == 0) st[kLnFrame] = lane_id - bp->lanes;
   } else {
-    for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = (int)cld32(gst + i);
+    for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = *G(gst + i);
   }
   __syncthreads();
   if (!first && st[kLnActive]) {
     const int R = st[kLnRows];
-    for (int i = tid(); i < R; i += kThreads) sh->vr[i] = (int)cld32(bp->vres + lane_id * rpl + i);
+    for (int i = tid(); i < R; i += kThreads) sh->vr[i] = *G(bp->vres + lane_id * rpl + i);
     const int par = st[kLnPass] & 1;
     for (int i = tid(); i < R * K; i += kThreads) {
       const int r = i / K, jj = i - r * K;
       sh->dt[r][jj] = jj < row_drafts(p, st, r)
-                          ? (int)(uint32_t)cld64(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
+                          ? (int)(uint32_t)*G(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
                           : -1;
     }
   }
@@ -789,33 +793,51 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
   }
   __syncthreads();
   for (int i = tid(); i < kLaneInts; i += kThreads) cst32(gst + i, (uint32_t)st[i]);
-  // layer-0 input of the lane's rows
+  // layer-0 input of the lane's rows: one wave per row, lane l holds 8-element chunks l, l + 64, ..
   if (!st[kLnActive]) return;
   const float* g0 = bfw(p, p->o_attn_norm);
-  for (int r = 0; r < st[kLnRows]; ++r) {
+  const int lane = tid() & 63, wave = tid() >> 6, nch = H / 8;
+  for (int r = wave; r < st[kLnRows]; r += kWaves) {
     const int s = st[kLnFirst] + r, i = lane_id * rpl + r;
+    float xv[kRowChunks][8];
     float ss = 0.f;
-    for (int e = tid(); e < H; e += kThreads) {
-      float v;
-      if (s == 0) {
-        v = G(call.frame_hidden)[(size_t)st[kLnFrame] * H + e];
-      } else {
-        const bf16_t* tab = bw(p, p->o_emb0 + (uint64_t)(s - 1) * p->table_stride);
-        v = __uint_as_float((uint32_t)G(tab)[(size_t)st[kLnInCode + s] * H + e] << 16);
-      }
-      xs[e] = v;
-      cstf(bp->x + (size_t)i * H + e, v);
-      ss = fmaf(v, v, ss);
-    }
-    ss = block_sum(sh, ss);
-    const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
-    for (int c = tid(); c < H / 8; c += kThreads) {
-      float h8[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) h8[e] = xs[8 * c + e] * rs * G(g0)[8 * c + e];
-      store_split(A0 + (size_t)i * H + 8 * c, h8);
+    for (int q = 0; q < kRowChunks; ++q) {
+      const int c = lane + 64 * q;
+      if (c < nch) {
+        if (s == 0) {
+          const float* fr = call.frame_hidden + (size_t)st[kLnFrame] * H + 8 * c;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) xv[q][e] = G(fr)[e];
+        } else {
+          const bf16_t* tab = bw(p, p->o_emb0 + (uint64_t)(s - 1) * p->table_stride);
+          const W16 w = *G(reinterpret_cast<const W16*>(tab + (size_t)st[kLnInCode + s] * H + 8 * c));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            xv[q][2 * e] = __uint_as_float(w[e] << 16);
+            xv[q][2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+          }
+        }
+        float* xd = bp->x + (size_t)i * H + 8 * c;
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          cst64(xd + e, (uint64_t)__float_as_uint(xv[q][e]) | ((uint64_t)__float_as_uint(xv[q][e + 1]) << 32));
+          ss = fmaf(xv[q][e], xv[q][e], fmaf(xv[q][e + 1], xv[q][e + 1], ss));
+        }
+      }
     }
-    __syncthreads();
+    ss = wave_sum(ss);
+    const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
+#pragma unroll
+    for (int q = 0; q < kRowChunks; ++q) {
+      const int c = lane + 64 * q;
+      if (c < nch) {
+        float h8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) h8[e] = xv[q][e] * rs * G(g0)[8 * c + e];
+        store_split(A0 + (size_t)i * H + 8 * c, h8);
+      }
+    }
   }
 }
 
@@ -847,12 +869,16 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
   uint32_t* A1 = bp->a + (size_t)bp->M * max(max(H, p->qdim), p->F);
   const bool lane_wg = (int)blockIdx.x < bp->lanes;
   bool first = true, ok = true;
+  // passes and their algorithmic bytes, counted by the last workgroup while the first
+  // residual phase keeps it idle (it owns no row when nwg > M)
+  const bool counter_wg = (int)blockIdx.x == bp->nwg - 1;
+  unsigned long long n_pass = 0, n_bytes = 0;
   while (ok) {
     if (lane_wg) lane_commit(bp, sh, call, first, dyn, A0);
     first = false;
     if (!(ok = grid_sync(bp, gen, sh))) break;
     for (int i = tid(); i < bp->lanes * kLaneInts; i += kThreads)
-      sh->ln[i / kLaneInts][i % kLaneInts] = (int)cld32(bp->lane + i);
+      sh->ln[i / kLaneInts][i % kLaneInts] = *G(bp->lane + i);
     __syncthreads();
     int any = 0;
     for (int i = 0; i < bp->lanes; ++i) any |= sh->ln[i][kLnActive];
@@ -865,6 +891,10 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
       if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
       ok = ok && grid_sync(bp, gen, sh);
       if (ok) phase_resid(bp, sh, bp->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, 0, dyn);
+      if (ok && l == 0 && counter_wg && tid() == 0) {
+        n_pass += 1;
+        n_bytes += pass_bytes_batch(bp, sh);
+      }
       ok = ok && grid_sync(bp, gen, sh);
       if (ok) phase_gu(bp, l, A0, A1, dyn);
       ok = ok && grid_sync(bp, gen, sh);
@@ -880,13 +910,13 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
     phase_heads(bp, sh, dyn);
     if (!(ok = grid_sync(bp, gen, sh))) break;
     phase_sample(bp, sh, call, dyn);
-    if (blockIdx.x == 0 && tid() == 0) {
-      bp->totals[0] += 1ull;
-      bp->totals[1] += pass_bytes_batch(bp, sh);
-    }
     if (!(ok = grid_sync(bp, gen, sh))) break;
   }
   if (!ok && lane_wg) lane_abort(bp, sh, call);
+  if (counter_wg && tid() == 0) {
+    bp->totals[0] = n_pass;
+    bp->totals[1] = n_bytes;
+  }
 }
 
 }  // namespace
