@@ -131,7 +131,7 @@ rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out);
  * independent frame streams the batched calls below decode together; with 1
  * only the single-frame calls are available. Batched streams need bf16
  * weights, max_streams * max(draft_len + 1, 2) <= 80 rows, hidden a multiple
- * of 256 and q width and ffn multiples of 128 (else EUNSUPPORTED).
+ * of 512 (at most 2048) and q width and ffn multiples of 256 (else EUNSUPPORTED).
  * A stream owns its device work buffers and pinned staging; use one host
  * thread per stream. */
 rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, rvqsd_stream** out);

@@ -191,8 +191,8 @@ int batch_setup(rvqsd_stream* s, int lanes) {
   if (c.dtype != RVQSD_DTYPE_BF16) return set_err(RVQSD_EUNSUPPORTED, "batched streams need bf16 weights");
   if (M > kBatchMaxRows)
     return set_err(RVQSD_EUNSUPPORTED, "max_streams * max(draft_len + 1, 2) = %d rows > %d", M, kBatchMaxRows);
-  if (k.H % 256 || k.qdim % 128 || k.F % 128 || k.H > 2048)
-    return set_err(RVQSD_EUNSUPPORTED, "batched streams need hidden %% 256 == 0 (<= 2048), q width and ffn %% 128 == 0");
+  if (k.H % 512 || k.qdim % 256 || k.F % 256 || k.H > 2048)
+    return set_err(RVQSD_EUNSUPPORTED, "batched streams need hidden %% 512 == 0 (<= 2048), q width and ffn %% 256 == 0");
   if (m->nwg < 8) return set_err(RVQSD_EUNSUPPORTED, "batched streams need at least 8 workgroups");
   BParams b;
   memset(&b, 0, sizeof(b));
@@ -200,9 +200,10 @@ int batch_setup(rvqsd_stream* s, int lanes) {
   b.rpl = rpl;
   b.M = M;
   b.nwg = m->nwg;
-  b.ks_qkv = pick_ks(k.H, 2, (k.nqkv + 63) / 64, m->nwg);
-  b.ks_o = pick_ks(k.qdim, 2, (k.H + 63) / 64, m->nwg);
-  b.ks_down = pick_ks(k.F, 2, (k.H + 63) / 64, m->nwg);
+  // 64-column units with the k range of a unit split over 4 waves (and over units by ks)
+  b.ks_qkv = pick_ks(k.H, 4, (k.nqkv + 63) / 64, m->nwg);
+  b.ks_o = pick_ks(k.qdim, 4, (k.H + 63) / 64, m->nwg);
+  b.ks_down = pick_ks(k.F, 4, (k.H + 63) / 64, m->nwg);
   b.hrows = M * (k.K + 1);
   b.sup_words = 1 + 2 * k.topk;
   const size_t kmax = (size_t)(k.H > k.qdim ? (k.H > k.F ? k.H : k.F) : (k.qdim > k.F ? k.qdim : k.F));
@@ -254,7 +255,7 @@ int batch_setup(rvqsd_stream* s, int lanes) {
     return set_err(RVQSD_EHIP, "batched buffers: %s", hipGetErrorString(e));
   }
   // LDS: projection tiles and the SiLU staging, attention rows, sampling arrays, one row
-  size_t lds = ((size_t)kWaves * kBatchMTiles * 256 + (size_t)kBatchMaxRows * 16) * 4;
+  size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
   const size_t attn = (size_t)(2 * kMaxRows + 2 * kMaxPos) * k.d * 4;
   const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + 3 * kMaxTopk * 8 + kMaxTopk * 4 + kTopkBuckets * 4;
   if (attn > lds) lds = attn;

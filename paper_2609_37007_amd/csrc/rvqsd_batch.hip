@@ -190,29 +190,39 @@ __device__ __forceinline__ bool head_slot_used(const KParams* p, const int* st, 
 // MFMA roles as in the frame kernel: A = 16 weight rows, B = 16 activation
 // rows; lane group q = lane / 16 covers the 16 consecutive k of a 64-wide step
 // in two instructions, and the activation chunk of 8 enters as bf16 hi + lo.
-template <int NTU, typename WRow, typename RowOf>
+template <int NTU, int NTW, typename WRow, typename RowOf>
 __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uint32_t* A, int lda, int mtiles,
                                           RowOf rowof, float* red) {
-  constexpr int KW = kWaves / NTU;
+  constexpr int NG = NTU / NTW, KW = kWaves / NG;
   const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6), lane = tid() & 63;
-  const int nt = wave % NTU, kw = wave / NTU;
+  const int ng = wave % NG, kw = wave / NG;
   const int kper = klen / KW;
   const int kb = k0 + kw * kper;
   const int q = lane >> 4, ml = lane & 15;
-  const bf16_t* wr = wrow(nt, ml);
-  const bf16_t* wp = wr ? wr + kb + 16 * q : nullptr;
+  const bf16_t* wp[NTW];
+#pragma unroll
+  for (int t = 0; t < NTW; ++t) {
+    const bf16_t* wr = wrow(ng * NTW + t, ml);
+    wp[t] = wr ? wr + kb + 16 * q : nullptr;
+  }
   int arow[kBatchMTiles];
 #pragma unroll
   for (int mt = 0; mt < kBatchMTiles; ++mt) arow[mt] = mt < mtiles ? rowof(16 * mt + ml) : -1;
-  f32x4 acc[kBatchMTiles];
+  f32x4 acc[NTW][kBatchMTiles];
 #pragma unroll
-  for (int mt = 0; mt < kBatchMTiles; ++mt) acc[mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < NTW; ++t)
+#pragma unroll
+    for (int mt = 0; mt < kBatchMTiles; ++mt) acc[t][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
   const int nsteps = kper >> 6;
   for (int u = 0; u < nsteps; ++u) {
-    W16 a0 = (W16)(0u), a1 = (W16)(0u);
-    if (wp) {
-      a0 = *G(reinterpret_cast<const W16*>(wp + 64 * u));
-      a1 = *G(reinterpret_cast<const W16*>(wp + 64 * u + 8));
+    W16 a0[NTW], a1[NTW];
+#pragma unroll
+    for (int t = 0; t < NTW; ++t) {
+      a0[t] = a1[t] = (W16)(0u);
+      if (wp[t]) {
+        a0[t] = *G(reinterpret_cast<const W16*>(wp[t] + 64 * u));
+        a1[t] = *G(reinterpret_cast<const W16*>(wp[t] + 64 * u + 8));
+      }
     }
     const int chunk = (kb + 64 * u + 16 * q) >> 3;
     W16 bh0[kBatchMTiles], bl0[kBatchMTiles], bh1[kBatchMTiles], bl1[kBatchMTiles];
@@ -227,33 +237,47 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
         bl1[mt] = load_w16(ap + 12);
       }
     }
-    const bf16x8 x0 = __builtin_bit_cast(bf16x8, a0), x1 = __builtin_bit_cast(bf16x8, a1);
 #pragma unroll
-    for (int mt = 0; mt < kBatchMTiles; ++mt) {
-      if (mt < mtiles) {
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bh0[mt]), acc[mt], 0, 0, 0);
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bl0[mt]), acc[mt], 0, 0, 0);
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bh1[mt]), acc[mt], 0, 0, 0);
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bl1[mt]), acc[mt], 0, 0, 0);
+    for (int t = 0; t < NTW; ++t) {
+      const bf16x8 x0 = __builtin_bit_cast(bf16x8, a0[t]), x1 = __builtin_bit_cast(bf16x8, a1[t]);
+#pragma unroll
+      for (int mt = 0; mt < kBatchMTiles; ++mt) {
+        if (mt < mtiles) {
+          acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bh0[mt]), acc[t][mt], 0, 0, 0);
+          acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bl0[mt]), acc[t][mt], 0, 0, 0);
+          acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bh1[mt]), acc[t][mt], 0, 0, 0);
+          acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bl1[mt]), acc[t][mt], 0, 0, 0);
+        }
       }
     }
   }
 #pragma unroll
-  for (int mt = 0; mt < kBatchMTiles; ++mt)
-    if (mt < mtiles)
-      *reinterpret_cast<f32x4*>(red + ((size_t)((kw * NTU + nt) * kBatchMTiles + mt) << 8) + 4 * lane) = acc[mt];
+  for (int t = 0; t < NTW; ++t)
+#pragma unroll
+    for (int mt = 0; mt < kBatchMTiles; ++mt)
+      if (mt < mtiles)
+        *reinterpret_cast<f32x4*>(red + ((size_t)((kw * NTU + ng * NTW + t) * kBatchMTiles + mt) << 8) + 4 * lane) =
+            acc[t][mt];
   __syncthreads();
   if (KW > 1) {
     for (int e = tid(); e < NTU * mtiles * 256; e += kThreads) {
       const int t = e / (mtiles * 256), rem = e - t * (mtiles * 256), mt = rem >> 8, x = rem & 255;
-      float s = red[((size_t)(t * kBatchMTiles + mt) << 8) + x];
+      float sum = red[((size_t)(t * kBatchMTiles + mt) << 8) + x];
 #pragma unroll
-      for (int k = 1; k < KW; ++k) s += red[((size_t)((k * NTU + t) * kBatchMTiles + mt) << 8) + x];
-      red[((size_t)(t * kBatchMTiles + mt) << 8) + x] = s;
+      for (int k = 1; k < KW; ++k) sum += red[((size_t)((k * NTU + t) * kBatchMTiles + mt) << 8) + x];
+      red[((size_t)(t * kBatchMTiles + mt) << 8) + x] = sum;
     }
     __syncthreads();
   }
 }
+// LDS floats of one unit's k-part tiles
+template <int NTU, int NTW>
+constexpr int gemm_red_floats() {
+  return kWaves / (NTU / NTW) * NTU * kBatchMTiles * 256;
+}
+constexpr int kProjNTW = 2, kGuNTW = 2;  // n-tiles per wave (activation fragments reused NTW times)
+static_assert(gemm_red_floats<4, kProjNTW>() <= kBatchRedFloats && gemm_red_floats<2, kGuNTW>() <= kBatchRedFloats,
+              "LDS reduction area");
 
 // ------------------------------------------------------------ projections
 
@@ -265,7 +289,7 @@ __device__ void proj_partial(const BParams* bp, const bf16_t* W, int N, int K, i
   float* part = bp->part;
   for (int u = blockIdx.x; u < units; u += bp->nwg) {
     const int g = u % cg, ks = u / cg, n0 = g * 16 * NTU;
-    gemm_unit<NTU>(
+    gemm_unit<NTU, kProjNTW>(
         [&](int nt, int m) -> const bf16_t* {
           const int f = n0 + 16 * nt + m;
           return f < N ? W + (size_t)f * K : nullptr;
@@ -292,10 +316,10 @@ __device__ void phase_gu(const BParams* bp, int l, const uint32_t* A, uint32_t* 
   const int M = bp->M, mtiles = (M + 15) >> 4, H = p->H, F = p->F;
   const bf16_t* wg = bw(p, boff(p, l, p->o_wg));
   const bf16_t* wu = bw(p, boff(p, l, p->o_wu));
-  float* act = red + (size_t)kWaves * kBatchMTiles * 256;  // [80][16]
+  float* act = red + gemm_red_floats<2, kGuNTW>();  // [80][16]
   for (int u = blockIdx.x; u < F / 16; u += bp->nwg) {
     const int f0 = u * 16;
-    gemm_unit<2>([&](int nt, int m) -> const bf16_t* { return (nt ? wu : wg) + (size_t)(f0 + m) * H; }, 0, H, A, H,
+    gemm_unit<2, kGuNTW>([&](int nt, int m) -> const bf16_t* { return (nt ? wu : wg) + (size_t)(f0 + m) * H; }, 0, H, A, H,
                  mtiles, [&](int i) { return i < M ? i : -1; }, red);
     for (int e = tid(); e < mtiles * 256; e += kThreads) {
       const int mt = e >> 8, x = e & 255, ln = x >> 2, v = x & 3;
@@ -493,7 +517,7 @@ __device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
     if (nr == 0) continue;
     const int n0 = gi * 64;
     const bf16_t* W = bw(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
-    gemm_unit<4>(
+    gemm_unit<4, kProjNTW>(
         [&](int nt, int m) -> const bf16_t* {
           const int f = n0 + 16 * nt + m;
           return f < V ? W + (size_t)f * H : nullptr;

@@ -85,6 +85,7 @@ int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int
 constexpr int kMaxLanes = 16;
 constexpr int kBatchMaxRows = 80;  // lanes * rpl: five 16-row MFMA tiles
 constexpr int kBatchMTiles = kBatchMaxRows / 16;
+constexpr int kBatchRedFloats = 16 * kBatchMTiles * 256;  // LDS partial tiles of one MFMA unit (k parts x n-tiles)
 // lane state record (int32 words)
 constexpr int kLnActive = 0, kLnFrame = 1, kLnPass = 2, kLnM = 3, kLnKp = 4, kLnFirst = 5, kLnRows = 6,
               kLnPrevAnchor = 7, kLnCalls = 8, kLnRounds = 9, kLnDrafted = 10, kLnAccepted = 11, kLnMask = 12,
