@@ -41,7 +41,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "RVQ codes/sec single-stream; accepted tok/call; verify-step GB/s vs roofline"
-KERNEL_SOURCES = ("paper_2609_37007_amd/csrc/rvqsd_frame.hip", "paper_2609_37007_amd/csrc/rvqsd_internal.h")
+KERNEL_SOURCES = ("paper_2609_37007_amd/csrc/rvqsd_frame.hip", "paper_2609_37007_amd/csrc/rvqsd_device.h",
+                  "paper_2609_37007_amd/csrc/rvqsd_internal.h")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "frame_kernel_mcd1024_k4_hbm_traffic.txt")
 
 WORKLOADS = {
@@ -90,7 +91,23 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--streams", type=int, default=1, help="independent streams verified together (1..16)")
     ap.add_argument("--frames-per-stream", type=int, default=500)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
+                    help="only run 5 plain device copies of MB MiB (the reference kernel for HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_calibration(mb: int) -> int:
+    """Plain device-to-device copies of known size: rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE of
+    this run give the counter reading per byte moved, used to scale the frame kernel's readings."""
+    import torch
+    n = mb * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": n * 4, "launches": 5}), flush=True)
+    return 0
 
 
 def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order):
@@ -251,6 +268,8 @@ def main() -> int:
               "has no multi-GPU path (independent streams would shard across GPUs with no exchange). "
               "Run with --gpus 1.", file=sys.stderr)
         return 2
+    if a.copy_calibration:
+        return copy_calibration(a.copy_calibration)
     if a.streams > 1:
         return run_streams(a)
 
