@@ -77,6 +77,7 @@ def lib():
         L.orc_set_threads.argtypes = [i32]
         L.orc_get_threads.restype = i32
         L.orc_forward.argtypes = [vp, vp, vp, i32, vp]
+        L.orc_forward_vectors.argtypes = [vp, vp, i32, vp]
         L.orc_logits.argtypes = [vp, vp, i32, i32, vp]
         L.orc_topk_softmax.argtypes = [vp, i32, i32, f64, vp, vp]
         L.orc_sample.argtypes = [vp, vp, i32, f64]
@@ -86,7 +87,7 @@ def lib():
         L.orc_uniforms_from_seed.argtypes = [ctypes.c_uint64, i32, vp]
         L.orc_splitmix64_at.restype = ctypes.c_uint64
         L.orc_splitmix64_at.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
-        for name in ("orc_forward", "orc_logits", "orc_topk_softmax", "orc_sample", "orc_accept_or_resample",
+        for name in ("orc_forward", "orc_forward_vectors", "orc_logits", "orc_topk_softmax", "orc_sample", "orc_accept_or_resample",
                      "orc_ar_frame", "orc_spec_frame", "orc_abi_version"):
             getattr(L, name).restype = i32
         _lib = L
@@ -148,6 +149,13 @@ class Oracle:
         n_pos = ic.size + 1
         out = np.zeros((n_pos, self.H), dtype=np.float64)
         _check(lib().orc_forward(self._h, _ptr(f), _ptr(ic) if ic.size else None, n_pos, _ptr(out)), "orc_forward")
+        return out
+
+    def forward_vectors(self, rows: np.ndarray) -> np.ndarray:
+        """Final-normed hidden states of positions 0..n-1 for input rows [n][H] (fp64)."""
+        x = np.ascontiguousarray(rows, dtype=np.float64)
+        out = np.zeros_like(x)
+        _check(lib().orc_forward_vectors(self._h, _ptr(x), x.shape[0], _ptr(out)), "orc_forward_vectors")
         return out
 
     def logits(self, h: np.ndarray, head: int, offset: int = 0) -> np.ndarray:
@@ -239,3 +247,39 @@ def set_threads(n: int):
 
 def get_threads() -> int:
     return int(lib().orc_get_threads())
+
+
+def pipeline_frames(outer: Oracle, emb0: np.ndarray, tables: np.ndarray, inner: Oracle, t: np.ndarray,
+                    u_c0: np.ndarray, uni: np.ndarray, topk: int, temperature: float):
+    """The full per-frame pipeline of Fig. 1 from scratch (test reference).
+
+    Frame i: the outer decoder's input is x_i = t_i + E_0[c_0] + sum_j E_j[c_j] of frame
+    i - 1 (x_0 = t_0); the outer decoder runs over x_0..x_i (positions 0..i) and its
+    final-normed hidden h_i gives the c_0 logits through its head; entries at or above
+    the inner codebook size are masked (codes the inner tables cannot embed); c_0 is the
+    top-k, temperature-T sample at u_c0[i]; the inner loop decodes c_1..c_15 from
+    (float32(h_i), c_0) with the frame's uniforms.  emb0: [V_outer][H] (outer E_0);
+    tables: [15][V_inner][H].  Returns codes [n][16], inner stats, and the h_i [n][H].
+    """
+    n, H = t.shape
+    V_in = inner.V
+    rows, codes, stats, hs = [], [], [], []
+    prev = None
+    for i in range(n):
+        x = t[i].astype(np.float64)
+        if prev is not None:
+            x = x + emb0[prev[0]].astype(np.float64)
+            for j in range(1, len(prev)):
+                x = x + tables[j - 1][prev[j]].astype(np.float64)
+        rows.append(x)
+        h = outer.forward_vectors(np.stack(rows))[-1]
+        lg = outer.logits(h, 1)
+        lg[V_in:] = -np.inf
+        idx, p = topk_softmax(lg, topk, temperature)
+        c0 = sample(idx, p, float(u_c0[i]))
+        c, st, _ = inner.spec_frame(h.astype(np.float32), c0, uni[i])
+        prev = [c0] + [int(v) for v in c]
+        codes.append(prev)
+        stats.append(st)
+        hs.append(h)
+    return np.array(codes, dtype=np.int32), stats, np.stack(hs)

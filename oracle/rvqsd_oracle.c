@@ -218,16 +218,12 @@ static void rope(double* v, int d, int pos, double base) {
 
 static double silu(double z) { return z / (1.0 + exp(-z)); }
 
-int32_t orc_forward(orc_model* m, const float* frame_hidden, const int32_t* in_codes, int32_t n_pos, double* hfin) {
-  if (!m || !frame_hidden || !hfin || n_pos < 1 || n_pos > m->cfg.n_codes + 1 || (n_pos > 1 && !in_codes))
-    return ORC_EINVAL;
+/* The decoder stack over input rows x[np][H] (overwritten): positions 0..np-1,
+ * causal attention, final RMSNorm into hfin[np][H]. */
+static int32_t forward_rows(orc_model* m, double* x, int32_t np, double* hfin) {
   const orc_cfg* c = &m->cfg;
   const int H = c->hidden, d = c->head_dim, nq = c->n_q_heads, nkv = c->n_kv_heads, F = c->ffn;
-  const int qd = nq * d, kd = nkv * d, rep = nq / nkv, np = n_pos;
-  for (int s = 1; s < np; ++s)
-    if (in_codes[s - 1] < 0 || in_codes[s - 1] >= c->vocab) return ORC_EINVAL;
-
-  double* x = (double*)malloc(sizeof(double) * np * H);
+  const int qd = nq * d, kd = nkv * d, rep = nq / nkv;
   double* a = (double*)malloc(sizeof(double) * np * H);
   double* Q = (double*)malloc(sizeof(double) * np * qd);
   double* Kc = (double*)malloc(sizeof(double) * np * kd);
@@ -236,17 +232,10 @@ int32_t orc_forward(orc_model* m, const float* frame_hidden, const int32_t* in_c
   double* Y = (double*)malloc(sizeof(double) * np * (H > F ? H : F));
   double* G = (double*)malloc(sizeof(double) * np * F);
   double* U = (double*)malloc(sizeof(double) * np * F);
-  double* tmp = (double*)malloc(sizeof(double) * (d > MAX_POS ? d : MAX_POS));
-  if (!x || !a || !Q || !Kc || !Vc || !O || !Y || !G || !U || !tmp) {
-    free(x); free(a); free(Q); free(Kc); free(Vc); free(O); free(Y); free(G); free(U); free(tmp);
+  double* tmp = (double*)malloc(sizeof(double) * (d > np ? d : np));
+  if (!a || !Q || !Kc || !Vc || !O || !Y || !G || !U || !tmp) {
+    free(a); free(Q); free(Kc); free(Vc); free(O); free(Y); free(G); free(U); free(tmp);
     return ORC_ENOMEM;
-  }
-
-  /* inputs: x_0 = frame hidden, x_s = E_{s-1}[code consumed at s] */
-  for (int i = 0; i < H; ++i) x[i] = (double)frame_hidden[i];
-  for (int s = 1; s < np; ++s) {
-    const float* e = m->emb[s - 1] + (size_t)in_codes[s - 1] * H;
-    for (int i = 0; i < H; ++i) x[(size_t)s * H + i] = (double)e[i];
   }
 
   const double scale = 1.0 / sqrt((double)d);
@@ -310,8 +299,39 @@ int32_t orc_forward(orc_model* m, const float* frame_hidden, const int32_t* in_c
   }
   for (int p = 0; p < np; ++p) rmsnorm(x + (size_t)p * H, m->final_norm, H, c->rms_eps, hfin + (size_t)p * H);
 
-  free(x); free(a); free(Q); free(Kc); free(Vc); free(O); free(Y); free(G); free(U); free(tmp);
+  free(a); free(Q); free(Kc); free(Vc); free(O); free(Y); free(G); free(U); free(tmp);
   return ORC_OK;
+}
+
+int32_t orc_forward(orc_model* m, const float* frame_hidden, const int32_t* in_codes, int32_t n_pos, double* hfin) {
+  if (!m || !frame_hidden || !hfin || n_pos < 1 || n_pos > m->cfg.n_codes + 1 || (n_pos > 1 && !in_codes))
+    return ORC_EINVAL;
+  const orc_cfg* c = &m->cfg;
+  const int H = c->hidden, np = n_pos;
+  for (int s = 1; s < np; ++s)
+    if (in_codes[s - 1] < 0 || in_codes[s - 1] >= c->vocab) return ORC_EINVAL;
+  double* x = (double*)malloc(sizeof(double) * np * H);
+  if (!x) return ORC_ENOMEM;
+  /* inputs: x_0 = frame hidden, x_s = E_{s-1}[code consumed at s] */
+  for (int i = 0; i < H; ++i) x[i] = (double)frame_hidden[i];
+  for (int s = 1; s < np; ++s) {
+    const float* e = m->emb[s - 1] + (size_t)in_codes[s - 1] * H;
+    for (int i = 0; i < H; ++i) x[(size_t)s * H + i] = (double)e[i];
+  }
+  const int32_t st = forward_rows(m, x, np, hfin);
+  free(x);
+  return st;
+}
+
+int32_t orc_forward_vectors(orc_model* m, const double* rows, int32_t n_pos, double* hfin) {
+  if (!m || !rows || !hfin || n_pos < 1 || n_pos > ORC_MAX_VECTOR_POS) return ORC_EINVAL;
+  const size_t cnt = (size_t)n_pos * m->cfg.hidden;
+  double* x = (double*)malloc(sizeof(double) * cnt);
+  if (!x) return ORC_ENOMEM;
+  memcpy(x, rows, sizeof(double) * cnt);
+  const int32_t st = forward_rows(m, x, n_pos, hfin);
+  free(x);
+  return st;
 }
 
 int32_t orc_logits(orc_model* m, const double* h, int32_t head, int32_t offset, double* out) {

@@ -93,6 +93,12 @@ int32_t orc_get_threads(void);
 /* Final-normed hidden states h_0..h_{n_pos-1}; in_codes[s-1] is the code
  * consumed at position s (s >= 1). hfin: [n_pos][H]. */
 int32_t orc_forward(orc_model* m, const float* frame_hidden, const int32_t* in_codes, int32_t n_pos, double* hfin);
+
+/* The same decoder stack over caller-given input rows (fp64 [n_pos][hidden]) at
+ * positions 0..n_pos-1: the outer CodeDecoder of Fig. 1, whose input per frame
+ * is a vector, not an embedded code. Final-normed hidden states into hfin. */
+#define ORC_MAX_VECTOR_POS 4096
+int32_t orc_forward_vectors(orc_model* m, const double* rows, int32_t n_pos, double* hfin);
 /* LMH_head (1..n_codes) applied to h (+ b_offset if offset >= 1). out: [vocab]. */
 int32_t orc_logits(orc_model* m, const double* h, int32_t head, int32_t offset, double* out);
 

@@ -77,6 +77,35 @@ MCD_1024 = ModelShape(n_layers=5, hidden=1024, n_q_heads=16, n_kv_heads=8, head_
                       ffn=3072, n_codes=15, vocab=2048, max_draft=14, dtype=DTYPE_BF16)
 
 
+# The outer CodeDecoder of the full pipeline (Fig. 1): 28 layers of the same block, one
+# code table (E_0 over its 3072-entry codebook) and one head in the blob layout above
+# (n_codes = 1, max_draft = 0); the 15 tables of the residual codes come separately
+# (make_outer_tables).
+OUTER_1024 = ModelShape(n_layers=28, hidden=1024, n_q_heads=16, n_kv_heads=8, head_dim=128,
+                        ffn=3072, n_codes=1, vocab=3072, max_draft=0, dtype=DTYPE_BF16)
+
+
+def make_outer_tables(s: ModelShape, n_tables: int, vocab: int, seed: int = 5, std: float = 0.02) -> bytes:
+    """Embedding tables E_1..E_n of the residual codes for the outer decoder's input:
+    [n_tables][vocab][hidden] in the matrix dtype of s, N(0, std) drawn in that order."""
+    v = (np.random.default_rng(seed).standard_normal((n_tables, vocab, s.hidden)) * std).astype(np.float32)
+    return v.tobytes() if s.dtype == DTYPE_F32 else f32_to_bf16_bits(v).tobytes()
+
+
+def unpack_outer_tables(s: ModelShape, blob: bytes, n_tables: int, vocab: int) -> np.ndarray:
+    if s.dtype == DTYPE_F32:
+        return np.frombuffer(blob, dtype=np.float32).reshape(n_tables, vocab, s.hidden).copy()
+    return bf16_bits_to_f32(np.frombuffer(blob, dtype=np.uint16)).reshape(n_tables, vocab, s.hidden)
+
+
+def pipeline_inputs(s: ModelShape, frames: int, seed_t: int = 3, seed_u: int = 4):
+    """Per-frame text-side input vectors t_i ~ N(0,1) [frames, H] float32 and the uniform of
+    each frame's c_0 draw [frames] float32 (prefix-stable)."""
+    t = np.random.default_rng(seed_t + 1000).standard_normal((frames, s.hidden)).astype(np.float32)
+    u = np.minimum(np.random.default_rng(seed_u).random(frames), 1.0 - 2.0 ** -24).astype(np.float32)
+    return t, u
+
+
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 to bfloat16 (nearest even); returns the uint16 bit patterns."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)

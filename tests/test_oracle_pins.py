@@ -169,14 +169,18 @@ def test_residual_without_mass_falls_back_to_p():
 
 # ------------------------------------------------------------ forward pass
 
-def _torch_forward(s, W, f, in_codes, eps=1e-6, base=1e6):
-    """Independent fp64 rebuild from PyTorch library routines; RoPE in complex form."""
+def _torch_forward(s, W, f, in_codes, eps=1e-6, base=1e6, rows=None):
+    """Independent fp64 rebuild from PyTorch library routines; RoPE in complex form.
+    rows: input vectors [n][H] instead of (f, embedded codes)."""
     import torch
     import torch.nn.functional as F
     t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64))
     H, d, nq, nkv = s.hidden, s.head_dim, s.n_q_heads, s.n_kv_heads
-    rows = [t(f)] + [t(W[f"emb{i}"][c]) for i, c in enumerate(in_codes)]
-    x = torch.stack(rows)
+    if rows is None:
+        rows = [t(f)] + [t(W[f"emb{i}"][c]) for i, c in enumerate(in_codes)]
+        x = torch.stack(rows)
+    else:
+        x = t(rows)
     n = x.shape[0]
     pos = torch.arange(n, dtype=torch.float64)
     inv = base ** (-torch.arange(0, d // 2, dtype=torch.float64) * 2.0 / d)
@@ -243,6 +247,42 @@ def test_forward_matches_torch_rebuild(shape_name, std):
         np.testing.assert_allclose(orc.logits(h[1], 1 + j, j),
                                    W[f"lmh{1 + j}"].astype(np.float64) @ (ref[1] + W["offsets"][j - 1]),
                                    rtol=0, atol=1e-9)
+
+
+def test_forward_vectors_is_the_code_forward_on_embedded_rows():
+    """Vector inputs (the outer decoder's form) reduce to the code forward when the rows
+    are the frame hidden and the embedded codes: bit for bit."""
+    s = S.ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, n_codes=6, vocab=32,
+                     max_draft=5, dtype=S.DTYPE_BF16)
+    blob = S.make_weights(s, seed=4, std=0.2)
+    W = S.unpack_weights(s, blob)
+    orc = Hh.make_oracle(s, blob, topk=4, temperature=0.9, draft_len=1)
+    f, c0 = S.frame_inputs(s, 1)
+    codes = [int(c0[0]), 3, 17, 5, 30, 1]
+    rows = [f[0].astype(np.float64)] + [W[f"emb{i}"][c].astype(np.float64) for i, c in enumerate(codes)]
+    a = orc.forward(f[0], codes)
+    b = orc.forward_vectors(np.stack(rows))
+    assert np.array_equal(a, b)
+    orc.close()
+
+
+def test_forward_vectors_long_sequence_matches_torch_rebuild():
+    """40 positions (beyond a frame's 16): RoPE at large positions and long causal attention
+    against the independent rebuild; a later row never changes an earlier hidden state."""
+    s = S.ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, n_codes=1, vocab=48,
+                     max_draft=0, dtype=S.DTYPE_BF16)
+    blob = S.make_weights(s, seed=6, std=0.2)
+    W = S.unpack_weights(s, blob)
+    orc = Hh.make_oracle(s, blob, topk=4, temperature=0.9, draft_len=0)
+    rows = np.random.default_rng(11).standard_normal((40, s.hidden))
+    h = orc.forward_vectors(rows)
+    ref = _torch_forward(s, W, None, None, rows=rows)
+    assert np.max(np.abs(h - ref)) < 1e-9
+    rows2 = rows.copy()
+    rows2[25:] += 1.0
+    h2 = orc.forward_vectors(rows2)
+    assert np.array_equal(h[:25], h2[:25]) and not np.allclose(h[25:], h2[25:])
+    orc.close()
 
 
 def test_rope_position_zero_is_identity_and_rows_are_causal():
