@@ -184,6 +184,39 @@ rvqsd_status rvqsd_decode_frames_batched_async(rvqsd_stream* s, int32_t n, const
  * KV cache read). Synchronises the stream. */
 rvqsd_status rvqsd_batch_totals(rvqsd_stream* s, uint64_t* passes, uint64_t* bytes);
 
+/* ---- Outer CodeDecoder step and the full per-frame pipeline (Fig. 1) ----
+ * The outer decoder emits c_0 once per frame from an input vector that adds the
+ * frame's text-side vector t and the embeddings of the previous frame's 16
+ * codes; its final-normed hidden state is the inner loop's frame_hidden.
+ * outer_model: a model created with rvqsd_create from the outer decoder's blob
+ * (same block layout; n_codes = 1: its E_0 table over the outer codebook and its
+ * head; max_draft = draft_len = 0). code_tables: host, [n_tables][table_vocab]
+ * [hidden] bf16, the embeddings of codes 1..n_tables (copied). c_0 is a top-k,
+ * temperature-T draw over the first min(outer vocab, table_vocab) logits (the
+ * codes the inner model can embed). max_frames (<= 4096) bounds the KV cache,
+ * which grows by one position per frame until rvqsd_outer_reset. bf16 only,
+ * hidden a multiple of 512 (<= 2048), q width and ffn multiples of 256. */
+typedef struct rvqsd_outer rvqsd_outer;
+rvqsd_status rvqsd_outer_create(rvqsd_model* outer_model, const void* code_tables, int32_t n_tables,
+                                int32_t table_vocab, int32_t topk, double temperature, int32_t max_frames,
+                                rvqsd_outer** out);
+void rvqsd_outer_destroy(rvqsd_outer* o);
+/* Next frame is position 0 again (no previous codes). Call when the stream is idle. */
+rvqsd_status rvqsd_outer_reset(rvqsd_outer* o);
+
+/* Enqueue n frames of the full pipeline on the inner stream s (device pointers,
+ * returns after the launches): per frame one outer step (c_0 and the hidden
+ * state) and one inner frame decode (c_1..c_15), chained on the device with no
+ * host synchronisation. d_t float[n][hidden]; d_u_c0 float[n] (uniform of each
+ * c_0 draw); d_uniforms float[n][n_codes][3] (inner uniforms); d_codes out
+ * int32[n][1 + n_codes] (c_0, c_1..c_n); d_stats out rvqsd_stats[n] (inner
+ * loop; an outer-step error shows as c_0 = -1 and status EINVAL); d_hidden out
+ * float[n][hidden] or NULL. The outer tables must match the inner model
+ * (n_tables = n_codes, table_vocab = vocab); EUNSUPPORTED beyond max_frames. */
+rvqsd_status rvqsd_pipeline_frames_async(rvqsd_stream* s, rvqsd_outer* o, int32_t n, const float* d_t,
+                                         const float* d_u_c0, const float* d_uniforms, int32_t* d_codes,
+                                         rvqsd_stats* d_stats, float* d_hidden);
+
 /* Return a stream to its initial state. Needed after a frame enqueued with
  * rvqsd_decode_frame_async reported a device-side error in its stats (later
  * frames on the stream then fail with RVQSD_EHIP until the reset); the

@@ -101,6 +101,20 @@ struct rvqsd_stream {
   size_t bstage_bytes;
 };
 
+struct rvqsd_outer {
+  rvqsd_model* m;       // the outer decoder (blob with one code table and one head)
+  void* buf;            // device buffers and parameter blocks
+  OParams op;           // host copy
+  OParams* dop;         // device copy
+  KParams* dkp;         // device copy of the outer model's parameter block
+  int32_t* last_codes;  // device [1 + n_tables]: codes of the last frame of the previous call
+  float* f;             // device [H]: hidden state handed to the inner loop when the caller keeps none
+  size_t sync_bytes;    // barrier and status words at the start of buf
+  size_t lds;
+  int pos;              // frames decoded since the last reset
+  int n_tables;
+};
+
 namespace {
 
 int validate_cfg(const rvqsd_cfg* c, int nwg) {
@@ -736,6 +750,162 @@ rvqsd_status rvqsd_batch_totals(rvqsd_stream* s, uint64_t* passes, uint64_t* byt
   HIPCHK(hipMemcpy(t, s->bp.totals, sizeof(t), hipMemcpyDeviceToHost));
   *passes = t[0];
   *bytes = t[1];
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t n_tables, int32_t table_vocab,
+                                int32_t topk, double temperature, int32_t max_frames, rvqsd_outer** out) {
+  if (!m || !out || (n_tables > 0 && !code_tables)) return set_err(RVQSD_EINVAL, "null argument");
+  *out = nullptr;
+  const KParams& k = m->base;
+  if (n_tables < 0 || n_tables > kMaxCodes || table_vocab < 1 || topk < 1 || topk > kMaxTopk ||
+      !(temperature > 0.0) || max_frames < 1 || max_frames > 4096)
+    return set_err(RVQSD_EINVAL, "invalid outer-step argument");
+  if (m->cfg.dtype != RVQSD_DTYPE_BF16) return set_err(RVQSD_EUNSUPPORTED, "the outer step needs bf16 weights");
+  if (k.H % 512 || k.qdim % 256 || k.F % 256 || k.H > 2048 || m->nwg < 8)
+    return set_err(RVQSD_EUNSUPPORTED, "the outer step needs hidden %% 512 == 0 (<= 2048), q width and ffn %% 256 == 0");
+  rvqsd_outer* o = new (std::nothrow) rvqsd_outer;
+  if (!o) return set_err(RVQSD_ENOMEM, "host allocation");
+  memset(o, 0, sizeof(*o));
+  o->m = m;
+  o->n_tables = n_tables;
+  OParams b;
+  memset(&b, 0, sizeof(b));
+  b.nwg = m->nwg;
+  b.M = 1;
+  b.ks_qkv = pick_ks(k.H, 4, (k.nqkv + 63) / 64, m->nwg);
+  b.ks_o = pick_ks(k.qdim, 4, (k.H + 63) / 64, m->nwg);
+  b.ks_down = pick_ks(k.F, 4, (k.H + 63) / 64, m->nwg);
+  b.n_tables = n_tables;
+  b.table_vocab = table_vocab;
+  b.max_frames = max_frames;
+  b.topk = topk;
+  b.temperature = temperature;
+  const size_t kmax = (size_t)(k.H > k.qdim ? (k.H > k.F ? k.H : k.F) : (k.qdim > k.F ? k.qdim : k.F));
+  size_t part = (size_t)b.ks_qkv * k.nqkv;
+  if ((size_t)b.ks_o * k.H > part) part = (size_t)b.ks_o * k.H;
+  if ((size_t)b.ks_down * k.H > part) part = (size_t)b.ks_down * k.H;
+  const size_t tab_bytes = (size_t)n_tables * table_vocab * k.H * 2;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return at;
+  };
+  const size_t o_bar = take(10 * 64 * 4), o_status = take(4);
+  const size_t sync_bytes = off;
+  const size_t o_tab = take(tab_bytes), o_rope = take((size_t)max_frames * k.d * 4), o_x = take((size_t)k.H * 4),
+               o_a = take(2 * kmax * 4), o_part = take(part * 4),
+               o_kv = take((size_t)k.L * k.nkv * max_frames * 2 * k.d * 4),
+               o_apart = take((size_t)k.nq * kAttnChunks * (k.d + 2) * 4), o_log = take((size_t)k.V * 4),
+               o_last = take((size_t)(1 + kMaxCodes) * 4), o_f = take((size_t)k.H * 4), o_op = take(sizeof(OParams)),
+               o_kp = take(sizeof(KParams));
+  hipError_t e = dev_alloc(&o->buf, off);
+  if (e != hipSuccess) {
+    delete o;
+    return set_err(RVQSD_ENOMEM, "outer-step buffers (%zu bytes): %s", off, hipGetErrorString(e));
+  }
+  uint8_t* base = (uint8_t*)o->buf;
+  b.k = (const KParams*)(base + o_kp);
+  b.bar = (uint32_t*)(base + o_bar);
+  b.status = (int32_t*)(base + o_status);
+  b.tables = (const uint16_t*)(base + o_tab);
+  b.rope = (const float*)(base + o_rope);
+  b.x = (float*)(base + o_x);
+  b.a = (uint32_t*)(base + o_a);
+  b.part = (float*)(base + o_part);
+  b.kv = (float*)(base + o_kv);
+  b.apart = (float*)(base + o_apart);
+  b.logits = (float*)(base + o_log);
+  o->last_codes = (int32_t*)(base + o_last);
+  o->f = (float*)(base + o_f);
+  o->dop = (OParams*)(base + o_op);
+  o->dkp = (KParams*)(base + o_kp);
+  o->op = b;
+  o->sync_bytes = sync_bytes;
+  e = hipMemset(o->buf, 0, off);
+  if (e == hipSuccess && tab_bytes) e = hipMemcpy((void*)b.tables, code_tables, tab_bytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(o->dop, &o->op, sizeof(OParams), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(o->dkp, &m->base, sizeof(KParams), hipMemcpyHostToDevice);
+  if (e == hipSuccess) {
+    // rotary table of every frame position, computed in double
+    const int half = k.d / 2;
+    float* tab = (float*)malloc((size_t)max_frames * half * 2 * sizeof(float));
+    if (!tab) e = hipErrorOutOfMemory;
+    for (int pos = 0; tab && pos < max_frames; ++pos)
+      for (int i = 0; i < half; ++i) {
+        const double th = (double)pos * pow(k.rope_base, -2.0 * (double)i / (double)k.d);
+        tab[(pos * half + i) * 2 + 0] = (float)cos(th);
+        tab[(pos * half + i) * 2 + 1] = (float)sin(th);
+      }
+    if (tab) e = hipMemcpy((void*)b.rope, tab, (size_t)max_frames * half * 2 * sizeof(float), hipMemcpyHostToDevice);
+    free(tab);
+  }
+  if (e != hipSuccess) {
+    (void)hipFree(o->buf);
+    delete o;
+    return set_err(RVQSD_EHIP, "outer-step set-up: %s", hipGetErrorString(e));
+  }
+  size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
+  const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + kMaxTopk * 8 + kTopkBuckets * 4;
+  const size_t attn = ((size_t)3 * k.d + (max_frames + kAttnChunks - 1) / kAttnChunks) * 4;
+  if (samp > lds) lds = samp;
+  if (attn > lds) lds = attn;
+  if ((size_t)k.H * 4 > lds) lds = (size_t)k.H * 4;
+  o->lds = lds + 64;
+  *out = o;
+  return RVQSD_OK;
+}
+
+void rvqsd_outer_destroy(rvqsd_outer* o) {
+  if (!o) return;
+  (void)hipDeviceSynchronize();
+  (void)hipFree(o->buf);
+  delete o;
+}
+
+rvqsd_status rvqsd_outer_reset(rvqsd_outer* o) {
+  if (!o) return set_err(RVQSD_EINVAL, "null argument");
+  o->pos = 0;
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_pipeline_frames_async(rvqsd_stream* s, rvqsd_outer* o, int32_t n, const float* d_t,
+                                         const float* d_u_c0, const float* d_uniforms, int32_t* d_codes,
+                                         rvqsd_stats* d_stats, float* d_hidden) {
+  if (!s || !o) return set_err(RVQSD_EINVAL, "null argument");
+  if (n < 0) return set_err(RVQSD_EINVAL, "n = %d < 0", n);
+  if (n == 0) return RVQSD_OK;
+  if (!d_t || !d_u_c0 || !d_uniforms || !d_codes || !d_stats) return set_err(RVQSD_EINVAL, "null argument");
+  const rvqsd_cfg& ic = s->m->cfg;
+  const KParams& ok = o->m->base;
+  if (ic.hidden != ok.H) return set_err(RVQSD_EINVAL, "inner hidden %d != outer hidden %d", ic.hidden, ok.H);
+  if (o->n_tables != ic.n_codes || o->op.table_vocab != ic.vocab)
+    return set_err(RVQSD_EINVAL, "outer code tables (%d x %d) do not match the inner model (%d codes of %d)",
+                   o->n_tables, o->op.table_vocab, ic.n_codes, ic.vocab);
+  if (o->pos + n > o->op.max_frames)
+    return set_err(RVQSD_EUNSUPPORTED, "%d frames after %d exceed the outer KV capacity %d", n, o->pos,
+                   o->op.max_frames);
+  const int nc = ic.n_codes, H = ok.H;
+  float* fbuf = d_hidden;
+  for (int i = 0; i < n; ++i) {
+    HIPCHK(hipMemsetAsync(o->buf, 0, o->sync_bytes, s->stream));
+    OCall c;
+    c.t = d_t + (size_t)i * H;
+    c.u_c0 = d_u_c0 + i;
+    c.prev_codes = o->pos == 0 ? nullptr : (i > 0 ? d_codes + (size_t)(i - 1) * (1 + nc) : o->last_codes);
+    c.c0_out = d_codes + (size_t)i * (1 + nc);
+    c.hidden_out = fbuf ? fbuf + (size_t)i * H : o->f;
+    c.pos = o->pos;
+    char err[256];
+    int st = launch_outer(o->dop, c, o->m->nwg, (void*)s->stream, o->lds, err, sizeof(err));
+    if (st) return set_err(st, "%s", err);
+    st = launch_one(s, c.hidden_out, c.c0_out, d_uniforms + (size_t)i * nc * 3, c.c0_out + 1, d_stats + i);
+    if (st) return st;
+    o->pos += 1;
+  }
+  HIPCHK(hipMemcpyAsync(o->last_codes, d_codes + (size_t)(n - 1) * (1 + nc), (size_t)(1 + nc) * 4,
+                        hipMemcpyDeviceToDevice, s->stream));
   return RVQSD_OK;
 }
 

@@ -82,7 +82,8 @@ __device__ __forceinline__ const float* bfw(const KParams* p, uint64_t off) {
 }
 __device__ __forceinline__ uint64_t boff(const KParams* p, int l, uint64_t o) { return (uint64_t)l * p->layer_stride + o; }
 
-__device__ __forceinline__ void raise_status(const BParams* bp, int code) {
+template <typename BP>
+__device__ __forceinline__ void raise_status(const BP* bp, int code) {
   int expected = 0;
   __hip_atomic_compare_exchange_strong(G(bp->status), &expected, code, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT);
@@ -106,7 +107,8 @@ struct BShared {
 // Arrival counts per XCD group (workgroup w is counted in group w % 8), the
 // last arrival of a group bumps the top counter, the last group publishes the
 // generation. Before arriving, every wave waits for its own stores.
-__device__ bool grid_sync(const BParams* bp, uint32_t& gen, BShared* sh) {
+template <typename BP>
+__device__ bool grid_sync(const BP* bp, uint32_t& gen, BShared* sh) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   ++gen;
@@ -282,8 +284,8 @@ static_assert(gemm_red_floats<4, kProjNTW>() <= kBatchRedFloats && gemm_red_floa
 // ------------------------------------------------------------ projections
 
 // Y partial sums: part[ks][i][n] = sum over k in split ks of A[i][k] W[n][k], for every row i < M.
-template <int NTU>
-__device__ void proj_partial(const BParams* bp, const bf16_t* W, int N, int K, int KS, const uint32_t* A, float* red) {
+template <int NTU, typename BP>
+__device__ void proj_partial(const BP* bp, const bf16_t* W, int N, int K, int KS, const uint32_t* A, float* red) {
   const int M = bp->M, mtiles = (M + 15) >> 4;
   const int cg = (N + 16 * NTU - 1) / (16 * NTU), units = cg * KS, klen = K / KS;
   float* part = bp->part;
@@ -311,7 +313,8 @@ __device__ void proj_partial(const BParams* bp, const bf16_t* W, int N, int K, i
 
 // gate/up: n-tile 0 = gate rows f0 .. f0 + 15, n-tile 1 = the same up rows, full k;
 // act = SiLU(gate) * up goes straight to the split input of the down projection.
-__device__ void phase_gu(const BParams* bp, int l, const uint32_t* A, uint32_t* Aout, float* red) {
+template <typename BP>
+__device__ void phase_gu(const BP* bp, int l, const uint32_t* A, uint32_t* Aout, float* red) {
   const KParams* p = bp->k;
   const int M = bp->M, mtiles = (M + 15) >> 4, H = p->H, F = p->F;
   const bf16_t* wg = bw(p, boff(p, l, p->o_wg));
@@ -943,6 +946,267 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
   }
 }
 
+// ------------------------------------------------------------ outer decoder step
+// One position of the outer CodeDecoder (Fig. 1): input row x = t + E_0[c_0] +
+// sum_j E_j[c_j] of the previous frame, the decoder stack with the KV cache of
+// all earlier frames, the head's logits over the codes the inner tables can
+// embed, and a top-k, temperature-T draw of c_0. Same phase chain as the batched
+// kernel with M = 1; attention is split over key chunks (16 per query head) whose
+// partial softmax sums are merged by a second phase.
+
+// row set-up (workgroup 0): x and the split, normalised layer-0 input
+__device__ void outer_input(const OParams* op, BShared* sh, const OCall& call, uint32_t* A0, float* xs) {
+  const KParams* p = op->k;
+  const int H = p->H;
+  float ss = 0.f;
+  // the previous frame's codes must be in range (a failed frame leaves -1): else no input
+  bool codes_ok = call.prev_codes != nullptr;
+  for (int j = 0; codes_ok && j <= op->n_tables; ++j) {
+    const int c = G(call.prev_codes)[j];
+    codes_ok = c >= 0 && c < (j == 0 ? min(p->V, op->table_vocab) : op->table_vocab);
+  }
+  if (call.prev_codes && !codes_ok && tid() == 0) raise_status(op, RVQSD_EINVAL);
+  for (int e = tid(); e < H; e += kThreads) {
+    float v = G(call.t)[e];
+    if (codes_ok) {
+      const bf16_t* e0 = bw(p, p->o_emb0);
+      v += __uint_as_float((uint32_t)G(e0)[(size_t)G(call.prev_codes)[0] * H + e] << 16);
+      for (int j = 1; j <= op->n_tables; ++j)
+        v += __uint_as_float(
+            (uint32_t)G(op->tables)[((size_t)(j - 1) * op->table_vocab + G(call.prev_codes)[j]) * H + e] << 16);
+    }
+    cstf(op->x + e, v);
+    xs[e] = v;
+    ss = fmaf(v, v, ss);
+  }
+  ss = block_sum(sh, ss);
+  const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
+  const float* g0 = bfw(p, p->o_attn_norm);
+  for (int c = tid(); c < H / 8; c += kThreads) {
+    float h8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h8[e] = xs[8 * c + e] * rs * G(g0)[8 * c + e];
+    store_split(A0 + 8 * c, h8);
+  }
+}
+
+// chunk attention: unit (query head h, key chunk c) over positions of that chunk
+__device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float* lds) {
+  const KParams* p = op->k;
+  const int d = p->d, nq = p->nq, grp = nq / p->nkv, N = p->nqkv, KS = op->ks_qkv, half = d / 2;
+  const int lane = tid() & 63, wave = tid() >> 6;
+  const int np = pos + 1, ch = (np + kAttnChunks - 1) / kAttnChunks, nch = (np + ch - 1) / ch;
+  float* qv = lds;            // [d]
+  float* kn = qv + d;         // [d] this position's k
+  float* vn = kn + d;         // [d] this position's v
+  float* sc = vn + d;         // [chunk] scores
+  const float* qn = bfw(p, boff(p, l, p->o_qn));
+  const float* kng = bfw(p, boff(p, l, p->o_kn));
+  const float scale = 1.f / sqrtf((float)d);
+  for (int u = blockIdx.x; u < nq * nch; u += op->nwg) {
+    const int h = u / nch, c = u - h * nch, g = h / grp;
+    const int t0 = c * ch, t1 = min(np, t0 + ch);
+    float* kvc = op->kv + (((size_t)l * p->nkv + g) * op->max_frames) * 2 * d;
+    for (int e = tid(); e < 3 * d; e += kThreads) {
+      const int part = e / d, i = e - part * d;
+      const int col = part == 0 ? h * d + i : p->qdim + (part - 1) * p->kvdim + g * d + i;
+      const float v = sum_parts(op->part + col, (size_t)N, KS);
+      (part == 0 ? qv : part == 1 ? kn : vn)[i] = v;
+    }
+    __syncthreads();
+    // per-head RMSNorm + RoPE of q (wave 0) and k (wave 1) at this position
+    if (wave < 2) {
+      float* x = wave == 0 ? qv : kn;
+      const float* gn = wave == 0 ? qn : kng;
+      float s2 = 0.f;
+      for (int i = lane; i < d; i += 64) s2 = fmaf(x[i], x[i], s2);
+      s2 = wave_sum(s2);
+      const float rs = p->qk_norm ? 1.f / sqrtf(s2 / (float)d + p->rms_eps) : 1.f;
+      for (int i = lane; i < half; i += 64) {
+        float a = x[i], b = x[i + half];
+        if (p->qk_norm) {
+          a = a * rs * G(gn)[i];
+          b = b * rs * G(gn)[i + half];
+        }
+        const float cs = G(op->rope)[((size_t)pos * half + i) * 2], sn = G(op->rope)[((size_t)pos * half + i) * 2 + 1];
+        x[i] = a * cs - b * sn;
+        x[i + half] = b * cs + a * sn;
+      }
+    }
+    __syncthreads();
+    if (h % grp == 0 && c == 0)
+      for (int e = tid(); e < 2 * d; e += kThreads) cstf(kvc + (size_t)pos * 2 * d + e, e < d ? kn[e] : vn[e - d]);
+    // scores of the chunk: one wave per position
+    for (int t = t0 + wave; t < t1; t += kWaves) {
+      const float* kt = t == pos ? kn : kvc + (size_t)t * 2 * d;
+      float a = 0.f;
+      for (int i = lane; i < d; i += 64) a = fmaf(qv[i], t == pos ? kt[i] : ldf(kt + i), a);
+      a = wave_sum(a) * scale;
+      if (lane == 0) sc[t - t0] = a;
+    }
+    __syncthreads();
+    float mx = -INFINITY;
+    for (int t = 0; t < t1 - t0; ++t) mx = fmaxf(mx, sc[t]);
+    float* dst = op->apart + ((size_t)h * kAttnChunks + c) * (d + 2);
+    for (int i = tid(); i < d; i += kThreads) {
+      float o = 0.f, z = 0.f;
+      for (int t = t0; t < t1; ++t) {
+        const float w = expf(sc[t - t0] - mx);
+        z += w;
+        o = fmaf(w, t == pos ? vn[i] : ldf(kvc + (size_t)t * 2 * d + d + i), o);
+      }
+      cstf(dst + 2 + i, o);
+      if (i == 0) {
+        cstf(dst, mx);
+        cstf(dst + 1, z);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// merge the chunk partials of query head h (workgroup h) into the O projection's input
+__device__ void outer_attn_merge(const OParams* op, int pos, uint32_t* Aout) {
+  const KParams* p = op->k;
+  const int d = p->d, np = pos + 1, ch = (np + kAttnChunks - 1) / kAttnChunks, nch = (np + ch - 1) / ch;
+  for (int h = blockIdx.x; h < p->nq; h += op->nwg) {
+    const float* src = op->apart + (size_t)h * kAttnChunks * (d + 2);
+    float mx = -INFINITY;
+    for (int c = 0; c < nch; ++c) mx = fmaxf(mx, ldf(src + (size_t)c * (d + 2)));
+    float z = 0.f;
+    for (int c = 0; c < nch; ++c) z += ldf(src + (size_t)c * (d + 2) + 1) * expf(ldf(src + (size_t)c * (d + 2)) - mx);
+    const float iz = 1.f / z;
+    for (int q8 = tid(); q8 < d / 8; q8 += kThreads) {
+      float x8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float o = 0.f;
+        for (int c = 0; c < nch; ++c)
+          o += ldf(src + (size_t)c * (d + 2) + 2 + 8 * q8 + e) * expf(ldf(src + (size_t)c * (d + 2)) - mx);
+        x8[e] = o * iz;
+      }
+      store_split(Aout + h * d + 8 * q8, x8);
+    }
+  }
+}
+
+// residual + norm of the single row (workgroup 0); final: hidden out and the head input
+__device__ void outer_resid(const OParams* op, BShared* sh, int KS, const float* gain, uint32_t* Aout,
+                            float* hidden_out, float* xs) {
+  if (blockIdx.x != 0) return;
+  const KParams* p = op->k;
+  const int H = p->H;
+  float ss = 0.f;
+  for (int e = tid(); e < H; e += kThreads) {
+    const float v = ldf(op->x + e) + sum_parts(op->part + e, (size_t)H, KS);
+    cstf(op->x + e, v);
+    xs[e] = v;
+    ss = fmaf(v, v, ss);
+  }
+  ss = block_sum(sh, ss);
+  const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
+  for (int c = tid(); c < H / 8; c += kThreads) {
+    float h8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h8[e] = xs[8 * c + e] * rs * G(gain)[8 * c + e];
+    store_split(Aout + 8 * c, h8);
+    if (hidden_out)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) hidden_out[8 * c + e] = h8[e];
+  }
+}
+
+// c_0: top-k over the logits of the codes the inner tables embed, fp64 softmax, inverse CDF
+__device__ void outer_sample(const OParams* op, BShared* sh, const OCall& call, float* lds) {
+  if (blockIdx.x != 0) return;
+  const KParams* p = op->k;
+  const int V = min(p->V, op->table_vocab);
+  float* lg = lds;
+  int* sidx = reinterpret_cast<int*>(lg + V);
+  float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);
+  double* prob = reinterpret_cast<double*>((reinterpret_cast<uintptr_t>(slog + kMaxTopk) + 7) & ~(uintptr_t)7);
+  unsigned* hist = reinterpret_cast<unsigned*>(prob + kMaxTopk);
+  for (int i = tid(); i < V; i += kThreads) lg[i] = ldf(op->logits + i);
+  __syncthreads();
+  int ns = topk_buckets(&sh->tk, lg, V, op->topk, sidx, slog, hist);
+  if (ns < 0) ns = topk_select(&sh->tk, lg, V, op->topk, sidx, slog);
+  softmax_support(slog, ns, op->temperature, prob);
+  __syncthreads();
+  if (tid() < 64) {
+    bool fin = false;
+    for (int i = tid(); i < ns; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
+    const bool any_fin = __any(fin);
+    const int pos = inverse_cdf(prob, ns, (double)G(call.u_c0)[0]);
+    if (tid() == 0) {
+      if (!any_fin) raise_status(op, RVQSD_ENUMERIC);
+      call.c0_out[0] = any_fin ? sidx[pos] : -1;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __restrict__ opp, OCall call) {
+  __shared__ BShared shs;
+  extern __shared__ __align__(16) float dyn[];
+  const OParams* op = opp;
+  const KParams* p = op->k;
+  BShared* sh = &shs;
+  uint32_t gen = 0;
+  const int L = p->L, H = p->H;
+  uint32_t* A0 = op->a;
+  uint32_t* A1 = op->a + max(max(H, p->qdim), p->F);
+  if (blockIdx.x == 0) outer_input(op, sh, call, A0, dyn);
+  bool ok = grid_sync(op, gen, sh);
+  for (int l = 0; l < L && ok; ++l) {
+    proj_partial<4>(op, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, op->ks_qkv, A0, dyn);
+    ok = grid_sync(op, gen, sh);
+    if (ok) outer_attn(op, sh, l, call.pos, dyn);
+    ok = ok && grid_sync(op, gen, sh);
+    if (ok) outer_attn_merge(op, call.pos, A1);
+    ok = ok && grid_sync(op, gen, sh);
+    if (ok) proj_partial<4>(op, bw(p, boff(p, l, p->o_wo)), H, p->qdim, op->ks_o, A1, dyn);
+    ok = ok && grid_sync(op, gen, sh);
+    if (ok) outer_resid(op, sh, op->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, nullptr, dyn);
+    ok = ok && grid_sync(op, gen, sh);
+    if (ok) phase_gu(op, l, A0, A1, dyn);
+    ok = ok && grid_sync(op, gen, sh);
+    if (ok) proj_partial<4>(op, bw(p, boff(p, l, p->o_wd)), H, p->F, op->ks_down, A1, dyn);
+    ok = ok && grid_sync(op, gen, sh);
+    if (ok) {
+      if (l + 1 < L) outer_resid(op, sh, op->ks_down, bfw(p, boff(p, l + 1, p->o_attn_norm)), A0, nullptr, dyn);
+      else outer_resid(op, sh, op->ks_down, bfw(p, p->o_final_norm), A0, call.hidden_out, dyn);
+    }
+    ok = ok && grid_sync(op, gen, sh);
+  }
+  if (ok) {
+    // head: 64-column units over the full hidden width, one row
+    const bf16_t* W = bw(p, p->o_lmh1);
+    const int V = p->V;
+    for (int u = blockIdx.x; u < (V + 63) / 64; u += op->nwg) {
+      const int n0 = u * 64;
+      gemm_unit<4, kProjNTW>(
+          [&](int nt, int m) -> const bf16_t* {
+            const int f = n0 + 16 * nt + m;
+            return f < V ? W + (size_t)f * H : nullptr;
+          },
+          0, H, A0, H, 1, [&](int i) { return i < 1 ? 0 : -1; }, dyn);
+      for (int e = tid(); e < 4 * 64; e += kThreads) {
+        const int nt = e >> 6, ln = e & 63;
+        if ((ln & 15) == 0) {
+          const float* sv = dyn + ((size_t)(nt * kBatchMTiles) << 8) + 4 * ln;
+          for (int v = 0; v < 4; ++v) {
+            const int f = n0 + 16 * nt + 4 * (ln >> 4) + v;
+            if (f < V) cstf(op->logits + f, sv[v]);
+          }
+        }
+      }
+      __syncthreads();
+    }
+    ok = grid_sync(op, gen, sh);
+  }
+  if (ok) outer_sample(op, sh, call, dyn);
+  if (!ok && blockIdx.x == 0 && tid() == 0) call.c0_out[0] = -1;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------- host
@@ -962,6 +1226,34 @@ int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, si
   const BParams* bpp = bp;
   BCall c = call;
   void* args[] = {&bpp, &c};
+  hipError_t e = hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(kThreads), args, (unsigned)lds_bytes,
+                                            reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    snprintf(err, errlen, "hipLaunchCooperativeKernel: %s", hipGetErrorString(e));
+    return RVQSD_EHIP;
+  }
+  return RVQSD_OK;
+}
+
+}  // namespace rvqsd
+
+namespace rvqsd {
+
+int launch_outer(const OParams* op, const OCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
+                 size_t errlen) {
+  const void* fn = reinterpret_cast<const void*>(&outer_kernel);
+  static size_t attr_bytes = 0;
+  if (lds_bytes > attr_bytes) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    if (e != hipSuccess) {
+      snprintf(err, errlen, "hipFuncSetAttribute(%zu bytes LDS): %s", lds_bytes, hipGetErrorString(e));
+      return RVQSD_EHIP;
+    }
+    attr_bytes = lds_bytes;
+  }
+  const OParams* opa = op;
+  OCall c = call;
+  void* args[] = {&opa, &c};
   hipError_t e = hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(kThreads), args, (unsigned)lds_bytes,
                                             reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) {

@@ -124,6 +124,42 @@ struct BCall {
 
 int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
                  size_t errlen);
+
+// ---------------------------------------------------------------- outer decoder step
+// The outer CodeDecoder of the per-frame pipeline: one position per frame, a KV
+// cache that grows across frames, c_0 sampled from its head.
+constexpr int kAttnChunks = 16;  // key chunks per query head (split-sequence attention)
+
+struct OParams {
+  const KParams* k;      // the outer model's parameter block (dimensions, weights)
+  int32_t nwg, M;        // M = 1 row
+  int32_t ks_qkv, ks_o, ks_down;
+  int32_t n_tables, table_vocab, max_frames, topk;
+  double temperature;
+  const uint16_t* tables;  // [n_tables][table_vocab][H] bf16: embeddings of codes 1..n_tables
+  const float* rope;     // [max_frames][d/2][2] cos, sin of position * rope_base^(-2i/d)
+  float* x;              // [H] residual stream
+  uint32_t* a;           // [2][max(H, qdim, F)] split activations
+  float* part;           // [max ks][max N] partial sums
+  float* kv;             // [L][nkv][max_frames][2][d] KV cache (k after norm and RoPE, v)
+  float* apart;          // [nq][kAttnChunks][d + 2] per-chunk attention partials (max, sum, o)
+  float* logits;         // [V]
+  uint32_t* bar;         // grid barrier words
+  int32_t* status;       // first device-side error of the step (0 = none)
+};
+
+// Per-step arguments (device pointers), passed by value.
+struct OCall {
+  const float* t;            // [H] this frame's text-side input vector
+  const float* u_c0;         // [1] uniform of the c_0 draw
+  const int32_t* prev_codes; // [1 + n_tables] codes of the previous frame (nullptr at position 0)
+  int32_t* c0_out;           // [1] sampled c_0 (-1 after a device error)
+  float* hidden_out;         // [H] final-normed hidden state (the inner loop's frame input)
+  int32_t pos;               // position = frame index since the last reset
+};
+
+int launch_outer(const OParams* op, const OCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
+                 size_t errlen);
 int frame_lds_head_floats(int mr, int cpw);
 int frame_max_rows(int K);
 

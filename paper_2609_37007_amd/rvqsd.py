@@ -23,7 +23,8 @@ TRACE_ROUND_INTS = 32
 EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_stream_destroy",
            "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset",
            "rvqsd_set_trace", "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async",
-           "rvqsd_batch_totals", "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
+           "rvqsd_batch_totals", "rvqsd_outer_create", "rvqsd_outer_destroy", "rvqsd_outer_reset",
+           "rvqsd_pipeline_frames_async", "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
 
 
 class rvqsd_cfg(ctypes.Structure):
@@ -99,6 +100,11 @@ def lib():
         L.rvqsd_decode_frames_batched.argtypes = [vp, i32, vp, vp, vp, vp, vp]
         L.rvqsd_decode_frames_batched_async.argtypes = [vp, i32, vp, vp, vp, vp, vp]
         L.rvqsd_batch_totals.argtypes = [vp, P(ctypes.c_uint64), P(ctypes.c_uint64)]
+        L.rvqsd_outer_create.argtypes = [vp, vp, i32, i32, i32, ctypes.c_double, i32, P(vp)]
+        L.rvqsd_outer_destroy.argtypes = [vp]
+        L.rvqsd_outer_destroy.restype = None
+        L.rvqsd_outer_reset.argtypes = [vp]
+        L.rvqsd_pipeline_frames_async.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp, vp]
         L.rvqsd_stream_reset.argtypes = [vp]
         L.rvqsd_uniforms_from_seed.argtypes = [ctypes.c_uint64, i32, vp]
         L.rvqsd_status_str.argtypes = [i32]
@@ -108,6 +114,7 @@ def lib():
         for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_decode_frame",
                   "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset", "rvqsd_set_trace",
                   "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async", "rvqsd_batch_totals",
+                  "rvqsd_outer_create", "rvqsd_outer_reset", "rvqsd_pipeline_frames_async",
                   "rvqsd_uniforms_from_seed"):
             getattr(L, n).restype = i32
         _lib = L
@@ -247,3 +254,34 @@ class Stream:
                         wg_ready_ptr or None)
         _check(lib().rvqsd_set_trace(self._h, ctypes.byref(t)), "rvqsd_set_trace")
         self._trace = t
+
+
+class Outer:
+    """rvqsd_outer_create / rvqsd_outer_reset / rvqsd_pipeline_frames_async."""
+
+    def __init__(self, model: Model, code_tables: bytes, n_tables: int, table_vocab: int, topk: int,
+                 temperature: float, max_frames: int):
+        self.model = model
+        tab = bytes(code_tables)
+        h = ctypes.c_void_p()
+        _check(lib().rvqsd_outer_create(model._h, ctypes.c_char_p(tab), n_tables, table_vocab, topk,
+                                        float(temperature), max_frames, ctypes.byref(h)), "rvqsd_outer_create")
+        self._h = h
+
+    def reset(self):
+        _check(lib().rvqsd_outer_reset(self._h), "rvqsd_outer_reset")
+
+    def pipeline_async(self, stream: "Stream", n: int, d_t: int, d_u_c0: int, d_uniforms: int, d_codes: int,
+                       d_stats: int, d_hidden: int = 0):
+        """Device pointers (ints); enqueues n frames on the inner stream."""
+        _check(lib().rvqsd_pipeline_frames_async(stream._h, self._h, int(n), ctypes.c_void_p(d_t),
+                                                 ctypes.c_void_p(d_u_c0), ctypes.c_void_p(d_uniforms),
+                                                 ctypes.c_void_p(d_codes), ctypes.c_void_p(d_stats),
+                                                 ctypes.c_void_p(d_hidden or None)), "rvqsd_pipeline_frames_async")
+
+    def close(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.rvqsd_outer_destroy(self._h)
+        self._h = None
+
+    __del__ = close
