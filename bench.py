@@ -19,6 +19,12 @@ model verified together (S x (K + 1) rows per pass, stream i with frame seeds
 of the batched kernel through rvqsd_decode_frames_batched_async; `value` is
 then the aggregate codes/s of all streams.
 
+With --pipeline the workload is the full per-frame pipeline: the 28-layer outer
+CodeDecoder step (KV cache growing to the frame count, 3072-entry head, c_0
+sampled with top-k 50) chained on the device with the inner loop (K = 4),
+1500 frames through rvqsd_pipeline_frames_async; `value` is then 16 codes per
+frame over the wall time.
+
 Prints ONE JSON line.  `roofline` prices the frame kernel against HBM
 bandwidth with the algorithmic bytes the device counts per frame (layer
 weights per pass, the distinct LM heads a pass touches, gathered embedding
@@ -91,6 +97,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--streams", type=int, default=1, help="independent streams verified together (1..16)")
     ap.add_argument("--frames-per-stream", type=int, default=500)
+    ap.add_argument("--pipeline", action="store_true", help="outer CodeDecoder step + inner loop per frame")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="only run 5 plain device copies of MB MiB (the reference kernel for HBM byte counters)")
     return ap.parse_args()
@@ -130,6 +137,159 @@ def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order
     return {"value": round(s.n_codes * done / c_el, 3), "unit": "codes/s", "cores": threads, "kind": "oracle",
             "sample": f"{done} of the timed frames ({c_el:.1f} s, fp64 full-recompute oracle, OpenMP over output "
                       f"rows); {same}/{done} frames give codes identical to the GPU's"}
+
+
+def run_pipeline(a) -> int:
+    """Outer CodeDecoder step + inner speculative loop per frame, chained on the device."""
+    import numpy as np
+    import torch
+
+    from oracle import oracle as O
+    from paper_2609_37007_amd import rvqsd as R
+    from paper_2609_37007_amd import synth as S
+
+    R.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    so, si = S.OUTER_1024, S.MCD_1024
+    topk, K, temperature = 50, (4 if a.draft_len is None else a.draft_len), 0.9
+    N = 1500 if a.steps is None else a.steps
+    W = max(1, min(a.warmup, 8))
+    nc = si.n_codes
+    print(f"[bench] building outer and inner weights; {N} frames", file=sys.stderr, flush=True)
+    oblob = S.make_weights(so, seed=0)
+    iblob = S.make_weights(si, seed=0, head_scale=a.head_scale)
+    tables = S.make_outer_tables(so, nc, si.vocab)
+    ocfg = R.make_cfg(n_layers=so.n_layers, hidden=so.hidden, n_q_heads=so.n_q_heads, n_kv_heads=so.n_kv_heads,
+                      head_dim=so.head_dim, ffn=so.ffn, n_codes=so.n_codes, vocab=so.vocab, max_draft=so.max_draft,
+                      dtype=so.dtype, topk=topk, temperature=temperature, draft_len=0)
+    icfg = R.make_cfg(n_layers=si.n_layers, hidden=si.hidden, n_q_heads=si.n_q_heads, n_kv_heads=si.n_kv_heads,
+                      head_dim=si.head_dim, ffn=si.ffn, n_codes=nc, vocab=si.vocab, max_draft=si.max_draft,
+                      dtype=si.dtype, topk=topk, temperature=temperature, draft_len=K)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    torch_stream = torch.cuda.current_stream(dev)
+    omodel, imodel = R.Model(oblob, ocfg), R.Model(iblob, icfg)
+    info = imodel.info()
+    oinfo = omodel.info()
+    stream = R.Stream(imodel, hip_stream=torch_stream.cuda_stream)
+    outer = R.Outer(omodel, tables, nc, si.vocab, topk, temperature, max(N, W))
+    t, u_c0 = S.pipeline_inputs(so, N)
+    uni = S.uniforms(N, nc)
+    d_t = torch.from_numpy(t).to(dev)
+    d_u0 = torch.from_numpy(u_c0).to(dev)
+    d_u = torch.from_numpy(np.ascontiguousarray(uni)).to(dev)
+    d_codes = torch.full((N, 1 + nc), -1, dtype=torch.int32, device=dev)
+    sb = R.STATS_DTYPE.itemsize
+    d_st = torch.zeros(N * sb, dtype=torch.uint8, device=dev)
+
+    def run(n):
+        outer.pipeline_async(stream, n, d_t.data_ptr(), d_u0.data_ptr(), d_u.data_ptr(), d_codes.data_ptr(),
+                             d_st.data_ptr())
+
+    print(f"[bench] warmup {W} frames", file=sys.stderr, flush=True)
+    run(W)
+    torch.cuda.synchronize()
+    outer.reset()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    print(f"[bench] timing {N} frames", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    ev0.record(torch_stream)
+    run(N)
+    ev1.record(torch_stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    st = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)
+    codes = d_codes.cpu().numpy()
+    if (st["status"] != 0).any() or (codes[:, 0] < 0).any():
+        bad = int(np.argmax((st["status"] != 0) | (codes[:, 0] < 0)))
+        print(f"[bench] frame {bad} failed with status {int(st['status'][bad])}", file=sys.stderr)
+        return 1
+    # algorithmic bytes: per frame the outer layers and head, the outer KV read (positions 0..i,
+    # fp32 k and v), and the inner loop's own count
+    H, L = so.hidden, so.n_layers
+    outer_w = oinfo["layer_weight_bytes"] + oinfo["head_bytes"]
+    kv_b = sum((i + 1) for i in range(N)) * L * so.n_kv_heads * so.head_dim * 2 * 4
+    total_b = N * outer_w + kv_b + float(st["weight_bytes"].astype(np.float64).sum())
+    achieved = total_b / (gpu_ms * 1e-3) / 1e9
+    cpu = None
+    if not a.no_cpu_baseline:
+        oorc = O.Oracle(oblob, n_layers=so.n_layers, hidden=so.hidden, n_q_heads=so.n_q_heads,
+                        n_kv_heads=so.n_kv_heads, head_dim=so.head_dim, ffn=so.ffn, n_codes=so.n_codes,
+                        vocab=so.vocab, max_draft=so.max_draft, dtype=so.dtype, topk=topk,
+                        temperature=temperature, draft_len=0)
+        iorc = O.Oracle(iblob, n_layers=si.n_layers, hidden=si.hidden, n_q_heads=si.n_q_heads,
+                        n_kv_heads=si.n_kv_heads, head_dim=si.head_dim, ffn=si.ffn, n_codes=nc, vocab=si.vocab,
+                        max_draft=si.max_draft, dtype=si.dtype, topk=topk, temperature=temperature, draft_len=K)
+        emb0 = S.unpack_weights(so, oblob)["emb0"]
+        tab = S.unpack_outer_tables(so, tables, nc, si.vocab)
+        threads = O.get_threads()
+        print(f"[bench] oracle pipeline sample on {threads} threads, ~{a.cpu_seconds:.0f} s", file=sys.stderr,
+              flush=True)
+        done = min(N, 3)
+        c_t0 = time.perf_counter()
+        oc, _, _ = O.pipeline_frames(oorc, emb0, tab, iorc, t[:done], u_c0[:done], uni[:done], topk, temperature)
+        c_el = time.perf_counter() - c_t0
+        same = int(sum((oc[i] == codes[i]).all() for i in range(done)))
+        oorc.close()
+        iorc.close()
+        cpu = {"value": round((nc + 1) * done / c_el, 3), "unit": "codes/s", "cores": threads, "kind": "oracle",
+               "sample": f"the first {done} frames of the timed run through the fp64 oracle pipeline ({c_el:.1f} s, "
+                         f"outer decoder recomputed over all earlier positions each frame); {same}/{done} frames give "
+                         f"codes identical to the GPU's"}
+    out = {
+        "metric": METRIC,
+        "value": round((nc + 1) * N / elapsed, 1),
+        "unit": "codes/s",
+        "n_gpus": 1,
+        "steps": N,
+        "warmup": W,
+        "ms_per_step": round(elapsed * 1e3 / N, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (random-init weights, seeded text-side vectors and uniforms)",
+        "config": {
+            "workload": (f"pipeline: outer {so.n_layers}-layer CodeDecoder (hidden {so.hidden}, {so.n_q_heads}/"
+                         f"{so.n_kv_heads} heads x {so.head_dim}, ffn {so.ffn}, {so.vocab}-entry head, KV to {N} "
+                         f"positions, c0 top-k {topk}) + inner mcd1024 (draft length {K}, top-k {topk}), "
+                         f"temperature {temperature}, batch 1, {N} frames"),
+            "frames": N,
+            "draft_len": K,
+            "topk": topk,
+            "temperature": temperature,
+            "parallelism": "single GPU, one persistent launch per outer step and per inner frame",
+        },
+        "frames_per_s": round(N / elapsed, 2),
+        "real_time_factor": round(N / elapsed / 12.5, 2),
+        "frame_ms_mean": round(gpu_ms / N, 4),
+        "accepted_tokens_per_call": round(nc * N / float(st["target_calls"].sum()), 4),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "outer_kernel + frame_kernel",
+            "algorithmic_bytes_per_frame": round(total_b / N, 1),
+        },
+        "cpu_baseline": cpu,
+        "device": torch.cuda.get_device_name(dev),
+        "workgroups": info["workgroups"],
+    }
+    del d_t, d_u0, d_u, d_codes, d_st
+    torch.cuda.synchronize()
+    outer.close()
+    stream.close()
+    imodel.close()
+    omodel.close()
+    torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def run_streams(a) -> int:
@@ -272,6 +432,8 @@ def main() -> int:
         return copy_calibration(a.copy_calibration)
     if a.streams > 1:
         return run_streams(a)
+    if a.pipeline:
+        return run_pipeline(a)
 
     import numpy as np
     import torch
