@@ -848,7 +848,8 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
   }
   size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
   const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + kMaxTopk * 8 + kTopkBuckets * 4;
-  const size_t attn = ((size_t)3 * k.d + (max_frames + kAttnChunks - 1) / kAttnChunks) * 4;
+  const size_t chunk = (max_frames + kAttnChunks - 1) / kAttnChunks;  // key positions per chunk at most
+  const size_t attn = ((size_t)3 * k.d + chunk + chunk * k.d) * 4;
   if (samp > lds) lds = samp;
   if (attn > lds) lds = attn;
   if ((size_t)k.H * 4 > lds) lds = (size_t)k.H * 4;

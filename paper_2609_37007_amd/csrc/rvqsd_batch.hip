@@ -1000,6 +1000,7 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
   float* kn = qv + d;         // [d] this position's k
   float* vn = kn + d;         // [d] this position's v
   float* sc = vn + d;         // [chunk] scores
+  float* kvs = sc + ch;       // [chunk][d] the chunk's keys, then its values
   const float* qn = bfw(p, boff(p, l, p->o_qn));
   const float* kng = bfw(p, boff(p, l, p->o_kn));
   const float scale = 1.f / sqrtf((float)d);
@@ -1036,13 +1037,23 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
     __syncthreads();
     if (h % grp == 0 && c == 0)
       for (int e = tid(); e < 2 * d; e += kThreads) cstf(kvc + (size_t)pos * 2 * d + e, e < d ? kn[e] : vn[e - d]);
-    // scores of the chunk: one wave per position
+    // the chunk's keys into LDS (all loads issued together), then one wave per position
+    for (int e = tid(); e < (t1 - t0) * d; e += kThreads) {
+      const int t = t0 + e / d, i = e - (e / d) * d;
+      kvs[e] = t == pos ? kn[i] : ldf(kvc + (size_t)t * 2 * d + i);
+    }
+    __syncthreads();
     for (int t = t0 + wave; t < t1; t += kWaves) {
-      const float* kt = t == pos ? kn : kvc + (size_t)t * 2 * d;
       float a = 0.f;
-      for (int i = lane; i < d; i += 64) a = fmaf(qv[i], t == pos ? kt[i] : ldf(kt + i), a);
+      for (int i = lane; i < d; i += 64) a = fmaf(qv[i], kvs[(t - t0) * d + i], a);
       a = wave_sum(a) * scale;
       if (lane == 0) sc[t - t0] = a;
+    }
+    __syncthreads();
+    // then its values
+    for (int e = tid(); e < (t1 - t0) * d; e += kThreads) {
+      const int t = t0 + e / d, i = e - (e / d) * d;
+      kvs[e] = t == pos ? vn[i] : ldf(kvc + (size_t)t * 2 * d + d + i);
     }
     __syncthreads();
     float mx = -INFINITY;
@@ -1050,10 +1061,10 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
     float* dst = op->apart + ((size_t)h * kAttnChunks + c) * (d + 2);
     for (int i = tid(); i < d; i += kThreads) {
       float o = 0.f, z = 0.f;
-      for (int t = t0; t < t1; ++t) {
-        const float w = expf(sc[t - t0] - mx);
+      for (int t = 0; t < t1 - t0; ++t) {
+        const float w = expf(sc[t] - mx);
         z += w;
-        o = fmaf(w, t == pos ? vn[i] : ldf(kvc + (size_t)t * 2 * d + d + i), o);
+        o = fmaf(w, kvs[t * d + i], o);
       }
       cstf(dst + 2 + i, o);
       if (i == 0) {
