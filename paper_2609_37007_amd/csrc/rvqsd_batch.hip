@@ -52,10 +52,12 @@ __device__ __forceinline__ float ldf(const float* p) { return *G(p); }
 // Sum of KS <= kMaxSplit partial sums at p, p + stride, ... in split order; the loads are
 // issued together (a loop with a run-time bound would wait for each before the next).
 constexpr int kMaxSplit = 32;
+template <bool COH = false>
 __device__ __forceinline__ float sum_parts(const float* p, size_t stride, int KS) {
   float v[kMaxSplit];
 #pragma unroll
-  for (int k = 0; k < kMaxSplit; ++k) v[k] = k < KS ? ldf(p + k * stride) : 0.f;
+  for (int k = 0; k < kMaxSplit; ++k)
+    v[k] = k < KS ? (COH ? __uint_as_float(cld32(p + k * stride)) : ldf(p + k * stride)) : 0.f;
   float s = v[0];
 #pragma unroll
   for (int k = 1; k < kMaxSplit; ++k) s += v[k];
@@ -73,6 +75,38 @@ __device__ __forceinline__ void store_split(uint32_t* dst, const float (&x)[8]) 
   cst64(dst + 6, (uint64_t)lo[2] | ((uint64_t)lo[3] << 32));
 }
 __device__ __forceinline__ W16 load_w16(const uint32_t* p) { return *G(reinterpret_cast<const W16*>(p)); }
+// the same through device-coherent 8-byte loads (no cache invalidate needed before them)
+__device__ __forceinline__ W16 load_w16c(const uint32_t* p) {
+  const uint64_t a = __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t b = __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p + 2)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  W16 r;
+  r[0] = (uint32_t)a;
+  r[1] = (uint32_t)(a >> 32);
+  r[2] = (uint32_t)b;
+  r[3] = (uint32_t)(b >> 32);
+  return r;
+}
+__device__ __forceinline__ float cldf(const float* p) { return __uint_as_float(cld32(p)); }
+
+// dst[e] = src(e) for e < n, e = row * ncols + col -> src + row * row_stride + col; each thread
+// issues 8 loads before it stores (a plain copy loop would wait for every load in turn)
+template <bool COH>
+__device__ __forceinline__ void lds_fill(float* dst, const float* src, int n, int ncols, size_t row_stride) {
+  for (int base = 0; base < n; base += 8 * kThreads) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int e = base + k * kThreads + tid();
+      const float* a = src + (size_t)(e / ncols) * row_stride + (e % ncols);
+      v[k] = e < n ? (COH ? cldf(a) : ldf(a)) : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int e = base + k * kThreads + tid();
+      if (e < n) dst[e] = v[k];
+    }
+  }
+}
 
 __device__ __forceinline__ const bf16_t* bw(const KParams* p, uint64_t off) {
   return reinterpret_cast<const bf16_t*>(p->wbase + off);
@@ -107,7 +141,7 @@ struct BShared {
 // Arrival counts per XCD group (workgroup w is counted in group w % 8), the
 // last arrival of a group bumps the top counter, the last group publishes the
 // generation. Before arriving, every wave waits for its own stores.
-template <typename BP>
+template <typename BP, bool ACQ = true>
 __device__ bool grid_sync(const BP* bp, uint32_t& gen, BShared* sh) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -143,8 +177,9 @@ __device__ bool grid_sync(const BP* bp, uint32_t& gen, BShared* sh) {
     if (!ab && cld32(bp->status) != 0) ab = 1;
     sh->abort = ab;
   }
-  // drop this CU's and this XCD's cached copies of lines written by others
-  if (tid() < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // drop this CU's and this XCD's cached copies of lines written by others (not needed by
+  // a kernel that reads every cross-workgroup value with device-coherent loads)
+  if (ACQ && tid() < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
   return sh->abort == 0;
 }
@@ -192,7 +227,7 @@ __device__ __forceinline__ bool head_slot_used(const KParams* p, const int* st, 
 // MFMA roles as in the frame kernel: A = 16 weight rows, B = 16 activation
 // rows; lane group q = lane / 16 covers the 16 consecutive k of a 64-wide step
 // in two instructions, and the activation chunk of 8 enters as bf16 hi + lo.
-template <int NTU, int NTW, typename WRow, typename RowOf>
+template <int NTU, int NTW, bool COH = false, typename WRow, typename RowOf>
 __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uint32_t* A, int lda, int mtiles,
                                           RowOf rowof, float* red) {
   constexpr int NG = NTU / NTW, KW = kWaves / NG;
@@ -233,10 +268,10 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
       bh0[mt] = bl0[mt] = bh1[mt] = bl1[mt] = (W16)(0u);
       if (mt < mtiles && arow[mt] >= 0) {
         const uint32_t* ap = A + (size_t)arow[mt] * lda + (size_t)chunk * 8;
-        bh0[mt] = load_w16(ap);
-        bl0[mt] = load_w16(ap + 4);
-        bh1[mt] = load_w16(ap + 8);
-        bl1[mt] = load_w16(ap + 12);
+        bh0[mt] = COH ? load_w16c(ap) : load_w16(ap);
+        bl0[mt] = COH ? load_w16c(ap + 4) : load_w16(ap + 4);
+        bh1[mt] = COH ? load_w16c(ap + 8) : load_w16(ap + 8);
+        bl1[mt] = COH ? load_w16c(ap + 12) : load_w16(ap + 12);
       }
     }
 #pragma unroll
@@ -284,14 +319,14 @@ static_assert(gemm_red_floats<4, kProjNTW>() <= kBatchRedFloats && gemm_red_floa
 // ------------------------------------------------------------ projections
 
 // Y partial sums: part[ks][i][n] = sum over k in split ks of A[i][k] W[n][k], for every row i < M.
-template <int NTU, typename BP>
+template <int NTU, typename BP, bool COH = false>
 __device__ void proj_partial(const BP* bp, const bf16_t* W, int N, int K, int KS, const uint32_t* A, float* red) {
   const int M = bp->M, mtiles = (M + 15) >> 4;
   const int cg = (N + 16 * NTU - 1) / (16 * NTU), units = cg * KS, klen = K / KS;
   float* part = bp->part;
   for (int u = blockIdx.x; u < units; u += bp->nwg) {
     const int g = u % cg, ks = u / cg, n0 = g * 16 * NTU;
-    gemm_unit<NTU, kProjNTW>(
+    gemm_unit<NTU, kProjNTW, COH>(
         [&](int nt, int m) -> const bf16_t* {
           const int f = n0 + 16 * nt + m;
           return f < N ? W + (size_t)f * K : nullptr;
@@ -313,7 +348,7 @@ __device__ void proj_partial(const BP* bp, const bf16_t* W, int N, int K, int KS
 
 // gate/up: n-tile 0 = gate rows f0 .. f0 + 15, n-tile 1 = the same up rows, full k;
 // act = SiLU(gate) * up goes straight to the split input of the down projection.
-template <typename BP>
+template <typename BP, bool COH = false>
 __device__ void phase_gu(const BP* bp, int l, const uint32_t* A, uint32_t* Aout, float* red) {
   const KParams* p = bp->k;
   const int M = bp->M, mtiles = (M + 15) >> 4, H = p->H, F = p->F;
@@ -322,7 +357,7 @@ __device__ void phase_gu(const BP* bp, int l, const uint32_t* A, uint32_t* Aout,
   float* act = red + gemm_red_floats<2, kGuNTW>();  // [80][16]
   for (int u = blockIdx.x; u < F / 16; u += bp->nwg) {
     const int f0 = u * 16;
-    gemm_unit<2, kGuNTW>([&](int nt, int m) -> const bf16_t* { return (nt ? wu : wg) + (size_t)(f0 + m) * H; }, 0, H, A, H,
+    gemm_unit<2, kGuNTW, COH>([&](int nt, int m) -> const bf16_t* { return (nt ? wu : wg) + (size_t)(f0 + m) * H; }, 0, H, A, H,
                  mtiles, [&](int i) { return i < M ? i : -1; }, red);
     for (int e = tid(); e < mtiles * 256; e += kThreads) {
       const int mt = e >> 8, x = e & 255, ln = x >> 2, v = x & 3;
@@ -370,7 +405,7 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
       if (part == 0) qs[r * d + i] = s;
       else kvs[(size_t)(fp + r) * 2 * d + (part - 1) * d + i] = s;
     }
-    for (int e = tid(); e < fp * 2 * d; e += kThreads) kvs[e] = ldf(kvc + e);
+    lds_fill<false>(kvs, kvc, fp * 2 * d, 2 * d, (size_t)2 * d);
     __syncthreads();
     // q rows (v < R) and k rows (v >= R): norm + RoPE, one wave per vector
     for (int v = wave; v < 2 * R; v += kWaves) {
@@ -599,7 +634,7 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
       }
     }
     const float* src = bp->logits + (size_t)u * V;
-    for (int i = tid(); i < V; i += kThreads) lg[i] = ldf(src + i);
+    lds_fill<false>(lg, src, V, V, 0);
     __syncthreads();
     int ns = topk_buckets(&sh->tk, lg, V, p->topk, sidx, slog, hist);
     if (ns < 0) ns = topk_select(&sh->tk, lg, V, p->topk, sidx, slog);
@@ -1011,7 +1046,7 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
     for (int e = tid(); e < 3 * d; e += kThreads) {
       const int part = e / d, i = e - part * d;
       const int col = part == 0 ? h * d + i : p->qdim + (part - 1) * p->kvdim + g * d + i;
-      const float v = sum_parts(op->part + col, (size_t)N, KS);
+      const float v = sum_parts<true>(op->part + col, (size_t)N, KS);
       (part == 0 ? qv : part == 1 ? kn : vn)[i] = v;
     }
     __syncthreads();
@@ -1038,10 +1073,11 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
     if (h % grp == 0 && c == 0)
       for (int e = tid(); e < 2 * d; e += kThreads) cstf(kvc + (size_t)pos * 2 * d + e, e < d ? kn[e] : vn[e - d]);
     // the chunk's keys into LDS (all loads issued together), then one wave per position
-    for (int e = tid(); e < (t1 - t0) * d; e += kThreads) {
-      const int t = t0 + e / d, i = e - (e / d) * d;
-      kvs[e] = t == pos ? kn[i] : ldf(kvc + (size_t)t * 2 * d + i);
-    }
+    lds_fill<false>(kvs, kvc + (size_t)t0 * 2 * d, (t1 - t0) * d, d, (size_t)2 * d);
+    __syncthreads();
+    // this frame's position is not in the cache yet (written in this phase): its own k
+    if (t1 - 1 == pos)
+      for (int i = tid(); i < d; i += kThreads) kvs[(pos - t0) * d + i] = kn[i];
     __syncthreads();
     for (int t = t0 + wave; t < t1; t += kWaves) {
       float a = 0.f;
@@ -1051,10 +1087,10 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
     }
     __syncthreads();
     // then its values
-    for (int e = tid(); e < (t1 - t0) * d; e += kThreads) {
-      const int t = t0 + e / d, i = e - (e / d) * d;
-      kvs[e] = t == pos ? vn[i] : ldf(kvc + (size_t)t * 2 * d + d + i);
-    }
+    lds_fill<false>(kvs, kvc + (size_t)t0 * 2 * d + d, (t1 - t0) * d, d, (size_t)2 * d);
+    __syncthreads();
+    if (t1 - 1 == pos)
+      for (int i = tid(); i < d; i += kThreads) kvs[(pos - t0) * d + i] = vn[i];
     __syncthreads();
     float mx = -INFINITY;
     for (int t = 0; t < t1 - t0; ++t) mx = fmaxf(mx, sc[t]);
@@ -1083,9 +1119,9 @@ __device__ void outer_attn_merge(const OParams* op, int pos, uint32_t* Aout) {
   for (int h = blockIdx.x; h < p->nq; h += op->nwg) {
     const float* src = op->apart + (size_t)h * kAttnChunks * (d + 2);
     float mx = -INFINITY;
-    for (int c = 0; c < nch; ++c) mx = fmaxf(mx, ldf(src + (size_t)c * (d + 2)));
+    for (int c = 0; c < nch; ++c) mx = fmaxf(mx, cldf(src + (size_t)c * (d + 2)));
     float z = 0.f;
-    for (int c = 0; c < nch; ++c) z += ldf(src + (size_t)c * (d + 2) + 1) * expf(ldf(src + (size_t)c * (d + 2)) - mx);
+    for (int c = 0; c < nch; ++c) z += cldf(src + (size_t)c * (d + 2) + 1) * expf(cldf(src + (size_t)c * (d + 2)) - mx);
     const float iz = 1.f / z;
     for (int q8 = tid(); q8 < d / 8; q8 += kThreads) {
       float x8[8];
@@ -1093,7 +1129,7 @@ __device__ void outer_attn_merge(const OParams* op, int pos, uint32_t* Aout) {
       for (int e = 0; e < 8; ++e) {
         float o = 0.f;
         for (int c = 0; c < nch; ++c)
-          o += ldf(src + (size_t)c * (d + 2) + 2 + 8 * q8 + e) * expf(ldf(src + (size_t)c * (d + 2)) - mx);
+          o += cldf(src + (size_t)c * (d + 2) + 2 + 8 * q8 + e) * expf(cldf(src + (size_t)c * (d + 2)) - mx);
         x8[e] = o * iz;
       }
       store_split(Aout + h * d + 8 * q8, x8);
@@ -1109,7 +1145,7 @@ __device__ void outer_resid(const OParams* op, BShared* sh, int KS, const float*
   const int H = p->H;
   float ss = 0.f;
   for (int e = tid(); e < H; e += kThreads) {
-    const float v = ldf(op->x + e) + sum_parts(op->part + e, (size_t)H, KS);
+    const float v = cldf(op->x + e) + sum_parts<true>(op->part + e, (size_t)H, KS);
     cstf(op->x + e, v);
     xs[e] = v;
     ss = fmaf(v, v, ss);
@@ -1137,7 +1173,7 @@ __device__ void outer_sample(const OParams* op, BShared* sh, const OCall& call, 
   float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);
   double* prob = reinterpret_cast<double*>((reinterpret_cast<uintptr_t>(slog + kMaxTopk) + 7) & ~(uintptr_t)7);
   unsigned* hist = reinterpret_cast<unsigned*>(prob + kMaxTopk);
-  for (int i = tid(); i < V; i += kThreads) lg[i] = ldf(op->logits + i);
+  lds_fill<true>(lg, op->logits, V, V, 0);
   __syncthreads();
   int ns = topk_buckets(&sh->tk, lg, V, op->topk, sidx, slog, hist);
   if (ns < 0) ns = topk_select(&sh->tk, lg, V, op->topk, sidx, slog);
@@ -1166,27 +1202,27 @@ __global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __res
   uint32_t* A0 = op->a;
   uint32_t* A1 = op->a + max(max(H, p->qdim), p->F);
   if (blockIdx.x == 0) outer_input(op, sh, call, A0, dyn);
-  bool ok = grid_sync(op, gen, sh);
+  bool ok = grid_sync<OParams, false>(op, gen, sh);
   for (int l = 0; l < L && ok; ++l) {
-    proj_partial<4>(op, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, op->ks_qkv, A0, dyn);
-    ok = grid_sync(op, gen, sh);
+    proj_partial<4, OParams, true>(op, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, op->ks_qkv, A0, dyn);
+    ok = grid_sync<OParams, false>(op, gen, sh);
     if (ok) outer_attn(op, sh, l, call.pos, dyn);
-    ok = ok && grid_sync(op, gen, sh);
+    ok = ok && grid_sync<OParams, false>(op, gen, sh);
     if (ok) outer_attn_merge(op, call.pos, A1);
-    ok = ok && grid_sync(op, gen, sh);
-    if (ok) proj_partial<4>(op, bw(p, boff(p, l, p->o_wo)), H, p->qdim, op->ks_o, A1, dyn);
-    ok = ok && grid_sync(op, gen, sh);
+    ok = ok && grid_sync<OParams, false>(op, gen, sh);
+    if (ok) proj_partial<4, OParams, true>(op, bw(p, boff(p, l, p->o_wo)), H, p->qdim, op->ks_o, A1, dyn);
+    ok = ok && grid_sync<OParams, false>(op, gen, sh);
     if (ok) outer_resid(op, sh, op->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, nullptr, dyn);
-    ok = ok && grid_sync(op, gen, sh);
-    if (ok) phase_gu(op, l, A0, A1, dyn);
-    ok = ok && grid_sync(op, gen, sh);
-    if (ok) proj_partial<4>(op, bw(p, boff(p, l, p->o_wd)), H, p->F, op->ks_down, A1, dyn);
-    ok = ok && grid_sync(op, gen, sh);
+    ok = ok && grid_sync<OParams, false>(op, gen, sh);
+    if (ok) phase_gu<OParams, true>(op, l, A0, A1, dyn);
+    ok = ok && grid_sync<OParams, false>(op, gen, sh);
+    if (ok) proj_partial<4, OParams, true>(op, bw(p, boff(p, l, p->o_wd)), H, p->F, op->ks_down, A1, dyn);
+    ok = ok && grid_sync<OParams, false>(op, gen, sh);
     if (ok) {
       if (l + 1 < L) outer_resid(op, sh, op->ks_down, bfw(p, boff(p, l + 1, p->o_attn_norm)), A0, nullptr, dyn);
       else outer_resid(op, sh, op->ks_down, bfw(p, p->o_final_norm), A0, call.hidden_out, dyn);
     }
-    ok = ok && grid_sync(op, gen, sh);
+    ok = ok && grid_sync<OParams, false>(op, gen, sh);
   }
   if (ok) {
     // head: 64-column units over the full hidden width, one row
@@ -1194,7 +1230,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __res
     const int V = p->V;
     for (int u = blockIdx.x; u < (V + 63) / 64; u += op->nwg) {
       const int n0 = u * 64;
-      gemm_unit<4, kProjNTW>(
+      gemm_unit<4, kProjNTW, true>(
           [&](int nt, int m) -> const bf16_t* {
             const int f = n0 + 16 * nt + m;
             return f < V ? W + (size_t)f * H : nullptr;
@@ -1212,7 +1248,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __res
       }
       __syncthreads();
     }
-    ok = grid_sync(op, gen, sh);
+    ok = grid_sync<OParams, false>(op, gen, sh);
   }
   if (ok) outer_sample(op, sh, call, dyn);
   if (!ok && blockIdx.x == 0 && tid() == 0) call.c0_out[0] = -1;
