@@ -1113,27 +1113,29 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
 }
 
 // merge the chunk partials of query head h (workgroup h) into the O projection's input
-__device__ void outer_attn_merge(const OParams* op, int pos, uint32_t* Aout) {
+__device__ void outer_attn_merge(const OParams* op, int pos, uint32_t* Aout, float* lds) {
   const KParams* p = op->k;
   const int d = p->d, np = pos + 1, ch = (np + kAttnChunks - 1) / kAttnChunks, nch = (np + ch - 1) / ch;
   for (int h = blockIdx.x; h < p->nq; h += op->nwg) {
-    const float* src = op->apart + (size_t)h * kAttnChunks * (d + 2);
+    // the head's chunk partials (max, sum, o[d]) into LDS, all loads in flight together
+    lds_fill<true>(lds, op->apart + (size_t)h * kAttnChunks * (d + 2), nch * (d + 2), nch * (d + 2), 0);
+    __syncthreads();
     float mx = -INFINITY;
-    for (int c = 0; c < nch; ++c) mx = fmaxf(mx, cldf(src + (size_t)c * (d + 2)));
+    for (int c = 0; c < nch; ++c) mx = fmaxf(mx, lds[c * (d + 2)]);
     float z = 0.f;
-    for (int c = 0; c < nch; ++c) z += cldf(src + (size_t)c * (d + 2) + 1) * expf(cldf(src + (size_t)c * (d + 2)) - mx);
+    for (int c = 0; c < nch; ++c) z += lds[c * (d + 2) + 1] * expf(lds[c * (d + 2)] - mx);
     const float iz = 1.f / z;
     for (int q8 = tid(); q8 < d / 8; q8 += kThreads) {
       float x8[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float o = 0.f;
-        for (int c = 0; c < nch; ++c)
-          o += cldf(src + (size_t)c * (d + 2) + 2 + 8 * q8 + e) * expf(cldf(src + (size_t)c * (d + 2)) - mx);
+        for (int c = 0; c < nch; ++c) o += lds[c * (d + 2) + 2 + 8 * q8 + e] * expf(lds[c * (d + 2)] - mx);
         x8[e] = o * iz;
       }
       store_split(Aout + h * d + 8 * q8, x8);
     }
+    __syncthreads();
   }
 }
 
@@ -1208,7 +1210,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __res
     ok = grid_sync<OParams, false>(op, gen, sh);
     if (ok) outer_attn(op, sh, l, call.pos, dyn);
     ok = ok && grid_sync<OParams, false>(op, gen, sh);
-    if (ok) outer_attn_merge(op, call.pos, A1);
+    if (ok) outer_attn_merge(op, call.pos, A1, dyn);
     ok = ok && grid_sync<OParams, false>(op, gen, sh);
     if (ok) proj_partial<4, OParams, true>(op, bw(p, boff(p, l, p->o_wo)), H, p->qdim, op->ks_o, A1, dyn);
     ok = ok && grid_sync<OParams, false>(op, gen, sh);
