@@ -398,12 +398,41 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
     if (!st[kLnActive]) continue;
     const int fp = st[kLnFirst], R = st[kLnRows], row0 = ln * bp->rpl;
     float* kvc = bp->kv + (((size_t)ln * p->L + l) * p->nkv + g) * kMaxPos * 2 * d;
-    for (int e = tid(); e < R * 3 * d; e += kThreads) {
-      const int r = e / (3 * d), w = e - r * 3 * d, part = w / d, i = w - part * d;
-      const int col = part == 0 ? h * d + i : qdim + (part - 1) * kvdim + g * d + i;
-      const float s = sum_parts(bp->part + (size_t)(row0 + r) * N + col, (size_t)M * N, KS);
-      if (part == 0) qs[r * d + i] = s;
-      else kvs[(size_t)(fp + r) * 2 * d + (part - 1) * d + i] = s;
+    // q, k, v of the lane's rows: the partial sums of 4 elements x 4 splits are in flight at once
+    const int tot = R * 3 * d;
+    for (int base = 0; base < tot; base += 4 * kThreads) {
+      const float* src[4];
+      float acc[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + k * kThreads + tid();
+        const int r = e / (3 * d), w = e - r * 3 * d, part = w / d, i = w - part * d;
+        const int col = part == 0 ? h * d + i : qdim + (part - 1) * kvdim + g * d + i;
+        src[k] = e < tot ? bp->part + (size_t)(row0 + r) * N + col : nullptr;
+        acc[k] = 0.f;
+      }
+      for (int ks0 = 0; ks0 < KS; ks0 += 4) {
+        float t[4][4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            t[k][j] = (src[k] && ks0 + j < KS) ? ldf(src[k] + (size_t)(ks0 + j) * M * N) : 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (ks0 + j < KS) acc[k] += t[k][j];
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + k * kThreads + tid();
+        if (e < tot) {
+          const int r = e / (3 * d), w = e - r * 3 * d, part = w / d, i = w - part * d;
+          if (part == 0) qs[r * d + i] = acc[k];
+          else kvs[(size_t)(fp + r) * 2 * d + (part - 1) * d + i] = acc[k];
+        }
+      }
     }
     lds_fill<false>(kvs, kvc, fp * 2 * d, 2 * d, (size_t)2 * d);
     __syncthreads();
