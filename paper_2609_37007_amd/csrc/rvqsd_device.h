@@ -172,6 +172,18 @@ __device__ __forceinline__ double wave_scan_incld(double v) {
 // 16 bytes of weights (a builtin vector type, so address-space qualified loads copy it)
 typedef uint32_t W16 __attribute__((ext_vector_type(4)));
 
+// Four activation words through one device-coherent 16-byte load. The load is
+// issued here and completes at vm_wait, which names the result as an operand so
+// that no use of it is scheduled before the wait; several loads issued back to
+// back are in flight together. Each 32-bit word is written atomically by its
+// producer, so every word's parity bit is checked on its own.
+__device__ __forceinline__ W16 pload4(const uint32_t* p) {
+  W16 r;
+  asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+__device__ __forceinline__ void vm_wait(W16& r) { asm volatile("s_waitcnt vmcnt(0)" : "+v"(r)::"memory"); }
+
 // Sum over the 32 lanes of each half of the wave (every lane gets its half's sum).
 __device__ __forceinline__ float half_sum(float v) {
   v = row16_sum(v);

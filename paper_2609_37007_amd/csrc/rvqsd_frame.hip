@@ -386,7 +386,7 @@ __device__ __forceinline__ void put_split(uint32_t* xsp, int stride, int m, int 
 }
 
 // Poll rows 0..R-1 of a parity activation buffer [kMaxRows][K] chunk by chunk
-// (8 floats = 4 words of 8 bytes) and store them split into xsp. With GAIN the
+// (8 floats = two 16-byte halves) and store them split into xsp. With GAIN the
 // stored value is gain[k] * x (gain global, [K]) and sqc ([R][K/8]) receives
 // each chunk's sum of squares of the raw x for the row's RMSNorm.
 // Chunk i of the pass is handled by thread i % kThreads; up to CB chunks per
@@ -414,21 +414,38 @@ __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, i
     uint64_t t0 = 0;
     int spins = 0;
     while (pending) {
+      // 16-byte loads: half hh of a chunk (words 4 hh .. 4 hh + 3) is reloaded while any of its words is missing
+      W16 v4[CB][2];
 #pragma unroll
       for (int b = 0; b < CB; ++b) {
         const int idx = base + b * kThreads + tid();
         const int m = idx / nch, q = idx - m * nch;
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-          if (pending & (1u << (4 * b + w))) v[b][w] = pload2(src + (size_t)m * K + q * 8 + 2 * w);
+        for (int hh = 0; hh < 2; ++hh) {
+          v4[b][hh] = (W16)(0u);
+          if (pending & (3u << (4 * b + 2 * hh))) v4[b][hh] = pload4(src + (size_t)m * K + q * 8 + 4 * hh);
+        }
       }
 #pragma unroll
       for (int b = 0; b < CB; ++b)
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-          if (pending & (1u << (4 * b + w))) {
-            const uint32_t lo = (uint32_t)v[b][w], hi = (uint32_t)(v[b][w] >> 32);
-            if ((lo & 1u) == par && (hi & 1u) == par) pending &= ~(1u << (4 * b + w));
+        for (int hh = 0; hh < 2; ++hh) vm_wait(v4[b][hh]);
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          if (pending & (3u << (4 * b + 2 * hh))) {
+            v[b][2 * hh] = (uint64_t)v4[b][hh][0] | ((uint64_t)v4[b][hh][1] << 32);
+            v[b][2 * hh + 1] = (uint64_t)v4[b][hh][2] | ((uint64_t)v4[b][hh][3] << 32);
+          }
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          if (pending & (3u << (4 * b + 2 * hh))) {
+            const W16 w4 = v4[b][hh];
+            if ((w4[0] & 1u) == par && (w4[1] & 1u) == par && (w4[2] & 1u) == par && (w4[3] & 1u) == par)
+              pending &= ~(3u << (4 * b + 2 * hh));
           }
       if (!pending) break;
       if ((++spins & 31) == 0) {
