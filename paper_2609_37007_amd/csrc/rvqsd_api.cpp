@@ -759,7 +759,7 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
   *out = nullptr;
   const KParams& k = m->base;
   if (n_tables < 0 || n_tables > kMaxCodes || table_vocab < 1 || topk < 1 || topk > kMaxTopk ||
-      !(temperature > 0.0) || max_frames < 1 || max_frames > 4096)
+      !(temperature > 0.0) || max_frames < 1 || max_frames > kMaxOuterFrames)
     return set_err(RVQSD_EINVAL, "invalid outer-step argument");
   if (m->cfg.dtype != RVQSD_DTYPE_BF16) return set_err(RVQSD_EUNSUPPORTED, "the outer step needs bf16 weights");
   if (k.H % 512 || k.qdim % 256 || k.F % 256 || k.H > 2048 || m->nwg < 8)
@@ -797,7 +797,7 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
   const size_t o_tab = take(tab_bytes), o_rope = take((size_t)max_frames * k.d * 4), o_x = take((size_t)k.H * 4),
                o_a = take(2 * kmax * 4), o_part = take(part * 4),
                o_kv = take((size_t)k.L * k.nkv * max_frames * 2 * k.d * 4),
-               o_apart = take((size_t)k.nq * kAttnChunks * (k.d + 2) * 4), o_log = take((size_t)k.V * 4),
+               o_apart = take((size_t)k.nq * kAttnMaxChunks * (k.d + 2) * 4), o_log = take((size_t)k.V * 4),
                o_last = take((size_t)(1 + kMaxCodes) * 4), o_f = take((size_t)k.H * 4), o_op = take(sizeof(OParams)),
                o_kp = take(sizeof(KParams));
   hipError_t e = dev_alloc(&o->buf, off);
@@ -848,10 +848,14 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
   }
   size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
   const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + kMaxTopk * 8 + kTopkBuckets * 4;
-  const size_t chunk = (max_frames + kAttnChunks - 1) / kAttnChunks;  // key positions per chunk at most
-  const size_t attn = ((size_t)3 * k.d + chunk + chunk * k.d) * 4;
+  // attention: q, k, v, scores, group sums, then the chunk's keys and values (16-byte aligned)
+  const size_t chunk = (size_t)attn_chunk_len(max_frames, k.d), G = (size_t)(kThreads / k.d);
+  const size_t attn = (((3 * (size_t)k.d + chunk + G * k.d + G + 3) & ~(size_t)3) + chunk * 2 * k.d) * 4;
+  // merge: the chunk partials of one head, the chunk weights and the merged output
+  const size_t merge = ((size_t)kAttnMaxChunks * (k.d + 2) + kAttnMaxChunks + k.d) * 4;
   if (samp > lds) lds = samp;
   if (attn > lds) lds = attn;
+  if (merge > lds) lds = merge;
   if ((size_t)k.H * 4 > lds) lds = (size_t)k.H * 4;
   o->lds = lds + 64;
   *out = o;

@@ -1054,24 +1054,48 @@ __device__ void outer_input(const OParams* op, BShared* sh, const OCall& call, u
   }
 }
 
-// chunk attention: unit (query head h, key chunk c) over positions of that chunk
+// dst[e] = src[e] for n4 16-byte groups (both 16-byte aligned); each thread has 16 loads in flight
+__device__ __forceinline__ void lds_fill4(float* dst, const float* src, int n4) {
+  for (int base = 0; base < n4; base += 16 * kThreads) {
+    f32x4 v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int e = base + k * kThreads + tid();
+      v[k] = e < n4 ? G(reinterpret_cast<const f32x4*>(src))[e] : (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int e = base + k * kThreads + tid();
+      if (e < n4) reinterpret_cast<f32x4*>(dst)[e] = v[k];
+    }
+  }
+}
+
+// Chunk attention: unit (query head h, key chunk c) over the positions of that chunk.
+// The chunk's keys and values come into LDS in one batch of loads; each position's
+// softmax weight exp(s_t - max) is taken once, and the weighted sum of the values is
+// split over nog = kThreads / d groups of positions that are added in group order.
 __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float* lds) {
   const KParams* p = op->k;
   const int d = p->d, nq = p->nq, grp = nq / p->nkv, N = p->nqkv, KS = op->ks_qkv, half = d / 2;
   const int lane = tid() & 63, wave = tid() >> 6;
-  const int np = pos + 1, ch = (np + kAttnChunks - 1) / kAttnChunks, nch = (np + ch - 1) / ch;
-  float* qv = lds;            // [d]
-  float* kn = qv + d;         // [d] this position's k
-  float* vn = kn + d;         // [d] this position's v
-  float* sc = vn + d;         // [chunk] scores
-  float* kvs = sc + ch;       // [chunk][d] the chunk's keys, then its values
+  const int np = pos + 1, ch = attn_chunk_len(np, d), nch = (np + ch - 1) / ch;
+  const int nog = kThreads / d;
+  float* qv = lds;                // [d]
+  float* kn = qv + d;             // [d] this position's k
+  float* vn = kn + d;             // [d] this position's v
+  float* sc = vn + d;             // [ch] scores, then softmax weights
+  float* og = sc + ch;            // [nog][d] group sums of the weighted values
+  float* zg = og + nog * d;       // [nog] group sums of the weights
+  float* kvs = lds + ((3 * d + ch + nog * d + nog + 3) & ~3);  // [ch][2d] the chunk's keys and values
   const float* qn = bfw(p, boff(p, l, p->o_qn));
   const float* kng = bfw(p, boff(p, l, p->o_kn));
   const float scale = 1.f / sqrtf((float)d);
   for (int u = blockIdx.x; u < nq * nch; u += op->nwg) {
     const int h = u / nch, c = u - h * nch, g = h / grp;
-    const int t0 = c * ch, t1 = min(np, t0 + ch);
+    const int t0 = c * ch, t1 = min(np, t0 + ch), n = t1 - t0;
     float* kvc = op->kv + (((size_t)l * p->nkv + g) * op->max_frames) * 2 * d;
+    lds_fill4(kvs, kvc + (size_t)t0 * 2 * d, n * d / 2);
     for (int e = tid(); e < 3 * d; e += kThreads) {
       const int part = e / d, i = e - part * d;
       const int col = part == 0 ? h * d + i : p->qdim + (part - 1) * p->kvdim + g * d + i;
@@ -1101,38 +1125,43 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
     __syncthreads();
     if (h % grp == 0 && c == 0)
       for (int e = tid(); e < 2 * d; e += kThreads) cstf(kvc + (size_t)pos * 2 * d + e, e < d ? kn[e] : vn[e - d]);
-    // the chunk's keys into LDS (all loads issued together), then one wave per position
-    lds_fill<false>(kvs, kvc + (size_t)t0 * 2 * d, (t1 - t0) * d, d, (size_t)2 * d);
-    __syncthreads();
-    // this frame's position is not in the cache yet (written in this phase): its own k
+    // this frame's position is not in the cache yet (it is written in this phase): its own k and v
     if (t1 - 1 == pos)
-      for (int i = tid(); i < d; i += kThreads) kvs[(pos - t0) * d + i] = kn[i];
+      for (int i = tid(); i < 2 * d; i += kThreads) kvs[(pos - t0) * 2 * d + i] = i < d ? kn[i] : vn[i - d];
     __syncthreads();
-    for (int t = t0 + wave; t < t1; t += kWaves) {
+    // scores, one wave per position
+    for (int t = wave; t < n; t += kWaves) {
       float a = 0.f;
-      for (int i = lane; i < d; i += 64) a = fmaf(qv[i], kvs[(t - t0) * d + i], a);
+      for (int i = lane; i < d; i += 64) a = fmaf(qv[i], kvs[t * 2 * d + i], a);
       a = wave_sum(a) * scale;
-      if (lane == 0) sc[t - t0] = a;
+      if (lane == 0) sc[t] = a;
     }
     __syncthreads();
-    // then its values
-    lds_fill<false>(kvs, kvc + (size_t)t0 * 2 * d + d, (t1 - t0) * d, d, (size_t)2 * d);
-    __syncthreads();
-    if (t1 - 1 == pos)
-      for (int i = tid(); i < d; i += kThreads) kvs[(pos - t0) * d + i] = vn[i];
-    __syncthreads();
     float mx = -INFINITY;
-    for (int t = 0; t < t1 - t0; ++t) mx = fmaxf(mx, sc[t]);
-    float* dst = op->apart + ((size_t)h * kAttnChunks + c) * (d + 2);
-    for (int i = tid(); i < d; i += kThreads) {
+    for (int t = 0; t < n; ++t) mx = fmaxf(mx, sc[t]);
+    __syncthreads();  // every thread has its maximum before the scores become weights
+    for (int t = tid(); t < n; t += kThreads) sc[t] = expf(sc[t] - mx);
+    __syncthreads();
+    if (tid() < nog * d) {
+      const int gi = tid() / d, i = tid() - gi * d;
       float o = 0.f, z = 0.f;
-      for (int t = 0; t < t1 - t0; ++t) {
-        const float w = expf(sc[t] - mx);
+      for (int t = gi; t < n; t += nog) {
+        const float w = sc[t];
+        o = fmaf(w, kvs[t * 2 * d + d + i], o);
         z += w;
-        o = fmaf(w, kvs[t * d + i], o);
       }
+      og[gi * d + i] = o;
+      if (i == 0) zg[gi] = z;
+    }
+    __syncthreads();
+    float* dst = op->apart + ((size_t)h * kAttnMaxChunks + c) * (d + 2);
+    for (int i = tid(); i < d; i += kThreads) {
+      float o = og[i];
+      for (int gi = 1; gi < nog; ++gi) o += og[gi * d + i];
       cstf(dst + 2 + i, o);
       if (i == 0) {
+        float z = zg[0];
+        for (int gi = 1; gi < nog; ++gi) z += zg[gi];
         cstf(dst, mx);
         cstf(dst + 1, z);
       }
@@ -1144,24 +1173,30 @@ __device__ void outer_attn(const OParams* op, BShared* sh, int l, int pos, float
 // merge the chunk partials of query head h (workgroup h) into the O projection's input
 __device__ void outer_attn_merge(const OParams* op, int pos, uint32_t* Aout, float* lds) {
   const KParams* p = op->k;
-  const int d = p->d, np = pos + 1, ch = (np + kAttnChunks - 1) / kAttnChunks, nch = (np + ch - 1) / ch;
+  const int d = p->d, np = pos + 1, ch = attn_chunk_len(np, d), nch = (np + ch - 1) / ch;
+  float* w = lds + nch * (d + 2);  // [nch] chunk weights exp(m_c - max)
+  float* xo = w + nch;             // [d] the merged output
   for (int h = blockIdx.x; h < p->nq; h += op->nwg) {
     // the head's chunk partials (max, sum, o[d]) into LDS, all loads in flight together
-    lds_fill<true>(lds, op->apart + (size_t)h * kAttnChunks * (d + 2), nch * (d + 2), nch * (d + 2), 0);
+    lds_fill<true>(lds, op->apart + (size_t)h * kAttnMaxChunks * (d + 2), nch * (d + 2), nch * (d + 2), 0);
     __syncthreads();
     float mx = -INFINITY;
     for (int c = 0; c < nch; ++c) mx = fmaxf(mx, lds[c * (d + 2)]);
+    for (int c = tid(); c < nch; c += kThreads) w[c] = expf(lds[c * (d + 2)] - mx);
+    __syncthreads();
     float z = 0.f;
-    for (int c = 0; c < nch; ++c) z += lds[c * (d + 2) + 1] * expf(lds[c * (d + 2)] - mx);
+    for (int c = 0; c < nch; ++c) z += lds[c * (d + 2) + 1] * w[c];
     const float iz = 1.f / z;
+    for (int i = tid(); i < d; i += kThreads) {
+      float o = 0.f;
+      for (int c = 0; c < nch; ++c) o += lds[c * (d + 2) + 2 + i] * w[c];
+      xo[i] = o * iz;
+    }
+    __syncthreads();
     for (int q8 = tid(); q8 < d / 8; q8 += kThreads) {
       float x8[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float o = 0.f;
-        for (int c = 0; c < nch; ++c) o += lds[c * (d + 2) + 2 + 8 * q8 + e] * expf(lds[c * (d + 2)] - mx);
-        x8[e] = o * iz;
-      }
+      for (int e = 0; e < 8; ++e) x8[e] = xo[8 * q8 + e];
       store_split(Aout + h * d + 8 * q8, x8);
     }
     __syncthreads();

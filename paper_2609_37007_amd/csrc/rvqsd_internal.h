@@ -128,7 +128,16 @@ int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, si
 // ---------------------------------------------------------------- outer decoder step
 // The outer CodeDecoder of the per-frame pipeline: one position per frame, a KV
 // cache that grows across frames, c_0 sampled from its head.
-constexpr int kAttnChunks = 16;  // key chunks per query head (split-sequence attention)
+constexpr int kAttnChunks = 16;       // key chunks per query head the split aims for (split-sequence attention)
+constexpr int kAttnKVFloats = 32768;  // LDS floats for one chunk's keys and values (128 KB)
+constexpr int kMaxOuterFrames = 4096; // KV capacity of the outer decoder at most
+constexpr int kAttnMaxChunks = 64;    // chunks per head at most: 4096 positions in chunks of >= 64 (head_dim <= 256)
+// Key positions per chunk when np positions are attended: about np / kAttnChunks,
+// at most what kAttnKVFloats holds for keys and values of head dimension d.
+constexpr int attn_chunk_len(int np, int d) {
+  return (np + kAttnChunks - 1) / kAttnChunks < kAttnKVFloats / (2 * d) ? (np + kAttnChunks - 1) / kAttnChunks
+                                                                       : kAttnKVFloats / (2 * d);
+}
 
 struct OParams {
   const KParams* k;      // the outer model's parameter block (dimensions, weights)
@@ -142,7 +151,7 @@ struct OParams {
   uint32_t* a;           // [2][max(H, qdim, F)] split activations
   float* part;           // [max ks][max N] partial sums
   float* kv;             // [L][nkv][max_frames][2][d] KV cache (k after norm and RoPE, v)
-  float* apart;          // [nq][kAttnChunks][d + 2] per-chunk attention partials (max, sum, o)
+  float* apart;          // [nq][kAttnMaxChunks][d + 2] per-chunk attention partials (max, sum, o)
   float* logits;         // [V]
   uint32_t* bar;         // grid barrier words
   int32_t* status;       // first device-side error of the step (0 = none)
