@@ -162,34 +162,37 @@ __device__ __forceinline__ bool poll_range(const Ctx& c, const uint64_t* src, in
   return poll_words(c, n, tag, [=](int i) { return src + i; }, sink);
 }
 
-// Poll n2 pairs of parity words; addr(i) gives pair i (8-byte aligned),
-// sink(i, lo, hi) receives both values once both carry parity `par`.
+// Poll n4 groups of four parity words; addr(i) gives group i (16-byte aligned),
+// sink(i, w) receives the group's words once all four carry parity `par`.
 template <typename Addr, typename Sink>
-__device__ __forceinline__ bool poll_pairs(const Ctx& c, int n2, uint32_t par, Addr addr, Sink sink) {
-  constexpr int B = 8;
-  for (int base = 0; base < n2; base += B * kThreads) {
+__device__ __forceinline__ bool poll_quads(const Ctx& c, int n4, uint32_t par, Addr addr, Sink sink) {
+  constexpr int B = 4;
+  for (int base = 0; base < n4; base += B * kThreads) {
     int idx[B];
     bool got[B];
 #pragma unroll
     for (int k = 0; k < B; ++k) {
       idx[k] = base + k * kThreads + tid();
-      got[k] = idx[k] >= n2;
+      got[k] = idx[k] >= n4;
     }
     uint64_t t0 = 0;
     int spins = 0;
     while (true) {
-      uint64_t v[B];
+      W16 v[B];
 #pragma unroll
-      for (int k = 0; k < B; ++k)
-        if (!got[k]) v[k] = pload2(addr(idx[k]));
+      for (int k = 0; k < B; ++k) {
+        v[k] = (W16)(0u);
+        if (!got[k]) v[k] = pload4(addr(idx[k]));
+      }
+#pragma unroll
+      for (int k = 0; k < B; ++k) vm_wait(v[k]);
       bool all = true;
 #pragma unroll
       for (int k = 0; k < B; ++k) {
         if (!got[k]) {
-          const uint32_t lo = (uint32_t)v[k], hi = (uint32_t)(v[k] >> 32);
-          if ((lo & 1u) == par && (hi & 1u) == par) {
+          if ((v[k][0] & 1u) == par && (v[k][1] & 1u) == par && (v[k][2] & 1u) == par && (v[k][3] & 1u) == par) {
             got[k] = true;
-            sink(idx[k], __uint_as_float(lo), __uint_as_float(hi));
+            sink(idx[k], v[k]);
           } else {
             all = false;
           }
@@ -706,11 +709,11 @@ __device__ __forceinline__ void chunk_from_lds(const float* xs, int ld, int kc, 
 template <int MR>
 __device__ __forceinline__ bool stage_par(const Ctx& c, const uint32_t* src, int ncols, int R, uint32_t par, float* xs) {
   for (int i = tid(); i < (MR - R) * ncols; i += kThreads) xs[R * ncols + i] = 0.f;
-  const bool ok = poll_pairs(
-      c, R * ncols / 2, par, [=](int i) { return src + 2 * i; },
-      [=](int i, float lo, float hi) {
-        xs[2 * i] = lo;
-        xs[2 * i + 1] = hi;
+  const bool ok = poll_quads(
+      c, R * ncols / 4, par, [=](int i) { return src + 4 * i; },
+      [=](int i, W16 w) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) xs[4 * i + e] = __uint_as_float(w[e]);
       });
   return wg_sync_ok(c, ok);
 }
@@ -837,21 +840,21 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
     pw[i] = wi < past_words ? xload(gkv + wi) : 0ull;
   }
   const uint32_t par = par_layer(c, sh->pass, l);
-  // q of head h, k and v of kv head g, for every row of the pass (pairs of words);
+  // q of head h, k and v of kv head g, for every row of the pass (groups of four words);
   // qs, ks, vs are consecutive [kMaxRows][d] blocks and v of kv head g follows k at +kvdim
-  const int rd2 = R * d / 2, d2 = d / 2, kvdim = p->kvdim;
+  const int rd4 = R * d / 4, d4 = d / 4, kvdim = p->kvdim;
   const uint32_t* qkvb = p->qkvb;
-  bool ok = poll_pairs(
-      c, 3 * rd2, par,
+  bool ok = poll_quads(
+      c, 3 * rd4, par,
       [=](int i) {
-        const int part = i / rd2, rem = i - part * rd2, r = rem / d2, k = 2 * (rem - r * d2);
+        const int part = i / rd4, rem = i - part * rd4, r = rem / d4, k = 4 * (rem - r * d4);
         const int off = part == 0 ? qoff : koff + (part - 1) * kvdim;
         return qkvb + (size_t)r * N + off + k;
       },
-      [=](int i, float lo, float hi) {
-        const int part = i / rd2, rem = i - part * rd2;
-        qs[part * kMaxRows * d + 2 * rem] = lo;
-        qs[part * kMaxRows * d + 2 * rem + 1] = hi;
+      [=](int i, W16 w) {
+        const int part = i / rd4, rem = i - part * rd4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qs[part * kMaxRows * d + 4 * rem + e] = __uint_as_float(w[e]);
       });
 #pragma unroll
   for (int i = 0; i < KVW; ++i) {
@@ -943,18 +946,18 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
       const float rsum = row16_sum(qj == 0 ? e : 0.f);
       const float z = (lane_val(rsum, 15) + lane_val(rsum, 31)) + (lane_val(rsum, 47) + lane_val(rsum, 63));
       const float pr = e * __builtin_amdgcn_rcpf(z);
-      // o[r][i] = sum_t pr_t v[t][i] for i = lane + 64 j (head_dim <= 256); positions after this
-      // row's own hold this pass's later rows with weight 0, so only the pass-wide bound branches
+      // o[r][i] = sum_t pr_t v[t][i] for i = lane + 64 j (head_dim <= 256). Positions after this
+      // row's own carry weight 0; those at or past npos read the finite row npos - 1 instead
+      // of their unset LDS rows, so the loop has no branch and its LDS loads can all be issued
+      // ahead of the products.
       float o[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int tt = 0; tt < kMaxPos; ++tt) {
-        if (tt < npos) {
-          const float pt = lane_val(pr, 4 * tt);
-          const float* vv = kv + (size_t)tt * ps + d;
+        const float pt = lane_val(pr, 4 * tt);
+        const float* vv = kv + (size_t)min(tt, npos - 1) * ps + d;
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (lane + 64 * j < d) o[j] = fmaf(pt, vv[lane + 64 * j], o[j]);
-        }
+        for (int j = 0; j < 4; ++j)
+          if (lane + 64 * j < d) o[j] = fmaf(pt, vv[lane + 64 * j], o[j]);
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j)
@@ -1476,8 +1479,9 @@ __device__ __forceinline__ bool phase_sample(const Ctx& c) {
   float* lg = c.work;                                          // [V]
   int* sidx = reinterpret_cast<int*>(lg + V);                  // [kMaxTopk]
   float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);     // [kMaxTopk]
-  double* prob = reinterpret_cast<double*>(
-      (reinterpret_cast<uintptr_t>(slog + kMaxTopk) + 7) & ~(uintptr_t)7);  // [kMaxTopk]
+  // fp64 arrays from the next 8-byte boundary (the work area is 8-byte aligned); an index,
+  // not an integer cast of the pointer, so that the compiler keeps them in the LDS address space
+  double* prob = reinterpret_cast<double*>(lg + ((V + 2 * kMaxTopk + 1) & ~1));  // [kMaxTopk]
   double* qprob = prob + kMaxTopk;                             // [kMaxTopk]
   double* res = qprob + kMaxTopk;                              // [kMaxTopk]
   int* qidx = reinterpret_cast<int*>(res + kMaxTopk);          // [kMaxTopk]
