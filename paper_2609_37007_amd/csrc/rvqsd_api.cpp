@@ -180,7 +180,7 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
     need((size_t)mr * H + (size_t)rows_out * mr);
     need((size_t)mr * stage_cols + (size_t)cpw * mr);
   }
-  need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4));  // attention: q, k, v rows and the head's KV
+  need((size_t)3 * kMaxRows * d + (size_t)kMaxPos * (2 * d + 4) + (size_t)kMaxRows * kMaxPos);  // attention: q, k, v rows, the head's KV, softmax weights
   need((size_t)V + 2 * kMaxTopk + 2 + 2 * 3 * kMaxTopk + kMaxTopk + kTopkBuckets + 8);  // sampling
   return w;
 }

@@ -636,8 +636,9 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
   float* lg = lds;                                            // [V]
   int* sidx = reinterpret_cast<int*>(lg + V);                 // [kMaxTopk]
   float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);    // [kMaxTopk]
-  double* prob = reinterpret_cast<double*>(
-      (reinterpret_cast<uintptr_t>(slog + kMaxTopk) + 7) & ~(uintptr_t)7);  // [kMaxTopk]
+  // fp64 arrays from the next 8-byte boundary (lg is 8-byte aligned); an index, not an
+  // integer cast of the pointer, so that the compiler keeps them in the LDS address space
+  double* prob = reinterpret_cast<double*>(lg + ((V + 2 * kMaxTopk + 1) & ~1));  // [kMaxTopk]
   double* qprob = prob + kMaxTopk;
   double* res = qprob + kMaxTopk;
   int* qidx = reinterpret_cast<int*>(res + kMaxTopk);         // [kMaxTopk]
@@ -1237,7 +1238,7 @@ __device__ void outer_sample(const OParams* op, BShared* sh, const OCall& call, 
   float* lg = lds;
   int* sidx = reinterpret_cast<int*>(lg + V);
   float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);
-  double* prob = reinterpret_cast<double*>((reinterpret_cast<uintptr_t>(slog + kMaxTopk) + 7) & ~(uintptr_t)7);
+  double* prob = reinterpret_cast<double*>(lg + ((V + 2 * kMaxTopk + 1) & ~1));  // 8-byte aligned, as above
   unsigned* hist = reinterpret_cast<unsigned*>(prob + kMaxTopk);
   lds_fill<true>(lg, op->logits, V, V, 0);
   __syncthreads();

@@ -828,6 +828,7 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   float* ks = qs + kMaxRows * d;
   float* vs = ks + kMaxRows * d;
   float* kv = vs + kMaxRows * d;   // [kMaxPos][ps]: k, v of every position
+  float* pw_lds = kv + kMaxPos * ps;  // [kMaxRows][kMaxPos] softmax weights of each row
   uint64_t* gkv = reinterpret_cast<uint64_t*>(p->kvc + ((size_t)h * p->L + l) * kMaxPos * 2 * d);
   const int lane = tid() & 63, wave = tid() >> 6;
   // past positions 0 .. fp-1: issue the loads now, store them to LDS after the wait
@@ -946,19 +947,27 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
       const float rsum = row16_sum(qj == 0 ? e : 0.f);
       const float z = (lane_val(rsum, 15) + lane_val(rsum, 31)) + (lane_val(rsum, 47) + lane_val(rsum, 63));
       const float pr = e * __builtin_amdgcn_rcpf(z);
+      // the row's weights go through LDS (written and read back by this wave only, in order)
+      // and come back to every lane as four 16-byte broadcasts
+      float* pwr = pw_lds + r * kMaxPos;
+      if (qj == 0) pwr[t] = pr;
+      f32x4 pq[kMaxPos / 4];
+#pragma unroll
+      for (int q4 = 0; q4 < kMaxPos / 4; ++q4) pq[q4] = reinterpret_cast<const f32x4*>(pwr)[q4];
       // o[r][i] = sum_t pr_t v[t][i] for i = lane + 64 j (head_dim <= 256). Positions after this
       // row's own carry weight 0; those at or past npos read the finite row npos - 1 instead
-      // of their unset LDS rows, so the loop has no branch and its LDS loads can all be issued
-      // ahead of the products.
-      float o[4] = {0.f, 0.f, 0.f, 0.f};
+      // of their unset LDS rows, so all the value loads are issued before the products.
+      float vv[kMaxPos][4];
 #pragma unroll
-      for (int tt = 0; tt < kMaxPos; ++tt) {
-        const float pt = lane_val(pr, 4 * tt);
-        const float* vv = kv + (size_t)min(tt, npos - 1) * ps + d;
+      for (int tt = 0; tt < kMaxPos; ++tt)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          if (lane + 64 * j < d) o[j] = fmaf(pt, vv[lane + 64 * j], o[j]);
-      }
+          vv[tt][j] = lane + 64 * j < d ? kv[(size_t)min(tt, npos - 1) * ps + d + lane + 64 * j] : 0.f;
+      float o[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int tt = 0; tt < kMaxPos; ++tt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = fmaf(pq[tt >> 2][tt & 3], vv[tt][j], o[j]);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (lane + 64 * j < d) pstore(p->attnb + (size_t)r * p->qdim + qoff + lane + 64 * j, o[j], par);
