@@ -604,23 +604,35 @@ __device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
 // Algorithmic bytes of one batched pass: the layer weights and every LM head
 // some lane uses (each read once), the gathered embedding rows and the KV
 // cache every lane attends over.
+// Called by the 64 threads of one wave: thread i counts stream lane i, and the
+// wave adds the counts and merges the used heads (integer sums: the order does
+// not matter). The result is valid in every thread.
 __device__ unsigned long long pass_bytes_batch(const BParams* bp, const BShared* sh) {
   const KParams* p = bp->k;
-  unsigned long long b = (unsigned long long)p->L * p->layer_stride;
+  const int lane = tid() & 63;
+  const int H = p->H;
+  const unsigned long long kv_pos = (unsigned long long)p->L * p->nkv * p->d * 2 * 4;  // KV bytes per position
   unsigned used = 0;  // bit t: head t used
-  for (int ln = 0; ln < bp->lanes; ++ln) {
-    const int* st = sh->ln[ln];
-    if (!st[kLnActive]) continue;
-    for (int r = 0; r < st[kLnRows]; ++r) {
-      const int s = st[kLnFirst] + r;
-      if (row_is_verify(st, r)) used |= 1u << s;
-      for (int j = 1; j <= row_drafts(p, st, r); ++j) used |= 1u << (s + j);
-      b += (s == 0) ? 4ull * p->H : 2ull * p->H;
+  unsigned long long b = 0;
+  if (lane < bp->lanes) {
+    const int* st = sh->ln[lane];
+    if (st[kLnActive]) {
+      const int first = st[kLnFirst], rows = st[kLnRows];
+      for (int r = 0; r < rows; ++r) {
+        const int s = first + r;
+        if (row_is_verify(st, r)) used |= 1u << s;
+        const int nd = row_drafts(p, st, r);
+        for (int j = 1; j <= nd; ++j) used |= 1u << (s + j);
+        b += (s == 0) ? 4ull * H : 2ull * H;
+      }
+      b += kv_pos * (unsigned long long)(first + rows);
     }
-    b += (unsigned long long)p->L * (st[kLnFirst] + st[kLnRows]) * p->nkv * p->d * 2 * 4;
   }
-  b += (unsigned long long)__popc(used) * p->table_stride;
-  return b;
+  for (int o = 32; o > 0; o >>= 1) {
+    used |= (unsigned)__shfl_xor((int)used, o);
+    b += (unsigned long long)__shfl_xor((long long)b, o);
+  }
+  return b + (unsigned long long)p->L * p->layer_stride + (unsigned long long)__popc(used) * p->table_stride;
 }
 
 // ------------------------------------------------------------ sampling
@@ -983,9 +995,12 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
       if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
       ok = ok && grid_sync(bp, gen, sh);
       if (ok) phase_resid(bp, sh, bp->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, 0, dyn);
-      if (ok && l == 0 && counter_wg && tid() == 0) {
-        n_pass += 1;
-        n_bytes += pass_bytes_batch(bp, sh);
+      if (ok && l == 0 && counter_wg && tid() < 64) {
+        const unsigned long long pb = pass_bytes_batch(bp, sh);
+        if (tid() == 0) {
+          n_pass += 1;
+          n_bytes += pb;
+        }
       }
       ok = ok && grid_sync(bp, gen, sh);
       if (ok) phase_gu(bp, l, A0, A1, dyn);
