@@ -1039,21 +1039,35 @@ __device__ void outer_input(const OParams* op, BShared* sh, const OCall& call, u
   const KParams* p = op->k;
   const int H = p->H;
   float ss = 0.f;
-  // the previous frame's codes must be in range (a failed frame leaves -1): else no input
-  bool codes_ok = call.prev_codes != nullptr;
-  for (int j = 0; codes_ok && j <= op->n_tables; ++j) {
-    const int c = G(call.prev_codes)[j];
-    codes_ok = c >= 0 && c < (j == 0 ? min(p->V, op->table_vocab) : op->table_vocab);
+  // the previous frame's codes (one thread each) must be in range (a failed frame leaves -1):
+  // else no input
+  __shared__ int pcodes[kMaxCodes + 1];
+  __shared__ int pbad;
+  const int nt = op->n_tables;
+  if (tid() == 0) pbad = 0;
+  __syncthreads();
+  if (call.prev_codes && tid() <= nt) {
+    const int c = G(call.prev_codes)[tid()];
+    pcodes[tid()] = c;
+    if (!(c >= 0 && c < (tid() == 0 ? min(p->V, op->table_vocab) : op->table_vocab))) pbad = 1;
   }
+  __syncthreads();
+  const bool codes_ok = call.prev_codes != nullptr && pbad == 0;
   if (call.prev_codes && !codes_ok && tid() == 0) raise_status(op, RVQSD_EINVAL);
   for (int e = tid(); e < H; e += kThreads) {
     float v = G(call.t)[e];
     if (codes_ok) {
+      // every table row of this element is loaded before the sum (in table order) is taken
       const bf16_t* e0 = bw(p, p->o_emb0);
-      v += __uint_as_float((uint32_t)G(e0)[(size_t)G(call.prev_codes)[0] * H + e] << 16);
-      for (int j = 1; j <= op->n_tables; ++j)
-        v += __uint_as_float(
-            (uint32_t)G(op->tables)[((size_t)(j - 1) * op->table_vocab + G(call.prev_codes)[j]) * H + e] << 16);
+      uint32_t tv[kMaxCodes + 1];
+      tv[0] = G(e0)[(size_t)pcodes[0] * H + e];
+#pragma unroll
+      for (int j = 1; j <= kMaxCodes; ++j)
+        tv[j] = j <= nt ? G(op->tables)[((size_t)(j - 1) * op->table_vocab + pcodes[j]) * H + e] : 0u;
+      v += __uint_as_float(tv[0] << 16);
+#pragma unroll
+      for (int j = 1; j <= kMaxCodes; ++j)
+        if (j <= nt) v += __uint_as_float(tv[j] << 16);
     }
     cstf(op->x + e, v);
     xs[e] = v;
