@@ -503,7 +503,7 @@ __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, i
   }
   return wg_sync_ok(c, true);
 }
-// 1 / sqrt(mean of squares + eps) of staged row m from the per-wave sums of stage_split / split_rows
+// 1 / sqrt(mean of squares + eps) of staged row m from the per-wave sums of stage_split / gather_split_rows
 __device__ __forceinline__ float rstd_of(const Ctx& c, const float* sqc, int K, int m) {
   const int G = K >> 9;
   float s = 0.f;
@@ -511,7 +511,7 @@ __device__ __forceinline__ float rstd_of(const Ctx& c, const float* sqc, int K, 
   return 1.f / sqrtf(s / (float)K + c.p->rms_eps);
 }
 
-// rstd[m] from the per-wave sums of stage_split / split_rows, m < R.
+// rstd[m] from the per-wave sums of stage_split / gather_split_rows, m < R.
 __device__ __forceinline__ void rstd_from_chunks_w(const Ctx& c, const float* sqc, int K, int R) {
   if (tid() < R) c.sh->rstd[tid()] = rstd_of(c, sqc, K, tid());
   __syncthreads();
@@ -656,35 +656,6 @@ struct MTile {
   }
 };
 
-// Split rows 0..R-1 of fp32 activations xs[MR][K] into xsp, times gain
-// (global, nullable); sqc (nullable) receives each chunk's sum of squares of
-// the raw values.
-__device__ __forceinline__ void split_rows(const float* xs, uint32_t* xsp, int K, int R, const float* gain, float* sqc) {
-  const int nch = K >> 3, total = R * nch;
-  for (int base = 0; base < total; base += kThreads) {
-    const int idx = base + tid();
-    float s2 = 0.f;
-    if (idx < total) {
-      const int m = idx / nch, q = idx - m * nch;
-      float x[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float v = xs[(size_t)idx * 8 + e];
-        s2 = fmaf(v, v, s2);
-        x[e] = gain ? v * G(gain)[q * 8 + e] : v;
-      }
-      put_split(xsp, split_stride(K), m, q, x);
-    }
-    // one sum per wave (64 chunks of one row, K a multiple of 512), as stage_split
-    const int i0 = base + (tid() & ~63);
-    if (sqc && i0 < total) {
-      s2 = wave_sum63(s2);
-      if ((tid() & 63) == 63) sqc[i0 >> 6] = s2;
-    }
-  }
-  __syncthreads();
-}
-
 // This thread's chunk of the staged activations xs[MR][ld] (k = kc*EPC ..),
 // times g[e] when g != nullptr; sq[m] = sum of squares of the raw chunk.
 // Threads outside the row groups get zeros.
@@ -753,6 +724,51 @@ __device__ __forceinline__ void gather_rows(const Ctx& c, float* xs) {
       }
     }
     xs[i] = v;
+  }
+  __syncthreads();
+}
+
+// Layer-0 input rows of the bf16 path, gathered straight into the split layout
+// (as stage_split does for the exchanged rows): chunk (m, q) = 8 values of row m,
+// one 16-byte embedding load; this workgroup's residual columns go to xown, the
+// gain-scaled values to xsp, and one sum of squares per wave (64 chunks of one
+// row, hidden a multiple of 512) to sqc. Rows R.. of xown are zero.
+template <int MR>
+__device__ __forceinline__ void gather_split_rows(const Ctx& c, uint32_t* xsp, const float* gain, float* sqc) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int H = p->H, R = sh->rows, nch = H >> 3, total = R * nch;
+  const int o0 = blockIdx.x * c.cpw;
+  for (int i = tid(); i < kMaxRows * c.cpw; i += kThreads)
+    if (i / c.cpw >= R || o0 + i % c.cpw >= H) c.xown[i] = 0.f;
+  for (int base = 0; base < total; base += kThreads) {
+    const int idx = base + tid();
+    float s2 = 0.f;
+    if (idx < total) {
+      const int m = idx / nch, q = idx - m * nch, s = sh->first_pos + m;
+      float x[8];
+      if (s == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = G(sh->fa.frame_hidden)[8 * q + e];
+      } else {
+        const bf16_t* tab = wptr<bf16_t>(p, p->o_emb0 + (uint64_t)(s - 1) * p->table_stride);
+        const W16 w = *G(reinterpret_cast<const W16*>(tab + (size_t)sh->in_code[s] * H + 8 * q));
+        WTraits<bf16_t>::widen(w, x);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int j = 8 * q + e - o0;
+        if (j >= 0 && j < c.cpw) c.xown[m * c.cpw + j] = x[e];
+        s2 = fmaf(x[e], x[e], s2);
+        x[e] *= G(gain)[8 * q + e];
+      }
+      put_split(xsp, split_stride(H), m, q, x);
+    }
+    const int i0 = base + (tid() & ~63);
+    if (i0 < total) {
+      s2 = wave_sum63(s2);
+      if ((tid() & 63) == 63) sqc[i0 >> 6] = s2;
+    }
   }
   __syncthreads();
 }
@@ -1133,17 +1149,8 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   float* sqc = c.work + MR * (H + 4);                   // [MR][H/8]
   float* red = sqc + MR * (H >> 3);                     // [kWaves][1][256]
   float* out = red + kWaves * 256;                      // [nrows][MR]
-  float* xs = out + mt.ntiles * 16 * MR;                // [MR][H] fp32 gathered rows (layer 0)
   if (l == 0) {
-    gather_rows<bf16_t, MR>(c, xs);
-    // keep this workgroup's residual columns
-    const int o0 = blockIdx.x * c.cpw;
-    for (int i = tid(); i < kMaxRows * c.cpw; i += kThreads) {
-      const int m = i / c.cpw, j = i % c.cpw;
-      c.xown[i] = (m < MR && o0 + j < H) ? xs[m * H + o0 + j] : 0.f;
-    }
-    __syncthreads();
-    split_rows(xs, xsp, H, R, gain, sqc);
+    gather_split_rows<MR>(c, xsp, gain, sqc);
   } else {
     if (nrows == 0) return true;
     if (!stage_split<2, true>(c, p->xb, H, R, kParDown, gain, xsp, sqc)) return false;
