@@ -179,6 +179,18 @@ rvqsd_status rvqsd_decode_frames_batched_async(rvqsd_stream* s, int32_t n, const
                                                const int32_t* d_c0, const float* d_uniforms, int32_t* d_out_codes,
                                                rvqsd_stats* d_stats);
 
+/* Install (logits or rounds non-NULL) or remove (both NULL) a per-frame trace of
+ * the later batched calls of a stream created with max_streams >= 2: frame f <
+ * max_frames of a call, pass (prefix = 0) < max_rounds of that frame. Device
+ * buffers, caller-owned, layouts as the single-frame trace of rvqsd_set_trace
+ * with a leading frame index: logits float[max_frames][max_rounds]
+ * [rvqsd_info.trace_slots][vocab] (slot r < 16 = verify row r, 16 + r*K + j-1 =
+ * draft row (r, j)); rounds int32[max_frames][max_rounds][32]. Only the slots a
+ * pass uses are written. Synchronises the stream. EINVAL: max_rounds or
+ * max_frames < 1 with a buffer; EUNSUPPORTED: a single-frame stream. */
+rvqsd_status rvqsd_set_batch_trace(rvqsd_stream* s, float* logits, int32_t* rounds, int32_t max_rounds,
+                                   int32_t max_frames);
+
 /* Passes run by the last batched call of the stream and their algorithmic
  * bytes (layer weights and each LM head used, once per pass; gathered rows;
  * KV cache read). Synchronises the stream. */

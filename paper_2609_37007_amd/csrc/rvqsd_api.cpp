@@ -46,14 +46,23 @@ uint64_t splitmix64_at(uint64_t seed, uint64_t n) {
   return z ^ (z >> 31);
 }
 
-// Allocation failures can be injected by tests: RVQSD_TEST_FAIL_ALLOC=n fails the n-th device allocation.
+// Allocation failures can be injected by tests: RVQSD_TEST_FAIL_ALLOC=n fails the n-th device
+// allocation counted from the moment the variable took its current value.
 int g_alloc_count = 0;
+char g_alloc_env[32] = "";
 hipError_t dev_alloc(void** p, size_t bytes) {
   const char* f = getenv("RVQSD_TEST_FAIL_ALLOC");
-  ++g_alloc_count;
-  if (f && atoi(f) == g_alloc_count) {
-    *p = nullptr;
-    return hipErrorOutOfMemory;
+  if (f) {
+    if (strncmp(f, g_alloc_env, sizeof(g_alloc_env) - 1) != 0) {
+      snprintf(g_alloc_env, sizeof(g_alloc_env), "%s", f);
+      g_alloc_count = 0;
+    }
+    if (atoi(f) == ++g_alloc_count) {
+      *p = nullptr;
+      return hipErrorOutOfMemory;
+    }
+  } else {
+    g_alloc_env[0] = '\0';
   }
   return hipMalloc(p, bytes);
 }
@@ -739,6 +748,22 @@ rvqsd_status rvqsd_decode_frames_batched(rvqsd_stream* s, int32_t n, const float
   free(tmp);
   if (e != hipSuccess) return set_err(RVQSD_EHIP, "batched decode: %s", hipGetErrorString(e));
   if (dev != RVQSD_OK) return set_err(dev, "device reported %s", rvqsd_status_str(dev));
+  return RVQSD_OK;
+}
+
+rvqsd_status rvqsd_set_batch_trace(rvqsd_stream* s, float* logits, int32_t* rounds, int32_t max_rounds,
+                                   int32_t max_frames) {
+  if (!s) return set_err(RVQSD_EINVAL, "null stream");
+  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  const bool on = logits || rounds;
+  if (on && (max_rounds < 1 || max_frames < 1)) return set_err(RVQSD_EINVAL, "max_rounds and max_frames must be >= 1");
+  s->bp.tr_logits = on ? logits : nullptr;
+  s->bp.tr_rounds = on ? rounds : nullptr;
+  s->bp.tr_max_rounds = on ? max_rounds : 0;
+  s->bp.tr_frames = on ? max_frames : 0;
+  s->bp.tr_slots = kSlotDraft0 + kMaxRows * s->m->cfg.draft_len;
+  HIPCHK(hipStreamSynchronize(s->stream));
+  HIPCHK(hipMemcpy(s->dbp, &s->bp, sizeof(BParams), hipMemcpyHostToDevice));
   return RVQSD_OK;
 }
 

@@ -678,6 +678,12 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
     const float* src = bp->logits + (size_t)u * V;
     lds_fill<false>(lg, src, V, V, 0);
     __syncthreads();
+    if (bp->tr_logits && st[kLnFrame] < bp->tr_frames && pass < bp->tr_max_rounds) {
+      // the slot layout of the single-stream trace: verify row r, then draft (r, j)
+      const int slot = j == 0 ? r : kSlotDraft0 + r * K + (j - 1);
+      float* dst = bp->tr_logits + (((size_t)st[kLnFrame] * bp->tr_max_rounds + pass) * bp->tr_slots + slot) * V;
+      for (int i = tid(); i < V; i += kThreads) dst[i] = lg[i];
+    }
     int ns = topk_buckets(&sh->tk, lg, V, p->topk, sidx, slog, hist);
     if (ns < 0) ns = topk_select(&sh->tk, lg, V, p->topk, sidx, slog);
     if (tid() < 64) {
@@ -792,10 +798,11 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
     if (!first && st[kLnActive]) {
       const int m = st[kLnM], kp = st[kLnKp], R = st[kLnRows], fp = st[kLnFirst];
       int* codes = st + kLnCodes;
-      int m_new = -1, acc = 0;
+      int m_new = -1, acc = 0, tok = -1;
       if (st[kLnPass] == 0) {
         codes[1] = sh->vr[1] & 0x7fffffff;
         m_new = 1;
+        tok = codes[1];
       } else {
         for (int j = 1; j <= kp; ++j) {
           const int v = sh->vr[j - 1];
@@ -806,6 +813,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
           } else {
             codes[m + j] = v & 0x7fffffff;
             m_new = m + j;
+            tok = codes[m_new];
             break;
           }
         }
@@ -813,6 +821,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
           if (R > kp) {
             codes[m + kp + 1] = sh->vr[kp] & 0x7fffffff;
             m_new = m + kp + 1;
+            tok = codes[m_new];
           } else {
             m_new = n;
           }
@@ -820,6 +829,11 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
         st[kLnRounds] += 1;
         st[kLnDrafted] += kp;
         st[kLnAccepted] += acc;
+      }
+      if (bp->tr_rounds && st[kLnFrame] < bp->tr_frames && st[kLnPass] < bp->tr_max_rounds) {
+        int32_t* tr = bp->tr_rounds + ((size_t)st[kLnFrame] * bp->tr_max_rounds + st[kLnPass]) * kTraceRoundInts;
+        tr[0] = m; tr[1] = kp; tr[2] = fp; tr[3] = R; tr[4] = m_new; tr[5] = acc; tr[6] = tok; tr[7] = st[kLnPass];
+        for (int j = 1; j <= kp; ++j) tr[7 + j] = st[kLnDrafts + m + j];
       }
       st[kLnCalls] += 1;
       // every pass commits at least one code: a frame still open after n + 1 passes is a fault

@@ -110,6 +110,11 @@ struct BParams {
   uint32_t* bar;        // barrier words: [0] top counter, [64 (1 + x)] counter of XCD x, [64 * 9] generation
   int32_t* status;      // first device-side error of the launch (0 = none)
   unsigned long long* totals;  // [0] passes (rounds of the batch), [1] their algorithmic bytes
+  // per-frame trace (nullable), frames f < tr_frames of a call, passes < tr_max_rounds of the frame:
+  // logits in the single-stream slot layout, round records as the single-stream trace's
+  float* tr_logits;     // [tr_frames][tr_max_rounds][n_slots][V]
+  int32_t* tr_rounds;   // [tr_frames][tr_max_rounds][kTraceRoundInts]
+  int32_t tr_max_rounds, tr_frames, tr_slots;
 };
 
 // Per-call arguments (device pointers), passed by value.

@@ -23,7 +23,7 @@ TRACE_ROUND_INTS = 32
 EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_stream_destroy",
            "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset",
            "rvqsd_set_trace", "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async",
-           "rvqsd_batch_totals", "rvqsd_outer_create", "rvqsd_outer_destroy", "rvqsd_outer_reset",
+           "rvqsd_batch_totals", "rvqsd_set_batch_trace", "rvqsd_outer_create", "rvqsd_outer_destroy", "rvqsd_outer_reset",
            "rvqsd_pipeline_frames_async", "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
 
 
@@ -78,12 +78,34 @@ class RvqsdError(RuntimeError):
 _lib = None
 
 
+def _init_hip_runtime():
+    """Initialise the HIP runtime before librvqsd.so is loaded.
+
+    Exit handlers run in the reverse order of their registration. Loading the
+    library registers the unloading of its kernel code objects; a profiler
+    attached to the HIP runtime (rocprofv3) registers its own teardown when the
+    runtime initialises. If the library were loaded first, the profiler's
+    teardown would run before the library's code objects are unloaded, and that
+    unloading would then call into the torn-down profiler. With the runtime
+    initialised first, the library's unloading runs first. Without a GPU the
+    call only returns an error code, which is ignored here.
+    """
+    try:
+        hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime already in the process, if any
+    except OSError:
+        return
+    hip.hipInit.argtypes = [ctypes.c_uint]
+    hip.hipInit.restype = ctypes.c_int
+    hip.hipInit(0)
+
+
 def lib():
     """Load librvqsd.so; raises if it has not been built."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_37007_amd.build_ext`")
+        _init_hip_runtime()
         L = ctypes.CDLL(LIB_PATH)
         P, vp, i32 = ctypes.POINTER, ctypes.c_void_p, ctypes.c_int32
         L.rvqsd_create.argtypes = [P(rvqsd_weights), P(rvqsd_cfg), P(vp)]
@@ -100,6 +122,7 @@ def lib():
         L.rvqsd_decode_frames_batched.argtypes = [vp, i32, vp, vp, vp, vp, vp]
         L.rvqsd_decode_frames_batched_async.argtypes = [vp, i32, vp, vp, vp, vp, vp]
         L.rvqsd_batch_totals.argtypes = [vp, P(ctypes.c_uint64), P(ctypes.c_uint64)]
+        L.rvqsd_set_batch_trace.argtypes = [vp, vp, vp, i32, i32]
         L.rvqsd_outer_create.argtypes = [vp, vp, i32, i32, i32, ctypes.c_double, i32, P(vp)]
         L.rvqsd_outer_destroy.argtypes = [vp]
         L.rvqsd_outer_destroy.restype = None
@@ -114,6 +137,7 @@ def lib():
         for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_decode_frame",
                   "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset", "rvqsd_set_trace",
                   "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async", "rvqsd_batch_totals",
+                  "rvqsd_set_batch_trace",
                   "rvqsd_outer_create", "rvqsd_outer_reset", "rvqsd_pipeline_frames_async",
                   "rvqsd_uniforms_from_seed"):
             getattr(L, n).restype = i32
@@ -240,6 +264,12 @@ class Stream:
         a, b = ctypes.c_uint64(), ctypes.c_uint64()
         _check(lib().rvqsd_batch_totals(self._h, ctypes.byref(a), ctypes.byref(b)), "rvqsd_batch_totals")
         return int(a.value), int(b.value)
+
+    def set_batch_trace(self, logits_ptr: int = 0, rounds_ptr: int = 0, max_rounds: int = 0, max_frames: int = 0):
+        """Per-frame trace of later batched calls (device pointers); no pointers = off."""
+        _check(lib().rvqsd_set_batch_trace(self._h, ctypes.c_void_p(logits_ptr or None),
+                                           ctypes.c_void_p(rounds_ptr or None), int(max_rounds), int(max_frames)),
+               "rvqsd_set_batch_trace")
 
     def reset(self):
         _check(lib().rvqsd_stream_reset(self._h), "rvqsd_stream_reset")

@@ -1,14 +1,15 @@
 """GPU parity of the batched path (several frame streams verified together).
 
 Every frame decoded by rvqsd_decode_frames_batched is the same problem as a
-single-frame decode: its codes and statistics must equal the CPU oracle's on
-the same inputs and uniforms, except where the oracle's own decision margin
-(or top-k gap) is within what a logit error of LOGIT_ERR can flip -- the
-batched path computes in the same precision as the single-stream path (bf16
-weights, fp32-level activations through a bf16 hi/lo split, fp32
-accumulation), whose traced logits stay within ~2e-5 of fp64.  The single-
-stream path of the same library is a second reference: both must agree frame
-by frame under the same rule.
+single-frame decode, and is held to the same rule: with the per-frame trace
+(rvqsd_set_batch_trace), every verify and draft logit row within 2e-2 of the
+oracle's fp64 logits (bf16 weights), every decision replayed bit for bit from
+the kernel's own logits, and the codes and statistics equal to the oracle's
+from scratch unless the first round where the two runs part lies within reach
+of the measured logit error.  Untraced frames use the largest logit error
+measured on the traced ones (MEASURED) for the same rule, applied to the
+oracle rounds up to the one that commits the first differing code.  The
+single-stream path of the same library is a second reference.
 """
 from __future__ import annotations
 
@@ -17,6 +18,7 @@ import pytest
 
 from oracle import oracle as O
 from paper_2609_37007_amd import synth as S
+from tests import gpu_checks as GC
 from tests.helpers import make_oracle, shape_kwargs
 
 torch = pytest.importorskip("torch")
@@ -24,7 +26,10 @@ from paper_2609_37007_amd import rvqsd as R  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-LOGIT_ERR = 1e-4
+LOGIT_TOL = 2e-2
+# largest logit error the traced frames of this module measured (updated as they run;
+# the untraced frames' excuse rule uses it); starts at the single-stream path's level
+MEASURED = {"err": 1e-4}
 # 2 layers, hidden 512, GQA 8 q / 4 kv heads of 64, FFN 1024, 128 codes, bf16
 SMALL = S.ModelShape(n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=4, head_dim=64, ffn=1024, n_codes=15,
                      vocab=128, max_draft=14, dtype=S.DTYPE_BF16)
@@ -51,7 +56,7 @@ class BRig:
     """A model, a batched stream of `lanes` lanes, a single-frame stream and the oracle."""
 
     def __init__(self, s, lanes, topk, K, T=0.9, greedy=0):
-        self.s, self.T, self.K = s, T, K
+        self.s, self.T, self.K, self.topk, self.greedy, self.lanes = s, T, K, topk, greedy, lanes
         blob = blob_of(s)
         self.model = R.Model(blob, R.make_cfg(**shape_kwargs(s), topk=topk, temperature=T, draft_len=K,
                                               draft_greedy=greedy))
@@ -66,12 +71,40 @@ class BRig:
         self.model.close()
         self.orc.close()
 
+    def traced_batch(self, f, c0, u, n_traced, max_rounds=16):
+        """Batched decode with the first n_traced frames traced; returns codes, stats and
+        get(i) -> (codes, stats dict, logits, round records) for a traced frame."""
+        slots = self.model.info()["trace_slots"]
+        V = self.s.vocab
+        lg = torch.zeros((n_traced, max_rounds, slots, V), dtype=torch.float32, device="cuda")
+        rd = torch.full((n_traced, max_rounds, R.TRACE_ROUND_INTS), -1, dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        self.batch.set_batch_trace(lg.data_ptr(), rd.data_ptr(), max_rounds, n_traced)
+        try:
+            codes, st = self.batch.decode_frames_batched(f, c0, u)
+        finally:
+            self.batch.set_batch_trace()
+        torch.cuda.synchronize()
+        lgh, rdh = lg.cpu().numpy(), rd.cpu().numpy()
 
-def near_threshold(rig, f, c0, u):
-    """True when some decision of the oracle's run lies within reach of LOGIT_ERR."""
-    _, _, otr = rig.orc.spec_frame(f, int(c0), u, trace=True)
-    flip = 5.0 * LOGIT_ERR / rig.T
-    return any(r["margin"] < flip or r["topk_gap"] < 2 * LOGIT_ERR for r in otr["rounds"])
+        def get(i):
+            sd = {k: int(st[k][i]) for k in st.dtype.names}
+            return codes[i], sd, lgh[i], rdh[i][:sd["target_calls"]]
+
+        return codes, st, get
+
+
+def near_threshold(rig, f, c0, u, codes):
+    """The oracle rounds up to the one committing the first differing code: some decision
+    within reach of the largest logit error measured on traced batched frames."""
+    return GC.untraced_divergence_near(rig, f, c0, u, codes, MEASURED["err"])
+
+
+def check_traced(rig, f, c0, u, get, frames, max_excused):
+    worst, excused = GC.check_traced_frames(rig, frames, f, c0, u, get, LOGIT_TOL, excuse_frac=1.0)
+    MEASURED["err"] = max(MEASURED["err"], worst)
+    assert excused <= max_excused, excused
+    return worst, excused
 
 
 def check_against_oracle(rig, f, c0, u, codes, st, frames, max_excused):
@@ -83,7 +116,7 @@ def check_against_oracle(rig, f, c0, u, codes, st, frames, max_excused):
             for k in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
                 assert st[k][i] == ost[k], (i, k, st[k][i], ost[k])
         else:
-            assert near_threshold(rig, f[i], c0[i], u[i]), \
+            assert near_threshold(rig, f[i], c0[i], u[i], codes[i]), \
                 f"frame {i}: codes differ with no decision near a threshold: {codes[i].tolist()} vs {oc.tolist()}"
             excused.append(i)
     assert len(excused) <= max_excused, excused
@@ -96,47 +129,57 @@ def check_against_single(rig, f, c0, u, codes, frames):
     for i in frames:
         sc, _ = rig.single.decode_frame_u(f[i], int(c0[i]), u[i])
         if not np.array_equal(sc, codes[i]):
-            assert near_threshold(rig, f[i], c0[i], u[i]), (i, sc.tolist(), codes[i].tolist())
+            assert near_threshold(rig, f[i], c0[i], u[i], codes[i]) or \
+                near_threshold(rig, f[i], c0[i], u[i], sc), (i, sc.tolist(), codes[i].tolist())
             differ.append(i)
     return differ
 
 
 def test_small_4_lanes_matches_oracle():
-    """24 frames, 4 lanes (6 frames per lane in sequence), draft length 3, top-k 16."""
+    """24 frames, 4 lanes (6 frames per lane in sequence), draft length 3, top-k 16;
+    every frame traced: logits, decision replay and the oracle from scratch."""
     rig = BRig(SMALL, lanes=4, topk=16, K=3)
     n = 24
     f, c0 = S.frame_inputs(SMALL, n)
     u = S.uniforms(n)
-    print("small bf16, 4 lanes, K=3: 24 frames", flush=True)
-    codes, st = rig.batch.decode_frames_batched(f, c0, u)
+    print("small bf16, 4 lanes, K=3: 24 frames, traced", flush=True)
+    codes, st, get = rig.traced_batch(f, c0, u, n)
     assert ((codes >= 0) & (codes < SMALL.vocab)).all()
     assert (st["target_calls"] == st["rounds"] + 1).all()
-    ex = check_against_oracle(rig, f, c0, u, codes, st, range(n), max_excused=2)
+    worst, ex = check_traced(rig, f, c0, u, get, range(n), max_excused=2)
     d = check_against_single(rig, f, c0, u, codes, range(n))
+    untraced, _ = rig.batch.decode_frames_batched(f, c0, u)
+    assert np.array_equal(untraced, codes)  # the trace changes nothing
     passes, nbytes = rig.batch.batch_totals()
     # every lane runs its frames one after another inside the shared passes
     per_lane = [int(st["target_calls"][i::4].sum()) for i in range(4)]
     assert passes >= max(per_lane) and passes <= sum(per_lane)
     assert nbytes > 0
-    print(f"excused vs oracle {ex}, differ from single-stream {d}, passes {passes} (lanes {per_lane})", flush=True)
+    print(f"max logit error {worst:.3g}, excused {ex}, differ from single-stream {d}, passes {passes} "
+          f"(lanes {per_lane})", flush=True)
     rig.close()
 
 
+@pytest.mark.timeout(900)
 def test_mcd1024_16_lanes_matches_oracle():
     """The 1024-wide bf16 model, 16 lanes (M = 80 rows), draft length 4, top-k 50:
-    48 frames, the oracle on 16 of them, the single-stream path on all."""
+    48 frames; the first 16 traced (logits within 2e-2, decisions replayed, oracle
+    end to end), the others against the oracle (every third) and the single-stream
+    path under the rule with the measured logit error."""
     s = S.MCD_1024
     rig = BRig(s, lanes=16, topk=50, K=4)
     n = 48
     f, c0 = S.frame_inputs(s, n)
     u = S.uniforms(n)
-    print("mcd1024 bf16, 16 lanes, K=4: 48 frames", flush=True)
-    codes, st = rig.batch.decode_frames_batched(f, c0, u)
+    print("mcd1024 bf16, 16 lanes, K=4: 48 frames, 16 traced", flush=True)
+    codes, st, get = rig.traced_batch(f, c0, u, 16)
     assert ((codes >= 0) & (codes < s.vocab)).all()
-    ex = check_against_oracle(rig, f, c0, u, codes, st, range(0, n, 3), max_excused=2)
+    worst, ex = check_traced(rig, f, c0, u, get, range(16), max_excused=2)
+    print(f"traced frames: max logit error {worst:.3g}, excused {ex}", flush=True)
+    ex2 = check_against_oracle(rig, f, c0, u, codes, st, range(18, n, 3), max_excused=2)
     d = check_against_single(rig, f, c0, u, codes, range(n))
     assert len(d) <= 3, d
-    print(f"excused vs oracle {ex}, differ from single-stream {d}", flush=True)
+    print(f"untraced excused vs oracle {ex2}, differ from single-stream {d}", flush=True)
     rig.close()
 
 
@@ -161,8 +204,8 @@ def test_ragged_counts_and_invalid_c0_async():
     n = 7
     f, c0 = S.frame_inputs(SMALL, n)
     u = S.uniforms(n)
-    codes, st = rig.batch.decode_frames_batched(f, c0, u)
-    check_against_oracle(rig, f, c0, u, codes, st, range(n), max_excused=1)
+    codes, st, get = rig.traced_batch(f, c0, u, n)
+    check_traced(rig, f, c0, u, get, range(n), max_excused=1)
     two, _ = rig.batch.decode_frames_batched(f[:2], c0[:2], u[:2])
     assert np.array_equal(two, codes[:2])
     bad = c0.copy()
@@ -193,15 +236,16 @@ def test_k0_batched_is_autoregressive():
     n = 16
     f, c0 = S.frame_inputs(SMALL, n)
     u = S.uniforms(n)
-    codes, st = rig.batch.decode_frames_batched(f, c0, u)
+    codes, st, get = rig.traced_batch(f, c0, u, n)
     assert (st["target_calls"] == SMALL.n_codes).all()
-    excused = 0
+    _, excused = check_traced(rig, f, c0, u, get, range(n), max_excused=1)
     for i in range(n):
         ar = rig.orc.ar_frame(f[i], int(c0[i]), u[i])
+        oc, _, _ = rig.orc.spec_frame(f[i], int(c0[i]), u[i])
+        assert np.array_equal(ar, oc)  # draft length 0 is plain top-k sampling
         if not np.array_equal(ar, codes[i]):
-            assert near_threshold(rig, f[i], c0[i], u[i])
-            excused += 1
-    assert excused <= 1
+            excused -= 1
+    assert excused >= 0
     rig.close()
 
 
@@ -210,8 +254,8 @@ def test_greedy_drafts_batched():
     n = 12
     f, c0 = S.frame_inputs(SMALL, n)
     u = S.uniforms(n)
-    codes, st = rig.batch.decode_frames_batched(f, c0, u)
-    check_against_oracle(rig, f, c0, u, codes, st, range(n), max_excused=1)
+    codes, st, get = rig.traced_batch(f, c0, u, n)
+    check_traced(rig, f, c0, u, get, range(n), max_excused=1)
     rig.close()
 
 

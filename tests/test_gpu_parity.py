@@ -26,6 +26,7 @@ import pytest
 
 from oracle import oracle as O
 from paper_2609_37007_amd import synth as S
+from tests import gpu_checks as GC
 from tests.helpers import make_oracle, shape_kwargs
 
 torch = pytest.importorskip("torch")
@@ -34,8 +35,6 @@ from paper_2609_37007_amd import rvqsd as R  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = {S.DTYPE_F32: 1e-4, S.DTYPE_BF16: 2e-2}
-SLOT_DRAFT0 = 16
-CDF_EXCUSE = 1e-6
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -47,8 +46,22 @@ def _gpu():
 
 
 @functools.lru_cache(maxsize=4)
-def blob_of(s: S.ModelShape, head_scale: float = 1.0) -> bytes:
-    return S.make_weights(s, seed=0, head_scale=head_scale)
+def blob_of(s: S.ModelShape, head_scale: float = 1.0, tied_rows_from: int = -1) -> bytes:
+    """Seed-0 weights; tied_rows_from >= 0 zeroes every LM-head row from that index on,
+    so that all their logits tie at exactly 0."""
+    blob = S.make_weights(s, seed=0, head_scale=head_scale)
+    if tied_rows_from < 0:
+        return blob
+    b = bytearray(blob)
+    wb = 4 if s.dtype == S.DTYPE_F32 else 2
+    off = S.HEADER_BYTES
+    for name, shp, kind in S.tensor_list(s):
+        nb = int(np.prod(shp)) * (wb if kind == "mat" else 4)
+        if name.startswith("lmh"):
+            row = s.hidden * wb
+            b[off + tied_rows_from * row:off + nb] = bytes(nb - tied_rows_from * row)
+        off += nb
+    return bytes(b)
 
 
 def shape_with(base: S.ModelShape, **kw) -> S.ModelShape:
@@ -60,9 +73,9 @@ def shape_with(base: S.ModelShape, **kw) -> S.ModelShape:
 class Rig:
     """A GPU model + stream and an oracle with the same configuration."""
 
-    def __init__(self, s, topk, K, T=0.9, greedy=0, head_scale=1.0, hip_stream=None):
+    def __init__(self, s, topk, K, T=0.9, greedy=0, head_scale=1.0, hip_stream=None, tied_rows_from=-1):
         self.s, self.topk, self.K, self.T, self.greedy = s, topk, K, T, greedy
-        blob = blob_of(s, head_scale)
+        blob = blob_of(s, head_scale, tied_rows_from)
         self.model = R.Model(blob, R.make_cfg(**shape_kwargs(s), topk=topk, temperature=T, draft_len=K,
                                               draft_greedy=greedy))
         self.stream = R.Stream(self.model, hip_stream=hip_stream)
@@ -89,160 +102,10 @@ class Rig:
         return codes, st, lg.cpu().numpy(), rd.cpu().numpy()[:st["target_calls"]]
 
 
-# ------------------------------------------------------------------ trace logic
-
-def pass_rows(K, n, row):
-    """Verify rows and (row, j) draft slots the kernel computes in one pass."""
-    fp, R_, ps = int(row[2]), int(row[3]), int(row[7])
-    verify = [r for r in range(R_) if (ps > 0 or r == 1) and fp + r >= 1]
-    drafts = []
-    for r in range(R_):
-        s = fp + r
-        if s < 1 or s > n - 1 or (ps == 0 and r != 1):
-            continue
-        drafts += [(r, j) for j in range(1, min(K, n - s) + 1)]
-    return verify, drafts
-
-
-def pass_inputs(codes_full, row):
-    """Codes consumed by positions 1 .. first_pos+rows-1 of a traced pass:
-    committed codes up to the anchor m, then the round's drafts."""
-    m, fp, R_ = int(row[0]), int(row[2]), int(row[3])
-    ic = []
-    for s in range(1, fp + R_):
-        x = s - 1
-        ic.append(int(codes_full[x]) if x <= m else int(row[8 + (x - m - 1)]))
-    return ic
-
-
-def logit_error(rig, f, c0, codes, lg, rd):
-    """Max-abs difference of every traced logit row from the oracle's fp64 logits."""
-    K, n = rig.K, rig.s.n_codes
-    codes_full = [int(c0)] + [int(c) for c in codes]
-    worst = 0.0
-    for i, row in enumerate(rd):
-        h = rig.orc.forward(f, pass_inputs(codes_full, row))
-        fp = int(row[2])
-        verify, drafts = pass_rows(K, n, row)
-        for r in verify:
-            ref = rig.orc.logits(h[fp + r], fp + r, 0)
-            worst = max(worst, float(np.abs(lg[i, r].astype(np.float64) - ref).max()))
-        for r, j in drafts:
-            ref = rig.orc.logits(h[fp + r], fp + r + j, j)
-            worst = max(worst, float(np.abs(lg[i, SLOT_DRAFT0 + r * K + j - 1].astype(np.float64) - ref).max()))
-    return worst
-
-
-def cdf_margin(prob, u):
-    """Distance of u from the nearest step of the normalised ascending-index CDF."""
-    c = np.cumsum(prob) / prob.sum()
-    return float(np.min(np.abs(c - u)))
-
-
-def residual_probs(pi, pp, qi, qp):
-    q = dict(zip((int(x) for x in qi), (float(x) for x in qp)))
-    r = np.array([max(0.0, float(p) - q.get(int(i), 0.0)) for i, p in zip(pi, pp)])
-    return r if r.sum() > 0 else np.asarray(pp, dtype=np.float64)
-
-
-class _Excused(Exception):
-    pass
-
-
-def replay(rig, lg, rd, u, codes):
-    """Re-take every decision of the frame from the kernel's own logits with the
-    oracle's primitives.  Returns 1 when the frame diverged at a decision whose
-    threshold lies within 1e-6 of its uniform (summation-order rounding), else 0."""
-    K, n, topk, T = rig.K, rig.s.n_codes, rig.topk, rig.T
-
-    def check(gpu, mine, margin, what):
-        if gpu == mine:
-            return
-        assert margin < CDF_EXCUSE, f"{what}: kernel {gpu}, oracle primitives {mine}, margin {margin:.3g}"
-        raise _Excused
-
-    mine = {}
-    try:
-        for i, row in enumerate(rd):
-            m, kp, fp, R_, m_new, acc, tok = (int(x) for x in row[:7])
-            if i == 0:
-                pi, pp = O.topk_softmax(lg[0, 1], topk, T)
-                us = float(u[0, 2])
-                check(tok, O.sample(pi, pp, us), cdf_margin(pp, us), "prefix sample")
-                assert m_new == 1
-                mine[1] = tok
-                continue
-            arow = m - int(rd[i - 1][2])
-            n_acc, my_new = 0, None
-            for j in range(1, kp + 1):
-                ud, ua, us = (float(x) for x in u[m + j - 1])
-                qi, qp = O.topk_softmax(lg[i - 1, SLOT_DRAFT0 + arow * K + j - 1], topk, T)
-                d = int(row[8 + j - 1])
-                if rig.greedy:
-                    check(d, int(qi[int(np.argmax(qp))]), 0.0, f"greedy draft {m + j}")
-                    qi, qp = np.array([d], dtype=np.int32), np.array([1.0])
-                else:
-                    check(d, O.sample(qi, qp, ud), cdf_margin(qp, ud), f"draft {m + j}")
-                pi, pp = O.topk_softmax(lg[i, j - 1], topk, T)
-                ok, t = O.accept_or_resample(pi, pp, qi, qp, d, ua, us)
-                pd = dict(zip(pi.tolist(), pp.tolist())).get(d, 0.0)
-                qd = dict(zip(qi.tolist(), qp.tolist())).get(d, 0.0)
-                gpu_ok = j <= acc
-                check(gpu_ok, ok, abs(ua - pd / qd) if qd > 0 else 1.0, f"accept {m + j}")
-                if not ok:
-                    check(tok, t, cdf_margin(residual_probs(pi, pp, qi, qp), us), f"residual {m + j}")
-                    my_new = m + j
-                    break
-                mine[m + j] = d
-                n_acc += 1
-            if my_new is None:
-                if m + kp < n:
-                    pi, pp = O.topk_softmax(lg[i, kp], topk, T)
-                    us = float(u[m + kp, 2])
-                    check(tok, O.sample(pi, pp, us), cdf_margin(pp, us), f"bonus {m + kp + 1}")
-                    my_new = m + kp + 1
-                else:
-                    my_new = n
-            assert (m_new, acc) == (my_new, n_acc), (i, row[:8].tolist(), my_new, n_acc)
-            if my_new > m + n_acc:
-                mine[my_new] = tok
-    except _Excused:
-        return 1
-    assert sorted(mine) == list(range(1, n + 1))
-    assert [mine[s] for s in range(1, n + 1)] == [int(c) for c in codes]
-    return 0
-
-
-def compare_end_to_end(rig, f, c0, u, codes, stats, logit_err):
-    """True when the oracle from scratch gives the same frame; False when the
-    first differing round is within reach of the measured logit error."""
-    oc, ost, otr = rig.orc.spec_frame(f, int(c0), u, trace=True)
-    if np.array_equal(oc, codes):
-        for k in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
-            assert stats[k] == ost[k], (k, stats[k], ost[k])
-        return True
-    # the kernel committed a different sequence: excusable only near a threshold
-    flip = 5.0 * max(logit_err, 1e-7) / rig.T
-    near = [r for r in otr["rounds"] if r["margin"] < flip or r["topk_gap"] < 2 * max(logit_err, 1e-7)]
-    assert near, f"codes differ with no decision near a threshold: gpu {codes.tolist()} oracle {oc.tolist()}"
-    return False
-
-
 def check_frames(rig, frames, f, c0, u, excuse_frac=0.1):
     tol = LOGIT_TOL[rig.s.dtype]
-    excused = 0
-    worst = 0.0
-    for i in frames:
-        codes, st, lg, rd = rig.traced(f[i], c0[i], u[i])
-        assert st["status"] == 0
-        err = logit_error(rig, f[i], c0[i], codes, lg, rd)
-        worst = max(worst, err)
-        assert err <= tol, f"frame {i}: logit max-abs {err:.3g} > {tol}"
-        ex = replay(rig, lg, rd, u[i], codes)
-        if not compare_end_to_end(rig, f[i], c0[i], u[i], codes, st, err) or ex:
-            excused += 1
-    assert excused <= max(1, int(excuse_frac * len(frames))), excused
-    return worst, excused
+    return GC.check_traced_frames(rig, frames, f, c0, u, lambda i: rig.traced(f[i], c0[i], u[i]), tol,
+                                  excuse_frac=excuse_frac)
 
 
 # ------------------------------------------------------------------ tests
@@ -272,16 +135,18 @@ def test_mcd1024_bf16_sampled_frames():
     rig.close()
 
 
+@pytest.mark.timeout(600)
 def test_mcd1024_async_launch_matches_oracle():
     """The benchmark's launch configuration: device-resident inputs, one async
-    launch per frame on a torch stream, frames of the 1000-frame workload."""
+    launch per frame on a torch stream, all 1000 frames of the workload; every
+    10th frame (100 frames) against the oracle from scratch."""
     s = S.MCD_1024
     ts = torch.cuda.current_stream()
     rig = Rig(s, topk=50, K=4, hip_stream=ts.cuda_stream)
     N = 1000
     f, c0 = S.frame_inputs(s, N)
     u = S.uniforms(N)
-    pick = [0, 3, 250, 777, 998]
+    pick = list(range(0, N, 10))
     d_f = torch.from_numpy(f).cuda()
     d_c0 = torch.from_numpy(c0).cuda()
     d_u = torch.from_numpy(np.ascontiguousarray(u)).cuda()
@@ -301,22 +166,27 @@ def test_mcd1024_async_launch_matches_oracle():
     # every frame: the committed-code count equals the accounting of its rounds
     assert (st["target_calls"] == st["rounds"] + 1).all()
     assert (st["accepted"] <= st["drafted"]).all()
+    print(f"1000 frames decoded; oracle on {len(pick)} of them", flush=True)
     differ = []
-    for i in pick:
+    for k, i in enumerate(pick):
         oc, ost, _ = rig.orc.spec_frame(f[i], int(c0[i]), u[i])
         if np.array_equal(oc, codes[i]):
-            assert int(st["accept_mask"][i]) == ost["accept_mask"]
+            for key in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
+                assert int(st[key][i]) == ost[key], (i, key)
         else:
             differ.append(i)
+        if k % 25 == 24:
+            print(f"  {k + 1} frames checked", flush=True)
     # a frame that differs from the oracle must come out the same through the traced host
     # path (no dependence on the frames before it) and pass the parity rule: logits within
-    # tolerance, decisions replayed exactly, a difference only at a decision near a threshold
+    # tolerance, decisions replayed exactly, and the first round where the two runs part
+    # within reach of the measured logit error
     for i in differ:
         tcodes, _, _, _ = rig.traced(f[i], int(c0[i]), u[i])
         assert np.array_equal(tcodes, codes[i]), (i, tcodes.tolist(), codes[i].tolist())
     if differ:
         check_frames(rig, differ, f, c0, u, excuse_frac=1.0)
-    assert len(differ) <= 2, differ
+    assert len(differ) <= 5, differ
     print(f"frames differing from the oracle (excused near a threshold): {differ}", flush=True)
     rig.close()
 
@@ -343,23 +213,51 @@ def test_tiny_draft_lengths(K):
     rig.close()
 
 
-@pytest.mark.parametrize("K", [1, 7, 14])
+@pytest.mark.parametrize("K", [0, 1, 2, 3, 5, 7, 14])
 def test_mcd1024_draft_lengths(K):
+    """Every kernel instantiation of the bf16 model: 2 rows (K = 0, 1), 4 (K = 2, 3),
+    5 (K = 4, the sampled-frames test), 8 (K = 5, 7) and 16 rows (K = 14, VALU path)."""
     s = S.MCD_1024
     rig = Rig(s, topk=50, K=K)
+    f, c0 = S.frame_inputs(s, 2)
+    u = S.uniforms(2)
+    print(f"mcd1024 bf16 K={K}: frames 0, 1", flush=True)
+    check_frames(rig, range(2), f, c0, u)
+    if K == 0:
+        # draft length 0 is plain top-k sampling, the baseline of the speedup figures
+        for i in range(2):
+            codes, st = rig.stream.decode_frame_u(f[i], int(c0[i]), u[i])
+            assert st["target_calls"] == s.n_codes and st["drafted"] == 0
+            assert np.array_equal(codes, rig.orc.ar_frame(f[i], int(c0[i]), u[i]))
+    rig.close()
+
+
+@pytest.mark.parametrize("scale", [3.0, 6.0])
+def test_mcd1024_peaked_heads(scale):
+    """LM heads scaled 3x and 6x (the sharper targets of the draft-length sweep)."""
+    s = S.MCD_1024
+    rig = Rig(s, topk=50, K=4, head_scale=scale)
     f, c0 = S.frame_inputs(s, 2)
     u = S.uniforms(2)
     check_frames(rig, range(2), f, c0, u)
     rig.close()
 
 
-def test_mcd1024_peaked_heads():
-    """LM heads scaled 6x (peaked logits, high acceptance)."""
-    s = S.MCD_1024
-    rig = Rig(s, topk=50, K=4, head_scale=6.0)
+@pytest.mark.parametrize("shape,topk,tied_from", [("TINY", 8, 0), ("TINY", 8, 5), ("MCD", 50, 0), ("MCD", 50, 10)])
+def test_tied_logits_reach_the_exact_topk_select(shape, topk, tied_from):
+    """All logits equal (heads of zeros), or 10 distinct rows and every other logit tied at 0:
+    more than 64 values in the boundary bucket of the bucket top-k, so the exact selection
+    runs; ties go to the lower token index on both sides."""
+    s = S.TINY if shape == "TINY" else S.MCD_1024
+    rig = Rig(s, topk=topk, K=3, tied_rows_from=tied_from)
     f, c0 = S.frame_inputs(s, 2)
     u = S.uniforms(2)
     check_frames(rig, range(2), f, c0, u)
+    if tied_from == 0:
+        # p is uniform over tokens 0..topk-1 and every draft is accepted
+        for i in range(2):
+            codes, st = rig.stream.decode_frame_u(f[i], int(c0[i]), u[i])
+            assert (codes < topk).all() and st["accepted"] == st["drafted"]
     rig.close()
 
 
@@ -619,3 +517,38 @@ def test_chi_square_against_autoregressive():
         ps.append(ss.chi2_contingency(tab)[1])
     print("per-position homogeneity p-values:", " ".join(f"{p:.3f}" for p in ps), flush=True)
     assert min(ps) > P_MIN, ps
+
+
+def test_injected_allocation_failures_leave_the_library_usable(monkeypatch):
+    """RVQSD_TEST_FAIL_ALLOC=n fails the n-th device allocation after it is set: the
+    weights (1), a stream's buffers (2), a batched stream's buffers (3). Each call
+    reports ENOMEM and releases what it had taken; afterwards everything works."""
+    s = shape_with(S.MCD_1024, n_layers=1)
+    blob = S.make_weights(s, seed=0)
+    cfg = R.make_cfg(**shape_kwargs(s), topk=50, temperature=0.9, draft_len=3)
+    monkeypatch.setenv("RVQSD_TEST_FAIL_ALLOC", "1")
+    with pytest.raises(R.RvqsdError) as e:
+        R.Model(blob, cfg)
+    assert e.value.status == R.ENOMEM
+    monkeypatch.setenv("RVQSD_TEST_FAIL_ALLOC", "2")
+    model = R.Model(blob, cfg)
+    with pytest.raises(R.RvqsdError) as e:
+        R.Stream(model)
+    assert e.value.status == R.ENOMEM
+    model.close()
+    monkeypatch.setenv("RVQSD_TEST_FAIL_ALLOC", "3")
+    model = R.Model(blob, cfg)
+    with pytest.raises(R.RvqsdError) as e:
+        R.Stream(model, max_streams=4)
+    assert e.value.status == R.ENOMEM
+    monkeypatch.delenv("RVQSD_TEST_FAIL_ALLOC")
+    stream = R.Stream(model)
+    orc = make_oracle(s, blob, topk=50, temperature=0.9, draft_len=3)
+    f, c0 = S.frame_inputs(s, 1)
+    u = S.uniforms(1)
+    codes, st = stream.decode_frame_u(f[0], int(c0[0]), u[0])
+    rig = type("MiniRig", (), dict(s=s, K=3, topk=50, T=0.9, greedy=0, orc=orc))()
+    assert GC.untraced_divergence_near(rig, f[0], int(c0[0]), u[0], codes, 1e-4)
+    stream.close()
+    model.close()
+    orc.close()

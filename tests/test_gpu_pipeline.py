@@ -16,6 +16,7 @@ import pytest
 
 from oracle import oracle as O
 from paper_2609_37007_amd import synth as S
+from tests import gpu_checks as GC
 from tests.helpers import make_oracle, shape_kwargs
 
 torch = pytest.importorskip("torch")
@@ -24,6 +25,9 @@ from paper_2609_37007_amd import rvqsd as R  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 HIDDEN_TOL = 2e-3
+# inner-loop logit error bound for the excuse rule: the single-stream kernel's traced
+# logits stay within 1e-4 of the oracle's at bf16 (measured ~2e-5)
+INNER_ERR = 1e-4
 INNER_SMALL = S.ModelShape(n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=4, head_dim=64, ffn=1024, n_codes=15,
                            vocab=128, max_draft=14, dtype=S.DTYPE_BF16)
 OUTER_SMALL = S.ModelShape(n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=4, head_dim=64, ffn=1024, n_codes=1,
@@ -54,6 +58,8 @@ class PRig:
         self.emb0 = S.unpack_weights(outer_s, self.oblob)["emb0"]
         self.tab = S.unpack_outer_tables(outer_s, self.tables, inner_s.n_codes, inner_s.vocab)
         self.outer_s, self.inner_s = outer_s, inner_s
+        # the inner loop as a parity rig (gpu_checks)
+        self.inner = type("InnerRig", (), dict(s=inner_s, K=K, topk=topk, T=T, greedy=0, orc=self.iorc))()
 
     def run_gpu(self, t, u_c0, uni):
         n, H = t.shape
@@ -98,8 +104,10 @@ def compare(rig, t, u_c0, uni, codes, st, hs):
             if codes[i][0] != ocodes[i][0]:
                 assert c0_near_threshold(rig, ohs[i], float(u_c0[i])), (i, codes[i][0], ocodes[i][0])
             else:
-                _, _, otr = rig.iorc.spec_frame(ohs[i].astype(np.float32), int(ocodes[i][0]), uni[i], trace=True)
-                assert any(r["margin"] < 5e-4 or r["topk_gap"] < 2e-4 for r in otr["rounds"]), \
+                # same c_0: the inner loop parted; the first differing code must come from an
+                # oracle round within reach of the error (inner logits plus the hidden-state error)
+                assert GC.untraced_divergence_near(rig.inner, ohs[i].astype(np.float32), int(ocodes[i][0]), uni[i],
+                                                   codes[i][1:], INNER_ERR + 10 * err), \
                     (i, codes[i].tolist(), ocodes[i].tolist())
             return i, err
         assert err < HIDDEN_TOL, (i, err)
@@ -153,4 +161,57 @@ def test_full_size_pipeline_first_frames():
     codes, st, hs = rig.run_gpu(t, u_c0, uni)
     matched, _ = compare(rig, t, u_c0, uni, codes, st, hs)
     assert matched >= 1, matched
+    rig.close()
+
+
+@pytest.mark.timeout(900)
+def test_small_pipeline_200_frames_teacher_forced():
+    """200 chained frames, so the outer KV grows to 200 positions and its split-sequence
+    attention takes about 13 keys per chunk (multi-key chunk softmax, a partial last chunk,
+    the merge of 16 chunks). The outer inputs are rebuilt from the GPU's own codes (teacher
+    forcing): one oracle forward over the 200 rows gives every frame's hidden state, which
+    must be within HIDDEN_TOL; every c_0 must be the oracle's draw from it or sit near a
+    CDF step; every inner frame, run by the oracle from the GPU's hidden state and c_0,
+    must match or part first at a decision within reach of the inner logit error."""
+    rig = PRig(OUTER_SMALL, INNER_SMALL, topk=16, K=3, max_frames=256)
+    n = 200
+    t, u_c0 = S.pipeline_inputs(OUTER_SMALL, n)
+    uni = S.uniforms(n)
+    print("small pipeline: 200 frames, teacher forced", flush=True)
+    codes, st, hs = rig.run_gpu(t, u_c0, uni)
+    assert (st["status"] == 0).all()
+    rows = np.zeros((n, OUTER_SMALL.hidden), dtype=np.float64)
+    for i in range(n):
+        x = t[i].astype(np.float64)
+        if i > 0:
+            prev = codes[i - 1]
+            x = x + rig.emb0[prev[0]].astype(np.float64)
+            for j in range(1, 1 + INNER_SMALL.n_codes):
+                x = x + rig.tab[j - 1][prev[j]].astype(np.float64)
+        rows[i] = x
+    href = rig.oorc.forward_vectors(rows)
+    herr = np.abs(hs.astype(np.float64) - href).max(axis=1)
+    print(f"outer hidden max error {herr.max():.3g} (position of the worst: {int(herr.argmax())})", flush=True)
+    assert herr.max() < HIDDEN_TOL
+    c0_excused, inner_excused = [], []
+    for i in range(n):
+        lg = rig.oorc.logits(href[i], 1)
+        lg[INNER_SMALL.vocab:] = -np.inf
+        idx, p = O.topk_softmax(lg, rig.topk, rig.T)
+        c0 = O.sample(idx, p, float(u_c0[i]))
+        if c0 != codes[i][0]:
+            assert c0_near_threshold(rig, href[i], float(u_c0[i])), (i, c0, codes[i][0])
+            c0_excused.append(i)
+        oc, ost, _ = rig.iorc.spec_frame(hs[i], int(codes[i][0]), uni[i])
+        if np.array_equal(oc, codes[i][1:]):
+            for k in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
+                assert st[k][i] == ost[k], (i, k)
+        else:
+            assert GC.untraced_divergence_near(rig.inner, hs[i], int(codes[i][0]), uni[i], codes[i][1:], INNER_ERR), \
+                (i, codes[i].tolist(), oc.tolist())
+            inner_excused.append(i)
+        if i % 50 == 49:
+            print(f"  {i + 1} frames checked", flush=True)
+    print(f"c_0 near a CDF step: {c0_excused}; inner frames excused: {inner_excused}", flush=True)
+    assert len(c0_excused) <= 2 and len(inner_excused) <= 4
     rig.close()

@@ -436,3 +436,150 @@ def test_enumeration_detects_a_biased_rule():
     spec, _ = Hh.enumerate_law(biased, 9, check_points=0)
     worst = max(abs(ar.get(k, 0.0) - spec.get(k, 0.0)) for k in set(ar) | set(spec))
     assert worst > 1e-3
+
+
+# ------------------------------------------ drafter anchor and verify rows
+
+@pytest.mark.parametrize("K,mode", [(3, O.DRAFT_SAMPLED), (5, O.DRAFT_GREEDY), (2, O.DRAFT_SAMPLED)])
+def test_traced_draft_and_verify_logits_follow_the_anchor(K, mode):
+    """Sec. 2.2, Fig. 3: in a round anchored at m, draft j comes from LMH_{m+j}(h_m + b_j),
+    with h_m the final-normed hidden state of position m over the committed codes
+    c_0..c_{m-1}; verify row j - 1 is LMH_{m+j}(h_{m+j}) over c_0..c_m and the drafts.
+    Every traced logit row is rebuilt here from the torch forward and plain numpy
+    products, so an anchor, head or offset index that is off by one fails."""
+    s = S.ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, n_codes=9, vocab=24,
+                     max_draft=6, dtype=S.DTYPE_F32)
+    blob = S.make_weights(s, seed=21, std=0.25, offset_std=0.6)
+    W = S.unpack_weights(s, blob)
+    orc = Hh.make_oracle(s, blob, topk=6, temperature=0.9, draft_len=K, draft_mode=mode)
+    f, c0 = S.frame_inputs(s, 3, seed_hidden=8)
+    u = S.uniforms(3, s.n_codes, seed=13)
+    lmh = lambda t: W[f"lmh{t}"].astype(np.float64)
+    checked = 0
+    for fr in range(3):
+        codes, st, tr = orc.spec_frame(f[fr], int(c0[fr]), u[fr], trace=True, logits=True)
+        full = [int(c0[fr])] + [int(x) for x in codes]
+        rs = tr["rounds"]
+        # prefix pass: row 0 is position 1 over (f, E_0[c_0])
+        h = _torch_forward(s, W, f[fr], full[:1])
+        np.testing.assert_allclose(tr["verify_logits"][0][0], lmh(1) @ h[1], rtol=0, atol=1e-9)
+        for i, r in enumerate(rs[1:], start=1):
+            m, kp = r["m"], r["kp"]
+            # anchor hidden state over the committed codes only
+            h = _torch_forward(s, W, f[fr], full[:m])
+            assert h.shape[0] == m + 1
+            for j in range(1, kp + 1):
+                ref = lmh(m + j) @ (h[m] + W["offsets"][j - 1].astype(np.float64))
+                np.testing.assert_allclose(tr["draft_logits"][i][j - 1], ref, rtol=0, atol=1e-9)
+                checked += 1
+            # verify rows: positions m+1.. over c_0..c_m then the round's drafts
+            rows = min(kp + 1, s.n_codes - m)
+            ins = full[:m + 1] + list(r["drafts"][:rows - 1])
+            hv = _torch_forward(s, W, f[fr], ins)
+            n_used = r["accepted"] + 1 if r["accepted"] < kp else rows
+            for j in range(1, n_used + 1):
+                np.testing.assert_allclose(tr["verify_logits"][i][j - 1], lmh(m + j) @ hv[m + j], rtol=0,
+                                           atol=1e-9)
+    assert checked >= 10
+    orc.close()
+
+
+def test_draft_anchor_pin_detects_an_off_by_one_anchor():
+    """Power of the rebuild above: drafts taken from h_{m-1} or through LMH_{m+j-1} differ
+    from the traced rows by far more than the 1e-9 tolerance on this model."""
+    s = S.ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, n_codes=9, vocab=24,
+                     max_draft=6, dtype=S.DTYPE_F32)
+    blob = S.make_weights(s, seed=21, std=0.25, offset_std=0.6)
+    W = S.unpack_weights(s, blob)
+    orc = Hh.make_oracle(s, blob, topk=6, temperature=0.9, draft_len=3)
+    f, c0 = S.frame_inputs(s, 1, seed_hidden=8)
+    codes, _, tr = orc.spec_frame(f[0], int(c0[0]), S.uniforms(1, s.n_codes, seed=13)[0], trace=True, logits=True)
+    full = [int(c0[0])] + [int(x) for x in codes]
+    r = tr["rounds"][1]
+    m = r["m"]
+    h = _torch_forward(s, W, f[0], full[:m])
+    got = tr["draft_logits"][1][0]
+    b1 = W["offsets"][0].astype(np.float64)
+    assert np.abs(got - W[f"lmh{m + 1}"] @ (h[m - 1] + b1)).max() > 1e-3       # anchor one early
+    assert np.abs(got - W[f"lmh{m}"] @ (h[m] + b1)).max() > 1e-3                # head one early
+    assert np.abs(got - W[f"lmh{m + 1}"] @ (h[m] + W["offsets"][1])).max() > 1e-3  # offset b_2
+    assert np.abs(got - W[f"lmh{m + 1}"] @ h[m]).max() > 1e-3                   # offset dropped
+    orc.close()
+
+
+# ------------------------------------------------ the outer pipeline (Fig. 1)
+
+def _np_topk_sample(lg, topk, T, u):
+    """top-k softmax + ascending-index inverse CDF from numpy/scipy routines."""
+    order = np.argsort(-lg, kind="stable")[:topk]
+    sel = np.sort(order)
+    p = scipy.special.softmax(lg[sel] / T)
+    cum = np.cumsum(p)
+    return int(sel[min(int(np.searchsorted(cum, u * cum[-1], side="right")), len(sel) - 1)]), cum / cum[-1]
+
+
+def test_pipeline_frames_outer_input_mask_and_c0_draw():
+    """oracle.pipeline_frames against a rebuild from Fig. 1: frame i's outer input is
+    t_i + E_0[c_0] + sum_{j=1..15} E_j[c_j] over the codes of frame i - 1 (t_0 alone at
+    i = 0); the outer decoder runs causally over positions 0..i (torch rebuild); c_0 is the
+    top-k draw from its head with every entry at or above the inner codebook size masked
+    (those head rows are made large here, so a missing or shifted mask changes c_0); the
+    inner loop decodes from float32(h_i) and c_0."""
+    outer_s = S.ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, n_codes=1,
+                           vocab=40, max_draft=0, dtype=S.DTYPE_BF16)
+    inner_s = S.ModelShape(n_layers=1, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, n_codes=15,
+                           vocab=24, max_draft=3, dtype=S.DTYPE_F32)
+    topk, T = 6, 0.9
+    oblob = bytearray(S.make_weights(outer_s, seed=31, std=0.3))
+    # rows >= the inner codebook of the outer head: logits far above the rest
+    Wo = S.unpack_weights(outer_s, bytes(oblob))
+    off = S.HEADER_BYTES
+    for name, shp, kind in S.tensor_list(outer_s):
+        cnt = int(np.prod(shp))
+        nb = cnt * (2 if kind == "mat" else 4)
+        if name == "lmh1":
+            head = Wo["lmh1"].copy()
+            big = np.random.default_rng(77).standard_normal(head[inner_s.vocab:].shape) * 2.0
+            head[inner_s.vocab:] = big
+            oblob[off:off + nb] = S.f32_to_bf16_bits(head.astype(np.float32)).tobytes()
+        off += nb
+    oblob = bytes(oblob)
+    Wo = S.unpack_weights(outer_s, oblob)
+    iblob = S.make_weights(inner_s, seed=32, std=0.3)
+    tables = S.unpack_outer_tables(outer_s, S.make_outer_tables(outer_s, inner_s.n_codes, inner_s.vocab, std=0.3),
+                                   inner_s.n_codes, inner_s.vocab)
+    oorc = Hh.make_oracle(outer_s, oblob, topk=topk, temperature=T, draft_len=0)
+    iorc = Hh.make_oracle(inner_s, iblob, topk=topk, temperature=T, draft_len=3)
+    n = 4
+    t, u_c0 = S.pipeline_inputs(outer_s, n)
+    uni = S.uniforms(n, inner_s.n_codes, seed=17)
+    codes, stats, hs = O.pipeline_frames(oorc, Wo["emb0"], tables, iorc, t, u_c0, uni, topk, T)
+    assert codes.shape == (n, 16)
+    rows = []
+    hits_first_masked = 0
+    for i in range(n):
+        x = t[i].astype(np.float64)
+        if i > 0:
+            prev = codes[i - 1]
+            x = x + Wo["emb0"][prev[0]].astype(np.float64)
+            for j in range(1, 16):
+                x = x + tables[j - 1][prev[j]].astype(np.float64)
+        rows.append(x)
+        h = _torch_forward(outer_s, Wo, None, None, rows=np.stack(rows))[-1]
+        assert np.max(np.abs(h - hs[i])) < 1e-9, i
+        lg = Wo["lmh1"].astype(np.float64) @ h
+        # unmasked, the large rows would win the draw: the mask is what keeps c_0 embeddable
+        assert np.argmax(lg) >= inner_s.vocab
+        hits_first_masked += int(inner_s.vocab in np.argsort(-lg, kind="stable")[:topk])
+        lg[inner_s.vocab:] = -np.inf
+        c0, _ = _np_topk_sample(lg, topk, T, float(u_c0[i]))
+        assert codes[i][0] == c0 < inner_s.vocab, (i, codes[i][0], c0)
+        inner, st, _ = iorc.spec_frame(h.astype(np.float32), c0, uni[i])
+        assert codes[i][1:].tolist() == inner.tolist()
+        assert st == stats[i]
+    # the chain is live: a frame's codes change the next frame's input
+    assert len({tuple(c) for c in codes}) == n
+    # the first masked entry is a top-k candidate somewhere, so a mask starting one late shows
+    assert hits_first_masked >= 1
+    oorc.close()
+    iorc.close()
