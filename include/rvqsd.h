@@ -156,6 +156,25 @@ rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, in
 rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidden, const int32_t* d_c0,
                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats);
 
+/* rvqsd_decode_frame_async for callers that cannot allocate memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation. It
+ * needs no stream object: the frame's device buffers (exchange words, KV cache,
+ * parameter block) live in a fixed 16 MiB array of this library on each GPU it
+ * runs on, held until the process ends; the call allocates nothing (no
+ * hipMalloc, hipFree or allocating library routine) and enqueues two kernels on
+ * hip_stream (NULL = the null stream): one that clears that array's frame region
+ * and writes the parameter block, then the frame kernel. Arguments and outputs
+ * as rvqsd_decode_frame_async (device pointers; d_stats reports device-side
+ * errors); the codes equal a fresh stream's. Every call on one GPU shares its
+ * array: calls whose work overlaps on that GPU (other streams, other threads)
+ * race and must be serialised by the caller. EUNSUPPORTED when the model's frame
+ * buffers exceed the array (model info: the 1024-wide 2048-code model needs 5.6
+ * MB at draft length 4, 12.8 MB at 14); EINVAL for a null argument or when the
+ * current device is not the model's. */
+rvqsd_status rvqsd_decode_frame_noalloc(const rvqsd_model* m, void* hip_stream, const float* d_frame_hidden,
+                                        const int32_t* d_c0, const float* d_uniforms, int32_t* d_out_codes,
+                                        rvqsd_stats* d_stats);
+
 /* Decode n independent frames with max_streams of them in flight (the
  * multi-stream verification of a batch of utterances; each frame is the same
  * problem as rvqsd_decode_frame_u). Frame f runs in lane f % max_streams after

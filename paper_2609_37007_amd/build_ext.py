@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "librvqsd.so")
 SOURCES = [os.path.join(CSRC, "rvqsd_frame.hip"), os.path.join(CSRC, "rvqsd_batch.hip"),
-           os.path.join(CSRC, "rvqsd_api.cpp")]
+           os.path.join(CSRC, "rvqsd_noalloc.hip"), os.path.join(CSRC, "rvqsd_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # packed FP32 instructions are disabled for all device code
 FLAGS = ["-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC", "-Wall",

@@ -69,18 +69,7 @@ hipError_t dev_alloc(void** p, size_t bytes) {
 
 }  // namespace
 
-struct rvqsd_model {
-  rvqsd_cfg cfg;
-  int device;
-  int nwg;
-  int mr;               // rows the kernel is instantiated for
-  int wbytes;           // bytes per matrix element
-  size_t lds_bytes;
-  int stage_cols;
-  void* dweights;
-  uint64_t dweight_bytes;
-  KParams base;         // weight offsets and dimensions (buffers filled per stream)
-};
+int rvqsd::set_last_error(int st, const char* msg) { return set_err(st, "%s", msg); }
 
 struct rvqsd_stream {
   rvqsd_model* m;
@@ -398,6 +387,9 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   }
   m->wbytes = (int)wb;
   m->dweight_bytes = o;
+  // the rotary table follows the weights: [kMaxPos][d/2][2] cos, sin of position * base^(-2i/d)
+  const uint64_t rope_off = (o + 255) & ~(uint64_t)255;
+  const size_t rope_bytes = (size_t)kMaxPos * (k.d / 2) * 2 * sizeof(float);
   // LDS: stage the widest activation if it fits, else the down projection polls its chunks directly
   const int cpw = (k.H + nwg - 1) / nwg;
   const size_t head = (size_t)frame_lds_head_floats(m->mr, cpw);
@@ -423,18 +415,35 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   m->lds_bytes = lds;
   m->stage_cols = stage;
   k.stage_cols = stage;
-  hipError_t e = dev_alloc(&m->dweights, o);
+  hipError_t e = dev_alloc(&m->dweights, rope_off + rope_bytes);
   if (e != hipSuccess) {
     delete m;
     return set_err(RVQSD_ENOMEM, "device weights (%llu bytes): %s", (unsigned long long)o, hipGetErrorString(e));
   }
   e = hipMemcpy(m->dweights, b + 64, o, hipMemcpyHostToDevice);
+  if (e == hipSuccess) {
+    // computed in double, stored as float
+    const int half = k.d / 2;
+    float* tab = (float*)malloc(rope_bytes);
+    if (!tab) e = hipErrorOutOfMemory;
+    for (int pos = 0; tab && pos < kMaxPos; ++pos)
+      for (int i = 0; i < half; ++i) {
+        const double th = (double)pos * pow(k.rope_base, -2.0 * (double)i / (double)k.d);
+        tab[(pos * half + i) * 2 + 0] = (float)cos(th);
+        tab[(pos * half + i) * 2 + 1] = (float)sin(th);
+      }
+    if (tab) e = hipMemcpy((uint8_t*)m->dweights + rope_off, tab, rope_bytes, hipMemcpyHostToDevice);
+    free(tab);
+  }
   if (e != hipSuccess) {
     (void)hipFree(m->dweights);
     delete m;
     return set_err(RVQSD_EHIP, "weight upload: %s", hipGetErrorString(e));
   }
   k.wbase = (const uint8_t*)m->dweights;
+  k.rope = (const float*)((const uint8_t*)m->dweights + rope_off);
+  const FrameLayout fl = frame_layout(k);
+  m->frame_bytes = fl.bytes;
   m->base = k;
   *out = m;
   return RVQSD_OK;
@@ -470,30 +479,17 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
   s->m = m;
   s->stream = (hipStream_t)hip_stream;
   KParams k = m->base;
-  k.n_slots = kSlotDraft0 + kMaxRows * k.K;
-  k.drec_words = 1 + 3 * kMaxTopk;
-  const size_t H = k.H, V = k.V;
-  size_t off = 0;
+  const size_t H = k.H;
+  // the frame buffers, then this stream's staging of the synchronous calls
+  const FrameLayout fl = frame_layout(k);
+  size_t off = fl.bytes;
   auto take = [&](size_t bytes) {
     size_t at = off;
     off += (bytes + 255) & ~(size_t)255;
     return at;
   };
-  // Layout: constants | parity words (initialised to parity 1) | pass count |
-  // tagged words (cleared to tag 0) | scratch, staging and the parameter block.
-  const size_t o_rope = take((size_t)kMaxPos * k.d * 4);
-  const size_t par_begin = off;
-  const size_t o_x = take(kMaxRows * H * 4), o_qkv = take((size_t)kMaxRows * k.nqkv * 4),
-               o_attn = take((size_t)kMaxRows * k.qdim * 4), o_act = take((size_t)kMaxRows * k.F * 4);
-  const size_t par_end = off;
-  const size_t o_pc = take(4);
-  const size_t tag_begin = off;
-  const size_t o_log = take((size_t)2 * k.n_slots * V * 8), o_vres = take((size_t)2 * kMaxRows * 8),
-               o_drec = take((size_t)2 * k.n_slots * k.drec_words * 8), o_status = take(8);
-  const size_t tag_end = off;
-  const size_t o_kvc = take((size_t)k.nq * k.L * kMaxPos * 2 * k.d * 4),
-               o_in = take(((size_t)H + 3 * kMaxCodes + 4) * 4), o_out = take((kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64),
-               o_kp = take(sizeof(KParams));
+  const size_t o_in = take(((size_t)H + 3 * kMaxCodes + 4) * 4),
+               o_out = take((kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64);
   s->dbuf_bytes = off;
   hipError_t e = dev_alloc(&s->dbuf, off);
   if (e != hipSuccess) {
@@ -501,7 +497,8 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     return set_err(RVQSD_ENOMEM, "stream buffers (%zu bytes): %s", off, hipGetErrorString(e));
   }
   e = hipMemset(s->dbuf, 0, off);
-  if (e == hipSuccess) e = hipMemsetD8((hipDeviceptr_t)((uint8_t*)s->dbuf + par_begin), 0x01, par_end - par_begin);
+  if (e == hipSuccess)
+    e = hipMemsetD8((hipDeviceptr_t)((uint8_t*)s->dbuf + fl.par_begin), 0x01, fl.par_end - fl.par_begin);
   if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_in, ((size_t)H + 3 * kMaxCodes + 4) * 4, hipHostMallocDefault);
   if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_out, (kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64, hipHostMallocDefault);
   if (e != hipSuccess) {
@@ -511,41 +508,17 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     return set_err(RVQSD_ENOMEM, "stream staging: %s", hipGetErrorString(e));
   }
   uint8_t* base = (uint8_t*)s->dbuf;
-  k.xb = (uint32_t*)(base + o_x);
-  k.qkvb = (uint32_t*)(base + o_qkv);
-  k.attnb = (uint32_t*)(base + o_attn);
-  k.actb = (uint32_t*)(base + o_act);
-  k.pass_count = (uint32_t*)(base + o_pc);
-  s->par_begin = par_begin;
-  s->par_end = par_end;
-  s->tag_begin = tag_begin;
-  s->tag_end = tag_end;
-  k.logb = (uint64_t*)(base + o_log);
-  k.vres = (uint64_t*)(base + o_vres);
-  k.drec = (uint64_t*)(base + o_drec);
-  k.kvc = (float*)(base + o_kvc);
-  k.status = (uint64_t*)(base + o_status);
-  k.rope = (const float*)(base + o_rope);
+  frame_bind(&k, base, fl);
+  s->par_begin = fl.par_begin;
+  s->par_end = fl.par_end;
+  s->tag_begin = fl.tag_begin;
+  s->tag_end = fl.tag_end;
   s->status = k.status;
   s->d_in = (float*)(base + o_in);
   s->d_out = (int32_t*)(base + o_out);
-  s->dkp = (KParams*)(base + o_kp);
+  s->dkp = (KParams*)(base + fl.o_kp);
   s->kp = k;
-  {
-    // rotary table: angle = position * base^(-2i/d), computed in double
-    const int half = k.d / 2;
-    float* tab = (float*)malloc((size_t)kMaxPos * half * 2 * sizeof(float));
-    if (!tab) e = hipErrorOutOfMemory;
-    for (int pos = 0; tab && pos < kMaxPos; ++pos)
-      for (int i = 0; i < half; ++i) {
-        const double th = (double)pos * pow(k.rope_base, -2.0 * (double)i / (double)k.d);
-        tab[(pos * half + i) * 2 + 0] = (float)cos(th);
-        tab[(pos * half + i) * 2 + 1] = (float)sin(th);
-      }
-    if (tab) e = hipMemcpy((void*)k.rope, tab, (size_t)kMaxPos * half * 2 * sizeof(float), hipMemcpyHostToDevice);
-    free(tab);
-  }
-  if (e == hipSuccess) e = hipMemcpy(s->dkp, &s->kp, sizeof(KParams), hipMemcpyHostToDevice);
+  e = hipMemcpy(s->dkp, &s->kp, sizeof(KParams), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipHostFree(s->h_in);
     (void)hipHostFree(s->h_out);
@@ -553,8 +526,7 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
     delete s;
     return set_err(RVQSD_EHIP, "parameter upload: %s", hipGetErrorString(e));
   }
-  const int tags_per_frame = kMaxPos * phases_per_pass(k.L) + 2;
-  s->epoch_step = (uint32_t)((tags_per_frame + 4095) & ~4095);
+  s->epoch_step = frame_epoch_step(k.L);
   s->epoch = s->epoch_step;
   s->lanes = 1;
   if (max_streams > 1) {

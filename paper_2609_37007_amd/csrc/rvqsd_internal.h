@@ -52,7 +52,7 @@ struct KParams {
   uint64_t* drec;  // [2][n_slots][drec_words] draft records: token, then (idx, prob lo, prob hi) x support
   int32_t n_slots, drec_words;
   float* kvc;      // [nq][L][kMaxPos][2][d] KV cache of each attention workgroup (k after norm and RoPE, v)
-  const float* rope;  // [kMaxPos][d/2][2] cos, sin of position * rope_base^(-2i/d)
+  const float* rope;  // [kMaxPos][d/2][2] cos, sin of position * rope_base^(-2i/d) (held by the model)
   int32_t work_floats;  // floats of the LDS work area (the attention constants follow it)
   uint64_t* status; // device status word: (epoch_base << 32) | error code of that frame
   // trace (nullable)
@@ -73,6 +73,78 @@ struct FrameArgs {
   rvqsd_stats* out_stats;     // [1]
   uint32_t epoch_base;        // tags of this frame are epoch_base + 1 ..
 };
+
+// Device buffers of one frame decode (the exchange words, the KV cache and the
+// parameter block), laid out from one base address:
+//   parity words (x, q/k/v, attention output, activation; initialised to parity 1) |
+//   pass count | tagged words (logits, verdicts, draft records, status; cleared to
+//   tag 0) | KV cache | parameter block. A decode stream owns one such region; the
+//   allocation-free entry point places it in a fixed device array.
+struct FrameLayout {
+  size_t o_x, o_qkv, o_attn, o_act;  // parity words
+  size_t par_begin, par_end;
+  size_t o_pc;                       // pass count
+  size_t o_log, o_vres, o_drec, o_status;  // tagged words
+  size_t tag_begin, tag_end;
+  size_t o_kvc, o_kp;
+  size_t bytes;                      // total, 256-byte aligned
+  int32_t n_slots, drec_words;
+};
+
+inline FrameLayout frame_layout(const KParams& k) {
+  FrameLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return at;
+  };
+  L.n_slots = kSlotDraft0 + kMaxRows * k.K;
+  L.drec_words = 1 + 3 * kMaxTopk;
+  const size_t H = (size_t)k.H, V = (size_t)k.V;
+  L.par_begin = off;
+  L.o_x = take(kMaxRows * H * 4);
+  L.o_qkv = take((size_t)kMaxRows * k.nqkv * 4);
+  L.o_attn = take((size_t)kMaxRows * k.qdim * 4);
+  L.o_act = take((size_t)kMaxRows * k.F * 4);
+  L.par_end = off;
+  L.o_pc = take(4);
+  L.tag_begin = off;
+  L.o_log = take((size_t)2 * L.n_slots * V * 8);
+  L.o_vres = take((size_t)2 * kMaxRows * 8);
+  L.o_drec = take((size_t)2 * L.n_slots * L.drec_words * 8);
+  L.o_status = take(8);
+  L.tag_end = off;
+  L.o_kvc = take((size_t)k.nq * k.L * kMaxPos * 2 * k.d * 4);
+  L.o_kp = take(sizeof(KParams));
+  L.bytes = off;
+  return L;
+}
+
+// Point the buffer fields of k into the region at base (device address).
+inline void frame_bind(KParams* k, uint8_t* base, const FrameLayout& L) {
+  k->n_slots = L.n_slots;
+  k->drec_words = L.drec_words;
+  k->xb = (uint32_t*)(base + L.o_x);
+  k->qkvb = (uint32_t*)(base + L.o_qkv);
+  k->attnb = (uint32_t*)(base + L.o_attn);
+  k->actb = (uint32_t*)(base + L.o_act);
+  k->pass_count = (uint32_t*)(base + L.o_pc);
+  k->logb = (uint64_t*)(base + L.o_log);
+  k->vres = (uint64_t*)(base + L.o_vres);
+  k->drec = (uint64_t*)(base + L.o_drec);
+  k->status = (uint64_t*)(base + L.o_status);
+  k->kvc = (float*)(base + L.o_kvc);
+}
+
+// Frame tags step per frame: enough for every pass and phase of one frame.
+inline uint32_t frame_epoch_step(int L) {
+  const int tags_per_frame = kMaxPos * phases_per_pass(L) + 2;
+  return (uint32_t)((tags_per_frame + 4095) & ~4095);
+}
+
+// Record st and msg as the calling thread's last error (rvqsd_last_error); returns st.
+int set_last_error(int st, const char* msg);
 
 // Host entry into the kernel translation unit. gp: KParams in device memory.
 int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream,
@@ -178,3 +250,18 @@ int frame_lds_head_floats(int mr, int cpw);
 int frame_max_rows(int K);
 
 }  // namespace rvqsd
+
+// A created model (host object behind the opaque rvqsd_model handle).
+struct rvqsd_model {
+  rvqsd_cfg cfg;
+  int device;
+  int nwg;
+  int mr;               // rows the frame kernel is instantiated for
+  int wbytes;           // bytes per matrix element
+  size_t lds_bytes;
+  int stage_cols;
+  void* dweights;       // the blob payload, then the rotary table
+  uint64_t dweight_bytes;
+  size_t frame_bytes;   // device buffers of one frame decode (FrameLayout::bytes)
+  rvqsd::KParams base;  // dimensions, weight offsets and the rotary table; buffers are set per decode region
+};

@@ -21,7 +21,8 @@ TRACE_ROUND_INTS = 32
 
 # every symbol include/rvqsd.h declares
 EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_stream_destroy",
-           "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset",
+           "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frame_noalloc",
+           "rvqsd_stream_reset",
            "rvqsd_set_trace", "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async",
            "rvqsd_batch_totals", "rvqsd_set_batch_trace", "rvqsd_outer_create", "rvqsd_outer_destroy", "rvqsd_outer_reset",
            "rvqsd_pipeline_frames_async", "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
@@ -118,6 +119,7 @@ def lib():
         L.rvqsd_decode_frame.argtypes = [vp, vp, i32, ctypes.c_uint64, vp, P(rvqsd_stats)]
         L.rvqsd_decode_frame_u.argtypes = [vp, vp, i32, vp, vp, P(rvqsd_stats)]
         L.rvqsd_decode_frame_async.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.rvqsd_decode_frame_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.rvqsd_set_trace.argtypes = [vp, P(rvqsd_trace)]
         L.rvqsd_decode_frames_batched.argtypes = [vp, i32, vp, vp, vp, vp, vp]
         L.rvqsd_decode_frames_batched_async.argtypes = [vp, i32, vp, vp, vp, vp, vp]
@@ -135,7 +137,8 @@ def lib():
         L.rvqsd_last_error.argtypes = []
         L.rvqsd_last_error.restype = ctypes.c_char_p
         for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_decode_frame",
-                  "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_stream_reset", "rvqsd_set_trace",
+                  "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frame_noalloc",
+                  "rvqsd_stream_reset", "rvqsd_set_trace",
                   "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async", "rvqsd_batch_totals",
                   "rvqsd_set_batch_trace",
                   "rvqsd_outer_create", "rvqsd_outer_reset", "rvqsd_pipeline_frames_async",
@@ -188,6 +191,14 @@ class Model:
         i = rvqsd_info()
         _check(lib().rvqsd_model_info(self._h, ctypes.byref(i)), "rvqsd_model_info")
         return i.as_dict()
+
+    def decode_frame_noalloc(self, hip_stream, d_frame_hidden: int, d_c0: int, d_uniforms: int, d_out_codes: int,
+                             d_stats: int):
+        """The allocation-free decode (device pointers, ints); enqueues only."""
+        _check(lib().rvqsd_decode_frame_noalloc(self._h, ctypes.c_void_p(hip_stream or 0),
+                                                ctypes.c_void_p(d_frame_hidden), ctypes.c_void_p(d_c0),
+                                                ctypes.c_void_p(d_uniforms), ctypes.c_void_p(d_out_codes),
+                                                ctypes.c_void_p(d_stats)), "rvqsd_decode_frame_noalloc")
 
     def close(self):
         if getattr(self, "_h", None) and _lib is not None:
