@@ -6,8 +6,10 @@ there is no CPU fallback.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 
 import numpy as np
 
@@ -79,25 +81,35 @@ class RvqsdError(RuntimeError):
 _lib = None
 
 
-def _init_hip_runtime():
-    """Initialise the HIP runtime before librvqsd.so is loaded.
+# live handles, closed in this order by the exit hook below
+_live = {"outer": weakref.WeakSet(), "stream": weakref.WeakSet(), "model": weakref.WeakSet()}
 
-    Exit handlers run in the reverse order of their registration. Loading the
-    library registers the unloading of its kernel code objects; a profiler
-    attached to the HIP runtime (rocprofv3) registers its own teardown when the
-    runtime initialises. If the library were loaded first, the profiler's
-    teardown would run before the library's code objects are unloaded, and that
-    unloading would then call into the torn-down profiler. With the runtime
-    initialised first, the library's unloading runs first. Without a GPU the
-    call only returns an error code, which is ignored here.
-    """
-    try:
-        hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime already in the process, if any
-    except OSError:
+
+def _shutdown():
+    """Interpreter-exit hook: close every live handle, then unload the library.
+
+    Unloading runs the library's code-object unregistration now, while the HIP
+    runtime (and any profiler attached to it) is still up, instead of from the
+    C exit handlers after the process has begun tearing the runtime down. Objects
+    that outlive this hook see the library gone and release nothing."""
+    global _lib
+    if _lib is None:
         return
-    hip.hipInit.argtypes = [ctypes.c_uint]
-    hip.hipInit.restype = ctypes.c_int
-    hip.hipInit(0)
+    for kind in ("outer", "stream", "model"):
+        for obj in list(_live[kind]):
+            try:
+                obj.close()
+            except Exception:
+                pass
+    L, _lib = _lib, None
+    try:
+        import _ctypes
+        _ctypes.dlclose(L._handle)
+    except Exception:
+        pass
+
+
+atexit.register(_shutdown)
 
 
 def lib():
@@ -106,7 +118,6 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_37007_amd.build_ext`")
-        _init_hip_runtime()
         L = ctypes.CDLL(LIB_PATH)
         P, vp, i32 = ctypes.POINTER, ctypes.c_void_p, ctypes.c_int32
         L.rvqsd_create.argtypes = [P(rvqsd_weights), P(rvqsd_cfg), P(vp)]
@@ -185,6 +196,7 @@ class Model:
         h = ctypes.c_void_p()
         _check(lib().rvqsd_create(ctypes.byref(w), ctypes.byref(cfg), ctypes.byref(h)), "rvqsd_create")
         self._h = h
+        _live["model"].add(self)
         self._blob = None  # the library copied the weights
 
     def info(self) -> dict:
@@ -218,6 +230,7 @@ class Stream:
         _check(lib().rvqsd_stream_create(model._h, ctypes.c_void_p(hip_stream or 0), max_streams, ctypes.byref(h)),
                "rvqsd_stream_create")
         self._h = h
+        _live["stream"].add(self)
         self._trace = None
 
     def close(self):
@@ -308,6 +321,7 @@ class Outer:
         _check(lib().rvqsd_outer_create(model._h, ctypes.c_char_p(tab), n_tables, table_vocab, topk,
                                         float(temperature), max_frames, ctypes.byref(h)), "rvqsd_outer_create")
         self._h = h
+        _live["outer"].add(self)
 
     def reset(self):
         _check(lib().rvqsd_outer_reset(self._h), "rvqsd_outer_reset")
