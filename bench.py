@@ -98,9 +98,38 @@ def parse():
     ap.add_argument("--streams", type=int, default=1, help="independent streams verified together (1..16)")
     ap.add_argument("--frames-per-stream", type=int, default=500)
     ap.add_argument("--pipeline", action="store_true", help="outer CodeDecoder step + inner loop per frame")
+    ap.add_argument("--offsets", default="seed", metavar="seed|zero|FILE.npy",
+                    help="draft offsets: the blob's own N(0, 0.02) draw (seed), all zero (the reused heads of "
+                         "Sec. 2.2), or a trained float32 [max_draft][hidden] array")
+    ap.add_argument("--residency", action="store_true",
+                    help="only measure whether the weights stay in the Infinity Cache: warm against cold frames "
+                         "(a 2 GiB sweep between frames) and a plain streaming read of a weight-sized buffer")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="only run 5 plain device copies of MB MiB (the reference kernel for HBM byte counters)")
     return ap.parse_args()
+
+
+def make_blob(S, s, a):
+    """The workload's weight blob with the draft offsets chosen by --offsets."""
+    import numpy as np
+    if a.offsets == "seed":
+        return S.make_weights(s, seed=0, head_scale=a.head_scale)
+    if a.offsets == "zero":
+        return S.make_weights(s, seed=0, head_scale=a.head_scale, offsets=np.zeros((s.max_draft, s.hidden)))
+    path = a.offsets if os.path.isabs(a.offsets) else os.path.join(ROOT, a.offsets)
+    ofs = np.load(path, allow_pickle=False)
+    return S.make_weights(s, seed=0, head_scale=a.head_scale, offsets=ofs)
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def copy_calibration(mb: int) -> int:
@@ -117,26 +146,41 @@ def copy_calibration(mb: int) -> int:
     return 0
 
 
-def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order):
-    """Time the CPU oracle on frames `order` until `seconds` pass; returns the cpu_baseline object."""
+def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order, one_thread_seconds=8.0):
+    """Time the CPU oracle on frames `order` until `seconds` pass (all host threads), then on
+    the next frames with one thread for `one_thread_seconds`; returns the cpu_baseline object."""
     from oracle import oracle as O
     orc = O.Oracle(blob, n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
                    head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
                    dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K)
     threads = O.get_threads()
     print(f"[bench] oracle sample on {threads} threads, ~{seconds:.0f} s", file=sys.stderr, flush=True)
-    done, same = 0, 0
-    c_t0 = time.perf_counter()
-    while done < len(order) and (time.perf_counter() - c_t0) < seconds:
-        i = order[done]
-        oc, _, _ = orc.spec_frame(f[i], int(c0[i]), u[i])
-        same += int((oc == codes[i]).all())
-        done += 1
-    c_el = time.perf_counter() - c_t0
+
+    def run(start, budget):
+        done, same = 0, 0
+        t0 = time.perf_counter()
+        while start + done < len(order) and (time.perf_counter() - t0) < budget:
+            i = order[start + done]
+            oc, _, _ = orc.spec_frame(f[i], int(c0[i]), u[i])
+            same += int((oc == codes[i]).all())
+            done += 1
+        return done, same, time.perf_counter() - t0
+
+    done, same, c_el = run(0, seconds)
+    one = None
+    if one_thread_seconds > 0 and done < len(order):
+        O.set_threads(1)
+        d1, s1, e1 = run(done, one_thread_seconds)
+        O.set_threads(threads)
+        if d1:
+            one = {"value": round(s.n_codes * d1 / e1, 3), "frames": d1, "seconds": round(e1, 1),
+                   "identical_to_gpu": s1}
     orc.close()
     return {"value": round(s.n_codes * done / c_el, 3), "unit": "codes/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} of the timed frames ({c_el:.1f} s, fp64 full-recompute oracle, OpenMP over output "
-                      f"rows); {same}/{done} frames give codes identical to the GPU's"}
+            "cpu_model": cpu_model(), "nproc": os.cpu_count(),
+            "sample": f"{done} of the timed frames ({c_el:.1f} s on {threads} threads, fp64 full-recompute oracle, "
+                      f"OpenMP over output rows); {same}/{done} frames give codes identical to the GPU's",
+            "one_thread": one}
 
 
 def run_pipeline(a) -> int:
@@ -420,6 +464,112 @@ def run_streams(a) -> int:
     return 0
 
 
+def run_residency(a) -> int:
+    """Whether the frame kernel's weights stay in the 256 MB Infinity Cache (MALL).
+
+    * warm: frames back to back (the weights of one pass are the weights of the next);
+    * cold: a 2 GiB read-and-write sweep of a separate buffer before each frame, so the
+      frame's first pass reads its weights from HBM; every pass of a frame is clocked by
+      the kernel's own trace (device clock at the end of each pass);
+    * stream: plain torch reductions over a buffer of the round's weight bytes, warm
+      (repeated) and cold (after the same sweep): the box's cache and HBM read rates."""
+    import numpy as np
+    import torch
+
+    from paper_2609_37007_amd import rvqsd as R
+    from paper_2609_37007_amd import synth as S
+
+    R.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    shape_name, topk, K_default, _ = WORKLOADS[a.workload]
+    s = getattr(S, shape_name)
+    K = K_default if a.draft_len is None else a.draft_len
+    blob = make_blob(S, s, a)
+    cfg = R.make_cfg(n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
+                     head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
+                     dtype=s.dtype, topk=topk, temperature=0.9, draft_len=K)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ts = torch.cuda.current_stream(dev)
+    model = R.Model(blob, cfg)
+    stream = R.Stream(model, hip_stream=ts.cuda_stream)
+    F = a.steps or 100
+    f, c0 = S.frame_inputs(s, F)
+    u = S.uniforms(F, s.n_codes)
+    d_f, d_c0 = torch.from_numpy(f).to(dev), torch.from_numpy(c0).to(dev)
+    d_u = torch.from_numpy(np.ascontiguousarray(u)).to(dev)
+    n, H, sb = s.n_codes, s.hidden, R.STATS_DTYPE.itemsize
+    d_codes = torch.zeros((F, n), dtype=torch.int32, device=dev)
+    d_st = torch.zeros(F * sb, dtype=torch.uint8, device=dev)
+    nph = 5 * s.n_layers + 5
+    clk = torch.zeros((16, nph), dtype=torch.int64, device=dev)
+    sweep = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB, read and written: 2 GiB through the cache
+
+    def frame(i, evict):
+        if evict:
+            sweep.add_(1.0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        clk.zero_()
+        stream.set_trace(0, 0, clk.data_ptr(), 16)
+        e0.record(ts)
+        stream.decode_frame_async(d_f.data_ptr() + i * H * 4, d_c0.data_ptr() + i * 4, d_u.data_ptr() + i * n * 12,
+                                  d_codes.data_ptr() + i * n * 4, d_st.data_ptr() + i * sb)
+        e1.record(ts)
+        torch.cuda.synchronize()
+        st = np.frombuffer(d_st[i * sb:(i + 1) * sb].cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)[0]
+        c = clk.cpu().numpy()[:int(st["target_calls"]), 5 * s.n_layers + 2].astype(np.float64)  # commit end
+        start = float(st["clk_start"])
+        passes = np.diff(np.concatenate([[start], c])) * 0.01  # 100 MHz clock -> us
+        return e0.elapsed_time(e1) * 1e3, passes
+
+    for i in range(5):
+        frame(i, False)
+    res = {}
+    for mode, evict in (("warm", False), ("cold", True)):
+        print(f"[bench] residency: {mode} frames", file=sys.stderr, flush=True)
+        fr, p0, rest = [], [], []
+        for i in range(F):
+            us, passes = frame(i, evict)
+            fr.append(us)
+            p0.append(passes[0])
+            rest.extend(passes[1:])
+        res[mode] = {"frame_us_mean": round(float(np.mean(fr)), 2), "first_pass_us_mean": round(float(np.mean(p0)), 2),
+                     "later_pass_us_mean": round(float(np.mean(rest)), 2), "frames": F}
+    stream.set_trace()
+    # plain streaming reads of a buffer the size of one round's weights
+    wb = int(model.info()["layer_weight_bytes"] + 9 * model.info()["head_bytes"])
+    buf = torch.ones(wb // 4, dtype=torch.float32, device=dev)
+    out = torch.empty((), dtype=torch.float32, device=dev)
+
+    def read_rate(evict, reps=20):
+        t = 0.0
+        for _ in range(reps):
+            if evict:
+                sweep.add_(1.0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(ts)
+            torch.sum(buf, dim=0, out=out)
+            e1.record(ts)
+            torch.cuda.synchronize()
+            t += e0.elapsed_time(e1) * 1e-3
+        return wb * reps / t / 1e9
+
+    read_rate(False, 3)
+    res["stream_read_gbs"] = {"bytes": wb, "warm": round(read_rate(False), 1), "cold": round(read_rate(True), 1)}
+    w, c = res["warm"], res["cold"]
+    res["first_pass_extra_us_cold"] = round(c["first_pass_us_mean"] - w["first_pass_us_mean"], 2)
+    res["later_pass_extra_us_cold"] = round(c["later_pass_us_mean"] - w["later_pass_us_mean"], 2)
+    res["workload"] = f"{a.workload}, draft length {K}, offsets {a.offsets}"
+    res["weight_bytes_per_round"] = wb
+    del sweep, buf
+    stream.close()
+    model.close()
+    print(json.dumps({"residency": res}), flush=True)
+    return 0
+
+
 def main() -> int:
     a = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -434,6 +584,8 @@ def main() -> int:
         return run_streams(a)
     if a.pipeline:
         return run_pipeline(a)
+    if a.residency:
+        return run_residency(a)
 
     import numpy as np
     import torch
@@ -452,7 +604,7 @@ def main() -> int:
     W = a.warmup
     temperature = 0.9
     print(f"[bench] building {a.workload} weights", file=sys.stderr, flush=True)
-    blob = S.make_weights(s, seed=0, head_scale=a.head_scale)
+    blob = make_blob(S, s, a)
     blob_sha = hashlib.sha256(blob).hexdigest()[:16]
     cfg = R.make_cfg(n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
                      head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
@@ -542,6 +694,7 @@ def main() -> int:
             "topk": topk,
             "temperature": temperature,
             "head_scale": a.head_scale,
+            "offsets": a.offsets,
             "batch": 1,
             "weights_sha256_16": blob_sha,
             "parallelism": "single GPU, one persistent workgroup per compute unit",

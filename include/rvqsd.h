@@ -88,8 +88,10 @@ typedef struct {
  *          logits LMH_{s+j}(h_s + b_j) of row r.
  *  rounds: int32[max_rounds][32]: m, K', first_pos, rows, m_new, accepted, token,
  *          pass index, drafts d_{m+1..m+K'} at [8..8+K'), then reserved.
- *  clock:  uint64[max_rounds][5*n_layers+5]: device clock at each phase end of a pass
- *          (workgroup 0's view), last entry = pass end.
+ *  clock:  uint64[max_rounds][5*n_layers+5]: device clock (workgroup 0's view) at the end
+ *          of each phase of a pass: per layer QKV, attention, O, gate/up, down at
+ *          [5l..5l+4], then the LM heads [5L], sampling [5L+1] and the commit [5L+2],
+ *          which ends the pass; the last two entries are unused.
  *  wg_clock: uint64[max_rounds][5*n_layers+5][workgroups]: the same for every workgroup.
  *  wg_ready: uint64[max_rounds][5*n_layers+5][workgroups]: device clock at which each
  *          workgroup held every input of the phase (after its last wait), 0 if it had none. */
