@@ -58,6 +58,38 @@ class OrcTrace(ctypes.Structure):
                 ("n_rounds", ctypes.c_int32)]
 
 
+MAX_TREE = 80
+
+
+class OrcTree(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int32), ("parent", ctypes.c_int32 * (MAX_TREE + 1)),
+                ("rank", ctypes.c_int32 * (MAX_TREE + 1))]
+
+
+class OrcTreeRound(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int32), ("depth", ctypes.c_int32), ("n_rows", ctypes.c_int32),
+                ("m_new", ctypes.c_int32), ("n_cand", ctypes.c_int32), ("accepted", ctypes.c_int32),
+                ("token", ctypes.c_int32),
+                ("tokens", ctypes.c_int32 * (MAX_TREE + 1)), ("path", ctypes.c_int32 * 16),
+                ("margin", ctypes.c_double), ("topk_gap", ctypes.c_double)]
+
+
+class OrcTreeTrace(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.POINTER(OrcTreeRound)), ("verify_logits", ctypes.POINTER(ctypes.c_double)),
+                ("draft_logits", ctypes.POINTER(ctypes.c_double)), ("max_rounds", ctypes.c_int32),
+                ("n_rounds", ctypes.c_int32)]
+
+
+def make_tree(parents, ranks) -> OrcTree:
+    """parents[i], ranks[i] of packed rows 1..N (row 0 is the root)."""
+    t = OrcTree()
+    t.n_nodes = len(parents)
+    for i, (p, r) in enumerate(zip(parents, ranks), start=1):
+        t.parent[i] = int(p)
+        t.rank[i] = int(r)
+    return t
+
+
 PROBE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_double), ctypes.c_int32)
 
 _lib = None
@@ -85,10 +117,14 @@ def lib():
         L.orc_ar_frame.argtypes = [vp, vp, i32, vp, vp]
         L.orc_spec_frame.argtypes = [vp, vp, i32, vp, vp, P(OrcStats), P(OrcTrace), PROBE_FN, vp]
         L.orc_uniforms_from_seed.argtypes = [ctypes.c_uint64, i32, vp]
+        L.orc_tree_mask.argtypes = [P(OrcTree), vp]
+        L.orc_tree_hidden.argtypes = [vp, P(OrcTree), vp, vp, i32, vp, i32, vp]
+        L.orc_tree_frame.argtypes = [vp, P(OrcTree), vp, i32, vp, vp, P(OrcStats), P(OrcTreeTrace), PROBE_FN, vp]
         L.orc_splitmix64_at.restype = ctypes.c_uint64
         L.orc_splitmix64_at.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         for name in ("orc_forward", "orc_forward_vectors", "orc_logits", "orc_topk_softmax", "orc_sample", "orc_accept_or_resample",
-                     "orc_ar_frame", "orc_spec_frame", "orc_abi_version"):
+                     "orc_ar_frame", "orc_spec_frame", "orc_abi_version", "orc_tree_mask", "orc_tree_hidden",
+                     "orc_tree_frame"):
             getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -202,6 +238,63 @@ class Oracle:
                 tdict["verify_logits"] = vl[:tr.n_rounds]
                 tdict["draft_logits"] = dl[:tr.n_rounds]
         return out, st.as_dict(), tdict
+
+
+def tree_mask(tree: OrcTree) -> np.ndarray:
+    n = tree.n_nodes + 1
+    out = np.zeros(n * n, dtype=np.int32)
+    _check(lib().orc_tree_mask(ctypes.byref(tree), _ptr(out)), "orc_tree_mask")
+    return out.reshape(n, n)
+
+
+def _tree_frame(self, tree: OrcTree, f, c0: int, uni, trace: bool = False, probe=None, logits: bool = False):
+    """Speculative frame with sparse-tree drafting. Returns (codes, stats, trace dict or None)."""
+    f = np.ascontiguousarray(f, dtype=np.float32)
+    u = np.ascontiguousarray(uni, dtype=np.float32)
+    out = np.zeros(self.n, dtype=np.int32)
+    st = OrcStats()
+    tr_p = None
+    if trace:
+        rounds = (OrcTreeRound * MAX_ROUNDS)()
+        vl = dl = None
+        if logits:
+            vl = np.zeros((MAX_ROUNDS, MAX_TREE + 1, self.V), dtype=np.float64)
+            dl = np.zeros((MAX_ROUNDS, TRACE_ROWS, self.V), dtype=np.float64)
+        tr = OrcTreeTrace(rounds, vl.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if logits else None,
+                          dl.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if logits else None, MAX_ROUNDS, 0)
+        tr_p = ctypes.byref(tr)
+    cb = PROBE_FN(probe) if probe is not None else PROBE_FN()
+    _check(lib().orc_tree_frame(self._h, ctypes.byref(tree), _ptr(f), int(c0), _ptr(u), _ptr(out), ctypes.byref(st),
+                                tr_p, cb, None), "orc_tree_frame")
+    tdict = None
+    if trace:
+        rs = []
+        for i in range(tr.n_rounds):
+            r = rounds[i]
+            rs.append(dict(m=r.m, depth=r.depth, n_rows=r.n_rows, n_cand=r.n_cand, m_new=r.m_new,
+                           accepted=r.accepted, token=r.token, tokens=list(r.tokens[:max(r.n_cand, r.n_rows)]), path=list(r.path[:r.accepted]), margin=r.margin,
+                           topk_gap=r.topk_gap))
+        tdict = {"rounds": rs}
+        if logits:
+            tdict["verify_logits"] = vl[:tr.n_rounds]
+            tdict["draft_logits"] = dl[:tr.n_rounds]
+    return out, st.as_dict(), tdict
+
+
+def _tree_hidden(self, tree: OrcTree, f, committed, tokens) -> np.ndarray:
+    """Hidden states of the packed rows: committed = c_0..c_m, tokens = tokens of rows 1..R-1."""
+    f = np.ascontiguousarray(f, dtype=np.float32)
+    cm = np.ascontiguousarray(np.asarray(committed, dtype=np.int32))
+    tk = np.ascontiguousarray(np.asarray([0] + list(tokens), dtype=np.int32))
+    n_rows = tk.size
+    out = np.zeros((n_rows, self.H), dtype=np.float64)
+    _check(lib().orc_tree_hidden(self._h, ctypes.byref(tree), _ptr(f), _ptr(cm), cm.size - 1, _ptr(tk), n_rows,
+                                 _ptr(out)), "orc_tree_hidden")
+    return out
+
+
+Oracle.tree_frame = _tree_frame
+Oracle.tree_hidden = _tree_hidden
 
 
 def topk_softmax(logits, topk: int, temperature: float):

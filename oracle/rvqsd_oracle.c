@@ -710,6 +710,275 @@ int32_t orc_spec_frame(orc_model* m, const float* frame_hidden, int32_t c0, cons
   return st;
 }
 
+/* ------------------------------------------------------ sparse-tree frames */
+
+/* depth of every packed row; ORC_EINVAL unless parents precede their children, the
+ * packing is breadth-first (depth never decreases) and siblings have distinct ranks */
+static int32_t tree_depths(const orc_tree* t, int* depth) {
+  if (!t || t->n_nodes < 0 || t->n_nodes > ORC_MAX_TREE) return ORC_EINVAL;
+  depth[0] = 0;
+  for (int r = 1; r <= t->n_nodes; ++r) {
+    const int pr = t->parent[r];
+    if (pr < 0 || pr >= r || t->rank[r] < 0) return ORC_EINVAL;
+    depth[r] = depth[pr] + 1;
+    if (depth[r] < depth[r - 1] || depth[r] > MAX_POS - 1) return ORC_EINVAL;
+    for (int q = 1; q < r; ++q)
+      if (t->parent[q] == pr && t->rank[q] == t->rank[r]) return ORC_EINVAL;
+  }
+  return ORC_OK;
+}
+
+int32_t orc_tree_mask(const orc_tree* t, int32_t* mask) {
+  int depth[ORC_MAX_TREE + 1];
+  if (!mask || tree_depths(t, depth) != ORC_OK) return ORC_EINVAL;
+  const int n = t->n_nodes + 1;
+  for (int i = 0; i < n; ++i) {
+    for (int j = 0; j < n; ++j) mask[i * n + j] = 0;
+    /* row i, then its parent, up to the root */
+    for (int a = i;; a = t->parent[a]) {
+      mask[i * n + a] = 1;
+      if (a == 0) break;
+    }
+  }
+  return ORC_OK;
+}
+
+int32_t orc_tree_hidden(orc_model* m, const orc_tree* t, const float* frame_hidden, const int32_t* committed,
+                        int32_t m_anchor, const int32_t* tokens, int32_t n_rows, double* hrows) {
+  int depth[ORC_MAX_TREE + 1];
+  if (!m || !frame_hidden || !committed || !hrows || n_rows < 1 || tree_depths(t, depth) != ORC_OK ||
+      n_rows > t->n_nodes + 1 || m_anchor < 0 || (n_rows > 1 && !tokens))
+    return ORC_EINVAL;
+  const int H = m->cfg.hidden;
+  if (m_anchor + 1 + depth[n_rows - 1] > m->cfg.n_codes) return ORC_EINVAL;
+  int done[ORC_MAX_TREE + 1] = {0};
+  double* h = (double*)malloc(sizeof(double) * (MAX_POS + 1) * H);
+  if (!h) return ORC_ENOMEM;
+  int32_t st = ORC_OK;
+  /* each row's hidden state is the causal forward over its own path: the committed
+   * codes c_0..c_m, then the tokens of its ancestors and itself; one forward per
+   * leaf of the rows serves every row on that leaf's path */
+  for (int r = n_rows - 1; r >= 0 && st == ORC_OK; --r) {
+    if (done[r]) continue;
+    int path[MAX_POS];
+    int np = 0;
+    for (int a = r; a != 0; a = t->parent[a]) path[np++] = a;  /* r, parent, ..., depth-1 row */
+    int32_t in[MAX_POS];
+    for (int s = 0; s <= m_anchor; ++s) in[s] = committed[s];
+    for (int d = 1; d <= np; ++d) in[m_anchor + d] = tokens[path[np - d]];
+    st = orc_forward(m, frame_hidden, in, m_anchor + 2 + np, h);
+    if (st != ORC_OK) break;
+    memcpy(hrows, h + (size_t)(m_anchor + 1) * H, sizeof(double) * H);  /* the root row */
+    done[0] = 1;
+    for (int d = 1; d <= np; ++d) {
+      const int row = path[np - d];
+      memcpy(hrows + (size_t)row * H, h + (size_t)(m_anchor + 1 + d) * H, sizeof(double) * H);
+      done[row] = 1;
+    }
+  }
+  free(h);
+  return st;
+}
+
+/* the n largest logits' indices in ranked order: larger value first, ties to the lower index */
+static int32_t ranked_candidates(const double* logits, int32_t V, int32_t n, int32_t* out, double* gap, int32_t need) {
+  vi_t* a = (vi_t*)malloc(sizeof(vi_t) * V);
+  if (!a) return ORC_ENOMEM;
+  for (int i = 0; i < V; ++i) {
+    a[i].v = isnan(logits[i]) ? -INFINITY : logits[i];
+    a[i].i = i;
+  }
+  qsort(a, (size_t)V, sizeof(vi_t), cmp_desc);
+  for (int r = 0; r < n; ++r) out[r] = a[r].i;
+  /* smallest gap between consecutive ranks among those that decide a candidate */
+  double g = INFINITY;
+  for (int r = 0; r < need && r + 1 < V; ++r)
+    if (a[r].v - a[r + 1].v < g) g = a[r].v - a[r + 1].v;
+  *gap = g;
+  free(a);
+  return n;
+}
+
+int32_t orc_tree_frame(orc_model* m, const orc_tree* t, const float* frame_hidden, int32_t c0, const float* uniforms,
+                       int32_t* out_codes, orc_stats* stats, orc_tree_trace* trace, orc_probe_fn probe,
+                       void* probe_ctx) {
+  int depth[ORC_MAX_TREE + 1];
+  if (!m || !frame_hidden || !uniforms || !out_codes || c0 < 0 || c0 >= m->cfg.vocab ||
+      tree_depths(t, depth) != ORC_OK)
+    return ORC_EINVAL;
+  const orc_cfg* c = &m->cfg;
+  const int n = c->n_codes, H = c->hidden, V = c->vocab, K = c->draft_len, N = t->n_nodes;
+  const int nsup = c->topk < V ? c->topk : V;
+  for (int r = 1; r <= N; ++r)
+    if (t->rank[r] >= nsup) return ORC_EINVAL; /* every candidate must exist in the draft's support */
+  int32_t st = ORC_OK;
+  int32_t codes[MAX_POS];
+  orc_stats S = {0, 0, 0, 0, 0};
+  dctx_t dc = {probe, probe_ctx, INFINITY};
+  double* hfin = (double*)malloc(sizeof(double) * (n + 1) * H);
+  double* hanc = (double*)malloc(sizeof(double) * H);
+  double* hrows = (double*)malloc(sizeof(double) * (N + 1) * H);
+  double* lg = (double*)malloc(sizeof(double) * V);
+  int32_t* pidx = (int32_t*)malloc(sizeof(int32_t) * V);
+  double* pp = (double*)malloc(sizeof(double) * V);
+  double* res = (double*)malloc(sizeof(double) * V);
+  int32_t* cand = (int32_t*)malloc(sizeof(int32_t) * (MAX_POS) * nsup);
+  if (!hfin || !hanc || !hrows || !lg || !pidx || !pp || !res || !cand) st = ORC_ENOMEM;
+  double gap = INFINITY;
+  codes[0] = c0;
+  int m_anchor = 0;
+  orc_tree_round* rec = NULL;
+  const size_t TR = ORC_MAX_TREE + 1;
+
+  /* prefix pass: positions 0 (frame hidden) and 1 (E_0[c_0]); c_1 from p_1 */
+  if (st == ORC_OK) st = orc_forward(m, frame_hidden, codes, 2, hfin);
+  if (st == ORC_OK) st = orc_logits(m, hfin + H, 1, 0, lg);
+  if (st == ORC_OK) {
+    S.target_calls = 1;
+    if (trace && trace->rounds && trace->n_rounds < trace->max_rounds) {
+      rec = &trace->rounds[trace->n_rounds];
+      memset(rec, 0, sizeof(*rec));
+      rec->n_rows = 2;
+      rec->token = -1;
+      rec->tokens[0] = c0;
+      if (trace->verify_logits) memcpy(trace->verify_logits + (size_t)trace->n_rounds * TR * V, lg, sizeof(double) * V);
+    }
+    int32_t k = topk_softmax_gap(lg, V, c->topk, c->temperature, pidx, pp, &gap);
+    if (k < 0) st = k;
+    else {
+      dc.margin = INFINITY;
+      codes[1] = sample_dist(pidx, pp, k, U(uniforms, 1, 2), &dc, 2);
+      m_anchor = 1;
+      memcpy(hanc, hfin + H, sizeof(double) * H);
+      if (rec) { rec->m_new = 1; rec->token = codes[1]; rec->margin = dc.margin; rec->topk_gap = gap; trace->n_rounds++; }
+    }
+  }
+
+  while (st == ORC_OK && m_anchor < n) {
+    const int mm = m_anchor;
+    const int kp = K < n - mm ? K : n - mm;
+    /* candidates: nodes down to depth K'; packed rows: those whose position m + 1 + depth is a
+     * code position (a candidate for position n_codes is verified but consumed by no row) */
+    int n_cand = 1;
+    while (n_cand <= N && depth[n_cand] <= kp) ++n_cand;
+    int n_rows = 1;
+    while (n_rows < n_cand && mm + 1 + depth[n_rows] <= n) ++n_rows;
+    dc.margin = INFINITY;
+    double round_gap = INFINITY;
+    rec = NULL;
+    if (trace && trace->rounds && trace->n_rounds < trace->max_rounds) {
+      rec = &trace->rounds[trace->n_rounds];
+      memset(rec, 0, sizeof(*rec));
+      rec->m = mm; rec->depth = kp; rec->n_rows = n_rows; rec->n_cand = n_cand; rec->token = -1;
+    }
+    /* draft candidates of every depth, from the anchor's hidden state plus b_d */
+    int max_rank[MAX_POS];
+    for (int d = 0; d < MAX_POS; ++d) max_rank[d] = -1;
+    for (int r = 1; r < n_cand; ++r)
+      if (t->rank[r] > max_rank[depth[r]]) max_rank[depth[r]] = t->rank[r];
+    for (int d = 1; d <= kp && st == ORC_OK; ++d) {
+      st = orc_logits(m, hanc, mm + d, d, lg);
+      if (st != ORC_OK) break;
+      if (rec && trace->draft_logits)
+        memcpy(trace->draft_logits + ((size_t)trace->n_rounds * 16 + (d - 1)) * V, lg, sizeof(double) * V);
+      double g;
+      const int32_t k = ranked_candidates(lg, V, nsup, cand + (size_t)d * nsup, &g, max_rank[d] + 1);
+      if (k < 0) { st = k; break; }
+      if (max_rank[d] >= 0 && g < round_gap) round_gap = g;
+    }
+    if (st != ORC_OK) break;
+    int32_t tokens[ORC_MAX_TREE + 1];
+    tokens[0] = codes[mm];
+    for (int r = 1; r < n_cand; ++r) tokens[r] = cand[(size_t)depth[r] * nsup + t->rank[r]];
+    if (rec) memcpy(rec->tokens, tokens, sizeof(int32_t) * n_cand);
+    /* verification: every packed row's hidden state under the ancestor mask */
+    st = orc_tree_hidden(m, t, frame_hidden, codes, mm, tokens, n_rows, hrows);
+    if (st != ORC_OK) break;
+    S.target_calls++;
+    S.rounds++;
+    S.drafted += n_cand - 1;
+    if (rec && trace->verify_logits)
+      for (int r = 0; r < n_rows && st == ORC_OK; ++r) {
+        st = orc_logits(m, hrows + (size_t)r * H, mm + 1 + depth[r], 0, lg);
+        memcpy(trace->verify_logits + ((size_t)trace->n_rounds * TR + r) * V, lg, sizeof(double) * V);
+      }
+    if (st != ORC_OK) break;
+    /* walk from the root: children tried in increasing rank under p of the current row */
+    int cur = 0, s = mm + 1, acc = 0, m_new = -1;
+    while (st == ORC_OK) {
+      st = orc_logits(m, hrows + (size_t)cur * H, s, 0, lg);
+      if (st != ORC_OK) break;
+      const int32_t k = topk_softmax_gap(lg, V, c->topk, c->temperature, pidx, pp, &gap);
+      if (k < 0) { st = k; break; }
+      if (gap < round_gap) round_gap = gap;
+      int kids[ORC_MAX_TREE];
+      int nk = 0;
+      for (int r = cur + 1; r < n_cand; ++r)
+        if (t->parent[r] == cur) {
+          int at = nk++;
+          while (at > 0 && t->rank[kids[at - 1]] > t->rank[r]) { kids[at] = kids[at - 1]; --at; }
+          kids[at] = r;
+        }
+      int taken = -1;
+      if (nk > 0) {
+        const double u = U(uniforms, s, 1);
+        double bps[ORC_MAX_TREE];
+        int nb = 0;
+        double cum = 0.0;
+        for (int i = 0; i < nk; ++i) {
+          cum += prob_of(pidx, pp, k, tokens[kids[i]]);
+          if (cum < 1.0) bps[nb++] = cum;
+          if (fabs(u - cum) < dc.margin) dc.margin = fabs(u - cum);
+          if (taken < 0 && u < cum) taken = kids[i];
+        }
+        if (dc.fn) dc.fn(dc.ctx, (s - 1) * 3 + 1, bps, nb);
+      }
+      if (taken >= 0) {
+        codes[s] = tokens[taken];
+        S.accept_mask |= 1u << s;
+        if (rec) rec->path[acc] = taken;
+        ++acc;
+        cur = taken;
+        ++s;
+        if (s > n) { m_new = n; break; }
+        continue;
+      }
+      /* no child accepted: the residual p without the children's tokens (p itself if empty) */
+      double rs = 0.0;
+      for (int j = 0; j < k; ++j) {
+        int is_kid = 0;
+        for (int i = 0; i < nk; ++i) is_kid |= tokens[kids[i]] == pidx[j];
+        res[j] = is_kid ? 0.0 : pp[j];
+        rs += res[j];
+      }
+      if (!(rs > 0.0))
+        for (int j = 0; j < k; ++j) res[j] = pp[j];
+      codes[s] = sample_dist(pidx, res, k, U(uniforms, s, 2), &dc, (s - 1) * 3 + 2);
+      if (rec) rec->token = codes[s];
+      m_new = s;
+      break;
+    }
+    if (st != ORC_OK) break;
+    S.accepted += acc;
+    /* the next anchor's hidden state: the row that produced c_{m_new} */
+    if (m_new < n) memcpy(hanc, hrows + (size_t)cur * H, sizeof(double) * H);
+    if (rec) {
+      rec->m_new = m_new;
+      rec->accepted = acc;
+      rec->margin = dc.margin;
+      rec->topk_gap = round_gap;
+      trace->n_rounds++;
+    }
+    m_anchor = m_new;
+  }
+  if (st == ORC_OK) {
+    for (int s2 = 1; s2 <= n; ++s2) out_codes[s2 - 1] = codes[s2];
+    if (stats) *stats = S;
+  }
+  free(hfin); free(hanc); free(hrows); free(lg); free(pidx); free(pp); free(res); free(cand);
+  return st;
+}
+
 /* ------------------------------------------------------------- uniforms */
 
 uint64_t orc_splitmix64_at(uint64_t seed, uint64_t n) {

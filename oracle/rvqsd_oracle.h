@@ -118,6 +118,58 @@ int32_t orc_spec_frame(orc_model* m, const float* frame_hidden, int32_t c0, cons
                        int32_t* out_codes, orc_stats* stats, orc_trace* trace,
                        orc_probe_fn probe, void* probe_ctx);
 
+/* ---- Sparse-tree verification (Sec. 2.2, "Tree attention increases acceptance rate",
+ * Fig. 2) ----
+ * A tree of N draft nodes is packed with the committed token's row (the root, row 0)
+ * into one query of N + 1 rows, rows 1..N in breadth-first order (depth never
+ * decreases). Row r >= 1 holds the token of rank rank[r] among the draft candidates of
+ * its depth d: the top-ranked support of q_{m+d} = topk-softmax(LMH_{m+d}(h_m + b_d) / T),
+ * shared by every node of that depth. Row r sits at position m + 1 + depth(r) and
+ * attends to the committed prefix and to its ancestors (and itself) only.
+ * Verification walks the tree from the root: at a node at position s, its children
+ * (in increasing rank) are tried in turn under p_s = topk-softmax(LMH_s(h_node) / T),
+ * child i accepted iff sum_{l < i} p(x_l) <= u_acc[s] < sum_{l <= i} p(x_l) (the
+ * standard rule with a point-mass draft per candidate, each rejection leaving the
+ * residual p without that candidate); when no child is accepted, c_s is drawn with
+ * u_samp[s] from p with every child's token removed (p itself when nothing is left). */
+#define ORC_MAX_TREE 80
+typedef struct {
+  int32_t n_nodes;                     /* N <= ORC_MAX_TREE */
+  int32_t parent[ORC_MAX_TREE + 1];    /* parent row of row r (r >= 1), 0 = the root; parent[r] < r */
+  int32_t rank[ORC_MAX_TREE + 1];      /* rank of row r's token among its depth's candidates */
+} orc_tree;
+
+typedef struct {
+  int32_t m, depth, n_rows, m_new;     /* depth: deepest level drafted this round (K'); n_rows: packed
+                                        * rows computed (a candidate at position n_codes + 1 has none) */
+  int32_t n_cand;                      /* root + candidate nodes of the round (depth <= K') */
+  int32_t accepted, token;             /* accepted nodes; committed residual / bonus / prefix token (-1 none) */
+  int32_t tokens[ORC_MAX_TREE + 1];    /* token consumed by each packed row (row 0: c_m) */
+  int32_t path[16];                    /* accepted rows, depth 1 .. accepted */
+  double margin, topk_gap;
+} orc_tree_round;
+
+typedef struct {
+  orc_tree_round* rounds;
+  double* verify_logits;  /* nullable, [max_rounds][ORC_MAX_TREE + 1][vocab]: LMH_{pos(r)}(h_r) of packed row r */
+  double* draft_logits;   /* nullable, [max_rounds][16][vocab]: d-1 = LMH_{m+d}(h_m + b_d) */
+  int32_t max_rounds;
+  int32_t n_rounds;
+} orc_tree_trace;
+
+/* Ancestor mask of the packed query: mask[i][j] = 1 iff row j is row i or an ancestor
+ * of it. mask: [(N+1)*(N+1)]. Returns ORC_EINVAL for a tree that is not in packed form. */
+int32_t orc_tree_mask(const orc_tree* t, int32_t* mask);
+/* Final-normed hidden states of the packed rows for committed codes c_0..c_m
+ * (committed[0..m]) and row tokens tokens[1..n_rows-1]: row r at position
+ * m + 1 + depth(r) over its own path (the mask's definition). hrows: [n_rows][H]. */
+int32_t orc_tree_hidden(orc_model* m, const orc_tree* t, const float* frame_hidden, const int32_t* committed,
+                        int32_t m_anchor, const int32_t* tokens, int32_t n_rows, double* hrows);
+/* Speculative frame with tree drafting (draft_len = the deepest level K). */
+int32_t orc_tree_frame(orc_model* m, const orc_tree* t, const float* frame_hidden, int32_t c0, const float* uniforms,
+                       int32_t* out_codes, orc_stats* stats, orc_tree_trace* trace, orc_probe_fn probe,
+                       void* probe_ctx);
+
 /* Uniforms from a 64-bit seed with SplitMix64 (Steele, Lea, Flood 2014): the
  * (n+1)-th output of the generator seeded with `seed` gives uniform n, as its
  * top 24 bits times 2^-24. out: [n_codes][3]. */

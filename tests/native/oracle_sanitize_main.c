@@ -108,6 +108,24 @@ int main(int argc, char** argv) {
     T.max_rounds = 2;
     EXPECT(orc_spec_frame(m, f, c0, uni, codes, &S, &T, NULL, NULL) == ORC_OK, "trace shorter than the frame");
     EXPECT(orc_spec_frame(m, f, c0, uni, codes, NULL, NULL, NULL, NULL) == ORC_OK, "untraced frame");
+    if (mode == 0 && c.draft_len >= 2 && c.topk >= 2) {
+      /* the sparse tree of Fig. 2 (depth 3 is cut to the draft length) */
+      orc_tree t;
+      memset(&t, 0, sizeof(t));
+      const int par[8] = {0, 0, 1, 1, 2, 3, 5, 5}, rk[8] = {0, 1, 0, 1, 0, 0, 0, 1};
+      t.n_nodes = 8;
+      for (int r = 1; r <= 8; ++r) { t.parent[r] = par[r - 1]; t.rank[r] = rk[r - 1]; }
+      int32_t mask[81];
+      EXPECT(orc_tree_mask(&t, mask) == ORC_OK && mask[8 * 9 + 5] == 1 && mask[8 * 9 + 3] == 0, "tree mask");
+      orc_tree_round tr[16];
+      double* tv = (double*)malloc(sizeof(double) * 16 * (ORC_MAX_TREE + 1) * V);
+      orc_tree_trace TT = {tr, tv, tl, 16, 0};
+      EXPECT(orc_tree_frame(m, &t, f, c0, uni, codes, &S, &TT, NULL, NULL) == ORC_OK, "tree frame, traced");
+      EXPECT(orc_tree_frame(m, &t, f, c0, uni, codes, &S, NULL, NULL, NULL) == ORC_OK, "tree frame, untraced");
+      t.parent[2] = 2;
+      EXPECT(orc_tree_frame(m, &t, f, c0, uni, codes, &S, NULL, NULL, NULL) == ORC_EINVAL, "malformed tree rejected");
+      free(tv);
+    }
     orc_destroy(m);
   }
   float u2[45];
