@@ -139,6 +139,33 @@ rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out);
 rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, rvqsd_stream** out);
 void rvqsd_stream_destroy(rvqsd_stream* s);
 
+/* Create a decode stream that verifies a sparse draft tree instead of a chain
+ * (Sec. 2.2, "Tree attention increases acceptance rate", Fig. 2). Each round
+ * drafts, for every depth d <= min(draft_len, codes left), the candidates of
+ * q_{m+d} = topk-softmax(LMH_{m+d}(h_m + b_d) / T) ranked by logit (ties to the
+ * lower token); the tree's nodes take the candidates of their depth by rank,
+ * shared by every parent. The committed token's row (the root) and the nodes
+ * form one query, each row attending to the committed prefix and to its
+ * ancestors only; the nodes' children are tried in increasing rank under the
+ * target distribution of their parent's row (child i accepted iff
+ * sum_{l<i} p(x_l) <= u_accept < sum_{l<=i} p(x_l)), and with none accepted the
+ * code is drawn with u_sample from p without the children's tokens. The output
+ * distribution stays that of plain top-k sampling.
+ * Tree (host arrays, length n_nodes, rows 1..n_nodes of the packed query):
+ * parents[i] = parent row of row i+1 (0 = the root, always an earlier row),
+ * ranks[i] = candidate rank of row i+1's token (< min(topk, vocab)); rows are
+ * packed breadth first (depth never decreases), siblings have distinct ranks,
+ * depth <= draft_len. lanes (1..16) frames are decoded together by the batched
+ * calls (lanes * (n_nodes + 1) <= 80 rows); the single-frame calls run one frame
+ * through the same kernel. Batched traces use round records of 128 ints
+ * ([0..7] as a chain round, [8] candidate rows, [16..) accepted rows,
+ * [32..) candidate tokens) and logit slots r (verify row r) and
+ * max(16, n_nodes + 1) + r*draft_len + j - 1 (draft row (r, j)). Needs bf16
+ * weights and the batched stream's shape limits; EINVAL for a malformed tree,
+ * EUNSUPPORTED when the rows or their LDS do not fit. */
+rvqsd_status rvqsd_tree_stream_create(rvqsd_model* m, void* hip_stream, int32_t lanes, int32_t n_nodes,
+                                      const int32_t* parents, const int32_t* ranks, rvqsd_stream** out);
+
 /* Decode one frame (host pointers, synchronous): frame_hidden float[hidden],
  * c0 in [0, vocab), uniforms expanded from rng_seed with SplitMix64 (see
  * rvqsd_uniforms_from_seed). Writes out_codes[n_codes] (codes c_1..c_n) and

@@ -90,6 +90,7 @@ struct rvqsd_stream {
   size_t tag_begin, tag_end;  // byte range of dbuf holding the tagged words
   // batched path (max_streams > 1)
   int lanes;            // frame streams decoded together
+  int tree;             // 1: every lane verifies a sparse draft tree (the batched kernel's tree rows)
   void* bbuf;           // batched work buffers; the barrier, status and totals words come first
   size_t bsync_bytes;   // bytes of those words (cleared before every launch)
   BParams bp;           // host copy of the batched parameter block
@@ -194,11 +195,52 @@ int pick_ks(int K, int kw, int colgroups, int nwg) {
 }
 
 // Work buffers and parameter block of the batched kernel.
-int batch_setup(rvqsd_stream* s, int lanes) {
+// Validate a packed draft tree (rows 1..n of the query; row 0 is the committed token's row)
+// and fill the tree fields of b.
+int tree_setup(BParams& b, const rvqsd_cfg& c, int n, const int32_t* parents, const int32_t* ranks) {
+  if (n < 1 || n > kMaxTreeRows - 1 || !parents || !ranks)
+    return set_err(RVQSD_EINVAL, "a tree needs 1..%d nodes and its parents and ranks", kMaxTreeRows - 1);
+  const int nsup = c.topk < c.vocab ? c.topk : c.vocab;
+  b.tree = 1;
+  b.tree_nodes = n;
+  b.t_depth[0] = 0;
+  for (int r = 1; r <= n; ++r) {
+    const int pr = parents[r - 1], rk = ranks[r - 1];
+    if (pr < 0 || pr >= r) return set_err(RVQSD_EINVAL, "node %d: parent %d is not an earlier row", r, pr);
+    if (rk < 0 || rk >= nsup) return set_err(RVQSD_EINVAL, "node %d: rank %d outside the top-%d candidates", r, rk, nsup);
+    b.t_parent[r] = pr;
+    b.t_rank[r] = rk;
+    b.t_depth[r] = b.t_depth[pr] + 1;
+    if (b.t_depth[r] < b.t_depth[r - 1])
+      return set_err(RVQSD_EINVAL, "node %d: rows must be packed breadth first (depth never decreases)", r);
+    if (b.t_depth[r] > c.draft_len)
+      return set_err(RVQSD_EINVAL, "node %d at depth %d: deeper than draft_len %d", r, b.t_depth[r], c.draft_len);
+    for (int q = 1; q < r; ++q)
+      if (b.t_parent[q] == pr && b.t_rank[q] == rk) return set_err(RVQSD_EINVAL, "nodes %d and %d: same parent and rank", q, r);
+    if (b.t_need[b.t_depth[r]] < rk + 1) b.t_need[b.t_depth[r]] = rk + 1;
+  }
+  for (int r = 0; r <= n; ++r) {
+    b.t_anc[r][0] = b.t_anc[r][1] = 0;
+    for (int a = r;; a = b.t_parent[a]) {
+      b.t_anc[r][a >> 6] |= 1ull << (a & 63);
+      if (a == 0) break;
+    }
+  }
+  return RVQSD_OK;
+}
+
+int batch_setup(rvqsd_stream* s, int lanes, int tree_n = 0, const int32_t* parents = nullptr,
+                const int32_t* ranks = nullptr) {
   const rvqsd_model* m = s->m;
   const KParams& k = s->kp;
   const rvqsd_cfg& c = m->cfg;
-  const int rpl = c.draft_len + 1 < 2 ? 2 : c.draft_len + 1;
+  BParams b;
+  memset(&b, 0, sizeof(b));
+  if (tree_n) {
+    const int st = tree_setup(b, c, tree_n, parents, ranks);
+    if (st) return st;
+  }
+  const int rpl = tree_n ? tree_n + 1 : (c.draft_len + 1 < 2 ? 2 : c.draft_len + 1);
   const int M = lanes * rpl;
   if (c.dtype != RVQSD_DTYPE_BF16) return set_err(RVQSD_EUNSUPPORTED, "batched streams need bf16 weights");
   if (M > kBatchMaxRows)
@@ -206,9 +248,10 @@ int batch_setup(rvqsd_stream* s, int lanes) {
   if (k.H % 512 || k.qdim % 256 || k.F % 256 || k.H > 2048)
     return set_err(RVQSD_EUNSUPPORTED, "batched streams need hidden %% 512 == 0 (<= 2048), q width and ffn %% 256 == 0");
   if (m->nwg < 8) return set_err(RVQSD_EUNSUPPORTED, "batched streams need at least 8 workgroups");
-  BParams b;
-  memset(&b, 0, sizeof(b));
   b.lanes = lanes;
+  b.kv_slots = tree_n ? kMaxPos + rpl : kMaxPos;
+  b.slot_draft0 = rpl > kSlotDraft0 ? rpl : kSlotDraft0;
+  b.tr_slots = tree_n ? b.slot_draft0 + rpl * k.K : kSlotDraft0 + kMaxRows * k.K;
   b.rpl = rpl;
   b.M = M;
   b.nwg = m->nwg;
@@ -233,7 +276,7 @@ int batch_setup(rvqsd_stream* s, int lanes) {
   const size_t sync_bytes = off;
   const size_t o_lane = take((size_t)lanes * kLaneInts * 4), o_x = take((size_t)M * k.H * 4),
                o_a = take(2 * (size_t)M * kmax * 4), o_ah = take((size_t)b.hrows * k.H * 4),
-               o_part = take(part * 4), o_kv = take((size_t)lanes * k.L * k.nkv * kMaxPos * 2 * k.d * 4),
+               o_part = take(part * 4), o_kv = take((size_t)lanes * k.L * k.nkv * b.kv_slots * 2 * k.d * 4),
                o_log = take((size_t)b.hrows * k.V * 4), o_vres = take((size_t)lanes * rpl * 4),
                o_drec = take((size_t)2 * lanes * rpl * kd * b.sup_words * 8), o_bp = take(sizeof(BParams));
   hipError_t e = dev_alloc(&s->bbuf, off);
@@ -268,12 +311,21 @@ int batch_setup(rvqsd_stream* s, int lanes) {
   }
   // LDS: projection tiles and the SiLU staging, attention rows, sampling arrays, one row
   size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
-  const size_t attn = (size_t)(2 * kMaxRows + 2 * kMaxPos) * k.d * 4;
+  const size_t attn = tree_n ? ((size_t)rpl * k.d + (size_t)b.kv_slots * 2 * k.d + (size_t)kWaves * b.kv_slots) * 4
+                             : (size_t)(2 * kMaxRows + 2 * kMaxPos) * k.d * 4;
   const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + 3 * kMaxTopk * 8 + kMaxTopk * 4 + kTopkBuckets * 4;
   if (attn > lds) lds = attn;
   if (samp > lds) lds = samp;
   if ((size_t)k.H * 4 > lds) lds = (size_t)k.H * 4;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, m->device) == hipSuccess && lds + 64 + 16384 > (size_t)prop.sharedMemPerBlock) {
+    (void)hipFree(s->bbuf);
+    s->bbuf = nullptr;
+    return set_err(RVQSD_EUNSUPPORTED, "the batched kernel needs %zu bytes of LDS (tree of %d rows), %zu available",
+                   lds + 64, rpl, (size_t)prop.sharedMemPerBlock);
+  }
   s->blds = lds + 64;
+  s->tree = tree_n ? 1 : 0;
   return RVQSD_OK;
 }
 
@@ -469,7 +521,21 @@ rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out) {
   return RVQSD_OK;
 }
 
+static rvqsd_status stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, int32_t tree_n,
+                                  const int32_t* parents, const int32_t* ranks, rvqsd_stream** out);
+
 rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, rvqsd_stream** out) {
+  return stream_create(m, hip_stream, max_streams, 0, nullptr, nullptr, out);
+}
+
+rvqsd_status rvqsd_tree_stream_create(rvqsd_model* m, void* hip_stream, int32_t lanes, int32_t n_nodes,
+                                      const int32_t* parents, const int32_t* ranks, rvqsd_stream** out) {
+  if (n_nodes < 1) return set_err(RVQSD_EINVAL, "a tree needs at least one node");
+  return stream_create(m, hip_stream, lanes, n_nodes, parents, ranks, out);
+}
+
+static rvqsd_status stream_create(rvqsd_model* m, void* hip_stream, int32_t max_streams, int32_t tree_n,
+                                  const int32_t* parents, const int32_t* ranks, rvqsd_stream** out) {
   if (!m || !out) return set_err(RVQSD_EINVAL, "null argument");
   if (max_streams < 1 || max_streams > kMaxLanes) return set_err(RVQSD_EINVAL, "max_streams must be 1..%d", kMaxLanes);
   *out = nullptr;
@@ -529,8 +595,8 @@ rvqsd_status rvqsd_stream_create(rvqsd_model* m, void* hip_stream, int32_t max_s
   s->epoch_step = frame_epoch_step(k.L);
   s->epoch = s->epoch_step;
   s->lanes = 1;
-  if (max_streams > 1) {
-    const int st = batch_setup(s, max_streams);
+  if (max_streams > 1 || tree_n > 0) {
+    const int st = batch_setup(s, max_streams, tree_n, parents, ranks);
     if (st != RVQSD_OK) {
       (void)hipHostFree(s->h_in);
       (void)hipHostFree(s->h_out);
@@ -607,12 +673,14 @@ rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidd
                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats) {
   if (!s || !d_frame_hidden || !d_c0 || !d_uniforms || !d_out_codes || !d_stats)
     return set_err(RVQSD_EINVAL, "null argument");
+  if (s->tree) return rvqsd_decode_frames_batched_async(s, 1, d_frame_hidden, d_c0, d_uniforms, d_out_codes, d_stats);
   return launch_one(s, d_frame_hidden, d_c0, d_uniforms, d_out_codes, d_stats);
 }
 
 rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, int32_t c0, const float* uniforms,
                                   int32_t* out_codes, rvqsd_stats* out_stats) {
   if (!s || !frame_hidden || !uniforms || !out_codes) return set_err(RVQSD_EINVAL, "null argument");
+  if (s->tree) return rvqsd_decode_frames_batched(s, 1, frame_hidden, &c0, uniforms, out_codes, out_stats);
   const rvqsd_cfg& c = s->m->cfg;
   if (c0 < 0 || c0 >= c.vocab) return set_err(RVQSD_EINVAL, "c0 = %d outside [0, %d)", c0, c.vocab);
   const int H = c.hidden, n = c.n_codes;
@@ -650,7 +718,7 @@ rvqsd_status rvqsd_decode_frames_batched_async(rvqsd_stream* s, int32_t n, const
                                                rvqsd_stats* d_stats) {
   if (!s) return set_err(RVQSD_EINVAL, "null stream");
   if (n < 0) return set_err(RVQSD_EINVAL, "n = %d < 0", n);
-  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  if (!s->bbuf) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
   if (n == 0) return RVQSD_OK;
   if (!d_frame_hidden || !d_c0 || !d_uniforms || !d_out_codes || !d_stats) return set_err(RVQSD_EINVAL, "null argument");
   HIPCHK(hipMemsetAsync(s->bbuf, 0, s->bsync_bytes, s->stream));
@@ -671,7 +739,7 @@ rvqsd_status rvqsd_decode_frames_batched(rvqsd_stream* s, int32_t n, const float
                                          const float* uniforms, int32_t* out_codes, rvqsd_stats* out_stats) {
   if (!s) return set_err(RVQSD_EINVAL, "null stream");
   if (n < 0) return set_err(RVQSD_EINVAL, "n = %d < 0", n);
-  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  if (!s->bbuf) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
   if (n == 0) return RVQSD_OK;
   if (!frame_hidden || !c0 || !uniforms || !out_codes) return set_err(RVQSD_EINVAL, "null argument");
   const rvqsd_cfg& c = s->m->cfg;
@@ -726,14 +794,13 @@ rvqsd_status rvqsd_decode_frames_batched(rvqsd_stream* s, int32_t n, const float
 rvqsd_status rvqsd_set_batch_trace(rvqsd_stream* s, float* logits, int32_t* rounds, int32_t max_rounds,
                                    int32_t max_frames) {
   if (!s) return set_err(RVQSD_EINVAL, "null stream");
-  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  if (!s->bbuf) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
   const bool on = logits || rounds;
   if (on && (max_rounds < 1 || max_frames < 1)) return set_err(RVQSD_EINVAL, "max_rounds and max_frames must be >= 1");
   s->bp.tr_logits = on ? logits : nullptr;
   s->bp.tr_rounds = on ? rounds : nullptr;
   s->bp.tr_max_rounds = on ? max_rounds : 0;
   s->bp.tr_frames = on ? max_frames : 0;
-  s->bp.tr_slots = kSlotDraft0 + kMaxRows * s->m->cfg.draft_len;
   HIPCHK(hipStreamSynchronize(s->stream));
   HIPCHK(hipMemcpy(s->dbp, &s->bp, sizeof(BParams), hipMemcpyHostToDevice));
   return RVQSD_OK;
@@ -741,7 +808,7 @@ rvqsd_status rvqsd_set_batch_trace(rvqsd_stream* s, float* logits, int32_t* roun
 
 rvqsd_status rvqsd_batch_totals(rvqsd_stream* s, uint64_t* passes, uint64_t* bytes) {
   if (!s || !passes || !bytes) return set_err(RVQSD_EINVAL, "null argument");
-  if (s->lanes < 2) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
+  if (!s->bbuf) return set_err(RVQSD_EUNSUPPORTED, "the stream was created with max_streams = 1");
   unsigned long long t[2];
   HIPCHK(hipStreamSynchronize(s->stream));
   HIPCHK(hipMemcpy(t, s->bp.totals, sizeof(t), hipMemcpyDeviceToHost));

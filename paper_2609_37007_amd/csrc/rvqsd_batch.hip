@@ -132,9 +132,14 @@ struct BShared {
   int hl_n, hl_t;                // LM-head row list of the current unit
   int hl_row[kBatchMaxRows];
   float red[kWaves];
-  int vr[kMaxRows];              // commit: verdicts of the lane's rows
-  int dt[kMaxRows][kMaxCodes];   // commit: draft tokens of every row of the lane
+  int vr[kBatchMaxRows];         // commit: verdicts of the lane's rows
+  int dt[kMaxRows][kMaxCodes];   // commit: draft tokens of every row of the lane (chain lanes)
   int tok;
+  // tree lanes
+  int kid[kMaxTreeRows];         // sampling: children of the row, in increasing rank
+  int nkid;
+  int c_mnew, c_arow, c_acc, c_m;  // commit: new anchor position and row, accepted nodes, old anchor
+  int c_path[kMaxCodes + 1];     // commit: accepted rows, depth 1 .. c_acc
 };
 
 // ------------------------------------------------------------ grid barrier
@@ -202,19 +207,30 @@ constexpr int kRowChunks = 4;  // 8-element chunks per lane of a row held in reg
 
 // ------------------------------------------------------------ pass geometry
 
-__device__ __forceinline__ bool row_is_verify(const int* st, int r) {
-  return r < st[kLnRows] && st[kLnFirst] + r >= 1 && (st[kLnPass] == 0 ? r == 1 : true);
+// A lane's pass has tree rows when the stream verifies trees and the prefix pass is done;
+// the prefix pass (rows at positions 0 and 1) and chain lanes put row r at position first + r.
+__device__ __forceinline__ bool tree_rows(const BParams* bp, const int* st) { return bp->tree && st[kLnPass] > 0; }
+__device__ __forceinline__ int row_pos(const BParams* bp, const int* st, int r) {
+  return st[kLnFirst] + (tree_rows(bp, st) ? bp->t_depth[r] : r);
 }
-__device__ __forceinline__ int row_drafts(const KParams* p, const int* st, int r) {
-  const int s = st[kLnFirst] + r;
+// whether row a is row r or one of its ancestors (the rows row r attends to)
+__device__ __forceinline__ bool row_sees(const BParams* bp, const int* st, int r, int a) {
+  if (!tree_rows(bp, st)) return a <= r;
+  return (bp->t_anc[r][a >> 6] >> (a & 63)) & 1ull;
+}
+__device__ __forceinline__ bool row_is_verify(const BParams* bp, const int* st, int r) {
+  return r < st[kLnRows] && row_pos(bp, st, r) >= 1 && (st[kLnPass] == 0 ? r == 1 : true);
+}
+__device__ __forceinline__ int row_drafts(const BParams* bp, const KParams* p, const int* st, int r) {
+  const int s = row_pos(bp, st, r);
   if (r >= st[kLnRows] || s < 1 || s > p->n_codes - 1) return 0;
   if (st[kLnPass] == 0 && r != 1) return 0;
   return min(p->K, p->n_codes - s);
 }
 // LM-head input row of (lane row i, offset j) and whether it is used this pass
-__device__ __forceinline__ bool head_slot_used(const KParams* p, const int* st, int r, int j) {
+__device__ __forceinline__ bool head_slot_used(const BParams* bp, const KParams* p, const int* st, int r, int j) {
   if (!st[kLnActive]) return false;
-  return j == 0 ? row_is_verify(st, r) : j <= row_drafts(p, st, r);
+  return j == 0 ? row_is_verify(bp, st, r) : j <= row_drafts(bp, p, st, r);
 }
 
 // ------------------------------------------------------------ MFMA tile unit
@@ -382,6 +398,134 @@ __device__ void phase_gu(const BP* bp, int l, const uint32_t* A, uint32_t* Aout,
 // per-head RMSNorm and rotate-half RoPE, KV append (first q head of each kv
 // group), causal softmax attention over positions 0 .. s, output split into the
 // O projection's input.
+// Attention of lanes whose rows form a draft tree (Sec. 2.2, Fig. 2): row r sits at
+// position first + depth(r), its K/V at slot first + r, and it attends to the committed
+// positions 0 .. first - 1 and to the slots of its ancestors and itself (the prefix
+// pass: rows at positions 0 and 1, causal). One workgroup per (lane, query head); one
+// wave per row for scores, softmax and output, the scores staged in LDS.
+__device__ void phase_attn_tree(const BParams* bp, BShared* sh, int l, uint32_t* Aout, float* lds) {
+  const KParams* p = bp->k;
+  const int d = p->d, nq = p->nq, grp = nq / p->nkv, N = p->nqkv, KS = bp->ks_qkv, M = bp->M, half = d / 2;
+  const int qdim = p->qdim, kvdim = p->kvdim, lane = tid() & 63, wave = tid() >> 6, slots = bp->kv_slots;
+  const float scale = 1.f / sqrtf((float)d);
+  float* qs = lds;                          // [rpl][d]: q rows, then each row's output
+  float* kvs = qs + (size_t)bp->rpl * d;    // [slots][2][d]
+  float* wsc = kvs + (size_t)slots * 2 * d; // [kWaves][slots] scores, then softmax weights
+  const float* qn = bfw(p, boff(p, l, p->o_qn));
+  const float* kn = bfw(p, boff(p, l, p->o_kn));
+  for (int u = blockIdx.x; u < bp->lanes * nq; u += bp->nwg) {
+    const int ln = u / nq, h = u - ln * nq, g = h / grp;
+    const int* st = sh->ln[ln];
+    if (!st[kLnActive]) continue;
+    const int fp = st[kLnFirst], R = st[kLnRows], row0 = ln * bp->rpl;
+    float* kvc = bp->kv + (((size_t)ln * p->L + l) * p->nkv + g) * slots * 2 * d;
+    const int tot = R * 3 * d;
+    for (int base = 0; base < tot; base += 4 * kThreads) {
+      const float* src[4];
+      float acc[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + k * kThreads + tid();
+        const int r = e / (3 * d), w = e - r * 3 * d, part = w / d, i = w - part * d;
+        const int col = part == 0 ? h * d + i : qdim + (part - 1) * kvdim + g * d + i;
+        src[k] = e < tot ? bp->part + (size_t)(row0 + r) * N + col : nullptr;
+        acc[k] = 0.f;
+      }
+      for (int ks0 = 0; ks0 < KS; ks0 += 4) {
+        float t[4][4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            t[k][j] = (src[k] && ks0 + j < KS) ? ldf(src[k] + (size_t)(ks0 + j) * M * N) : 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (ks0 + j < KS) acc[k] += t[k][j];
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + k * kThreads + tid();
+        if (e < tot) {
+          const int r = e / (3 * d), w = e - r * 3 * d, part = w / d, i = w - part * d;
+          if (part == 0) qs[r * d + i] = acc[k];
+          else kvs[(size_t)(fp + r) * 2 * d + (part - 1) * d + i] = acc[k];
+        }
+      }
+    }
+    lds_fill<false>(kvs, kvc, fp * 2 * d, 2 * d, (size_t)2 * d);
+    __syncthreads();
+    // q rows (v < R) and k rows (v >= R): norm + RoPE at the row's position, one wave per vector
+    for (int v = wave; v < 2 * R; v += kWaves) {
+      const bool isq = v < R;
+      const int r = isq ? v : v - R, pos = row_pos(bp, st, r);
+      float* x = isq ? qs + r * d : kvs + (size_t)(fp + r) * 2 * d;
+      const float* gn = isq ? qn : kn;
+      float ss = 0.f;
+      for (int i = lane; i < d; i += 64) ss = fmaf(x[i], x[i], ss);
+      ss = wave_sum(ss);
+      const float rs = p->qk_norm ? 1.f / sqrtf(ss / (float)d + p->rms_eps) : 1.f;
+      for (int i = lane; i < half; i += 64) {
+        float a = x[i], b = x[i + half];
+        if (p->qk_norm) {
+          a = a * rs * G(gn)[i];
+          b = b * rs * G(gn)[i + half];
+        }
+        const float cs = G(p->rope)[(pos * half + i) * 2], sn = G(p->rope)[(pos * half + i) * 2 + 1];
+        x[i] = a * cs - b * sn;
+        x[i + half] = b * cs + a * sn;
+      }
+    }
+    __syncthreads();
+    if (h % grp == 0)
+      for (int e = tid(); e < R * 2 * d; e += kThreads) cstf(kvc + (size_t)fp * 2 * d + e, kvs[(size_t)fp * 2 * d + e]);
+    float* w = wsc + (size_t)wave * slots;
+    for (int r = wave; r < R; r += kWaves) {
+      const int nkeys = fp + R;
+      float mx = -INFINITY;
+      for (int t = 0; t < nkeys; ++t) {
+        float sc = -INFINITY;
+        if (t < fp || row_sees(bp, st, r, t - fp)) {  // wave-uniform
+          float a = 0.f;
+          for (int i = lane; i < d; i += 64) a = fmaf(qs[r * d + i], kvs[(size_t)t * 2 * d + i], a);
+          sc = wave_sum(a) * scale;
+        }
+        if (lane == 0) w[t] = sc;
+        mx = fmaxf(mx, sc);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      float z = 0.f;
+      for (int t = lane; t < nkeys; t += 64) {
+        const float e = expf(w[t] - mx);
+        w[t] = e;
+        z += e;
+      }
+      z = wave_sum(z);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      const float iz = 1.f / z;
+      for (int i = lane; i < d; i += 64) {
+        float o = 0.f;
+        for (int t = 0; t < nkeys; ++t) o = fmaf(w[t], kvs[(size_t)t * 2 * d + d + i], o);
+        qs[r * d + i] = o * iz;
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    for (int c = tid(); c < R * (d / 8); c += kThreads) {
+      const int r = c / (d / 8), q8 = c - r * (d / 8);
+      float x8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x8[e] = qs[r * d + 8 * q8 + e];
+      store_split(Aout + (size_t)(row0 + r) * qdim + h * d + 8 * q8, x8);
+    }
+    __syncthreads();
+  }
+}
+
 __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout, float* lds) {
   const KParams* p = bp->k;
   const int d = p->d, nq = p->nq, grp = nq / p->nkv, N = p->nqkv, KS = bp->ks_qkv, M = bp->M, half = d / 2;
@@ -397,7 +541,7 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
     const int* st = sh->ln[ln];
     if (!st[kLnActive]) continue;
     const int fp = st[kLnFirst], R = st[kLnRows], row0 = ln * bp->rpl;
-    float* kvc = bp->kv + (((size_t)ln * p->L + l) * p->nkv + g) * kMaxPos * 2 * d;
+    float* kvc = bp->kv + (((size_t)ln * p->L + l) * p->nkv + g) * bp->kv_slots * 2 * d;
     // q, k, v of the lane's rows: the partial sums of 4 elements x 4 splits are in flight at once
     const int tot = R * 3 * d;
     for (int base = 0; base < tot; base += 4 * kThreads) {
@@ -532,7 +676,7 @@ __device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float*
       } else {
         const float* ofs = bfw(p, p->o_offsets);
         for (int j = 0; j <= K; ++j) {
-          if (!head_slot_used(p, st, r, j)) continue;
+          if (!head_slot_used(bp, p, st, r, j)) continue;
           float y8[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) y8[e] = j == 0 ? h8[e] : h8[e] + G(ofs)[(size_t)(j - 1) * H + 8 * c + e];
@@ -565,7 +709,7 @@ __device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
         if (c < ncand) {
           const int ln = c / (rpl * (K + 1)), rem = c - ln * rpl * (K + 1), r = rem / (K + 1), j = rem - r * (K + 1);
           const int* st = sh->ln[ln];
-          use = head_slot_used(p, st, r, j) && st[kLnFirst] + r + j == t;
+          use = head_slot_used(bp, p, st, r, j) && row_pos(bp, st, r) + j == t;
         }
         int tot;
         const int pos = block_excl_scan(&sh->tk, use ? 1 : 0, &tot);
@@ -619,9 +763,9 @@ __device__ unsigned long long pass_bytes_batch(const BParams* bp, const BShared*
     if (st[kLnActive]) {
       const int first = st[kLnFirst], rows = st[kLnRows];
       for (int r = 0; r < rows; ++r) {
-        const int s = first + r;
-        if (row_is_verify(st, r)) used |= 1u << s;
-        const int nd = row_drafts(p, st, r);
+        const int s = row_pos(bp, st, r);
+        if (row_is_verify(bp, st, r)) used |= 1u << s;
+        const int nd = row_drafts(bp, p, st, r);
         for (int j = 1; j <= nd; ++j) used |= 1u << (s + j);
         b += (s == 0) ? 4ull * H : 2ull * H;
       }
@@ -659,10 +803,11 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
   for (int u = blockIdx.x; u < nslots; u += bp->nwg) {
     const int ln = u / (rpl * (K + 1)), rem = u - ln * rpl * (K + 1), r = rem / (K + 1), j = rem - r * (K + 1);
     const int* st = sh->ln[ln];
-    if (!head_slot_used(p, st, r, j)) continue;
-    const int pass = st[kLnPass], s = st[kLnFirst] + r, t = s + j;
+    if (!head_slot_used(bp, p, st, r, j)) continue;
+    const int pass = st[kLnPass], s = row_pos(bp, st, r), t = s + j;
     const float* U = call.uniforms + (size_t)st[kLnFrame] * n * 3;
-    const bool has_draft = j == 0 && pass > 0 && r + 1 <= st[kLnKp];
+    const bool tree_pass = tree_rows(bp, st);
+    const bool has_draft = !bp->tree && j == 0 && pass > 0 && r + 1 <= st[kLnKp];
     int nq = 0, dtok = -1;
     if (has_draft) {
       // q of d_t: drafted last pass from the anchor's row, offset r + 1
@@ -680,7 +825,7 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
     __syncthreads();
     if (bp->tr_logits && st[kLnFrame] < bp->tr_frames && pass < bp->tr_max_rounds) {
       // the slot layout of the single-stream trace: verify row r, then draft (r, j)
-      const int slot = j == 0 ? r : kSlotDraft0 + r * K + (j - 1);
+      const int slot = j == 0 ? r : bp->slot_draft0 + r * K + (j - 1);
       float* dst = bp->tr_logits + (((size_t)st[kLnFrame] * bp->tr_max_rounds + pass) * bp->tr_slots + slot) * V;
       for (int i = tid(); i < V; i += kThreads) dst[i] = lg[i];
     }
@@ -691,8 +836,76 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
       for (int i = tid(); i < ns; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
       if (!__any(fin) && tid() == 0) raise_status(bp, RVQSD_ENUMERIC);
     }
+    if (bp->tree && j > 0) {
+      // tree lanes: the ranked candidates of depth j for the rows of a round anchored at
+      // this row: rank = larger logit first, ties to the lower token (within the top-k
+      // support, which holds every rank below top-k)
+      const int need = min(bp->t_need[j], ns);
+      uint64_t* rec = bp->drec + ((((size_t)(pass & 1) * bp->lanes + ln) * rpl + r) * K + (j - 1)) * SW;
+      for (int i = tid(); i < ns; i += kThreads) {
+        const float v = slog[i];
+        const int x = sidx[i];
+        int rank = 0;
+        for (int k = 0; k < ns; ++k) rank += (slog[k] > v || (slog[k] == v && sidx[k] < x)) ? 1 : 0;
+        if (rank < need) cst64(rec + 1 + rank, (uint64_t)(uint32_t)x);
+      }
+      if (tid() == 0) cst64(rec, (uint64_t)(uint32_t)need);
+      __syncthreads();
+      continue;
+    }
     softmax_support(slog, ns, p->temperature, prob);
     __syncthreads();
+    if (tree_pass) {
+      // verify row of a tree: its children (rows of the next depth under it, the candidates
+      // for position s) are tried in increasing rank; child i is accepted iff
+      // sum_{l<i} p(x_l) <= u_acc < sum_{l<=i} p(x_l); with none accepted, c_s is drawn with
+      // u_samp from p without the children's tokens (p itself when nothing is left)
+      if (tid() == 0) {
+        int nk = 0;
+        const int ncand = st[kLnCandN];
+        for (int c = r + 1; c < ncand; ++c)
+          if (bp->t_parent[c] == r) {
+            int at = nk++;
+            while (at > 0 && bp->t_rank[sh->kid[at - 1]] > bp->t_rank[c]) { sh->kid[at] = sh->kid[at - 1]; --at; }
+            sh->kid[at] = c;
+          }
+        sh->nkid = nk;
+      }
+      __syncthreads();
+      if (tid() < 64) {
+        const int nk = sh->nkid;
+        const double ua = (double)U[(s - 1) * 3 + 1];
+        double cum = 0.0;
+        int taken = -1;
+        for (int c = 0; c < nk; ++c) {
+          const int x = st[kLnCand + sh->kid[c]];
+          double pc = 0.0;
+          for (int i = tid(); i < ns; i += 64)
+            if (sidx[i] == x) pc = prob[i];
+          cum += wave_sumd_dpp(pc);
+          if (taken < 0 && ua < cum) taken = sh->kid[c];
+        }
+        int tok = 0;
+        if (taken < 0) {
+          double rs = 0.0;
+          for (int i = tid(); i < ns; i += 64) {
+            bool kid = false;
+            for (int c = 0; c < nk; ++c) kid |= sidx[i] == st[kLnCand + sh->kid[c]];
+            res[i] = kid ? 0.0 : prob[i];
+            rs += res[i];
+          }
+          rs = wave_sumd_dpp(rs);
+          if (!(rs > 0.0))
+            for (int i = tid(); i < ns; i += 64) res[i] = prob[i];
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          tok = sidx[inverse_cdf(res, ns, (double)U[(s - 1) * 3 + 2])];
+        }
+        if (tid() == 0) cst32(bp->vres + ln * rpl + r, (uint32_t)tok | ((uint32_t)(taken + 1) << 24));
+      }
+      __syncthreads();
+      continue;
+    }
     if (j > 0) {
       if (tid() < 64) {
         int pos;
@@ -781,21 +994,124 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
     for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = *G(gst + i);
   }
   __syncthreads();
-  if (!first && st[kLnActive]) {
+  const bool was_active = !first && st[kLnActive];
+  const bool tree_pass = was_active && tree_rows(bp, st);
+  if (was_active) {
     const int R = st[kLnRows];
     for (int i = tid(); i < R; i += kThreads) sh->vr[i] = *G(bp->vres + lane_id * rpl + i);
     const int par = st[kLnPass] & 1;
-    for (int i = tid(); i < R * K; i += kThreads) {
-      const int r = i / K, jj = i - r * K;
-      sh->dt[r][jj] = jj < row_drafts(p, st, r)
-                          ? (int)(uint32_t)*G(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
-                          : -1;
+    if (!bp->tree)
+      for (int i = tid(); i < R * K; i += kThreads) {
+        const int r = i / K, jj = i - r * K;
+        sh->dt[r][jj] = jj < row_drafts(bp, p, st, r)
+                            ? (int)(uint32_t)*G(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
+                            : -1;
+      }
+  }
+  __syncthreads();
+  // tree lanes: commit the pass (the prefix token, or a walk of the verdicts from the root),
+  // count it and trace it, before the candidates of the next round replace this round's
+  if (tid() == 0) {
+    sh->c_mnew = -1;
+    if (was_active && bp->tree) {
+      const int m = st[kLnM], fp = st[kLnFirst], R = st[kLnRows];
+      int* codes = st + kLnCodes;
+      int cur = 1, acc = 0, m_new = 1, tok = -1;
+      if (st[kLnPass] == 0) {
+        codes[1] = sh->vr[1] & 0x7fffffff;
+        tok = codes[1];
+      } else {
+        int pos = m + 1;
+        cur = 0;
+        while (true) {
+          const int v = sh->vr[cur];
+          const int child = (int)((uint32_t)v >> 24) - 1;
+          if (child >= 0) {
+            codes[pos] = st[kLnCand + child];
+            st[kLnMask] |= 1 << pos;
+            sh->c_path[acc++] = child;
+            cur = child;
+            if (++pos > n) { m_new = n; break; }
+            continue;
+          }
+          codes[pos] = v & 0xffffff;
+          tok = codes[pos];
+          m_new = pos;
+          break;
+        }
+        st[kLnRounds] += 1;
+        st[kLnDrafted] += st[kLnCandN] - 1;
+        st[kLnAccepted] += acc;
+      }
+      st[kLnCalls] += 1;
+      if (st[kLnCalls] > n + 1) raise_status(bp, RVQSD_ETIMEOUT);
+      if (bp->tr_rounds && st[kLnFrame] < bp->tr_frames && st[kLnPass] < bp->tr_max_rounds) {
+        int32_t* tr = bp->tr_rounds + ((size_t)st[kLnFrame] * bp->tr_max_rounds + st[kLnPass]) * kTreeRoundInts;
+        tr[0] = m; tr[1] = st[kLnKp]; tr[2] = fp; tr[3] = R; tr[4] = m_new; tr[5] = acc; tr[6] = tok;
+        tr[7] = st[kLnPass];
+        tr[8] = st[kLnPass] == 0 ? 2 : st[kLnCandN];
+        for (int j = 0; j < acc; ++j) tr[16 + j] = sh->c_path[j];
+        for (int r = 0; st[kLnPass] > 0 && r < st[kLnCandN]; ++r) tr[32 + r] = st[kLnCand + r];
+      }
+      sh->c_mnew = m_new;
+      sh->c_arow = cur;
+      sh->c_acc = acc;
+      sh->c_m = m;
+    }
+  }
+  __syncthreads();
+  if (was_active && bp->tree) {
+    const int m = sh->c_m, acc = tree_pass ? sh->c_acc : 0, m_new = sh->c_mnew, arow = sh->c_arow;
+    const int d = p->d, slots = bp->kv_slots;
+    // KV of the accepted path: row path[j-1] (slot m+1+row) becomes position m+1+j, every
+    // layer and kv head; destinations never overlap a later source (path[j-1] >= j)
+    for (int j = 1; j <= acc; ++j) {
+      const int src = m + 1 + sh->c_path[j - 1], dst = m + 1 + j;
+      if (src == dst) continue;
+      const int per = p->L * p->nkv * 2 * d;
+      for (int e = tid(); e < per; e += kThreads) {
+        const int lg = e / (2 * d), w = e - lg * 2 * d;
+        float* base = bp->kv + ((size_t)lane_id * p->L * p->nkv + lg) * slots * 2 * d;
+        cstf(base + (size_t)dst * 2 * d + w, ldf(base + (size_t)src * 2 * d + w));
+      }
+      __syncthreads();
+    }
+    // the next round's candidates: depth d's rank-r token from the new anchor row's drafts
+    if (m_new < n) {
+      const int kn = min(K, n - m_new), par = st[kLnPass] & 1;
+      for (int r = 1 + tid(); r <= bp->tree_nodes; r += kThreads)
+        if (bp->t_depth[r] <= kn)
+          st[kLnCand + r] = (int)(uint32_t)*G(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + arow) * K +
+                                                         (bp->t_depth[r] - 1)) * bp->sup_words + 1 + bp->t_rank[r]);
     }
   }
   __syncthreads();
   if (tid() == 0) {
     bool start = first || !st[kLnActive];
-    if (!first && st[kLnActive]) {
+    bool done = false;  // the lane's frame is complete
+    if (!first && st[kLnActive] && bp->tree) {
+      // tree lanes: the pass was committed above; set up the next round
+      const int m_new = sh->c_mnew;
+      int* codes = st + kLnCodes;
+      if (m_new < n) {
+        const int kn = min(K, n - m_new);
+        int ncand = 1;
+        while (ncand <= bp->tree_nodes && bp->t_depth[ncand] <= kn) ++ncand;
+        int R = 1;
+        while (R < ncand && m_new + 1 + bp->t_depth[R] <= n) ++R;
+        st[kLnCand + 0] = codes[m_new];
+        st[kLnCandN] = ncand;
+        st[kLnPrevAnchor] = sh->c_arow;
+        st[kLnKp] = kn;
+        st[kLnRows] = R;
+        st[kLnFirst] = m_new + 1;
+        st[kLnM] = m_new;
+        st[kLnPass] += 1;
+      } else {
+        done = true;
+      }
+    }
+    if (!first && st[kLnActive] && !bp->tree) {
       const int m = st[kLnM], kp = st[kLnKp], R = st[kLnRows], fp = st[kLnFirst];
       int* codes = st + kLnCodes;
       int m_new = -1, acc = 0, tok = -1;
@@ -851,22 +1167,26 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
         st[kLnM] = m_new;
         st[kLnPass] += 1;
       } else {
-        // frame complete
-        const int f = st[kLnFrame];
-        for (int s = 1; s <= n; ++s) call.out_codes[(size_t)f * n + s - 1] = codes[s];
-        rvqsd_stats o;
-        o.target_calls = st[kLnCalls];
-        o.rounds = st[kLnRounds];
-        o.drafted = st[kLnDrafted];
-        o.accepted = st[kLnAccepted];
-        o.accept_mask = (uint32_t)st[kLnMask];
-        o.status = RVQSD_OK;
-        o.weight_bytes = (uint64_t)(uint32_t)st[kLnBytesLo] | ((uint64_t)(uint32_t)st[kLnBytesHi] << 32);
-        o.clk_start = (uint64_t)(uint32_t)st[kLnClkLo] | ((uint64_t)(uint32_t)st[kLnClkHi] << 32);
-        o.clk_end = dclock();
-        call.out_stats[f] = o;
-        start = true;
+        done = true;
       }
+    }
+    if (done) {
+      // frame complete
+      const int f = st[kLnFrame];
+      int* codes = st + kLnCodes;
+      for (int s = 1; s <= n; ++s) call.out_codes[(size_t)f * n + s - 1] = codes[s];
+      rvqsd_stats o;
+      o.target_calls = st[kLnCalls];
+      o.rounds = st[kLnRounds];
+      o.drafted = st[kLnDrafted];
+      o.accepted = st[kLnAccepted];
+      o.accept_mask = (uint32_t)st[kLnMask];
+      o.status = RVQSD_OK;
+      o.weight_bytes = (uint64_t)(uint32_t)st[kLnBytesLo] | ((uint64_t)(uint32_t)st[kLnBytesHi] << 32);
+      o.clk_start = (uint64_t)(uint32_t)st[kLnClkLo] | ((uint64_t)(uint32_t)st[kLnClkHi] << 32);
+      o.clk_end = dclock();
+      call.out_stats[f] = o;
+      start = true;
     }
     if (start) {
       // the lane's next frame with a valid c0
@@ -895,14 +1215,14 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
       // the heads it touches, the gathered rows and the KV cache it attends over
       int t_lo = 1 << 20, t_hi = -1;
       for (int r = 0; r < st[kLnRows]; ++r) {
-        const int s = st[kLnFirst] + r;
-        if (row_is_verify(st, r)) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
-        const int nd = row_drafts(p, st, r);
+        const int s = row_pos(bp, st, r);
+        if (row_is_verify(bp, st, r)) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
+        const int nd = row_drafts(bp, p, st, r);
         if (nd > 0) { t_lo = min(t_lo, s + 1); t_hi = max(t_hi, s + nd); }
       }
       unsigned long long b = (unsigned long long)p->L * p->layer_stride;
       if (t_hi >= t_lo) b += (unsigned long long)(t_hi - t_lo + 1) * p->table_stride;
-      for (int r = 0; r < st[kLnRows]; ++r) b += (st[kLnFirst] + r == 0) ? 4ull * H : 2ull * H;
+      for (int r = 0; r < st[kLnRows]; ++r) b += (row_pos(bp, st, r) == 0) ? 4ull * H : 2ull * H;
       b += (unsigned long long)p->L * (st[kLnFirst] + st[kLnRows]) * p->nkv * p->d * 2 * 4;
       b += (uint64_t)(uint32_t)st[kLnBytesLo] | ((uint64_t)(uint32_t)st[kLnBytesHi] << 32);
       st[kLnBytesLo] = (int)(uint32_t)b;
@@ -915,8 +1235,10 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
   if (!st[kLnActive]) return;
   const float* g0 = bfw(p, p->o_attn_norm);
   const int lane = tid() & 63, wave = tid() >> 6, nch = H / 8;
+  const bool tree_next = tree_rows(bp, st);
   for (int r = wave; r < st[kLnRows]; r += kWaves) {
-    const int s = st[kLnFirst] + r, i = lane_id * rpl + r;
+    const int s = row_pos(bp, st, r), i = lane_id * rpl + r;
+    const int code = tree_next ? st[kLnCand + r] : st[kLnInCode + s];
     float xv[kRowChunks][8];
     float ss = 0.f;
 #pragma unroll
@@ -929,7 +1251,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
           for (int e = 0; e < 8; ++e) xv[q][e] = G(fr)[e];
         } else {
           const bf16_t* tab = bw(p, p->o_emb0 + (uint64_t)(s - 1) * p->table_stride);
-          const W16 w = *G(reinterpret_cast<const W16*>(tab + (size_t)st[kLnInCode + s] * H + 8 * c));
+          const W16 w = *G(reinterpret_cast<const W16*>(tab + (size_t)code * H + 8 * c));
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             xv[q][2 * e] = __uint_as_float(w[e] << 16);
@@ -1004,7 +1326,10 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
     for (int l = 0; l < L && ok; ++l) {
       proj_partial<4>(bp, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, bp->ks_qkv, A0, dyn);
       ok = grid_sync(bp, gen, sh);
-      if (ok) phase_attn(bp, sh, l, A1, dyn);
+      if (ok) {
+        if (bp->tree) phase_attn_tree(bp, sh, l, A1, dyn);
+        else phase_attn(bp, sh, l, A1, dyn);
+      }
       ok = ok && grid_sync(bp, gen, sh);
       if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
       ok = ok && grid_sync(bp, gen, sh);

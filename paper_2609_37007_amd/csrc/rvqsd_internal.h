@@ -162,11 +162,28 @@ constexpr int kBatchRedFloats = 16 * kBatchMTiles * 256;  // LDS partial tiles o
 constexpr int kLnActive = 0, kLnFrame = 1, kLnPass = 2, kLnM = 3, kLnKp = 4, kLnFirst = 5, kLnRows = 6,
               kLnPrevAnchor = 7, kLnCalls = 8, kLnRounds = 9, kLnDrafted = 10, kLnAccepted = 11, kLnMask = 12,
               kLnStatus = 13, kLnBytesLo = 14, kLnBytesHi = 15, kLnClkLo = 16, kLnClkHi = 17,
-              kLnCodes = 32, kLnDrafts = 48, kLnInCode = 64, kLaneInts = 80;
+              kLnCandN = 18,  // tree lanes: candidate rows of the pass (root + nodes down to depth K')
+              kLnCodes = 32, kLnDrafts = 48, kLnInCode = 64,
+              kLnCand = 80,   // tree lanes: token of every candidate row (row 0: the committed c_m)
+              kLaneInts = kLnCand + kBatchMaxRows + 16;
+// sparse-tree lanes: a tree of up to kBatchMaxRows - 1 draft nodes per lane
+constexpr int kMaxTreeRows = kBatchMaxRows;
+constexpr int kTreeRoundInts = 128;  // ints per traced round of a tree lane
 
 struct BParams {
   const KParams* k;     // device copy of the stream's parameter block (dimensions, weights, rotary table)
   int32_t lanes, rpl, M, nwg;
+  // sparse-tree verification (Sec. 2.2, Fig. 2): every lane's rows after its prefix pass are
+  // the committed token's row (the root) and a draft tree packed breadth first; rpl = nodes + 1
+  int32_t tree;         // 0: chain rows (the committed code and K drafts), 1: tree rows
+  int32_t tree_nodes;
+  int32_t kv_slots;     // KV slots per (lane, layer, kv head): committed positions, then the pass's rows
+  int32_t slot_draft0;  // first draft slot of the trace layout (16 for chains, max(16, rpl) for trees)
+  int32_t t_parent[kMaxTreeRows];   // row r >= 1: parent row
+  int32_t t_rank[kMaxTreeRows];     // row r >= 1: rank of its token among its depth's candidates
+  int32_t t_depth[kMaxTreeRows];    // row 0: 0
+  uint64_t t_anc[kMaxTreeRows][2];  // ancestor-or-self bits of row r over rows 0..127
+  int32_t t_need[kMaxCodes + 1];    // depth d: candidates to rank (largest rank at d plus one)
   int32_t ks_qkv, ks_o, ks_down;  // k splits of the projections whose partial sums the next phase adds
   int32_t hrows;        // LM-head input rows: M * (K + 1) (row i * (K + 1) + j: row i plus offset b_j)
   int32_t sup_words;    // 64-bit words of one support record: 1 + 2 * topk
@@ -175,17 +192,18 @@ struct BParams {
   uint32_t* a;          // [M][max(H, qdim, F)] split activations (8-element chunks: 4 words hi, 4 words lo)
   uint32_t* ah;         // [hrows][H] split LM-head inputs
   float* part;          // [max ks][M][max N] partial sums
-  float* kv;            // [lanes][L][nkv][kMaxPos][2][d] KV cache (k after norm and RoPE, v)
+  float* kv;            // [lanes][L][nkv][kv_slots][2][d] KV cache (k after norm and RoPE, v)
   float* logits;        // [hrows][V]
-  int32_t* vres;        // [lanes][rpl] verdicts: token | accepted << 31
+  int32_t* vres;        // [lanes][rpl] verdicts: token | accepted << 31 (chain); token | (child row + 1) << 24 (tree)
   uint64_t* drec;       // [2][lanes][rpl][K][sup_words] draft records: token, idx[topk], prob bits[topk]
+                        // (tree lanes: count, then the ranked candidate tokens)
   uint32_t* bar;        // barrier words: [0] top counter, [64 (1 + x)] counter of XCD x, [64 * 9] generation
   int32_t* status;      // first device-side error of the launch (0 = none)
   unsigned long long* totals;  // [0] passes (rounds of the batch), [1] their algorithmic bytes
   // per-frame trace (nullable), frames f < tr_frames of a call, passes < tr_max_rounds of the frame:
   // logits in the single-stream slot layout, round records as the single-stream trace's
   float* tr_logits;     // [tr_frames][tr_max_rounds][n_slots][V]
-  int32_t* tr_rounds;   // [tr_frames][tr_max_rounds][kTraceRoundInts]
+  int32_t* tr_rounds;   // [tr_frames][tr_max_rounds][kTraceRoundInts] (tree lanes: kTreeRoundInts)
   int32_t tr_max_rounds, tr_frames, tr_slots;
 };
 

@@ -22,7 +22,8 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 TRACE_ROUND_INTS = 32
 
 # every symbol include/rvqsd.h declares
-EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_stream_destroy",
+EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_tree_stream_create",
+           "rvqsd_stream_destroy",
            "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frame_noalloc",
            "rvqsd_stream_reset",
            "rvqsd_set_trace", "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async",
@@ -125,6 +126,7 @@ def lib():
         L.rvqsd_destroy.restype = None
         L.rvqsd_model_info.argtypes = [vp, P(rvqsd_info)]
         L.rvqsd_stream_create.argtypes = [vp, vp, i32, P(vp)]
+        L.rvqsd_tree_stream_create.argtypes = [vp, vp, i32, i32, vp, vp, P(vp)]
         L.rvqsd_stream_destroy.argtypes = [vp]
         L.rvqsd_stream_destroy.restype = None
         L.rvqsd_decode_frame.argtypes = [vp, vp, i32, ctypes.c_uint64, vp, P(rvqsd_stats)]
@@ -147,7 +149,8 @@ def lib():
         L.rvqsd_status_str.restype = ctypes.c_char_p
         L.rvqsd_last_error.argtypes = []
         L.rvqsd_last_error.restype = ctypes.c_char_p
-        for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_decode_frame",
+        for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_tree_stream_create",
+                  "rvqsd_decode_frame",
                   "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frame_noalloc",
                   "rvqsd_stream_reset", "rvqsd_set_trace",
                   "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async", "rvqsd_batch_totals",
@@ -223,12 +226,20 @@ class Model:
 class Stream:
     """rvqsd_stream_create and the decode calls; ``hip_stream`` is a raw hipStream_t (int) or None."""
 
-    def __init__(self, model: Model, hip_stream=None, max_streams: int = 1):
+    def __init__(self, model: Model, hip_stream=None, max_streams: int = 1, tree=None):
+        """tree: (parents, ranks) of packed rows 1..N for sparse-tree verification."""
         self.model = model
         self.n = model.cfg.n_codes
         h = ctypes.c_void_p()
-        _check(lib().rvqsd_stream_create(model._h, ctypes.c_void_p(hip_stream or 0), max_streams, ctypes.byref(h)),
-               "rvqsd_stream_create")
+        if tree is None:
+            _check(lib().rvqsd_stream_create(model._h, ctypes.c_void_p(hip_stream or 0), max_streams,
+                                             ctypes.byref(h)), "rvqsd_stream_create")
+        else:
+            par = np.ascontiguousarray(tree[0], dtype=np.int32)
+            rk = np.ascontiguousarray(tree[1], dtype=np.int32)
+            _check(lib().rvqsd_tree_stream_create(model._h, ctypes.c_void_p(hip_stream or 0), max_streams, par.size,
+                                                  _ptr(par), _ptr(rk), ctypes.byref(h)), "rvqsd_tree_stream_create")
+        self.tree = tree
         self._h = h
         _live["stream"].add(self)
         self._trace = None

@@ -239,3 +239,154 @@ def untraced_divergence_near(rig, f, c0, u, codes, err):
         if near_enough(rig, otr["rounds"][i], err, dl):
             return True
     return False
+
+
+# ------------------------------------------------------------ sparse-tree lanes
+# A tree rig adds tree (parents, ranks of rows 1..N), otree (oracle.make_tree of it)
+# and slot0 (the first draft slot: max(16, N + 1)). Tree round records (128 ints):
+# [0..7] m, K', first, rows, m_new, accepted, token, pass; [8] candidate rows;
+# [16..) accepted rows; [32..) candidate tokens (row 0 = c_m).
+
+def tree_depths(tree):
+    parents, _ = tree
+    d = [0]
+    for p in parents:
+        d.append(d[p] + 1)
+    return d
+
+
+def tree_logit_error(rig, f, c0, codes, lg, rd):
+    """Max-abs difference of every traced verify and draft row of a tree frame from the
+    oracle's fp64 logits over the same packed rows."""
+    K, n = rig.K, rig.s.n_codes
+    depth = tree_depths(rig.tree)
+    full = [int(c0)] + [int(c) for c in codes]
+    worst = 0.0
+    for i, row in enumerate(rd):
+        m, fp, R = int(row[0]), int(row[2]), int(row[3])
+        if i == 0:
+            h = rig.orc.forward(f, [int(c0)])
+            rows = [(1, h[1], 1)]  # (row, hidden, position)
+        else:
+            toks = [int(x) for x in row[32:32 + R]]
+            hr = rig.orc.tree_hidden(rig.otree, f, full[:m + 1], toks[1:])
+            rows = [(r, hr[r], fp + depth[r]) for r in range(R)]
+        for r, h, pos in rows:
+            ref = rig.orc.logits(h, pos, 0)
+            worst = max(worst, float(np.abs(lg[i, r].astype(np.float64) - ref).max()))
+            if pos <= n - 1:
+                for j in range(1, min(K, n - pos) + 1):
+                    ref = rig.orc.logits(h, pos + j, j)
+                    got = lg[i, rig.slot0 + r * K + j - 1].astype(np.float64)
+                    worst = max(worst, float(np.abs(got - ref).max()))
+    return worst
+
+
+def tree_replay(rig, lg, rd, u, codes):
+    """Re-take every decision of a tree frame from the kernel's own logits: the ranked
+    candidates of every depth, the sibling walks and the residual draws. Returns 1 when a
+    decision diverged within 1e-6 of its uniform, else 0."""
+    K, n, topk, T = rig.K, rig.s.n_codes, rig.topk, rig.T
+    parents, ranks = rig.tree
+    depth = tree_depths(rig.tree)
+    mine = {}
+    arow = 1
+    for i, row in enumerate(rd):
+        m, kp, fp, R, m_new, acc, tok = (int(x) for x in row[:7])
+        if i == 0:
+            pi, pp = O.topk_softmax(lg[0, 1], topk, T)
+            us = float(u[0, 2])
+            if tok != O.sample(pi, pp, us):
+                assert cdf_margin(pp, us) < CDF_EXCUSE
+                return 1
+            mine[1] = tok
+            arow = 1
+            continue
+        ncand = int(row[8])
+        cand = [int(x) for x in row[32:32 + ncand]]
+        # candidates: the anchor row's draft logits of the previous pass, ranked
+        for r in range(1, ncand):
+            d = depth[r]
+            order = np.lexsort((np.arange(rig.s.vocab), -lg[i - 1, rig.slot0 + arow * K + d - 1].astype(np.float64)))
+            assert cand[r] == int(order[ranks[r - 1]]), (i, r, cand[r], int(order[ranks[r - 1]]))
+        assert cand[0] == (mine[m] if m in mine else None), (i, cand[0])
+        cur, pos, path = 0, m + 1, []
+        while True:
+            pi, pp = O.topk_softmax(lg[i, cur], topk, T)
+            kids = sorted((c for c in range(cur + 1, ncand) if parents[c - 1] == cur), key=lambda c: ranks[c - 1])
+            pmap = dict(zip(pi.tolist(), pp.tolist()))
+            ua, us = float(u[pos - 1, 1]), float(u[pos - 1, 2])
+            cum, taken = 0.0, None
+            for c in kids:
+                cum += pmap.get(cand[c], 0.0)
+                if taken is None and ua < cum:
+                    taken = c
+            gpu_taken = int(row[16 + len(path)]) if len(path) < acc else None
+            if taken != gpu_taken:
+                cums = np.cumsum([pmap.get(cand[c], 0.0) for c in kids]) if kids else np.array([])
+                assert kids and np.min(np.abs(cums - ua)) < CDF_EXCUSE, (i, pos, taken, gpu_taken)
+                return 1
+            if taken is not None:
+                mine[pos] = cand[taken]
+                path.append(taken)
+                cur = taken
+                pos += 1
+                if pos > n:
+                    break
+                continue
+            kid_toks = {cand[c] for c in kids}
+            res = np.array([0.0 if int(x) in kid_toks else float(p) for x, p in zip(pi, pp)])
+            if not res.sum() > 0:
+                res = np.asarray(pp, dtype=np.float64)
+            t = O.sample(pi, res, us)
+            if t != tok:
+                assert cdf_margin(res, us) < CDF_EXCUSE, (i, pos, t, tok)
+                return 1
+            mine[pos] = t
+            break
+        assert (len(path), min(pos, n)) == (acc, m_new), (i, path, pos, acc, m_new)
+        arow = cur
+    assert sorted(mine) == list(range(1, n + 1))
+    assert [mine[s] for s in range(1, n + 1)] == [int(c) for c in codes]
+    return 0
+
+
+def tree_first_divergence(orounds, rd):
+    for i in range(max(len(orounds), len(rd))):
+        if i >= len(orounds) or i >= len(rd):
+            return i
+        o, g = orounds[i], [int(x) for x in rd[i]]
+        if (o["m"], o["m_new"], o["accepted"], o["token"]) != (g[0], g[4], g[5], g[6]):
+            return i
+        if i > 0:
+            nc = o["n_cand"]
+            if nc != g[8] or o["tokens"][:nc] != g[32:32 + nc] or o["path"] != g[16:16 + o["accepted"]]:
+                return i
+    return None
+
+
+def tree_compare_end_to_end(rig, f, c0, u, codes, stats, logit_err, rd):
+    oc, ost, otr = rig.orc.tree_frame(rig.otree, f, int(c0), u, trace=True)
+    if np.array_equal(oc, codes):
+        for k in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
+            assert stats[k] == ost[k], (k, stats[k], ost[k])
+        return True
+    i = tree_first_divergence(otr["rounds"], rd)
+    assert i is not None and i < len(otr["rounds"]) and near_enough(rig, otr["rounds"][i], logit_err), \
+        f"first differing round {i} is not near a threshold: gpu {codes.tolist()} oracle {oc.tolist()}"
+    return False
+
+
+def check_tree_frames(rig, frames, f, c0, u, get, tol, excuse_frac=0.1):
+    excused, worst = 0, 0.0
+    for i in frames:
+        codes, st, lg, rd = get(i)
+        assert st["status"] == 0
+        err = tree_logit_error(rig, f[i], c0[i], codes, lg, rd)
+        worst = max(worst, err)
+        assert err <= tol, f"frame {i}: logit max-abs {err:.3g} > {tol}"
+        ex = tree_replay(rig, lg, rd, u[i], codes)
+        if not tree_compare_end_to_end(rig, f[i], c0[i], u[i], codes, st, err, rd) or ex:
+            excused += 1
+    assert excused <= max(1, int(excuse_frac * len(frames))), excused
+    return worst, excused
