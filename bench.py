@@ -101,6 +101,10 @@ def parse():
     ap.add_argument("--offsets", default="seed", metavar="seed|zero|FILE.npy",
                     help="draft offsets: the blob's own N(0, 0.02) draw (seed), all zero (the reused heads of "
                          "Sec. 2.2), or a trained float32 [max_draft][hidden] array")
+    ap.add_argument("--tree", default=None, metavar="FILE.json",
+                    help="sparse-tree verification (Sec. 2.2, Fig. 2) with the packed tree of FILE (parents, ranks; "
+                         "paper_2609_37007_amd/tree.py writes them); the frames then run through the batched "
+                         "kernel's tree lane")
     ap.add_argument("--residency", action="store_true",
                     help="only measure whether the weights stay in the Infinity Cache: warm against cold frames "
                          "(a 2 GiB sweep between frames) and a plain streaming read of a weight-sized buffer")
@@ -146,7 +150,8 @@ def copy_calibration(mb: int) -> int:
     return 0
 
 
-def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order, one_thread_seconds=8.0):
+def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order, one_thread_seconds=8.0,
+                  tree=None):
     """Time the CPU oracle on frames `order` until `seconds` pass (all host threads), then on
     the next frames with one thread for `one_thread_seconds`; returns the cpu_baseline object."""
     from oracle import oracle as O
@@ -154,6 +159,7 @@ def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order
                    head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
                    dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K)
     threads = O.get_threads()
+    otree = O.make_tree(*tree) if tree is not None else None
     print(f"[bench] oracle sample on {threads} threads, ~{seconds:.0f} s", file=sys.stderr, flush=True)
 
     def run(start, budget):
@@ -161,7 +167,10 @@ def oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, seconds, order
         t0 = time.perf_counter()
         while start + done < len(order) and (time.perf_counter() - t0) < budget:
             i = order[start + done]
-            oc, _, _ = orc.spec_frame(f[i], int(c0[i]), u[i])
+            if tree is None:
+                oc, _, _ = orc.spec_frame(f[i], int(c0[i]), u[i])
+            else:
+                oc, _, _ = orc.tree_frame(otree, f[i], int(c0[i]), u[i])
             same += int((oc == codes[i]).all())
             done += 1
         return done, same, time.perf_counter() - t0
@@ -614,7 +623,12 @@ def main() -> int:
     torch_stream = torch.cuda.current_stream(dev)
     model = R.Model(blob, cfg)
     info = model.info()
-    stream = R.Stream(model, hip_stream=torch_stream.cuda_stream)
+    tree = None
+    if a.tree:
+        with open(a.tree if os.path.isabs(a.tree) else os.path.join(ROOT, a.tree)) as fh:
+            tj = json.load(fh)
+        tree = (tj["parents"], tj["ranks"])
+    stream = R.Stream(model, hip_stream=torch_stream.cuda_stream, tree=tree)
 
     f, c0 = S.frame_inputs(s, steps)
     u = S.uniforms(steps, s.n_codes)
@@ -664,12 +678,14 @@ def main() -> int:
     rounds = int(st["rounds"].sum())
     bytes_per_launch = st["weight_bytes"].astype(np.float64)
     achieved = float(bytes_per_launch.sum() / (launch_ms.sum() * 1e-3) / 1e9)
-    traffic = measured_traffic() if (a.workload == "mcd1024" and K == 4 and a.head_scale == 1.0) else None
+    traffic = measured_traffic() if (a.workload == "mcd1024" and K == 4 and a.head_scale == 1.0 and not tree
+                                     and a.offsets == "seed") else None
     codes_per_s = n * steps / elapsed
 
     cpu = None
     if not a.no_cpu_baseline:
-        cpu = oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, a.cpu_seconds, list(range(steps)))
+        cpu = oracle_sample(blob, s, topk, temperature, K, f, c0, u, codes, a.cpu_seconds, list(range(steps)),
+                            tree=tree)
 
     out = {
         "metric": METRIC,
@@ -688,7 +704,9 @@ def main() -> int:
             "workload": (f"{a.workload}: {s.n_layers} layers, hidden {s.hidden}, {s.n_q_heads}/{s.n_kv_heads} heads "
                          f"x {s.head_dim}, ffn {s.ffn}, {s.n_codes} codebooks of {s.vocab}, "
                          f"{'bf16' if s.dtype == S.DTYPE_BF16 else 'fp32'} weights; "
-                         f"draft length {K}, top-k {topk}, temperature {temperature}, batch 1"),
+                         + (f"sparse tree of {len(tree[0])} nodes, depth {K}" if tree else f"draft length {K}")
+                         + f", top-k {topk}, temperature {temperature}, batch 1"),
+            "tree_nodes": len(tree[0]) if tree else 0,
             "frames": steps,
             "draft_len": K,
             "topk": topk,
@@ -712,7 +730,7 @@ def main() -> int:
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": "frame_kernel",
+            "kernel": "batch_kernel" if tree else "frame_kernel",
             "algorithmic_bytes_per_launch": round(float(bytes_per_launch.mean()), 1),
             "launch_ms_mean": round(float(launch_ms.mean()), 5),
         },

@@ -118,3 +118,74 @@ def load(path):
     with open(path) as fh:
         d = json.load(fh)
     return d["parents"], d["ranks"]
+
+
+def calibrate(workload: str = "mcd1024", frames: int = 2048, depth: int = 4, ranks: int = 8, nodes=(16,),
+              offsets: str = "seed", seed: int = 0, device=None, log=print, head_scale: float = 1.0):
+    """Rank statistics of the model's own top-k samples (the stand-in for the paper's
+    calibration set) and the greedy tree of every node budget in `nodes`."""
+    import torch
+
+    from paper_2609_37007_amd import offsets as OF
+    from paper_2609_37007_amd import synth as S
+
+    shape_name, topk = OF.WORKLOADS[workload]
+    s = getattr(S, shape_name)
+    if offsets == "seed":
+        blob = S.make_weights(s, seed=0, head_scale=head_scale)
+    elif offsets == "zero":
+        blob = S.make_weights(s, seed=0, head_scale=head_scale, offsets=np.zeros((s.max_draft, s.hidden)))
+    else:
+        blob = S.make_weights(s, seed=0, head_scale=head_scale, offsets=np.load(offsets, allow_pickle=False))
+    dev = torch.device(device or ("cuda" if torch.cuda.is_available() else "cpu"))
+    dec = OF.Decoder(s, blob, dev)
+    f, c0 = S.frame_inputs(s, frames, seed_hidden=seed + 60, seed_c0=seed + 61)
+    gen = torch.Generator(device=dev).manual_seed(seed + 62)
+    with torch.no_grad():
+        fT = torch.from_numpy(f).to(dev)
+        cT = torch.from_numpy(c0.astype(np.int64)).to(dev)
+        codes, hs = [], []
+        for a in range(0, frames, 512):
+            c = dec.sample_frames(fT[a:a + 512], cT[a:a + 512], topk, 0.9, gen)
+            codes.append(c)
+            hs.append(dec.forward(dec.inputs(fT[a:a + 512], c[:, :-1])))
+        codes, hs = torch.cat(codes), torch.cat(hs)
+    P = rank_statistics(dec, hs, codes, S.unpack_weights(s, blob)["offsets"], topk, 0.9, depth, ranks)
+    log("acceptance by depth (rows) and rank (columns):\n" + np.array2string(P, precision=4))
+    trees = {}
+    for N in nodes:
+        paths = greedy_tree(P, N, depth)
+        parents, rks = pack(paths)
+        trees[N] = dict(parents=parents, ranks=rks, expected_accepted=expected_accepted(P, paths))
+    return P, trees
+
+
+def main(argv=None):
+    import argparse
+    import os
+    ap = argparse.ArgumentParser(description="Greedy sparse-tree calibration from the model's own samples")
+    ap.add_argument("--workload", default="mcd1024")
+    ap.add_argument("--frames", type=int, default=2048)
+    ap.add_argument("--depth", type=int, default=4)
+    ap.add_argument("--ranks", type=int, default=8)
+    ap.add_argument("--nodes", default="4,8,16,32,48,64")
+    ap.add_argument("--offsets", default="seed")
+    ap.add_argument("--head-scale", type=float, default=1.0)
+    ap.add_argument("--out-dir", required=True)
+    a = ap.parse_args(argv)
+    nodes = [int(x) for x in a.nodes.split(",")]
+    P, trees = calibrate(a.workload, a.frames, a.depth, a.ranks, nodes, a.offsets, head_scale=a.head_scale)
+    os.makedirs(a.out_dir, exist_ok=True)
+    for N, t in trees.items():
+        tag = "" if a.head_scale == 1.0 else f"_h{a.head_scale:g}"
+        path = os.path.join(a.out_dir, f"tree_{a.workload}{tag}_n{N}.json")
+        save(path, t["parents"], t["ranks"], workload=a.workload, depth=a.depth, frames=a.frames,
+             offsets=a.offsets, head_scale=a.head_scale, expected_accepted=t["expected_accepted"],
+             acceptance=P.tolist())
+        print(f"N = {N}: expected accepted nodes per round {t['expected_accepted']:.4f} -> {path}")
+    return 0
+
+
+if __name__ == "__main__":
+    import sys
+    sys.exit(main())
