@@ -34,15 +34,18 @@
 
 #define MAX_POS 17   /* 1 frame-hidden position + up to 16 code positions */
 
+/* Every weight is held as the exact value it stands for, in double: f32 and bf16
+ * values widen exactly; an int8 matrix (W8A16, dtype 2) holds s[o] * q[o][i], the
+ * product of its row's fp32 scale and int8 code, which a double represents exactly. */
 struct orc_model {
   orc_cfg cfg;
-  float* store;
+  double* store;
   /* per layer */
-  const float **attn_norm, **wq, **wk, **wv, **q_norm, **k_norm, **wo, **mlp_norm, **wgate, **wup, **wdown;
-  const float* final_norm;
-  const float** emb; /* [n_codes], E_i embeds c_i */
-  const float** lmh; /* [n_codes + 1], LMH_s emits c_s (index 0 unused) */
-  const float* offsets; /* [max_draft][H] */
+  const double **attn_norm, **wq, **wk, **wv, **q_norm, **k_norm, **wo, **mlp_norm, **wgate, **wup, **wdown;
+  const double* final_norm;
+  const double** emb; /* [n_codes], E_i embeds c_i */
+  const double** lmh; /* [n_codes + 1], LMH_s emits c_s (index 0 unused) */
+  const double* offsets; /* [max_draft][H] */
 };
 
 int32_t orc_abi_version(void) { return 1; }
@@ -85,7 +88,7 @@ orc_model* orc_create(const orc_cfg* cfg, const void* blob, size_t blob_bytes, i
     if (c->n_layers <= 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
         (c->head_dim % 2) != 0 || c->ffn <= 0 || c->n_codes <= 0 || c->n_codes > MAX_POS - 1 || c->vocab <= 0 ||
         c->max_draft < 0 || c->topk <= 0 || c->draft_len < 0 || c->draft_len > c->max_draft ||
-        (c->n_q_heads % c->n_kv_heads) != 0 || !(c->temperature > 0.0) || (c->dtype != 0 && c->dtype != 1) ||
+        (c->n_q_heads % c->n_kv_heads) != 0 || !(c->temperature > 0.0) || (c->dtype < 0 || c->dtype > 2) ||
         c->draft_mode < 0 || c->draft_mode > 2) {
       st = ORC_EINVAL;
       goto out;
@@ -104,65 +107,88 @@ orc_model* orc_create(const orc_cfg* cfg, const void* blob, size_t blob_bytes, i
   {
     const int L = cfg->n_layers, H = cfg->hidden, d = cfg->head_dim, F = cfg->ffn, V = cfg->vocab, n = cfg->n_codes;
     const size_t qd = (size_t)cfg->n_q_heads * d, kd = (size_t)cfg->n_kv_heads * d;
-    const size_t wb = cfg->dtype == 0 ? 4 : 2;
-    size_t n_vec = 0, n_mat = 0;
+    /* bytes of a [rows][cols] matrix in the blob: f32, bf16, or int8 codes + fp32 row
+     * scales padded to 16 bytes */
+#define MAT_BYTES(rows, cols)                                                                  \
+  (cfg->dtype == 0 ? (size_t)(rows) * (cols) * 4                                               \
+                   : cfg->dtype == 1 ? (size_t)(rows) * (cols) * 2                             \
+                                     : (((size_t)(rows) * (cols) + 4 * (size_t)(rows) + 15) / 16 * 16))
+    size_t n_vec = 0, n_mat = 0, mat_bytes = 0;
     n_vec += (size_t)L * (H + d + d + H);
     n_mat += (size_t)L * (qd * H + 2 * kd * H + H * qd + 2 * (size_t)F * H + (size_t)H * F);
+    mat_bytes += (size_t)L * (MAT_BYTES(qd, H) + 2 * MAT_BYTES(kd, H) + MAT_BYTES(H, qd) + 2 * MAT_BYTES(F, H) +
+                              MAT_BYTES(H, F));
     n_vec += H;
     n_mat += (size_t)2 * n * V * H;
+    mat_bytes += (size_t)2 * n * MAT_BYTES(V, H);
     n_vec += (size_t)cfg->max_draft * H;
-    if (blob_bytes != 64 + n_vec * 4 + n_mat * wb) { st = ORC_EBLOB; goto out; }
+    if (blob_bytes != 64 + n_vec * 4 + mat_bytes) { st = ORC_EBLOB; goto out; }
 
     m = (orc_model*)calloc(1, sizeof(orc_model));
     if (!m) { st = ORC_ENOMEM; goto out; }
     m->cfg = *cfg;
-    m->store = (float*)malloc((n_vec + n_mat) * sizeof(float));
-    const float*** lay[11] = {&m->attn_norm, &m->wq, &m->wk, &m->wv, &m->q_norm, &m->k_norm,
-                              &m->wo, &m->mlp_norm, &m->wgate, &m->wup, &m->wdown};
+    m->store = (double*)malloc((n_vec + n_mat) * sizeof(double));
+    const double*** lay[11] = {&m->attn_norm, &m->wq, &m->wk, &m->wv, &m->q_norm, &m->k_norm,
+                               &m->wo, &m->mlp_norm, &m->wgate, &m->wup, &m->wdown};
     int fail = !m->store;
     for (int i = 0; i < 11; ++i) {
-      *lay[i] = (const float**)calloc((size_t)L, sizeof(float*));
+      *lay[i] = (const double**)calloc((size_t)L, sizeof(double*));
       fail |= !*lay[i];
     }
-    m->emb = (const float**)calloc((size_t)n, sizeof(float*));
-    m->lmh = (const float**)calloc((size_t)n + 1, sizeof(float*));
+    m->emb = (const double**)calloc((size_t)n, sizeof(double*));
+    m->lmh = (const double**)calloc((size_t)n + 1, sizeof(double*));
     if (fail || !m->emb || !m->lmh) { st = ORC_ENOMEM; goto out; }
 
     const unsigned char* src = (const unsigned char*)blob + 64;
-    float* dst = m->store;
-    /* copy one tensor of cnt elements; matrices may be bf16 */
-#define TAKE(ptr, cnt, is_mat)                                                      \
-  do {                                                                              \
-    size_t cnt_ = (cnt);                                                            \
-    (ptr) = dst;                                                                    \
-    if ((is_mat) && wb == 2) {                                                      \
-      for (size_t i_ = 0; i_ < cnt_; ++i_)                                          \
-        dst[i_] = bf16_to_float((uint16_t)(src[2 * i_] | (src[2 * i_ + 1] << 8)));  \
-      src += 2 * cnt_;                                                              \
-    } else {                                                                        \
-      memcpy(dst, src, 4 * cnt_);                                                   \
-      src += 4 * cnt_;                                                              \
-    }                                                                               \
-    dst += cnt_;                                                                    \
+    double* dst = m->store;
+    /* one tensor of `rows` x `cols` elements; vectors are f32, matrices f32, bf16 or int8
+     * codes with fp32 row scales (weight = scale * code) */
+#define TAKE(ptr, rows, cols, is_mat)                                                           \
+  do {                                                                                          \
+    const size_t r_ = (rows), c_ = (cols), cnt_ = r_ * c_;                                      \
+    (ptr) = dst;                                                                                \
+    if ((is_mat) && cfg->dtype == 1) {                                                          \
+      for (size_t i_ = 0; i_ < cnt_; ++i_)                                                      \
+        dst[i_] = (double)bf16_to_float((uint16_t)(src[2 * i_] | (src[2 * i_ + 1] << 8)));      \
+      src += 2 * cnt_;                                                                          \
+    } else if ((is_mat) && cfg->dtype == 2) {                                                   \
+      const unsigned char* sc_ = src + cnt_;                                                    \
+      for (size_t o_ = 0; o_ < r_; ++o_) {                                                      \
+        float s_;                                                                               \
+        memcpy(&s_, sc_ + 4 * o_, 4);                                                           \
+        for (size_t i_ = 0; i_ < c_; ++i_)                                                      \
+          dst[o_ * c_ + i_] = (double)s_ * (double)(int8_t)src[o_ * c_ + i_];                   \
+      }                                                                                         \
+      src += MAT_BYTES(r_, c_);                                                                 \
+    } else {                                                                                    \
+      for (size_t i_ = 0; i_ < cnt_; ++i_) {                                                    \
+        float f_;                                                                               \
+        memcpy(&f_, src + 4 * i_, 4);                                                           \
+        dst[i_] = (double)f_;                                                                   \
+      }                                                                                         \
+      src += 4 * cnt_;                                                                          \
+    }                                                                                           \
+    dst += cnt_;                                                                                \
   } while (0)
     for (int l = 0; l < L; ++l) {
-      TAKE(m->attn_norm[l], (size_t)H, 0);
-      TAKE(m->wq[l], qd * H, 1);
-      TAKE(m->wk[l], kd * H, 1);
-      TAKE(m->wv[l], kd * H, 1);
-      TAKE(m->q_norm[l], (size_t)d, 0);
-      TAKE(m->k_norm[l], (size_t)d, 0);
-      TAKE(m->wo[l], (size_t)H * qd, 1);
-      TAKE(m->mlp_norm[l], (size_t)H, 0);
-      TAKE(m->wgate[l], (size_t)F * H, 1);
-      TAKE(m->wup[l], (size_t)F * H, 1);
-      TAKE(m->wdown[l], (size_t)H * F, 1);
+      TAKE(m->attn_norm[l], 1, (size_t)H, 0);
+      TAKE(m->wq[l], qd, (size_t)H, 1);
+      TAKE(m->wk[l], kd, (size_t)H, 1);
+      TAKE(m->wv[l], kd, (size_t)H, 1);
+      TAKE(m->q_norm[l], 1, (size_t)d, 0);
+      TAKE(m->k_norm[l], 1, (size_t)d, 0);
+      TAKE(m->wo[l], (size_t)H, qd, 1);
+      TAKE(m->mlp_norm[l], 1, (size_t)H, 0);
+      TAKE(m->wgate[l], (size_t)F, (size_t)H, 1);
+      TAKE(m->wup[l], (size_t)F, (size_t)H, 1);
+      TAKE(m->wdown[l], (size_t)H, (size_t)F, 1);
     }
-    TAKE(m->final_norm, (size_t)H, 0);
-    for (int i = 0; i < n; ++i) TAKE(m->emb[i], (size_t)V * H, 1);
-    for (int t = 1; t <= n; ++t) TAKE(m->lmh[t], (size_t)V * H, 1);
-    TAKE(m->offsets, (size_t)cfg->max_draft * H, 0);
+    TAKE(m->final_norm, 1, (size_t)H, 0);
+    for (int i = 0; i < n; ++i) TAKE(m->emb[i], (size_t)V, (size_t)H, 1);
+    for (int t = 1; t <= n; ++t) TAKE(m->lmh[t], (size_t)V, (size_t)H, 1);
+    TAKE(m->offsets, (size_t)cfg->max_draft, (size_t)H, 0);
 #undef TAKE
+#undef MAT_BYTES
   }
 out:
   if (st != ORC_OK && m) { orc_destroy(m); m = NULL; }
@@ -183,22 +209,22 @@ void orc_destroy(orc_model* m) {
 /* --------------------------------------------------------------- forward */
 
 /* y = x / sqrt(mean(x^2) + eps) * g */
-static void rmsnorm(const double* x, const float* g, int n, double eps, double* y) {
+static void rmsnorm(const double* x, const double* g, int n, double eps, double* y) {
   double ss = 0.0;
   for (int i = 0; i < n; ++i) ss += x[i] * x[i];
   double r = 1.0 / sqrt(ss / n + eps);
-  for (int i = 0; i < n; ++i) y[i] = x[i] * r * (double)g[i];
+  for (int i = 0; i < n; ++i) y[i] = x[i] * r * g[i];
 }
 
 /* Y[p][o] = sum_k W[o][k] * X[p][k] for p < np (W: [rows][cols]) */
-static void matmul(const float* W, int rows, int cols, const double* X, int np, double* Y) {
+static void matmul(const double* W, int rows, int cols, const double* X, int np, double* Y) {
 #pragma omp parallel for schedule(static) if ((long)rows * cols * np >= 1L << 18)
   for (int o = 0; o < rows; ++o) {
-    const float* w = W + (size_t)o * cols;
+    const double* w = W + (size_t)o * cols;
     for (int p = 0; p < np; ++p) {
       const double* x = X + (size_t)p * cols;
       double acc = 0.0;
-      for (int k = 0; k < cols; ++k) acc += (double)w[k] * x[k];
+      for (int k = 0; k < cols; ++k) acc += w[k] * x[k];
       Y[(size_t)p * rows + o] = acc;
     }
   }
@@ -315,8 +341,8 @@ int32_t orc_forward(orc_model* m, const float* frame_hidden, const int32_t* in_c
   /* inputs: x_0 = frame hidden, x_s = E_{s-1}[code consumed at s] */
   for (int i = 0; i < H; ++i) x[i] = (double)frame_hidden[i];
   for (int s = 1; s < np; ++s) {
-    const float* e = m->emb[s - 1] + (size_t)in_codes[s - 1] * H;
-    for (int i = 0; i < H; ++i) x[(size_t)s * H + i] = (double)e[i];
+    const double* e = m->emb[s - 1] + (size_t)in_codes[s - 1] * H;
+    for (int i = 0; i < H; ++i) x[(size_t)s * H + i] = e[i];
   }
   const int32_t st = forward_rows(m, x, np, hfin);
   free(x);
@@ -340,7 +366,7 @@ int32_t orc_logits(orc_model* m, const double* h, int32_t head, int32_t offset, 
   const int H = m->cfg.hidden;
   double* v = (double*)malloc(sizeof(double) * H);
   if (!v) return ORC_ENOMEM;
-  for (int i = 0; i < H; ++i) v[i] = h[i] + (offset > 0 ? (double)m->offsets[(size_t)(offset - 1) * H + i] : 0.0);
+  for (int i = 0; i < H; ++i) v[i] = h[i] + (offset > 0 ? m->offsets[(size_t)(offset - 1) * H + i] : 0.0);
   matmul(m->lmh[head], m->cfg.vocab, H, v, 1, out);
   free(v);
   return ORC_OK;

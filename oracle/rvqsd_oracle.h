@@ -44,7 +44,7 @@ typedef struct {
   int32_t n_codes;   /* residual codes per frame (15 in the paper) */
   int32_t vocab;     /* codebook size per position */
   int32_t max_draft; /* number of offsets stored in the blob */
-  int32_t dtype;     /* matrix storage in the blob: 0 = f32, 1 = bf16 */
+  int32_t dtype;     /* matrix storage in the blob: 0 = f32, 1 = bf16, 2 = int8 codes with fp32 row scales */
   int32_t qk_norm;   /* 1: per-head RMSNorm of q and k before RoPE */
   int32_t topk;
   int32_t draft_len; /* K; 0 = plain autoregressive */

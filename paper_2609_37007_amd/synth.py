@@ -25,7 +25,12 @@ Weight blob layout (little endian, no padding between tensors)::
     LMH_1 .. LMH_{n_codes}    [V][H]   (LMH_s emits code c_s)
     b_1 .. b_{max_draft}      f32[H]   (position-aware draft offsets)
 
-All matrices are [out][in] row-major.  Values: N(0, std) from
+All matrices are [out][in] row-major.  With dtype 2 (int8, the W8A16 weights of
+Sec. 3.4) every matrix is stored as int8 codes q [out][in] followed by its fp32
+per-row (output channel) scales s [out], then zero bytes up to the next 16-byte
+boundary; the weight is s[o] * q[o][i]: s = max_i |w[o][i]| / 127 (fp32, computed
+in fp64), q = round-half-even(w / s) in [-127, 127], w being the fp32 value the
+other dtypes store (a row of zeros has s = 0 and q = 0).  Values: N(0, std) from
 ``numpy.random.default_rng(seed).standard_normal`` drawn tensor by tensor in
 the order above (norm gains are 1.0 and draw nothing); the LM heads are
 multiplied by ``head_scale`` before rounding; the offsets are drawn last (N(0,
@@ -43,6 +48,7 @@ MAGIC = b"RVQSDW1\0"
 VERSION = 1
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
+DTYPE_I8 = 2
 HEADER_BYTES = 64
 
 
@@ -75,6 +81,9 @@ TINY = ModelShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=4, head_dim=64
 # FFN 3072, codebook 2048, bf16 weights).
 MCD_1024 = ModelShape(n_layers=5, hidden=1024, n_q_heads=16, n_kv_heads=8, head_dim=128,
                       ffn=3072, n_codes=15, vocab=2048, max_draft=14, dtype=DTYPE_BF16)
+# The same model with W8A16 weights (int8 per output channel), the precision of Sec. 3.4.
+MCD_1024_W8 = ModelShape(n_layers=5, hidden=1024, n_q_heads=16, n_kv_heads=8, head_dim=128,
+                         ffn=3072, n_codes=15, vocab=2048, max_draft=14, dtype=DTYPE_I8)
 
 
 # The outer CodeDecoder of the full pipeline (Fig. 1): 28 layers of the same block, one
@@ -143,13 +152,36 @@ def tensor_list(s: ModelShape):
     return out
 
 
+def mat_bytes(s: ModelShape, shape) -> int:
+    """Bytes of one matrix in the blob (int8: codes, row scales, padding to 16 bytes)."""
+    cnt = int(np.prod(shape))
+    if s.dtype == DTYPE_I8:
+        raw = cnt + 4 * shape[0]
+        return (raw + 15) // 16 * 16
+    return cnt * (4 if s.dtype == DTYPE_F32 else 2)
+
+
 def blob_size(s: ModelShape) -> int:
-    wb = 4 if s.dtype == DTYPE_F32 else 2
     n = HEADER_BYTES
     for _, shape, kind in tensor_list(s):
-        cnt = int(np.prod(shape))
-        n += cnt * (wb if kind == "mat" else 4)
+        n += mat_bytes(s, shape) if kind == "mat" else 4 * int(np.prod(shape))
     return n
+
+
+def quantize_rows(w32: np.ndarray):
+    """Symmetric per-row int8: (q int8 [rows][cols], s float32 [rows])."""
+    w = np.asarray(w32, dtype=np.float32).astype(np.float64)
+    s = (np.abs(w).max(axis=1) / 127.0).astype(np.float32)
+    sd = s.astype(np.float64)
+    q = np.zeros(w.shape, dtype=np.float64)
+    nz = sd > 0
+    q[nz] = np.rint(w[nz] / sd[nz, None])
+    return np.clip(q, -127, 127).astype(np.int8), s
+
+
+def dequantize_rows(q: np.ndarray, s: np.ndarray) -> np.ndarray:
+    """The weights an int8 matrix stands for, exactly (float64)."""
+    return q.astype(np.float64) * np.asarray(s, dtype=np.float32).astype(np.float64)[:, None]
 
 
 def make_header(s: ModelShape) -> bytes:
@@ -176,6 +208,10 @@ def make_weights(s: ModelShape, seed: int = 0, std: float = 0.02, head_scale: fl
         v32 = v.astype(np.float32)
         if s.dtype == DTYPE_F32:
             parts.append(v32.tobytes())
+        elif s.dtype == DTYPE_I8:
+            q, sc = quantize_rows(v32)
+            raw = q.tobytes() + sc.tobytes()
+            parts.append(raw + b"\0" * (mat_bytes(s, shape) - len(raw)))
         else:
             parts.append(f32_to_bf16_bits(v32).tobytes())
     ostd = std if offset_std is None else offset_std
@@ -189,13 +225,19 @@ def make_weights(s: ModelShape, seed: int = 0, std: float = 0.02, head_scale: fl
 
 
 def unpack_weights(s: ModelShape, blob: bytes) -> dict:
-    """Decode the blob into float32 numpy arrays (bf16 matrices widened exactly)."""
+    """Decode the blob into float32 numpy arrays (bf16 matrices widened exactly; int8
+    matrices dequantized exactly into float64)."""
     wb = 4 if s.dtype == DTYPE_F32 else 2
     off = HEADER_BYTES
     out = {}
     for name, shape, kind in tensor_list(s):
         cnt = int(np.prod(shape))
-        if kind == "mat" and s.dtype == DTYPE_BF16:
+        if kind == "mat" and s.dtype == DTYPE_I8:
+            q = np.frombuffer(blob, dtype=np.int8, count=cnt, offset=off).reshape(shape)
+            sc = np.frombuffer(blob, dtype=np.float32, count=shape[0], offset=off + cnt)
+            out[name] = dequantize_rows(q, sc)
+            off += mat_bytes(s, shape)
+        elif kind == "mat" and s.dtype == DTYPE_BF16:
             a = np.frombuffer(blob, dtype=np.uint16, count=cnt, offset=off)
             out[name] = bf16_bits_to_f32(a).reshape(shape)
             off += cnt * 2

@@ -583,3 +583,78 @@ def test_pipeline_frames_outer_input_mask_and_c0_draw():
     assert hits_first_masked >= 1
     oorc.close()
     iorc.close()
+
+
+# ------------------------------------------------ W8A16 weights (Sec. 3.4)
+
+def _i8_shape(**kw):
+    d = dict(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, n_codes=6, vocab=32,
+             max_draft=5, dtype=S.DTYPE_I8)
+    d.update(kw)
+    return S.ModelShape(**d)
+
+
+def test_int8_blob_is_the_per_channel_quantization_of_the_fp32_draws():
+    """The int8 blob of a seed against the fp32 blob of the same seed: every row's scale is
+    its absmax / 127, every code the nearest integer of w / s (ties to even), |q| <= 127,
+    so the dequantized weight is within s / 2 of the fp32 one."""
+    s8 = _i8_shape()
+    s32 = _i8_shape(dtype=S.DTYPE_F32)
+    b8 = S.make_weights(s8, seed=7, std=0.3)
+    b32 = S.make_weights(s32, seed=7, std=0.3)
+    W32 = S.unpack_weights(s32, b32)
+    off = S.HEADER_BYTES
+    checked = 0
+    for name, shp, kind in S.tensor_list(s8):
+        if kind == "vec":
+            off += 4 * int(np.prod(shp))
+            continue
+        cnt = int(np.prod(shp))
+        q = np.frombuffer(b8, dtype=np.int8, count=cnt, offset=off).reshape(shp).astype(np.float64)
+        sc = np.frombuffer(b8, dtype=np.float32, count=shp[0], offset=off + cnt).astype(np.float64)
+        w = W32[name].astype(np.float64)
+        amax = np.abs(w).max(axis=1)
+        assert np.array_equal(sc, (amax / 127.0).astype(np.float32).astype(np.float64)), name
+        assert np.abs(q).max() <= 127 and (np.abs(q).max(axis=1) == 127).all(), name
+        assert np.array_equal(q, np.rint(w / sc[:, None])), name
+        assert (np.abs(w - q * sc[:, None]) <= sc[:, None] / 2 + 1e-12).all(), name
+        off += S.mat_bytes(s8, shp)
+        checked += 1
+    assert off == len(b8) and checked == 2 * 7 + 2 * 6
+
+
+def test_int8_forward_matches_torch_rebuild_over_dequantized_weights():
+    """The oracle's forward and heads on an int8 blob equal the independent fp64 rebuild over
+    the dequantized weights s * q."""
+    s = _i8_shape()
+    blob = S.make_weights(s, seed=8, std=0.3, offset_std=0.5)
+    W = S.unpack_weights(s, blob)
+    orc = Hh.make_oracle(s, blob, topk=4, temperature=0.9, draft_len=2)
+    f, c0 = S.frame_inputs(s, 2)
+    rng = np.random.default_rng(4)
+    for fr in range(2):
+        codes = [int(c0[fr])] + [int(x) for x in rng.integers(0, s.vocab, s.n_codes - 1)]
+        h = orc.forward(f[fr], codes)
+        ref = _torch_forward(s, W, f[fr], codes)
+        assert np.max(np.abs(h - ref)) < 1e-9
+        for sp in range(1, s.n_codes + 1):
+            np.testing.assert_allclose(orc.logits(h[sp], sp), W[f"lmh{sp}"] @ ref[sp], rtol=0, atol=1e-9)
+        np.testing.assert_allclose(orc.logits(h[2], 4, 2), W["lmh4"] @ (ref[2] + W["offsets"][1]), rtol=0, atol=1e-9)
+    orc.close()
+
+
+def test_int8_k0_is_autoregressive_and_speculation_is_lossless():
+    s = Hh.micro_shape(4, 3)
+    s = S.ModelShape(**{**{f: getattr(s, f) for f in s.__dataclass_fields__}, "dtype": S.DTYPE_I8})
+    blob = S.make_weights(s, seed=12, std=0.35, offset_std=0.5)
+    ar_orc = Hh.make_oracle(s, blob, topk=3, temperature=0.9, draft_len=0)
+    f, c0 = S.frame_inputs(s, 2)
+    u = S.uniforms(2, s.n_codes)
+    for i in range(2):
+        assert np.array_equal(ar_orc.spec_frame(f[i], int(c0[i]), u[i])[0], ar_orc.ar_frame(f[i], int(c0[i]), u[i]))
+    orc = Hh.make_oracle(s, blob, topk=3, temperature=0.9, draft_len=2)
+    ar = Hh.ar_law(orc, f[0], int(c0[0]), 3, 0.9)
+    law, _ = Hh.enumerate_law(Hh.spec_runner(orc, f[0], int(c0[0])), s.n_codes * 3)
+    assert max(abs(ar.get(k, 0.0) - law.get(k, 0.0)) for k in set(ar) | set(law)) <= 1e-12
+    ar_orc.close()
+    orc.close()
