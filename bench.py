@@ -54,6 +54,7 @@ PMC_SUMMARY = os.path.join(ROOT, "profiles", "frame_kernel_mcd1024_k4_hbm_traffi
 WORKLOADS = {
     # name: (shape, top-k, draft length, frames)
     "mcd1024": ("MCD_1024", 50, 4, 1000),
+    "mcd1024-w8": ("MCD_1024_W8", 50, 4, 1000),  # the same model with W8A16 weights (Sec. 3.4)
     "tiny": ("TINY", 8, 3, 32),
 }
 
@@ -698,12 +699,12 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if s.dtype == S.DTYPE_BF16 else "f32",
+        "dtype": {S.DTYPE_BF16: "bf16", S.DTYPE_I8: "int8 weights (W8A16), fp32 activations"}.get(s.dtype, "f32"),
         "data": "synthetic (random-init weights, seeded frame inputs and uniforms)",
         "config": {
             "workload": (f"{a.workload}: {s.n_layers} layers, hidden {s.hidden}, {s.n_q_heads}/{s.n_kv_heads} heads "
                          f"x {s.head_dim}, ffn {s.ffn}, {s.n_codes} codebooks of {s.vocab}, "
-                         f"{'bf16' if s.dtype == S.DTYPE_BF16 else 'fp32'} weights; "
+                         f"{ {S.DTYPE_BF16: 'bf16', S.DTYPE_I8: 'int8 (per-channel scales)'}.get(s.dtype, 'fp32')} weights; "
                          + (f"sparse tree of {len(tree[0])} nodes, depth {K}" if tree else f"draft length {K}")
                          + f", top-k {topk}, temperature {temperature}, batch 1"),
             "tree_nodes": len(tree[0]) if tree else 0,

@@ -45,6 +45,11 @@ typedef int32_t rvqsd_status;
 
 #define RVQSD_DTYPE_F32 0
 #define RVQSD_DTYPE_BF16 1
+/* W8A16 (Sec. 3.4): int8 codes per matrix row followed by the row's fp32 scale
+ * (weight = scale * code), zero-padded to 16 bytes; decoded on MFMA with the
+ * activations at fp32 accuracy (bf16 hi + lo); draft_len <= 7, single-frame
+ * calls and the allocation-free decode only */
+#define RVQSD_DTYPE_I8 2
 
 /* Model configuration. The shape fields must equal the weight blob's header. */
 typedef struct {

@@ -122,7 +122,7 @@ int validate_cfg(const rvqsd_cfg* c, int nwg) {
   if (c->n_layers <= 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
       c->ffn <= 0 || c->n_codes < 1 || c->n_codes > kMaxCodes || c->vocab < 2 || c->max_draft < 0 ||
       c->topk < 1 || c->draft_len < 0 || c->draft_len > c->max_draft || !(c->temperature > 0.0) ||
-      !(c->rms_eps > 0.0) || !(c->rope_base > 0.0) || (c->dtype != RVQSD_DTYPE_F32 && c->dtype != RVQSD_DTYPE_BF16) ||
+      !(c->rms_eps > 0.0) || !(c->rope_base > 0.0) || (c->dtype < RVQSD_DTYPE_F32 || c->dtype > RVQSD_DTYPE_I8) ||
       (c->n_q_heads % c->n_kv_heads) != 0 || (c->qk_norm != 0 && c->qk_norm != 1) ||
       (c->draft_greedy != 0 && c->draft_greedy != 1))
     return set_err(RVQSD_EINVAL, "invalid configuration field");
@@ -163,15 +163,16 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
   auto need = [&](size_t f) {
     if (f > w) w = f;
   };
-  if (c->dtype == RVQSD_DTYPE_BF16 && mr <= 8) {
+  if (c->dtype != RVQSD_DTYPE_F32 && mr <= 8) {
     // MFMA phases: split activations, chunk sums of squares, wave partial tiles, outputs
     // split rows carry 4 words of padding; wave partials: 1 tile (QKV, O, down),
     // 2 (gate/up), 5 (heads) at a time
-    need((size_t)mr * (H + 4) + (size_t)mr * (H / 8) + kWaves * 256 + tiles(rpw_qkv) * 16 * mr + (size_t)mr * H);
-    need((size_t)mr * (H + 4) + (size_t)mr * (H / 8) + kWaves * 2 * 256 + tiles(2 * fpw) * 16 * mr);
-    need((size_t)mr * (qd + 4) + kWaves * 256 + tiles(cpw) * 16 * mr);
-    need((size_t)mr * (F + 4) + kWaves * 256 + tiles(cpw) * 16 * mr);
-    need((size_t)mr * H + (size_t)mr * (H + 4) + kWaves * 5 * 256 + tiles(rpw_heads) * 16 * mr);
+    // (+ one row scale per output row for int8 weights)
+    need((size_t)mr * (H + 4) + (size_t)mr * (H / 8) + kWaves * 256 + tiles(rpw_qkv) * 16 * (mr + 1) + (size_t)mr * H);
+    need((size_t)mr * (H + 4) + (size_t)mr * (H / 8) + kWaves * 2 * 256 + tiles(2 * fpw) * 16 * (mr + 1));
+    need((size_t)mr * (qd + 4) + kWaves * 256 + tiles(cpw) * 16 * (mr + 1));
+    need((size_t)mr * (F + 4) + kWaves * 256 + tiles(cpw) * 16 * (mr + 1));
+    need((size_t)mr * H + (size_t)mr * (H + 4) + kWaves * 5 * 256 + tiles(rpw_heads) * 16 * (mr + 1));
   } else {
     int rows_out = rpw_qkv;
     if (2 * fpw > rows_out) rows_out = 2 * fpw;
@@ -401,24 +402,29 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   k.temperature = cfg->temperature;
   k.rope_base = cfg->rope_base;
   k.nwg = nwg;
-  const uint64_t wb = cfg->dtype == RVQSD_DTYPE_F32 ? 4 : 2;
+  const uint64_t wb = cfg->dtype == RVQSD_DTYPE_F32 ? 4 : (cfg->dtype == RVQSD_DTYPE_BF16 ? 2 : 1);
   const uint64_t H = k.H, qd = k.qdim, kd = k.kvdim, F = k.F, d = k.d, V = k.V, n = k.n_codes;
+  // bytes of a [rows][cols] matrix: int8 codes are followed by fp32 row scales, padded to 16 bytes
+  auto mat = [&](uint64_t rows, uint64_t cols) -> uint64_t {
+    return cfg->dtype == RVQSD_DTYPE_I8 ? (rows * cols + 4 * rows + 15) / 16 * 16 : rows * cols * wb;
+  };
   uint64_t o = 0;
   k.o_attn_norm = o; o += H * 4;
-  k.o_wq = o; o += qd * H * wb;
-  k.o_wk = o; o += kd * H * wb;
-  k.o_wv = o; o += kd * H * wb;
+  k.o_wq = o; o += mat(qd, H);
+  k.o_wk = o; o += mat(kd, H);
+  k.o_wv = o; o += mat(kd, H);
   k.o_qn = o; o += d * 4;
   k.o_kn = o; o += d * 4;
-  k.o_wo = o; o += H * qd * wb;
+  k.o_wo = o; o += mat(H, qd);
   k.o_mlp_norm = o; o += H * 4;
-  k.o_wg = o; o += F * H * wb;
-  k.o_wu = o; o += F * H * wb;
-  k.o_wd = o; o += H * F * wb;
+  k.o_wg = o; o += mat(F, H);
+  k.o_wu = o; o += mat(F, H);
+  k.o_wd = o; o += mat(H, F);
   k.layer_stride = o;
   o = k.layer_stride * k.L;
   k.o_final_norm = o; o += H * 4;
-  k.table_stride = V * H * wb;
+  k.table_stride = mat(V, H);
+  k.emb_row_bytes = cfg->dtype == RVQSD_DTYPE_I8 ? H + 4 : H * wb;
   k.o_emb0 = o; o += n * k.table_stride;
   k.o_lmh1 = o; o += n * k.table_stride;
   k.o_offsets = o; o += (uint64_t)cfg->max_draft * H * 4;
@@ -431,7 +437,21 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   m->device = dev;
   m->nwg = nwg;
   m->mr = frame_max_rows(cfg->draft_len);
-  if (cfg->dtype == RVQSD_DTYPE_BF16 && m->mr <= 8 &&
+  if (cfg->dtype == RVQSD_DTYPE_I8 && m->mr > 8) {
+    delete m;
+    return set_err(RVQSD_EUNSUPPORTED, "int8 weights run on the matrix-core path only: draft_len <= 7");
+  }
+  if (cfg->dtype == RVQSD_DTYPE_I8) {
+    // every workgroup holds one row scale per thread for the head rows it multiplies
+    int nh = 2 * cfg->draft_len + 1 < cfg->n_codes ? 2 * cfg->draft_len + 1 : cfg->n_codes;
+    if (nh < 1) nh = 1;
+    const int rpw = (cfg->vocab + nwg / nh - 1) / (nwg / nh);
+    if (rpw > kThreads || (int)((k.nqkv + nwg - 1) / nwg) > kThreads || 2 * (int)((k.F + nwg - 1) / nwg) > kThreads) {
+      delete m;
+      return set_err(RVQSD_EUNSUPPORTED, "int8 weights: a workgroup's rows of one matrix exceed %d", kThreads);
+    }
+  }
+  if (cfg->dtype != RVQSD_DTYPE_F32 && m->mr <= 8 &&
       (k.H > 512 * kUptH || k.qdim > 512 * kUptQ || k.F > 512 * kUptF)) {
     delete m;
     return set_err(RVQSD_EUNSUPPORTED, "bf16 matrix path takes hidden <= %d, n_q_heads*head_dim <= %d, ffn <= %d",
@@ -516,7 +536,7 @@ rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out) {
   out->lds_bytes = m->lds_bytes;
   out->layer_weight_bytes = m->base.layer_stride * (uint64_t)m->base.L;
   out->head_bytes = m->base.table_stride;
-  out->emb_row_bytes = (uint64_t)m->base.H * m->wbytes;
+  out->emb_row_bytes = m->base.emb_row_bytes;
   out->device_weight_bytes = m->dweight_bytes;
   return RVQSD_OK;
 }

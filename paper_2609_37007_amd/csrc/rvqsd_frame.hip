@@ -372,10 +372,46 @@ template <>
 struct IsBf16<bf16_t> {
   static constexpr bool value = true;
 };
+// int8 weight codes with fp32 per-row scales (W8A16): MFMA path only
+template <typename WT>
+struct IsI8 {
+  static constexpr bool value = false;
+};
+template <>
+struct IsI8<int8_t> {
+  static constexpr bool value = true;
+};
 template <typename WT, int MR>
 struct UseMfma {
-  static constexpr bool value = IsBf16<WT>::value && MR <= 8;
+  static constexpr bool value = (IsBf16<WT>::value || IsI8<WT>::value) && MR <= 8;
 };
+
+// Scale of row `row` of the [rows][cols] matrix at byte offset off: its fp32 row scale for
+// int8 codes (stored after the codes), 1 otherwise.
+template <typename WE>
+__device__ __forceinline__ float row_scale(const KParams* p, uint64_t off, int rows, int cols, int row) {
+  if constexpr (IsI8<WE>::value)
+    return G(reinterpret_cast<const float*>(p->wbase + off + (uint64_t)rows * cols))[row];
+  else
+    return 1.f;
+}
+
+// 16 int8 codes (one 16-byte load) -> the same values as two groups of 8 bf16 (exact:
+// every integer in [-128, 127] is a bf16)
+__device__ __forceinline__ uint32_t i8pair_bf16(uint32_t w, int sh) {
+  const float f0 = (float)(int8_t)(uint8_t)(w >> sh), f1 = (float)(int8_t)(uint8_t)(w >> (sh + 8));
+  return (__float_as_uint(f0) >> 16) | (__float_as_uint(f1) & 0xffff0000u);
+}
+__device__ __forceinline__ void widen_i8x16(const W16& v, W16& lo, W16& hi) {
+  lo[0] = i8pair_bf16(v[0], 0);
+  lo[1] = i8pair_bf16(v[0], 16);
+  lo[2] = i8pair_bf16(v[1], 0);
+  lo[3] = i8pair_bf16(v[1], 16);
+  hi[0] = i8pair_bf16(v[2], 0);
+  hi[1] = i8pair_bf16(v[2], 16);
+  hi[2] = i8pair_bf16(v[3], 0);
+  hi[3] = i8pair_bf16(v[3], 16);
+}
 
 // Split activations in LDS: row m, 8-element chunk q -> 8 words at m * (K + 4) + q * 8:
 // 4 words of hi, then 4 words of lo. The 4 words of padding per row put the 16
@@ -534,7 +570,7 @@ __device__ __forceinline__ void rstd_from_chunks(const Ctx& c, const float* sqc,
 // every 16-row tile, so one read of a unit's B operand serves all tiles. Up to
 // NT tiles are held at a time (tile groups), UPT >= upt. Each wave writes its
 // partial tiles to red[kWaves][NT][256]; reduce() adds the 8 partials.
-template <int MR, int NT, int UPT>
+template <int MR, int NT, int UPT, typename WE = bf16_t>
 struct MTile {
   int U, upt, ntiles, nrows, wave, lane;
   W16 a[NT][UPT][2];
@@ -557,9 +593,9 @@ struct MTile {
       for (int j = 0; j < UPT; ++j) {
         W16 v0 = (W16)(0u), v1 = (W16)(0u);
         if (tb + tt < ntiles && j < upt && row < nrows) {
-          const bf16_t* w = rowptr(row) + (wave + 8 * j) * 64 + 16 * (lane >> 4);
-          v0 = *G(reinterpret_cast<const W16*>(w));
-          v1 = *G(reinterpret_cast<const W16*>(w + 8));
+          const WE* w = rowptr(row) + (wave + 8 * j) * 64 + 16 * (lane >> 4);
+          v0 = *G(reinterpret_cast<const W16*>(w));  // int8: all 16 codes
+          if constexpr (!IsI8<WE>::value) v1 = *G(reinterpret_cast<const W16*>(w + 8));
         }
         a[tt][j][0] = v0;
         a[tt][j][1] = v1;
@@ -599,7 +635,9 @@ struct MTile {
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt) {
           if (tb + tt < ntiles) {
-            const bf16x8 a0 = __builtin_bit_cast(bf16x8, a[tt][j][0]), a1 = __builtin_bit_cast(bf16x8, a[tt][j][1]);
+            W16 w0 = a[tt][j][0], w1 = a[tt][j][1];
+            if constexpr (IsI8<WE>::value) widen_i8x16(a[tt][j][0], w0, w1);
+            const bf16x8 a0 = __builtin_bit_cast(bf16x8, w0), a1 = __builtin_bit_cast(bf16x8, w1);
             acc[tt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, b[j][0]), acc[tt][0], 0, 0, 0);
             acc[tt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, b[j][1]), acc[tt][1], 0, 0, 0);
             acc[tt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, b[j][2]), acc[tt][0], 0, 0, 0);
@@ -633,7 +671,7 @@ struct MTile {
   // one tile group (ntiles <= NT, weights preloaded), wave partials in red after the barrier;
   // psum(red, r, m) then gives the product of row r and activation row m
   __device__ __forceinline__ void run1(const uint32_t* xsp, int R, float* red) {
-    mma(0, true, [](int) -> const bf16_t* { return nullptr; }, xsp, R, red);
+    mma(0, true, [](int) -> const WE* { return nullptr; }, xsp, R, red);
     lds_barrier();
   }
   __device__ __forceinline__ float psum(const float* red, int r, int m) const {
@@ -733,7 +771,7 @@ __device__ __forceinline__ void gather_rows(const Ctx& c, float* xs) {
 // one 16-byte embedding load; this workgroup's residual columns go to xown, the
 // gain-scaled values to xsp, and one sum of squares per wave (64 chunks of one
 // row, hidden a multiple of 512) to sqc. Rows R.. of xown are zero.
-template <int MR>
+template <typename WE, int MR>
 __device__ __forceinline__ void gather_split_rows(const Ctx& c, uint32_t* xsp, const float* gain, float* sqc) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -750,6 +788,14 @@ __device__ __forceinline__ void gather_split_rows(const Ctx& c, uint32_t* xsp, c
       if (s == 0) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) x[e] = G(sh->fa.frame_hidden)[8 * q + e];
+      } else if constexpr (IsI8<WE>::value) {
+        // int8 row: 8 codes times the row's scale
+        const uint64_t toff = p->o_emb0 + (uint64_t)(s - 1) * p->table_stride;
+        const int code = sh->in_code[s];
+        const uint64_t w = *G(reinterpret_cast<const uint64_t*>(p->wbase + toff + (size_t)code * H + 8 * q));
+        const float sc = row_scale<WE>(p, toff, p->V, H, code);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = (float)(int8_t)(uint8_t)(w >> (8 * e)) * sc;
       } else {
         const bf16_t* tab = wptr<bf16_t>(p, p->o_emb0 + (uint64_t)(s - 1) * p->table_stride);
         const W16 w = *G(reinterpret_cast<const W16*>(tab + (size_t)sh->in_code[s] * H + 8 * q));
@@ -1124,24 +1170,25 @@ __device__ __forceinline__ bool phase_gu(const Ctx& c, int l) {
 // Same partition of weight rows over workgroups as the phases above; the
 // weights of the first round are loaded before the wait for the activations.
 
-template <int MR>
+template <typename WE, int MR>
 __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
   const int H = p->H, R = sh->rows, N = p->nqkv;
   const int rpw = (N + p->nwg - 1) / p->nwg, row0 = blockIdx.x * rpw;
   const int nrows = max(0, min(rpw, N - row0));
-  const bf16_t* wq = wptr<bf16_t>(p, layer_off(p, l, p->o_wq));
-  const bf16_t* wk = wptr<bf16_t>(p, layer_off(p, l, p->o_wk));
-  const bf16_t* wv = wptr<bf16_t>(p, layer_off(p, l, p->o_wv));
+  const uint64_t oq = layer_off(p, l, p->o_wq), ok = layer_off(p, l, p->o_wk), ov = layer_off(p, l, p->o_wv);
+  const WE* wq = wptr<WE>(p, oq);
+  const WE* wk = wptr<WE>(p, ok);
+  const WE* wv = wptr<WE>(p, ov);
   const int qd = p->qdim, kd = p->kvdim;
-  auto rowptr = [&](int r) -> const bf16_t* {
+  auto rowptr = [&](int r) -> const WE* {
     const int o = row0 + r;
     if (o < qd) return wq + (size_t)o * H;
     if (o < qd + kd) return wk + (size_t)(o - qd) * H;
     return wv + (size_t)(o - qd - kd) * H;
   };
-  MTile<MR, 1, kUptH> mt;
+  MTile<MR, 1, kUptH, WE> mt;
   mt.setup(H, nrows);
   mt.load(0, rowptr);
   const float* gain = fptr(p, layer_off(p, l, p->o_attn_norm));
@@ -1149,18 +1196,36 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
   float* sqc = c.work + MR * (H + 4);                   // [MR][H/8]
   float* red = sqc + MR * (H >> 3);                     // [kWaves][1][256]
   float* out = red + kWaves * 256;                      // [nrows][MR]
+  float* rsc = out + (size_t)((nrows + 15) & ~15) * MR;  // [nrows] row scales (int8 weights)
+  // int8: the row scales are loaded into registers with the weights and reach LDS only
+  // after the input wait (a store now would wait for every load in flight)
+  float sc_reg = 0.f;
+  if constexpr (IsI8<WE>::value) {
+    if (tid() < nrows) {
+      const int o = row0 + tid();
+      sc_reg = o < qd ? row_scale<WE>(p, oq, qd, H, o)
+                      : (o < qd + kd ? row_scale<WE>(p, ok, kd, H, o - qd) : row_scale<WE>(p, ov, kd, H, o - qd - kd));
+    }
+  }
+  auto scale = [&](int r) -> float {
+    if constexpr (IsI8<WE>::value) return rsc[r];
+    else return 1.f;
+  };
   if (l == 0) {
-    gather_split_rows<MR>(c, xsp, gain, sqc);
+    gather_split_rows<WE, MR>(c, xsp, gain, sqc);
   } else {
     if (nrows == 0) return true;
     if (!stage_split<2, true>(c, p->xb, H, R, kParDown, gain, xsp, sqc)) return false;
   }
+  if constexpr (IsI8<WE>::value)
+    if (tid() < nrows) rsc[tid()] = sc_reg;  // read after the tile barrier below
   if (nrows > 0 && mt.ntiles <= 1) {
     mt.run1(xsp, R, red);
     const uint32_t par = par_layer(c, sh->pass, l);
     for (int i = tid(); i < MR * nrows; i += kThreads) {
       const int r = i / MR, m = i - r * MR;
-      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? mt.psum(red, r, m) * rstd_of(c, sqc, H, m) : 0.f, par);
+      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? mt.psum(red, r, m) * scale(r) * rstd_of(c, sqc, H, m) : 0.f,
+             par);
     }
   } else if (nrows > 0) {
     rstd_from_chunks_w(c, sqc, H, R);
@@ -1168,7 +1233,7 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
     const uint32_t par = par_layer(c, sh->pass, l);
     for (int i = tid(); i < MR * nrows; i += kThreads) {
       const int m = i / nrows, r = i % nrows;
-      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] : 0.f, par);
+      pstore(p->qkvb + (size_t)m * N + row0 + r, m < R ? out[r * MR + m] * scale(r) : 0.f, par);
     }
   }
   lds_barrier();  // the work area is reused by the next phase
@@ -1176,7 +1241,7 @@ __device__ __forceinline__ bool phase_qkv_m(const Ctx& c, int l) {
 }
 
 // O projection (layer l) or down projection: x_own += W * act; publish x_own.
-template <int MR, int CB, int UPT>
+template <typename WE, int MR, int CB, int UPT>
 __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -1185,17 +1250,28 @@ __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) 
   const int row0 = blockIdx.x * c.cpw;
   const int nrows = max(0, min(c.cpw, H - row0));
   if (nrows == 0) return true;
-  const bf16_t* W = wptr<bf16_t>(p, layer_off(p, l, is_down ? p->o_wd : p->o_wo));
-  auto rowptr = [&](int r) -> const bf16_t* { return W + (size_t)(row0 + r) * K; };
-  MTile<MR, 1, UPT> mt;
+  const uint64_t ow = layer_off(p, l, is_down ? p->o_wd : p->o_wo);
+  const WE* W = wptr<WE>(p, ow);
+  auto rowptr = [&](int r) -> const WE* { return W + (size_t)(row0 + r) * K; };
+  MTile<MR, 1, UPT, WE> mt;
   mt.setup(K, nrows);
   mt.load(0, rowptr);
   uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);  // [MR][K + 4] split
   float* red = c.work + MR * (K + 4);                   // [kWaves][1][256]
   float* out = red + kWaves * 256;                      // [nrows][MR]
+  float* rsc = out + (size_t)((nrows + 15) & ~15) * MR;  // [nrows] row scales (int8 weights)
+  float sc_reg = 0.f;
+  if constexpr (IsI8<WE>::value)
+    if (tid() < nrows) sc_reg = row_scale<WE>(p, ow, H, K, row0 + tid());
+  auto scale = [&](int r) -> float {
+    if constexpr (IsI8<WE>::value) return rsc[r];
+    else return 1.f;
+  };
   const uint32_t* src = is_down ? p->actb : p->attnb;
   const uint32_t par = par_layer(c, sh->pass, l);
   if (!stage_split<CB, false>(c, src, K, R, par, nullptr, xsp, nullptr)) return false;
+  if constexpr (IsI8<WE>::value)
+    if (tid() < nrows) rsc[tid()] = sc_reg;
   const uint32_t xpar = is_down ? kParDown : kParO;
   if (mt.ntiles <= 1) {
     mt.run1(xsp, R, red);
@@ -1203,7 +1279,7 @@ __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) 
       const int r = i / MR, m = i - r * MR;
       float v = 0.f;
       if (m < R) {
-        v = c.xown[m * c.cpw + r] + mt.psum(red, r, m);
+        v = c.xown[m * c.cpw + r] + mt.psum(red, r, m) * scale(r);
         c.xown[m * c.cpw + r] = v;
       }
       pstore(p->xb + (size_t)m * H + row0 + r, v, xpar);
@@ -1214,7 +1290,7 @@ __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) 
       const int m = i / nrows, r = i % nrows;
       float v = 0.f;
       if (m < R) {
-        v = c.xown[m * c.cpw + r] + out[r * MR + m];
+        v = c.xown[m * c.cpw + r] + out[r * MR + m] * scale(r);
         c.xown[m * c.cpw + r] = v;
       }
       pstore(p->xb + (size_t)m * H + row0 + r, v, xpar);
@@ -1225,7 +1301,7 @@ __device__ __forceinline__ bool phase_proj_m(const Ctx& c, int l, bool is_down) 
 }
 
 // gate and up rows interleaved (2j = gate row f0 + j, 2j + 1 = up row); act = SiLU(gate) * up.
-template <int MR>
+template <typename WE, int MR>
 __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
@@ -1233,18 +1309,29 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
   const int fpw = (F + p->nwg - 1) / p->nwg, f0 = blockIdx.x * fpw;
   const int nf = max(0, min(fpw, F - f0));
   if (nf == 0) return true;
-  const bf16_t* wg = wptr<bf16_t>(p, layer_off(p, l, p->o_wg));
-  const bf16_t* wu = wptr<bf16_t>(p, layer_off(p, l, p->o_wu));
-  auto rowptr = [&](int r) -> const bf16_t* { return ((r & 1) ? wu : wg) + (size_t)(f0 + (r >> 1)) * H; };
-  MTile<MR, 2, kUptH> mt;
+  const uint64_t og = layer_off(p, l, p->o_wg), ou = layer_off(p, l, p->o_wu);
+  const WE* wg = wptr<WE>(p, og);
+  const WE* wu = wptr<WE>(p, ou);
+  auto rowptr = [&](int r) -> const WE* { return ((r & 1) ? wu : wg) + (size_t)(f0 + (r >> 1)) * H; };
+  MTile<MR, 2, kUptH, WE> mt;
   mt.setup(H, 2 * nf);
   mt.load(0, rowptr);
   uint32_t* xsp = reinterpret_cast<uint32_t*>(c.work);  // [MR][H + 4] split
   float* sqc = c.work + MR * (H + 4);                   // [MR][H/8]
   float* red = sqc + MR * (H >> 3);                     // [kWaves][2][256]
   float* out = red + kWaves * 2 * 256;                  // [2 nf][MR]
+  float* rsc = out + (size_t)((2 * nf + 15) & ~15) * MR;  // [2 nf] row scales (int8 weights)
+  float sc_reg = 0.f;
+  if constexpr (IsI8<WE>::value)
+    if (tid() < 2 * nf) sc_reg = row_scale<WE>(p, (tid() & 1) ? ou : og, F, H, f0 + (tid() >> 1));
+  auto scale = [&](int r) -> float {
+    if constexpr (IsI8<WE>::value) return rsc[r];
+    else return 1.f;
+  };
   const float* gain = fptr(p, layer_off(p, l, p->o_mlp_norm));
   if (!stage_split<2, true>(c, p->xb, H, R, kParO, gain, xsp, sqc)) return false;
+  if constexpr (IsI8<WE>::value)
+    if (tid() < 2 * nf) rsc[tid()] = sc_reg;
   const uint32_t par = par_layer(c, sh->pass, l);
   if (mt.ntiles <= 2) {
     mt.run1(xsp, R, red);
@@ -1253,7 +1340,7 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
       float a = 0.f;
       if (m < R) {
         const float rs = rstd_of(c, sqc, H, m);
-        const float gt = mt.psum(red, 2 * j, m) * rs, up = mt.psum(red, 2 * j + 1, m) * rs;
+        const float gt = mt.psum(red, 2 * j, m) * scale(2 * j) * rs, up = mt.psum(red, 2 * j + 1, m) * scale(2 * j + 1) * rs;
         a = gt / (1.f + expf(-gt)) * up;
       }
       pstore(p->actb + (size_t)m * F + f0 + j, a, par);
@@ -1265,7 +1352,7 @@ __device__ __forceinline__ bool phase_gu_m(const Ctx& c, int l) {
       const int m = i / nf, j = i % nf;
       float a = 0.f;
       if (m < R) {
-        const float gt = out[(2 * j) * MR + m], up = out[(2 * j + 1) * MR + m];
+        const float gt = out[(2 * j) * MR + m] * scale(2 * j), up = out[(2 * j + 1) * MR + m] * scale(2 * j + 1);
         a = gt / (1.f + expf(-gt)) * up;
       }
       pstore(p->actb + (size_t)m * F + f0 + j, a, par);
@@ -1367,7 +1454,7 @@ __device__ __forceinline__ bool phase_heads(const Ctx& c) {
 // LM heads on MFMA: same head/row assignment as phase_heads. The vectors of a
 // head (verify rows and h_s + b_j draft rows, final-normed) form the B columns;
 // the head's rows are processed in groups of 4 tiles.
-template <int MR>
+template <typename WE, int MR>
 __device__ __forceinline__ bool phase_heads_m(const Ctx& c) {
   const KParams* p = c.p;
   Shared* sh = c.sh;
@@ -1386,10 +1473,11 @@ __device__ __forceinline__ bool phase_heads_m(const Ctx& c) {
   const int rpw = (V + wph - 1) / wph, v0 = (blockIdx.x % wph) * rpw;
   const int nrows = hi < nh ? max(0, min(rpw, V - v0)) : 0;
   if (nrows == 0) return true;
-  const bf16_t* W = wptr<bf16_t>(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
-  auto rowptr = [&](int r) -> const bf16_t* { return W + (size_t)(v0 + r) * H; };
+  const uint64_t oh = p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride;
+  const WE* W = wptr<WE>(p, oh);
+  auto rowptr = [&](int r) -> const WE* { return W + (size_t)(v0 + r) * H; };
   constexpr int TG = 5;  // tiles per group
-  MTile<MR, TG, kUptH> mt;
+  MTile<MR, TG, kUptH, WE> mt;
   mt.setup(H, nrows);
   mt.load(0, rowptr);
   if (tid() == 0) {
@@ -1417,6 +1505,10 @@ __device__ __forceinline__ bool phase_heads_m(const Ctx& c) {
   uint32_t* vsp = reinterpret_cast<uint32_t*>(xs + MR * H);   // [MR][H + 4] split vectors
   float* red = xs + MR * H + MR * (H + 4);                    // [kWaves][TG][256]
   float* out = red + kWaves * TG * 256;                       // [nrows][MR]
+  float* rsc = out + (size_t)((nrows + 15) & ~15) * MR;       // [nrows] row scales (int8 weights)
+  float sc_reg = 0.f;
+  if constexpr (IsI8<WE>::value)
+    if (tid() < nrows) sc_reg = row_scale<WE>(p, oh, V, H, v0 + tid());
   for (int base = 0; base < nv * nch; base += VC * kThreads) {
     float gq[VC][8], oq[VC][8];
 #pragma unroll
@@ -1447,12 +1539,16 @@ __device__ __forceinline__ bool phase_heads_m(const Ctx& c) {
       }
     }
   }
+  if constexpr (IsI8<WE>::value)
+    if (tid() < nrows) rsc[tid()] = sc_reg;
   __syncthreads();
   mt.run(rowptr, vsp, nv, red, out, nullptr);
   const uint32_t tag = tag_of(c, sh->pass, ph_heads(L));
   for (int i = tid(); i < nv * nrows; i += kThreads) {
     const int v = i / nrows, r = i % nrows;
-    xstoref(p->logb + ((size_t)(sh->pass & 1) * p->n_slots + sh->hv_slot[v]) * V + v0 + r, tag, out[r * MR + v]);
+    float lgt = out[r * MR + v];
+    if constexpr (IsI8<WE>::value) lgt *= rsc[r];
+    xstoref(p->logb + ((size_t)(sh->pass & 1) * p->n_slots + sh->hv_slot[v]) * V + v0 + r, tag, lgt);
   }
   lds_barrier();  // the work area is reused by the next phase
   return true;
@@ -1716,7 +1812,7 @@ __device__ __forceinline__ bool commit_and_advance(const Ctx& c) {
 
 // algorithmic bytes one pass must read: layer weights, the heads it touches,
 // the gathered embedding rows and the KV cache it attends over
-__device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c, int wbytes) {
+__device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
   int t_lo = 1 << 20, t_hi = -1;
@@ -1727,8 +1823,8 @@ __device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c, int wbyte
     if (nd > 0) { t_lo = min(t_lo, s + 1); t_hi = max(t_hi, s + nd); }
   }
   unsigned long long b = (unsigned long long)p->L * p->layer_stride;
-  b += (unsigned long long)(t_hi - t_lo + 1) * p->V * p->H * wbytes;
-  for (int r = 0; r < sh->rows; ++r) b += (sh->first_pos + r == 0) ? 4ull * p->H : (unsigned long long)p->H * wbytes;
+  b += (unsigned long long)(t_hi - t_lo + 1) * p->table_stride;
+  for (int r = 0; r < sh->rows; ++r) b += (sh->first_pos + r == 0) ? 4ull * p->H : (unsigned long long)p->emb_row_bytes;
   b += (unsigned long long)p->L * (sh->first_pos + sh->rows) * p->nkv * p->d * 2 * 4;
   return b;
 }
@@ -1781,10 +1877,9 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   }
   __syncthreads();
   bool ok = c0_ok;
-  const int wbytes = (int)sizeof(WT);
   const int L = p->L;
   while (ok) {
-    if (blockIdx.x == 0 && tid() == 0) shs.st_bytes += pass_bytes(c, wbytes);
+    if (blockIdx.x == 0 && tid() == 0) shs.st_bytes += pass_bytes(c);
     const int nph = phases_per_pass(L) + 1;
     const bool clk_on = blockIdx.x == 0 && p->tr_clock && shs.pass < p->tr_max_rounds;
     uint64_t* clk_row = clk_on ? p->tr_clock + (size_t)shs.pass * nph : nullptr;
@@ -1803,7 +1898,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   } while (0)
     for (int l = 0; l < L && ok; ++l) {
       RVQSD_READY(5 * l + 0);
-      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<MR>(c, l);
+      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<WT, MR>(c, l);
       else ok = phase_qkv<WT, MR, 4>(c, l);
       RVQSD_STAMP(5 * l + 0);
       RVQSD_READY(5 * l + 1);
@@ -1811,21 +1906,21 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
       RVQSD_STAMP(5 * l + 1);
       RVQSD_READY(5 * l + 2);
       if constexpr (UseMfma<WT, MR>::value) {
-        if (ok) ok = phase_proj_m<MR, (MR + 1) / 2, kUptQ>(c, l, false);
+        if (ok) ok = phase_proj_m<WT, MR, (MR + 1) / 2, kUptQ>(c, l, false);
       } else {
         if (ok) ok = phase_proj<WT, MR, 4>(c, l, false);
       }
       RVQSD_STAMP(5 * l + 2);
       RVQSD_READY(5 * l + 3);
       if constexpr (UseMfma<WT, MR>::value) {
-        if (ok) ok = phase_gu_m<MR>(c, l);
+        if (ok) ok = phase_gu_m<WT, MR>(c, l);
       } else {
         if (ok) ok = phase_gu<WT, MR, (MR <= 8 ? 8 : 4)>(c, l);
       }
       RVQSD_STAMP(5 * l + 3);
       RVQSD_READY(5 * l + 4);
       if constexpr (UseMfma<WT, MR>::value) {
-        if (ok) ok = phase_proj_m<MR, (3 * MR + 3) / 4, kUptF>(c, l, true);
+        if (ok) ok = phase_proj_m<WT, MR, (3 * MR + 3) / 4, kUptF>(c, l, true);
       } else {
         if (ok) ok = phase_proj<WT, MR, 4>(c, l, true);
       }
@@ -1833,7 +1928,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     }
     RVQSD_READY(ph_heads(L));
     if constexpr (UseMfma<WT, MR>::value) {
-      if (ok) ok = phase_heads_m<MR>(c);
+      if (ok) ok = phase_heads_m<WT, MR>(c);
     } else {
       if (ok) ok = phase_heads<WT, MR, (MR <= 5 ? 8 : 4)>(c);
     }
@@ -1918,6 +2013,8 @@ int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int
   if (mr == M) return launch_t<T, M>(gp, fa, nwg, stream, lds_bytes, err, errlen);
   if (dtype == RVQSD_DTYPE_F32) {
     RVQSD_CASE(float, 2) RVQSD_CASE(float, 4) RVQSD_CASE(float, 5) RVQSD_CASE(float, 8) RVQSD_CASE(float, 16)
+  } else if (dtype == RVQSD_DTYPE_I8) {
+    RVQSD_CASE(int8_t, 2) RVQSD_CASE(int8_t, 4) RVQSD_CASE(int8_t, 5) RVQSD_CASE(int8_t, 8)
   } else {
     RVQSD_CASE(bf16_t, 2) RVQSD_CASE(bf16_t, 4) RVQSD_CASE(bf16_t, 5) RVQSD_CASE(bf16_t, 8) RVQSD_CASE(bf16_t, 16)
   }

@@ -39,6 +39,7 @@ struct KParams {
   uint64_t layer_stride;
   uint64_t o_attn_norm, o_wq, o_wk, o_wv, o_qn, o_kn, o_wo, o_mlp_norm, o_wg, o_wu, o_wd;  // inside a layer
   uint64_t o_final_norm, o_emb0, o_lmh1, o_offsets, table_stride;                      // global
+  uint64_t emb_row_bytes;  // bytes read to gather one embedding row (int8: codes and the row scale)
   // activation exchange buffers: fp32 bit patterns whose lowest mantissa bit
   // carries the parity of the write epoch (every epoch rewrites every word)
   uint32_t* xb;    // [kMaxRows][H]      residual stream (parity 0 after O, 1 after down)

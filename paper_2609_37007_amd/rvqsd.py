@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "librvqsd.so")
 
 RVQSD_ABI_VERSION = 1
 OK, EINVAL, EBLOB, ENOMEM, EHIP, EUNSUPPORTED, ENUMERIC, ETIMEOUT = 0, -1, -2, -3, -4, -5, -6, -7
-DTYPE_F32, DTYPE_BF16 = 0, 1
+DTYPE_F32, DTYPE_BF16, DTYPE_I8 = 0, 1, 2
 TRACE_ROUND_INTS = 32
 
 # every symbol include/rvqsd.h declares

@@ -34,7 +34,7 @@ from paper_2609_37007_amd import rvqsd as R  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-LOGIT_TOL = {S.DTYPE_F32: 1e-4, S.DTYPE_BF16: 2e-2}
+LOGIT_TOL = {S.DTYPE_F32: 1e-4, S.DTYPE_BF16: 2e-2, S.DTYPE_I8: 2e-2}
 
 
 @pytest.fixture(scope="module", autouse=True)
