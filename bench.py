@@ -106,6 +106,8 @@ def parse():
                     help="sparse-tree verification (Sec. 2.2, Fig. 2) with the packed tree of FILE (parents, ranks; "
                          "paper_2609_37007_amd/tree.py writes them); the frames then run through the batched "
                          "kernel's tree lane")
+    ap.add_argument("--phases", action="store_true",
+                    help="per-phase time of the frame kernel's passes from its per-workgroup clock trace")
     ap.add_argument("--residency", action="store_true",
                     help="only measure whether the weights stay in the Infinity Cache: warm against cold frames "
                          "(a 2 GiB sweep between frames) and a plain streaming read of a weight-sized buffer")
@@ -580,6 +582,96 @@ def run_residency(a) -> int:
     return 0
 
 
+def run_phases(a) -> int:
+    """Where a pass of the frame kernel spends its time, phase by phase.
+
+    Every workgroup stamps the device clock (100 MHz) when the input of a phase is complete
+    ("ready") and when it leaves the phase ("end"). Per phase and pass:
+    * path: the increment of the latest end over all workgroups (the critical path);
+    * wait: median over the phase's workgroups of ready minus that workgroup's previous end;
+    * work: median of end minus ready.
+    Passes after the prefix pass of frames 5.. (the first frames warm the clocks up)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_37007_amd import rvqsd as R
+    from paper_2609_37007_amd import synth as S
+
+    R.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    shape_name, topk, K_default, _ = WORKLOADS[a.workload]
+    s = getattr(S, shape_name)
+    K = K_default if a.draft_len is None else a.draft_len
+    blob = make_blob(S, s, a)
+    cfg = R.make_cfg(n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
+                     head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
+                     dtype=s.dtype, topk=topk, temperature=0.9, draft_len=K)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ts = torch.cuda.current_stream(dev)
+    model = R.Model(blob, cfg)
+    nwg = int(model.info()["workgroups"])
+    stream = R.Stream(model, hip_stream=ts.cuda_stream)
+    F = a.steps or 60
+    f, c0 = S.frame_inputs(s, F)
+    u = S.uniforms(F, s.n_codes)
+    L, n, H = s.n_layers, s.n_codes, s.hidden
+    nph, MAXR = 5 * L + 5, 16
+    names = [f"L{l}.{p}" for l in range(L) for p in ("qkv", "attn", "o", "gu", "down")] + ["heads", "sample", "commit"]
+    wg = torch.zeros(MAXR * nph * nwg, dtype=torch.int64, device=dev)
+    rd = torch.zeros(MAXR * nph * nwg, dtype=torch.int64, device=dev)
+    stream.set_trace(wg_clock_ptr=wg.data_ptr(), wg_ready_ptr=rd.data_ptr(), max_rounds=MAXR)
+    d_f, d_c0 = torch.from_numpy(f).to(dev), torch.from_numpy(c0).to(dev)
+    d_u = torch.from_numpy(np.ascontiguousarray(u)).to(dev)
+    sb = R.STATS_DTYPE.itemsize
+    d_codes = torch.zeros((1, n), dtype=torch.int32, device=dev)
+    d_st = torch.zeros(sb, dtype=torch.uint8, device=dev)
+    nrow = len(names)
+    path, wait, work, total = [[] for _ in range(nrow)], [[] for _ in range(nrow)], [[] for _ in range(nrow)], []
+    print(f"[bench] phase trace over {F} frames", file=sys.stderr, flush=True)
+    for i in range(F):
+        wg.zero_()
+        rd.zero_()
+        stream.decode_frame_async(d_f.data_ptr() + i * H * 4, d_c0.data_ptr() + i * 4, d_u.data_ptr() + i * n * 12,
+                                  d_codes.data_ptr(), d_st.data_ptr())
+        torch.cuda.synchronize()
+        st = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)[0]
+        if int(st["status"]) != 0:
+            print(f"[bench] frame {i} failed with status {int(st['status'])}", file=sys.stderr)
+            return 1
+        if i < 5:
+            continue
+        w = wg.cpu().numpy().reshape(MAXR, nph, nwg).astype(np.int64)
+        r = rd.cpu().numpy().reshape(MAXR, nph, nwg).astype(np.int64)
+        for p in range(1, min(int(st["target_calls"]), MAXR)):
+            prev_end = w[p - 1, nrow - 1]
+            total.append((w[p, nrow - 1].max() - w[p - 1, nrow - 1].max()) * 0.01)
+            for ph in range(nrow):
+                e = w[p, ph]
+                path[ph].append((e.max() - prev_end.max()) * 0.01)
+                ok = r[p, ph] > 0
+                if ok.any():
+                    wait[ph].append(np.median((r[p, ph] - prev_end)[ok]) * 0.01)
+                    work[ph].append(np.median((e - r[p, ph])[ok]) * 0.01)
+                prev_end = e
+    stream.set_trace()
+    stream.close()
+    model.close()
+    rows = []
+    for ph in range(nrow):
+        rows.append({"phase": names[ph], "path_us": round(float(np.mean(path[ph])), 2),
+                     "wait_us": round(float(np.mean(wait[ph])), 2) if wait[ph] else None,
+                     "work_us": round(float(np.mean(work[ph])), 2) if work[ph] else None})
+    for row in rows:
+        print(f"{row['phase']:8s} path {row['path_us']:6.2f}  wait {row['wait_us'] if row['wait_us'] is not None else '-':>6}"
+              f"  work {row['work_us'] if row['work_us'] is not None else '-':>6}", file=sys.stderr)
+    print(json.dumps({"phases": rows, "pass_us_mean": round(float(np.mean(total)), 2), "passes": len(total),
+                      "workload": f"{a.workload}, draft length {K}"}), flush=True)
+    return 0
+
+
 def main() -> int:
     a = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -596,6 +688,8 @@ def main() -> int:
         return run_pipeline(a)
     if a.residency:
         return run_residency(a)
+    if a.phases:
+        return run_phases(a)
 
     import numpy as np
     import torch

@@ -91,10 +91,15 @@ struct Ctx {
   uint64_t* rdy;    // trace: this workgroup's input-complete stamp of the current phase (nullable)
 };
 
-// parity of the per-layer buffers (q/k/v, attention output, activation):
-// one write per layer per pass, so it alternates with every write
+// Parity of the per-layer buffers (q/k/v, attention output, activation): one write per
+// layer per pass, so it alternates with every write. It counts from the start of the frame:
+// a frame begins with every such word at parity 1 (set when the stream is created, and again
+// by the frame kernel at the end of every complete frame), and its first write has parity 0.
+// The parity thus depends only on the pass and the layer within the frame, and so does the
+// lowest mantissa bit of every exchanged value: a frame's codes do not depend on what the
+// stream decoded before it.
 __device__ __forceinline__ uint32_t par_layer(const Ctx& c, int pass, int l) {
-  return (uint32_t)(((uint64_t)(c.pass0 + pass) * (uint64_t)c.p->L + (uint64_t)l) & 1u);
+  return (uint32_t)(((uint64_t)pass * (uint64_t)c.p->L + (uint64_t)l) & 1u);
 }
 constexpr uint32_t kParO = 0, kParDown = 1;  // residual stream: written after O, then after down
 
@@ -1945,6 +1950,15 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   }
 #undef RVQSD_STAMP
 #undef RVQSD_READY
+  if (ok) {
+    // back to parity 1 for the next frame. Every workgroup is past its last read of these words:
+    // ending the frame took the last pass's verdicts, hence its logits, hence the residual after
+    // the last down projection from every workgroup, each of which had read them all before.
+    uint64_t* w2 = reinterpret_cast<uint64_t*>(p->qkvb);
+    const int n2 = (int)((reinterpret_cast<const uint32_t*>(p->pass_count) - p->qkvb) / 2);
+    for (int i = blockIdx.x * kThreads + tid(); i < n2; i += p->nwg * kThreads)
+      __hip_atomic_store(G(w2 + i), 0x0101010101010101ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   if (blockIdx.x == 0 && tid() == 0) {
     rvqsd_stats* st = fa.out_stats;
     st->target_calls = shs.st_calls;

@@ -191,6 +191,33 @@ def test_mcd1024_async_launch_matches_oracle():
     rig.close()
 
 
+def test_frames_do_not_depend_on_stream_history():
+    """The same frame decoded at two points of a stream's life -- fresh, and after other frames
+    whose passes add up to an odd count -- gives bit-identical logits, decisions and codes: the
+    exchange words' parity (and with it their lowest mantissa bit) counts from the frame start."""
+    s = S.MCD_1024
+    rig = Rig(s, topk=50, K=4)
+    f, c0 = S.frame_inputs(s, 600)
+    u = S.uniforms(600)
+    frames = list(range(12))
+    first = [rig.traced(f[i], c0[i], u[i]) for i in frames]
+    passes, j = 0, 500
+    while passes % 2 == 0 or j < 503:
+        _, st = rig.stream.decode_frame_u(f[j], int(c0[j]), u[j])
+        passes += int(st["target_calls"])
+        j += 1
+    print(f"{j - 500} frames ({passes} passes) in between", flush=True)
+    for i, (c1, s1, l1, r1) in zip(frames, first):
+        c2, s2, l2, r2 = rig.traced(f[i], c0[i], u[i])
+        assert np.array_equal(c1, c2), (i, c1.tolist(), c2.tolist())
+        for key in ("status", "target_calls", "rounds", "drafted", "accepted", "accept_mask", "weight_bytes"):
+            assert s1[key] == s2[key], (i, key, s1[key], s2[key])
+        n = s1["target_calls"]
+        assert np.array_equal(l1[:n].view(np.uint32), l2[:n].view(np.uint32)), i
+        assert np.array_equal(r1, r2), i
+    rig.close()
+
+
 def test_k0_is_autoregressive():
     s = S.TINY
     rig = Rig(s, topk=8, K=0)
