@@ -750,7 +750,7 @@ rvqsd_status rvqsd_decode_frames_batched_async(rvqsd_stream* s, int32_t n, const
   call.out_stats = d_stats;
   call.n = n;
   char err[256];
-  const int st = launch_batch(s->dbp, call, s->m->nwg, (void*)s->stream, s->blds, err, sizeof(err));
+  const int st = launch_batch(s->dbp, call, s->m->nwg, (void*)s->stream, s->blds, s->tree != 0, err, sizeof(err));
   if (st) return set_err(st, "%s", err);
   return RVQSD_OK;
 }

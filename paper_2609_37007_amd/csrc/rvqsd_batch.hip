@@ -209,28 +209,34 @@ constexpr int kRowChunks = 4;  // 8-element chunks per lane of a row held in reg
 
 // A lane's pass has tree rows when the stream verifies trees and the prefix pass is done;
 // the prefix pass (rows at positions 0 and 1) and chain lanes put row r at position first + r.
-__device__ __forceinline__ bool tree_rows(const BParams* bp, const int* st) { return bp->tree && st[kLnPass] > 0; }
+template <bool TR>
+__device__ __forceinline__ bool tree_rows(const BParams* bp, const int* st) { return TR && st[kLnPass] > 0; }
+template <bool TR>
 __device__ __forceinline__ int row_pos(const BParams* bp, const int* st, int r) {
-  return st[kLnFirst] + (tree_rows(bp, st) ? bp->t_depth[r] : r);
+  return st[kLnFirst] + (tree_rows<TR>(bp, st) ? bp->t_depth[r] : r);
 }
 // whether row a is row r or one of its ancestors (the rows row r attends to)
+template <bool TR>
 __device__ __forceinline__ bool row_sees(const BParams* bp, const int* st, int r, int a) {
-  if (!tree_rows(bp, st)) return a <= r;
+  if (!tree_rows<TR>(bp, st)) return a <= r;
   return (bp->t_anc[r][a >> 6] >> (a & 63)) & 1ull;
 }
+template <bool TR>
 __device__ __forceinline__ bool row_is_verify(const BParams* bp, const int* st, int r) {
-  return r < st[kLnRows] && row_pos(bp, st, r) >= 1 && (st[kLnPass] == 0 ? r == 1 : true);
+  return r < st[kLnRows] && row_pos<TR>(bp, st, r) >= 1 && (st[kLnPass] == 0 ? r == 1 : true);
 }
+template <bool TR>
 __device__ __forceinline__ int row_drafts(const BParams* bp, const KParams* p, const int* st, int r) {
-  const int s = row_pos(bp, st, r);
+  const int s = row_pos<TR>(bp, st, r);
   if (r >= st[kLnRows] || s < 1 || s > p->n_codes - 1) return 0;
   if (st[kLnPass] == 0 && r != 1) return 0;
   return min(p->K, p->n_codes - s);
 }
 // LM-head input row of (lane row i, offset j) and whether it is used this pass
+template <bool TR>
 __device__ __forceinline__ bool head_slot_used(const BParams* bp, const KParams* p, const int* st, int r, int j) {
   if (!st[kLnActive]) return false;
-  return j == 0 ? row_is_verify(bp, st, r) : j <= row_drafts(bp, p, st, r);
+  return j == 0 ? row_is_verify<TR>(bp, st, r) : j <= row_drafts<TR>(bp, p, st, r);
 }
 
 // ------------------------------------------------------------ MFMA tile unit
@@ -459,7 +465,7 @@ __device__ void phase_attn_tree(const BParams* bp, BShared* sh, int l, uint32_t*
     // q rows (v < R) and k rows (v >= R): norm + RoPE at the row's position, one wave per vector
     for (int v = wave; v < 2 * R; v += kWaves) {
       const bool isq = v < R;
-      const int r = isq ? v : v - R, pos = row_pos(bp, st, r);
+      const int r = isq ? v : v - R, pos = row_pos<true>(bp, st, r);
       float* x = isq ? qs + r * d : kvs + (size_t)(fp + r) * 2 * d;
       const float* gn = isq ? qn : kn;
       float ss = 0.f;
@@ -486,7 +492,7 @@ __device__ void phase_attn_tree(const BParams* bp, BShared* sh, int l, uint32_t*
       float mx = -INFINITY;
       for (int t = 0; t < nkeys; ++t) {
         float sc = -INFINITY;
-        if (t < fp || row_sees(bp, st, r, t - fp)) {  // wave-uniform
+        if (t < fp || row_sees<true>(bp, st, r, t - fp)) {  // wave-uniform
           float a = 0.f;
           for (int i = lane; i < d; i += 64) a = fmaf(qs[r * d + i], kvs[(size_t)t * 2 * d + i], a);
           sc = wave_sum(a) * scale;
@@ -649,6 +655,7 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
 // Row i: x += sum of the KS partial sums of the projection just run, then the
 // next input: RMSNorm(x) * gain split into Aout (mode 0), or the final norm
 // h and the LM-head inputs h + b_j of the row's used slots (mode 1).
+template <bool TR>
 __device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float* gain, uint32_t* Aout, int mode,
                             float* xs) {
   const KParams* p = bp->k;
@@ -676,7 +683,7 @@ __device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float*
       } else {
         const float* ofs = bfw(p, p->o_offsets);
         for (int j = 0; j <= K; ++j) {
-          if (!head_slot_used(bp, p, st, r, j)) continue;
+          if (!head_slot_used<TR>(bp, p, st, r, j)) continue;
           float y8[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) y8[e] = j == 0 ? h8[e] : h8[e] + G(ofs)[(size_t)(j - 1) * H + 8 * c + e];
@@ -692,6 +699,7 @@ __device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float*
 // Unit (head t, 64 vocabulary columns): every used slot (lane row, offset j)
 // whose position plus offset is t, i.e. the verify rows at position t and the
 // draft rows of distance j from it.
+template <bool TR>
 __device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
   const KParams* p = bp->k;
   const int H = p->H, V = p->V, K = p->K, n = p->n_codes, rpl = bp->rpl;
@@ -709,7 +717,7 @@ __device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
         if (c < ncand) {
           const int ln = c / (rpl * (K + 1)), rem = c - ln * rpl * (K + 1), r = rem / (K + 1), j = rem - r * (K + 1);
           const int* st = sh->ln[ln];
-          use = head_slot_used(bp, p, st, r, j) && row_pos(bp, st, r) + j == t;
+          use = head_slot_used<TR>(bp, p, st, r, j) && row_pos<TR>(bp, st, r) + j == t;
         }
         int tot;
         const int pos = block_excl_scan(&sh->tk, use ? 1 : 0, &tot);
@@ -751,6 +759,7 @@ __device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
 // Called by the 64 threads of one wave: thread i counts stream lane i, and the
 // wave adds the counts and merges the used heads (integer sums: the order does
 // not matter). The result is valid in every thread.
+template <bool TR>
 __device__ unsigned long long pass_bytes_batch(const BParams* bp, const BShared* sh) {
   const KParams* p = bp->k;
   const int lane = tid() & 63;
@@ -763,9 +772,9 @@ __device__ unsigned long long pass_bytes_batch(const BParams* bp, const BShared*
     if (st[kLnActive]) {
       const int first = st[kLnFirst], rows = st[kLnRows];
       for (int r = 0; r < rows; ++r) {
-        const int s = row_pos(bp, st, r);
-        if (row_is_verify(bp, st, r)) used |= 1u << s;
-        const int nd = row_drafts(bp, p, st, r);
+        const int s = row_pos<TR>(bp, st, r);
+        if (row_is_verify<TR>(bp, st, r)) used |= 1u << s;
+        const int nd = row_drafts<TR>(bp, p, st, r);
         for (int j = 1; j <= nd; ++j) used |= 1u << (s + j);
         b += (s == 0) ? 4ull * H : 2ull * H;
       }
@@ -786,6 +795,7 @@ __device__ unsigned long long pass_bytes_batch(const BParams* bp, const BShared*
 // u_acc q(d) < p(d), else resample from max(0, p - q) at u_samp; j = 0
 // without a draft (prefix token, or the extra token after every draft was
 // accepted) -> sample p at u_samp. Verdict: token | accepted << 31.
+template <bool TR>
 __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, float* lds) {
   const KParams* p = bp->k;
   const int V = p->V, K = p->K, rpl = bp->rpl, n = p->n_codes, SW = bp->sup_words;
@@ -803,11 +813,11 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
   for (int u = blockIdx.x; u < nslots; u += bp->nwg) {
     const int ln = u / (rpl * (K + 1)), rem = u - ln * rpl * (K + 1), r = rem / (K + 1), j = rem - r * (K + 1);
     const int* st = sh->ln[ln];
-    if (!head_slot_used(bp, p, st, r, j)) continue;
-    const int pass = st[kLnPass], s = row_pos(bp, st, r), t = s + j;
+    if (!head_slot_used<TR>(bp, p, st, r, j)) continue;
+    const int pass = st[kLnPass], s = row_pos<TR>(bp, st, r), t = s + j;
     const float* U = call.uniforms + (size_t)st[kLnFrame] * n * 3;
-    const bool tree_pass = tree_rows(bp, st);
-    const bool has_draft = !bp->tree && j == 0 && pass > 0 && r + 1 <= st[kLnKp];
+    const bool tree_pass = tree_rows<TR>(bp, st);
+    const bool has_draft = !TR && j == 0 && pass > 0 && r + 1 <= st[kLnKp];
     int nq = 0, dtok = -1;
     if (has_draft) {
       // q of d_t: drafted last pass from the anchor's row, offset r + 1
@@ -836,7 +846,7 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
       for (int i = tid(); i < ns; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
       if (!__any(fin) && tid() == 0) raise_status(bp, RVQSD_ENUMERIC);
     }
-    if (bp->tree && j > 0) {
+    if (TR && j > 0) {
       // tree lanes: the ranked candidates of depth j for the rows of a round anchored at
       // this row: rank = larger logit first, ties to the lower token (within the top-k
       // support, which holds every rank below top-k)
@@ -981,6 +991,7 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
 // Lane workgroup: commit the verdicts of the pass just sampled, pick the next
 // anchor and its drafts (or finish the frame and start the lane's next one),
 // then gather and normalise the new rows (layer 0 input). first: no pass yet.
+template <bool TR>
 __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, bool first, float* xs,
                             uint32_t* A0) {
   const KParams* p = bp->k;
@@ -995,15 +1006,15 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
   }
   __syncthreads();
   const bool was_active = !first && st[kLnActive];
-  const bool tree_pass = was_active && tree_rows(bp, st);
+  const bool tree_pass = was_active && tree_rows<TR>(bp, st);
   if (was_active) {
     const int R = st[kLnRows];
     for (int i = tid(); i < R; i += kThreads) sh->vr[i] = *G(bp->vres + lane_id * rpl + i);
     const int par = st[kLnPass] & 1;
-    if (!bp->tree)
+    if (!TR)
       for (int i = tid(); i < R * K; i += kThreads) {
         const int r = i / K, jj = i - r * K;
-        sh->dt[r][jj] = jj < row_drafts(bp, p, st, r)
+        sh->dt[r][jj] = jj < row_drafts<TR>(bp, p, st, r)
                             ? (int)(uint32_t)*G(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
                             : -1;
       }
@@ -1013,7 +1024,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
   // count it and trace it, before the candidates of the next round replace this round's
   if (tid() == 0) {
     sh->c_mnew = -1;
-    if (was_active && bp->tree) {
+    if (was_active && TR) {
       const int m = st[kLnM], fp = st[kLnFirst], R = st[kLnRows];
       int* codes = st + kLnCodes;
       int cur = 1, acc = 0, m_new = 1, tok = -1;
@@ -1060,7 +1071,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
     }
   }
   __syncthreads();
-  if (was_active && bp->tree) {
+  if (was_active && TR) {
     const int m = sh->c_m, acc = tree_pass ? sh->c_acc : 0, m_new = sh->c_mnew, arow = sh->c_arow;
     const int d = p->d, slots = bp->kv_slots;
     // KV of the accepted path: row path[j-1] (slot m+1+row) becomes position m+1+j, every
@@ -1089,7 +1100,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
   if (tid() == 0) {
     bool start = first || !st[kLnActive];
     bool done = false;  // the lane's frame is complete
-    if (!first && st[kLnActive] && bp->tree) {
+    if (!first && st[kLnActive] && TR) {
       // tree lanes: the pass was committed above; set up the next round
       const int m_new = sh->c_mnew;
       int* codes = st + kLnCodes;
@@ -1111,7 +1122,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
         done = true;
       }
     }
-    if (!first && st[kLnActive] && !bp->tree) {
+    if (!first && st[kLnActive] && !TR) {
       const int m = st[kLnM], kp = st[kLnKp], R = st[kLnRows], fp = st[kLnFirst];
       int* codes = st + kLnCodes;
       int m_new = -1, acc = 0, tok = -1;
@@ -1215,14 +1226,14 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
       // the heads it touches, the gathered rows and the KV cache it attends over
       int t_lo = 1 << 20, t_hi = -1;
       for (int r = 0; r < st[kLnRows]; ++r) {
-        const int s = row_pos(bp, st, r);
-        if (row_is_verify(bp, st, r)) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
-        const int nd = row_drafts(bp, p, st, r);
+        const int s = row_pos<TR>(bp, st, r);
+        if (row_is_verify<TR>(bp, st, r)) { t_lo = min(t_lo, s); t_hi = max(t_hi, s); }
+        const int nd = row_drafts<TR>(bp, p, st, r);
         if (nd > 0) { t_lo = min(t_lo, s + 1); t_hi = max(t_hi, s + nd); }
       }
       unsigned long long b = (unsigned long long)p->L * p->layer_stride;
       if (t_hi >= t_lo) b += (unsigned long long)(t_hi - t_lo + 1) * p->table_stride;
-      for (int r = 0; r < st[kLnRows]; ++r) b += (row_pos(bp, st, r) == 0) ? 4ull * H : 2ull * H;
+      for (int r = 0; r < st[kLnRows]; ++r) b += (row_pos<TR>(bp, st, r) == 0) ? 4ull * H : 2ull * H;
       b += (unsigned long long)p->L * (st[kLnFirst] + st[kLnRows]) * p->nkv * p->d * 2 * 4;
       b += (uint64_t)(uint32_t)st[kLnBytesLo] | ((uint64_t)(uint32_t)st[kLnBytesHi] << 32);
       st[kLnBytesLo] = (int)(uint32_t)b;
@@ -1235,9 +1246,9 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
   if (!st[kLnActive]) return;
   const float* g0 = bfw(p, p->o_attn_norm);
   const int lane = tid() & 63, wave = tid() >> 6, nch = H / 8;
-  const bool tree_next = tree_rows(bp, st);
+  const bool tree_next = tree_rows<TR>(bp, st);
   for (int r = wave; r < st[kLnRows]; r += kWaves) {
-    const int s = row_pos(bp, st, r), i = lane_id * rpl + r;
+    const int s = row_pos<TR>(bp, st, r), i = lane_id * rpl + r;
     const int code = tree_next ? st[kLnCand + r] : st[kLnInCode + s];
     float xv[kRowChunks][8];
     float ss = 0.f;
@@ -1297,6 +1308,7 @@ __device__ void lane_abort(const BParams* bp, BShared* sh, const BCall& call) {
   }
 }
 
+template <bool TR>
 __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __restrict__ bpp, BCall call) {
   __shared__ BShared shs;
   extern __shared__ __align__(16) float dyn[];
@@ -1314,7 +1326,7 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
   const bool counter_wg = (int)blockIdx.x == bp->nwg - 1;
   unsigned long long n_pass = 0, n_bytes = 0;
   while (ok) {
-    if (lane_wg) lane_commit(bp, sh, call, first, dyn, A0);
+    if (lane_wg) lane_commit<TR>(bp, sh, call, first, dyn, A0);
     first = false;
     if (!(ok = grid_sync(bp, gen, sh))) break;
     for (int i = tid(); i < bp->lanes * kLaneInts; i += kThreads)
@@ -1327,15 +1339,15 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
       proj_partial<4>(bp, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, bp->ks_qkv, A0, dyn);
       ok = grid_sync(bp, gen, sh);
       if (ok) {
-        if (bp->tree) phase_attn_tree(bp, sh, l, A1, dyn);
+        if (TR) phase_attn_tree(bp, sh, l, A1, dyn);
         else phase_attn(bp, sh, l, A1, dyn);
       }
       ok = ok && grid_sync(bp, gen, sh);
       if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
       ok = ok && grid_sync(bp, gen, sh);
-      if (ok) phase_resid(bp, sh, bp->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, 0, dyn);
+      if (ok) phase_resid<TR>(bp, sh, bp->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, 0, dyn);
       if (ok && l == 0 && counter_wg && tid() < 64) {
-        const unsigned long long pb = pass_bytes_batch(bp, sh);
+        const unsigned long long pb = pass_bytes_batch<TR>(bp, sh);
         if (tid() == 0) {
           n_pass += 1;
           n_bytes += pb;
@@ -1347,15 +1359,15 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
       if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wd)), H, p->F, bp->ks_down, A1, dyn);
       ok = ok && grid_sync(bp, gen, sh);
       if (ok) {
-        if (l + 1 < L) phase_resid(bp, sh, bp->ks_down, bfw(p, boff(p, l + 1, p->o_attn_norm)), A0, 0, dyn);
-        else phase_resid(bp, sh, bp->ks_down, bfw(p, p->o_final_norm), nullptr, 1, dyn);
+        if (l + 1 < L) phase_resid<TR>(bp, sh, bp->ks_down, bfw(p, boff(p, l + 1, p->o_attn_norm)), A0, 0, dyn);
+        else phase_resid<TR>(bp, sh, bp->ks_down, bfw(p, p->o_final_norm), nullptr, 1, dyn);
       }
       ok = ok && grid_sync(bp, gen, sh);
     }
     if (!ok) break;
-    phase_heads(bp, sh, dyn);
+    phase_heads<TR>(bp, sh, dyn);
     if (!(ok = grid_sync(bp, gen, sh))) break;
-    phase_sample(bp, sh, call, dyn);
+    phase_sample<TR>(bp, sh, call, dyn);
     if (!(ok = grid_sync(bp, gen, sh))) break;
   }
   if (!ok && lane_wg) lane_abort(bp, sh, call);
@@ -1693,17 +1705,19 @@ __global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __res
 
 // ------------------------------------------------------------------- host
 
-int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
-                 size_t errlen) {
-  const void* fn = reinterpret_cast<const void*>(&batch_kernel);
-  static size_t attr_bytes = 0;
-  if (lds_bytes > attr_bytes) {
+// The tree and chain forms are separate instantiations: the chain kernel carries no tree code.
+int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, size_t lds_bytes, bool tree,
+                 char* err, size_t errlen) {
+  const void* fn = tree ? reinterpret_cast<const void*>(&batch_kernel<true>)
+                        : reinterpret_cast<const void*>(&batch_kernel<false>);
+  static size_t attr_bytes[2] = {0, 0};
+  if (lds_bytes > attr_bytes[tree]) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) {
       snprintf(err, errlen, "hipFuncSetAttribute(%zu bytes LDS): %s", lds_bytes, hipGetErrorString(e));
       return RVQSD_EHIP;
     }
-    attr_bytes = lds_bytes;
+    attr_bytes[tree] = lds_bytes;
   }
   const BParams* bpp = bp;
   BCall c = call;

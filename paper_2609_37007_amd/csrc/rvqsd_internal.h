@@ -218,8 +218,8 @@ struct BCall {
   int32_t n;
 };
 
-int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
-                 size_t errlen);
+int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, size_t lds_bytes, bool tree,
+                 char* err, size_t errlen);
 
 // ---------------------------------------------------------------- outer decoder step
 // The outer CodeDecoder of the per-frame pipeline: one position per frame, a KV
