@@ -49,7 +49,7 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "RVQ codes/sec single-stream; accepted tok/call; verify-step GB/s vs roofline"
 KERNEL_SOURCES = ("paper_2609_37007_amd/csrc/rvqsd_frame.hip", "paper_2609_37007_amd/csrc/rvqsd_device.h",
                   "paper_2609_37007_amd/csrc/rvqsd_internal.h")
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "frame_kernel_mcd1024_k4_hbm_traffic.txt")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "frame_kernel_mcd1024_k4_fetch_write_counters.txt")
 
 WORKLOADS = {
     # name: (shape, top-k, draft length, frames)
@@ -68,8 +68,10 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic():
-    """HBM bytes per launch from the committed counter summary, or None when
-    the summary is absent or the kernel sources changed since it was taken."""
+    """Bytes per launch that the L2 caches fetched from and wrote to the memory fabric
+    (rocprofv3 FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy), from the committed
+    counter summary, or None when the summary is absent or the kernel sources changed
+    since it was taken. The counters see Infinity Cache (MALL) hits as fabric traffic."""
     if not os.path.exists(PMC_SUMMARY):
         return None
     kv = {}
@@ -81,7 +83,7 @@ def measured_traffic():
     if kv.get("kernel_source_sha256") != kernel_source_hash():
         return None
     try:
-        return float(kv["hbm_bytes_per_launch"])
+        return float(kv["fetch_write_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
@@ -476,6 +478,34 @@ def run_streams(a) -> int:
     return 0
 
 
+def stream_read_rates(torch, dev, ts, nbytes, reps=20):
+    """The box's own streaming-read rate: torch.sum over a buffer of nbytes, warm (read back
+    to back, so it sits in the Infinity Cache when it fits) and cold (a 2 GiB read-and-write
+    sweep of another buffer before each read). GB/s."""
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    sweep = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    out = torch.empty((), dtype=torch.float32, device=dev)
+
+    def rate(evict, n):
+        t = 0.0
+        for _ in range(n):
+            if evict:
+                sweep.add_(1.0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(ts)
+            torch.sum(buf, dim=0, out=out)
+            e1.record(ts)
+            torch.cuda.synchronize()
+            t += e0.elapsed_time(e1) * 1e-3
+        return buf.numel() * 4 * n / t / 1e9
+
+    rate(False, 3)
+    res = {"bytes": buf.numel() * 4, "warm": round(rate(False, reps), 1), "cold": round(rate(True, reps), 1)}
+    del buf, sweep, out
+    torch.cuda.empty_cache()
+    return res
+
+
 def run_residency(a) -> int:
     """Whether the frame kernel's weights stay in the 256 MB Infinity Cache (MALL).
 
@@ -552,30 +582,13 @@ def run_residency(a) -> int:
     stream.set_trace()
     # plain streaming reads of a buffer the size of one round's weights
     wb = int(model.info()["layer_weight_bytes"] + 9 * model.info()["head_bytes"])
-    buf = torch.ones(wb // 4, dtype=torch.float32, device=dev)
-    out = torch.empty((), dtype=torch.float32, device=dev)
-
-    def read_rate(evict, reps=20):
-        t = 0.0
-        for _ in range(reps):
-            if evict:
-                sweep.add_(1.0)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(ts)
-            torch.sum(buf, dim=0, out=out)
-            e1.record(ts)
-            torch.cuda.synchronize()
-            t += e0.elapsed_time(e1) * 1e-3
-        return wb * reps / t / 1e9
-
-    read_rate(False, 3)
-    res["stream_read_gbs"] = {"bytes": wb, "warm": round(read_rate(False), 1), "cold": round(read_rate(True), 1)}
+    del sweep
+    res["stream_read_gbs"] = stream_read_rates(torch, dev, ts, wb)
     w, c = res["warm"], res["cold"]
     res["first_pass_extra_us_cold"] = round(c["first_pass_us_mean"] - w["first_pass_us_mean"], 2)
     res["later_pass_extra_us_cold"] = round(c["later_pass_us_mean"] - w["later_pass_us_mean"], 2)
     res["workload"] = f"{a.workload}, draft length {K}, offsets {a.offsets}"
     res["weight_bytes_per_round"] = wb
-    del sweep, buf
     stream.close()
     model.close()
     print(json.dumps({"residency": res}), flush=True)
@@ -776,6 +789,8 @@ def main() -> int:
     traffic = measured_traffic() if (a.workload == "mcd1024" and K == 4 and a.head_scale == 1.0 and not tree
                                      and a.offsets == "seed") else None
     codes_per_s = n * steps / elapsed
+    # the box's own read rates for a buffer of one launch's mean bytes per pass
+    box = stream_read_rates(torch, dev, torch_stream, int(bytes_per_launch.sum() / calls) & ~255)
 
     cpu = None
     if not a.no_cpu_baseline:
@@ -828,6 +843,11 @@ def main() -> int:
             "kernel": "batch_kernel" if tree else "frame_kernel",
             "algorithmic_bytes_per_launch": round(float(bytes_per_launch.mean()), 1),
             "launch_ms_mean": round(float(launch_ms.mean()), 5),
+            "traffic_counts": "L2-to-fabric bytes (FETCH_SIZE + WRITE_SIZE, Infinity Cache hits included)",
+            "box_read_gbs": {"warm": box["warm"], "cold": box["cold"], "bytes": box["bytes"],
+                             "how": "torch.sum over one pass's bytes: warm = back to back (Infinity Cache), "
+                                    "cold = after a 2 GiB sweep (HBM)"},
+            "frac_of_box_warm_read": round(achieved / box["warm"], 4),
         },
         "cpu_baseline": cpu,
         "device": torch.cuda.get_device_name(dev),

@@ -126,7 +126,10 @@ typedef struct {
 } rvqsd_info;
 
 /* Create a model: validates cfg against the blob, copies the weights to the
- * current HIP device. Errors: EINVAL (bad cfg / NULL), EBLOB, EUNSUPPORTED
+ * current HIP device. The weights are those of the inner MultiCodeDecoder
+ * (Fig. 1): its decoder layers, the per-position code tables E_0..E_{n-1} and
+ * LM heads LMH_1..LMH_n (Sec. 2.1), the final norm and the draft offsets
+ * b_1..b_max_draft (Sec. 2.2, Fig. 3). Errors: EINVAL (bad cfg / NULL), EBLOB, EUNSUPPORTED
  * (hidden, q/kv width and ffn must be multiples of 512 for bf16 and 256 for
  * f32, head_dim a multiple of 64, n_kv_heads <= 256 workgroups, ...), ENOMEM, EHIP. */
 rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_model** out);
@@ -134,7 +137,9 @@ void rvqsd_destroy(rvqsd_model* m);
 rvqsd_status rvqsd_model_info(const rvqsd_model* m, rvqsd_info* out);
 
 /* Create a decode stream on a caller-owned hipStream_t (borrowed, never
- * destroyed; NULL = the null stream). max_streams (1..16) is the number of
+ * destroyed; NULL = the null stream): the state of one frame's speculative
+ * rounds (Sec. 2.2), i.e. the KV cache of positions 0..15 and the exchange
+ * buffers of the frame kernel. max_streams (1..16) is the number of
  * independent frame streams the batched calls below decode together; with 1
  * only the single-frame calls are available. Batched streams need bf16
  * weights, max_streams * max(draft_len + 1, 2) <= 80 rows, hidden a multiple
@@ -171,22 +176,32 @@ void rvqsd_stream_destroy(rvqsd_stream* s);
 rvqsd_status rvqsd_tree_stream_create(rvqsd_model* m, void* hip_stream, int32_t lanes, int32_t n_nodes,
                                       const int32_t* parents, const int32_t* ranks, rvqsd_stream** out);
 
-/* Decode one frame (host pointers, synchronous): frame_hidden float[hidden],
- * c0 in [0, vocab), uniforms expanded from rng_seed with SplitMix64 (see
+/* Decode one frame (host pointers, synchronous): the inner loop of Fig. 1
+ * run speculatively as in Sec. 2.2 and Fig. 3. Position 0 holds frame_hidden
+ * (float[hidden], the outer decoder's state), position 1 consumes c0 (in
+ * [0, vocab)) through E_0; each round drafts the next K' codes from the
+ * anchor's heads LMH_{m+j}(h_m + b_j), verifies them in one pass and keeps
+ * them by the acceptance rule with residual resampling (bonus code when all
+ * are accepted). Uniforms expanded from rng_seed with SplitMix64 (see
  * rvqsd_uniforms_from_seed). Writes out_codes[n_codes] (codes c_1..c_n) and
  * *out_stats (nullable) only on success. */
 rvqsd_status rvqsd_decode_frame(rvqsd_stream* s, const float* frame_hidden, int32_t c0, uint64_t rng_seed,
                                 int32_t* out_codes, rvqsd_stats* out_stats);
 
-/* Same with a caller-supplied uniform table (host float[n_codes][3]). */
+/* Same with a caller-supplied uniform table (host float[n_codes][3], each in
+ * [0, 1): the draft, accept and sample draws of Sec. 2.2 per code position;
+ * EINVAL otherwise). */
 rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, int32_t c0, const float* uniforms,
                                   int32_t* out_codes, rvqsd_stats* out_stats);
 
-/* Enqueue one frame on the stream with device pointers only; returns after
- * the launch, the caller synchronises. d_c0: int32[1]; d_uniforms:
- * float[n_codes][3]; d_out_codes: int32[n_codes]; d_stats: rvqsd_stats[1]
- * (written by the device; its status field reports device-side errors).
- * Inputs must stay valid until the stream reaches the frame. */
+/* rvqsd_decode_frame_u enqueued with device pointers only (the same frame
+ * of Sec. 2.2); returns after the launch, the caller synchronises. d_c0:
+ * int32[1]; d_uniforms: float[n_codes][3]; d_out_codes: int32[n_codes];
+ * d_stats: rvqsd_stats[1] (written by the device; its status field reports
+ * device-side errors). A c0 outside [0, vocab) or a uniform outside [0, 1)
+ * (NaN included) is found on the device: the frame is not decoded, its status
+ * is EINVAL and its codes -1, and the stream stays usable. Inputs must stay
+ * valid until the stream reaches the frame. */
 rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidden, const int32_t* d_c0,
                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats);
 
@@ -224,8 +239,8 @@ rvqsd_status rvqsd_decode_frames_batched(rvqsd_stream* s, int32_t n, const float
                                          const float* uniforms, int32_t* out_codes, rvqsd_stats* out_stats);
 
 /* Same with device pointers only (same layouts, d_stats required); returns
- * after the launch. A frame whose c0 is out of range gets status EINVAL and
- * codes -1; after a device-side error every frame not completed gets that
+ * after the launch. A frame whose c0 is out of range or any of whose
+ * uniforms lies outside [0, 1) (NaN included) gets status EINVAL and codes -1; after a device-side error every frame not completed gets that
  * error in its status and codes -1. Inputs must stay valid until the stream
  * reaches the launch. */
 rvqsd_status rvqsd_decode_frames_batched_async(rvqsd_stream* s, int32_t n, const float* d_frame_hidden,
@@ -283,12 +298,17 @@ rvqsd_status rvqsd_pipeline_frames_async(rvqsd_stream* s, rvqsd_outer* o, int32_
                                          rvqsd_stats* d_stats, float* d_hidden);
 
 /* Return a stream to its initial state. Needed after a frame enqueued with
- * rvqsd_decode_frame_async reported a device-side error in its stats (later
- * frames on the stream then fail with RVQSD_EHIP until the reset); the
- * synchronous calls reset by themselves. Synchronises the stream. */
+ * rvqsd_decode_frame_async reported a device-side error other than EINVAL in
+ * its stats (later frames on the stream then fail with RVQSD_EHIP until the
+ * reset); the synchronous calls reset by themselves. Synchronises the stream. */
 rvqsd_status rvqsd_stream_reset(rvqsd_stream* s);
 
-/* Install (trace != NULL) or remove (NULL) a per-round trace for later frames of this stream. */
+/* Install (trace != NULL) or remove (NULL) a per-round trace for later frames
+ * of this stream (layouts at rvqsd_trace): the verify logits LMH_s(h_s) and the
+ * draft logits LMH_{s+j}(h_s + b_j) of every row of every pass, and the round
+ * records (anchor, drafts, accepted count, committed token) of the speculative
+ * rounds of Sec. 2.2; the buffers stay the caller's. Synchronises the stream.
+ * EINVAL for a NULL stream or max_rounds < 0. */
 rvqsd_status rvqsd_set_trace(rvqsd_stream* s, const rvqsd_trace* trace);
 
 /* The library's uniform generator (host only): uniform i = (n_codes*3 table

@@ -991,6 +991,20 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
 // Lane workgroup: commit the verdicts of the pass just sampled, pick the next
 // anchor and its drafts (or finish the frame and start the lane's next one),
 // then gather and normalise the new rows (layer 0 input). first: no pass yet.
+// c0 in [0, V) and every uniform of the frame in [0, 1) (NaN fails): a frame that fails
+// is not decoded; it reports EINVAL
+__device__ __forceinline__ bool frame_inputs_ok(const BCall& call, int f, int V, int n) {
+  const int c0 = call.c0[f];
+  if (c0 < 0 || c0 >= V) return false;
+  const float* U = call.uniforms + (size_t)f * n * 3;
+  bool ok = true;
+  for (int i = 0; i < 3 * n; ++i) {
+    const float u = U[i];
+    ok &= u >= 0.f && u < 1.f;
+  }
+  return ok;
+}
+
 template <bool TR>
 __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, bool first, float* xs,
                             uint32_t* A0) {
@@ -1202,7 +1216,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
     if (start) {
       // the lane's next frame with a valid c0
       int f = st[kLnFrame] + bp->lanes;
-      while (f < call.n && (call.c0[f] < 0 || call.c0[f] >= p->V)) {
+      while (f < call.n && !frame_inputs_ok(call, f, p->V, n)) {
         rvqsd_stats o = {};
         o.status = RVQSD_EINVAL;
         call.out_stats[f] = o;

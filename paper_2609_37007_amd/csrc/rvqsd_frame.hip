@@ -1857,14 +1857,22 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     }
     for (int i = tid(); i < kMaxPos * d; i += kThreads) c.attn_const[p->L * 2 * d + i] = G(p->rope)[i];
   }
-  if (tid() < 3 * p->n_codes) shs.uni[tid()] = G(fa.uniforms)[tid()];
+  // every uniform in [0, 1) (NaN fails), or the frame is not decoded and reports EINVAL;
+  // every workgroup reads the same table, so all of them agree
+  int u_bad = 0;
+  if (tid() < 3 * p->n_codes) {
+    const float u = G(fa.uniforms)[tid()];
+    shs.uni[tid()] = u;
+    u_bad = !(u >= 0.f && u < 1.f);
+  }
+  const bool u_ok = __syncthreads_or(u_bad) == 0;
   c.tag_base = fa.epoch_base;
   c.pass0 = *G(p->pass_count);
   c.rdy = nullptr;
   const uint64_t t_start = dclock();
   const int c0 = fa.c0[0];
   const bool poisoned = c.pass0 == 0xffffffffu;
-  const bool c0_ok = c0 >= 0 && c0 < p->V && !poisoned;
+  const bool c0_ok = c0 >= 0 && c0 < p->V && u_ok && !poisoned;
   if (tid() == 0) {
     shs.fa = fa;
     shs.abort = c0_ok ? 0 : 1;

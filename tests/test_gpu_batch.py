@@ -199,7 +199,8 @@ def test_frames_do_not_depend_on_lane_or_neighbours():
 
 
 def test_ragged_counts_and_invalid_c0_async():
-    """n not a multiple of the lanes, n below the lanes, and (async) one frame with a bad c0."""
+    """n not a multiple of the lanes, n below the lanes, and (async) one frame with a bad c0
+    and one with a uniform outside [0, 1)."""
     rig = BRig(SMALL, lanes=4, topk=16, K=2)
     n = 7
     f, c0 = S.frame_inputs(SMALL, n)
@@ -212,7 +213,9 @@ def test_ragged_counts_and_invalid_c0_async():
     bad[3] = SMALL.vocab + 5
     d_f = torch.from_numpy(f).cuda()
     d_c0 = torch.from_numpy(bad).cuda()
-    d_u = torch.from_numpy(np.ascontiguousarray(u)).cuda()
+    ubad = np.ascontiguousarray(u).copy()
+    ubad[5, 0, 1] = np.nan
+    d_u = torch.from_numpy(ubad).cuda()
     d_codes = torch.zeros((n, SMALL.n_codes), dtype=torch.int32, device="cuda")
     sb = R.STATS_DTYPE.itemsize
     d_st = torch.zeros(n * sb, dtype=torch.uint8, device="cuda")
@@ -221,8 +224,9 @@ def test_ragged_counts_and_invalid_c0_async():
     torch.cuda.synchronize()
     acodes = d_codes.cpu().numpy()
     ast = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)
-    assert ast["status"][3] == R.EINVAL and (acodes[3] == -1).all()
-    ok = [i for i in range(n) if i != 3]
+    for i in (3, 5):
+        assert ast["status"][i] == R.EINVAL and (acodes[i] == -1).all(), i
+    ok = [i for i in range(n) if i not in (3, 5)]
     assert (ast["status"][ok] == 0).all()
     assert np.array_equal(acodes[ok], codes[ok])
     with pytest.raises(R.RvqsdError):

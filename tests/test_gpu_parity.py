@@ -400,6 +400,19 @@ def test_invalid_inputs_and_recovery():
     torch.cuda.synchronize()
     st = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)[0]
     assert int(st["status"]) == R.EINVAL
+    # so is a device-side uniform outside [0, 1) or NaN: the frame is not decoded
+    d_c0.fill_(int(c0[0]))
+    for val in (1.0, -0.25, float("nan")):
+        ub = u[0].copy()
+        ub[s.n_codes - 1, 2] = val
+        d_ub = torch.from_numpy(np.ascontiguousarray(ub)).cuda()
+        d_codes.fill_(7)
+        rig.stream.decode_frame_async(d_f.data_ptr(), d_c0.data_ptr(), d_ub.data_ptr(), d_codes.data_ptr(),
+                                      d_st.data_ptr())
+        torch.cuda.synchronize()
+        st = np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)[0]
+        assert int(st["status"]) == R.EINVAL, val
+        assert (d_codes.cpu().numpy() == -1).all(), val
     codes, _ = rig.stream.decode_frame_u(f[1], int(c0[1]), u[1])
     assert np.array_equal(codes, rig.orc.spec_frame(f[1], int(c0[1]), u[1])[0])
     rig.stream.reset()
