@@ -602,7 +602,9 @@ def run_phases(a) -> int:
     ("ready") and when it leaves the phase ("end"). Per phase and pass:
     * path: the increment of the latest end over all workgroups (the critical path);
     * wait: median over the phase's workgroups of ready minus that workgroup's previous end;
-    * work: median of end minus ready.
+    * work: median of end minus ready;
+    * exchange: ready minus the latest end among the workgroups that worked in the phase
+      before (median and minimum over the consumers): the cost of handing the data over.
     Passes after the prefix pass of frames 5.. (the first frames warm the clocks up)."""
     import numpy as np
     import torch
@@ -643,6 +645,8 @@ def run_phases(a) -> int:
     d_st = torch.zeros(sb, dtype=torch.uint8, device=dev)
     nrow = len(names)
     path, wait, work, total = [[] for _ in range(nrow)], [[] for _ in range(nrow)], [[] for _ in range(nrow)], []
+    # exchange: consumer input complete minus the last end of the previous phase's workers
+    xmed, xmin = [[] for _ in range(nrow)], [[] for _ in range(nrow)]
     print(f"[bench] phase trace over {F} frames", file=sys.stderr, flush=True)
     for i in range(F):
         wg.zero_()
@@ -668,6 +672,11 @@ def run_phases(a) -> int:
                 if ok.any():
                     wait[ph].append(np.median((r[p, ph] - prev_end)[ok]) * 0.01)
                     work[ph].append(np.median((e - r[p, ph])[ok]) * 0.01)
+                    workers = r[p, ph - 1] > 0 if ph > 0 else np.zeros(nwg, dtype=bool)
+                    if workers.any():
+                        last = prev_end[workers].max()
+                        xmed[ph].append(np.median(r[p, ph][ok] - last) * 0.01)
+                        xmin[ph].append(np.min(r[p, ph][ok] - last) * 0.01)
                 prev_end = e
     stream.set_trace()
     stream.close()
@@ -676,7 +685,9 @@ def run_phases(a) -> int:
     for ph in range(nrow):
         rows.append({"phase": names[ph], "path_us": round(float(np.mean(path[ph])), 2),
                      "wait_us": round(float(np.mean(wait[ph])), 2) if wait[ph] else None,
-                     "work_us": round(float(np.mean(work[ph])), 2) if work[ph] else None})
+                     "work_us": round(float(np.mean(work[ph])), 2) if work[ph] else None,
+                     "exchange_median_us": round(float(np.mean(xmed[ph])), 2) if xmed[ph] else None,
+                     "exchange_min_us": round(float(np.mean(xmin[ph])), 2) if xmin[ph] else None})
     for row in rows:
         print(f"{row['phase']:8s} path {row['path_us']:6.2f}  wait {row['wait_us'] if row['wait_us'] is not None else '-':>6}"
               f"  work {row['work_us'] if row['work_us'] is not None else '-':>6}", file=sys.stderr)
