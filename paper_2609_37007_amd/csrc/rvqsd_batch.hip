@@ -75,18 +75,10 @@ __device__ __forceinline__ void store_split(uint32_t* dst, const float (&x)[8]) 
   cst64(dst + 6, (uint64_t)lo[2] | ((uint64_t)lo[3] << 32));
 }
 __device__ __forceinline__ W16 load_w16(const uint32_t* p) { return *G(reinterpret_cast<const W16*>(p)); }
-// the same through device-coherent 8-byte loads (no cache invalidate needed before them)
-__device__ __forceinline__ W16 load_w16c(const uint32_t* p) {
-  const uint64_t a = __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint64_t b = __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p + 2)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  W16 r;
-  r[0] = (uint32_t)a;
-  r[1] = (uint32_t)(a >> 32);
-  r[2] = (uint32_t)b;
-  r[3] = (uint32_t)(b >> 32);
-  return r;
-}
 __device__ __forceinline__ float cldf(const float* p) { return __uint_as_float(cld32(p)); }
+__device__ __forceinline__ uint64_t cld64(const void* p) {
+  return __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // dst[e] = src(e) for e < n, e = row * ncols + col -> src + row * row_stride + col; each thread
 // issues 8 loads before it stores (a plain copy loop would wait for every load in turn)
@@ -290,10 +282,27 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
       bh0[mt] = bl0[mt] = bh1[mt] = bl1[mt] = (W16)(0u);
       if (mt < mtiles && arow[mt] >= 0) {
         const uint32_t* ap = A + (size_t)arow[mt] * lda + (size_t)chunk * 8;
-        bh0[mt] = COH ? load_w16c(ap) : load_w16(ap);
-        bl0[mt] = COH ? load_w16c(ap + 4) : load_w16(ap + 4);
-        bh1[mt] = COH ? load_w16c(ap + 8) : load_w16(ap + 8);
-        bl1[mt] = COH ? load_w16c(ap + 12) : load_w16(ap + 12);
+        if constexpr (COH) {
+          bh0[mt] = pload4(ap);
+          bl0[mt] = pload4(ap + 4);
+          bh1[mt] = pload4(ap + 8);
+          bl1[mt] = pload4(ap + 12);
+        } else {
+          bh0[mt] = load_w16(ap);
+          bl0[mt] = load_w16(ap + 4);
+          bh1[mt] = load_w16(ap + 8);
+          bl1[mt] = load_w16(ap + 12);
+        }
+      }
+    }
+    if constexpr (COH) {
+      // the device-coherent loads are issued from inline assembly: wait for them explicitly
+#pragma unroll
+      for (int mt = 0; mt < kBatchMTiles; ++mt) {
+        vm_wait(bh0[mt]);
+        vm_wait(bl0[mt]);
+        vm_wait(bh1[mt]);
+        vm_wait(bl1[mt]);
       }
     }
 #pragma unroll
@@ -443,7 +452,7 @@ __device__ void phase_attn_tree(const BParams* bp, BShared* sh, int l, uint32_t*
         for (int k = 0; k < 4; ++k)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            t[k][j] = (src[k] && ks0 + j < KS) ? ldf(src[k] + (size_t)(ks0 + j) * M * N) : 0.f;
+            t[k][j] = (src[k] && ks0 + j < KS) ? cldf(src[k] + (size_t)(ks0 + j) * M * N) : 0.f;
 #pragma unroll
         for (int k = 0; k < 4; ++k)
 #pragma unroll
@@ -460,7 +469,7 @@ __device__ void phase_attn_tree(const BParams* bp, BShared* sh, int l, uint32_t*
         }
       }
     }
-    lds_fill<false>(kvs, kvc, fp * 2 * d, 2 * d, (size_t)2 * d);
+    lds_fill<true>(kvs, kvc, fp * 2 * d, 2 * d, (size_t)2 * d);
     __syncthreads();
     // q rows (v < R) and k rows (v >= R): norm + RoPE at the row's position, one wave per vector
     for (int v = wave; v < 2 * R; v += kWaves) {
@@ -567,7 +576,7 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
         for (int k = 0; k < 4; ++k)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            t[k][j] = (src[k] && ks0 + j < KS) ? ldf(src[k] + (size_t)(ks0 + j) * M * N) : 0.f;
+            t[k][j] = (src[k] && ks0 + j < KS) ? cldf(src[k] + (size_t)(ks0 + j) * M * N) : 0.f;
 #pragma unroll
         for (int k = 0; k < 4; ++k)
 #pragma unroll
@@ -584,7 +593,7 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
         }
       }
     }
-    lds_fill<false>(kvs, kvc, fp * 2 * d, 2 * d, (size_t)2 * d);
+    lds_fill<true>(kvs, kvc, fp * 2 * d, 2 * d, (size_t)2 * d);
     __syncthreads();
     // q rows (v < R) and k rows (v >= R): norm + RoPE, one wave per vector
     for (int v = wave; v < 2 * R; v += kWaves) {
@@ -667,7 +676,7 @@ __device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float*
     float* x = bp->x + (size_t)i * H;
     float ss = 0.f;
     for (int e = tid(); e < H; e += kThreads) {
-      const float v = ldf(x + e) + sum_parts(bp->part + (size_t)i * H + e, (size_t)M * H, KS);
+      const float v = cldf(x + e) + sum_parts<true>(bp->part + (size_t)i * H + e, (size_t)M * H, KS);
       cstf(x + e, v);
       xs[e] = v;
       ss = fmaf(v, v, ss);
@@ -736,7 +745,7 @@ __device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
     if (nr == 0) continue;
     const int n0 = gi * 64;
     const bf16_t* W = bw(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
-    gemm_unit<4, kProjNTW>(
+    gemm_unit<4, kProjNTW, true>(
         [&](int nt, int m) -> const bf16_t* {
           const int f = n0 + 16 * nt + m;
           return f < V ? W + (size_t)f * H : nullptr;
@@ -822,16 +831,16 @@ __device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, 
     if (has_draft) {
       // q of d_t: drafted last pass from the anchor's row, offset r + 1
       const uint64_t* rec = bp->drec + ((((size_t)((pass - 1) & 1) * bp->lanes + ln) * rpl + st[kLnPrevAnchor]) * K + r) * SW;
-      const uint64_t w0 = *G(rec);
+      const uint64_t w0 = cld64(rec);
       dtok = (int)(uint32_t)w0;
       nq = (int)(w0 >> 32);
       for (int i = tid(); i < nq; i += kThreads) {
-        qidx[i] = (int)(uint32_t)*G(rec + 1 + i);
-        qprob[i] = __longlong_as_double((long long)*G(rec + 1 + p->topk + i));
+        qidx[i] = (int)(uint32_t)cld64(rec + 1 + i);
+        qprob[i] = __longlong_as_double((long long)cld64(rec + 1 + p->topk + i));
       }
     }
     const float* src = bp->logits + (size_t)u * V;
-    lds_fill<false>(lg, src, V, V, 0);
+    lds_fill<true>(lg, src, V, V, 0);
     __syncthreads();
     if (bp->tr_logits && st[kLnFrame] < bp->tr_frames && pass < bp->tr_max_rounds) {
       // the slot layout of the single-stream trace: verify row r, then draft (r, j)
@@ -1016,20 +1025,20 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
     for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = 0;
     if (tid() == 0) st[kLnFrame] = lane_id - bp->lanes;
   } else {
-    for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = *G(gst + i);
+    for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = (int)cld32(gst + i);
   }
   __syncthreads();
   const bool was_active = !first && st[kLnActive];
   const bool tree_pass = was_active && tree_rows<TR>(bp, st);
   if (was_active) {
     const int R = st[kLnRows];
-    for (int i = tid(); i < R; i += kThreads) sh->vr[i] = *G(bp->vres + lane_id * rpl + i);
+    for (int i = tid(); i < R; i += kThreads) sh->vr[i] = (int)cld32(bp->vres + lane_id * rpl + i);
     const int par = st[kLnPass] & 1;
     if (!TR)
       for (int i = tid(); i < R * K; i += kThreads) {
         const int r = i / K, jj = i - r * K;
         sh->dt[r][jj] = jj < row_drafts<TR>(bp, p, st, r)
-                            ? (int)(uint32_t)*G(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
+                            ? (int)(uint32_t)cld64(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + r) * K + jj) * bp->sup_words)
                             : -1;
       }
   }
@@ -1097,7 +1106,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
       for (int e = tid(); e < per; e += kThreads) {
         const int lg = e / (2 * d), w = e - lg * 2 * d;
         float* base = bp->kv + ((size_t)lane_id * p->L * p->nkv + lg) * slots * 2 * d;
-        cstf(base + (size_t)dst * 2 * d + w, ldf(base + (size_t)src * 2 * d + w));
+        cstf(base + (size_t)dst * 2 * d + w, cldf(base + (size_t)src * 2 * d + w));
       }
       __syncthreads();
     }
@@ -1106,7 +1115,7 @@ __device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, b
       const int kn = min(K, n - m_new), par = st[kLnPass] & 1;
       for (int r = 1 + tid(); r <= bp->tree_nodes; r += kThreads)
         if (bp->t_depth[r] <= kn)
-          st[kLnCand + r] = (int)(uint32_t)*G(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + arow) * K +
+          st[kLnCand + r] = (int)(uint32_t)cld64(bp->drec + ((((size_t)par * bp->lanes + lane_id) * rpl + arow) * K +
                                                          (bp->t_depth[r] - 1)) * bp->sup_words + 1 + bp->t_rank[r]);
     }
   }
@@ -1342,23 +1351,23 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
   while (ok) {
     if (lane_wg) lane_commit<TR>(bp, sh, call, first, dyn, A0);
     first = false;
-    if (!(ok = grid_sync(bp, gen, sh))) break;
+    if (!(ok = grid_sync<BParams, false>(bp, gen, sh))) break;
     for (int i = tid(); i < bp->lanes * kLaneInts; i += kThreads)
-      sh->ln[i / kLaneInts][i % kLaneInts] = *G(bp->lane + i);
+      sh->ln[i / kLaneInts][i % kLaneInts] = (int)cld32(bp->lane + i);
     __syncthreads();
     int any = 0;
     for (int i = 0; i < bp->lanes; ++i) any |= sh->ln[i][kLnActive];
     if (!any) break;
     for (int l = 0; l < L && ok; ++l) {
-      proj_partial<4>(bp, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, bp->ks_qkv, A0, dyn);
-      ok = grid_sync(bp, gen, sh);
+      proj_partial<4, BParams, true>(bp, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, bp->ks_qkv, A0, dyn);
+      ok = grid_sync<BParams, false>(bp, gen, sh);
       if (ok) {
         if (TR) phase_attn_tree(bp, sh, l, A1, dyn);
         else phase_attn(bp, sh, l, A1, dyn);
       }
-      ok = ok && grid_sync(bp, gen, sh);
-      if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
-      ok = ok && grid_sync(bp, gen, sh);
+      ok = ok && grid_sync<BParams, false>(bp, gen, sh);
+      if (ok) proj_partial<4, BParams, true>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
+      ok = ok && grid_sync<BParams, false>(bp, gen, sh);
       if (ok) phase_resid<TR>(bp, sh, bp->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, 0, dyn);
       if (ok && l == 0 && counter_wg && tid() < 64) {
         const unsigned long long pb = pass_bytes_batch<TR>(bp, sh);
@@ -1367,22 +1376,22 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
           n_bytes += pb;
         }
       }
-      ok = ok && grid_sync(bp, gen, sh);
-      if (ok) phase_gu(bp, l, A0, A1, dyn);
-      ok = ok && grid_sync(bp, gen, sh);
-      if (ok) proj_partial<4>(bp, bw(p, boff(p, l, p->o_wd)), H, p->F, bp->ks_down, A1, dyn);
-      ok = ok && grid_sync(bp, gen, sh);
+      ok = ok && grid_sync<BParams, false>(bp, gen, sh);
+      if (ok) phase_gu<BParams, true>(bp, l, A0, A1, dyn);
+      ok = ok && grid_sync<BParams, false>(bp, gen, sh);
+      if (ok) proj_partial<4, BParams, true>(bp, bw(p, boff(p, l, p->o_wd)), H, p->F, bp->ks_down, A1, dyn);
+      ok = ok && grid_sync<BParams, false>(bp, gen, sh);
       if (ok) {
         if (l + 1 < L) phase_resid<TR>(bp, sh, bp->ks_down, bfw(p, boff(p, l + 1, p->o_attn_norm)), A0, 0, dyn);
         else phase_resid<TR>(bp, sh, bp->ks_down, bfw(p, p->o_final_norm), nullptr, 1, dyn);
       }
-      ok = ok && grid_sync(bp, gen, sh);
+      ok = ok && grid_sync<BParams, false>(bp, gen, sh);
     }
     if (!ok) break;
     phase_heads<TR>(bp, sh, dyn);
-    if (!(ok = grid_sync(bp, gen, sh))) break;
+    if (!(ok = grid_sync<BParams, false>(bp, gen, sh))) break;
     phase_sample<TR>(bp, sh, call, dyn);
-    if (!(ok = grid_sync(bp, gen, sh))) break;
+    if (!(ok = grid_sync<BParams, false>(bp, gen, sh))) break;
   }
   if (!ok && lane_wg) lane_abort(bp, sh, call);
   if (counter_wg && tid() == 0) {
