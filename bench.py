@@ -108,6 +108,8 @@ def parse():
                     help="sparse-tree verification (Sec. 2.2, Fig. 2) with the packed tree of FILE (parents, ranks; "
                          "paper_2609_37007_amd/tree.py writes them); the frames then run through the batched "
                          "kernel's tree lane")
+    ap.add_argument("--gemv", action="store_true",
+                    help="projections and LM heads on the VALU GEMV instead of the matrix cores (cfg matrix_path 1)")
     ap.add_argument("--phases", action="store_true",
                     help="per-phase time of the frame kernel's passes from its per-workgroup clock trace")
     ap.add_argument("--residency", action="store_true",
@@ -371,7 +373,7 @@ def run_streams(a) -> int:
     blob = S.make_weights(s, seed=0, head_scale=a.head_scale)
     cfg = R.make_cfg(n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
                      head_dim=s.head_dim, ffn=s.ffn, n_codes=n, vocab=s.vocab, max_draft=s.max_draft,
-                     dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K)
+                     dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K, matrix_path=1 if a.gemv else 0)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     torch_stream = torch.cuda.current_stream(dev)
@@ -622,7 +624,7 @@ def run_phases(a) -> int:
     blob = make_blob(S, s, a)
     cfg = R.make_cfg(n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
                      head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
-                     dtype=s.dtype, topk=topk, temperature=0.9, draft_len=K)
+                     dtype=s.dtype, topk=topk, temperature=0.9, draft_len=K, matrix_path=1 if a.gemv else 0)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     ts = torch.cuda.current_stream(dev)
@@ -736,7 +738,7 @@ def main() -> int:
     blob_sha = hashlib.sha256(blob).hexdigest()[:16]
     cfg = R.make_cfg(n_layers=s.n_layers, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
                      head_dim=s.head_dim, ffn=s.ffn, n_codes=s.n_codes, vocab=s.vocab, max_draft=s.max_draft,
-                     dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K)
+                     dtype=s.dtype, topk=topk, temperature=temperature, draft_len=K, matrix_path=1 if a.gemv else 0)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     torch_stream = torch.cuda.current_stream(dev)
@@ -798,7 +800,7 @@ def main() -> int:
     bytes_per_launch = st["weight_bytes"].astype(np.float64)
     achieved = float(bytes_per_launch.sum() / (launch_ms.sum() * 1e-3) / 1e9)
     traffic = measured_traffic() if (a.workload == "mcd1024" and K == 4 and a.head_scale == 1.0 and not tree
-                                     and a.offsets == "seed") else None
+                                     and a.offsets == "seed" and not a.gemv) else None
     codes_per_s = n * steps / elapsed
     # the box's own read rates for a buffer of one launch's mean bytes per pass
     box = stream_read_rates(torch, dev, torch_stream, int(bytes_per_launch.sum() / calls) & ~255)
@@ -837,6 +839,7 @@ def main() -> int:
             "batch": 1,
             "weights_sha256_16": blob_sha,
             "parallelism": "single GPU, one persistent workgroup per compute unit",
+            "matrix_path": "VALU GEMV" if a.gemv else "matrix cores when the pass has at most 8 rows",
         },
         "accepted_tokens_per_call": round(n * steps / calls, 4),
         "mean_tokens_per_round": round((n * steps - steps) / max(rounds, 1), 4),

@@ -63,7 +63,12 @@ typedef struct {
   int32_t topk;        /* 1..256 */
   int32_t draft_len;   /* K, 0..min(max_draft, 14); 0 = plain autoregressive sampling */
   int32_t draft_greedy;/* 0: drafts sampled from the draft distribution; 1: its argmax */
-  int32_t reserved[3];
+  int32_t matrix_path; /* projections and LM heads of the single-frame kernel: 0 = matrix cores
+                        * (MFMA, activations as bf16 hi + lo) for bf16 and int8 weights when a
+                        * pass has at most 8 rows, else the VALU GEMV; 1 = the VALU GEMV (bf16
+                        * or f32 weights; EUNSUPPORTED for int8). Same results within the
+                        * logit tolerance; the choice is a measured one (bench.py --gemv). */
+  int32_t reserved[2];
   double rms_eps, rope_base, temperature;
 } rvqsd_cfg;
 

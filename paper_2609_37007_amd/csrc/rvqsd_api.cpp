@@ -124,8 +124,10 @@ int validate_cfg(const rvqsd_cfg* c, int nwg) {
       c->topk < 1 || c->draft_len < 0 || c->draft_len > c->max_draft || !(c->temperature > 0.0) ||
       !(c->rms_eps > 0.0) || !(c->rope_base > 0.0) || (c->dtype < RVQSD_DTYPE_F32 || c->dtype > RVQSD_DTYPE_I8) ||
       (c->n_q_heads % c->n_kv_heads) != 0 || (c->qk_norm != 0 && c->qk_norm != 1) ||
-      (c->draft_greedy != 0 && c->draft_greedy != 1))
+      (c->draft_greedy != 0 && c->draft_greedy != 1) || (c->matrix_path != 0 && c->matrix_path != 1))
     return set_err(RVQSD_EINVAL, "invalid configuration field");
+  if (c->dtype == RVQSD_DTYPE_I8 && c->matrix_path == 1)
+    return set_err(RVQSD_EUNSUPPORTED, "int8 weights run on the matrix cores only (matrix_path 0)");
   const int epc = c->dtype == RVQSD_DTYPE_F32 ? 4 : 8;
   const int qd = c->n_q_heads * c->head_dim;
   const int quant = 64 * epc;
@@ -148,7 +150,7 @@ int validate_cfg(const rvqsd_cfg* c, int nwg) {
 }
 
 // Work-area floats needed by every phase for a given staging width.
-size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
+size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, bool mfma, int stage_cols) {
   const int H = c->hidden, qd = c->n_q_heads * c->head_dim, kd = c->n_kv_heads * c->head_dim, F = c->ffn;
   const int V = c->vocab, d = c->head_dim, K = c->draft_len;
   const int cpw = (H + nwg - 1) / nwg;
@@ -163,7 +165,7 @@ size_t work_floats(const rvqsd_cfg* c, int nwg, int mr, int stage_cols) {
   auto need = [&](size_t f) {
     if (f > w) w = f;
   };
-  if (c->dtype != RVQSD_DTYPE_F32 && mr <= 8) {
+  if (mfma) {
     // MFMA phases: split activations, chunk sums of squares, wave partial tiles, outputs
     // split rows carry 4 words of padding; wave partials: 1 tile (QKV, O, down),
     // 2 (gate/up), 5 (heads) at a time
@@ -437,6 +439,7 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   m->device = dev;
   m->nwg = nwg;
   m->mr = frame_max_rows(cfg->draft_len);
+  m->mfma = cfg->dtype != RVQSD_DTYPE_F32 && m->mr <= 8 && cfg->matrix_path == 0;
   if (cfg->dtype == RVQSD_DTYPE_I8 && m->mr > 8) {
     delete m;
     return set_err(RVQSD_EUNSUPPORTED, "int8 weights run on the matrix-core path only: draft_len <= 7");
@@ -451,7 +454,7 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
       return set_err(RVQSD_EUNSUPPORTED, "int8 weights: a workgroup's rows of one matrix exceed %d", kThreads);
     }
   }
-  if (cfg->dtype != RVQSD_DTYPE_F32 && m->mr <= 8 &&
+  if (m->mfma &&
       (k.H > 512 * kUptH || k.qdim > 512 * kUptQ || k.F > 512 * kUptF)) {
     delete m;
     return set_err(RVQSD_EUNSUPPORTED, "bf16 matrix path takes hidden <= %d, n_q_heads*head_dim <= %d, ffn <= %d",
@@ -471,7 +474,7 @@ rvqsd_status rvqsd_create(const rvqsd_weights* w, const rvqsd_cfg* cfg, rvqsd_mo
   const int epc = cfg->dtype == RVQSD_DTYPE_F32 ? 4 : 8;
   int stage = (int)(qd > H ? qd : H);
   if (2 * ((int)F / epc) <= kThreads && (int)F > stage) stage = (int)F;
-  const size_t work = work_floats(cfg, nwg, m->mr, stage);
+  const size_t work = work_floats(cfg, nwg, m->mr, m->mfma, stage);
   size_t lds = (head + work) * 4;
   if (lds > budget) {
     delete m;
@@ -671,7 +674,7 @@ static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t
   fa.epoch_base = s->epoch;
   s->epoch += s->epoch_step;
   char err[256];
-  int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, (void*)s->stream, s->m->lds_bytes, err,
+  int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, s->m->mfma, (void*)s->stream, s->m->lds_bytes, err,
                         sizeof(err));
   if (st) return set_err(st, "%s", err);
   return RVQSD_OK;

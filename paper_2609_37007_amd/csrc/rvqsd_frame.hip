@@ -386,10 +386,6 @@ template <>
 struct IsI8<int8_t> {
   static constexpr bool value = true;
 };
-template <typename WT, int MR>
-struct UseMfma {
-  static constexpr bool value = (IsBf16<WT>::value || IsI8<WT>::value) && MR <= 8;
-};
 
 // Scale of row `row` of the [rows][cols] matrix at byte offset off: its fp32 row scale for
 // int8 codes (stored after the codes), 1 otherwise.
@@ -1834,7 +1830,9 @@ __device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c) {
   return b;
 }
 
-template <typename WT, int MR>
+// MF: projections and LM heads on the matrix cores (bf16 or int8 weights, at most 8 rows), else
+// on the VALU GEMV
+template <typename WT, int MR, bool MF>
 __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
   constexpr int RPT = MR <= 8 ? 8 : 4;
   __shared__ Shared shs;
@@ -1911,28 +1909,28 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   } while (0)
     for (int l = 0; l < L && ok; ++l) {
       RVQSD_READY(5 * l + 0);
-      if constexpr (UseMfma<WT, MR>::value) ok = phase_qkv_m<WT, MR>(c, l);
+      if constexpr (MF) ok = phase_qkv_m<WT, MR>(c, l);
       else ok = phase_qkv<WT, MR, 4>(c, l);
       RVQSD_STAMP(5 * l + 0);
       RVQSD_READY(5 * l + 1);
       if (ok) ok = phase_attn<MR>(c, l);
       RVQSD_STAMP(5 * l + 1);
       RVQSD_READY(5 * l + 2);
-      if constexpr (UseMfma<WT, MR>::value) {
+      if constexpr (MF) {
         if (ok) ok = phase_proj_m<WT, MR, (MR + 1) / 2, kUptQ>(c, l, false);
       } else {
         if (ok) ok = phase_proj<WT, MR, 4>(c, l, false);
       }
       RVQSD_STAMP(5 * l + 2);
       RVQSD_READY(5 * l + 3);
-      if constexpr (UseMfma<WT, MR>::value) {
+      if constexpr (MF) {
         if (ok) ok = phase_gu_m<WT, MR>(c, l);
       } else {
         if (ok) ok = phase_gu<WT, MR, (MR <= 8 ? 8 : 4)>(c, l);
       }
       RVQSD_STAMP(5 * l + 3);
       RVQSD_READY(5 * l + 4);
-      if constexpr (UseMfma<WT, MR>::value) {
+      if constexpr (MF) {
         if (ok) ok = phase_proj_m<WT, MR, (3 * MR + 3) / 4, kUptF>(c, l, true);
       } else {
         if (ok) ok = phase_proj<WT, MR, 4>(c, l, true);
@@ -1940,7 +1938,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
       RVQSD_STAMP(5 * l + 4);
     }
     RVQSD_READY(ph_heads(L));
-    if constexpr (UseMfma<WT, MR>::value) {
+    if constexpr (MF) {
       if (ok) ok = phase_heads_m<WT, MR>(c);
     } else {
       if (ok) ok = phase_heads<WT, MR, (MR <= 5 ? 8 : 4)>(c);
@@ -2005,9 +2003,9 @@ int frame_lds_head_floats(int mr, int cpw) {
   return kMaxRows * cpw + kWaves * (rpt + 1) * mr;
 }
 
-template <typename WT, int MR>
+template <typename WT, int MR, bool MF>
 static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* stream, size_t lds, char* err, size_t errlen) {
-  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR>);
+  const void* fn = reinterpret_cast<const void*>(&frame_kernel<WT, MR, MF>);
   static size_t attr_bytes = 0;  // per instantiation
   if (lds > attr_bytes) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -2029,16 +2027,20 @@ static int launch_t(const KParams* gp, const FrameArgs& fa, int nwg, void* strea
   return RVQSD_OK;
 }
 
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream,
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, bool mfma, void* stream,
                  size_t lds_bytes, char* err, size_t errlen) {
-#define RVQSD_CASE(T, M) \
-  if (mr == M) return launch_t<T, M>(gp, fa, nwg, stream, lds_bytes, err, errlen);
+#define RVQSD_CASE(T, M, F) \
+  if (mr == M) return launch_t<T, M, F>(gp, fa, nwg, stream, lds_bytes, err, errlen);
   if (dtype == RVQSD_DTYPE_F32) {
-    RVQSD_CASE(float, 2) RVQSD_CASE(float, 4) RVQSD_CASE(float, 5) RVQSD_CASE(float, 8) RVQSD_CASE(float, 16)
+    RVQSD_CASE(float, 2, false) RVQSD_CASE(float, 4, false) RVQSD_CASE(float, 5, false) RVQSD_CASE(float, 8, false)
+    RVQSD_CASE(float, 16, false)
   } else if (dtype == RVQSD_DTYPE_I8) {
-    RVQSD_CASE(int8_t, 2) RVQSD_CASE(int8_t, 4) RVQSD_CASE(int8_t, 5) RVQSD_CASE(int8_t, 8)
+    if (mfma) { RVQSD_CASE(int8_t, 2, true) RVQSD_CASE(int8_t, 4, true) RVQSD_CASE(int8_t, 5, true) RVQSD_CASE(int8_t, 8, true) }
+  } else if (mfma) {
+    RVQSD_CASE(bf16_t, 2, true) RVQSD_CASE(bf16_t, 4, true) RVQSD_CASE(bf16_t, 5, true) RVQSD_CASE(bf16_t, 8, true)
   } else {
-    RVQSD_CASE(bf16_t, 2) RVQSD_CASE(bf16_t, 4) RVQSD_CASE(bf16_t, 5) RVQSD_CASE(bf16_t, 8) RVQSD_CASE(bf16_t, 16)
+    RVQSD_CASE(bf16_t, 2, false) RVQSD_CASE(bf16_t, 4, false) RVQSD_CASE(bf16_t, 5, false) RVQSD_CASE(bf16_t, 8, false)
+    RVQSD_CASE(bf16_t, 16, false)
   }
 #undef RVQSD_CASE
   snprintf(err, errlen, "no kernel for %d rows", mr);

@@ -148,7 +148,7 @@ inline uint32_t frame_epoch_step(int L) {
 int set_last_error(int st, const char* msg);
 
 // Host entry into the kernel translation unit. gp: KParams in device memory.
-int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, void* stream,
+int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int mr, bool mfma, void* stream,
                  size_t lds_bytes, char* err, size_t errlen);
 
 // ---------------------------------------------------------------- batched path
@@ -276,6 +276,7 @@ struct rvqsd_model {
   int device;
   int nwg;
   int mr;               // rows the frame kernel is instantiated for
+  bool mfma;            // projections and heads on the matrix cores (else the VALU GEMV)
   int wbytes;           // bytes per matrix element
   size_t lds_bytes;
   int stage_cols;

@@ -35,7 +35,8 @@ class rvqsd_cfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "abi_version", "n_layers", "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "n_codes", "vocab",
         "max_draft", "dtype", "qk_norm", "topk", "draft_len", "draft_greedy")] + [
-        ("reserved", ctypes.c_int32 * 3), ("rms_eps", ctypes.c_double), ("rope_base", ctypes.c_double),
+        ("matrix_path", ctypes.c_int32), ("reserved", ctypes.c_int32 * 2), ("rms_eps", ctypes.c_double),
+        ("rope_base", ctypes.c_double),
         ("temperature", ctypes.c_double)]
 
 
@@ -172,12 +173,14 @@ def _ptr(a: np.ndarray):
 
 
 def make_cfg(*, n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, n_codes, vocab, max_draft, dtype, topk,
-             temperature, draft_len, draft_greedy=0, qk_norm=1, rms_eps=1e-6, rope_base=1e6) -> rvqsd_cfg:
+             temperature, draft_len, draft_greedy=0, qk_norm=1, rms_eps=1e-6, rope_base=1e6,
+             matrix_path=0) -> rvqsd_cfg:
     c = rvqsd_cfg()
     c.abi_version = RVQSD_ABI_VERSION
     for k, v in dict(n_layers=n_layers, hidden=hidden, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
                      head_dim=head_dim, ffn=ffn, n_codes=n_codes, vocab=vocab, max_draft=max_draft, dtype=dtype,
-                     qk_norm=qk_norm, topk=topk, draft_len=draft_len, draft_greedy=draft_greedy).items():
+                     qk_norm=qk_norm, topk=topk, draft_len=draft_len, draft_greedy=draft_greedy,
+                     matrix_path=matrix_path).items():
         setattr(c, k, int(v))
     c.rms_eps, c.rope_base, c.temperature = float(rms_eps), float(rope_base), float(temperature)
     return c

@@ -73,11 +73,12 @@ def shape_with(base: S.ModelShape, **kw) -> S.ModelShape:
 class Rig:
     """A GPU model + stream and an oracle with the same configuration."""
 
-    def __init__(self, s, topk, K, T=0.9, greedy=0, head_scale=1.0, hip_stream=None, tied_rows_from=-1):
+    def __init__(self, s, topk, K, T=0.9, greedy=0, head_scale=1.0, hip_stream=None, tied_rows_from=-1,
+                 matrix_path=0):
         self.s, self.topk, self.K, self.T, self.greedy = s, topk, K, T, greedy
         blob = blob_of(s, head_scale, tied_rows_from)
         self.model = R.Model(blob, R.make_cfg(**shape_kwargs(s), topk=topk, temperature=T, draft_len=K,
-                                              draft_greedy=greedy))
+                                              draft_greedy=greedy, matrix_path=matrix_path))
         self.stream = R.Stream(self.model, hip_stream=hip_stream)
         self.orc = make_oracle(s, blob, topk=topk, temperature=T, draft_len=K,
                                draft_mode=O.DRAFT_GREEDY if greedy else O.DRAFT_SAMPLED)
@@ -256,6 +257,20 @@ def test_mcd1024_draft_lengths(K):
             codes, st = rig.stream.decode_frame_u(f[i], int(c0[i]), u[i])
             assert st["target_calls"] == s.n_codes and st["drafted"] == 0
             assert np.array_equal(codes, rig.orc.ar_frame(f[i], int(c0[i]), u[i]))
+    rig.close()
+
+
+@pytest.mark.parametrize("K", [1, 4, 7])
+def test_mcd1024_valu_gemv_path(K):
+    """The VALU GEMV form of the projections and heads (matrix_path 1) on the bf16 model, every
+    instantiation the matrix cores otherwise take (2, 5 and 8 rows): same parity rule."""
+    s = S.MCD_1024
+    rig = Rig(s, topk=50, K=K, matrix_path=1)
+    f, c0 = S.frame_inputs(s, 1000)
+    u = S.uniforms(1000)
+    print(f"mcd1024 bf16 K={K} on the VALU GEMV: frames 0, 1, 500", flush=True)
+    worst, excused = check_frames(rig, [0, 1, 500], f, c0, u)
+    print(f"max logit error {worst:.3g}, excused frames {excused}", flush=True)
     rig.close()
 
 
@@ -439,7 +454,7 @@ def test_blob_and_config_errors():
     assert status_of(blob[:-4], cfg) == R.EBLOB
     cfg2 = R.make_cfg(**{**shape_kwargs(s), "vocab": 65}, topk=8, temperature=0.9, draft_len=3)
     assert status_of(blob, cfg2) == R.EBLOB
-    for kw in ({"topk": 0}, {"draft_len": 15}, {"temperature": 0.0}):
+    for kw in ({"topk": 0}, {"draft_len": 15}, {"temperature": 0.0}, {"matrix_path": 2}):
         args = dict(topk=8, temperature=0.9, draft_len=3)
         args.update(kw)
         assert status_of(blob, R.make_cfg(**shape_kwargs(s), **args)) in (R.EINVAL, R.EUNSUPPORTED)

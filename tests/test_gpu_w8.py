@@ -79,6 +79,9 @@ def test_w8_limits():
     with pytest.raises(R.RvqsdError) as e:  # 15 rows: beyond the matrix-core path
         R.Model(blob, R.make_cfg(**shape_kwargs(s), topk=16, temperature=0.9, draft_len=14))
     assert e.value.status == R.EUNSUPPORTED
+    with pytest.raises(R.RvqsdError) as e:  # int8 codes are widened for the matrix cores only
+        R.Model(blob, R.make_cfg(**shape_kwargs(s), topk=16, temperature=0.9, draft_len=3, matrix_path=1))
+    assert e.value.status == R.EUNSUPPORTED
     model = R.Model(blob, R.make_cfg(**shape_kwargs(s), topk=16, temperature=0.9, draft_len=3))
     with pytest.raises(R.RvqsdError) as e:  # the batched kernel reads bf16 only
         R.Stream(model, max_streams=4)
