@@ -176,6 +176,16 @@ typedef uint32_t W16 __attribute__((ext_vector_type(4)));
 // issued here and completes at vm_wait, which names the result as an operand so
 // that no use of it is scheduled before the wait; several loads issued back to
 // back are in flight together. Each 32-bit word is written atomically by its
+// Four parity words through one device-coherent 16-byte vector store (p 16-byte aligned): each
+// word's lowest mantissa bit carries the parity; a reader checks every word on its own.
+__device__ __forceinline__ void pstore4(uint32_t* p, float a, float b, float c, float d, uint32_t par) {
+  W16 w;
+  w[0] = (__float_as_uint(a) & ~1u) | par;
+  w[1] = (__float_as_uint(b) & ~1u) | par;
+  w[2] = (__float_as_uint(c) & ~1u) | par;
+  w[3] = (__float_as_uint(d) & ~1u) | par;
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(w) : "memory");
+}
 // producer, so every word's parity bit is checked on its own.
 __device__ __forceinline__ W16 pload4(const uint32_t* p) {
   W16 r;

@@ -877,12 +877,195 @@ __device__ __forceinline__ bool phase_qkv(const Ctx& c, int l) {
 // prefetched into LDS while the workgroup waits for this pass's q, k and v.
 // In LDS each position's k and v are padded to 2d + 4 floats so that the 16
 // positions read by one wave fall on different banks.
+// phase_attn for a head dimension D known at compile time (the 1024-wide model's 128): every
+// per-lane loop has a fixed trip count (no per-element lane masks), the weighted value sum reads
+// 16 bytes per lane (lane = position group gi, dimensions 4 li .. 4 li + 3; the groups are added
+// across the wave in a fixed order), and the output goes out as one 16-byte parity store per lane.
+template <int MR, int D>
+__device__ __forceinline__ bool phase_attn_d(const Ctx& c, int l) {
+  const KParams* p = c.p;
+  const Shared* sh = c.sh;
+  const int h = blockIdx.x;
+  constexpr int half = D / 2;
+  const int R = sh->rows, N = p->nqkv, fp = sh->first_pos;
+  const int g = h / (p->nq / p->nkv);
+  const int qoff = h * D, koff = p->qdim + g * D;
+  constexpr int ps = 2 * D + 4;    // LDS floats per position
+  float* qs = c.work;              // [kMaxRows][D], then ks, vs
+  float* ks = qs + kMaxRows * D;
+  float* vs = ks + kMaxRows * D;
+  float* kv = vs + kMaxRows * D;   // [kMaxPos][ps]: k, v of every position
+  float* pw_lds = kv + kMaxPos * ps;  // [kMaxRows][kMaxPos] softmax weights of each row
+  uint64_t* gkv = reinterpret_cast<uint64_t*>(p->kvc + ((size_t)h * p->L + l) * kMaxPos * 2 * D);
+  const int lane = tid() & 63, wave = tid() >> 6;
+  // past positions 0 .. fp-1: issue the loads now, store them to LDS after the wait
+  constexpr int KVW = (kMaxPos * D + kThreads - 1) / kThreads;  // 64-bit words per thread
+  const int past_words = fp * D;
+  uint64_t pw[KVW];
+#pragma unroll
+  for (int i = 0; i < KVW; ++i) {
+    const int wi = tid() + i * kThreads;
+    pw[i] = wi < past_words ? xload(gkv + wi) : 0ull;
+  }
+  const uint32_t par = par_layer(c, sh->pass, l);
+  constexpr int d4 = D / 4;
+  const int rd4 = R * d4, kvdim = p->kvdim;
+  const uint32_t* qkvb = p->qkvb;
+  bool ok = poll_quads(
+      c, 3 * rd4, par,
+      [=](int i) {
+        const int part = i / rd4, rem = i - part * rd4, r = rem / d4, k = 4 * (rem - r * d4);
+        const int off = part == 0 ? qoff : koff + (part - 1) * kvdim;
+        return qkvb + (size_t)r * N + off + k;
+      },
+      [=](int i, W16 w) {
+        const int part = i / rd4, rem = i - part * rd4;
+        *reinterpret_cast<W16*>(qs + part * kMaxRows * D + 4 * rem) = w;
+      });
+#pragma unroll
+  for (int i = 0; i < KVW; ++i) {
+    const int wi = tid() + i * kThreads;
+    if (wi < past_words) {
+      const int pos = wi / D, w = wi - pos * D;
+      reinterpret_cast<uint64_t*>(kv + (size_t)pos * ps)[w] = pw[i];
+    }
+  }
+  if (!wg_sync_ok(c, ok)) return false;
+  // per-head RMSNorm + RoPE of q (vectors 0..R-1) and k (R..2R-1), one half-wave per vector;
+  // lane i of the half holds dimensions i + 32 j (j < D / 64) and their partners i + 32 j + D/2
+  const float* qn = c.attn_const + (size_t)l * 2 * D;
+  const float* kn = qn + D;
+  const float* rope = c.attn_const + (size_t)p->L * 2 * D;
+  constexpr int J = D / 64;
+  const int hl = lane & 31;
+  for (int v = 2 * wave + (lane >> 5); v < 2 * R; v += 2 * kWaves) {
+    const bool isq = v < R;
+    const int r = isq ? v : v - R;
+    const float* x = isq ? qs + r * D : ks + r * D;
+    const float* gn = isq ? qn : kn;
+    const int pos = fp + r;
+    float a[J], b[J], ga[J], gb[J], cs[J], sn[J];
+    float s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int i = hl + 32 * j;
+      a[j] = x[i];
+      b[j] = x[i + half];
+      ga[j] = gn[i];
+      gb[j] = gn[i + half];
+      cs[j] = rope[(pos * half + i) * 2];
+      sn[j] = rope[(pos * half + i) * 2 + 1];
+      s2 = fmaf(a[j], a[j], fmaf(b[j], b[j], s2));
+    }
+    float* dst = isq ? qs + r * D : kv + (size_t)pos * ps;
+    const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)D + p->rms_eps) : 1.f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int i = hl + 32 * j;
+      float u = a[j], w = b[j];
+      if (p->qk_norm) {
+        u = u * rs * ga[j];
+        w = w * rs * gb[j];
+      }
+      dst[i] = u * cs[j] - w * sn[j];
+      dst[i + half] = w * cs[j] + u * sn[j];
+    }
+    if (!isq) {
+#pragma unroll
+      for (int j = 0; j < D / 32; ++j) kv[(size_t)pos * ps + D + hl + 32 * j] = vs[r * D + hl + 32 * j];
+    }
+  }
+  __syncthreads();
+  // device copy of the new k, v for later passes: the stores go out while the scores are computed
+  for (int wi = tid(); wi < R * D; wi += kThreads) {
+    const int pos = fp + wi / D, w = wi % D;
+    __hip_atomic_store(G(gkv + (size_t)pos * D + w), reinterpret_cast<const uint64_t*>(kv + (size_t)pos * ps)[w],
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // one wave per row. Scores: lane = (position t = lane / 4, quarter qj of the dimensions)
+  const float scale = 1.f / sqrtf((float)D);
+  const int npos = fp + R;  // positions holding this pass's keys and values
+  constexpr int DQ = D / 4;
+  constexpr int LPD = D / 4;                     // lanes per position group
+  constexpr int NG = LPD >= 64 ? 1 : 64 / LPD;   // position groups
+  constexpr int PPG = kMaxPos / NG;              // positions per group
+  const int t = lane >> 2, qj = lane & 3;
+  const int gi = lane / LPD, li = lane - gi * LPD;
+  for (int r = wave; r < MR; r += kWaves) {
+    if (r < R) {
+      const int last = fp + r;
+      float part = 0.f;
+      if (t <= last) {
+        const f32x4* qv = reinterpret_cast<const f32x4*>(qs + r * D + qj * DQ);
+        const f32x4* kk = reinterpret_cast<const f32x4*>(kv + (size_t)t * ps + qj * DQ);
+        float p0 = 0.f, p1 = 0.f;
+#pragma unroll
+        for (int e = 0; e < DQ / 4; ++e) {
+          const f32x4 qa = qv[e], ka = kk[e];
+          p0 = fmaf(qa.x, ka.x, p0);
+          p1 = fmaf(qa.y, ka.y, p1);
+          p0 = fmaf(qa.z, ka.z, p0);
+          p1 = fmaf(qa.w, ka.w, p1);
+        }
+        part = p0 + p1;
+      }
+      part += dpp<0xB1>(part);
+      part += dpp<0x4E>(part);
+      const float sc = t <= last ? part * scale : -INFINITY;
+      const float rm = row16_max(sc);
+      const float mx = fmaxf(fmaxf(lane_val(rm, 15), lane_val(rm, 31)), fmaxf(lane_val(rm, 47), lane_val(rm, 63)));
+      const float e = t <= last ? expf(sc - mx) : 0.f;
+      const float rsum = row16_sum(qj == 0 ? e : 0.f);
+      const float z = (lane_val(rsum, 15) + lane_val(rsum, 31)) + (lane_val(rsum, 47) + lane_val(rsum, 63));
+      const float pr = e * __builtin_amdgcn_rcpf(z);
+      // the row's weights go through LDS (written and read back by this wave only, in order);
+      // positions at or past npos read the finite row npos - 1 (weight 0) instead of unset rows
+      float* pwr = pw_lds + r * kMaxPos;
+      if (qj == 0) pwr[t] = pr;
+      f32x4 o = {0.f, 0.f, 0.f, 0.f};
+      if (gi < NG) {
+        f32x4 wq[PPG / 4];
+#pragma unroll
+        for (int q4 = 0; q4 < PPG / 4; ++q4) wq[q4] = reinterpret_cast<const f32x4*>(pwr + gi * PPG)[q4];
+        f32x4 vv[PPG];
+#pragma unroll
+        for (int k = 0; k < PPG; ++k)
+          vv[k] = *reinterpret_cast<const f32x4*>(kv + (size_t)min(gi * PPG + k, npos - 1) * ps + D + 4 * li);
+#pragma unroll
+        for (int k = 0; k < PPG; ++k) {
+          const float w = wq[k >> 2][k & 3];
+          o.x = fmaf(w, vv[k].x, o.x);
+          o.y = fmaf(w, vv[k].y, o.y);
+          o.z = fmaf(w, vv[k].z, o.z);
+          o.w = fmaf(w, vv[k].w, o.w);
+        }
+      }
+#pragma unroll
+      for (int xo = LPD; xo < 64 && NG > 1; xo <<= 1) {
+        o.x += __shfl_xor(o.x, xo, 64);
+        o.y += __shfl_xor(o.y, xo, 64);
+        o.z += __shfl_xor(o.z, xo, 64);
+        o.w += __shfl_xor(o.w, xo, 64);
+      }
+      if (gi == 0) pstore4(p->attnb + (size_t)r * p->qdim + qoff + 4 * li, o.x, o.y, o.z, o.w, par);
+    } else {
+#pragma unroll
+      for (int j = 0; j < (D + 63) / 64; ++j)
+        if (lane + 64 * j < D) pstore(p->attnb + (size_t)r * p->qdim + qoff + lane + 64 * j, 0.f, par);
+    }
+  }
+  // the next phase reuses the work area: no wave may still be reading it
+  lds_barrier();
+  return true;
+}
+
 template <int MR>
 __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
   const KParams* p = c.p;
   const Shared* sh = c.sh;
   const int h = blockIdx.x;
   if (h >= p->nq) return true;
+  if (p->d == 128) return phase_attn_d<MR, 128>(c, l);
   const int d = p->d, R = sh->rows, N = p->nqkv, fp = sh->first_pos, half = d / 2;
   const int g = h / (p->nq / p->nkv);
   const int qoff = h * d, koff = p->qdim + g * d;
