@@ -339,7 +339,7 @@ struct Gemv {
           if (sq) {
             float ss = 0.f;
             for (int w = 0; w < wpg; ++w) ss += c.red[w * NVR + RPT * MR + m];
-            sum *= 1.f / sqrtf(ss * inv_k + c.p->rms_eps);
+            sum *= __builtin_amdgcn_rsqf(ss * inv_k + (float)c.p->rms_eps);
           }
           out[r * MR + m] = sum;
         }
@@ -541,11 +541,12 @@ __device__ __forceinline__ bool stage_split(const Ctx& c, const uint32_t* src, i
   return wg_sync_ok(c, true);
 }
 // 1 / sqrt(mean of squares + eps) of staged row m from the per-wave sums of stage_split / gather_split_rows
+// (RMSNorm scales here and below use the hardware reciprocal square root, within 1 ulp)
 __device__ __forceinline__ float rstd_of(const Ctx& c, const float* sqc, int K, int m) {
   const int G = K >> 9;
   float s = 0.f;
   for (int k = 0; k < G; ++k) s += sqc[m * G + k];
-  return 1.f / sqrtf(s / (float)K + c.p->rms_eps);
+  return __builtin_amdgcn_rsqf(s / (float)K + (float)c.p->rms_eps);
 }
 
 // rstd[m] from the per-wave sums of stage_split / gather_split_rows, m < R.
@@ -560,7 +561,7 @@ __device__ __forceinline__ void rstd_from_chunks(const Ctx& c, const float* sqc,
     float s = 0.f;
     for (int q = lane; q < nch; q += 64) s += sqc[m * nch + q];
     s = wave_sum63(s);
-    if (lane == 63) c.sh->rstd[m] = 1.f / sqrtf(s / (float)K + c.p->rms_eps);
+    if (lane == 63) c.sh->rstd[m] = __builtin_amdgcn_rsqf(s / (float)K + (float)c.p->rms_eps);
   }
   __syncthreads();
 }
@@ -737,7 +738,7 @@ __device__ __forceinline__ void row_rstd(const Ctx& c, const float* xs, int ncol
     if (m < R)
       for (int k = lane; k < ncols; k += 64) s += xs[m * ncols + k] * xs[m * ncols + k];
     s = wave_sum63(s);
-    if (lane == 63) c.sh->rstd[m] = m < R ? 1.f / sqrtf(s / (float)ncols + c.p->rms_eps) : 0.f;
+    if (lane == 63) c.sh->rstd[m] = m < R ? __builtin_amdgcn_rsqf(s / (float)ncols + (float)c.p->rms_eps) : 0.f;
   }
   __syncthreads();
 }
@@ -958,7 +959,8 @@ __device__ __forceinline__ bool phase_attn_d(const Ctx& c, int l) {
       s2 = fmaf(a[j], a[j], fmaf(b[j], b[j], s2));
     }
     float* dst = isq ? qs + r * D : kv + (size_t)pos * ps;
-    const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)D + p->rms_eps) : 1.f;
+    // 1 / sqrt(mean of squares + eps) through the hardware reciprocal square root (1 ulp)
+    const float rs = p->qk_norm ? __builtin_amdgcn_rsqf(half_sum(s2) * (1.f / (float)D) + (float)p->rms_eps) : 1.f;
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       const int i = hl + 32 * j;
@@ -1135,7 +1137,7 @@ __device__ __forceinline__ bool phase_attn(const Ctx& c, int l) {
       s2 = fmaf(a[j], a[j], fmaf(b[j], b[j], s2));
     }
     float* dst = isq ? qs + r * d : kv + (size_t)pos * ps;
-    const float rs = p->qk_norm ? 1.f / sqrtf(half_sum(s2) / (float)d + p->rms_eps) : 1.f;
+    const float rs = p->qk_norm ? __builtin_amdgcn_rsqf(half_sum(s2) / (float)d + (float)p->rms_eps) : 1.f;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int i = hl + 32 * j;
