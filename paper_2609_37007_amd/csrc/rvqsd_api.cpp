@@ -315,7 +315,7 @@ int batch_setup(rvqsd_stream* s, int lanes, int tree_n = 0, const int32_t* paren
   // LDS: projection tiles and the SiLU staging, attention rows, sampling arrays, one row
   size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
   const size_t attn = tree_n ? ((size_t)rpl * k.d + (size_t)b.kv_slots * 2 * k.d + (size_t)kWaves * b.kv_slots) * 4
-                             : (size_t)(2 * kMaxRows + 2 * kMaxPos) * k.d * 4;
+                             : ((size_t)2 * kMaxRows * k.d + (size_t)kMaxPos * (2 * k.d + 4) + kMaxRows * kMaxPos) * 4;
   const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + 3 * kMaxTopk * 8 + kMaxTopk * 4 + kTopkBuckets * 4;
   if (attn > lds) lds = attn;
   if (samp > lds) lds = samp;

@@ -350,8 +350,10 @@ static_assert(gemm_red_floats<4, kProjNTW>() <= kBatchRedFloats && gemm_red_floa
 // ------------------------------------------------------------ projections
 
 // Y partial sums: part[ks][i][n] = sum over k in split ks of A[i][k] W[n][k], for every row i < M.
+// Inlined into the kernels: as out-of-line calls these two spill to scratch (the call ABI) and
+// their phases run 4-6 us slower.
 template <int NTU, typename BP, bool COH = false>
-__device__ void proj_partial(const BP* bp, const bf16_t* W, int N, int K, int KS, const uint32_t* A, float* red) {
+__device__ __forceinline__ void proj_partial(const BP* bp, const bf16_t* W, int N, int K, int KS, const uint32_t* A, float* red) {
   const int M = bp->M, mtiles = (M + 15) >> 4;
   const int cg = (N + 16 * NTU - 1) / (16 * NTU), units = cg * KS, klen = K / KS;
   float* part = bp->part;
@@ -380,7 +382,7 @@ __device__ void proj_partial(const BP* bp, const bf16_t* W, int N, int K, int KS
 // gate/up: n-tile 0 = gate rows f0 .. f0 + 15, n-tile 1 = the same up rows, full k;
 // act = SiLU(gate) * up goes straight to the split input of the down projection.
 template <typename BP, bool COH = false>
-__device__ void phase_gu(const BP* bp, int l, const uint32_t* A, uint32_t* Aout, float* red) {
+__device__ __forceinline__ void phase_gu(const BP* bp, int l, const uint32_t* A, uint32_t* Aout, float* red) {
   const KParams* p = bp->k;
   const int M = bp->M, mtiles = (M + 15) >> 4, H = p->H, F = p->F;
   const bf16_t* wg = bw(p, boff(p, l, p->o_wg));
@@ -541,7 +543,201 @@ __device__ void phase_attn_tree(const BParams* bp, BShared* sh, int l, uint32_t*
   }
 }
 
-__device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout, float* lds) {
+// phase_attn for a head dimension D known at compile time: K/V rows padded to 2D + 4 floats in
+// LDS (no bank conflicts between positions), norm + RoPE one half-wave per vector with DPP
+// sums, scores one wave per row with the 16 positions spread over the lanes (4 lanes each),
+// softmax with DPP, and the weighted value sum over position groups of 16-byte reads added in a
+// fixed order across the wave.
+template <int D>
+__device__ __forceinline__ void phase_attn_d(const BParams* bp, BShared* sh, int l, uint32_t* Aout, float* lds) {
+  const KParams* p = bp->k;
+  const int nq = p->nq, grp = nq / p->nkv, N = p->nqkv, KS = bp->ks_qkv, M = bp->M;
+  constexpr int half = D / 2, PS = 2 * D + 4;
+  const int qdim = p->qdim, kvdim = p->kvdim, lane = tid() & 63, wave = tid() >> 6;
+  const float scale = 1.f / sqrtf((float)D);
+  float* qs = lds;                          // [kMaxRows][D]
+  float* kvs = qs + kMaxRows * D;           // [kMaxPos][PS]: k, then v
+  float* os = kvs + kMaxPos * PS;           // [kMaxRows][D]
+  float* pwl = os + kMaxRows * D;           // [kMaxRows][kMaxPos] softmax weights
+  const float* qn = bfw(p, boff(p, l, p->o_qn));
+  const float* kn = bfw(p, boff(p, l, p->o_kn));
+  for (int u = blockIdx.x; u < bp->lanes * nq; u += bp->nwg) {
+    const int ln = u / nq, h = u - ln * nq, g = h / grp;
+    const int* st = sh->ln[ln];
+    if (!st[kLnActive]) continue;
+    const int fp = st[kLnFirst], R = st[kLnRows], row0 = ln * bp->rpl;
+    float* kvc = bp->kv + (((size_t)ln * p->L + l) * p->nkv + g) * bp->kv_slots * 2 * D;
+    // q, k, v of the lane's rows: the partial sums of 4 elements x 4 splits are in flight at once
+    const int tot = R * 3 * D;
+    for (int base = 0; base < tot; base += 4 * kThreads) {
+      const float* src[4];
+      float acc[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + k * kThreads + tid();
+        const int r = e / (3 * D), w = e - r * 3 * D, part = w / D, i = w - part * D;
+        const int col = part == 0 ? h * D + i : qdim + (part - 1) * kvdim + g * D + i;
+        src[k] = e < tot ? bp->part + (size_t)(row0 + r) * N + col : nullptr;
+        acc[k] = 0.f;
+      }
+      for (int ks0 = 0; ks0 < KS; ks0 += 4) {
+        float t[4][4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            t[k][j] = (src[k] && ks0 + j < KS) ? cldf(src[k] + (size_t)(ks0 + j) * M * N) : 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (ks0 + j < KS) acc[k] += t[k][j];
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + k * kThreads + tid();
+        if (e < tot) {
+          const int r = e / (3 * D), w = e - r * 3 * D, part = w / D, i = w - part * D;
+          if (part == 0) qs[r * D + i] = acc[k];
+          else kvs[(size_t)(fp + r) * PS + (part - 1) * D + i] = acc[k];
+        }
+      }
+    }
+    // committed positions 0 .. fp-1 from the lane's cache, eight loads in flight per thread
+    for (int b0 = 0; b0 < fp * 2 * D; b0 += 8 * kThreads) {
+      float v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int e = b0 + k * kThreads + tid();
+        v[k] = e < fp * 2 * D ? cldf(kvc + e) : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int e = b0 + k * kThreads + tid();
+        if (e < fp * 2 * D) kvs[(size_t)(e / (2 * D)) * PS + e % (2 * D)] = v[k];
+      }
+    }
+    __syncthreads();
+    // per-head RMSNorm + RoPE of q (vectors 0..R-1) and k (R..2R-1), one half-wave per vector;
+    // lane i of the half holds dimensions i + 32 j (j < D / 64) and their partners i + 32 j + D/2
+    constexpr int J = D / 64;
+    const int hl = lane & 31;
+    for (int v = 2 * wave + (lane >> 5); v < 2 * R; v += 2 * kWaves) {
+      const bool isq = v < R;
+      const int r = isq ? v : v - R, pos = fp + r;
+      float* x = isq ? qs + r * D : kvs + (size_t)pos * PS;
+      const float* gn = isq ? qn : kn;
+      float a[J], b[J], ga[J], gb[J], cs[J], sn[J];
+      float s2 = 0.f;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int i = hl + 32 * j;
+        a[j] = x[i];
+        b[j] = x[i + half];
+        ga[j] = G(gn)[i];
+        gb[j] = G(gn)[i + half];
+        cs[j] = G(p->rope)[(pos * half + i) * 2];
+        sn[j] = G(p->rope)[(pos * half + i) * 2 + 1];
+        s2 = fmaf(a[j], a[j], fmaf(b[j], b[j], s2));
+      }
+      const float rs = p->qk_norm ? __builtin_amdgcn_rsqf(half_sum(s2) * (1.f / (float)D) + (float)p->rms_eps) : 1.f;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int i = hl + 32 * j;
+        float ua = a[j], ub = b[j];
+        if (p->qk_norm) {
+          ua = ua * rs * ga[j];
+          ub = ub * rs * gb[j];
+        }
+        x[i] = ua * cs[j] - ub * sn[j];
+        x[i + half] = ub * cs[j] + ua * sn[j];
+      }
+    }
+    __syncthreads();
+    if (h % grp == 0)
+      for (int e = tid(); e < R * 2 * D; e += kThreads)
+        cstf(kvc + (size_t)fp * 2 * D + e, kvs[(size_t)(fp + e / (2 * D)) * PS + e % (2 * D)]);
+    // one wave per row. Scores: lane = (position t = lane / 4, quarter qj of the dimensions);
+    // values: lane = (position group gi, dimensions 4 li .. 4 li + 3)
+    const int npos = fp + R;
+    constexpr int DQ = D / 4, LPD = D / 4;
+    constexpr int NG = LPD >= 64 ? 1 : 64 / LPD;
+    constexpr int PPG = kMaxPos / NG;
+    const int t = lane >> 2, qj = lane & 3;
+    const int gi = lane / LPD, li = lane - gi * LPD;
+    for (int r = wave; r < R; r += kWaves) {
+      const int last = fp + r;  // causal: positions 0 .. last
+      float part = 0.f;
+      if (t <= last) {
+        const f32x4* qv = reinterpret_cast<const f32x4*>(qs + r * D + qj * DQ);
+        const f32x4* kk = reinterpret_cast<const f32x4*>(kvs + (size_t)t * PS + qj * DQ);
+        float p0 = 0.f, p1 = 0.f;
+#pragma unroll
+        for (int e = 0; e < DQ / 4; ++e) {
+          const f32x4 qa = qv[e], ka = kk[e];
+          p0 = fmaf(qa.x, ka.x, p0);
+          p1 = fmaf(qa.y, ka.y, p1);
+          p0 = fmaf(qa.z, ka.z, p0);
+          p1 = fmaf(qa.w, ka.w, p1);
+        }
+        part = p0 + p1;
+      }
+      part += dpp<0xB1>(part);  // quad sums: xor 1, xor 2
+      part += dpp<0x4E>(part);
+      const float sc = t <= last ? part * scale : -INFINITY;
+      const float rm = row16_max(sc);
+      const float mx = fmaxf(fmaxf(lane_val(rm, 15), lane_val(rm, 31)), fmaxf(lane_val(rm, 47), lane_val(rm, 63)));
+      const float ex = t <= last ? expf(sc - mx) : 0.f;
+      const float rsum = row16_sum(qj == 0 ? ex : 0.f);
+      const float z = (lane_val(rsum, 15) + lane_val(rsum, 31)) + (lane_val(rsum, 47) + lane_val(rsum, 63));
+      const float pr = ex / z;
+      // the row's weights go through LDS (written and read back by this wave only, in order);
+      // positions at or past npos read the finite row npos - 1 (weight 0) instead of unset rows
+      float* pwr = pwl + r * kMaxPos;
+      if (qj == 0) pwr[t] = pr;
+      f32x4 o = {0.f, 0.f, 0.f, 0.f};
+      if (gi < NG) {
+        f32x4 wq[PPG / 4];
+#pragma unroll
+        for (int q4 = 0; q4 < PPG / 4; ++q4) wq[q4] = reinterpret_cast<const f32x4*>(pwr + gi * PPG)[q4];
+        f32x4 vv[PPG];
+#pragma unroll
+        for (int k = 0; k < PPG; ++k)
+          vv[k] = *reinterpret_cast<const f32x4*>(kvs + (size_t)min(gi * PPG + k, npos - 1) * PS + D + 4 * li);
+#pragma unroll
+        for (int k = 0; k < PPG; ++k) {
+          const float w = wq[k >> 2][k & 3];
+          o.x = fmaf(w, vv[k].x, o.x);
+          o.y = fmaf(w, vv[k].y, o.y);
+          o.z = fmaf(w, vv[k].z, o.z);
+          o.w = fmaf(w, vv[k].w, o.w);
+        }
+      }
+      // groups added in a fixed order: (g0 + g1) + (g2 + g3)
+#pragma unroll
+      for (int xo = LPD; xo < 64 && NG > 1; xo <<= 1) {
+        o.x += __shfl_xor(o.x, xo, 64);
+        o.y += __shfl_xor(o.y, xo, 64);
+        o.z += __shfl_xor(o.z, xo, 64);
+        o.w += __shfl_xor(o.w, xo, 64);
+      }
+      if (gi == 0) *reinterpret_cast<f32x4*>(os + r * D + 4 * li) = o;
+    }
+    __syncthreads();
+    for (int c = tid(); c < R * (D / 8); c += kThreads) {
+      const int r = c / (D / 8), q8 = c - r * (D / 8);
+      float x8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x8[e] = os[r * D + 8 * q8 + e];
+      store_split(Aout + (size_t)(row0 + r) * qdim + h * D + 8 * q8, x8);
+    }
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout, float* lds) {
+  if (bp->k->d == 128) return phase_attn_d<128>(bp, sh, l, Aout, lds);
+  if (bp->k->d == 64) return phase_attn_d<64>(bp, sh, l, Aout, lds);
   const KParams* p = bp->k;
   const int d = p->d, nq = p->nq, grp = nq / p->nkv, N = p->nqkv, KS = bp->ks_qkv, M = bp->M, half = d / 2;
   const int qdim = p->qdim, kvdim = p->kvdim, lane = tid() & 63, wave = tid() >> 6;
@@ -665,7 +861,7 @@ __device__ void phase_attn(const BParams* bp, BShared* sh, int l, uint32_t* Aout
 // next input: RMSNorm(x) * gain split into Aout (mode 0), or the final norm
 // h and the LM-head inputs h + b_j of the row's used slots (mode 1).
 template <bool TR>
-__device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float* gain, uint32_t* Aout, int mode,
+__device__ __forceinline__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float* gain, uint32_t* Aout, int mode,
                             float* xs) {
   const KParams* p = bp->k;
   const int H = p->H, M = bp->M, K = p->K;
@@ -709,7 +905,7 @@ __device__ void phase_resid(const BParams* bp, BShared* sh, int KS, const float*
 // whose position plus offset is t, i.e. the verify rows at position t and the
 // draft rows of distance j from it.
 template <bool TR>
-__device__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
+__device__ __forceinline__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
   const KParams* p = bp->k;
   const int H = p->H, V = p->V, K = p->K, n = p->n_codes, rpl = bp->rpl;
   const int cg = (V + 63) / 64, ncand = bp->lanes * rpl * (K + 1);
@@ -805,7 +1001,7 @@ __device__ unsigned long long pass_bytes_batch(const BParams* bp, const BShared*
 // without a draft (prefix token, or the extra token after every draft was
 // accepted) -> sample p at u_samp. Verdict: token | accepted << 31.
 template <bool TR>
-__device__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, float* lds) {
+__device__ __forceinline__ void phase_sample(const BParams* bp, BShared* sh, const BCall& call, float* lds) {
   const KParams* p = bp->k;
   const int V = p->V, K = p->K, rpl = bp->rpl, n = p->n_codes, SW = bp->sup_words;
   float* lg = lds;                                            // [V]
@@ -1015,7 +1211,7 @@ __device__ __forceinline__ bool frame_inputs_ok(const BCall& call, int f, int V,
 }
 
 template <bool TR>
-__device__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, bool first, float* xs,
+__device__ __forceinline__ void lane_commit(const BParams* bp, BShared* sh, const BCall& call, bool first, float* xs,
                             uint32_t* A0) {
   const KParams* p = bp->k;
   const int lane_id = blockIdx.x, rpl = bp->rpl, K = p->K, n = p->n_codes, H = p->H;
