@@ -241,7 +241,13 @@ __device__ __forceinline__ bool head_slot_used(const BParams* bp, const KParams*
 // MFMA roles as in the frame kernel: A = 16 weight rows, B = 16 activation
 // rows; lane group q = lane / 16 covers the 16 consecutive k of a 64-wide step
 // in two instructions, and the activation chunk of 8 enters as bf16 hi + lo.
-template <int NTU, int NTW, bool COH = false, typename WRow, typename RowOf>
+// With STG (device-coherent operands, several n-tile groups) the activation
+// words of each step are copied once per workgroup into LDS (at red, before
+// the partial tiles are written there) and every wave reads its fragments from
+// LDS: the waves of different n-tile groups share one copy instead of each
+// reading it from the memory side. The k ranges of the waves, and so the
+// summation order, are the same with and without STG.
+template <int NTU, int NTW, bool COH = false, bool STG = false, typename WRow, typename RowOf>
 __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uint32_t* A, int lda, int mtiles,
                                           RowOf rowof, float* red) {
   constexpr int NG = NTU / NTW, KW = kWaves / NG;
@@ -265,6 +271,66 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
 #pragma unroll
     for (int mt = 0; mt < kBatchMTiles; ++mt) acc[t][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
   const int nsteps = kper >> 6;
+  if constexpr (STG) {
+    static_assert(COH && NG > 1, "staging serves coherent operands shared by n-tile groups");
+    // step u stages, for every k part kw, words kb(kw) + 64 u .. + 63 of each of the
+    // 16 mtiles rows: stg[row][kw * 64 + j], row stride KW * 64 + 4 words
+    constexpr int SW = KW * 64 + 4, NV = 16 * KW;  // row stride; 16-byte vectors per row
+    constexpr int SPT = (kBatchMTiles * 16 * NV + kThreads - 1) / kThreads;
+    static_assert(kBatchMTiles * 16 * SW <= kBatchRedFloats + kBatchMaxRows * 16, "staged rows fit the unit's LDS area");
+    uint32_t* stg = reinterpret_cast<uint32_t*>(red);
+    const int nvec = 16 * mtiles * NV;
+    const __amdgpu_buffer_rsrc_t ars = coh_rsrc(A);
+    for (int u = 0; u < nsteps; ++u) {
+      W16 a0[NTW], a1[NTW];
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) {
+        a0[t] = a1[t] = (W16)(0u);
+        if (wp[t]) {
+          a0[t] = *G(reinterpret_cast<const W16*>(wp[t] + 64 * u));
+          a1[t] = *G(reinterpret_cast<const W16*>(wp[t] + 64 * u + 8));
+        }
+      }
+      W16 sv[SPT];
+#pragma unroll
+      for (int i = 0; i < SPT; ++i) {
+        const int e = tid() + i * kThreads;
+        sv[i] = (W16)(0u);
+        if (e < nvec) {
+          const int row = e / NV, rem = e - row * NV, pk = rem >> 4, j4 = rem & 15;
+          const int ar = rowof(row);
+          if (ar >= 0) sv[i] = bload4(ars, (uint32_t)((size_t)ar * lda + (k0 + pk * kper + 64 * u + 4 * j4)) * 4u);
+        }
+      }
+      if (u > 0) __syncthreads();  // every wave is done with the previous step's copy
+#pragma unroll
+      for (int i = 0; i < SPT; ++i) {
+        const int e = tid() + i * kThreads;
+        if (e < nvec) {
+          const int row = e / NV, rem = e - row * NV;
+          *reinterpret_cast<W16*>(stg + row * SW + 4 * rem) = sv[i];
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) {
+        const bf16x8 x0 = __builtin_bit_cast(bf16x8, a0[t]), x1 = __builtin_bit_cast(bf16x8, a1[t]);
+#pragma unroll
+        for (int mt = 0; mt < kBatchMTiles; ++mt) {
+          if (mt < mtiles) {
+            const uint32_t* sp = stg + (16 * mt + ml) * SW + kw * 64 + 16 * q;
+            const W16 bh0 = *reinterpret_cast<const W16*>(sp), bl0 = *reinterpret_cast<const W16*>(sp + 4);
+            const W16 bh1 = *reinterpret_cast<const W16*>(sp + 8), bl1 = *reinterpret_cast<const W16*>(sp + 12);
+            acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bh0), acc[t][mt], 0, 0, 0);
+            acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bl0), acc[t][mt], 0, 0, 0);
+            acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bh1), acc[t][mt], 0, 0, 0);
+            acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bl1), acc[t][mt], 0, 0, 0);
+          }
+        }
+      }
+    }
+    __syncthreads();  // the staged copy is read before red receives the partial tiles
+  } else
   for (int u = 0; u < nsteps; ++u) {
     W16 a0[NTW], a1[NTW];
 #pragma unroll
@@ -344,7 +410,10 @@ constexpr int gemm_red_floats() {
   return kWaves / (NTU / NTW) * NTU * kBatchMTiles * 256;
 }
 constexpr int kProjNTW = 2, kGuNTW = 2;  // n-tiles per wave (activation fragments reused NTW times)
-static_assert(gemm_red_floats<4, kProjNTW>() <= kBatchRedFloats && gemm_red_floats<2, kGuNTW>() <= kBatchRedFloats,
+// LM-head units: 16 kHeadNTU columns, so that the 15 heads of the 1024-wide model take one unit per workgroup
+constexpr int kHeadNTU = 8;
+static_assert(gemm_red_floats<4, kProjNTW>() <= kBatchRedFloats && gemm_red_floats<2, kGuNTW>() <= kBatchRedFloats &&
+                  gemm_red_floats<kHeadNTU, kProjNTW>() <= kBatchRedFloats,
               "LDS reduction area");
 
 // ------------------------------------------------------------ projections
@@ -352,14 +421,14 @@ static_assert(gemm_red_floats<4, kProjNTW>() <= kBatchRedFloats && gemm_red_floa
 // Y partial sums: part[ks][i][n] = sum over k in split ks of A[i][k] W[n][k], for every row i < M.
 // Inlined into the kernels: as out-of-line calls these two spill to scratch (the call ABI) and
 // their phases run 4-6 us slower.
-template <int NTU, typename BP, bool COH = false>
+template <int NTU, typename BP, bool COH = false, bool STG = false>
 __device__ __forceinline__ void proj_partial(const BP* bp, const bf16_t* W, int N, int K, int KS, const uint32_t* A, float* red) {
   const int M = bp->M, mtiles = (M + 15) >> 4;
   const int cg = (N + 16 * NTU - 1) / (16 * NTU), units = cg * KS, klen = K / KS;
   float* part = bp->part;
   for (int u = blockIdx.x; u < units; u += bp->nwg) {
     const int g = u % cg, ks = u / cg, n0 = g * 16 * NTU;
-    gemm_unit<NTU, kProjNTW, COH>(
+    gemm_unit<NTU, kProjNTW, COH, STG>(
         [&](int nt, int m) -> const bf16_t* {
           const int f = n0 + 16 * nt + m;
           return f < N ? W + (size_t)f * K : nullptr;
@@ -908,7 +977,8 @@ template <bool TR>
 __device__ __forceinline__ void phase_heads(const BParams* bp, BShared* sh, float* red) {
   const KParams* p = bp->k;
   const int H = p->H, V = p->V, K = p->K, n = p->n_codes, rpl = bp->rpl;
-  const int cg = (V + 63) / 64, ncand = bp->lanes * rpl * (K + 1);
+  constexpr int NTU = TR ? 4 : kHeadNTU;  // the tree instantiation spills with the wider unit
+  const int cg = (V + 16 * NTU - 1) / (16 * NTU), ncand = bp->lanes * rpl * (K + 1);
   if (tid() == 0) sh->hl_t = -1;
   __syncthreads();
   for (int u = blockIdx.x; u < n * cg; u += bp->nwg) {
@@ -939,15 +1009,15 @@ __device__ __forceinline__ void phase_heads(const BParams* bp, BShared* sh, floa
     }
     const int nr = sh->hl_n;
     if (nr == 0) continue;
-    const int n0 = gi * 64;
+    const int n0 = gi * 16 * NTU;
     const bf16_t* W = bw(p, p->o_lmh1 + (uint64_t)(t - 1) * p->table_stride);
-    gemm_unit<4, kProjNTW, true>(
+    gemm_unit<NTU, kProjNTW, true, true>(
         [&](int nt, int m) -> const bf16_t* {
           const int f = n0 + 16 * nt + m;
           return f < V ? W + (size_t)f * H : nullptr;
         },
         0, H, bp->ah, H, (nr + 15) >> 4, [&](int i) { return i < nr ? sh->hl_row[i] : -1; }, red);
-    for (int e = tid(); e < 4 * ((nr + 15) >> 4) * 256; e += kThreads) {
+    for (int e = tid(); e < NTU * ((nr + 15) >> 4) * 256; e += kThreads) {
       const int mtiles = (nr + 15) >> 4;
       const int nt = e / (mtiles * 256), rem = e - nt * (mtiles * 256), mt = rem >> 8, x = rem & 255;
       const int ln = x >> 2, v = x & 3;
@@ -1555,14 +1625,14 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
     for (int i = 0; i < bp->lanes; ++i) any |= sh->ln[i][kLnActive];
     if (!any) break;
     for (int l = 0; l < L && ok; ++l) {
-      proj_partial<4, BParams, true>(bp, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, bp->ks_qkv, A0, dyn);
+      proj_partial<4, BParams, true, true>(bp, bw(p, boff(p, l, p->o_wq)), p->nqkv, H, bp->ks_qkv, A0, dyn);
       ok = grid_sync<BParams, false>(bp, gen, sh);
       if (ok) {
         if (TR) phase_attn_tree(bp, sh, l, A1, dyn);
         else phase_attn(bp, sh, l, A1, dyn);
       }
       ok = ok && grid_sync<BParams, false>(bp, gen, sh);
-      if (ok) proj_partial<4, BParams, true>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
+      if (ok) proj_partial<4, BParams, true, true>(bp, bw(p, boff(p, l, p->o_wo)), H, p->qdim, bp->ks_o, A1, dyn);
       ok = ok && grid_sync<BParams, false>(bp, gen, sh);
       if (ok) phase_resid<TR>(bp, sh, bp->ks_o, bfw(p, boff(p, l, p->o_mlp_norm)), A0, 0, dyn);
       if (ok && l == 0 && counter_wg && tid() < 64) {
@@ -1575,7 +1645,7 @@ __global__ void __launch_bounds__(kThreads, 1) batch_kernel(const BParams* __res
       ok = ok && grid_sync<BParams, false>(bp, gen, sh);
       if (ok) phase_gu<BParams, true>(bp, l, A0, A1, dyn);
       ok = ok && grid_sync<BParams, false>(bp, gen, sh);
-      if (ok) proj_partial<4, BParams, true>(bp, bw(p, boff(p, l, p->o_wd)), H, p->F, bp->ks_down, A1, dyn);
+      if (ok) proj_partial<4, BParams, true, true>(bp, bw(p, boff(p, l, p->o_wd)), H, p->F, bp->ks_down, A1, dyn);
       ok = ok && grid_sync<BParams, false>(bp, gen, sh);
       if (ok) {
         if (l + 1 < L) phase_resid<TR>(bp, sh, bp->ks_down, bfw(p, boff(p, l + 1, p->o_attn_norm)), A0, 0, dyn);

@@ -172,10 +172,6 @@ __device__ __forceinline__ double wave_scan_incld(double v) {
 // 16 bytes of weights (a builtin vector type, so address-space qualified loads copy it)
 typedef uint32_t W16 __attribute__((ext_vector_type(4)));
 
-// Four activation words through one device-coherent 16-byte load. The load is
-// issued here and completes at vm_wait, which names the result as an operand so
-// that no use of it is scheduled before the wait; several loads issued back to
-// back are in flight together. Each 32-bit word is written atomically by its
 // Four parity words through one device-coherent 16-byte vector store (p 16-byte aligned): each
 // word's lowest mantissa bit carries the parity; a reader checks every word on its own.
 __device__ __forceinline__ void pstore4(uint32_t* p, float a, float b, float c, float d, uint32_t par) {
@@ -186,6 +182,10 @@ __device__ __forceinline__ void pstore4(uint32_t* p, float a, float b, float c, 
   w[3] = (__float_as_uint(d) & ~1u) | par;
   asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(w) : "memory");
 }
+// Four activation words through one device-coherent 16-byte load. The load is
+// issued here and completes at vm_wait, which names the result as an operand so
+// that no use of it is scheduled before the wait; several loads issued back to
+// back are in flight together. Each 32-bit word is written atomically by its
 // producer, so every word's parity bit is checked on its own.
 __device__ __forceinline__ W16 pload4(const uint32_t* p) {
   W16 r;
@@ -193,6 +193,18 @@ __device__ __forceinline__ W16 pload4(const uint32_t* p) {
   return r;
 }
 __device__ __forceinline__ void vm_wait(W16& r) { asm volatile("s_waitcnt vmcnt(0)" : "+v"(r)::"memory"); }
+// The same device-coherent 16-byte load as a raw buffer load with cache policy
+// sc1 (resource of the given base, 32-bit data format, no stride or range limit).
+// The compiler tracks it like any load and waits for it where the result is used,
+// so it needs no vm_wait and is safe where register pressure makes the compiler
+// copy registers between an inline-assembly load and its wait. Not for polling:
+// a loop that re-reads one address must also clobber memory between the reads.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coh_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ W16 bload4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 16);
+}
 
 // Sum over the 32 lanes of each half of the wave (every lane gets its half's sum).
 __device__ __forceinline__ float half_sum(float v) {
