@@ -1095,15 +1095,17 @@ __device__ __forceinline__ void phase_sample(const BParams* bp, BShared* sh, con
     const bool has_draft = !TR && j == 0 && pass > 0 && r + 1 <= st[kLnKp];
     int nq = 0, dtok = -1;
     if (has_draft) {
-      // q of d_t: drafted last pass from the anchor's row, offset r + 1
+      // q of d_t: drafted last pass from the anchor's row, offset r + 1; the whole support
+      // area (topk entries, of which the first nq are this record's) is read together with
+      // the header and the logits instead of after the header
       const uint64_t* rec = bp->drec + ((((size_t)((pass - 1) & 1) * bp->lanes + ln) * rpl + st[kLnPrevAnchor]) * K + r) * SW;
       const uint64_t w0 = cld64(rec);
-      dtok = (int)(uint32_t)w0;
-      nq = (int)(w0 >> 32);
-      for (int i = tid(); i < nq; i += kThreads) {
+      for (int i = tid(); i < p->topk; i += kThreads) {
         qidx[i] = (int)(uint32_t)cld64(rec + 1 + i);
         qprob[i] = __longlong_as_double((long long)cld64(rec + 1 + p->topk + i));
       }
+      dtok = (int)(uint32_t)w0;
+      nq = (int)(w0 >> 32);
     }
     const float* src = bp->logits + (size_t)u * V;
     lds_fill<true>(lg, src, V, V, 0);
@@ -1287,13 +1289,26 @@ __device__ __forceinline__ void lane_commit(const BParams* bp, BShared* sh, cons
   const int lane_id = blockIdx.x, rpl = bp->rpl, K = p->K, n = p->n_codes, H = p->H;
   int* st = sh->ln[lane_id];
   int* gst = bp->lane + (size_t)lane_id * kLaneInts;
+  // st already holds this lane's state: every workgroup loads all lane states at the start of a
+  // pass, and only this workgroup writes them
+  const int f_next = (first ? lane_id - bp->lanes : st[kLnFrame]) + bp->lanes;
   if (first) {
     for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = 0;
     if (tid() == 0) st[kLnFrame] = lane_id - bp->lanes;
-  } else {
-    for (int i = tid(); i < kLaneInts; i += kThreads) st[i] = (int)cld32(gst + i);
   }
-  __syncthreads();
+  // inputs of the lane's next frame (c0 and its uniforms), checked by many threads now
+  // rather than by one when the frame starts
+  int c0_next = -1, bad_next = 0;
+  if (f_next < call.n && tid() <= 3 * n) {
+    if (tid() == 0) {
+      c0_next = call.c0[f_next];
+      bad_next = c0_next < 0 || c0_next >= p->V;
+    } else {
+      const float u = call.uniforms[(size_t)f_next * n * 3 + tid() - 1];
+      bad_next = !(u >= 0.f && u < 1.f);
+    }
+  }
+  const bool next_ok = !__syncthreads_or(bad_next);
   const bool was_active = !first && st[kLnActive];
   const bool tree_pass = was_active && tree_rows<TR>(bp, st);
   if (was_active) {
@@ -1491,12 +1506,15 @@ __device__ __forceinline__ void lane_commit(const BParams* bp, BShared* sh, cons
     if (start) {
       // the lane's next frame with a valid c0
       int f = st[kLnFrame] + bp->lanes;
-      while (f < call.n && !frame_inputs_ok(call, f, p->V, n)) {
+      bool f_ok = next_ok;  // f == f_next
+      while (f < call.n && !f_ok) {
         rvqsd_stats o = {};
         o.status = RVQSD_EINVAL;
         call.out_stats[f] = o;
         for (int s = 0; s < n; ++s) call.out_codes[(size_t)f * n + s] = -1;
         f += bp->lanes;
+        f_ok = f < call.n && frame_inputs_ok(call, f, p->V, n);
+        if (f < call.n) c0_next = call.c0[f];
       }
       for (int i = 0; i < kLaneInts; ++i) st[i] = 0;
       st[kLnFrame] = f;
@@ -1504,8 +1522,8 @@ __device__ __forceinline__ void lane_commit(const BParams* bp, BShared* sh, cons
         const uint64_t now = dclock();
         st[kLnActive] = 1;
         st[kLnRows] = 2;
-        st[kLnCodes] = call.c0[f];
-        st[kLnInCode + 1] = call.c0[f];
+        st[kLnCodes] = c0_next;
+        st[kLnInCode + 1] = c0_next;
         st[kLnClkLo] = (int)(uint32_t)now;
         st[kLnClkHi] = (int)(uint32_t)(now >> 32);
       }
