@@ -89,7 +89,10 @@ typedef struct {
   uint32_t accept_mask; /* bit s set when the draft at code position s was accepted */
   int32_t status;       /* device-side status of this frame (RVQSD_OK or an error) */
   uint64_t weight_bytes;/* algorithmic bytes the frame's passes must read (weights + gathered rows + KV) */
-  uint64_t clk_start, clk_end; /* device constant clock (100 MHz) at kernel start / end */
+  uint64_t clk_start, clk_end; /* device constant clock (100 MHz) at kernel start / end: the frame's
+                                * device time in microseconds is (clk_end - clk_start) / 100; every
+                                * pass of the frame, the prefix pass included, is a verification pass,
+                                * so this is also its verification time */
 } rvqsd_stats;
 
 /* Optional per-round trace (device buffers, caller-owned). Any pointer may be NULL.
