@@ -428,12 +428,14 @@ __device__ __forceinline__ void proj_partial(const BP* bp, const bf16_t* W, int 
   float* part = bp->part;
   for (int u = blockIdx.x; u < units; u += bp->nwg) {
     const int g = u % cg, ks = u / cg, n0 = g * 16 * NTU;
-    gemm_unit<NTU, kProjNTW, COH, STG>(
-        [&](int nt, int m) -> const bf16_t* {
-          const int f = n0 + 16 * nt + m;
-          return f < N ? W + (size_t)f * K : nullptr;
-        },
-        ks * klen, klen, A, K, mtiles, [&](int i) { return i < M ? i : -1; }, red);
+    auto wrow = [&](int nt, int m) -> const bf16_t* {
+      const int f = n0 + 16 * nt + m;
+      return f < N ? W + (size_t)f * K : nullptr;
+    };
+    auto rowof = [&](int i) { return i < M ? i : -1; };
+    // staging pays from two row tiles on; with one the waves read their fragments directly
+    if (STG && mtiles >= 2) gemm_unit<NTU, kProjNTW, COH, STG>(wrow, ks * klen, klen, A, K, mtiles, rowof, red);
+    else gemm_unit<NTU, kProjNTW, COH, false>(wrow, ks * klen, klen, A, K, mtiles, rowof, red);
     for (int e = tid(); e < NTU * mtiles * 64; e += kThreads) {
       const int nt = e / (mtiles * 64), rem = e - nt * (mtiles * 64), mt = rem >> 6, ln = rem & 63;
       const int row = 16 * mt + (ln & 15), f = n0 + 16 * nt + 4 * (ln >> 4);
