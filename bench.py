@@ -334,7 +334,7 @@ def run_pipeline(a) -> int:
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": None,
-            "kernel": "outer_kernel + frame_kernel",
+            "kernel": "outer_flow_kernel + frame_kernel",
             "algorithmic_bytes_per_frame": round(total_b / N, 1),
         },
         "cpu_baseline": cpu,

@@ -112,6 +112,8 @@ struct rvqsd_outer {
   size_t lds;
   int pos;              // frames decoded since the last reset
   int n_tables;
+  uint32_t epoch;       // launches so far (tags the exchange words of the step without grid barriers)
+  int flow_steps;       // > 0: the step without grid barriers, its units' k steps per wave
 };
 
 namespace {
@@ -869,6 +871,27 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
   b.topk = topk;
   b.temperature = temperature;
   const size_t kmax = (size_t)(k.H > k.qdim ? (k.H > k.F ? k.H : k.F) : (k.qdim > k.F ? k.qdim : k.F));
+  // the step without grid barriers: units of 16 rows over the whole k range or a k split that is a
+  // multiple of 512 (eight waves of 64-wide steps)
+  auto split512 = [](int K, int most) {
+    for (int ks = most; ks >= 1; --ks)
+      if (K % (ks * 512) == 0) return ks;
+    return 0;
+  };
+  b.ks_o2 = split512(k.qdim, kOutOSplit);
+  b.ks_d2 = split512(k.F, kOutDSplit);
+  // its poll staging (the partial sums, a k range) stays below the split input row in LDS, and a
+  // unit's weights fit in registers (at most kFlowSteps 64-wide k steps per wave)
+  const int stage = kBatchRedFloats + kBatchMaxRows * 16;
+  int flow_steps = 0;
+  if (k.H % 512 == 0 && b.ks_o2 > 0 && b.ks_d2 > 0 && k.nqkv % 16 == 0 && kOutOSplit * k.H <= stage &&
+      k.qdim / b.ks_o2 <= stage && k.F / b.ks_d2 <= stage) {
+    int kr = k.H;
+    if (k.qdim / b.ks_o2 > kr) kr = k.qdim / b.ks_o2;
+    if (k.F / b.ks_d2 > kr) kr = k.F / b.ks_d2;
+    if (kr <= kFlowSteps * 512) flow_steps = kr / 512;
+  }
+  const bool flow = flow_steps > 0;
   size_t part = (size_t)b.ks_qkv * k.nqkv;
   if ((size_t)b.ks_o * k.H > part) part = (size_t)b.ks_o * k.H;
   if ((size_t)b.ks_down * k.H > part) part = (size_t)b.ks_down * k.H;
@@ -887,6 +910,17 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
                o_apart = take((size_t)k.nq * kAttnMaxChunks * (k.d + 2) * 4), o_log = take((size_t)k.V * 4),
                o_last = take((size_t)(1 + kMaxCodes) * 4), o_f = take((size_t)k.H * 4), o_op = take(sizeof(OParams)),
                o_kp = take(sizeof(KParams));
+  size_t o_tq = 0, o_tch = 0, o_tat = 0, o_top = 0, o_tact = 0, o_tdp = 0, o_tlog = 0;
+  if (flow) {
+    // tagged exchange words, one set per layer
+    o_tq = take((size_t)k.L * k.nqkv * 8);
+    o_tch = take((size_t)k.L * k.nq * kAttnMaxChunks * (k.d + 2) * 8);
+    o_tat = take((size_t)k.L * k.qdim * 8);
+    o_top = take((size_t)k.L * kOutOSplit * k.H * 8);
+    o_tact = take((size_t)k.L * k.F * 8);
+    o_tdp = take((size_t)k.L * kOutDSplit * k.H * 8);
+    o_tlog = take((size_t)k.V * 8);
+  }
   hipError_t e = dev_alloc(&o->buf, off);
   if (e != hipSuccess) {
     delete o;
@@ -904,10 +938,41 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
   b.kv = (float*)(base + o_kv);
   b.apart = (float*)(base + o_apart);
   b.logits = (float*)(base + o_log);
+  if (flow) {
+    b.tq = (uint64_t*)(base + o_tq);
+    b.tch = (uint64_t*)(base + o_tch);
+    b.tat = (uint64_t*)(base + o_tat);
+    b.top = (uint64_t*)(base + o_top);
+    b.tact = (uint64_t*)(base + o_tact);
+    b.tdp = (uint64_t*)(base + o_tdp);
+    b.tlog = (uint64_t*)(base + o_tlog);
+  }
   o->last_codes = (int32_t*)(base + o_last);
   o->f = (float*)(base + o_f);
   o->dop = (OParams*)(base + o_op);
   o->dkp = (KParams*)(base + o_kp);
+  size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
+  const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + kMaxTopk * 8 + kTopkBuckets * 4;
+  // attention: q, k, v, scores, group sums, then the chunk's keys and values (16-byte aligned)
+  const size_t chunk = (size_t)attn_chunk_len(max_frames, k.d), G = (size_t)(kThreads / k.d);
+  const size_t attn = (((3 * (size_t)k.d + chunk + G * k.d + G + 3) & ~(size_t)3) + chunk * 2 * k.d) * 4;
+  // merge: the chunk partials of one head, the chunk weights and the merged output
+  const size_t merge = ((size_t)kAttnMaxChunks * (k.d + 2) + kAttnMaxChunks + k.d) * 4;
+  if (samp > lds) lds = samp;
+  if (attn > lds) lds = attn;
+  if (merge > lds) lds = merge;
+  if ((size_t)k.H * 4 > lds) lds = (size_t)k.H * 4;
+  if (flow) {
+    // the step without barriers also keeps its split input row after the unit area and the
+    // residual row after everything else
+    size_t need = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16 + kmax) * 4;
+    if ((size_t)kOutOSplit * k.H * 4 > need) need = (size_t)kOutOSplit * k.H * 4;
+    if (lds > need) need = lds;
+    need = (need + 15) / 16 * 16;
+    b.xoff = (int32_t)(need / 4);
+    lds = need + (size_t)k.H * 4;
+  }
+  o->flow_steps = flow_steps;
   o->op = b;
   o->sync_bytes = sync_bytes;
   e = hipMemset(o->buf, 0, off);
@@ -933,17 +998,6 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
     delete o;
     return set_err(RVQSD_EHIP, "outer-step set-up: %s", hipGetErrorString(e));
   }
-  size_t lds = ((size_t)kBatchRedFloats + (size_t)kBatchMaxRows * 16) * 4;
-  const size_t samp = ((size_t)k.V + 2 * kMaxTopk) * 4 + 8 + kMaxTopk * 8 + kTopkBuckets * 4;
-  // attention: q, k, v, scores, group sums, then the chunk's keys and values (16-byte aligned)
-  const size_t chunk = (size_t)attn_chunk_len(max_frames, k.d), G = (size_t)(kThreads / k.d);
-  const size_t attn = (((3 * (size_t)k.d + chunk + G * k.d + G + 3) & ~(size_t)3) + chunk * 2 * k.d) * 4;
-  // merge: the chunk partials of one head, the chunk weights and the merged output
-  const size_t merge = ((size_t)kAttnMaxChunks * (k.d + 2) + kAttnMaxChunks + k.d) * 4;
-  if (samp > lds) lds = samp;
-  if (attn > lds) lds = attn;
-  if (merge > lds) lds = merge;
-  if ((size_t)k.H * 4 > lds) lds = (size_t)k.H * 4;
   o->lds = lds + 64;
   *out = o;
   return RVQSD_OK;
@@ -989,8 +1043,9 @@ rvqsd_status rvqsd_pipeline_frames_async(rvqsd_stream* s, rvqsd_outer* o, int32_
     c.c0_out = d_codes + (size_t)i * (1 + nc);
     c.hidden_out = fbuf ? fbuf + (size_t)i * H : o->f;
     c.pos = o->pos;
+    c.epoch = ++o->epoch;
     char err[256];
-    int st = launch_outer(o->dop, c, o->m->nwg, (void*)s->stream, o->lds, err, sizeof(err));
+    int st = launch_outer(o->dop, c, o->m->nwg, (void*)s->stream, o->lds, o->flow_steps, err, sizeof(err));
     if (st) return set_err(st, "%s", err);
     st = launch_one(s, c.hidden_out, c.c0_out, d_uniforms + (size_t)i * nc * 3, c.c0_out + 1, d_stats + i);
     if (st) return st;

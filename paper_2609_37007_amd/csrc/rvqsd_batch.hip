@@ -247,7 +247,8 @@ __device__ __forceinline__ bool head_slot_used(const BParams* bp, const KParams*
 // LDS: the waves of different n-tile groups share one copy instead of each
 // reading it from the memory side. The k ranges of the waves, and so the
 // summation order, are the same with and without STG.
-template <int NTU, int NTW, bool COH = false, bool STG = false, typename WRow, typename RowOf>
+// With ALDS, A is a split row block in LDS that the caller filled.
+template <int NTU, int NTW, bool COH = false, bool STG = false, bool ALDS = false, typename WRow, typename RowOf>
 __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uint32_t* A, int lda, int mtiles,
                                           RowOf rowof, float* red) {
   constexpr int NG = NTU / NTW, KW = kWaves / NG;
@@ -348,7 +349,12 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
       bh0[mt] = bl0[mt] = bh1[mt] = bl1[mt] = (W16)(0u);
       if (mt < mtiles && arow[mt] >= 0) {
         const uint32_t* ap = A + (size_t)arow[mt] * lda + (size_t)chunk * 8;
-        if constexpr (COH) {
+        if constexpr (ALDS) {
+          bh0[mt] = *reinterpret_cast<const W16*>(ap);
+          bl0[mt] = *reinterpret_cast<const W16*>(ap + 4);
+          bh1[mt] = *reinterpret_cast<const W16*>(ap + 8);
+          bl1[mt] = *reinterpret_cast<const W16*>(ap + 12);
+        } else if constexpr (COH) {
           bh0[mt] = pload4(ap);
           bl0[mt] = pload4(ap + 4);
           bh1[mt] = pload4(ap + 8);
@@ -361,7 +367,7 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
         }
       }
     }
-    if constexpr (COH) {
+    if constexpr (COH && !ALDS) {
       // the device-coherent loads are issued from inline assembly: wait for them explicitly
 #pragma unroll
       for (int mt = 0; mt < kBatchMTiles; ++mt) {
@@ -2010,6 +2016,484 @@ __global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __res
   if (!ok && blockIdx.x == 0 && tid() == 0) call.c0_out[0] = -1;
 }
 
+// ------------------------------------------------------------ outer step without grid barriers
+// The same step as outer_kernel, with every value one workgroup hands to another carried by a
+// 64-bit word whose upper half is a tag unique to (launch, layer, kind): a reader polls the
+// words until its tag appears, so no grid barrier separates the phases. Every layer has words of
+// its own, so no word is written twice in one launch and a reader that falls behind still finds
+// its tag; the next launch on the stream starts after this one has ended. With one row, every
+// workgroup keeps the whole residual row in LDS and adds the O and down partial sums to it
+// itself, in split order, so all copies are equal.
+
+constexpr int kTagQKV = 0, kTagChunk = 1, kTagMerge = 2, kTagO = 3, kTagAct = 4, kTagDown = 5;
+__device__ __forceinline__ uint32_t otag(const OCall& call, int l, int kind) {
+  return (call.epoch << 10) | (uint32_t)(8 * l + kind);
+}
+__device__ __forceinline__ void tstore(uint64_t* p, uint32_t tag, float v) {
+  cst64(p, ((uint64_t)tag << 32) | __float_as_uint(v));
+}
+
+// n tagged words: sink(i, payload) once word addr(i) carries tag. Thread t takes words t, t + 512,
+// ...; up to eight loads in flight each. False for every thread when a wait ran out (2 s) or
+// another workgroup raised the status.
+template <typename Addr, typename Sink>
+__device__ bool opoll(const OParams* op, int n, uint32_t tag, Addr addr, Sink sink) {
+  constexpr int B = 8;
+  int bad = 0;
+  for (int base = 0; base < n && !bad; base += B * kThreads) {
+    uint32_t pend = 0;
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+      if (base + b * kThreads + tid() < n) pend |= 1u << b;
+    uint64_t t0 = 0;
+    int spins = 0;
+    while (pend) {
+      uint64_t v[B];
+#pragma unroll
+      for (int b = 0; b < B; ++b) v[b] = (pend >> b) & 1u ? cld64(addr(base + b * kThreads + tid())) : 0ull;
+#pragma unroll
+      for (int b = 0; b < B; ++b)
+        if (((pend >> b) & 1u) && (uint32_t)(v[b] >> 32) == tag) {
+          sink(base + b * kThreads + tid(), (uint32_t)v[b]);
+          pend &= ~(1u << b);
+        }
+      if (!pend) break;
+      if ((++spins & 31) == 0) {
+        const uint64_t now = dclock();
+        if (t0 == 0) {
+          t0 = now;
+        } else if (now - t0 > kTimeoutTicks) {
+          raise_status(op, RVQSD_ETIMEOUT);
+          bad = 1;
+          break;
+        }
+        if (cld32(op->status) != 0) {
+          bad = 1;
+          break;
+        }
+      }
+    }
+  }
+  return !__syncthreads_or(bad);
+}
+
+// x (LDS, [H]) normalised with gain, split into the LDS row a (its words k0 .. k0 + n - 1 of the
+// row are written for k in [k0, k0 + n), the whole row when n = H); hidden_out (workgroup 0)
+// receives the normalised values
+__device__ void norm_split(const OParams* op, BShared* sh, const float* x, const float* gain, uint32_t* a,
+                           float* hidden_out) {
+  const KParams* p = op->k;
+  const int H = p->H;
+  float ss = 0.f;
+  for (int e = tid(); e < H; e += kThreads) ss = fmaf(x[e], x[e], ss);
+  ss = block_sum(sh, ss);
+  const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
+  for (int c = tid(); c < H / 8; c += kThreads) {
+    float h8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h8[e] = x[8 * c + e] * rs * G(gain)[8 * c + e];
+    W16 hi, lo;
+    split8(h8, hi, lo);
+    *reinterpret_cast<W16*>(a + 8 * c) = hi;
+    *reinterpret_cast<W16*>(a + 8 * c + 4) = lo;
+    if (hidden_out && blockIdx.x == 0)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) hidden_out[8 * c + e] = h8[e];
+  }
+  __syncthreads();
+}
+
+// x += the ns partial sums P[k][H] (tagged), in split order
+__device__ bool fold_parts(const OParams* op, const uint64_t* P, int ns, uint32_t tag, float* x, float* tmp) {
+  const int H = op->k->H;
+  const bool ok = opoll(op, ns * H, tag, [=](int i) { return P + i; }, [&](int i, uint32_t v) { tmp[i] = __uint_as_float(v); });
+  if (!ok) return false;
+  for (int e = tid(); e < H; e += kThreads) {
+    float s2 = tmp[e];
+    for (int k = 1; k < ns; ++k) s2 += tmp[(size_t)k * H + e];
+    x[e] = x[e] + s2;
+  }
+  __syncthreads();
+  return true;
+}
+
+// n tagged words from T into the split LDS row a at words k0 .. k0 + n - 1 (n a multiple of 8)
+__device__ bool fill_split(const OParams* op, const uint64_t* T, int k0, int n, uint32_t tag, uint32_t* a, float* tmp) {
+  const bool ok = opoll(op, n, tag, [=](int i) { return T + k0 + i; }, [&](int i, uint32_t v) { tmp[i] = __uint_as_float(v); });
+  if (!ok) return false;
+  for (int c = tid(); c < n / 8; c += kThreads) {
+    float x8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x8[e] = tmp[8 * c + e];
+    W16 hi, lo;
+    split8(x8, hi, lo);
+    *reinterpret_cast<W16*>(a + k0 + 8 * c) = hi;
+    *reinterpret_cast<W16*>(a + k0 + 8 * c + 4) = lo;
+  }
+  __syncthreads();
+  return true;
+}
+
+// A unit whose weight fragments are loaded into registers before its input row is ready, so the
+// load overlaps the wait: NT n-tiles of 16 rows, k in [k0, k0 + klen) split over the eight waves
+// in 64-wide steps (at most NS per wave).
+template <int NT, int NS>
+struct WPre {
+  W16 a0[NT][NS], a1[NT][NS];
+};
+template <int NT, int NS, typename WRow>
+__device__ __forceinline__ void wfetch(WPre<NT, NS>& w, WRow wrow, int k0, int klen) {
+  const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6), lane = tid() & 63;
+  const int q = lane >> 4, ml = lane & 15;
+  const int kper = klen / kWaves, kb = k0 + wave * kper, nsteps = kper >> 6;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const bf16_t* wr = wrow(t, ml);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      w.a0[t][s] = w.a1[t][s] = (W16)(0u);
+      if (wr && s < nsteps) {
+        w.a0[t][s] = *G(reinterpret_cast<const W16*>(wr + kb + 16 * q + 64 * s));
+        w.a1[t][s] = *G(reinterpret_cast<const W16*>(wr + kb + 16 * q + 64 * s + 8));
+      }
+    }
+  }
+}
+// the unit's NT x 16 outputs for the one row held split in LDS (a, words k0 .. k0 + klen - 1):
+// out(f, s) with s[t] the output of n-tile t, row f; the wave partials are added in wave order
+template <int NT, int NS, typename Out>
+__device__ __forceinline__ void wdot(const WPre<NT, NS>& w, int k0, int klen, const uint32_t* a, float* red, Out out) {
+  const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6), lane = tid() & 63;
+  const int q = lane >> 4, ml = lane & 15;
+  const int kper = klen / kWaves, kb = k0 + wave * kper, nsteps = kper >> 6;
+  f32x4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    if (s < nsteps) {
+      W16 bh0 = (W16)(0u), bl0 = bh0, bh1 = bh0, bl1 = bh0;
+      if (ml == 0) {  // activation column 0 is the row; the other 15 stay zero
+        const uint32_t* ap = a + kb + 64 * s + 16 * q;
+        bh0 = *reinterpret_cast<const W16*>(ap);
+        bl0 = *reinterpret_cast<const W16*>(ap + 4);
+        bh1 = *reinterpret_cast<const W16*>(ap + 8);
+        bl1 = *reinterpret_cast<const W16*>(ap + 12);
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const bf16x8 x0 = __builtin_bit_cast(bf16x8, w.a0[t][s]), x1 = __builtin_bit_cast(bf16x8, w.a1[t][s]);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bh0), acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, __builtin_bit_cast(bf16x8, bl0), acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bh1), acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, __builtin_bit_cast(bf16x8, bl1), acc[t], 0, 0, 0);
+      }
+    }
+  }
+  // output row 4 q + v of n-tile t sits in lane 16 q, element v
+  if (ml == 0)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) red[(wave * NT + t) * 16 + 4 * q + v] = acc[t][v];
+  __syncthreads();
+  if (tid() < 16) {
+    float sum[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      sum[t] = red[t * 16 + tid()];
+      for (int wv = 1; wv < kWaves; ++wv) sum[t] += red[(wv * NT + t) * 16 + tid()];
+    }
+    out(tid(), sum);
+  }
+  __syncthreads();
+}
+
+template <int NS>
+__global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* __restrict__ opp, OCall call) {
+  __shared__ BShared shs;
+  extern __shared__ __align__(16) float dyn[];
+  const OParams* op = opp;
+  const KParams* p = op->k;
+  BShared* sh = &shs;
+  const int L = p->L, H = p->H, d = p->d, N = p->nqkv, qd = p->qdim, F = p->F, nq = p->nq;
+  float* red = dyn;                                                      // unit partial tiles
+  uint32_t* arow = reinterpret_cast<uint32_t*>(dyn + kBatchRedFloats + kBatchMaxRows * 16);  // split input row
+  float* xr = dyn + op->xoff;                                            // the residual row [H]
+  float* tmp = dyn;  // poll staging (before a unit runs, or in phases without units)
+  const int pos = call.pos, np = pos + 1, ch = attn_chunk_len(np, d), nch = (np + ch - 1) / ch;
+  bool ok = true;
+  // x_0 = t + E_0[c_0] + sum_j E_j[c_j] of the previous frame, built by every workgroup
+  {
+    __shared__ int pcodes[kMaxCodes + 1];
+    __shared__ int pbad;
+    const int nt = op->n_tables;
+    if (tid() == 0) pbad = 0;
+    __syncthreads();
+    if (call.prev_codes && tid() <= nt) {
+      const int c = G(call.prev_codes)[tid()];
+      pcodes[tid()] = c;
+      if (!(c >= 0 && c < (tid() == 0 ? min(p->V, op->table_vocab) : op->table_vocab))) pbad = 1;
+    }
+    __syncthreads();
+    const bool codes_ok = call.prev_codes != nullptr && pbad == 0;
+    if (call.prev_codes && !codes_ok && tid() == 0 && blockIdx.x == 0) raise_status(op, RVQSD_EINVAL);
+    for (int e = tid(); e < H; e += kThreads) {
+      float v = G(call.t)[e];
+      if (codes_ok) {
+        const bf16_t* e0 = bw(p, p->o_emb0);
+        uint32_t tv[kMaxCodes + 1];
+        tv[0] = G(e0)[(size_t)pcodes[0] * H + e];
+#pragma unroll
+        for (int j = 1; j <= kMaxCodes; ++j)
+          tv[j] = j <= nt ? G(op->tables)[((size_t)(j - 1) * op->table_vocab + pcodes[j]) * H + e] : 0u;
+        v += __uint_as_float(tv[0] << 16);
+#pragma unroll
+        for (int j = 1; j <= kMaxCodes; ++j)
+          if (j <= nt) v += __uint_as_float(tv[j] << 16);
+      }
+      xr[e] = v;
+    }
+    __syncthreads();
+  }
+  const int grp = nq / p->nkv, half = d / 2;
+  const int nwg = op->nwg, me = blockIdx.x;
+  const int nuq = (N + 15) / 16, cg = H / 16, nuo = cg * op->ks_o2, nud = cg * op->ks_d2;
+  const int klo = qd / op->ks_o2, kld = F / op->ks_d2;
+  WPre<1, NS> w1;  // QKV, O and down units
+  WPre<2, NS> w2;  // gate/up units
+  for (int l = 0; l < L && ok; ++l) {
+    const size_t b = (size_t)l;  // this layer's exchange words
+    // ---- QKV: the residual row after layer l - 1, normalised; 16 output columns per unit
+    const bf16_t* Wq = bw(p, boff(p, l, p->o_wq));  // q, k, v rows are consecutive in the blob
+    auto qrows = [=](int u) {
+      return [=](int, int m) -> const bf16_t* { return u * 16 + m < N ? Wq + (size_t)(u * 16 + m) * H : nullptr; };
+    };
+    if (me < nuq) wfetch(w1, qrows(me), 0, H);
+    if (l > 0) ok = fold_parts(op, op->tdp + (b - 1) * kOutDSplit * H, op->ks_d2, otag(call, l - 1, kTagDown), xr, tmp);
+    if (!ok) break;
+    norm_split(op, sh, xr, bfw(p, boff(p, l, p->o_attn_norm)), arow, nullptr);
+    {
+      const uint32_t tg = otag(call, l, kTagQKV);
+      for (int u = me; u < nuq; u += nwg) {
+        if (u != me) wfetch(w1, qrows(u), 0, H);
+        wdot(w1, 0, H, arow, red, [&](int f, const float* v) { if (u * 16 + f < N) tstore(op->tq + b * N + u * 16 + f, tg, v[0]); });
+      }
+    }
+    // the first O unit's weights, loaded during attention
+    const bf16_t* Wo = bw(p, boff(p, l, p->o_wo));
+    auto orows = [=](int u) {
+      const int g = u % cg;
+      return [=](int, int m) -> const bf16_t* { return Wo + (size_t)(g * 16 + m) * qd; };
+    };
+    if (me < nuo) wfetch(w1, orows(me), (me / cg) * klo, klo);
+    // ---- attention over the key chunks: unit (query head h, chunk c)
+    for (int u = blockIdx.x; u < nq * nch && ok; u += op->nwg) {
+      const int h = u / nch, c = u - h * nch, g = h / grp;
+      const int t0 = c * ch, t1 = min(np, t0 + ch), n = t1 - t0;
+      const int nog = kThreads / d;
+      float* qv = dyn;  // [d], then k, v of this position
+      float* kn = qv + d;
+      float* vn = kn + d;
+      float* sc = vn + d;                 // [ch]
+      float* og = sc + ch;                // [nog][d]
+      float* zg = og + nog * d;           // [nog]
+      float* kvs = dyn + ((3 * d + ch + nog * d + nog + 3) & ~3);  // [ch][2d]
+      float* kvc = op->kv + (((size_t)l * p->nkv + g) * op->max_frames) * 2 * d;
+      lds_fill4(kvs, kvc + (size_t)t0 * 2 * d, n * d / 2);
+      ok = opoll(op, 3 * d, otag(call, l, kTagQKV),
+                 [=](int e) {
+                   const int part = e / d, i = e - part * d;
+                   const int col = part == 0 ? h * d + i : qd + (part - 1) * p->kvdim + g * d + i;
+                   return op->tq + b * N + col;
+                 },
+                 [&](int e, uint32_t v) { dyn[e] = __uint_as_float(v); });
+      if (!ok) break;
+      const int lane = tid() & 63, wave = tid() >> 6;
+      if (wave < 2) {
+        float* x = wave == 0 ? qv : kn;
+        const float* gn = bfw(p, boff(p, l, wave == 0 ? p->o_qn : p->o_kn));
+        float s2 = 0.f;
+        for (int i = lane; i < d; i += 64) s2 = fmaf(x[i], x[i], s2);
+        s2 = wave_sum(s2);
+        const float rs = p->qk_norm ? 1.f / sqrtf(s2 / (float)d + p->rms_eps) : 1.f;
+        for (int i = lane; i < half; i += 64) {
+          float a = x[i], bb = x[i + half];
+          if (p->qk_norm) {
+            a = a * rs * G(gn)[i];
+            bb = bb * rs * G(gn)[i + half];
+          }
+          const float cs = G(op->rope)[((size_t)pos * half + i) * 2], sn = G(op->rope)[((size_t)pos * half + i) * 2 + 1];
+          x[i] = a * cs - bb * sn;
+          x[i + half] = bb * cs + a * sn;
+        }
+      }
+      __syncthreads();
+      if (h % grp == 0 && c == 0)
+        for (int e = tid(); e < 2 * d; e += kThreads) cstf(kvc + (size_t)pos * 2 * d + e, e < d ? kn[e] : vn[e - d]);
+      if (t1 - 1 == pos)
+        for (int i = tid(); i < 2 * d; i += kThreads) kvs[(pos - t0) * 2 * d + i] = i < d ? kn[i] : vn[i - d];
+      __syncthreads();
+      const float scale = 1.f / sqrtf((float)d);
+      for (int t = wave; t < n; t += kWaves) {
+        float a = 0.f;
+        for (int i = lane; i < d; i += 64) a = fmaf(qv[i], kvs[t * 2 * d + i], a);
+        a = wave_sum(a) * scale;
+        if (lane == 0) sc[t] = a;
+      }
+      __syncthreads();
+      float mx = -INFINITY;
+      for (int t = 0; t < n; ++t) mx = fmaxf(mx, sc[t]);
+      __syncthreads();
+      for (int t = tid(); t < n; t += kThreads) sc[t] = expf(sc[t] - mx);
+      __syncthreads();
+      if (tid() < nog * d) {
+        const int gi = tid() / d, i = tid() - gi * d;
+        float o = 0.f, z = 0.f;
+        for (int t = gi; t < n; t += nog) {
+          const float w = sc[t];
+          o = fmaf(w, kvs[t * 2 * d + d + i], o);
+          z += w;
+        }
+        og[gi * d + i] = o;
+        if (i == 0) zg[gi] = z;
+      }
+      __syncthreads();
+      uint64_t* dst = op->tch + ((b * nq + h) * kAttnMaxChunks + c) * (d + 2);
+      const uint32_t tg = otag(call, l, kTagChunk);
+      for (int i = tid(); i < d; i += kThreads) {
+        float o = og[i];
+        for (int gi = 1; gi < nog; ++gi) o += og[gi * d + i];
+        tstore(dst + 2 + i, tg, o);
+        if (i == 0) {
+          float z = zg[0];
+          for (int gi = 1; gi < nog; ++gi) z += zg[gi];
+          tstore(dst, tg, mx);
+          tstore(dst + 1, tg, z);
+        }
+      }
+      __syncthreads();
+    }
+    if (!ok) break;
+    // ---- merge the chunk partials of head h (workgroup h)
+    for (int h = blockIdx.x; h < nq && ok; h += op->nwg) {
+      const uint64_t* src = op->tch + (b * nq + h) * kAttnMaxChunks * (d + 2);
+      ok = opoll(op, nch * (d + 2), otag(call, l, kTagChunk), [=](int i) { return src + i; },
+                 [&](int i, uint32_t v) { dyn[i] = __uint_as_float(v); });
+      if (!ok) break;
+      float* w = dyn + nch * (d + 2);
+      float mx = -INFINITY;
+      for (int c = 0; c < nch; ++c) mx = fmaxf(mx, dyn[c * (d + 2)]);
+      for (int c = tid(); c < nch; c += kThreads) w[c] = expf(dyn[c * (d + 2)] - mx);
+      __syncthreads();
+      float z = 0.f;
+      for (int c = 0; c < nch; ++c) z += dyn[c * (d + 2) + 1] * w[c];
+      const float iz = 1.f / z;
+      const uint32_t tg = otag(call, l, kTagMerge);
+      for (int i = tid(); i < d; i += kThreads) {
+        float o = 0.f;
+        for (int c = 0; c < nch; ++c) o += dyn[c * (d + 2) + 2 + i] * w[c];
+        tstore(op->tat + b * qd + h * d + i, tg, o * iz);
+      }
+      __syncthreads();
+    }
+    if (!ok) break;
+    // ---- O: unit (16 columns, k split ks): partial sums
+    {
+      const uint32_t tg = otag(call, l, kTagO);
+      for (int u = me; u < nuo && ok; u += nwg) {
+        const int g = u % cg, ks = u / cg;
+        if (u != me) wfetch(w1, orows(u), ks * klo, klo);
+        ok = fill_split(op, op->tat + b * qd, ks * klo, klo, otag(call, l, kTagMerge), arow, tmp);
+        if (!ok) break;
+        wdot(w1, ks * klo, klo, arow, red, [&](int f, const float* v) { tstore(op->top + (b * kOutOSplit + ks) * H + g * 16 + f, tg, v[0]); });
+      }
+    }
+    if (!ok) break;
+    // ---- gate/up: x += O partial sums; 16 features per unit (n-tile 0 gate, 1 up)
+    const bf16_t* wg = bw(p, boff(p, l, p->o_wg));
+    const bf16_t* wu = bw(p, boff(p, l, p->o_wu));
+    auto gurows = [=](int u) {
+      return [=](int nt, int m) -> const bf16_t* { return (nt ? wu : wg) + (size_t)(u * 16 + m) * H; };
+    };
+    if (me < F / 16) wfetch(w2, gurows(me), 0, H);
+    ok = fold_parts(op, op->top + b * kOutOSplit * H, op->ks_o2, otag(call, l, kTagO), xr, tmp);
+    if (!ok) break;
+    if (me < F / 16) {
+      norm_split(op, sh, xr, bfw(p, boff(p, l, p->o_mlp_norm)), arow, nullptr);
+      const uint32_t tg = otag(call, l, kTagAct);
+      for (int u = me; u < F / 16; u += nwg) {
+        if (u != me) wfetch(w2, gurows(u), 0, H);
+        wdot(w2, 0, H, arow, red, [&](int f, const float* v) {
+          tstore(op->tact + b * F + u * 16 + f, tg, v[0] / (1.f + expf(-v[0])) * v[1]);
+        });
+      }
+    }
+    // ---- down: unit (16 columns, k split ks): partial sums
+    {
+      const bf16_t* Wd = bw(p, boff(p, l, p->o_wd));
+      auto drows = [=](int u) {
+        const int g = u % cg;
+        return [=](int, int m) -> const bf16_t* { return Wd + (size_t)(g * 16 + m) * F; };
+      };
+      const uint32_t tg = otag(call, l, kTagDown);
+      for (int u = me; u < nud && ok; u += nwg) {
+        const int g = u % cg, ks = u / cg;
+        wfetch(w1, drows(u), ks * kld, kld);
+        ok = fill_split(op, op->tact + b * F, ks * kld, kld, otag(call, l, kTagAct), arow, tmp);
+        if (!ok) break;
+        wdot(w1, ks * kld, kld, arow, red, [&](int f, const float* v) { tstore(op->tdp + (b * kOutDSplit + ks) * H + g * 16 + f, tg, v[0]); });
+      }
+    }
+  }
+  // ---- head: x += the last down partial sums, final norm (hidden_out), logits
+  const int Vh = p->V;
+  const int nuh = (Vh + 15) / 16;
+  if (ok && (me < nuh || me == 0)) {
+    const bf16_t* Wh = bw(p, p->o_lmh1);
+    auto hrows = [=](int u) {
+      return [=](int, int m) -> const bf16_t* { return u * 16 + m < Vh ? Wh + (size_t)(u * 16 + m) * H : nullptr; };
+    };
+    if (me < nuh) wfetch(w1, hrows(me), 0, H);
+    ok = fold_parts(op, op->tdp + (size_t)(L - 1) * kOutDSplit * H, op->ks_d2, otag(call, L - 1, kTagDown), xr, tmp);
+    if (ok) {
+      norm_split(op, sh, xr, bfw(p, p->o_final_norm), arow, call.hidden_out);
+      const uint32_t tg = otag(call, L, 0);
+      for (int u = me; u < nuh; u += nwg) {
+        if (u != me) wfetch(w1, hrows(u), 0, H);
+        wdot(w1, 0, H, arow, red, [&](int f, const float* v) { if (u * 16 + f < Vh) tstore(op->tlog + u * 16 + f, tg, v[0]); });
+      }
+    }
+  }
+  // ---- c_0: top-k over the logits of the codes the inner tables embed (workgroup 0)
+  if (ok && blockIdx.x == 0) {
+    const int V = min(Vh, op->table_vocab);
+    float* lg = dyn;
+    ok = opoll(op, V, otag(call, L, 0), [=](int i) { return op->tlog + i; }, [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); });
+    if (ok) {
+      int* sidx = reinterpret_cast<int*>(lg + V);
+      float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);
+      double* prob = reinterpret_cast<double*>(lg + ((V + 2 * kMaxTopk + 1) & ~1));
+      unsigned* hist = reinterpret_cast<unsigned*>(prob + kMaxTopk);
+      int ns = topk_buckets(&sh->tk, lg, V, op->topk, sidx, slog, hist);
+      if (ns < 0) ns = topk_select(&sh->tk, lg, V, op->topk, sidx, slog);
+      softmax_support(slog, ns, op->temperature, prob);
+      __syncthreads();
+      if (tid() < 64) {
+        bool fin = false;
+        for (int i = tid(); i < ns; i += 64) fin |= (slog[i] > -INFINITY && slog[i] < INFINITY);
+        const bool any_fin = __any(fin);
+        const int cp = inverse_cdf(prob, ns, (double)G(call.u_c0)[0]);
+        if (tid() == 0) {
+          if (!any_fin) raise_status(op, RVQSD_ENUMERIC);
+          call.c0_out[0] = any_fin ? sidx[cp] : -1;
+        }
+      }
+    }
+  }
+  if (!ok && blockIdx.x == 0 && tid() == 0) call.c0_out[0] = -1;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------- host
@@ -2044,17 +2528,26 @@ int launch_batch(const BParams* bp, const BCall& call, int nwg, void* stream, si
 
 namespace rvqsd {
 
-int launch_outer(const OParams* op, const OCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
+int launch_outer(const OParams* op, const OCall& call, int nwg, void* stream, size_t lds_bytes, int flow_steps, char* err,
                  size_t errlen) {
-  const void* fn = reinterpret_cast<const void*>(&outer_kernel);
-  static size_t attr_bytes = 0;
-  if (lds_bytes > attr_bytes) {
+  // flow_steps 0: the step with grid barriers; else the one without, whose units hold their
+  // weights in registers, flow_steps (<= kFlowSteps) 64-wide k steps per wave
+  if (flow_steps < 0 || flow_steps > kFlowSteps) {
+    snprintf(err, errlen, "outer step: %d k steps per wave (at most %d)", flow_steps, kFlowSteps);
+    return RVQSD_EINVAL;
+  }
+  const bool flow = flow_steps > 0;
+  const void* fn = flow ? reinterpret_cast<const void*>(&outer_flow_kernel<kFlowSteps>)
+                        : reinterpret_cast<const void*>(&outer_kernel);
+  const int slot = flow ? 1 : 0;
+  static size_t attr_bytes[2] = {0, 0};
+  if (lds_bytes > attr_bytes[slot]) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) {
       snprintf(err, errlen, "hipFuncSetAttribute(%zu bytes LDS): %s", lds_bytes, hipGetErrorString(e));
       return RVQSD_EHIP;
     }
-    attr_bytes = lds_bytes;
+    attr_bytes[slot] = lds_bytes;
   }
   const OParams* opa = op;
   OCall c = call;

@@ -156,6 +156,7 @@ int launch_frame(const KParams* gp, const FrameArgs& fa, int nwg, int dtype, int
 // i * rpl .. i * rpl + rpl - 1 of every pass (rpl = max(K + 1, 2)), so a
 // projection multiplies M = lanes * rpl rows at once on MFMA tiles.
 constexpr int kMaxLanes = 16;
+constexpr int kOutOSplit = 4, kOutDSplit = 3;  // k splits of the outer step's O and down projections
 constexpr int kBatchMaxRows = 80;  // lanes * rpl: five 16-row MFMA tiles
 constexpr int kBatchMTiles = kBatchMaxRows / 16;
 constexpr int kBatchRedFloats = 16 * kBatchMTiles * 256;  // LDS partial tiles of one MFMA unit (k parts x n-tiles)
@@ -251,6 +252,17 @@ struct OParams {
   float* logits;         // [V]
   uint32_t* bar;         // grid barrier words
   int32_t* status;       // first device-side error of the step (0 = none)
+  // tagged exchange words of the step without grid barriers (upper 32 bits: the tag of the write),
+  // one set per layer
+  uint64_t* tq;          // [L][nqkv] QKV outputs
+  uint64_t* tch;         // [L][nq][kAttnMaxChunks][d + 2] attention chunk partials (max, sum, o)
+  uint64_t* tat;         // [L][qdim] merged attention output
+  uint64_t* top;         // [L][kOutOSplit][H] O partial sums
+  uint64_t* tact;        // [L][F] SwiGLU activations
+  uint64_t* tdp;         // [L][kOutDSplit][H] down partial sums
+  uint64_t* tlog;        // [V] head logits
+  int32_t xoff;          // float offset in dynamic LDS of the residual row every workgroup keeps
+  int32_t ks_o2, ks_d2;  // k splits of its O and down projections (<= kOutOSplit, kOutDSplit)
 };
 
 // Per-step arguments (device pointers), passed by value.
@@ -261,10 +273,15 @@ struct OCall {
   int32_t* c0_out;           // [1] sampled c_0 (-1 after a device error)
   float* hidden_out;         // [H] final-normed hidden state (the inner loop's frame input)
   int32_t pos;               // position = frame index since the last reset
+  uint32_t epoch;            // launch counter of this outer step object (tags its exchange words)
 };
 
-int launch_outer(const OParams* op, const OCall& call, int nwg, void* stream, size_t lds_bytes, char* err,
-                 size_t errlen);
+// flow_steps 0: the step with a grid barrier between phases; 1 .. kFlowSteps: the step without
+// grid barriers, whose units hold up to flow_steps 64-wide k steps per wave of weights in registers
+// (k ranges up to 512 kFlowSteps)
+constexpr int kFlowSteps = 2;
+int launch_outer(const OParams* op, const OCall& call, int nwg, void* stream, size_t lds_bytes, int flow_steps,
+                 char* err, size_t errlen);
 int frame_lds_head_floats(int mr, int cpw);
 int frame_max_rows(int K);
 

@@ -32,6 +32,11 @@ INNER_SMALL = S.ModelShape(n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=4, he
                            vocab=128, max_draft=14, dtype=S.DTYPE_BF16)
 OUTER_SMALL = S.ModelShape(n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=4, head_dim=64, ffn=1024, n_codes=1,
                            vocab=192, max_draft=0, dtype=S.DTYPE_BF16)
+# an ffn of 2560 splits into no k ranges of 512 or 1024 (2560 is no multiple of 1024 or 1536), so
+# its down units would hold more weights than fit in registers: this outer step takes the kernel
+# with grid barriers; OUTER_SMALL and the full-size model take the one without
+OUTER_WIDE_FFN = S.ModelShape(n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=4, head_dim=64, ffn=2560, n_codes=1,
+                              vocab=192, max_draft=0, dtype=S.DTYPE_BF16)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -116,12 +121,13 @@ def compare(rig, t, u_c0, uni, codes, st, hs):
     return n, 0.0
 
 
-def test_small_pipeline_matches_oracle():
+@pytest.mark.parametrize("outer_s", [OUTER_SMALL, OUTER_WIDE_FFN], ids=["flow-step", "barrier-step"])
+def test_small_pipeline_matches_oracle(outer_s):
     """2-layer outer (192-entry head, c_0 over the inner 128 codes) + 2-layer inner, K = 3,
-    12 chained frames, then a reset replays the same frames."""
-    rig = PRig(OUTER_SMALL, INNER_SMALL, topk=16, K=3)
+    12 chained frames, then a reset replays the same frames; both outer-step kernels."""
+    rig = PRig(outer_s, INNER_SMALL, topk=16, K=3)
     n = 12
-    t, u_c0 = S.pipeline_inputs(OUTER_SMALL, n)
+    t, u_c0 = S.pipeline_inputs(outer_s, n)
     uni = S.uniforms(n)
     codes, st, hs = rig.run_gpu(t, u_c0, uni)
     assert (codes[:, 0] >= 0).all() and (codes[:, 0] < INNER_SMALL.vocab).all()
