@@ -2077,10 +2077,23 @@ __device__ bool opoll(const OParams* op, int n, uint32_t tag, Addr addr, Sink si
   return !__syncthreads_or(bad);
 }
 
-// x (LDS, [H]) normalised with gain, split into the LDS row a (its words k0 .. k0 + n - 1 of the
-// row are written for k in [k0, k0 + n), the whole row when n = H); hidden_out (workgroup 0)
+// Thread c < H / 8 holds gain elements 8c .. 8c + 7 (H <= 8 kThreads), loaded ahead of the
+// row they scale
+struct Gain8 {
+  f32x4 g0, g1;
+};
+__device__ __forceinline__ Gain8 gain_fetch(const float* gain, int H) {
+  Gain8 g = {(f32x4){0.f, 0.f, 0.f, 0.f}, (f32x4){0.f, 0.f, 0.f, 0.f}};
+  if (tid() < H / 8) {
+    g.g0 = G(reinterpret_cast<const f32x4*>(gain))[2 * tid()];
+    g.g1 = G(reinterpret_cast<const f32x4*>(gain))[2 * tid() + 1];
+  }
+  return g;
+}
+
+// x (LDS, [H]) normalised with the gain, split into the LDS row a; hidden_out (workgroup 0)
 // receives the normalised values
-__device__ void norm_split(const OParams* op, BShared* sh, const float* x, const float* gain, uint32_t* a,
+__device__ void norm_split(const OParams* op, BShared* sh, const float* x, const Gain8& gn, uint32_t* a,
                            float* hidden_out) {
   const KParams* p = op->k;
   const int H = p->H;
@@ -2088,10 +2101,14 @@ __device__ void norm_split(const OParams* op, BShared* sh, const float* x, const
   for (int e = tid(); e < H; e += kThreads) ss = fmaf(x[e], x[e], ss);
   ss = block_sum(sh, ss);
   const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
-  for (int c = tid(); c < H / 8; c += kThreads) {
+  const int c = tid();
+  if (c < H / 8) {
     float h8[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) h8[e] = x[8 * c + e] * rs * G(gain)[8 * c + e];
+    for (int e = 0; e < 4; ++e) {
+      h8[e] = x[8 * c + e] * rs * gn.g0[e];
+      h8[4 + e] = x[8 * c + 4 + e] * rs * gn.g1[e];
+    }
     W16 hi, lo;
     split8(h8, hi, lo);
     *reinterpret_cast<W16*>(a + 8 * c) = hi;
@@ -2270,9 +2287,10 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
       return [=](int, int m) -> const bf16_t* { return u * 16 + m < N ? Wq + (size_t)(u * 16 + m) * H : nullptr; };
     };
     if (me < nuq) wfetch(w1, qrows(me), 0, H);
+    const Gain8 gan = gain_fetch(bfw(p, boff(p, l, p->o_attn_norm)), H);
     if (l > 0) ok = fold_parts(op, op->tdp + (b - 1) * kOutDSplit * H, op->ks_d2, otag(call, l - 1, kTagDown), xr, tmp);
     if (!ok) break;
-    norm_split(op, sh, xr, bfw(p, boff(p, l, p->o_attn_norm)), arow, nullptr);
+    norm_split(op, sh, xr, gan, arow, nullptr);
     {
       const uint32_t tg = otag(call, l, kTagQKV);
       for (int u = me; u < nuq; u += nwg) {
@@ -2300,6 +2318,25 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
       float* zg = og + nog * d;           // [nog]
       float* kvs = dyn + ((3 * d + ch + nog * d + nog + 3) & ~3);  // [ch][2d]
       float* kvc = op->kv + (((size_t)l * p->nkv + g) * op->max_frames) * 2 * d;
+      const int lane = tid() & 63, wave = tid() >> 6;
+      // waves 0 and 1 normalise and rotate q and k: their gains and this position's rotary
+      // factors are loaded before the wait (head_dim <= 256: at most two elements per lane)
+      float gl[2] = {1.f, 1.f}, gh[2] = {1.f, 1.f}, rc[2] = {0.f, 0.f}, rsn[2] = {0.f, 0.f};
+      if (wave < 2) {
+        const float* gn = bfw(p, boff(p, l, wave == 0 ? p->o_qn : p->o_kn));
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int i = lane + 64 * j;
+          if (i < half) {
+            if (p->qk_norm) {
+              gl[j] = G(gn)[i];
+              gh[j] = G(gn)[i + half];
+            }
+            rc[j] = G(op->rope)[((size_t)pos * half + i) * 2];
+            rsn[j] = G(op->rope)[((size_t)pos * half + i) * 2 + 1];
+          }
+        }
+      }
       lds_fill4(kvs, kvc + (size_t)t0 * 2 * d, n * d / 2);
       ok = opoll(op, 3 * d, otag(call, l, kTagQKV),
                  [=](int e) {
@@ -2309,23 +2346,24 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
                  },
                  [&](int e, uint32_t v) { dyn[e] = __uint_as_float(v); });
       if (!ok) break;
-      const int lane = tid() & 63, wave = tid() >> 6;
       if (wave < 2) {
         float* x = wave == 0 ? qv : kn;
-        const float* gn = bfw(p, boff(p, l, wave == 0 ? p->o_qn : p->o_kn));
         float s2 = 0.f;
         for (int i = lane; i < d; i += 64) s2 = fmaf(x[i], x[i], s2);
         s2 = wave_sum(s2);
         const float rs = p->qk_norm ? 1.f / sqrtf(s2 / (float)d + p->rms_eps) : 1.f;
-        for (int i = lane; i < half; i += 64) {
-          float a = x[i], bb = x[i + half];
-          if (p->qk_norm) {
-            a = a * rs * G(gn)[i];
-            bb = bb * rs * G(gn)[i + half];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int i = lane + 64 * j;
+          if (i < half) {
+            float a = x[i], bb = x[i + half];
+            if (p->qk_norm) {
+              a = a * rs * gl[j];
+              bb = bb * rs * gh[j];
+            }
+            x[i] = a * rc[j] - bb * rsn[j];
+            x[i + half] = bb * rc[j] + a * rsn[j];
           }
-          const float cs = G(op->rope)[((size_t)pos * half + i) * 2], sn = G(op->rope)[((size_t)pos * half + i) * 2 + 1];
-          x[i] = a * cs - bb * sn;
-          x[i + half] = bb * cs + a * sn;
         }
       }
       __syncthreads();
@@ -2334,16 +2372,34 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
       if (t1 - 1 == pos)
         for (int i = tid(); i < 2 * d; i += kThreads) kvs[(pos - t0) * 2 * d + i] = i < d ? kn[i] : vn[i - d];
       __syncthreads();
+      // scores: eight lanes per position, each over d / 32 of the float4s of q and k; the
+      // position rotates the segment order so that the groups of a wave read different banks
       const float scale = 1.f / sqrtf((float)d);
-      for (int t = wave; t < n; t += kWaves) {
+      const int nseg = d / 32, gsub = tid() & 7;
+      for (int t = tid() >> 3; t < n; t += kThreads / 8) {
+        const float* kr = kvs + (size_t)t * 2 * d;
+        int sg = t % nseg;
         float a = 0.f;
-        for (int i = lane; i < d; i += 64) a = fmaf(qv[i], kvs[t * 2 * d + i], a);
-        a = wave_sum(a) * scale;
-        if (lane == 0) sc[t] = a;
+        for (int s2 = 0; s2 < nseg; ++s2) {
+          const int v4 = 4 * (gsub + 8 * sg);
+          const f32x4 kk = *reinterpret_cast<const f32x4*>(kr + v4), qq = *reinterpret_cast<const f32x4*>(qv + v4);
+          a = fmaf(qq[0], kk[0], a);
+          a = fmaf(qq[1], kk[1], a);
+          a = fmaf(qq[2], kk[2], a);
+          a = fmaf(qq[3], kk[3], a);
+          if (++sg == nseg) sg = 0;
+        }
+        a += __shfl_xor(a, 1, 64);
+        a += __shfl_xor(a, 2, 64);
+        a += __shfl_xor(a, 4, 64);
+        if (gsub == 0) sc[t] = a * scale;
       }
       __syncthreads();
+      // every wave takes the maximum itself
       float mx = -INFINITY;
-      for (int t = 0; t < n; ++t) mx = fmaxf(mx, sc[t]);
+      for (int t = lane; t < n; t += 64) mx = fmaxf(mx, sc[t]);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
       __syncthreads();
       for (int t = tid(); t < n; t += kThreads) sc[t] = expf(sc[t] - mx);
       __syncthreads();
@@ -2382,12 +2438,16 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
                  [&](int i, uint32_t v) { dyn[i] = __uint_as_float(v); });
       if (!ok) break;
       float* w = dyn + nch * (d + 2);
-      float mx = -INFINITY;
-      for (int c = 0; c < nch; ++c) mx = fmaxf(mx, dyn[c * (d + 2)]);
+      const int lane = tid() & 63;
+      float mx = -INFINITY;  // every wave takes the maximum and the normaliser itself
+      for (int c = lane; c < nch; c += 64) mx = fmaxf(mx, dyn[c * (d + 2)]);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
       for (int c = tid(); c < nch; c += kThreads) w[c] = expf(dyn[c * (d + 2)] - mx);
       __syncthreads();
       float z = 0.f;
-      for (int c = 0; c < nch; ++c) z += dyn[c * (d + 2) + 1] * w[c];
+      for (int c = lane; c < nch; c += 64) z += dyn[c * (d + 2) + 1] * w[c];
+      z = wave_sum(z);
       const float iz = 1.f / z;
       const uint32_t tg = otag(call, l, kTagMerge);
       for (int i = tid(); i < d; i += kThreads) {
@@ -2417,10 +2477,11 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
       return [=](int nt, int m) -> const bf16_t* { return (nt ? wu : wg) + (size_t)(u * 16 + m) * H; };
     };
     if (me < F / 16) wfetch(w2, gurows(me), 0, H);
+    const Gain8 gmn = gain_fetch(bfw(p, boff(p, l, p->o_mlp_norm)), H);
     ok = fold_parts(op, op->top + b * kOutOSplit * H, op->ks_o2, otag(call, l, kTagO), xr, tmp);
     if (!ok) break;
     if (me < F / 16) {
-      norm_split(op, sh, xr, bfw(p, boff(p, l, p->o_mlp_norm)), arow, nullptr);
+      norm_split(op, sh, xr, gmn, arow, nullptr);
       const uint32_t tg = otag(call, l, kTagAct);
       for (int u = me; u < F / 16; u += nwg) {
         if (u != me) wfetch(w2, gurows(u), 0, H);
@@ -2455,9 +2516,10 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
       return [=](int, int m) -> const bf16_t* { return u * 16 + m < Vh ? Wh + (size_t)(u * 16 + m) * H : nullptr; };
     };
     if (me < nuh) wfetch(w1, hrows(me), 0, H);
+    const Gain8 gfn = gain_fetch(bfw(p, p->o_final_norm), H);
     ok = fold_parts(op, op->tdp + (size_t)(L - 1) * kOutDSplit * H, op->ks_d2, otag(call, L - 1, kTagDown), xr, tmp);
     if (ok) {
-      norm_split(op, sh, xr, bfw(p, p->o_final_norm), arow, call.hidden_out);
+      norm_split(op, sh, xr, gfn, arow, call.hidden_out);
       const uint32_t tg = otag(call, L, 0);
       for (int u = me; u < nuh; u += nwg) {
         if (u != me) wfetch(w1, hrows(u), 0, H);
