@@ -871,11 +871,12 @@ rvqsd_status rvqsd_outer_create(rvqsd_model* m, const void* code_tables, int32_t
   b.topk = topk;
   b.temperature = temperature;
   const size_t kmax = (size_t)(k.H > k.qdim ? (k.H > k.F ? k.H : k.F) : (k.qdim > k.F ? k.qdim : k.F));
-  // the step without grid barriers: units of 16 rows over the whole k range or a k split that is a
-  // multiple of 512 (eight waves of 64-wide steps)
+  // the step without grid barriers: units of 16 rows over the whole k range or the fewest k splits
+  // (each a multiple of 512: eight waves of 64-wide steps) whose range fits a unit's registers; fewer
+  // splits mean fewer partial sums for every workgroup to read
   auto split512 = [](int K, int most) {
-    for (int ks = most; ks >= 1; --ks)
-      if (K % (ks * 512) == 0) return ks;
+    for (int ks = 1; ks <= most; ++ks)
+      if (K % (ks * 512) == 0 && K / ks <= kFlowSteps * 512) return ks;
     return 0;
   };
   b.ks_o2 = split512(k.qdim, kOutOSplit);
