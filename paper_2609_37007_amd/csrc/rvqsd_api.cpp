@@ -1044,7 +1044,8 @@ rvqsd_status rvqsd_pipeline_frames_async(rvqsd_stream* s, rvqsd_outer* o, int32_
     c.c0_out = d_codes + (size_t)i * (1 + nc);
     c.hidden_out = fbuf ? fbuf + (size_t)i * H : o->f;
     c.pos = o->pos;
-    c.epoch = ++o->epoch;
+    if (++o->epoch == 0) o->epoch = 1;  // the exchange words start at 0: launch number 0 is never used
+    c.epoch = o->epoch;
     char err[256];
     int st = launch_outer(o->dop, c, o->m->nwg, (void*)s->stream, o->lds, o->flow_steps, err, sizeof(err));
     if (st) return set_err(st, "%s", err);

@@ -2018,17 +2018,14 @@ __global__ void __launch_bounds__(kThreads, 1) outer_kernel(const OParams* __res
 
 // ------------------------------------------------------------ outer step without grid barriers
 // The same step as outer_kernel, with every value one workgroup hands to another carried by a
-// 64-bit word whose upper half is a tag unique to (launch, layer, kind): a reader polls the
-// words until its tag appears, so no grid barrier separates the phases. Every layer has words of
-// its own, so no word is written twice in one launch and a reader that falls behind still finds
-// its tag; the next launch on the stream starts after this one has ended. With one row, every
-// workgroup keeps the whole residual row in LDS and adds the O and down partial sums to it
-// itself, in split order, so all copies are equal.
+// 64-bit word whose upper half is the launch number of the write: a reader polls the words
+// until they carry this launch's number, so no grid barrier separates the phases. Every layer
+// and kind of value has words of its own, so no word is written twice in one launch and a
+// reader that falls behind still finds its value; the next launch on the stream starts after
+// this one has ended, and a launch that failed leaves only words of older launches. With one
+// row, every workgroup keeps the whole residual row in LDS and adds the O and down partial sums
+// to it itself, in split order, so all copies are equal.
 
-constexpr int kTagQKV = 0, kTagChunk = 1, kTagMerge = 2, kTagO = 3, kTagAct = 4, kTagDown = 5;
-__device__ __forceinline__ uint32_t otag(const OCall& call, int l, int kind) {
-  return (call.epoch << 10) | (uint32_t)(8 * l + kind);
-}
 __device__ __forceinline__ void tstore(uint64_t* p, uint32_t tag, float v) {
   cst64(p, ((uint64_t)tag << 32) | __float_as_uint(v));
 }
@@ -2288,11 +2285,11 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     };
     if (me < nuq) wfetch(w1, qrows(me), 0, H);
     const Gain8 gan = gain_fetch(bfw(p, boff(p, l, p->o_attn_norm)), H);
-    if (l > 0) ok = fold_parts(op, op->tdp + (b - 1) * kOutDSplit * H, op->ks_d2, otag(call, l - 1, kTagDown), xr, tmp);
+    if (l > 0) ok = fold_parts(op, op->tdp + (b - 1) * kOutDSplit * H, op->ks_d2, call.epoch, xr, tmp);
     if (!ok) break;
     norm_split(op, sh, xr, gan, arow, nullptr);
     {
-      const uint32_t tg = otag(call, l, kTagQKV);
+      const uint32_t tg = call.epoch;
       for (int u = me; u < nuq; u += nwg) {
         if (u != me) wfetch(w1, qrows(u), 0, H);
         wdot(w1, 0, H, arow, red, [&](int f, const float* v) { if (u * 16 + f < N) tstore(op->tq + b * N + u * 16 + f, tg, v[0]); });
@@ -2338,7 +2335,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
         }
       }
       lds_fill4(kvs, kvc + (size_t)t0 * 2 * d, n * d / 2);
-      ok = opoll(op, 3 * d, otag(call, l, kTagQKV),
+      ok = opoll(op, 3 * d, call.epoch,
                  [=](int e) {
                    const int part = e / d, i = e - part * d;
                    const int col = part == 0 ? h * d + i : qd + (part - 1) * p->kvdim + g * d + i;
@@ -2416,7 +2413,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
       }
       __syncthreads();
       uint64_t* dst = op->tch + ((b * nq + h) * kAttnMaxChunks + c) * (d + 2);
-      const uint32_t tg = otag(call, l, kTagChunk);
+      const uint32_t tg = call.epoch;
       for (int i = tid(); i < d; i += kThreads) {
         float o = og[i];
         for (int gi = 1; gi < nog; ++gi) o += og[gi * d + i];
@@ -2434,7 +2431,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     // ---- merge the chunk partials of head h (workgroup h)
     for (int h = blockIdx.x; h < nq && ok; h += op->nwg) {
       const uint64_t* src = op->tch + (b * nq + h) * kAttnMaxChunks * (d + 2);
-      ok = opoll(op, nch * (d + 2), otag(call, l, kTagChunk), [=](int i) { return src + i; },
+      ok = opoll(op, nch * (d + 2), call.epoch, [=](int i) { return src + i; },
                  [&](int i, uint32_t v) { dyn[i] = __uint_as_float(v); });
       if (!ok) break;
       float* w = dyn + nch * (d + 2);
@@ -2449,7 +2446,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
       for (int c = lane; c < nch; c += 64) z += dyn[c * (d + 2) + 1] * w[c];
       z = wave_sum(z);
       const float iz = 1.f / z;
-      const uint32_t tg = otag(call, l, kTagMerge);
+      const uint32_t tg = call.epoch;
       for (int i = tid(); i < d; i += kThreads) {
         float o = 0.f;
         for (int c = 0; c < nch; ++c) o += dyn[c * (d + 2) + 2 + i] * w[c];
@@ -2460,11 +2457,11 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     if (!ok) break;
     // ---- O: unit (16 columns, k split ks): partial sums
     {
-      const uint32_t tg = otag(call, l, kTagO);
+      const uint32_t tg = call.epoch;
       for (int u = me; u < nuo && ok; u += nwg) {
         const int g = u % cg, ks = u / cg;
         if (u != me) wfetch(w1, orows(u), ks * klo, klo);
-        ok = fill_split(op, op->tat + b * qd, ks * klo, klo, otag(call, l, kTagMerge), arow, tmp);
+        ok = fill_split(op, op->tat + b * qd, ks * klo, klo, call.epoch, arow, tmp);
         if (!ok) break;
         wdot(w1, ks * klo, klo, arow, red, [&](int f, const float* v) { tstore(op->top + (b * kOutOSplit + ks) * H + g * 16 + f, tg, v[0]); });
       }
@@ -2478,11 +2475,11 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     };
     if (me < F / 16) wfetch(w2, gurows(me), 0, H);
     const Gain8 gmn = gain_fetch(bfw(p, boff(p, l, p->o_mlp_norm)), H);
-    ok = fold_parts(op, op->top + b * kOutOSplit * H, op->ks_o2, otag(call, l, kTagO), xr, tmp);
+    ok = fold_parts(op, op->top + b * kOutOSplit * H, op->ks_o2, call.epoch, xr, tmp);
     if (!ok) break;
     if (me < F / 16) {
       norm_split(op, sh, xr, gmn, arow, nullptr);
-      const uint32_t tg = otag(call, l, kTagAct);
+      const uint32_t tg = call.epoch;
       for (int u = me; u < F / 16; u += nwg) {
         if (u != me) wfetch(w2, gurows(u), 0, H);
         wdot(w2, 0, H, arow, red, [&](int f, const float* v) {
@@ -2497,11 +2494,11 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
         const int g = u % cg;
         return [=](int, int m) -> const bf16_t* { return Wd + (size_t)(g * 16 + m) * F; };
       };
-      const uint32_t tg = otag(call, l, kTagDown);
+      const uint32_t tg = call.epoch;
       for (int u = me; u < nud && ok; u += nwg) {
         const int g = u % cg, ks = u / cg;
         wfetch(w1, drows(u), ks * kld, kld);
-        ok = fill_split(op, op->tact + b * F, ks * kld, kld, otag(call, l, kTagAct), arow, tmp);
+        ok = fill_split(op, op->tact + b * F, ks * kld, kld, call.epoch, arow, tmp);
         if (!ok) break;
         wdot(w1, ks * kld, kld, arow, red, [&](int f, const float* v) { tstore(op->tdp + (b * kOutDSplit + ks) * H + g * 16 + f, tg, v[0]); });
       }
@@ -2517,10 +2514,10 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     };
     if (me < nuh) wfetch(w1, hrows(me), 0, H);
     const Gain8 gfn = gain_fetch(bfw(p, p->o_final_norm), H);
-    ok = fold_parts(op, op->tdp + (size_t)(L - 1) * kOutDSplit * H, op->ks_d2, otag(call, L - 1, kTagDown), xr, tmp);
+    ok = fold_parts(op, op->tdp + (size_t)(L - 1) * kOutDSplit * H, op->ks_d2, call.epoch, xr, tmp);
     if (ok) {
       norm_split(op, sh, xr, gfn, arow, call.hidden_out);
-      const uint32_t tg = otag(call, L, 0);
+      const uint32_t tg = call.epoch;
       for (int u = me; u < nuh; u += nwg) {
         if (u != me) wfetch(w1, hrows(u), 0, H);
         wdot(w1, 0, H, arow, red, [&](int f, const float* v) { if (u * 16 + f < Vh) tstore(op->tlog + u * 16 + f, tg, v[0]); });
@@ -2531,7 +2528,7 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
   if (ok && blockIdx.x == 0) {
     const int V = min(Vh, op->table_vocab);
     float* lg = dyn;
-    ok = opoll(op, V, otag(call, L, 0), [=](int i) { return op->tlog + i; }, [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); });
+    ok = opoll(op, V, call.epoch, [=](int i) { return op->tlog + i; }, [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); });
     if (ok) {
       int* sidx = reinterpret_cast<int*>(lg + V);
       float* slog = reinterpret_cast<float*>(sidx + kMaxTopk);
