@@ -170,6 +170,52 @@ def test_full_size_pipeline_first_frames():
     rig.close()
 
 
+def teacher_forced_check(rig, t, u_c0, uni, codes, st, hs, inner_every=1):
+    """The outer inputs rebuilt from the GPU's own codes: one oracle forward over all rows gives
+    every frame's hidden state (within HIDDEN_TOL); every c_0 must be the oracle's draw from it
+    or sit near a CDF step; every inner_every-th inner frame, run by the oracle from the GPU's
+    hidden state and c_0, must match or part first at a decision within reach of the inner
+    logit error. Returns the frames excused for c_0 and for the inner loop."""
+    n = len(codes)
+    assert (st["status"] == 0).all()
+    nc = rig.inner_s.n_codes
+    rows = np.zeros((n, rig.outer_s.hidden), dtype=np.float64)
+    for i in range(n):
+        x = t[i].astype(np.float64)
+        if i > 0:
+            prev = codes[i - 1]
+            x = x + rig.emb0[prev[0]].astype(np.float64)
+            for j in range(1, 1 + nc):
+                x = x + rig.tab[j - 1][prev[j]].astype(np.float64)
+        rows[i] = x
+    href = rig.oorc.forward_vectors(rows)
+    herr = np.abs(hs.astype(np.float64) - href).max(axis=1)
+    print(f"outer hidden max error {herr.max():.3g} (position of the worst: {int(herr.argmax())})", flush=True)
+    assert herr.max() < HIDDEN_TOL
+    c0_excused, inner_excused = [], []
+    for i in range(n):
+        lg = rig.oorc.logits(href[i], 1)
+        lg[rig.inner_s.vocab:] = -np.inf
+        idx, p = O.topk_softmax(lg, rig.topk, rig.T)
+        c0 = O.sample(idx, p, float(u_c0[i]))
+        if c0 != codes[i][0]:
+            assert c0_near_threshold(rig, href[i], float(u_c0[i])), (i, c0, codes[i][0])
+            c0_excused.append(i)
+        if i % inner_every == 0:
+            oc, ost, _ = rig.iorc.spec_frame(hs[i], int(codes[i][0]), uni[i])
+            if np.array_equal(oc, codes[i][1:]):
+                for k in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
+                    assert st[k][i] == ost[k], (i, k)
+            else:
+                assert GC.untraced_divergence_near(rig.inner, hs[i], int(codes[i][0]), uni[i], codes[i][1:], INNER_ERR), \
+                    (i, codes[i].tolist(), oc.tolist())
+                inner_excused.append(i)
+        if i % 50 == 49:
+            print(f"  {i + 1} frames checked", flush=True)
+    print(f"c_0 near a CDF step: {c0_excused}; inner frames excused: {inner_excused}", flush=True)
+    return c0_excused, inner_excused
+
+
 @pytest.mark.timeout(900)
 def test_small_pipeline_200_frames_teacher_forced():
     """200 chained frames, so the outer KV grows to 200 positions and its split-sequence
@@ -185,39 +231,23 @@ def test_small_pipeline_200_frames_teacher_forced():
     uni = S.uniforms(n)
     print("small pipeline: 200 frames, teacher forced", flush=True)
     codes, st, hs = rig.run_gpu(t, u_c0, uni)
-    assert (st["status"] == 0).all()
-    rows = np.zeros((n, OUTER_SMALL.hidden), dtype=np.float64)
-    for i in range(n):
-        x = t[i].astype(np.float64)
-        if i > 0:
-            prev = codes[i - 1]
-            x = x + rig.emb0[prev[0]].astype(np.float64)
-            for j in range(1, 1 + INNER_SMALL.n_codes):
-                x = x + rig.tab[j - 1][prev[j]].astype(np.float64)
-        rows[i] = x
-    href = rig.oorc.forward_vectors(rows)
-    herr = np.abs(hs.astype(np.float64) - href).max(axis=1)
-    print(f"outer hidden max error {herr.max():.3g} (position of the worst: {int(herr.argmax())})", flush=True)
-    assert herr.max() < HIDDEN_TOL
-    c0_excused, inner_excused = [], []
-    for i in range(n):
-        lg = rig.oorc.logits(href[i], 1)
-        lg[INNER_SMALL.vocab:] = -np.inf
-        idx, p = O.topk_softmax(lg, rig.topk, rig.T)
-        c0 = O.sample(idx, p, float(u_c0[i]))
-        if c0 != codes[i][0]:
-            assert c0_near_threshold(rig, href[i], float(u_c0[i])), (i, c0, codes[i][0])
-            c0_excused.append(i)
-        oc, ost, _ = rig.iorc.spec_frame(hs[i], int(codes[i][0]), uni[i])
-        if np.array_equal(oc, codes[i][1:]):
-            for k in ("target_calls", "rounds", "drafted", "accepted", "accept_mask"):
-                assert st[k][i] == ost[k], (i, k)
-        else:
-            assert GC.untraced_divergence_near(rig.inner, hs[i], int(codes[i][0]), uni[i], codes[i][1:], INNER_ERR), \
-                (i, codes[i].tolist(), oc.tolist())
-            inner_excused.append(i)
-        if i % 50 == 49:
-            print(f"  {i + 1} frames checked", flush=True)
-    print(f"c_0 near a CDF step: {c0_excused}; inner frames excused: {inner_excused}", flush=True)
+    c0_excused, inner_excused = teacher_forced_check(rig, t, u_c0, uni, codes, st, hs)
     assert len(c0_excused) <= 2 and len(inner_excused) <= 4
+    rig.close()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_pipeline_160_frames_teacher_forced():
+    """The 28-layer outer decoder and the 1024-wide inner model (K = 4, top-k 50) over 160
+    chained frames, so that the outer step's attention ends with 10 keys per chunk over 16
+    chunks: every frame's outer hidden state and c_0 against one oracle forward over the rows
+    rebuilt from the GPU's own codes, and every 20th inner frame against the oracle."""
+    rig = PRig(S.OUTER_1024, S.MCD_1024, topk=50, K=4, max_frames=168)
+    n = 160
+    t, u_c0 = S.pipeline_inputs(S.OUTER_1024, n)
+    uni = S.uniforms(n)
+    print("outer 28 layers + mcd1024: 160 frames, teacher forced", flush=True)
+    codes, st, hs = rig.run_gpu(t, u_c0, uni)
+    c0_excused, inner_excused = teacher_forced_check(rig, t, u_c0, uni, codes, st, hs, inner_every=20)
+    assert len(c0_excused) <= 2 and len(inner_excused) <= 2
     rig.close()
