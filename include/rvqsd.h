@@ -295,12 +295,13 @@ rvqsd_status rvqsd_outer_reset(rvqsd_outer* o);
 /* Enqueue n frames of the full pipeline on the inner stream s (device pointers,
  * returns after the launches): per frame one outer step (c_0 and the hidden
  * state) and one inner frame decode (c_1..c_15), chained on the device with no
- * host synchronisation. d_t float[n][hidden]; d_u_c0 float[n] (uniform of each
- * c_0 draw); d_uniforms float[n][n_codes][3] (inner uniforms); d_codes out
- * int32[n][1 + n_codes] (c_0, c_1..c_n); d_stats out rvqsd_stats[n] (inner
- * loop; an outer-step error shows as c_0 = -1 and status EINVAL); d_hidden out
- * float[n][hidden] or NULL. The outer tables must match the inner model
- * (n_tables = n_codes, table_vocab = vocab); EUNSUPPORTED beyond max_frames. */
+ * host synchronisation. d_t float[n][hidden] (16-byte aligned, else EINVAL);
+ * d_u_c0 float[n] (uniform of each c_0 draw); d_uniforms float[n][n_codes][3]
+ * (inner uniforms); d_codes out int32[n][1 + n_codes] (c_0, c_1..c_n); d_stats
+ * out rvqsd_stats[n] (inner loop; an outer-step error shows as c_0 = -1 and
+ * status EINVAL); d_hidden out float[n][hidden] or NULL. The outer tables must
+ * match the inner model (n_tables = n_codes, table_vocab = vocab); EUNSUPPORTED
+ * beyond max_frames. */
 rvqsd_status rvqsd_pipeline_frames_async(rvqsd_stream* s, rvqsd_outer* o, int32_t n, const float* d_t,
                                          const float* d_u_c0, const float* d_uniforms, int32_t* d_codes,
                                          rvqsd_stats* d_stats, float* d_hidden);

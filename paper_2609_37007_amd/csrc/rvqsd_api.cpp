@@ -1024,6 +1024,7 @@ rvqsd_status rvqsd_pipeline_frames_async(rvqsd_stream* s, rvqsd_outer* o, int32_
   if (n < 0) return set_err(RVQSD_EINVAL, "n = %d < 0", n);
   if (n == 0) return RVQSD_OK;
   if (!d_t || !d_u_c0 || !d_uniforms || !d_codes || !d_stats) return set_err(RVQSD_EINVAL, "null argument");
+  if ((uintptr_t)d_t % 16) return set_err(RVQSD_EINVAL, "d_t must be 16-byte aligned");
   const rvqsd_cfg& ic = s->m->cfg;
   const KParams& ok = o->m->base;
   if (ic.hidden != ok.H) return set_err(RVQSD_EINVAL, "inner hidden %d != outer hidden %d", ic.hidden, ok.H);

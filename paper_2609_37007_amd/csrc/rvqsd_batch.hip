@@ -2252,21 +2252,32 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     __syncthreads();
     const bool codes_ok = call.prev_codes != nullptr && pbad == 0;
     if (call.prev_codes && !codes_ok && tid() == 0 && blockIdx.x == 0) raise_status(op, RVQSD_EINVAL);
-    for (int e = tid(); e < H; e += kThreads) {
-      float v = G(call.t)[e];
+    // thread c takes elements 8c .. 8c + 7: every table row's 16 bytes are requested together,
+    // then added in table order
+    for (int c8 = tid(); c8 < H / 8; c8 += kThreads) {
+      const f32x4 ta = G(reinterpret_cast<const f32x4*>(call.t))[2 * c8];
+      const f32x4 tb = G(reinterpret_cast<const f32x4*>(call.t))[2 * c8 + 1];
+      float v[8] = {ta[0], ta[1], ta[2], ta[3], tb[0], tb[1], tb[2], tb[3]};
       if (codes_ok) {
         const bf16_t* e0 = bw(p, p->o_emb0);
-        uint32_t tv[kMaxCodes + 1];
-        tv[0] = G(e0)[(size_t)pcodes[0] * H + e];
+        W16 tv[kMaxCodes + 1];
+        tv[0] = *G(reinterpret_cast<const W16*>(e0 + (size_t)pcodes[0] * H + 8 * c8));
 #pragma unroll
         for (int j = 1; j <= kMaxCodes; ++j)
-          tv[j] = j <= nt ? G(op->tables)[((size_t)(j - 1) * op->table_vocab + pcodes[j]) * H + e] : 0u;
-        v += __uint_as_float(tv[0] << 16);
+          tv[j] = j <= nt ? *G(reinterpret_cast<const W16*>(op->tables + ((size_t)(j - 1) * op->table_vocab + pcodes[j]) * H +
+                                                            8 * c8))
+                          : (W16)(0u);
 #pragma unroll
-        for (int j = 1; j <= kMaxCodes; ++j)
-          if (j <= nt) v += __uint_as_float(tv[j] << 16);
+        for (int j = 0; j <= kMaxCodes; ++j)
+          if (j <= nt)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const uint32_t w = tv[j][e >> 1];
+              v[e] += __uint_as_float((e & 1) ? (w & 0xFFFF0000u) : (w << 16));
+            }
       }
-      xr[e] = v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xr[8 * c8 + e] = v[e];
     }
     __syncthreads();
   }

@@ -140,7 +140,8 @@ def test_small_pipeline_matches_oracle(outer_s):
 
 
 def test_pipeline_continues_across_calls_and_bounds_frames():
-    """Two calls of 4 and 3 frames equal one call of 7; more frames than the KV capacity fail."""
+    """Two calls of 4 and 3 frames equal one call of 7; more frames than the KV capacity fail,
+    and so does a text-side input that is not 16-byte aligned."""
     rig = PRig(OUTER_SMALL, INNER_SMALL, topk=16, K=2, max_frames=8)
     n = 7
     t, u_c0 = S.pipeline_inputs(OUTER_SMALL, n)
@@ -153,6 +154,16 @@ def test_pipeline_continues_across_calls_and_bounds_frames():
     with pytest.raises(R.RvqsdError) as e:
         rig.run_gpu(t[:2], u_c0[:2], uni[:2])
     assert e.value.status == R.EUNSUPPORTED
+    rig.outer.reset()
+    d_t = torch.zeros(2 * OUTER_SMALL.hidden + 1, dtype=torch.float32, device="cuda")
+    d_u0 = torch.zeros(2, dtype=torch.float32, device="cuda")
+    d_u = torch.zeros((2, INNER_SMALL.n_codes, 3), dtype=torch.float32, device="cuda")
+    d_codes = torch.zeros((2, 1 + INNER_SMALL.n_codes), dtype=torch.int32, device="cuda")
+    d_st = torch.zeros(2 * R.STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    with pytest.raises(R.RvqsdError) as e:
+        rig.outer.pipeline_async(rig.stream, 2, d_t.data_ptr() + 4, d_u0.data_ptr(), d_u.data_ptr(),
+                                 d_codes.data_ptr(), d_st.data_ptr())
+    assert e.value.status == R.EINVAL
     rig.close()
 
 
