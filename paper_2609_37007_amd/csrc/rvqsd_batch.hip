@@ -2089,14 +2089,17 @@ __device__ __forceinline__ Gain8 gain_fetch(const float* gain, int H) {
 }
 
 // x (LDS, [H]) normalised with the gain, split into the LDS row a; hidden_out (workgroup 0)
-// receives the normalised values
+// receives the normalised values. ss_own: this thread's sum of squares over its elements
+// e = tid(), tid() + kThreads, ... when the caller has it (fold_parts)
 __device__ void norm_split(const OParams* op, BShared* sh, const float* x, const Gain8& gn, uint32_t* a,
-                           float* hidden_out) {
+                           float* hidden_out, const float* ss_own = nullptr) {
   const KParams* p = op->k;
   const int H = p->H;
   float ss = 0.f;
-  for (int e = tid(); e < H; e += kThreads) ss = fmaf(x[e], x[e], ss);
-  ss = block_sum(sh, ss);
+  if (ss_own) ss = *ss_own;
+  else
+    for (int e = tid(); e < H; e += kThreads) ss = fmaf(x[e], x[e], ss);
+  ss = block_sum(sh, ss);  // its barrier also orders the caller's writes of x before the reads below
   const float rs = 1.f / sqrtf(ss / (float)H + p->rms_eps);
   const int c = tid();
   if (c < H / 8) {
@@ -2117,17 +2120,23 @@ __device__ void norm_split(const OParams* op, BShared* sh, const float* x, const
   __syncthreads();
 }
 
-// x += the ns partial sums P[k][H] (tagged), in split order
-__device__ bool fold_parts(const OParams* op, const uint64_t* P, int ns, uint32_t tag, float* x, float* tmp) {
+// x += the ns partial sums P[k][H] (tagged), in split order. With ss, the thread's sum of
+// squares of the new x for norm_split, which must follow (its barrier ends this phase)
+__device__ bool fold_parts(const OParams* op, const uint64_t* P, int ns, uint32_t tag, float* x, float* tmp,
+                           float* ss = nullptr) {
   const int H = op->k->H;
   const bool ok = opoll(op, ns * H, tag, [=](int i) { return P + i; }, [&](int i, uint32_t v) { tmp[i] = __uint_as_float(v); });
   if (!ok) return false;
+  float sq = 0.f;
   for (int e = tid(); e < H; e += kThreads) {
     float s2 = tmp[e];
     for (int k = 1; k < ns; ++k) s2 += tmp[(size_t)k * H + e];
-    x[e] = x[e] + s2;
+    const float v = x[e] + s2;
+    x[e] = v;
+    sq = fmaf(v, v, sq);
   }
-  __syncthreads();
+  if (ss) *ss = sq;
+  else __syncthreads();
   return true;
 }
 
@@ -2296,9 +2305,10 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     };
     if (me < nuq) wfetch(w1, qrows(me), 0, H);
     const Gain8 gan = gain_fetch(bfw(p, boff(p, l, p->o_attn_norm)), H);
-    if (l > 0) ok = fold_parts(op, op->tdp + (b - 1) * kOutDSplit * H, op->ks_d2, call.epoch, xr, tmp);
+    float ss = 0.f;
+    if (l > 0) ok = fold_parts(op, op->tdp + (b - 1) * kOutDSplit * H, op->ks_d2, call.epoch, xr, tmp, &ss);
     if (!ok) break;
-    norm_split(op, sh, xr, gan, arow, nullptr);
+    norm_split(op, sh, xr, gan, arow, nullptr, l > 0 ? &ss : nullptr);
     {
       const uint32_t tg = call.epoch;
       for (int u = me; u < nuq; u += nwg) {
@@ -2486,10 +2496,10 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     };
     if (me < F / 16) wfetch(w2, gurows(me), 0, H);
     const Gain8 gmn = gain_fetch(bfw(p, boff(p, l, p->o_mlp_norm)), H);
-    ok = fold_parts(op, op->top + b * kOutOSplit * H, op->ks_o2, call.epoch, xr, tmp);
+    ok = fold_parts(op, op->top + b * kOutOSplit * H, op->ks_o2, call.epoch, xr, tmp, me < F / 16 ? &ss : nullptr);
     if (!ok) break;
     if (me < F / 16) {
-      norm_split(op, sh, xr, gmn, arow, nullptr);
+      norm_split(op, sh, xr, gmn, arow, nullptr, &ss);
       const uint32_t tg = call.epoch;
       for (int u = me; u < F / 16; u += nwg) {
         if (u != me) wfetch(w2, gurows(u), 0, H);
@@ -2525,9 +2535,10 @@ __global__ void __launch_bounds__(kThreads, 1) outer_flow_kernel(const OParams* 
     };
     if (me < nuh) wfetch(w1, hrows(me), 0, H);
     const Gain8 gfn = gain_fetch(bfw(p, p->o_final_norm), H);
-    ok = fold_parts(op, op->tdp + (size_t)(L - 1) * kOutDSplit * H, op->ks_d2, call.epoch, xr, tmp);
+    float ss = 0.f;
+    ok = fold_parts(op, op->tdp + (size_t)(L - 1) * kOutDSplit * H, op->ks_d2, call.epoch, xr, tmp, &ss);
     if (ok) {
-      norm_split(op, sh, xr, gfn, arow, call.hidden_out);
+      norm_split(op, sh, xr, gfn, arow, call.hidden_out, &ss);
       const uint32_t tg = call.epoch;
       for (int u = me; u < nuh; u += nwg) {
         if (u != me) wfetch(w1, hrows(u), 0, H);
