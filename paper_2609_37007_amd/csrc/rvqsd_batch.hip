@@ -74,7 +74,6 @@ __device__ __forceinline__ void store_split(uint32_t* dst, const float (&x)[8]) 
   cst64(dst + 4, (uint64_t)lo[0] | ((uint64_t)lo[1] << 32));
   cst64(dst + 6, (uint64_t)lo[2] | ((uint64_t)lo[3] << 32));
 }
-__device__ __forceinline__ W16 load_w16(const uint32_t* p) { return *G(reinterpret_cast<const W16*>(p)); }
 __device__ __forceinline__ float cldf(const float* p) { return __uint_as_float(cld32(p)); }
 __device__ __forceinline__ uint64_t cld64(const void* p) {
   return __hip_atomic_load(G(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -360,10 +359,10 @@ __device__ __forceinline__ void gemm_unit(WRow wrow, int k0, int klen, const uin
           bh1[mt] = pload4(ap + 8);
           bl1[mt] = pload4(ap + 12);
         } else {
-          bh0[mt] = load_w16(ap);
-          bl0[mt] = load_w16(ap + 4);
-          bh1[mt] = load_w16(ap + 8);
-          bl1[mt] = load_w16(ap + 12);
+          bh0[mt] = *G(reinterpret_cast<const W16*>(ap));
+          bl0[mt] = *G(reinterpret_cast<const W16*>(ap + 4));
+          bh1[mt] = *G(reinterpret_cast<const W16*>(ap + 8));
+          bl1[mt] = *G(reinterpret_cast<const W16*>(ap + 12));
         }
       }
     }
