@@ -3,9 +3,10 @@
 
 One step is one audio frame: the inner MultiCodeDecoder loop emitting the 15
 residual codes c_1..c_15 of a frame after c_0 (prefix pass plus speculative
-draft/verify rounds, Sec. 2.2 and Fig. 3 of the paper), run as one launch of
-the library's persistent frame kernel through rvqsd_decode_frame_async with
-every input already resident in device memory.
+draft/verify rounds, Sec. 2.2 and Fig. 3 of the paper), decoded by the
+library's persistent frame kernel through rvqsd_decode_frames_async (up to 1024
+frames per launch, a grid barrier between frames) with every input already
+resident in device memory.
 
 Workload (default): the 1024-wide MultiCodeDecoder (5 layers, hidden 1024, GQA
 16/8 heads of 128, SwiGLU FFN 3072, 15 codebooks of 2048, bf16 weights N(0,
@@ -47,6 +48,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "RVQ codes/sec single-stream; accepted tok/call; verify-step GB/s vs roofline"
+FRAMES_PER_LAUNCH = 1024  # frames per launch of the persistent frame kernel (rvqsd_decode_frames_async)
 KERNEL_SOURCES = ("paper_2609_37007_amd/csrc/rvqsd_frame.hip", "paper_2609_37007_amd/csrc/rvqsd_device.h",
                   "paper_2609_37007_amd/csrc/rvqsd_internal.h")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "frame_kernel_mcd1024_k4_fetch_write_counters.txt")
@@ -68,10 +70,11 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic():
-    """Bytes per launch that the L2 caches fetched from and wrote to the memory fabric
-    (rocprofv3 FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy), from the committed
-    counter summary, or None when the summary is absent or the kernel sources changed
-    since it was taken. The counters see Infinity Cache (MALL) hits as fabric traffic."""
+    """Bytes per frame that the L2 caches fetched from and wrote to the memory fabric
+    (rocprofv3 FETCH_SIZE + WRITE_SIZE of a launch, each scaled by a plain copy, over the
+    launch's frames), from the committed counter summary, or None when the summary is
+    absent or the kernel sources changed since it was taken. The counters see Infinity
+    Cache (MALL) hits as fabric traffic."""
     if not os.path.exists(PMC_SUMMARY):
         return None
     kv = {}
@@ -83,7 +86,7 @@ def measured_traffic():
     if kv.get("kernel_source_sha256") != kernel_source_hash():
         return None
     try:
-        return float(kv["fetch_write_bytes_per_launch"])
+        return float(kv["fetch_write_bytes_per_frame"])
     except (KeyError, ValueError):
         return None
 
@@ -761,29 +764,32 @@ def main() -> int:
     d_stats = torch.zeros(steps * sb, dtype=torch.uint8, device=dev)
     H, n = s.hidden, s.n_codes
 
-    def launch(i):
-        stream.decode_frame_async(d_f.data_ptr() + i * H * 4, d_c0.data_ptr() + i * 4,
-                                  d_u.data_ptr() + i * n * 3 * 4, d_codes.data_ptr() + i * n * 4,
-                                  d_stats.data_ptr() + i * sb)
+    def launch(i0, cnt):
+        # frames i0 .. i0 + cnt - 1, up to 1024 per launch of the persistent kernel
+        stream.decode_frames_async(cnt, d_f.data_ptr() + i0 * H * 4, d_c0.data_ptr() + i0 * 4,
+                                   d_u.data_ptr() + i0 * n * 3 * 4, d_codes.data_ptr() + i0 * n * 4,
+                                   d_stats.data_ptr() + i0 * sb)
 
     print(f"[bench] warmup {W} frames", file=sys.stderr, flush=True)
-    for i in range(W):
-        launch(i % steps)
+    for i0 in range(0, W, steps):
+        launch(0, min(steps, W - i0))
     torch.cuda.synchronize()
     ws = np.frombuffer(d_stats.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)[:min(W, steps)]
     if (ws["status"] != 0).any():
         print(f"[bench] warmup frame failed: status {ws['status'].tolist()}", file=sys.stderr)
         return 1
 
-    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    print(f"[bench] timing {steps} frames", file=sys.stderr, flush=True)
+    n_launch = (steps + FRAMES_PER_LAUNCH - 1) // FRAMES_PER_LAUNCH
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(n_launch)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(n_launch)]
+    print(f"[bench] timing {steps} frames in {n_launch} launch(es)", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(steps):
-        ev0[i].record(torch_stream)
-        launch(i)
-        ev1[i].record(torch_stream)
+    for j in range(n_launch):
+        i0 = j * FRAMES_PER_LAUNCH
+        ev0[j].record(torch_stream)
+        launch(i0, min(FRAMES_PER_LAUNCH, steps - i0))
+        ev1[j].record(torch_stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     elapsed = t1 - t0
@@ -794,16 +800,21 @@ def main() -> int:
         bad = int(np.argmax(st["status"] != 0))
         print(f"[bench] frame {bad} failed with status {int(st['status'][bad])}", file=sys.stderr)
         return 1
-    launch_ms = np.array([ev0[i].elapsed_time(ev1[i]) for i in range(steps)])
+    launch_ms = np.array([ev0[j].elapsed_time(ev1[j]) for j in range(n_launch)])
     calls = int(st["target_calls"].sum())
     rounds = int(st["rounds"].sum())
-    bytes_per_launch = st["weight_bytes"].astype(np.float64)
-    achieved = float(bytes_per_launch.sum() / (launch_ms.sum() * 1e-3) / 1e9)
+    frame_bytes = st["weight_bytes"].astype(np.float64)
+    achieved = float(frame_bytes.sum() / (launch_ms.sum() * 1e-3) / 1e9)
+    frames_per_launch = steps / n_launch
+    # each frame's device time (its stats clock, 100 MHz)
+    frame_ms = (st["clk_end"].astype(np.float64) - st["clk_start"].astype(np.float64)) / 1e5
     traffic = measured_traffic() if (a.workload == "mcd1024" and K == 4 and a.head_scale == 1.0 and not tree
                                      and a.offsets == "seed" and not a.gemv) else None
+    if traffic is not None:
+        traffic = round(traffic * frames_per_launch, 1)
     codes_per_s = n * steps / elapsed
     # the box's own read rates for a buffer of one launch's mean bytes per pass
-    box = stream_read_rates(torch, dev, torch_stream, int(bytes_per_launch.sum() / calls) & ~255)
+    box = stream_read_rates(torch, dev, torch_stream, int(frame_bytes.sum() / calls) & ~255)
 
     cpu = None
     if not a.no_cpu_baseline:
@@ -845,7 +856,7 @@ def main() -> int:
         "mean_tokens_per_round": round((n * steps - steps) / max(rounds, 1), 4),
         "accept_rate": round(float(st["accepted"].sum()) / max(int(st["drafted"].sum()), 1), 4),
         "target_calls_per_frame": round(calls / steps, 3),
-        "frame_ms_p50": round(float(np.median(launch_ms)), 4),
+        "frame_ms_p50": round(float(np.median(frame_ms)), 4),
         "pass_us_mean": round(float(launch_ms.sum() * 1e3 / calls), 2),
         "roofline": {
             "bound": "hbm",
@@ -855,8 +866,9 @@ def main() -> int:
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "kernel": "batch_kernel" if tree else "frame_kernel",
-            "algorithmic_bytes_per_launch": round(float(bytes_per_launch.mean()), 1),
+            "algorithmic_bytes_per_launch": round(float(frame_bytes.sum() / n_launch), 1),
             "launch_ms_mean": round(float(launch_ms.mean()), 5),
+            "frames_per_launch": round(frames_per_launch, 2),
             "traffic_counts": "L2-to-fabric bytes (FETCH_SIZE + WRITE_SIZE, Infinity Cache hits included)",
             "box_read_gbs": {"warm": box["warm"], "cold": box["cold"], "bytes": box["bytes"],
                              "how": "torch.sum over one pass's bytes: warm = back to back (Infinity Cache), "

@@ -213,6 +213,19 @@ rvqsd_status rvqsd_decode_frame_u(rvqsd_stream* s, const float* frame_hidden, in
 rvqsd_status rvqsd_decode_frame_async(rvqsd_stream* s, const float* d_frame_hidden, const int32_t* d_c0,
                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats);
 
+/* n frames of one stream in order, as n calls of rvqsd_decode_frame_async would
+ * decode them (the same codes and counts; Sec. 2.2 per frame), with up to 1024
+ * frames per launch of the persistent kernel, so the GPU does not idle between
+ * frames. Device pointers: d_frame_hidden float[n][hidden],
+ * d_c0 int32[n], d_uniforms float[n][n_codes][3], d_out_codes out
+ * int32[n][n_codes], d_stats out rvqsd_stats[n]. While a trace is set
+ * (rvqsd_set_trace), and on a tree stream, every frame gets a launch of its
+ * own. EINVAL for a null
+ * argument or n < 0; device-side errors as in rvqsd_decode_frame_async, per
+ * frame. */
+rvqsd_status rvqsd_decode_frames_async(rvqsd_stream* s, int32_t n, const float* d_frame_hidden, const int32_t* d_c0,
+                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats);
+
 /* rvqsd_decode_frame_async for callers that cannot allocate memory: code under
  * HIP graph capture, tight serving loops, harnesses that forbid allocation. It
  * needs no stream object: the frame's device buffers (exchange words, KV cache,

@@ -86,6 +86,7 @@ struct rvqsd_stream {
   int32_t* d_out;
   uint32_t epoch;       // tag base of the next frame
   uint32_t epoch_step;
+  uint32_t* fbar;       // arrivals between the frames of one launch (in dbuf)
   size_t par_begin, par_end;  // byte range of dbuf holding the parity-word buffers (pass count follows)
   size_t tag_begin, tag_end;  // byte range of dbuf holding the tagged words
   // batched path (max_streams > 1)
@@ -580,13 +581,14 @@ static rvqsd_status stream_create(rvqsd_model* m, void* hip_stream, int32_t max_
     return at;
   };
   const size_t o_in = take(((size_t)H + 3 * kMaxCodes + 4) * 4),
-               o_out = take((kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64);
+               o_out = take((kMaxCodes + 1) * 4 + sizeof(rvqsd_stats) + 64), o_fbar = take(4);
   s->dbuf_bytes = off;
   hipError_t e = dev_alloc(&s->dbuf, off);
   if (e != hipSuccess) {
     delete s;
     return set_err(RVQSD_ENOMEM, "stream buffers (%zu bytes): %s", off, hipGetErrorString(e));
   }
+  s->fbar = (uint32_t*)((uint8_t*)s->dbuf + o_fbar);
   e = hipMemset(s->dbuf, 0, off);
   if (e == hipSuccess)
     e = hipMemsetD8((hipDeviceptr_t)((uint8_t*)s->dbuf + fl.par_begin), 0x01, fl.par_end - fl.par_begin);
@@ -674,11 +676,69 @@ static rvqsd_status launch_one(rvqsd_stream* s, const float* d_fh, const int32_t
   fa.out_codes = d_codes;
   fa.out_stats = d_stats;
   fa.epoch_base = s->epoch;
+  fa.n_frames = 1;
+  fa.epoch_step = 0;
+  fa.fbar = s->fbar;
   s->epoch += s->epoch_step;
   char err[256];
   int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, s->m->mfma, (void*)s->stream, s->m->lds_bytes, err,
                         sizeof(err));
   if (st) return set_err(st, "%s", err);
+  return RVQSD_OK;
+}
+
+// frames of one launch at most (about 1.4 s of the 1024-wide model)
+constexpr int kFramesPerLaunch = 1024;
+
+rvqsd_status rvqsd_decode_frames_async(rvqsd_stream* s, int32_t n, const float* d_frame_hidden, const int32_t* d_c0,
+                                       const float* d_uniforms, int32_t* d_out_codes, rvqsd_stats* d_stats) {
+  if (!s || !d_frame_hidden || !d_c0 || !d_uniforms || !d_out_codes || !d_stats)
+    return set_err(RVQSD_EINVAL, "null argument");
+  if (n < 0) return set_err(RVQSD_EINVAL, "n = %d < 0", n);
+  const size_t H = s->m->base.H, nc = s->m->base.n_codes;
+  if (s->tree) {  // tree streams decode through the batched kernel, a frame per call
+    for (int f = 0; f < n; ++f) {
+      rvqsd_status st = rvqsd_decode_frame_async(s, d_frame_hidden + f * H, d_c0 + f, d_uniforms + f * nc * 3,
+                                                 d_out_codes + f * nc, d_stats + f);
+      if (st) return st;
+    }
+    return RVQSD_OK;
+  }
+  // a trace records the passes of one frame: traced frames get a launch each
+  const KParams& kp = s->kp;
+  const bool traced = kp.tr_logits || kp.tr_rounds || kp.tr_clock || kp.tr_wgclock || kp.tr_wgready;
+  for (int f0 = 0; f0 < n;) {
+    const int cnt = traced ? 1 : (n - f0 < kFramesPerLaunch ? n - f0 : kFramesPerLaunch);
+    if (cnt == 1) {
+      rvqsd_status st = launch_one(s, d_frame_hidden + f0 * H, d_c0 + f0, d_uniforms + f0 * nc * 3, d_out_codes + f0 * nc,
+                                   d_stats + f0);
+      if (st) return st;
+      f0 += 1;
+      continue;
+    }
+    // the tags of every frame of the launch must stay below the wrap
+    if ((uint64_t)s->epoch + (uint64_t)(cnt + 1) * s->epoch_step >= 0xFFFFFFFFull) {
+      HIPCHK(hipMemsetAsync((uint8_t*)s->dbuf + s->tag_begin, 0, s->tag_end - s->tag_begin, s->stream));
+      s->epoch = s->epoch_step;
+    }
+    HIPCHK(hipMemsetAsync(s->fbar, 0, sizeof(uint32_t), s->stream));
+    FrameArgs fa;
+    fa.frame_hidden = d_frame_hidden + f0 * H;
+    fa.c0 = d_c0 + f0;
+    fa.uniforms = d_uniforms + f0 * nc * 3;
+    fa.out_codes = d_out_codes + f0 * nc;
+    fa.out_stats = d_stats + f0;
+    fa.epoch_base = s->epoch;
+    fa.n_frames = cnt;
+    fa.epoch_step = s->epoch_step;
+    fa.fbar = s->fbar;
+    s->epoch += (uint32_t)cnt * s->epoch_step;
+    char err[256];
+    int st = launch_frame(s->dkp, fa, s->m->nwg, s->m->cfg.dtype, s->m->mr, s->m->mfma, (void*)s->stream, s->m->lds_bytes,
+                          err, sizeof(err));
+    if (st) return set_err(st, "%s", err);
+    f0 += cnt;
+  }
   return RVQSD_OK;
 }
 

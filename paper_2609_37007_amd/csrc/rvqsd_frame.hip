@@ -2015,31 +2015,11 @@ __device__ __forceinline__ unsigned long long pass_bytes(const Ctx& c) {
   return b;
 }
 
-// MF: projections and LM heads on the matrix cores (bf16 or int8 weights, at most 8 rows), else
-// on the VALU GEMV
+// One frame: the passes until its 15 codes are committed, then its statistics (workgroup 0)
 template <typename WT, int MR, bool MF>
-__global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
-  constexpr int RPT = MR <= 8 ? 8 : 4;
-  __shared__ Shared shs;
-  extern __shared__ __align__(16) float dyn[];
-  const KParams* p = gp;
-  Ctx c;
-  c.p = p;
-  c.sh = &shs;
-  c.cpw = (p->H + p->nwg - 1) / p->nwg;
-  c.dyn = dyn;
-  c.xown = dyn;
-  c.red = dyn + kMaxRows * c.cpw;
-  c.work = c.red + kWaves * (RPT + 1) * MR;
-  c.attn_const = c.work + p->work_floats;
-  if ((int)blockIdx.x < p->nq) {
-    const int d = p->d;
-    for (int i = tid(); i < p->L * 2 * d; i += kThreads) {
-      const int l = i / (2 * d), j = i % (2 * d);
-      c.attn_const[i] = G(fptr(p, layer_off(p, l, j < d ? p->o_qn : p->o_kn)))[j % d];
-    }
-    for (int i = tid(); i < kMaxPos * d; i += kThreads) c.attn_const[p->L * 2 * d + i] = G(p->rope)[i];
-  }
+__device__ __forceinline__ void decode_frame(Ctx& c, const FrameArgs& fa) {
+  const KParams* p = c.p;
+  Shared& shs = *c.sh;
   // every uniform in [0, 1) (NaN fails), or the frame is not decoded and reports EINVAL;
   // every workgroup reads the same table, so all of them agree
   int u_bad = 0;
@@ -2050,7 +2030,7 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
   }
   const bool u_ok = __syncthreads_or(u_bad) == 0;
   c.tag_base = fa.epoch_base;
-  c.pass0 = *G(p->pass_count);
+  c.pass0 = __hip_atomic_load(G(p->pass_count), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   c.rdy = nullptr;
   const uint64_t t_start = dclock();
   const int c0 = fa.c0[0];
@@ -2162,12 +2142,68 @@ __global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __res
     if (!c0_ok) status = poisoned ? RVQSD_EHIP : RVQSD_EINVAL;
     if (status == 0 && !ok) status = RVQSD_ETIMEOUT;
     // the parity state of the exchange buffers is only consistent after a complete frame
-    if (!poisoned) *G(p->pass_count) = (ok && c0_ok) ? c.pass0 + (uint32_t)shs.pass : (c0_ok ? 0xffffffffu : c.pass0);
+    if (!poisoned)
+      __hip_atomic_store(G(p->pass_count), (ok && c0_ok) ? c.pass0 + (uint32_t)shs.pass : (c0_ok ? 0xffffffffu : c.pass0),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     st->status = status;
     st->weight_bytes = shs.st_bytes;
     st->clk_start = t_start;
     st->clk_end = dclock();
     for (int s2 = 1; s2 <= p->n_codes; ++s2) fa.out_codes[s2 - 1] = ok ? shs.codes[s2] : -1;
+  }
+}
+
+// Between two frames of one launch: every workgroup has ended the earlier frame (its parity
+// resets and workgroup 0's statistics and pass count are done) before any starts the next.
+// bar counts arrivals from 0 (cleared before the launch); the wait is bounded like every other.
+__device__ __forceinline__ void frame_gap_sync(uint32_t* bar, uint32_t target) {
+  __syncthreads();
+  if (tid() == 0) {
+    __hip_atomic_fetch_add(G(bar), 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t t0 = dclock();
+    while (__hip_atomic_load(G(bar), __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target)
+      if (dclock() - t0 > kTimeoutTicks) break;  // the next frame then fails on its own waits
+  }
+  __syncthreads();
+}
+
+// MF: projections and LM heads on the matrix cores (bf16 or int8 weights, at most 8 rows), else
+// on the VALU GEMV. fa.n_frames frames, frame f's arguments at stride f from fa's and its tags
+// from fa.epoch_base + f * fa.epoch_step.
+template <typename WT, int MR, bool MF>
+__global__ void __launch_bounds__(kThreads, 1) frame_kernel(const KParams* __restrict__ gp, FrameArgs fa) {
+  constexpr int RPT = MR <= 8 ? 8 : 4;
+  __shared__ Shared shs;
+  extern __shared__ __align__(16) float dyn[];
+  const KParams* p = gp;
+  Ctx c;
+  c.p = p;
+  c.sh = &shs;
+  c.cpw = (p->H + p->nwg - 1) / p->nwg;
+  c.dyn = dyn;
+  c.xown = dyn;
+  c.red = dyn + kMaxRows * c.cpw;
+  c.work = c.red + kWaves * (RPT + 1) * MR;
+  c.attn_const = c.work + p->work_floats;
+  if ((int)blockIdx.x < p->nq) {
+    const int d = p->d;
+    for (int i = tid(); i < p->L * 2 * d; i += kThreads) {
+      const int l = i / (2 * d), j = i % (2 * d);
+      c.attn_const[i] = G(fptr(p, layer_off(p, l, j < d ? p->o_qn : p->o_kn)))[j % d];
+    }
+    for (int i = tid(); i < kMaxPos * d; i += kThreads) c.attn_const[p->L * 2 * d + i] = G(p->rope)[i];
+  }
+  for (int f = 0; f < fa.n_frames; ++f) {
+    if (f > 0) frame_gap_sync(fa.fbar, (uint32_t)f * (uint32_t)p->nwg);
+    FrameArgs fr = fa;
+    fr.frame_hidden = fa.frame_hidden + (size_t)f * p->H;
+    fr.c0 = fa.c0 + f;
+    fr.uniforms = fa.uniforms + (size_t)f * 3 * p->n_codes;
+    fr.out_codes = fa.out_codes + (size_t)f * p->n_codes;
+    fr.out_stats = fa.out_stats + f;
+    fr.epoch_base = fa.epoch_base + (uint32_t)f * fa.epoch_step;
+    fr.n_frames = 1;
+    decode_frame<WT, MR, MF>(c, fr);
   }
 }
 

@@ -73,6 +73,12 @@ struct FrameArgs {
   int32_t* out_codes;         // [n_codes]
   rvqsd_stats* out_stats;     // [1]
   uint32_t epoch_base;        // tags of this frame are epoch_base + 1 ..
+  // frames of one launch: frame f reads and writes each array above at f times its frame
+  // stride and tags from epoch_base + f * epoch_step; fbar counts arrivals between frames
+  // (cleared before a launch of more than one frame)
+  int32_t n_frames;
+  uint32_t epoch_step;
+  uint32_t* fbar;
 };
 
 // Device buffers of one frame decode (the exchange words, the KV cache and the

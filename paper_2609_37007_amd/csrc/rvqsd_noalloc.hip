@@ -136,6 +136,9 @@ int noalloc_launch(const rvqsd_model* m, void* hip_stream, const float* d_frame_
   fa.out_codes = d_out_codes;
   fa.out_stats = d_stats;
   fa.epoch_base = frame_epoch_step(k.L);  // every call starts from cleared tags
+  fa.n_frames = 1;
+  fa.epoch_step = 0;
+  fa.fbar = nullptr;
   return launch_frame(reinterpret_cast<const KParams*>(base + fl.o_kp), fa, m->nwg, m->cfg.dtype, m->mr, m->mfma, hip_stream,
                       m->lds_bytes, err, errlen);
 }

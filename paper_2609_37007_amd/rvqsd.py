@@ -24,8 +24,8 @@ TRACE_ROUND_INTS = 32
 # every symbol include/rvqsd.h declares
 EXPORTS = ("rvqsd_create", "rvqsd_destroy", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_tree_stream_create",
            "rvqsd_stream_destroy",
-           "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frame_noalloc",
-           "rvqsd_stream_reset",
+           "rvqsd_decode_frame", "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frames_async",
+           "rvqsd_decode_frame_noalloc", "rvqsd_stream_reset",
            "rvqsd_set_trace", "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async",
            "rvqsd_batch_totals", "rvqsd_set_batch_trace", "rvqsd_outer_create", "rvqsd_outer_destroy", "rvqsd_outer_reset",
            "rvqsd_pipeline_frames_async", "rvqsd_uniforms_from_seed", "rvqsd_status_str", "rvqsd_last_error")
@@ -133,6 +133,7 @@ def lib():
         L.rvqsd_decode_frame.argtypes = [vp, vp, i32, ctypes.c_uint64, vp, P(rvqsd_stats)]
         L.rvqsd_decode_frame_u.argtypes = [vp, vp, i32, vp, vp, P(rvqsd_stats)]
         L.rvqsd_decode_frame_async.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.rvqsd_decode_frames_async.argtypes = [vp, i32, vp, vp, vp, vp, vp]
         L.rvqsd_decode_frame_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.rvqsd_set_trace.argtypes = [vp, P(rvqsd_trace)]
         L.rvqsd_decode_frames_batched.argtypes = [vp, i32, vp, vp, vp, vp, vp]
@@ -152,7 +153,8 @@ def lib():
         L.rvqsd_last_error.restype = ctypes.c_char_p
         for n in ("rvqsd_create", "rvqsd_model_info", "rvqsd_stream_create", "rvqsd_tree_stream_create",
                   "rvqsd_decode_frame",
-                  "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frame_noalloc",
+                  "rvqsd_decode_frame_u", "rvqsd_decode_frame_async", "rvqsd_decode_frames_async",
+                  "rvqsd_decode_frame_noalloc",
                   "rvqsd_stream_reset", "rvqsd_set_trace",
                   "rvqsd_decode_frames_batched", "rvqsd_decode_frames_batched_async", "rvqsd_batch_totals",
                   "rvqsd_set_batch_trace",
@@ -276,6 +278,14 @@ class Stream:
         _check(lib().rvqsd_decode_frame_async(self._h, ctypes.c_void_p(d_frame_hidden), ctypes.c_void_p(d_c0),
                                               ctypes.c_void_p(d_uniforms), ctypes.c_void_p(d_out_codes),
                                               ctypes.c_void_p(d_stats)), "rvqsd_decode_frame_async")
+
+    def decode_frames_async(self, n: int, d_frame_hidden: int, d_c0: int, d_uniforms: int, d_out_codes: int,
+                            d_stats: int):
+        """n frames in order (device pointers to [n][H], [n], [n][n_codes][3], [n][n_codes], [n] stats);
+        enqueues only, up to 1024 frames per launch."""
+        _check(lib().rvqsd_decode_frames_async(self._h, int(n), ctypes.c_void_p(d_frame_hidden), ctypes.c_void_p(d_c0),
+                                               ctypes.c_void_p(d_uniforms), ctypes.c_void_p(d_out_codes),
+                                               ctypes.c_void_p(d_stats)), "rvqsd_decode_frames_async")
 
     def decode_frames_batched(self, frame_hidden, c0, uniforms):
         """Host arrays [n][H], [n], [n][n_codes][3] -> (codes [n][n_codes], stats structured array [n])."""

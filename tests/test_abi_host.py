@@ -69,6 +69,7 @@ def test_argument_errors():
     assert L.rvqsd_stream_reset(None) == R.EINVAL
     assert L.rvqsd_decode_frame_u(None, None, 0, None, None, None) == R.EINVAL
     assert L.rvqsd_decode_frame_async(None, None, None, None, None, None) == R.EINVAL
+    assert L.rvqsd_decode_frames_async(None, 2, None, None, None, None, None) == R.EINVAL
     info = R.rvqsd_info()
     assert L.rvqsd_model_info(None, ctypes.byref(info)) == R.EINVAL
     L.rvqsd_destroy(None)

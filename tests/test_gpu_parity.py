@@ -192,6 +192,52 @@ def test_mcd1024_async_launch_matches_oracle():
     rig.close()
 
 
+def test_frames_in_one_launch_equal_one_launch_each():
+    """rvqsd_decode_frames_async (up to 1024 frames per launch of the persistent kernel, a grid
+    barrier between frames; the benchmark's launch) gives the codes and counts of one launch per
+    frame: 1100 frames of the 1024-wide model (launches of 1024 and 76 frames), with frame 7's c0
+    and one uniform of frame 1030 out of range, which fail those frames alone (EINVAL)."""
+    s = S.MCD_1024
+    ts = torch.cuda.current_stream()
+    rig = Rig(s, topk=50, K=4, hip_stream=ts.cuda_stream)
+    N = 1100
+    f, c0 = S.frame_inputs(s, N)
+    u = np.array(S.uniforms(N), dtype=np.float32, copy=True)
+    c0 = np.array(c0, dtype=np.int32, copy=True)
+    c0[7] = s.vocab
+    u[1030][2][1] = 1.5
+    d_f = torch.from_numpy(f).cuda()
+    d_c0 = torch.from_numpy(c0).cuda()
+    d_u = torch.from_numpy(np.ascontiguousarray(u)).cuda()
+    H, n, sb = s.hidden, s.n_codes, R.STATS_DTYPE.itemsize
+
+    def run(one_launch):
+        d_codes = torch.full((N, n), -7, dtype=torch.int32, device="cuda")
+        d_st = torch.zeros(N * sb, dtype=torch.uint8, device="cuda")
+        if one_launch:
+            rig.stream.decode_frames_async(N, d_f.data_ptr(), d_c0.data_ptr(), d_u.data_ptr(), d_codes.data_ptr(),
+                                           d_st.data_ptr())
+        else:
+            for i in range(N):
+                rig.stream.decode_frame_async(d_f.data_ptr() + i * H * 4, d_c0.data_ptr() + i * 4,
+                                              d_u.data_ptr() + i * n * 12, d_codes.data_ptr() + i * n * 4,
+                                              d_st.data_ptr() + i * sb)
+        torch.cuda.synchronize()
+        return d_codes.cpu().numpy(), np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)
+
+    print("1100 frames, one launch per frame", flush=True)
+    a_codes, a_st = run(False)
+    print("1100 frames, 1024 per launch", flush=True)
+    b_codes, b_st = run(True)
+    assert a_st["status"][7] == R.EINVAL and a_st["status"][1030] == R.EINVAL
+    assert (np.delete(a_st["status"], [7, 1030]) == 0).all()
+    assert (a_codes[[7, 1030]] == -1).all()
+    assert np.array_equal(a_codes, b_codes)
+    for key in ("status", "target_calls", "rounds", "drafted", "accepted", "accept_mask", "weight_bytes"):
+        assert np.array_equal(a_st[key], b_st[key]), key
+    rig.close()
+
+
 def test_frames_do_not_depend_on_stream_history():
     """The same frame decoded at two points of a stream's life -- fresh, and after other frames
     whose passes add up to an odd count -- gives bit-identical logits, decisions and codes: the
