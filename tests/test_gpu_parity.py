@@ -192,20 +192,22 @@ def test_mcd1024_async_launch_matches_oracle():
     rig.close()
 
 
-def test_frames_in_one_launch_equal_one_launch_each():
+@pytest.mark.parametrize("shape,topk,K,N,bad", [("MCD_1024", 50, 4, 1100, (7, 1030)), ("TINY", 8, 3, 2100, (5, 2050))],
+                         ids=["mcd1024-bf16-mfma", "tiny-f32-gemv"])
+def test_frames_in_one_launch_equal_one_launch_each(shape, topk, K, N, bad):
     """rvqsd_decode_frames_async (up to 1024 frames per launch of the persistent kernel, a grid
     barrier between frames; the benchmark's launch) gives the codes and counts of one launch per
-    frame: 1100 frames of the 1024-wide model (launches of 1024 and 76 frames), with frame 7's c0
-    and one uniform of frame 1030 out of range, which fail those frames alone (EINVAL)."""
-    s = S.MCD_1024
+    frame: 1100 frames of the 1024-wide model (launches of 1024 and 76 frames) and 2100 of the
+    tiny fp32 model (1024, 1024, 52), with one frame's c0 and one uniform of a frame in a later
+    launch out of range, which fail those frames alone (EINVAL)."""
+    s = getattr(S, shape)
     ts = torch.cuda.current_stream()
-    rig = Rig(s, topk=50, K=4, hip_stream=ts.cuda_stream)
-    N = 1100
+    rig = Rig(s, topk=topk, K=K, hip_stream=ts.cuda_stream)
     f, c0 = S.frame_inputs(s, N)
-    u = np.array(S.uniforms(N), dtype=np.float32, copy=True)
+    u = np.array(S.uniforms(N, s.n_codes), dtype=np.float32, copy=True)
     c0 = np.array(c0, dtype=np.int32, copy=True)
-    c0[7] = s.vocab
-    u[1030][2][1] = 1.5
+    c0[bad[0]] = s.vocab
+    u[bad[1]][2][1] = 1.5
     d_f = torch.from_numpy(f).cuda()
     d_c0 = torch.from_numpy(c0).cuda()
     d_u = torch.from_numpy(np.ascontiguousarray(u)).cuda()
@@ -225,13 +227,13 @@ def test_frames_in_one_launch_equal_one_launch_each():
         torch.cuda.synchronize()
         return d_codes.cpu().numpy(), np.frombuffer(d_st.cpu().numpy().tobytes(), dtype=R.STATS_DTYPE)
 
-    print("1100 frames, one launch per frame", flush=True)
+    print(f"{shape}: {N} frames, one launch per frame", flush=True)
     a_codes, a_st = run(False)
-    print("1100 frames, 1024 per launch", flush=True)
+    print(f"{shape}: {N} frames, 1024 per launch", flush=True)
     b_codes, b_st = run(True)
-    assert a_st["status"][7] == R.EINVAL and a_st["status"][1030] == R.EINVAL
-    assert (np.delete(a_st["status"], [7, 1030]) == 0).all()
-    assert (a_codes[[7, 1030]] == -1).all()
+    assert (a_st["status"][list(bad)] == R.EINVAL).all()
+    assert (np.delete(a_st["status"], list(bad)) == 0).all()
+    assert (a_codes[list(bad)] == -1).all()
     assert np.array_equal(a_codes, b_codes)
     for key in ("status", "target_calls", "rounds", "drafted", "accepted", "accept_mask", "weight_bytes"):
         assert np.array_equal(a_st[key], b_st[key]), key
