@@ -779,16 +779,18 @@ def main() -> int:
         print(f"[bench] warmup frame failed: status {ws['status'].tolist()}", file=sys.stderr)
         return 1
 
-    n_launch = (steps + FRAMES_PER_LAUNCH - 1) // FRAMES_PER_LAUNCH
+    # a tree stream decodes through the batched kernel, one launch per frame
+    fpl = 1 if tree else FRAMES_PER_LAUNCH
+    n_launch = (steps + fpl - 1) // fpl
     ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(n_launch)]
     ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(n_launch)]
     print(f"[bench] timing {steps} frames in {n_launch} launch(es)", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for j in range(n_launch):
-        i0 = j * FRAMES_PER_LAUNCH
+        i0 = j * fpl
         ev0[j].record(torch_stream)
-        launch(i0, min(FRAMES_PER_LAUNCH, steps - i0))
+        launch(i0, min(fpl, steps - i0))
         ev1[j].record(torch_stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
